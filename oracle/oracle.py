@@ -1,0 +1,168 @@
+"""ctypes binding of ``fst_oracle.cpp`` (TEST INFRASTRUCTURE ONLY).
+
+The oracle is a serial C++ implementation of the composition definition of
+Argueta & Chiang §2 restricted to the pairs reachable by the breadth-first
+search of Algorithm 1 (§3.2).  It reads host numpy arrays in the coordinate
+layout of ``paper_1805_06383_amd.workloads.FST``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from pathlib import Path
+
+import numpy as np
+
+_HERE = Path(__file__).resolve().parent
+_SRC = _HERE / "fst_oracle.cpp"
+_LIB = _HERE / "liboracle.so"
+CXXFLAGS = ["-O2", "-std=c++17", "-ffp-contract=off", "-fPIC", "-shared", "-Wall"]
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+class _Fst(ctypes.Structure):
+    _fields_ = [
+        ("num_states", ctypes.c_uint32), ("start", ctypes.c_uint32),
+        ("num_isyms", ctypes.c_uint32), ("num_osyms", ctypes.c_uint32),
+        ("num_arcs", ctypes.c_uint64),
+        ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p),
+        ("ilabel", ctypes.c_void_p), ("olabel", ctypes.c_void_p),
+        ("weight", ctypes.c_void_p), ("final", ctypes.c_void_p),
+    ]
+
+
+def library_path() -> Path:
+    return _LIB
+
+
+def build(force: bool = True, out: Path | None = None, src: Path | None = None) -> Path:
+    """Compile the oracle with g++ into a shared library and return its path."""
+    out = Path(out) if out else _LIB
+    src = Path(src) if src else _SRC
+    tmp = out.with_suffix(f".so.tmp{os.getpid()}")
+    if not force and out.exists() and out.stat().st_mtime >= src.stat().st_mtime:
+        return out
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(tmp), str(src)], check=True)
+    os.replace(tmp, out)
+    return out
+
+
+_handle_cache: dict[str, ctypes.CDLL] = {}
+
+
+def _load(path: Path | None = None) -> ctypes.CDLL:
+    path = Path(path) if path else _LIB
+    key = str(path)
+    if key in _handle_cache:
+        return _handle_cache[key]
+    if path == _LIB and (not _LIB.exists() or _LIB.stat().st_mtime < _SRC.stat().st_mtime):
+        build(force=True)
+    lib = ctypes.CDLL(str(path))
+    vp, u32, u64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
+    lib.oracle_compose.argtypes = [ctypes.POINTER(_Fst), ctypes.POINTER(_Fst), u32,
+                                   ctypes.POINTER(vp)]
+    lib.oracle_compose.restype = ctypes.c_int
+    lib.oracle_expand_pairs.argtypes = [ctypes.POINTER(_Fst), ctypes.POINTER(_Fst), u64,
+                                        vp, vp, ctypes.POINTER(vp)]
+    lib.oracle_expand_pairs.restype = ctypes.c_int
+    lib.oracle_counts.argtypes = [vp, vp]
+    lib.oracle_counts.restype = None
+    lib.oracle_seconds.argtypes = [vp]
+    lib.oracle_seconds.restype = ctypes.c_double
+    lib.oracle_states.argtypes = [vp, vp, vp, vp, vp]
+    lib.oracle_states.restype = None
+    lib.oracle_arcs.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.oracle_arcs.restype = None
+    lib.oracle_free.argtypes = [vp]
+    lib.oracle_free.restype = None
+    _handle_cache[key] = lib
+    return lib
+
+
+def _as_struct(m):
+    arrs = [np.ascontiguousarray(m.src, np.uint32), np.ascontiguousarray(m.dst, np.uint32),
+            np.ascontiguousarray(m.ilabel, np.uint32), np.ascontiguousarray(m.olabel, np.uint32),
+            np.ascontiguousarray(m.weight, np.float32), np.ascontiguousarray(m.final, np.uint8)]
+    s = _Fst(m.num_states, m.start, m.num_isyms, m.num_osyms, len(arrs[0]),
+             *[a.ctypes.data for a in arrs])
+    return s, arrs  # arrays returned to keep them alive during the call
+
+
+@dataclass
+class OracleResult:
+    """Oracle output.  States are ids 0..n-1 with their pairs (q1, q2); arcs are
+    (src id, dst id, input symbol a, output symbol c, weight)."""
+
+    q1: np.ndarray
+    q2: np.ndarray
+    final: np.ndarray
+    depth: np.ndarray
+    src: np.ndarray
+    dst: np.ndarray
+    a: np.ndarray
+    c: np.ndarray
+    w: np.ndarray
+    num_premerge: int
+    levels: int
+    seconds: float
+
+    @property
+    def num_states(self) -> int:
+        return int(len(self.q1))
+
+    @property
+    def num_arcs(self) -> int:
+        return int(len(self.src))
+
+
+_ERRORS = {1: "invalid transducer", 2: "alphabet mismatch (|Gamma| of M1 output != M2 input)"}
+
+
+def _collect(lib, h) -> OracleResult:
+    counts = np.zeros(4, np.uint64)
+    lib.oracle_counts(h, counts.ctypes.data)
+    ns, na = int(counts[0]), int(counts[1])
+    q1 = np.empty(ns, np.uint32); q2 = np.empty(ns, np.uint32)
+    fin = np.empty(ns, np.uint8); dep = np.empty(ns, np.uint32)
+    lib.oracle_states(h, q1.ctypes.data, q2.ctypes.data, fin.ctypes.data, dep.ctypes.data)
+    src = np.empty(na, np.uint32); dst = np.empty(na, np.uint32)
+    a = np.empty(na, np.uint32); c = np.empty(na, np.uint32); w = np.empty(na, np.float32)
+    lib.oracle_arcs(h, src.ctypes.data, dst.ctypes.data, a.ctypes.data, c.ctypes.data,
+                    w.ctypes.data)
+    secs = lib.oracle_seconds(h)
+    lib.oracle_free(h)
+    return OracleResult(q1, q2, fin, dep, src, dst, a, c, w, int(counts[2]), int(counts[3]), secs)
+
+
+def compose(m1, m2, max_levels: int = 0, lib_path: Path | None = None) -> OracleResult:
+    """Reachable composition m1 o m2 (max_levels = 0: no level cap)."""
+    lib = _load(lib_path)
+    s1, k1 = _as_struct(m1)
+    s2, k2 = _as_struct(m2)
+    h = ctypes.c_void_p()
+    rc = lib.oracle_compose(ctypes.byref(s1), ctypes.byref(s2), int(max_levels), ctypes.byref(h))
+    del k1, k2
+    if rc != 0:
+        raise OracleError(_ERRORS.get(rc, f"oracle error {rc}"))
+    return _collect(lib, h)
+
+
+def expand_pairs(m1, m2, q1s, q2s, lib_path: Path | None = None) -> OracleResult:
+    """Merged out-arcs of each source pair (q1s[i], q2s[i]) on its own."""
+    lib = _load(lib_path)
+    s1, k1 = _as_struct(m1)
+    s2, k2 = _as_struct(m2)
+    q1s = np.ascontiguousarray(q1s, np.uint32)
+    q2s = np.ascontiguousarray(q2s, np.uint32)
+    h = ctypes.c_void_p()
+    rc = lib.oracle_expand_pairs(ctypes.byref(s1), ctypes.byref(s2), len(q1s),
+                                 q1s.ctypes.data, q2s.ctypes.data, ctypes.byref(h))
+    del k1, k2
+    if rc != 0:
+        raise OracleError(_ERRORS.get(rc, f"oracle error {rc}"))
+    return _collect(lib, h)

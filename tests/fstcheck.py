@@ -1,0 +1,176 @@
+"""Test-side checkers for composed transducers.
+
+Nothing here is part of the oracle or of the HIP path: these are the
+independent pins the oracle is checked against (brute force, path sums,
+accessible part of a single transducer) and the canonical comparison used to
+compare any two composition results.
+
+A composition result, from either side, is described by
+  q1, q2, final  -- per state id: its pair and accept flag
+  src, dst, a, c, w -- per arc: source id, target id, input symbol, output
+                       symbol, weight
+"""
+from __future__ import annotations
+
+from collections import defaultdict, deque
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass
+class Canon:
+    """Result with state ids replaced by their (q1, q2) pairs, sorted."""
+
+    states: np.ndarray   # (n, 2) uint64 rows (q1, q2), lexicographically sorted
+    finals: np.ndarray   # (n,) accept flag aligned with ``states``
+    keys: np.ndarray     # (m, 6) rows (src q1, src q2, dst q1, dst q2, a, c), sorted
+    w: np.ndarray        # (m,) float32 weights aligned with ``keys``
+
+
+def canon(q1, q2, final, src, dst, a, c, w) -> Canon:
+    q1 = np.asarray(q1, np.uint64); q2 = np.asarray(q2, np.uint64)
+    final = np.asarray(final).astype(np.uint8)
+    src = np.asarray(src, np.int64); dst = np.asarray(dst, np.int64)
+    st = np.stack([q1, q2], axis=1)
+    order = np.lexsort((q2, q1))
+    states = st[order]
+    finals = final[order]
+    keys = np.stack([q1[src], q2[src], q1[dst], q2[dst],
+                     np.asarray(a, np.uint64), np.asarray(c, np.uint64)], axis=1)
+    korder = np.lexsort(keys.T[::-1])
+    return Canon(states, finals, keys[korder], np.asarray(w, np.float32)[korder])
+
+
+def canon_of(res) -> Canon:
+    """Canonical form of any object exposing q1, q2, final, src, dst, a, c, w."""
+    return canon(res.q1, res.q2, res.final, res.src, res.dst, res.a, res.c, res.w)
+
+
+def unique_rows(x: np.ndarray) -> bool:
+    if len(x) < 2:
+        return True
+    return bool(np.any(x[1:] != x[:-1], axis=1).all())
+
+
+def assert_same(got: Canon, ref: Canon, rtol: float = 1e-5, what: str = ""):
+    """Bit-exact states, accept flags and arc keys; weights within rtol."""
+    assert unique_rows(got.states), f"{what}: duplicate states"
+    assert unique_rows(got.keys), f"{what}: duplicate arc keys (unmerged arcs)"
+    assert got.states.shape == ref.states.shape, \
+        f"{what}: {len(got.states)} states vs {len(ref.states)}"
+    assert np.array_equal(got.states, ref.states), f"{what}: state sets differ"
+    assert np.array_equal(got.finals, ref.finals), f"{what}: accept flags differ"
+    assert got.keys.shape == ref.keys.shape, f"{what}: {len(got.keys)} arcs vs {len(ref.keys)}"
+    assert np.array_equal(got.keys, ref.keys), f"{what}: arc key sets differ"
+    gw = got.w.astype(np.float64); rw = ref.w.astype(np.float64)
+    err = np.abs(gw - rw)
+    bad = err > rtol * np.abs(rw)
+    if bad.any():
+        i = int(np.argmax(bad))
+        raise AssertionError(f"{what}: {int(bad.sum())} weights off, e.g. key {ref.keys[i]} "
+                             f"got {gw[i]!r} ref {rw[i]!r}")
+
+
+# ---------------------------------------------------------------------------
+# Pins independent of the oracle's structure
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Plain:
+    q1: np.ndarray
+    q2: np.ndarray
+    final: np.ndarray
+    src: np.ndarray
+    dst: np.ndarray
+    a: np.ndarray
+    c: np.ndarray
+    w: np.ndarray
+
+
+def brute_force(m1, m2, max_levels: int = 0) -> Plain:
+    """Naive composition over all of Q1 x Q2, then trimmed to reachable pairs.
+
+    Every M1 arc is joined with every M2 arc that reads its output symbol
+    (all-pairs, §2 / §3.1), identical (src, dst, in, out) arcs are summed, and
+    a textbook BFS on the pair graph from (s1, s2) keeps the reachable pairs
+    (at depth <= max_levels when capped) and the arcs of pairs that are
+    expanded (depth < max_levels when capped).
+    """
+    by_in = defaultdict(list)
+    for e2 in range(m2.num_arcs):
+        by_in[int(m2.ilabel[e2])].append(e2)
+    acc: dict[tuple, float] = {}
+    for e1 in range(m1.num_arcs):
+        for e2 in by_in.get(int(m1.olabel[e1]), ()):
+            key = (int(m1.src[e1]), int(m2.src[e2]), int(m1.dst[e1]), int(m2.dst[e2]),
+                   int(m1.ilabel[e1]), int(m2.olabel[e2]))
+            p = np.float32(m1.weight[e1]) * np.float32(m2.weight[e2])
+            acc[key] = acc.get(key, 0.0) + float(p)
+    succ = defaultdict(set)
+    for k in acc:
+        succ[(k[0], k[1])].add((k[2], k[3]))
+    s = (int(m1.start), int(m2.start))
+    depth = {s: 0}
+    dq = deque([s])
+    while dq:
+        u = dq.popleft()
+        if max_levels and depth[u] >= max_levels:
+            continue
+        for v in sorted(succ.get(u, ())):
+            if v not in depth:
+                depth[v] = depth[u] + 1
+                dq.append(v)
+    states = sorted(depth)
+    sid = {p: i for i, p in enumerate(states)}
+    expanded = {p for p, d in depth.items() if not max_levels or d < max_levels}
+    arcs = [(k, v) for k, v in acc.items() if (k[0], k[1]) in expanded]
+    q1 = np.array([p[0] for p in states], np.uint32)
+    q2 = np.array([p[1] for p in states], np.uint32)
+    fin = np.array([int(m1.final[p[0]] and m2.final[p[1]]) for p in states], np.uint8)
+    src = np.array([sid[(k[0], k[1])] for k, _ in arcs], np.int64)
+    dst = np.array([sid[(k[2], k[3])] for k, _ in arcs], np.int64)
+    a = np.array([k[4] for k, _ in arcs], np.uint32)
+    c = np.array([k[5] for k, _ in arcs], np.uint32)
+    w = np.array([v for _, v in arcs], np.float64).astype(np.float32)
+    return Plain(q1, q2, fin, src, dst, a, c, w)
+
+
+def accessible(m) -> list[int]:
+    """States of a single transducer reachable from its start (BFS)."""
+    succ = defaultdict(set)
+    for e in range(m.num_arcs):
+        succ[int(m.src[e])].add(int(m.dst[e]))
+    seen = {int(m.start)}
+    dq = deque([int(m.start)])
+    while dq:
+        u = dq.popleft()
+        for v in succ.get(u, ()):
+            if v not in seen:
+                seen.add(v)
+                dq.append(v)
+    return sorted(seen)
+
+
+def label_matrices(num_states, start, nin, nout, src, dst, a, c, w):
+    """T[x, y] = num_states x num_states matrix of summed weights of arcs x:y (fp64)."""
+    T = np.zeros((nin, nout, num_states, num_states), np.float64)
+    np.add.at(T, (np.asarray(a, np.int64), np.asarray(c, np.int64),
+                  np.asarray(src, np.int64), np.asarray(dst, np.int64)),
+              np.asarray(w, np.float64))
+    return T
+
+
+def path_weights(T, start, end_vec, length):
+    """W[x_1..x_l, y_1..y_l] = sum over paths from start with those labels of
+    the product of arc weights, ending with weight end_vec[q] at state q.
+    Returned as an array indexed by flattened label tuples (x, y)."""
+    nin, nout, n, _ = T.shape
+    # v[x-seq, y-seq, state], built one step at a time.
+    v = np.zeros((1, 1, n))
+    v[0, 0, start] = 1.0
+    for _ in range(length):
+        # v'[X*nin + x, Y*nout + y, r] = sum_q v[X, Y, q] T[x, y, q, r]
+        nv = np.einsum("XYq,xyqr->XxYyr", v, T)
+        v = nv.reshape(v.shape[0] * nin, v.shape[1] * nout, n)
+    return v @ end_vec

@@ -1,0 +1,110 @@
+"""Planted mistakes in a copy of the oracle (CPU only): each must fail at
+least one of the pins, which shows the pins constrain every part of it.
+
+Each mutant is the oracle source with one plausible slip, compiled to a
+temporary library; the original file is never touched.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.oracle import CXXFLAGS
+from fstcheck import assert_same, brute_force, canon_of, label_matrices, path_weights
+from paper_1805_06383_amd import workloads as W
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "fst_oracle.cpp")
+
+MUTANTS = {
+    # output label taken from M2's input side instead of its output side
+    "wrong_output_label": ("m1->ilabel[e1], m2->olabel[e2]}", "m1->ilabel[e1], m2->ilabel[e2]}"),
+    # input label taken from M1's output side
+    "wrong_input_label": ("m1->ilabel[e1], m2->olabel[e2]}", "m1->olabel[e1], m2->olabel[e2]}"),
+    # join on M1's input symbol instead of its output (inner) symbol
+    "join_on_input": ("const uint32_t b = m1->olabel[e1];", "const uint32_t b = m1->ilabel[e1];"),
+    # one factor of the product dropped
+    "dropped_factor": ("m1->weight[e1] * m2->weight[e2]", "m1->weight[e1] * 1.0f"),
+    # duplicates overwrite instead of adding
+    "no_merge_sum": ("+= (double)prod;", "= (double)prod;"),
+    # target pair transposed
+    "swapped_target": ("ArcKey{m1->dst[e1], m2->dst[e2]", "ArcKey{m2->dst[e2], m1->dst[e1]"),
+    # accept test ignores M2
+    "final_ignores_m2": ("&& m2->final[res.pairs[i].second]", "&& 1"),
+    # level cap off by one
+    "cap_off_by_one": ("res.depth[u] >= max_levels", "res.depth[u] > max_levels"),
+    # new states not searched (no push on the frontier)
+    "no_push": ("        A.push_back(vid);\n", "\n"),
+}
+
+
+def _tiny(seed):
+    rng = np.random.default_rng(seed)
+    m1 = W.tiny_random(rng, 4, 2, 2, 12, final_frac=0.5)
+    m2 = W.tiny_random(rng, 4, 2, 2, 12, final_frac=0.5)
+    return m1, m2
+
+
+def run_pins(lib):
+    """Returns the names of the pins that fail for the library at ``lib``."""
+    failed = set()
+    for seed in range(12):
+        m1, m2 = _tiny(seed)
+        try:
+            got = oracle.compose(m1, m2, lib_path=lib)
+            assert_same(canon_of(got), canon_of(brute_force(m1, m2)), rtol=1e-6)
+        except (AssertionError, IndexError, ValueError):
+            failed.add("brute_force")
+        try:
+            got = oracle.compose(m1, m2, max_levels=2, lib_path=lib)
+            assert_same(canon_of(got), canon_of(brute_force(m1, m2, max_levels=2)), rtol=1e-6)
+        except (AssertionError, IndexError, ValueError):
+            failed.add("brute_force_cap")
+        try:
+            r = oracle.compose(m1, m2, lib_path=lib)
+            T1 = label_matrices(4, 0, 2, 2, m1.src, m1.dst, m1.ilabel, m1.olabel, m1.weight)
+            T2 = label_matrices(4, 0, 2, 2, m2.src, m2.dst, m2.ilabel, m2.olabel, m2.weight)
+            Tc = label_matrices(r.num_states, 0, 2, 2, r.src, r.dst, r.a, r.c, r.w)
+            for ln in (1, 2, 3):
+                W1 = path_weights(T1, m1.start, m1.final.astype(float), ln)
+                W2 = path_weights(T2, m2.start, m2.final.astype(float), ln)
+                Wc = path_weights(Tc, 0, r.final.astype(float), ln)
+                np.testing.assert_allclose(Wc, W1 @ W2, rtol=1e-5, atol=1e-12)
+        except (AssertionError, IndexError, ValueError):
+            failed.add("path_sum")
+    rng = np.random.default_rng(5)
+    A = W.random_weights(rng, 12).reshape(3, 4)
+    B = W.random_weights(rng, 8).reshape(4, 2)
+    try:
+        r = oracle.compose(W.one_state_dense(A), W.one_state_dense(B), lib_path=lib)
+        P = A.astype(np.float64) @ B.astype(np.float64)
+        np.testing.assert_allclose(r.w.astype(np.float64), P[r.a, r.c], rtol=1e-6)
+        assert r.num_arcs == 6
+    except (AssertionError, IndexError, ValueError):
+        failed.add("matrix_product")
+    return failed
+
+
+@pytest.fixture(scope="module")
+def mutant_dir(tmp_path_factory):
+    return tmp_path_factory.mktemp("oracle_mutants")
+
+
+def test_unmutated_copy_passes(mutant_dir):
+    out = mutant_dir / "liboracle_clean.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(out), SRC], check=True)
+    assert run_pins(out) == set()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, mutant_dir):
+    old, new = MUTANTS[name]
+    text = open(SRC).read()
+    assert text.count(old) >= 1, f"mutation site for {name} not found"
+    src = mutant_dir / f"{name}.cpp"
+    src.write_text(text.replace(old, new))
+    out = mutant_dir / f"lib{name}.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(out), str(src)], check=True)
+    failed = run_pins(out)
+    assert failed, f"planted mistake {name} passed every pin"
