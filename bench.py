@@ -1,0 +1,173 @@
+"""Throughput of reachable-state weighted FST composition on one MI355X.
+
+One step = one fstc_compose call over the whole workload (CSR build of both
+inputs, every breadth-first level: join count, arc-pair write, merge,
+visited-table insert, id assignment, result append), inputs already resident
+in HBM.  Prints one JSON line.
+
+Default workload: the HMM-like dense-inner-alphabet pair (|Q1| = |Q2| = 1000,
+64 inner symbols, 4 (outer symbol, target) slots per state, 256 arcs per
+state, seed 0), the configuration the HBM-fraction target is stated on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "composed arcs/sec (pre- and post-merge) + HBM GB/s fraction, 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+WORKLOAD_NAMES = {
+    1: "tiny random pair: |Q|=200, |Sigma|=|Delta|=50, |Gamma|=100, 2,000 arcs each",
+    2: "medium sparse pair: |Q|=10,000, 200,000 arcs each, inner Zipf(1.0) over 5,000, outer 2,000",
+    3: "lexicon trie pair: 50,000 words (3-12 of 30 chars), |Gamma|=50,000, 1-5 translations Zipf(1.1) over 20,000",
+    4: "HMM-like dense inner alphabet: |Q1|=|Q2|=1,000, m=64, 4 (outer, target) slots x 64 inner symbols = 256 arcs/state, |Sigma|=|Delta|=64",
+    5: "large power-law pair: |Q|=1,000,000, 20M arcs each, degree ~ d^-2.1 on [4, 10^4], inner Zipf(1.0) over 10^5",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--max-levels", type=int, default=0)
+    ap.add_argument("--oracle-levels", type=int, default=5,
+                    help="level cap of the bounded CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(st: dict, R: int, merged: int) -> dict:
+    """Bytes each of the two dominant kernels must move, per compose call.
+
+    write kernel: every unmerged record written once (key + float32 weight)
+      plus one 24-byte match descriptor read per matched (source, symbol);
+    merge kernel: every record of a tile-merged source read once, every
+      merged arc written once (16 bytes: slot, a, c, weight) and its target
+      pair probed once in the visited table (8-byte key).
+    """
+    rec = st["record_key_bytes"] + 4
+    tile_records = R - st["total_big_records"]
+    return {
+        "write": R * rec + st["total_matches"] * 24,
+        "merge": tile_records * rec + merged * (16 + 8),
+    }
+
+
+def cpu_baseline(m1, m2, levels: int) -> dict:
+    import oracle
+    r = oracle.compose(m1, m2, max_levels=levels)
+    return {
+        "value": r.num_premerge / r.seconds,
+        "unit": "arcs/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"same workload with the breadth-first search capped at depth {levels}: "
+                   f"{r.num_premerge} unmerged / {r.num_arcs} merged arcs, "
+                   f"{r.num_states} states, {r.seconds:.2f} s on 1 of {os.cpu_count()} host "
+                   f"cores ({platform.processor() or platform.machine()}); value = unmerged arcs/s"),
+        "post_merge_value": r.num_arcs / r.seconds,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the composition is not sharded across GPUs", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1805_06383_amd import fstc
+    from paper_1805_06383_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    h1, h2 = W.make_config(args.config, args.seed)
+    m1 = fstc.DeviceFST.from_host(h1, dev)
+    m2 = fstc.DeviceFST.from_host(h2, dev)
+    torch.cuda.synchronize()
+
+    def step():
+        return fstc.fstc_compose(m1, m2, max_levels=args.max_levels)
+
+    for _ in range(args.warmup):
+        r = step()
+        del r
+    torch.cuda.synchronize()
+    sums = {}
+    last = None
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        last = step()
+        for k, v in last.stats.items():
+            sums[k] = sums.get(k, 0) + v
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    secs = t1 - t0
+    R, merged = last.num_premerge_arcs, last.num_arcs
+    pre_rate = R * args.steps / secs
+    post_rate = merged * args.steps / secs
+
+    st = last.stats
+    ab = algorithmic_bytes(st, R, merged)
+    kern = {}
+    for name, ms_key, n_key in (("write", "ms_write_kernel", "write_launches"),
+                                ("merge", "ms_merge_kernel", "merge_launches")):
+        ms = sums[ms_key] / args.steps
+        launches = max(1, st[n_key])
+        gbs = ab[name] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+        kern[name] = {"ms_per_step": ms, "launches_per_step": st[n_key],
+                      "avg_launch_ms": ms / launches, "bytes_per_step": ab[name],
+                      "bytes_per_launch": ab[name] / launches, "GBps": gbs}
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    roof = {"bound": "hbm", "kernel": {"write": "k_expand", "merge": "k_merge_tiles"}[dom],
+            "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": kern[dom]["GBps"] / HBM_PEAK_GBS, "traffic": None}
+
+    out = {
+        "metric": METRIC,
+        "value": pre_rate,
+        "unit": "arcs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": secs * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"config {args.config}: {WORKLOAD_NAMES[args.config]}, seed {args.seed}"
+                        + (f", depth cap {args.max_levels}" if args.max_levels else ""),
+            "states": last.num_states,
+            "premerge_arcs": R,
+            "merged_arcs": merged,
+            "levels": last.num_levels,
+            "input_sha256": [h1.digest()[:16], h2.digest()[:16]],
+        },
+        "post_merge_arcs_per_s": post_rate,
+        "phase_ms_per_step": {k: sums[k] / args.steps for k in
+                              ("ms_csr", "ms_count", "ms_expand", "ms_merge", "ms_assign")},
+        "kernels": kern,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

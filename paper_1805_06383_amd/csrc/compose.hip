@@ -1,0 +1,658 @@
+// Host driver of the composition and the C ABI (include/fstc.h).
+//
+// Algorithm 2 of the paper keeps the frontier queue on the host and
+// launches work per popped pair, which the authors name as the largest
+// bottleneck (section 5).  Here the frontier and the visited set live on the
+// device and a whole breadth-first level is expanded per step:
+//
+//   per level (sources = the state ids found at the previous level):
+//     count + scan          -> records and matches per source      (sync 1)
+//     emit + write          -> unmerged composed arcs (records)
+//     merge                 -> merged arcs, new pairs claimed in the hash
+//     scan                  -> merged arcs per source              (sync 2)
+//     assign + append       -> ids for new pairs, arcs to the result
+//
+// The host reads a few counters twice per level; everything else stays in
+// HBM.  Buffers are grow-only and come from the caller's allocator (PyTorch's
+// caching allocator in the Python binding) or hipMallocAsync.
+#include <chrono>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <vector>
+
+#include "level.hpp"
+
+namespace fstc {
+
+// ---------------------------------------------------------------------------
+void *Allocator::alloc(size_t bytes) {
+  bytes = std::max<size_t>(256, (bytes + 255) & ~(size_t)255);
+  void *p = nullptr;
+  if (fa) {
+    p = fa(bytes, ctx, stream);
+  } else {
+    if (hipMallocAsync(&p, bytes, stream) != hipSuccess) p = nullptr;
+    if (!p) (void)hipGetLastError();
+  }
+  if (!p) throw Error(FSTC_ERR_OOM, "device allocation of " + std::to_string(bytes) + " bytes failed");
+  live_bytes += bytes;
+  peak_bytes = std::max(peak_bytes, live_bytes);
+  return p;
+}
+
+void Allocator::free(void *p, size_t bytes) {
+  if (!p) return;
+  bytes = std::max<size_t>(256, (bytes + 255) & ~(size_t)255);
+  if (ff) ff(p, bytes, ctx, stream);
+  else (void)hipFreeAsync(p, stream);
+  live_bytes -= std::min<u64>(live_bytes, bytes);
+}
+
+void *Buf::ensure(size_t bytes) {
+  if (bytes <= cap && p) return p;
+  release();
+  const size_t c = std::max<size_t>(256, (bytes + 255) & ~(size_t)255);
+  p = A->alloc(c);
+  cap = c;
+  return p;
+}
+
+void *Buf::grow_keep(size_t bytes, size_t used) {
+  if (bytes <= cap && p) return p;
+  const size_t c = std::max<size_t>(std::max<size_t>(256, (bytes + 255) & ~(size_t)255), 2 * cap);
+  void *q = A->alloc(c);
+  if (used && p) FSTC_HIP(hipMemcpyAsync(q, p, used, hipMemcpyDeviceToDevice, A->stream));
+  release();
+  p = q;
+  cap = c;
+  return p;
+}
+
+namespace {
+
+thread_local std::string g_detail;
+
+// Per-thread page-locked staging for the few counters the host reads.
+struct Staging {
+  Status st;
+  u64 words[16];
+};
+
+Staging *staging() {
+  thread_local Staging *p = nullptr;
+  if (!p) FSTC_HIP(hipHostMalloc((void **)&p, sizeof(Staging), hipHostMallocDefault));
+  return p;
+}
+
+// Keep freed blocks of the default stream-ordered pool instead of returning
+// them to the driver at every synchronisation.
+void tune_default_pool() {
+  static std::once_flag once;
+  std::call_once(once, [] {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return;
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) != hipSuccess) return;
+    uint64_t thr = ~0ull;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+    (void)hipGetLastError();
+  });
+}
+
+u64 next_pow2(u64 x) {
+  u64 p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+const char *device_error_text(u32 e) {
+  if (e & kErrBadArc) return "an arc's state or label is out of range";
+  if (e & kErrHashFull) return "visited table full";
+  if (e & kErrNewList) return "new-state list overflow";
+  if (e & kErrTileSize) return "merge tile exceeded its capacity";
+  return "device index check failed";
+}
+
+enum Phase { kCsr, kCount, kExpand, kMerge, kAssign, kWriteKernel, kMergeKernel, kNumPhases };
+
+// HIP-event timing of the phases on the call's stream (only with stats).
+struct Timer {
+  hipStream_t s = nullptr;
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> spans;
+  hipEvent_t open = nullptr;
+  size_t used = 0;
+
+  hipEvent_t get() {
+    if (used == pool.size()) {
+      hipEvent_t e;
+      FSTC_HIP(hipEventCreate(&e));
+      pool.push_back(e);
+    }
+    return pool[used++];
+  }
+  void begin() {
+    if (!on) return;
+    open = get();
+    FSTC_HIP(hipEventRecord(open, s));
+  }
+  void end(int phase) {
+    if (!on) return;
+    hipEvent_t e = get();
+    FSTC_HIP(hipEventRecord(e, s));
+    spans.push_back({phase, {open, e}});
+  }
+  void totals(double *ms) {
+    for (auto &sp : spans) {
+      float t = 0.f;
+      if (hipEventElapsedTime(&t, sp.second.first, sp.second.second) == hipSuccess) ms[sp.first] += t;
+    }
+  }
+  ~Timer() {
+    for (auto e : pool) (void)hipEventDestroy(e);
+  }
+};
+
+struct Composer {
+  const fstc_fst &m1, &m2;
+  fstc_opts o{};
+  hipStream_t s;
+  fstc_stats *stats;
+  Allocator A;
+  Timer T;
+  Staging *hs = nullptr;
+  Status *dst = nullptr;
+  u32 nsyncs = 0;
+
+  Composer(const fstc_fst &a, const fstc_fst &b, const fstc_opts *opts, hipStream_t st,
+           fstc_stats *sp)
+      : m1(a), m2(b), s(st), stats(sp) {
+    if (opts) o = *opts;
+    A.fa = o.alloc;
+    A.ff = o.free;
+    A.ctx = o.alloc_ctx;
+    A.stream = s;
+    T.s = s;
+    T.on = stats != nullptr;
+  }
+
+  void sync_status() {
+    FSTC_HIP(hipGetLastError());
+    FSTC_HIP(hipMemcpyAsync(&hs->st, dst, sizeof(Status), hipMemcpyDeviceToHost, s));
+    FSTC_HIP(hipStreamSynchronize(s));
+    ++nsyncs;
+    if (hs->st.err) {
+      throw Error((hs->st.err & kErrBadArc) ? FSTC_ERR_INVALID_ARG : FSTC_ERR_INTERNAL,
+                  device_error_text(hs->st.err));
+    }
+  }
+
+  void read_words(const u64 *d, int n) {
+    FSTC_HIP(hipGetLastError());
+    FSTC_HIP(hipMemcpyAsync(hs->words, d, n * sizeof(u64), hipMemcpyDeviceToHost, s));
+    FSTC_HIP(hipStreamSynchronize(s));
+    ++nsyncs;
+  }
+
+  void run(fstc_result *out);
+};
+
+void Composer::run(fstc_result *out) {
+  const auto t0 = std::chrono::steady_clock::now();
+  if (!o.alloc) tune_default_pool();
+  hs = staging();
+
+  Buf stb(&A), cntb(&A);
+  dst = (Status *)stb.ensure(sizeof(Status));
+  u64 *dcounts = (u64 *)cntb.ensure(8 * sizeof(u64));
+  fill_u32((u32 *)dst, 0, sizeof(Status) / 4, s);
+
+  // (a0) device layout of both inputs
+  Buf cb1[7], cb2[7];
+  Csr c1, c2;
+  alloc_csr(m1, A, cb1, c1);
+  alloc_csr(m2, A, cb2, c2);
+  T.begin();
+  build_csr(m1, true, A, c1, dcounts + 0, &dst->err, s);
+  build_csr(m2, false, A, c2, dcounts + 3, &dst->err, s);
+  T.end(kCsr);
+  sync_status();
+  read_words(dcounts, 6);
+  const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
+  const int b1 = (int)bits_for(maxp1 ? maxp1 - 1 : 0);
+  const int b2 = (int)bits_for(maxp2 ? maxp2 - 1 : 0);
+  const int key_bits = b1 + b2;
+  if (key_bits > kMaxKeyBits)
+    throw Error(FSTC_ERR_RANGE, "per-state (target, outer symbol) ranks need " +
+                                    std::to_string(key_bits) + " > 40 key bits");
+  const bool wide_keys = key_bits > 32;
+  const size_t rec_bytes = wide_keys ? 8 : 4;
+
+  // (a1) states, visited table, start pair
+  const u64 pairspace = (u64)m1.num_states * (u64)m2.num_states;
+  u64 state_limit = std::min<u64>(pairspace, 0xffffffffull);
+  if (o.max_states) state_limit = std::min<u64>(state_limit, o.max_states);
+  Buf sq1b(&A), sq2b(&A), hkb(&A), hvb(&A);
+  sq1b.ensure(1024 * 4);
+  sq2b.ensure(1024 * 4);
+  u64 hcap = next_pow2(std::max<u64>(4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1)));
+  hkb.ensure(hcap * 8);
+  hvb.ensure(hcap * 4);
+  fill_u64(hkb.as<u64>(), kEmptyKey, hcap, s);
+  launch_insert_start(hkb.as<u64>(), hcap - 1, hvb.as<u32>(), m1.start, m2.start, sq1b.as<u32>(),
+                      sq2b.as<u32>(), &dst->err, s);
+
+  u64 n_states = 1, arcs = 0, premerge = 0;
+  u32 lo = 0, hi = 1, depth = 0, new_levels = 0, expanded_levels = 0;
+  u64 max_frontier = 0, max_level_pre = 0, big_total = 0, total_matches = 0, big_records = 0;
+  u32 write_launches = 0, merge_launches = 0;
+
+  Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
+  Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
+      bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
+      stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A);
+
+  while (true) {
+    if (o.max_levels && depth >= o.max_levels) break;
+    const u32 nsrc = hi - lo;
+    if (nsrc == 0) break;
+    ++expanded_levels;
+    max_frontier = std::max<u64>(max_frontier, nsrc);
+    const u64 np1 = (u64)nsrc + 1;
+    cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
+    mcount.ensure(np1 * 4); aoff.ensure(np1 * 8);
+    wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
+    stmp.ensure(scan_temp_bytes(np1));
+
+    // (a2, a3) join counts and offsets
+    launch_reset_level(dst, s);
+    LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
+                 mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
+                 dst, nullptr, nullptr};
+    T.begin();
+    launch_count(la, s);
+    exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
+    exclusive_scan(mc.as<u32>(), moff.as<u64>(), nsrc, stmp.p, s);
+    launch_collect_big(roff.as<u64>(), nsrc, big.as<u32>(), dst, s);
+    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, s);
+    T.end(kCount);
+    sync_status();
+    const u64 R = hs->st.R, M = hs->st.M;
+    const u32 nbig = hs->st.nbig;
+    if (R == 0) break;  // no arc leaves this level: no new states either
+    premerge += R;
+    max_level_pre = std::max(max_level_pre, R);
+    big_total += nbig;
+
+    match.ensure(M * sizeof(uint4));
+    mrbase.ensure(M * 8);
+    rkey.ensure(R * rec_bytes);
+    rw.ensure(R * 4);
+    temp.ensure(R * sizeof(uint4));
+    const u64 newcap = std::min<u64>(R, pairspace - n_states);
+    newlist.ensure(std::max<u64>(newcap, 1) * 4);
+
+    // visited table: keep the load factor at most 1/2 for every pair this
+    // level could add
+    const u64 need = 2 * (n_states + newcap);
+    if (need > hcap) {
+      const u64 ncap = next_pow2(need);
+      Buf nk(&A), nv(&A);
+      nk.ensure(ncap * 8);
+      nv.ensure(ncap * 4);
+      fill_u64(nk.as<u64>(), kEmptyKey, ncap, s);
+      launch_rehash(hkb.as<u64>(), hvb.as<u32>(), hcap, nk.as<u64>(), nv.as<u32>(), ncap - 1,
+                    &dst->err, s);
+      std::swap(hkb.p, nk.p); std::swap(hkb.cap, nk.cap);
+      std::swap(hvb.p, nv.p); std::swap(hvb.cap, nv.cap);
+      hcap = ncap;
+    }
+
+    // (a4) match descriptors and the arc-pair write pass
+    la.match = match.as<uint4>();
+    la.mrbase = mrbase.as<u64>();
+    T.begin();
+    launch_emit(la, s);
+    T.end(kExpand);
+    T.begin();
+    launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
+                  rkey.p, rw.as<float>(), &dst->err, s);
+    T.end(kWriteKernel);
+    ++write_launches;
+    total_matches += M;
+
+    // (a6) merge identical arcs, claim new pairs
+    T.begin();
+    fill_u32(mcount.as<u32>(), 0, nsrc, s);
+    MergeArgs ma{};
+    ma.rec_key = rkey.p;
+    ma.rec_w = rw.as<float>();
+    ma.R = R;
+    ma.roff = roff.as<u64>();
+    ma.nsrc = nsrc;
+    ma.lo = lo;
+    ma.sq1 = sq1b.as<u32>();
+    ma.sq2 = sq2b.as<u32>();
+    ma.pbase1 = c1.part_base;
+    ma.pbase2 = c2.part_base;
+    ma.parts1 = c1.parts;
+    ma.parts2 = c2.parts;
+    ma.key_bits = key_bits;
+    ma.b2 = b2;
+    ma.hkeys = hkb.as<u64>();
+    ma.hmask = hcap - 1;
+    ma.newlist = newlist.as<u32>();
+    ma.newcap = newcap;
+    ma.temp = temp.as<uint4>();
+    ma.mcount = mcount.as<u32>();
+    ma.st = dst;
+    ma.big = big.as<u32>();
+    T.end(kMerge);
+    T.begin();
+    launch_merge_tiles(ma, wide_keys, s);
+    T.end(kMergeKernel);
+    ++merge_launches;
+    T.begin();
+    if (nbig) {
+      bigcnt.ensure((u64)nbig * 8);
+      bigoff.ensure(((u64)nbig + 1) * 8);
+      launch_big_counts(roff.as<u64>(), big.as<u32>(), nbig, bigcnt.as<u64>(), s);
+      exclusive_scan(bigcnt.as<u64>(), bigoff.as<u64>(), nbig, stmp.p, s);
+      read_words(bigoff.as<u64>() + nbig, 1);
+      const u64 RB = hs->words[0];
+      big_records += RB;
+      merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, A, s);
+    }
+    exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
+    launch_merged_total(aoff.as<u64>() + nsrc, dst, s);
+    T.end(kMerge);
+    sync_status();
+    const u32 nnew = hs->st.nnew;
+    const u64 merged = hs->st.merged;
+    if (n_states + nnew > state_limit)
+      throw Error(FSTC_ERR_CAPACITY, "reachable states exceed the state limit");
+    if (o.max_arcs && arcs + merged > o.max_arcs)
+      throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");
+
+    // (a5) ids for the new pairs; (a7) append the level's arcs
+    T.begin();
+    const u64 ns_new = n_states + nnew;
+    sq1b.grow_keep(ns_new * 4, n_states * 4);
+    sq2b.grow_keep(ns_new * 4, n_states * 4);
+    const u32 *slots = newlist.as<u32>();
+    if (o.deterministic_ids && nnew > 1) {
+      const int bq1 = (int)bits_for(m1.num_states - 1), bq2 = (int)bits_for(m2.num_states - 1);
+      dk.ensure((u64)nnew * 8); dv.ensure((u64)nnew * 4);
+      dka.ensure((u64)nnew * 8); dva.ensure((u64)nnew * 4);
+      dtmp.ensure(radix_temp_bytes(nnew));
+      launch_newkeys(newlist.as<u32>(), nnew, hkb.as<u64>(), bq2, dk.as<u64>(), dv.as<u32>(), s);
+      radix_sort_pairs(dk.as<u64>(), dv.as<u32>(), dka.as<u64>(), dva.as<u32>(), nnew, 0,
+                       bq1 + bq2, dtmp.p, s);
+      slots = dv.as<u32>();
+    }
+    launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), sq1b.as<u32>(),
+                  sq2b.as<u32>(), s);
+    if (merged) {
+      const u64 na = arcs + merged;
+      osrc.grow_keep(na * 4, arcs * 4);
+      odst.grow_keep(na * 4, arcs * 4);
+      oil.grow_keep(na * 4, arcs * 4);
+      ool.grow_keep(na * 4, arcs * 4);
+      ow.grow_keep(na * 4, arcs * 4);
+      launch_compact(temp.as<uint4>(), roff.as<u64>(), aoff.as<u64>(), nsrc, lo, merged,
+                     hvb.as<u32>(), osrc.as<u32>() + arcs, odst.as<u32>() + arcs,
+                     oil.as<u32>() + arcs, ool.as<u32>() + arcs, ow.as<float>() + arcs,
+                     &dst->err, s);
+    }
+    T.end(kAssign);
+    arcs += merged;
+    n_states = ns_new;
+    if (nnew) ++new_levels;
+    lo = hi;
+    hi = (u32)n_states;
+    ++depth;
+  }
+
+  // (a7) accept states
+  Buf finb(&A);
+  finb.ensure(n_states);
+  launch_finals(sq1b.as<u32>(), sq2b.as<u32>(), n_states, m1.final, m2.final, finb.as<uint8_t>(), s);
+  sync_status();
+
+  std::memset(out, 0, sizeof(*out));
+  out->num_states = n_states;
+  out->num_arcs = arcs;
+  out->num_premerge_arcs = premerge;
+  out->num_levels = new_levels + 1;
+  Buf *keep[8] = {&sq1b, &sq2b, &finb, &osrc, &odst, &oil, &ool, &ow};
+  void **fields[8] = {(void **)&out->state_q1, (void **)&out->state_q2, (void **)&out->final,
+                      (void **)&out->src, (void **)&out->dst, (void **)&out->ilabel,
+                      (void **)&out->olabel, (void **)&out->weight};
+  for (int i = 0; i < 8; ++i) {
+    size_t b = 0;
+    void *p = keep[i]->detach(&b);
+    out->alloc_ptr[i] = p;
+    out->alloc_bytes[i] = b;
+    *fields[i] = p;
+  }
+  if (stats) {
+    double ms[kNumPhases] = {};
+    T.totals(ms);
+    stats->ms_write_kernel = ms[kWriteKernel];
+    stats->ms_merge_kernel = ms[kMergeKernel];
+    stats->write_launches = write_launches;
+    stats->merge_launches = merge_launches;
+    stats->total_matches = total_matches;
+    stats->total_big_records = big_records;
+    stats->record_key_bytes = (u32)rec_bytes;
+    stats->key_bits = (u32)key_bits;
+    stats->num_levels = expanded_levels;
+    stats->num_host_syncs = nsyncs;
+    stats->max_frontier = max_frontier;
+    stats->max_level_premerge = max_level_pre;
+    stats->big_sources = big_total;
+    stats->hash_capacity = hcap;
+    stats->ms_csr = ms[kCsr];
+    stats->ms_count = ms[kCount];
+    stats->ms_expand = ms[kExpand] + ms[kWriteKernel];
+    stats->ms_merge = ms[kMerge] + ms[kMergeKernel];
+    stats->ms_assign = ms[kAssign];
+    stats->ms_total =
+        std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  }
+}
+
+int fail(int code, const std::string &msg) {
+  g_detail = msg;
+  return code;
+}
+
+int check_fst(const fstc_fst *m, const char *name) {
+  if (!m) return fail(FSTC_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  if (m->num_states == 0) return fail(FSTC_ERR_INVALID_ARG, std::string(name) + ": num_states is 0");
+  if (m->start >= m->num_states)
+    return fail(FSTC_ERR_INVALID_ARG, std::string(name) + ": start >= num_states");
+  if (!m->final) return fail(FSTC_ERR_INVALID_ARG, std::string(name) + ": final is NULL");
+  if (m->num_arcs && (!m->src || !m->dst || !m->ilabel || !m->olabel || !m->weight))
+    return fail(FSTC_ERR_INVALID_ARG, std::string(name) + ": an arc array is NULL");
+  if (m->num_arcs >= (1ull << 32))
+    return fail(FSTC_ERR_RANGE, std::string(name) + ": num_arcs must be below 2^32");
+  return FSTC_OK;
+}
+
+int run_guarded(const char *what, hipStream_t s, const std::function<void()> &f) {
+  try {
+    f();
+    return FSTC_OK;
+  } catch (const Error &e) {
+    (void)hipStreamSynchronize(s);
+    (void)hipGetLastError();
+    return fail(e.code, std::string(what) + ": " + e.what());
+  } catch (const std::bad_alloc &) {
+    return fail(FSTC_ERR_OOM, std::string(what) + ": host allocation failed");
+  } catch (const std::exception &e) {
+    return fail(FSTC_ERR_INTERNAL, std::string(what) + ": " + e.what());
+  }
+}
+
+__global__ void k_split_uint2(const uint2 *in, u64 n, u32 *x, u32 *y) {
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
+    const uint2 v = in[i];
+    x[i] = v.x;
+    y[i] = v.y;
+  }
+}
+
+}  // namespace
+}  // namespace fstc
+
+using namespace fstc;
+
+extern "C" {
+
+int fstc_compose(const fstc_fst *m1, const fstc_fst *m2, const fstc_opts *opts,
+                 hipStream_t stream, fstc_result *out, fstc_stats *stats) {
+  if (out) std::memset(out, 0, sizeof(*out));
+  if (stats) std::memset(stats, 0, sizeof(*stats));
+  if (!out) return fail(FSTC_ERR_INVALID_ARG, "out is NULL");
+  int rc = check_fst(m1, "m1");
+  if (rc) return rc;
+  rc = check_fst(m2, "m2");
+  if (rc) return rc;
+  if (m1->num_osyms != m2->num_isyms)
+    return fail(FSTC_ERR_ALPHABET, "m1->num_osyms != m2->num_isyms");
+  if (opts && ((opts->alloc == nullptr) != (opts->free == nullptr)))
+    return fail(FSTC_ERR_INVALID_ARG, "opts->alloc and opts->free must be set together");
+  try {
+    check_csr_ranges(*m1, true);
+    check_csr_ranges(*m2, false);
+  } catch (const Error &e) {
+    return fail(e.code, e.what());
+  }
+  return run_guarded("fstc_compose", stream, [&] {
+    Composer c(*m1, *m2, opts, stream, stats);
+    c.run(out);
+  });
+}
+
+void fstc_result_release(fstc_result *r, const fstc_opts *opts, hipStream_t stream) {
+  if (!r) return;
+  Allocator A;
+  if (opts) {
+    A.fa = opts->alloc;
+    A.ff = opts->free;
+    A.ctx = opts->alloc_ctx;
+  }
+  A.stream = stream;
+  for (int i = 0; i < 8; ++i)
+    if (r->alloc_ptr[i]) A.free(r->alloc_ptr[i], r->alloc_bytes[i]);
+  std::memset(r, 0, sizeof(*r));
+}
+
+int fstc_build_csr(const fstc_fst *m, int by_output, hipStream_t stream, uint32_t *row,
+                   uint32_t *seg_sym, uint32_t *seg_off, uint32_t *arc_part, float *arc_weight,
+                   uint32_t *part_base, uint32_t *part_target, uint32_t *part_outer,
+                   uint64_t *counts) {
+  int rc = check_fst(m, "m");
+  if (rc) return rc;
+  if (!row || !seg_off || !part_base || !counts)
+    return fail(FSTC_ERR_INVALID_ARG, "an output array is NULL");
+  if (m->num_arcs && (!seg_sym || !arc_part || !arc_weight || !part_target || !part_outer))
+    return fail(FSTC_ERR_INVALID_ARG, "an output array is NULL");
+  try {
+    check_csr_ranges(*m, by_output != 0);
+  } catch (const Error &e) {
+    return fail(e.code, e.what());
+  }
+  return run_guarded("fstc_build_csr", stream, [&] {
+    Allocator A;
+    A.stream = stream;
+    tune_default_pool();
+    const u64 n = m->num_arcs;
+    Buf arcs(&A), parts(&A), dc(&A), de(&A);
+    Csr c;
+    c.num_states = m->num_states;
+    c.num_arcs = n;
+    c.row = row;
+    c.seg_sym = seg_sym;
+    c.seg_off = seg_off;
+    c.part_base = part_base;
+    c.arcs = (uint2 *)arcs.ensure(std::max<u64>(n, 1) * sizeof(uint2));
+    c.parts = (uint2 *)parts.ensure(std::max<u64>(n, 1) * sizeof(uint2));
+    u64 *d_counts = (u64 *)dc.ensure(3 * 8);
+    u32 *d_err = (u32 *)de.ensure(4);
+    fill_u32(d_err, 0, 1, stream);
+    build_csr(*m, by_output != 0, A, c, d_counts, d_err, stream);
+    if (n) {
+      const unsigned g = (unsigned)std::min<u64>(ceil_div(n, 256), 1u << 16);
+      hipLaunchKernelGGL(k_split_uint2, dim3(g), dim3(256), 0, stream, c.arcs, n, arc_part,
+                         (u32 *)arc_weight);
+      hipLaunchKernelGGL(k_split_uint2, dim3(g), dim3(256), 0, stream, c.parts, n, part_target,
+                         part_outer);
+    }
+    Staging *hs = staging();
+    FSTC_HIP(hipGetLastError());
+    FSTC_HIP(hipMemcpyAsync(hs->words, d_counts, 3 * 8, hipMemcpyDeviceToHost, stream));
+    FSTC_HIP(hipMemcpyAsync(&hs->st.err, d_err, 4, hipMemcpyDeviceToHost, stream));
+    FSTC_HIP(hipStreamSynchronize(stream));
+    if (hs->st.err) throw Error(FSTC_ERR_INVALID_ARG, device_error_text(hs->st.err));
+    counts[0] = hs->words[0];
+    counts[1] = hs->words[1];
+    counts[2] = hs->words[2];
+  });
+}
+
+int fstc_sort_pairs(uint64_t *keys, uint32_t *values, uint64_t n, int bit_lo, int bit_hi,
+                    hipStream_t stream) {
+  if (n && (!keys || !values)) return fail(FSTC_ERR_INVALID_ARG, "keys or values is NULL");
+  if (bit_lo < 0 || bit_hi > 64 || bit_lo > bit_hi)
+    return fail(FSTC_ERR_INVALID_ARG, "bit range must satisfy 0 <= lo <= hi <= 64");
+  if (n >= (1ull << 32)) return fail(FSTC_ERR_RANGE, "n must be below 2^32");
+  return run_guarded("fstc_sort_pairs", stream, [&] {
+    if (n <= 1 || bit_lo == bit_hi) return;
+    Allocator A;
+    A.stream = stream;
+    tune_default_pool();
+    Buf ka(&A), va(&A), tmp(&A);
+    ka.ensure(n * 8);
+    va.ensure(n * 4);
+    tmp.ensure(radix_temp_bytes(n));
+    radix_sort_pairs(keys, values, ka.as<u64>(), va.as<u32>(), n, bit_lo, bit_hi, tmp.p, stream);
+    FSTC_HIP(hipGetLastError());
+  });
+}
+
+int fstc_exclusive_scan_u64(const uint64_t *in, uint64_t *out, uint64_t n, hipStream_t stream) {
+  if (!out || (n && !in)) return fail(FSTC_ERR_INVALID_ARG, "in or out is NULL");
+  return run_guarded("fstc_exclusive_scan_u64", stream, [&] {
+    Allocator A;
+    A.stream = stream;
+    tune_default_pool();
+    Buf tmp(&A);
+    tmp.ensure(scan_temp_bytes(n));
+    exclusive_scan(in, out, n, tmp.p, stream);
+    FSTC_HIP(hipGetLastError());
+  });
+}
+
+const char *fstc_strerror(int code) {
+  switch (code) {
+    case FSTC_OK: return "success";
+    case FSTC_ERR_INVALID_ARG: return "invalid argument";
+    case FSTC_ERR_ALPHABET: return "alphabet mismatch: m1 output alphabet != m2 input alphabet";
+    case FSTC_ERR_RANGE: return "size exceeds a packing limit";
+    case FSTC_ERR_CAPACITY: return "result exceeds a capacity limit";
+    case FSTC_ERR_OOM: return "device allocation failed";
+    case FSTC_ERR_HIP: return "HIP runtime error";
+    case FSTC_ERR_INTERNAL: return "internal consistency check failed";
+    default: return "unknown error code";
+  }
+}
+
+const char *fstc_last_error_detail(void) { return g_detail.c_str(); }
+
+const char *fstc_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,124 @@
+// Per-level kernels of the breadth-first composition: shared arguments and
+// launchers (expand.hip: join count, match emission, arc-pair write;
+// merge.hip: segmented sort + reduce, visited-table insert, id assignment,
+// result append).
+#pragma once
+
+#include "internal.hpp"
+
+namespace fstc {
+
+// Read-only view of a Csr on the device.
+struct CsrView {
+  const u32 *row, *seg_sym, *seg_off;
+  const uint2 *arcs;
+  const u32 *part_base;
+  const uint2 *parts;
+};
+
+inline CsrView view(const Csr &c) {
+  return CsrView{c.row, c.seg_sym, c.seg_off, c.arcs, c.part_base, c.parts};
+}
+
+// Host-visible per-level counters (one D2H copy per synchronisation).
+struct Status {
+  u64 R;        // unmerged composed arcs of the level
+  u64 M;        // matched (source, inner symbol) segment pairs of the level
+  u64 merged;   // merged arcs of the level
+  u64 RB;       // records of sources merged by the multi-block path
+  u32 nwide, nheavy, nbig, nnew;
+  u32 err;      // kErr* bits, sticky for the whole call
+  u32 pad[3];
+};
+
+// A source whose shorter segment list is longer than kWideMin is joined by a
+// wavefront, longer than kHeavyMin by a workgroup; others by one thread.
+constexpr u32 kWideMin = 24;
+constexpr u32 kHeavyMin = 2048;
+
+// Merge tiles: 512 threads x 8 items = 4096 records of LDS capacity; a tile
+// takes the sources whose first record falls in a 2048-record window, so
+// every source of at most 2048 records fits.  Larger sources take the
+// multi-block path.
+constexpr int kMergeNT = 512;
+constexpr int kMergeIT = 8;
+constexpr int kMergeCap = kMergeNT * kMergeIT;
+constexpr u64 kMergeWindow = kMergeCap / 2;
+constexpr int kIdxBits = 12;  // log2(kMergeCap)
+constexpr int kMaxKeyBits = 64 - 2 * kIdxBits;  // 40: part-rank bits of both sides
+
+// Arc-pair write pass: 256 threads x 8 records per workgroup.
+constexpr int kExpandNT = 256;
+constexpr int kExpandIT = 8;
+constexpr u64 kExpandTile = kExpandNT * kExpandIT;
+
+struct LevelArgs {
+  CsrView c1, c2;
+  const u32 *sq1, *sq2;  // state id -> q1, q2
+  u32 lo, nsrc;          // sources are state ids lo .. lo + nsrc - 1
+  u64 *cnt;              // [nsrc] unmerged arcs per source
+  u32 *mc;               // [nsrc] matched segment pairs per source
+  const u64 *roff;       // [nsrc + 1] exclusive scan of cnt
+  const u64 *moff;       // [nsrc + 1] exclusive scan of mc
+  u32 *wide, *heavy;     // source lists for wavefront / workgroup joins
+  Status *st;
+  uint4 *match;          // [M] (M1 arc start, M2 arc start, n1, n2)
+  u64 *mrbase;           // [M] first record of each match
+};
+
+void launch_count(const LevelArgs &a, hipStream_t s);
+void launch_emit(const LevelArgs &a, hipStream_t s);
+// Writes R records: key = (part1 << b2) | part2 (u32 when key_bits <= 32,
+// else u64), weight = p1 * p2.
+void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,
+                   const CsrView &c2, int b2, bool wide_keys, void *rec_key, float *rec_w,
+                   u32 *err, hipStream_t s);
+
+struct MergeArgs {
+  const void *rec_key;
+  const float *rec_w;
+  u64 R;
+  const u64 *roff;
+  u32 nsrc, lo;
+  const u32 *sq1, *sq2;
+  const u32 *pbase1, *pbase2;
+  const uint2 *parts1, *parts2;
+  int key_bits, b2;
+  u64 *hkeys;
+  u64 hmask;
+  u32 *newlist;
+  u64 newcap;
+  uint4 *temp;     // [R] merged arcs (slot, a, c, weight bits) at roff[u] + k
+  u32 *mcount;     // [nsrc] merged arcs per source
+  Status *st;
+  // multi-block path
+  u32 *big;        // [nbig] level-local source indices
+};
+
+void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStream_t s);
+void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s);
+// Multi-block merge of the nbig sources listed in a.big; bigoff has nbig + 1
+// entries (exclusive scan of their record counts, total RB).
+void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s);
+void merge_big(const MergeArgs &a, bool wide_keys, u32 nbig, const u64 *bigoff, u64 RB,
+               Allocator &A, hipStream_t s);
+
+void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1, u32 *sq2,
+                         u32 *err, hipStream_t s);
+void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32 *nvals,
+                   u64 nmask, u32 *err, hipStream_t s);
+// ids base .. base + nnew - 1 in new-list order (or the order in `order`).
+void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 *sq1,
+                   u32 *sq2, hipStream_t s);
+void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
+                    u32 *vals, hipStream_t s);
+void launch_compact(const uint4 *temp, const u64 *roff, const u64 *aoff, u32 nsrc, u32 lo,
+                    u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
+                    float *ow, u32 *err, hipStream_t s);
+void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
+                   uint8_t *fin, hipStream_t s);
+void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);
+void launch_merged_total(const u64 *a_total, Status *st, hipStream_t s);
+void launch_reset_level(Status *st, hipStream_t s);
+
+}  // namespace fstc

