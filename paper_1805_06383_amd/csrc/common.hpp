@@ -13,6 +13,7 @@
 
 namespace fstc {
 
+using u16 = uint16_t;
 using u32 = uint32_t;
 using u64 = uint64_t;
 

@@ -252,7 +252,8 @@ void Composer::run(fstc_result *out) {
   Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
   Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
       bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
-      stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A);
+      stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A), tiles_e(&A), tiles_m(&A), tstart(&A),
+      mend(&A);
 
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
@@ -262,7 +263,7 @@ void Composer::run(fstc_result *out) {
     max_frontier = std::max<u64>(max_frontier, nsrc);
     const u64 np1 = (u64)nsrc + 1;
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
-    mcount.ensure(np1 * 4); aoff.ensure(np1 * 8);
+    mcount.ensure(np1 * 4); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
     stmp.ensure(scan_temp_bytes(np1));
 
@@ -291,6 +292,8 @@ void Composer::run(fstc_result *out) {
     rkey.ensure(R * rec_bytes);
     rw.ensure(R * 4);
     temp.ensure(R * sizeof(uint4));
+    tiles_e.ensure((ceil_div(R, kExpandTile) + 1) * 8);
+    tiles_m.ensure((ceil_div(R, kMergeWindow) + 1) * 4);
     const u64 newcap = std::min<u64>(R, pairspace - n_states);
     newlist.ensure(std::max<u64>(newcap, 1) * 4);
 
@@ -318,14 +321,15 @@ void Composer::run(fstc_result *out) {
     T.end(kExpand);
     T.begin();
     launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
-                  rkey.p, rw.as<float>(), &dst->err, s);
+                  rkey.p, rw.as<float>(), tiles_e.as<u64>(), &dst->err, s);
     T.end(kWriteKernel);
     ++write_launches;
     total_matches += M;
 
     // (a6) merge identical arcs, claim new pairs
     T.begin();
-    fill_u32(mcount.as<u32>(), 0, nsrc, s);
+    fill_u64(tstart.as<u64>(), 0, nsrc, s);
+    fill_u64(mend.as<u64>(), 0, nsrc, s);
     MergeArgs ma{};
     ma.rec_key = rkey.p;
     ma.rec_w = rw.as<float>();
@@ -346,7 +350,9 @@ void Composer::run(fstc_result *out) {
     ma.newlist = newlist.as<u32>();
     ma.newcap = newcap;
     ma.temp = temp.as<uint4>();
-    ma.mcount = mcount.as<u32>();
+    ma.tile_src = tiles_m.as<u32>();
+    ma.tstart = tstart.as<u64>();
+    ma.mend = mend.as<u64>();
     ma.st = dst;
     ma.big = big.as<u32>();
     T.end(kMerge);
@@ -365,6 +371,7 @@ void Composer::run(fstc_result *out) {
       big_records += RB;
       merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, A, s);
     }
+    launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
     exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
     launch_merged_total(aoff.as<u64>() + nsrc, dst, s);
     T.end(kMerge);
@@ -401,7 +408,7 @@ void Composer::run(fstc_result *out) {
       oil.grow_keep(na * 4, arcs * 4);
       ool.grow_keep(na * 4, arcs * 4);
       ow.grow_keep(na * 4, arcs * 4);
-      launch_compact(temp.as<uint4>(), roff.as<u64>(), aoff.as<u64>(), nsrc, lo, merged,
+      launch_compact(temp.as<uint4>(), R, tstart.as<u64>(), aoff.as<u64>(), nsrc, lo, merged,
                      hvb.as<u32>(), osrc.as<u32>() + arcs, odst.as<u32>() + arcs,
                      oil.as<u32>() + arcs, ool.as<u32>() + arcs, ow.as<float>() + arcs,
                      &dst->err, s);

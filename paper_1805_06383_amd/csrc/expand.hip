@@ -262,20 +262,17 @@ template <class KT>
 __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const u64 *mrbase, u64 M,
                                                       u64 R, const uint2 *arcs1,
                                                       const uint2 *arcs2, int b2, KT *rec_key,
-                                                      float *rec_w, u32 *err) {
+                                                      float *rec_w, const u64 *tile_lb, u32 *err) {
   __shared__ u32 s_rel[kExpandTile];
   __shared__ uint4 s_m[kExpandTile];
-  __shared__ u64 s_k[2];
   const u64 r0 = (u64)blockIdx.x * kExpandTile;
   const u64 rend = min(r0 + kExpandTile, R);
-  if (threadIdx.x == 0) {
-    s_k[0] = last_le<u64>(mrbase, M, r0);
-    s_k[1] = last_le<u64>(mrbase, M, rend - 1);
-  }
-  __syncthreads();
-  const u64 k0 = s_k[0];
-  const u64 nm = s_k[1] - k0 + 1;
-  if (nm > kExpandTile) {  // impossible: every match has >= 1 record
+  // matches overlapping [r0, rend): the last one starting at or before r0
+  // through the last one starting before rend
+  const u64 lb0 = tile_lb[blockIdx.x], lb1 = tile_lb[blockIdx.x + 1];
+  const u64 k0 = (lb0 < M && mrbase[lb0] == r0) ? lb0 : lb0 - 1;
+  const u64 nm = lb1 - k0;
+  if (lb1 == 0 || lb1 <= k0 || nm > kExpandTile) {  // impossible: each match has >= 1 record
     if (threadIdx.x == 0) set_error(err, kErrBounds);
     return;
   }
@@ -285,7 +282,7 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
     s_m[i] = match[k0 + i];
   }
   __syncthreads();
-#pragma unroll 2
+#pragma unroll
   for (int j = 0; j < kExpandIT; ++j) {
     const u64 r = r0 + (u64)j * kExpandNT + threadIdx.x;
     if (r >= rend) continue;
@@ -309,6 +306,12 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   }
 }
 
+// tile_lb[t] = first match whose first record is >= min(t * kExpandTile, R).
+__global__ void k_tile_matches(const u64 *mrbase, u64 M, u64 R, u64 ntiles, u64 *tile_lb) {
+  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t <= ntiles; t += (u64)gridDim.x * blockDim.x)
+    tile_lb[t] = lower_bound_dev<u64>(mrbase, M, min(t * kExpandTile, R));
+}
+
 }  // namespace
 
 void launch_count(const LevelArgs &a, hipStream_t s) {
@@ -327,16 +330,18 @@ void launch_emit(const LevelArgs &a, hipStream_t s) {
 
 void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,
                    const CsrView &c2, int b2, bool wide_keys, void *rec_key, float *rec_w,
-                   u32 *err, hipStream_t s) {
+                   u64 *tile_lb, u32 *err, hipStream_t s) {
   if (R == 0) return;
   const u64 g = ceil_div(R, kExpandTile);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
+  const unsigned gs = (unsigned)std::min<u64>(ceil_div(g + 1, 256), 1u << 20);
+  hipLaunchKernelGGL(k_tile_matches, dim3(gs), dim3(256), 0, s, mrbase, M, R, g, tile_lb);
   if (wide_keys)
     hipLaunchKernelGGL((k_expand<u64>), dim3((unsigned)g), dim3(kExpandNT), 0, s, match, mrbase,
-                       M, R, c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, err);
+                       M, R, c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, tile_lb, err);
   else
     hipLaunchKernelGGL((k_expand<u32>), dim3((unsigned)g), dim3(kExpandNT), 0, s, match, mrbase,
-                       M, R, c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, err);
+                       M, R, c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, tile_lb, err);
 }
 
 }  // namespace fstc

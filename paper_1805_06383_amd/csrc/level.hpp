@@ -70,9 +70,10 @@ void launch_count(const LevelArgs &a, hipStream_t s);
 void launch_emit(const LevelArgs &a, hipStream_t s);
 // Writes R records: key = (part1 << b2) | part2 (u32 when key_bits <= 32,
 // else u64), weight = p1 * p2.
+// tile_lb: scratch of ceil(R / kExpandTile) + 1 u64.
 void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,
                    const CsrView &c2, int b2, bool wide_keys, void *rec_key, float *rec_w,
-                   u32 *err, hipStream_t s);
+                   u64 *tile_lb, u32 *err, hipStream_t s);
 
 struct MergeArgs {
   const void *rec_key;
@@ -88,8 +89,10 @@ struct MergeArgs {
   u64 hmask;
   u32 *newlist;
   u64 newcap;
-  uint4 *temp;     // [R] merged arcs (slot, a, c, weight bits) at roff[u] + k
-  u32 *mcount;     // [nsrc] merged arcs per source
+  uint4 *temp;     // [R] merged arcs (slot, a, c, weight bits)
+  u64 *tstart;     // [nsrc] first temp slot of each source's merged arcs (0 if none)
+  u64 *mend;       // [nsrc] one past its last slot (0 if none)
+  u32 *tile_src;   // [ceil(R / kMergeWindow) + 1] scratch: first source of each tile
   Status *st;
   // multi-block path
   u32 *big;        // [nbig] level-local source indices
@@ -112,9 +115,11 @@ void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *
                    u32 *sq2, hipStream_t s);
 void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
                     u32 *vals, hipStream_t s);
-void launch_compact(const uint4 *temp, const u64 *roff, const u64 *aoff, u32 nsrc, u32 lo,
-                    u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
+// Level merged arc k of source u is temp[tstart[u] + k - aoff[u]].
+void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff, u32 nsrc,
+                    u32 lo, u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
                     float *ow, u32 *err, hipStream_t s);
+void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
 void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);

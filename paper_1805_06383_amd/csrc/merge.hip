@@ -31,6 +31,11 @@ constexpr int NT = kMergeNT;
 constexpr int IT = kMergeIT;
 constexpr int C = kMergeCap;
 constexpr int NW = NT / kWave;
+constexpr int kEmitBatch = 2;  // items whose emission lookups are overlapped
+
+inline unsigned grid1(u64 n, int nt = 256) {
+  return (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(n, nt), 1u << 20));
+}
 
 // Linear-probing insert of `key` (never kEmptyKey).  Returns its slot and
 // sets is_new when this call claimed the slot.  The probe loop is bounded by
@@ -62,6 +67,31 @@ __device__ __forceinline__ u32 hash_insert(u64 *keys, u64 mask, u64 key, bool &i
   return 0;
 }
 
+// Position in the wave-striped layout (element e = w*512 + j*64 + lane) that
+// lane `lane` of wave w reads as item j, for the sorted element
+// p = w*512 + lane*8 + j: each thread then holds 8 consecutive elements.
+__device__ __forceinline__ u32 blocked_slot(u32 p) {
+  return (p & ~(u32)(kWave * IT - 1)) | ((p % IT) * kWave) | ((p / IT) % kWave);
+}
+
+// Exclusive prefix over the waves of the block of one value per wave (taken
+// from any lane); *total receives the block total.  All threads must call it.
+__device__ __forceinline__ u32 block_offset(u32 wave_value, u32 *s_tmp, u32 *total) {
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  __syncthreads();
+  if (lane == 0) s_tmp[w] = wave_value;
+  __syncthreads();
+  u32 base = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    const u32 t = s_tmp[i];
+    if ((u32)i < w) base += t;
+    tot += t;
+  }
+  *total = tot;
+  return base;
+}
+
 // Inclusive sum of v over the block in element order for wave-striped items;
 // *total receives the block total.  All threads must call it.
 __device__ __forceinline__ void striped_inclusive_sum(u32 (&v)[IT], u32 *s_tmp, u32 *total) {
@@ -88,24 +118,98 @@ __device__ __forceinline__ void striped_inclusive_sum(u32 (&v)[IT], u32 *s_tmp, 
   *total = tot;
 }
 
-// The merged arc of one run: maps the part ranks back to (r1, a) and (r2, c),
-// inserts the target pair, writes (slot, a, c, weight) to temp.
-__device__ __forceinline__ u32 emit_merged(const MergeArgs &a, u32 u, u64 key, u64 local,
-                                           double sum, bool &is_new) {
-  const u32 sid = a.lo + u;
-  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
-  const u32 part1 = (u32)(key >> a.b2);
-  const u32 part2 = (u32)(key & ((1ull << a.b2) - 1));
-  const uint2 P1 = a.parts1[a.pbase1[q1] + part1];  // (r1, a)
-  const uint2 P2 = a.parts2[a.pbase2[q2] + part2];  // (r2, c)
-  const u64 hk = ((u64)P1.x << 32) | (u64)P2.x;
-  const u32 slot = hash_insert(a.hkeys, a.hmask, hk, is_new, &a.st->err);
-  a.temp[a.roff[u] + local] = make_uint4(slot, P1.y, P2.y, __float_as_uint((float)sum));
-  return slot;
+// Linear-probing insert of B keys at once (lanes with act[i] unset skip
+// item i).  Each round issues the probe loads of all pending items before
+// testing any, so their latencies overlap.  Slots only ever change from
+// kEmptyKey to a key, so a stale read of kEmptyKey is settled by the CAS and
+// a plain (workgroup-scope) read is enough.  Bounded by the table size.
+template <int B>
+__device__ __forceinline__ void hash_insert_batch(u64 *keys, u64 mask, const u64 (&key)[B],
+                                                  const bool (&act)[B], u32 (&slot)[B],
+                                                  bool (&is_new)[B], u32 *err) {
+  u64 h[B];
+  bool pend[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    pend[i] = act[i];
+    is_new[i] = false;
+    slot[i] = 0;
+    h[i] = mix64(key[i]) & mask;
+  }
+  for (u64 probe = 0; probe <= mask; ++probe) {
+    u64 cur[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i)
+      cur[i] = pend[i] ? __hip_atomic_load(&keys[h[i]], __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP)
+                       : 0;
+    bool any = false;
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      if (!pend[i]) continue;
+      if (cur[i] == kEmptyKey) {
+        cur[i] = atomicCAS((unsigned long long *)&keys[h[i]], (unsigned long long)kEmptyKey,
+                           (unsigned long long)key[i]);
+        if (cur[i] == kEmptyKey) {
+          is_new[i] = true;
+          slot[i] = (u32)h[i];
+          pend[i] = false;
+          continue;
+        }
+      }
+      if (cur[i] == key[i]) {
+        slot[i] = (u32)h[i];
+        pend[i] = false;
+        continue;
+      }
+      h[i] = (h[i] + 1) & mask;
+      any = true;
+    }
+    if (!any) return;
+  }
+  set_error(err, kErrHashFull);
+}
+
+// Merged arcs of B runs: part ranks back to (r1, a) and (r2, c), the target
+// pair inserted in the visited table, (slot, a, c, weight) written to
+// temp[tpos], and new pairs appended to the new-state list.  Every lane of the
+// wave must call it.
+template <int B>
+__device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)[B],
+                                           const u32 (&u)[B], const u64 (&key)[B],
+                                           const u64 (&tpos)[B], const float (&w)[B]) {
+  u32 q1[B], q2[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    q1[i] = act[i] ? a.sq1[a.lo + u[i]] : 0;
+    q2[i] = act[i] ? a.sq2[a.lo + u[i]] : 0;
+  }
+  u32 pb1[B], pb2[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    pb1[i] = act[i] ? a.pbase1[q1[i]] : 0;
+    pb2[i] = act[i] ? a.pbase2[q2[i]] : 0;
+  }
+  uint2 P1[B], P2[B];
+  u64 hk[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    P1[i] = act[i] ? a.parts1[pb1[i] + (u32)(key[i] >> a.b2)] : make_uint2(0, 0);
+    P2[i] = act[i] ? a.parts2[pb2[i] + (u32)(key[i] & ((1ull << a.b2) - 1))] : make_uint2(0, 0);
+    hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
+  }
+  u32 slot[B];
+  bool is_new[B];
+  hash_insert_batch<B>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    if (act[i]) a.temp[tpos[i]] = make_uint4(slot[i], P1[i].y, P2[i].y, __float_as_uint(w[i]));
+    wave_append(is_new[i], slot[i], a.newlist, &a.st->nnew, a.newcap, &a.st->err, kErrNewList);
+  }
 }
 
 template <class KT>
-__global__ __launch_bounds__(NT) void k_merge_tiles(MergeArgs a) {
+__global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   __shared__ u64 s_keys[C];
   __shared__ float s_w[C];
   __shared__ u32 s_segsrc[C];
@@ -113,16 +217,15 @@ __global__ __launch_bounds__(NT) void k_merge_tiles(MergeArgs a) {
   __shared__ u32 s_base[256];
   __shared__ u32 s_tmp[NW];
   __shared__ u64 s_info[2];
+  __shared__ double s_wsum[NW];
+  __shared__ u32 s_wflag[NW];
 
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u64 tstart = (u64)blockIdx.x * kMergeWindow;
   if (tstart >= a.R) return;
-  const u64 tend = min(tstart + kMergeWindow, a.R);
   if (threadIdx.x == 0) {
-    u64 s0 = lower_bound_dev<u64>(a.roff, (u64)a.nsrc + 1, tstart);
-    u64 s1 = lower_bound_dev<u64>(a.roff, (u64)a.nsrc + 1, tend);
-    s0 = min(s0, (u64)a.nsrc);
-    s1 = min(s1, (u64)a.nsrc);
+    const u64 s0 = a.tile_src[blockIdx.x];
+    u64 s1 = a.tile_src[blockIdx.x + 1];
     // a source of more than kMergeWindow records can only be the last one
     // starting in the window; it is merged by the multi-block path
     if (s1 > s0 && a.roff[s1] - a.roff[s1 - 1] > kMergeWindow) --s1;
@@ -151,11 +254,14 @@ __global__ __launch_bounds__(NT) void k_merge_tiles(MergeArgs a) {
   }
   __syncthreads();
 
-  // 2. load records; sort key = segment : record key : element index
+  // 2. load records; sort key = segment : record key : element index.  The
+  //    segment of an element is the number of source starts at or before it
+  //    (a 0/1 prefix count: one ballot per item row).
   u64 skey[IT];
   bool valid[IT];
   u32 f[IT], mark[IT];
   const KT *rk = static_cast<const KT *>(a.rec_key);
+  u32 wrun = 0;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
     const u32 e = w * (kWave * IT) + j * kWave + lane;
@@ -168,10 +274,16 @@ __global__ __launch_bounds__(NT) void k_merge_tiles(MergeArgs a) {
       s_w[e] = a.rec_w[r];
       mark[j] = s_mark[e];
     }
-    f[j] = mark[j] ? 1u : 0u;
+    const u64 m = __ballot(mark[j] != 0);
+    f[j] = wrun + count_below(m) + (mark[j] ? 1u : 0u);
+    wrun += (u32)__popcll(m);
   }
   u32 nseg;
-  striped_inclusive_sum(f, s_tmp, &nseg);
+  {
+    const u32 wbase = block_offset(wrun, s_tmp, &nseg);
+#pragma unroll
+    for (int j = 0; j < IT; ++j) f[j] += wbase;
+  }
   const int segshift = a.key_bits + kIdxBits;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
@@ -186,92 +298,177 @@ __global__ __launch_bounds__(NT) void k_merge_tiles(MergeArgs a) {
   }
   __syncthreads();  // s_mark (aliasing s_keys) fully read
 
-  // 3. stable LSD radix sort on bits [kIdxBits, segshift + segbits)
+  // 3. stable LSD radix sort on bits [kIdxBits, segshift + segbits).  The
+  //    last pass stores sorted element p at blocked_slot(p), so that after the
+  //    read-back thread (w, lane) holds the consecutive sorted elements
+  //    w*512 + lane*8 + j, j = 0..7.
   const int hi_bit = segshift + bits_for_dev(nseg - 1);
-  for (int shift = kIdxBits; shift < hi_bit; shift += 8) {
+  const int npass = hi_bit > kIdxBits ? (hi_bit - kIdxBits + 7) / 8 : 0;
+  for (int pass = 0; pass < npass; ++pass) {
+    const int shift = kIdxBits + 8 * pass;
     const int bits = min(8, hi_bit - shift);
     const u32 dmask = (1u << bits) - 1u;
     u32 dig[IT], rid[IT];
 #pragma unroll
     for (int j = 0; j < IT; ++j) dig[j] = (u32)(skey[j] >> shift) & dmask;
     block_rank_digits<NT, IT>(dig, valid, bits, rid, s_cnt, s_base, s_tmp);
+    const bool last_pass = pass == npass - 1;
 #pragma unroll
-    for (int j = 0; j < IT; ++j)
-      if (valid[j]) s_keys[s_base[dig[j]] + rid[j]] = skey[j];
+    for (int j = 0; j < IT; ++j) {
+      if (!valid[j]) continue;
+      const u32 pos = s_base[dig[j]] + rid[j];
+      s_keys[last_pass ? blocked_slot(pos) : pos] = skey[j];
+    }
     __syncthreads();
+    // read back: striped positions e < n, or after the last pass the
+    // consecutive elements p = w*512 + lane*8 + j < n stored at slot e
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
       const u32 e = w * (kWave * IT) + j * kWave + lane;
-      if (valid[j]) skey[j] = s_keys[e];
+      const u32 p = w * (kWave * IT) + lane * IT + j;
+      if (last_pass ? p < n : e < n) skey[j] = s_keys[e];
     }
     __syncthreads();
   }
-  if (hi_bit <= kIdxBits) {
+  if (npass == 0) {
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
       const u32 e = w * (kWave * IT) + j * kWave + lane;
-      if (valid[j]) s_keys[e] = skey[j];
+      if (valid[j]) s_keys[blocked_slot(e)] = skey[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 e = w * (kWave * IT) + j * kWave + lane;
+      const u32 p = w * (kWave * IT) + lane * IT + j;
+      if (p < n) skey[j] = s_keys[e];
     }
     __syncthreads();
   }
 
-  // 4. runs of equal (segment, key): the first element of a run sums it
+  // 4. runs of equal (segment, key) over the thread's consecutive elements
+  //    p0 + j; run sums: serial within the thread, one segmented scan of the
+  //    per-thread open run across threads (float64, fixed combining order)
   const u64 KM = ~((1ull << kIdxBits) - 1);
   const u32 IM = (1u << kIdxBits) - 1;
-  double sum[IT];
-  u32 qend[IT], hf[IT];
+  const u32 p0 = w * (kWave * IT) + lane * IT;
+  u64 prevk = ~0ull, nextk = ~0ull;
+  if (p0 > 0 && p0 - 1 < n) prevk = s_keys[blocked_slot(p0 - 1)] & KM;
+  if (p0 + IT < n) nextk = s_keys[blocked_slot(p0 + IT)] & KM;
+  bool head[IT], tail[IT], nohead[IT];
+  double part[IT];
+  double acc = 0.0;
+  bool seen = false;
+  u32 hc = 0;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const u32 e = w * (kWave * IT) + j * kWave + lane;
-    hf[j] = 0;
-    sum[j] = 0.0;
-    qend[j] = 0;
-    if (!valid[j]) continue;
+    const bool v = p0 + j < n;
+    valid[j] = v;
     const u64 mk = skey[j] & KM;
-    if (e == 0 || (s_keys[e - 1] & KM) != mk) {
-      hf[j] = 1;
-      double acc = 0.0;
-      u32 q = e;
-      while (q < n && (s_keys[q] & KM) == mk) {
-        acc += (double)s_w[(u32)s_keys[q] & IM];
-        ++q;
-      }
-      sum[j] = acc;
-      qend[j] = q;
+    const u64 before = j == 0 ? prevk : (skey[j - 1] & KM);
+    const u64 after = j == IT - 1 ? nextk : (p0 + j + 1 < n ? (skey[j + 1] & KM) : ~0ull);
+    head[j] = v && (p0 + j == 0 || before != mk);
+    tail[j] = v && (p0 + j == n - 1 || after != mk);
+    if (head[j]) {
+      acc = 0.0;
+      seen = true;
+      ++hc;
+    }
+    if (v) acc += (double)s_w[(u32)skey[j] & IM];
+    part[j] = acc;
+    nohead[j] = !seen;
+  }
+  // segmented scan of (seen, acc) over lanes, then over waves
+  double x = acc;
+  u32 fl = seen ? 1u : 0u;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const double y = __shfl_up(x, d, kWave);
+    const u32 g = __shfl_up(fl, d, kWave);
+    if (lane >= (u32)d) {
+      if (!fl) x += y;
+      fl |= g;
     }
   }
-  __syncthreads();  // s_w fully read
-  u32 rinc[IT];
-#pragma unroll
-  for (int j = 0; j < IT; ++j) rinc[j] = hf[j];
+  double carry = __shfl_up(x, 1, kWave);
+  u32 cflag = __shfl_up(fl, 1, kWave);
+  if (lane == 0) {
+    carry = 0.0;
+    cflag = 0;
+  }
+  if (lane == kWave - 1) {
+    s_wsum[w] = x;
+    s_wflag[w] = fl;
+  }
+  // run index base: heads in earlier threads
+  const u32 hinc = wave_inclusive_sum(hc);
   u32 nruns;
-  striped_inclusive_sum(rinc, s_tmp, &nruns);
-  u32 *s_segfirst = reinterpret_cast<u32 *>(s_w);
+  const u32 hwave = block_offset(__shfl(hinc, kWave - 1, kWave), s_tmp, &nruns);  // has barriers
+  u32 hbase = hwave + hinc - hc;
+  if (!cflag) {
+    double pre = 0.0;
+    for (u32 v = 0; v < w; ++v) pre = s_wflag[v] ? s_wsum[v] : pre + s_wsum[v];
+    carry += pre;
+  }
+  double sum[IT];
+  u32 runidx[IT];
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const u32 e = w * (kWave * IT) + j * kWave + lane;
-    if (!valid[j]) continue;
-    const u32 seg = (u32)(skey[j] >> segshift);
-    if (e == 0 || (u32)(s_keys[e - 1] >> segshift) != seg) s_segfirst[seg] = rinc[j] - 1;
+    sum[j] = part[j] + (nohead[j] ? carry : 0.0);
+    if (head[j]) ++hbase;
+    runidx[j] = hbase - 1;
+  }
+  // 5. every run's last element publishes (sorted position, weight) under
+  //    its run number; the block then emits the runs in parallel, run r of
+  //    the tile to temp[rb + r].  The first and last run of a source record
+  //    where its merged arcs start and end.
+  __syncthreads();  // every s_w read done: run sums reuse s_w
+  float *s_runsum = s_w;
+  u16 *s_runpos = reinterpret_cast<u16 *>(s_cnt);  // sort counters are free now
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    if (!tail[j]) continue;
+    s_runsum[runidx[j]] = (float)sum[j];
+    s_runpos[runidx[j]] = (u16)(p0 + j);
   }
   __syncthreads();
-
-  // 5. one merged arc per run
   const u64 keymask = (1ull << a.key_bits) - 1;
+  for (u32 r0 = 0; r0 < nruns; r0 += NT * kEmitBatch) {
+    bool act[kEmitBatch];
+    u32 u_[kEmitBatch];
+    u64 key_[kEmitBatch], tpos[kEmitBatch];
+    float wt[kEmitBatch];
 #pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    bool is_new = false;
-    u32 slot = 0;
-    if (valid[j] && hf[j]) {
-      const u32 seg = (u32)(skey[j] >> segshift);
-      const u64 key = (skey[j] >> kIdxBits) & keymask;
-      const u32 u = s_segsrc[seg];
-      const u32 local = (rinc[j] - 1) - s_segfirst[seg];
-      const bool last = qend[j] == n || (u32)(s_keys[qend[j]] >> segshift) != seg;
-      if (last) a.mcount[u] = local + 1;
-      slot = emit_merged(a, u, key, local, sum[j], is_new);
+    for (int i = 0; i < kEmitBatch; ++i) {
+      const u32 r = r0 + i * NT + threadIdx.x;
+      act[i] = r < nruns;
+      u_[i] = 0;
+      key_[i] = 0;
+      tpos[i] = 0;
+      wt[i] = 0.f;
+      if (!act[i]) continue;
+      const u64 sk = s_keys[blocked_slot(s_runpos[r])];
+      const u64 seg = sk >> segshift;
+      key_[i] = (sk >> kIdxBits) & keymask;
+      u_[i] = s_segsrc[seg];
+      tpos[i] = rb + r;
+      wt[i] = s_runsum[r];
+      const bool first = r == 0 || (s_keys[blocked_slot(s_runpos[r - 1])] >> segshift) != seg;
+      const bool last =
+          r == nruns - 1 || (s_keys[blocked_slot(s_runpos[r + 1])] >> segshift) != seg;
+      if (first) a.tstart[u_[i]] = rb + r;
+      if (last) a.mend[u_[i]] = rb + r + 1;
     }
-    wave_append(is_new, slot, a.newlist, &a.st->nnew, a.newcap, &a.st->err, kErrNewList);
+    emit_batch<kEmitBatch>(a, act, u_, key_, tpos, wt);
+  }
+}
+
+// Per merge tile t, the first source whose records start at or after
+// min(t * kMergeWindow, R), for t in [0, ntiles].
+__global__ void k_tile_sources(const u64 *roff, u32 nsrc, u64 R, u64 ntiles, u32 *tile_src) {
+  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t <= ntiles; t += (u64)gridDim.x * blockDim.x) {
+    const u64 x = min(t * kMergeWindow, R);
+    tile_src[t] = (u32)min(lower_bound_dev<u64>(roff, (u64)nsrc + 1, x), (u64)nsrc);
   }
 }
 
@@ -308,8 +505,10 @@ __global__ void k_run_heads(const u64 *keys, u64 n, u32 *flags) {
 __global__ void k_big_reduce(MergeArgs a, const u64 *bigoff, u64 RB, const u64 *skey,
                              const u32 *sval, const u32 *flags, const u32 *ridx) {
   const u64 g = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  bool is_new = false;
-  u32 slot = 0;
+  bool act[1] = {false};
+  u32 u[1] = {0};
+  u64 key[1] = {0}, tpos[1] = {0};
+  float wt[1] = {0.f};
   if (g < RB && flags[g]) {
     const u64 mk = skey[g];
     const u32 i = (u32)(mk >> a.key_bits);
@@ -319,12 +518,23 @@ __global__ void k_big_reduce(MergeArgs a, const u64 *bigoff, u64 RB, const u64 *
       acc += (double)__uint_as_float(sval[q]);
       ++q;
     }
-    const u32 u = a.big[i];
+    u[0] = a.big[i];
     const u64 local = ridx[g] - ridx[bigoff[i]];
-    if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mcount[u] = (u32)(local + 1);
-    slot = emit_merged(a, u, mk & ((1ull << a.key_bits) - 1), local, acc, is_new);
+    const u64 base = a.roff[u[0]];
+    if (g == bigoff[i]) a.tstart[u[0]] = base;
+    if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mend[u[0]] = base + local + 1;
+    key[0] = mk & ((1ull << a.key_bits) - 1);
+    tpos[0] = base + local;
+    wt[0] = (float)acc;
+    act[0] = true;
   }
-  wave_append(is_new, slot, a.newlist, &a.st->nnew, a.newcap, &a.st->err, kErrNewList);
+  emit_batch<1>(a, act, u, key, tpos, wt);
+}
+
+// Merged arcs per source from where its runs start and end in temp.
+__global__ void k_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount) {
+  const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u < nsrc) mcount[u] = (u32)(mend[u] - tstart[u]);
 }
 
 // ---------------------------------------------------------------------------
@@ -370,13 +580,13 @@ __global__ void k_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq
   vals[i] = slot;
 }
 
-__global__ void k_compact(const uint4 *temp, const u64 *roff, const u64 *aoff, u32 nsrc, u32 lo,
-                          u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
-                          float *ow, u32 *err) {
+__global__ void k_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff, u32 nsrc,
+                          u32 lo, u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil,
+                          u32 *ool, float *ow, u32 *err) {
   for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < M; k += (u64)gridDim.x * blockDim.x) {
     const u32 u = (u32)last_le<u64>(aoff, nsrc, k);
-    const u64 t = roff[u] + (k - aoff[u]);
-    if (t >= roff[u + 1]) {
+    const u64 t = tstart[u] + (k - aoff[u]);
+    if (t >= R) {
       set_error(err, kErrBounds);
       continue;
     }
@@ -407,10 +617,6 @@ __global__ void k_reset_level(Status *st) {
   st->nwide = st->nheavy = st->nbig = st->nnew = 0;
 }
 
-inline unsigned grid1(u64 n, int nt = 256) {
-  return (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(n, nt), 1u << 20));
-}
-
 }  // namespace
 
 void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStream_t s) {
@@ -422,6 +628,8 @@ void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s) {
   if (a.R == 0) return;
   const u64 g = ceil_div(a.R, kMergeWindow);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
+  hipLaunchKernelGGL(k_tile_sources, dim3(grid1(g + 1)), dim3(256), 0, s, a.roff, a.nsrc, a.R, g,
+                     a.tile_src);
   if (wide_keys)
     hipLaunchKernelGGL((k_merge_tiles<u64>), dim3((unsigned)g), dim3(NT), 0, s, a);
   else
@@ -484,12 +692,17 @@ void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64
                      nnew, hkeys, bq2, keys, vals);
 }
 
-void launch_compact(const uint4 *temp, const u64 *roff, const u64 *aoff, u32 nsrc, u32 lo, u64 M,
-                    const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow,
+void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff, u32 nsrc, u32 lo,
+                    u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow,
                     u32 *err, hipStream_t s) {
   if (!M) return;
-  hipLaunchKernelGGL(k_compact, dim3(grid1(M)), dim3(256), 0, s, temp, roff, aoff, nsrc, lo, M,
-                     hvals, osrc, odst, oil, ool, ow, err);
+  hipLaunchKernelGGL(k_compact, dim3(grid1(M)), dim3(256), 0, s, temp, R, tstart, aoff, nsrc, lo,
+                     M, hvals, osrc, odst, oil, ool, ow, err);
+}
+
+void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s) {
+  hipLaunchKernelGGL(k_mcount, dim3((unsigned)ceil_div(nsrc, 256)), dim3(256), 0, s, tstart, mend,
+                     nsrc, mcount);
 }
 
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
