@@ -293,7 +293,10 @@ void Composer::run(fstc_result *out) {
     rw.ensure(R * 4);
     temp.ensure(R * sizeof(uint4));
     tiles_e.ensure((ceil_div(R, kExpandTile) + 1) * 8);
-    tiles_m.ensure((ceil_div(R, kMergeWindow) + 1) * 4);
+    // merge window: as wide as the largest small source allows (see level.hpp)
+    const u64 max_small = std::max<u32>(1, hs->st.max_small);
+    const u64 window = nbig ? kMergeSmall : (u64)kMergeCap - max_small + 1;
+    tiles_m.ensure((ceil_div(R, window) + 1) * 4);
     const u64 newcap = std::min<u64>(R, pairspace - n_states);
     newlist.ensure(std::max<u64>(newcap, 1) * 4);
 
@@ -351,6 +354,7 @@ void Composer::run(fstc_result *out) {
     ma.newcap = newcap;
     ma.temp = temp.as<uint4>();
     ma.tile_src = tiles_m.as<u32>();
+    ma.window = window;
     ma.tstart = tstart.as<u64>();
     ma.mend = mend.as<u64>();
     ma.st = dst;

@@ -28,7 +28,8 @@ struct Status {
   u64 RB;       // records of sources merged by the multi-block path
   u32 nwide, nheavy, nbig, nnew;
   u32 err;      // kErr* bits, sticky for the whole call
-  u32 pad[3];
+  u32 max_small;  // largest record count of a source merged by the tiles
+  u32 pad[2];
 };
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
@@ -36,14 +37,16 @@ struct Status {
 constexpr u32 kWideMin = 24;
 constexpr u32 kHeavyMin = 2048;
 
-// Merge tiles: 512 threads x 8 items = 4096 records of LDS capacity; a tile
-// takes the sources whose first record falls in a 2048-record window, so
-// every source of at most 2048 records fits.  Larger sources take the
-// multi-block path.
+// Merge tiles: 512 threads x 8 items = 4096 records of LDS capacity.  Sources
+// of more than kMergeSmall records take the multi-block path.  A tile takes
+// the sources whose first record falls in a window of W records; with m the
+// largest small-source count, every such source ends within the tile's
+// capacity when W <= kMergeCap - m + 1 (and, when multi-block sources exist,
+// W <= kMergeSmall keeps them last in their window).
 constexpr int kMergeNT = 512;
 constexpr int kMergeIT = 8;
 constexpr int kMergeCap = kMergeNT * kMergeIT;
-constexpr u64 kMergeWindow = kMergeCap / 2;
+constexpr u64 kMergeSmall = kMergeCap / 2;
 constexpr int kIdxBits = 12;  // log2(kMergeCap)
 constexpr int kMaxKeyBits = 64 - 2 * kIdxBits;  // 40: part-rank bits of both sides
 
@@ -92,7 +95,8 @@ struct MergeArgs {
   uint4 *temp;     // [R] merged arcs (slot, a, c, weight bits)
   u64 *tstart;     // [nsrc] first temp slot of each source's merged arcs (0 if none)
   u64 *mend;       // [nsrc] one past its last slot (0 if none)
-  u32 *tile_src;   // [ceil(R / kMergeWindow) + 1] scratch: first source of each tile
+  u64 window;      // W: tile t takes the sources starting in [t W, (t + 1) W)
+  u32 *tile_src;   // [ceil(R / W) + 1] scratch: first source of each tile
   Status *st;
   // multi-block path
   u32 *big;        // [nbig] level-local source indices

@@ -10,8 +10,8 @@
 //   * a record's key is (rank of its M1 (target, input) pair) : (rank of its
 //     M2 (target, output) pair), which fixes (r1r2, a, c) for its source;
 //     ranks are per state (csr.hip), so keys are short;
-//   * a workgroup takes whole sources whose records start in a 2048-record
-//     window (at most 4096 records), sorts them in LDS by (source, key) with
+//   * a workgroup takes the whole sources whose records start in a window
+//     (at most 4096 records in all), sorts them in LDS by (source, key) with
 //     a stable radix sort ranked by wave ballots, and sums every run of
 //     equal keys in float64; sources of more than 2048 records are merged by
 //     a device-wide radix sort and a segmented reduce;
@@ -65,6 +65,13 @@ __device__ __forceinline__ u32 hash_insert(u64 *keys, u64 mask, u64 key, bool &i
   set_error(err, kErrHashFull);
   is_new = false;
   return 0;
+}
+
+// Tile of workgroup b among g: workgroup b runs on XCD b % 8; XCD x gets
+// tiles [x * q + min(x, r), ...) in order (q = g / 8, r = g % 8).
+__device__ __forceinline__ u32 xcd_tile(u32 b, u32 g) {
+  const u32 x = b % 8, i = b / 8, q = g / 8, r = g % 8;
+  return x * q + min(x, r) + i;
 }
 
 // Position in the wave-striped layout (element e = w*512 + j*64 + lane) that
@@ -216,33 +223,42 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   __shared__ u32 s_cnt[NW * 256];
   __shared__ u32 s_base[256];
   __shared__ u32 s_tmp[NW];
-  __shared__ u64 s_info[2];
   __shared__ double s_wsum[NW];
   __shared__ u32 s_wflag[NW];
 
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
-  const u64 tstart = (u64)blockIdx.x * kMergeWindow;
-  if (tstart >= a.R) return;
-  if (threadIdx.x == 0) {
-    const u64 s0 = a.tile_src[blockIdx.x];
-    u64 s1 = a.tile_src[blockIdx.x + 1];
-    // a source of more than kMergeWindow records can only be the last one
-    // starting in the window; it is merged by the multi-block path
-    if (s1 > s0 && a.roff[s1] - a.roff[s1 - 1] > kMergeWindow) --s1;
-    s_info[0] = s0;
-    s_info[1] = s1;
+  // XCD-aware tile order: workgroups are dealt round-robin to the 8 XCDs, so
+  // give each XCD a contiguous run of tiles; neighbouring tiles share half of
+  // their record window, which then stays in that XCD's L2.
+  const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
+  const u64 tstart = (u64)tile * a.window;
+  // A tile's records lie in [tstart, tstart + kMergeCap): its sources start
+  // before tstart + W and each has at most kMergeCap - W + 1 records.  Load
+  // that range now, before the bounds are known, so the loads overlap the
+  // bound lookups.
+  const KT *rk = static_cast<const KT *>(a.rec_key);
+  KT wkey[IT];
+  float wwt[IT];
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u64 r = tstart + w * (kWave * IT) + j * kWave + lane;
+    wkey[j] = r < a.R ? rk[r] : KT(0);
+    wwt[j] = r < a.R ? a.rec_w[r] : 0.f;
   }
-  __syncthreads();
-  const u32 s0 = (u32)s_info[0], s1 = (u32)s_info[1];
+  const u32 s0 = a.tile_src[tile];
+  u32 s1 = a.tile_src[tile + 1];
+  // a multi-block source can only be the last one starting in the window
+  if (s1 > s0 && a.roff[s1] - a.roff[s1 - 1] > kMergeSmall) --s1;
   if (s0 >= s1) return;
   const u64 rb = a.roff[s0];
   const u64 span = a.roff[s1] - rb;
-  if (span > (u64)C) {
+  if (span > (u64)C || rb < tstart || rb + span > tstart + C) {
     if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
     return;
   }
   const u32 n = (u32)span;
   if (n == 0) return;
+  const u32 off = (u32)(rb - tstart);  // window position of tile element 0
 
   // 1. mark the first record of every non-empty source with its index + 1
   u32 *s_mark = reinterpret_cast<u32 *>(s_keys);
@@ -253,25 +269,30 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
     if (c) s_mark[a.roff[u] - rb] = u + 1;
   }
   __syncthreads();
+  if (s_mark[0] == 0) {  // impossible: element 0 starts a source
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
 
-  // 2. load records; sort key = segment : record key : element index.  The
-  //    segment of an element is the number of source starts at or before it
-  //    (a 0/1 prefix count: one ballot per item row).
+  // 2. sort key = segment : record key : element index.  Items are window
+  //    positions; window order is element order, which keeps the ranking
+  //    stable.  The segment of an element is the number of source starts at
+  //    or before it (a 0/1 prefix count: one ballot per item row).
   u64 skey[IT];
-  bool valid[IT];
   u32 f[IT], mark[IT];
-  const KT *rk = static_cast<const KT *>(a.rec_key);
+  u32 valid = 0;  // bit j: item j holds a tile element
   u32 wrun = 0;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const u32 e = w * (kWave * IT) + j * kWave + lane;
-    valid[j] = e < n;
+    const u32 wpos = w * (kWave * IT) + j * kWave + lane;
+    const u32 e = wpos - off;  // wraps (and fails e < n) before the tile
+    const bool v = wpos >= off && e < n;
+    valid |= (v ? 1u : 0u) << j;
     mark[j] = 0;
     skey[j] = 0;
-    if (valid[j]) {
-      const u64 r = rb + e;
-      skey[j] = ((u64)rk[r] << kIdxBits) | e;
-      s_w[e] = a.rec_w[r];
+    if (v) {
+      skey[j] = ((u64)wkey[j] << kIdxBits) | e;
+      s_w[e] = wwt[j];
       mark[j] = s_mark[e];
     }
     const u64 m = __ballot(mark[j] != 0);
@@ -287,14 +308,8 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   const int segshift = a.key_bits + kIdxBits;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    if (!valid[j]) continue;
-    if (f[j] == 0) {  // impossible: element 0 starts a source
-      set_error(&a.st->err, kErrBounds);
-      valid[j] = false;
-      continue;
-    }
     if (mark[j]) s_segsrc[f[j] - 1] = mark[j] - 1;
-    skey[j] |= (u64)(f[j] - 1) << segshift;
+    skey[j] |= (u64)(f[j] - 1) << segshift;  // f >= 1 for every valid item
   }
   __syncthreads();  // s_mark (aliasing s_keys) fully read
 
@@ -315,27 +330,30 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
     const bool last_pass = pass == npass - 1;
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
-      if (!valid[j]) continue;
+      if (!((valid >> j) & 1u)) continue;
       const u32 pos = s_base[dig[j]] + rid[j];
       s_keys[last_pass ? blocked_slot(pos) : pos] = skey[j];
     }
     __syncthreads();
     // read back: striped positions e < n, or after the last pass the
     // consecutive elements p = w*512 + lane*8 + j < n stored at slot e
+    valid = 0;
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
       const u32 e = w * (kWave * IT) + j * kWave + lane;
       const u32 p = w * (kWave * IT) + lane * IT + j;
-      if (last_pass ? p < n : e < n) skey[j] = s_keys[e];
+      const bool v = last_pass ? p < n : e < n;
+      if (v) skey[j] = s_keys[e];
+      valid |= (v ? 1u : 0u) << j;
     }
     __syncthreads();
   }
   if (npass == 0) {
+    // sorted order is element order: element e (index bits of the key) goes
+    // to blocked_slot(e)
 #pragma unroll
-    for (int j = 0; j < IT; ++j) {
-      const u32 e = w * (kWave * IT) + j * kWave + lane;
-      if (valid[j]) s_keys[blocked_slot(e)] = skey[j];
-    }
+    for (int j = 0; j < IT; ++j)
+      if ((valid >> j) & 1u) s_keys[blocked_slot((u32)skey[j] & ((1u << kIdxBits) - 1))] = skey[j];
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
@@ -347,40 +365,38 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   }
 
   // 4. runs of equal (segment, key) over the thread's consecutive elements
-  //    p0 + j; run sums: serial within the thread, one segmented scan of the
-  //    per-thread open run across threads (float64, fixed combining order)
+  //    p0 + j < n; run sums: serial within the thread, one segmented scan of
+  //    the per-thread open run across threads (float64, fixed combining order)
   const u64 KM = ~((1ull << kIdxBits) - 1);
   const u32 IM = (1u << kIdxBits) - 1;
   const u32 p0 = w * (kWave * IT) + lane * IT;
+  const u32 nv = p0 < n ? min((u32)IT, n - p0) : 0u;  // items holding elements
   u64 prevk = ~0ull, nextk = ~0ull;
   if (p0 > 0 && p0 - 1 < n) prevk = s_keys[blocked_slot(p0 - 1)] & KM;
   if (p0 + IT < n) nextk = s_keys[blocked_slot(p0 + IT)] & KM;
-  bool head[IT], tail[IT], nohead[IT];
+  u32 hmask = 0, tmask = 0, nhmask = 0;  // run head, run tail, before the thread's first head
   double part[IT];
   double acc = 0.0;
-  bool seen = false;
-  u32 hc = 0;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const bool v = p0 + j < n;
-    valid[j] = v;
+    const bool v = (u32)j < nv;
     const u64 mk = skey[j] & KM;
     const u64 before = j == 0 ? prevk : (skey[j - 1] & KM);
-    const u64 after = j == IT - 1 ? nextk : (p0 + j + 1 < n ? (skey[j + 1] & KM) : ~0ull);
-    head[j] = v && (p0 + j == 0 || before != mk);
-    tail[j] = v && (p0 + j == n - 1 || after != mk);
-    if (head[j]) {
-      acc = 0.0;
-      seen = true;
-      ++hc;
-    }
+    const u64 after = j == IT - 1 ? nextk : ((u32)j + 1 < nv ? (skey[j + 1] & KM) : ~0ull);
+    const bool hd = v && (p0 + j == 0 || before != mk);
+    const bool tl = v && (p0 + j == n - 1 || after != mk);
+    hmask |= (hd ? 1u : 0u) << j;
+    tmask |= (tl ? 1u : 0u) << j;
+    if (hd) acc = 0.0;
     if (v) acc += (double)s_w[(u32)skey[j] & IM];
     part[j] = acc;
-    nohead[j] = !seen;
   }
+  const u32 hc = __popc(hmask);
+  const u32 seen = hmask ? 1u : 0u;
+  nhmask = hmask ? ((1u << (__ffs(hmask) - 1)) - 1u) : 0xffu;
   // segmented scan of (seen, acc) over lanes, then over waves
   double x = acc;
-  u32 fl = seen ? 1u : 0u;
+  u32 fl = seen;
 #pragma unroll
   for (int d = 1; d < kWave; d <<= 1) {
     const double y = __shfl_up(x, d, kWave);
@@ -403,21 +419,14 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   // run index base: heads in earlier threads
   const u32 hinc = wave_inclusive_sum(hc);
   u32 nruns;
-  const u32 hwave = block_offset(__shfl(hinc, kWave - 1, kWave), s_tmp, &nruns);  // has barriers
-  u32 hbase = hwave + hinc - hc;
+  const u32 hwave = block_offset(__shfl(hinc, kWave - 1, kWave), s_tmp, &nruns);  // barriers
+  const u32 hbase = hwave + hinc - hc;
   if (!cflag) {
     double pre = 0.0;
     for (u32 v = 0; v < w; ++v) pre = s_wflag[v] ? s_wsum[v] : pre + s_wsum[v];
     carry += pre;
   }
-  double sum[IT];
-  u32 runidx[IT];
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    sum[j] = part[j] + (nohead[j] ? carry : 0.0);
-    if (head[j]) ++hbase;
-    runidx[j] = hbase - 1;
-  }
+
   // 5. every run's last element publishes (sorted position, weight) under
   //    its run number; the block then emits the runs in parallel, run r of
   //    the tile to temp[rb + r].  The first and last run of a source record
@@ -427,9 +436,12 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   u16 *s_runpos = reinterpret_cast<u16 *>(s_cnt);  // sort counters are free now
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    if (!tail[j]) continue;
-    s_runsum[runidx[j]] = (float)sum[j];
-    s_runpos[runidx[j]] = (u16)(p0 + j);
+    if (!((tmask >> j) & 1u)) continue;
+    // runs started at or before item j: heads in earlier threads + own heads
+    const u32 r = hbase + __popc(hmask & ((2u << j) - 1u)) - 1u;
+    const double sm = part[j] + (((nhmask >> j) & 1u) ? carry : 0.0);
+    s_runsum[r] = (float)sm;
+    s_runpos[r] = (u16)(p0 + j);
   }
   __syncthreads();
   const u64 keymask = (1ull << a.key_bits) - 1;
@@ -464,20 +476,24 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
 }
 
 // Per merge tile t, the first source whose records start at or after
-// min(t * kMergeWindow, R), for t in [0, ntiles].
-__global__ void k_tile_sources(const u64 *roff, u32 nsrc, u64 R, u64 ntiles, u32 *tile_src) {
+// min(t * W, R), for t in [0, ntiles].
+__global__ void k_tile_sources(const u64 *roff, u32 nsrc, u64 R, u64 W, u64 ntiles,
+                               u32 *tile_src) {
   for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t <= ntiles; t += (u64)gridDim.x * blockDim.x) {
-    const u64 x = min(t * kMergeWindow, R);
+    const u64 x = min(t * W, R);
     tile_src[t] = (u32)min(lower_bound_dev<u64>(roff, (u64)nsrc + 1, x), (u64)nsrc);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Multi-block path for sources of more than kMergeWindow records.
+// Multi-block path for sources of more than kMergeSmall records.
 __global__ void k_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st) {
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool is_big = u < nsrc && roff[u + 1] - roff[u] > kMergeWindow;
+  const u64 c = u < nsrc ? roff[u + 1] - roff[u] : 0;
+  const bool is_big = c > kMergeSmall;
   wave_append(is_big, (u32)u, big, &st->nbig);
+  const u32 m = wave_max((u32)(is_big ? 0 : c));
+  if (lane_id() == 0 && m) atomicMax(&st->max_small, m);
 }
 
 __global__ void k_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt) {
@@ -615,6 +631,7 @@ __global__ void k_merged_total(const u64 *at, Status *st) { st->merged = *at; }
 __global__ void k_reset_level(Status *st) {
   st->R = st->M = st->merged = st->RB = 0;
   st->nwide = st->nheavy = st->nbig = st->nnew = 0;
+  st->max_small = 0;
 }
 
 }  // namespace
@@ -626,10 +643,10 @@ void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStre
 
 void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s) {
   if (a.R == 0) return;
-  const u64 g = ceil_div(a.R, kMergeWindow);
+  const u64 g = ceil_div(a.R, a.window);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
-  hipLaunchKernelGGL(k_tile_sources, dim3(grid1(g + 1)), dim3(256), 0, s, a.roff, a.nsrc, a.R, g,
-                     a.tile_src);
+  hipLaunchKernelGGL(k_tile_sources, dim3(grid1(g + 1)), dim3(256), 0, s, a.roff, a.nsrc, a.R,
+                     a.window, g, a.tile_src);
   if (wide_keys)
     hipLaunchKernelGGL((k_merge_tiles<u64>), dim3((unsigned)g), dim3(NT), 0, s, a);
   else

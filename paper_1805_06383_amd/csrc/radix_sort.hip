@@ -43,19 +43,20 @@ __global__ __launch_bounds__(kNT) void k_digit_scatter(const u64 *keys, const u3
   const u64 base = (u64)blockIdx.x * kTile + (u64)w * (kWave * kIT);
   u64 key[kIT];
   u32 val[kIT], dig[kIT], rid[kIT];
-  bool valid[kIT];
+  u32 valid = 0;
 #pragma unroll
   for (int j = 0; j < kIT; ++j) {
     const u64 e = base + (u64)j * kWave + lane;
-    valid[j] = e < n;
-    key[j] = valid[j] ? keys[e] : 0;
-    val[j] = valid[j] ? vals[e] : 0;
+    const bool v = e < n;
+    valid |= (v ? 1u : 0u) << j;
+    key[j] = v ? keys[e] : 0;
+    val[j] = v ? vals[e] : 0;
     dig[j] = (u32)(key[j] >> shift) & mask;
   }
   block_rank_digits<kNT, kIT>(dig, valid, bits, rid, s_cnt, s_base, s_tmp);
 #pragma unroll
   for (int j = 0; j < kIT; ++j) {
-    if (!valid[j]) continue;
+    if (!((valid >> j) & 1u)) continue;
     const u64 pos = (u64)offs[(u64)dig[j] * nb + blockIdx.x] + rid[j];
     keys_out[pos] = key[j];
     vals_out[pos] = val[j];
