@@ -42,10 +42,39 @@ def parse():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--max-levels", type=int, default=0)
-    ap.add_argument("--oracle-levels", type=int, default=5,
-                    help="level cap of the bounded CPU-oracle sample")
+    ap.add_argument("--oracle-levels", type=int, default=0,
+                    help="depth cap of the CPU-oracle sample (0: the whole workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="first run a plain device copy of this many MiB three times "
+                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+def kernel_source_digest(name: str) -> str:
+    import hashlib
+    path = os.path.join(ROOT, "paper_1805_06383_amd", "csrc", name)
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def recorded_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary,
+    or None when there is none or the kernel's source changed since."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    src = fields.get("source")
+    if not src or kernel_source_digest(src) != fields.get("source_sha256"):
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def algorithmic_bytes(st: dict, R: int, merged: int) -> dict:
@@ -73,7 +102,8 @@ def cpu_baseline(m1, m2, levels: int) -> dict:
         "unit": "arcs/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": (f"same workload with the breadth-first search capped at depth {levels}: "
+        "sample": ((f"same workload with the breadth-first search capped at depth {levels}: "
+                    if levels else "the whole workload: ") +
                    f"{r.num_premerge} unmerged / {r.num_arcs} merged arcs, "
                    f"{r.num_states} states, {r.seconds:.2f} s on 1 of {os.cpu_count()} host "
                    f"cores ({platform.processor() or platform.machine()}); value = unmerged arcs/s"),
@@ -94,6 +124,15 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_probe_mib:
+        nbytes = args.copy_probe_mib << 20
+        a_ = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        b_ = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            b_.copy_(a_)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3}), file=sys.stderr, flush=True)
+        del a_, b_
     h1, h2 = W.make_config(args.config, args.seed)
     m1 = fstc.DeviceFST.from_host(h1, dev)
     m2 = fstc.DeviceFST.from_host(h2, dev)
@@ -132,9 +171,12 @@ def main():
                       "avg_launch_ms": ms / launches, "bytes_per_step": ab[name],
                       "bytes_per_launch": ab[name] / launches, "GBps": gbs}
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
-    roof = {"bound": "hbm", "kernel": {"write": "k_expand", "merge": "k_merge_tiles"}[dom],
+    kname = {"write": "k_expand", "merge": "k_merge_tiles"}[dom]
+    roof = {"bound": "hbm", "kernel": kname,
             "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": kern[dom]["GBps"] / HBM_PEAK_GBS, "traffic": None}
+            "frac": kern[dom]["GBps"] / HBM_PEAK_GBS,
+            "traffic": (recorded_traffic(kname, f"config{args.config}")
+                        if not args.max_levels else None)}
 
     out = {
         "metric": METRIC,
