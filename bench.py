@@ -83,14 +83,13 @@ def algorithmic_bytes(st: dict, R: int, merged: int) -> dict:
     write kernel: every unmerged record written once (key + float32 weight)
       plus one 24-byte match descriptor read per matched (source, symbol);
     merge kernel: every record of a tile-merged source read once, every
-      merged arc written once (16 bytes: slot, a, c, weight) and its target
-      pair probed once in the visited table (8-byte key).
+      merged run written once (16 bytes: source, part-rank key, weight).
     """
     rec = st["record_key_bytes"] + 4
     tile_records = R - st["total_big_records"]
     return {
         "write": R * rec + st["total_matches"] * 24,
-        "merge": tile_records * rec + merged * (16 + 8),
+        "merge": tile_records * rec + merged * 16,
     }
 
 

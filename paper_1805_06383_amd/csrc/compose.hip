@@ -296,7 +296,7 @@ void Composer::run(fstc_result *out) {
     // merge window: as wide as the largest small source allows (see level.hpp)
     const u64 max_small = std::max<u32>(1, hs->st.max_small);
     const u64 window = nbig ? kMergeSmall : (u64)kMergeCap - max_small + 1;
-    tiles_m.ensure((ceil_div(R, window) + 1) * 4);
+    tiles_m.ensure(ceil_div(R, window) * sizeof(uint4));
     const u64 newcap = std::min<u64>(R, pairspace - n_states);
     newlist.ensure(std::max<u64>(newcap, 1) * 4);
 
@@ -353,7 +353,7 @@ void Composer::run(fstc_result *out) {
     ma.newlist = newlist.as<u32>();
     ma.newcap = newcap;
     ma.temp = temp.as<uint4>();
-    ma.tile_src = tiles_m.as<u32>();
+    ma.tiles = tiles_m.as<uint4>();
     ma.window = window;
     ma.tstart = tstart.as<u64>();
     ma.mend = mend.as<u64>();
@@ -377,6 +377,7 @@ void Composer::run(fstc_result *out) {
     }
     launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
     exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
+    launch_emit_runs(ma, aoff.as<u64>(), s);
     launch_merged_total(aoff.as<u64>() + nsrc, dst, s);
     T.end(kMerge);
     sync_status();

@@ -253,11 +253,24 @@ __global__ __launch_bounds__(kHeavyNT) void k_emit_heavy(LevelArgs a) {
   }
 }
 
+// 8 consecutive record keys with 16-byte stores (p is 32-byte aligned).
+__device__ __forceinline__ void store_record_row(u32 *p, const u32 (&k)[8]) {
+  uint4 *q = reinterpret_cast<uint4 *>(p);
+  q[0] = make_uint4(k[0], k[1], k[2], k[3]);
+  q[1] = make_uint4(k[4], k[5], k[6], k[7]);
+}
+__device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[8]) {
+  ulonglong2 *q = reinterpret_cast<ulonglong2 *>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) q[i] = make_ulonglong2(k[2 * i], k[2 * i + 1]);
+}
+
 // ---------------------------------------------------------------------------
 // Arc-pair write pass.  Workgroup b produces records [b*2048, (b+1)*2048):
-// the matches overlapping the window are staged in LDS, each record finds its
-// match by binary search there, and (i, j) = divmod(offset, n2) selects the
-// M1 and M2 arcs.  Record = (part1 << b2 | part2, p1 * p2).
+// the matches overlapping the window are staged in LDS; each thread finds the
+// match of its first record by binary search there, takes
+// (i, j) = divmod(offset, n2) to select the M1 and M2 arcs, and steps through
+// its 8 consecutive records.  Record = (part1 << b2 | part2, p1 * p2).
 template <class KT>
 __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const u64 *mrbase, u64 M,
                                                       u64 R, const uint2 *arcs1,
@@ -282,27 +295,55 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
     s_m[i] = match[k0 + i];
   }
   __syncthreads();
+  // thread t writes the consecutive records r0 + 8t .. r0 + 8t + 7: one
+  // search and one division, then (i1, i2) advance through the match
+  const u32 rel0 = threadIdx.x * kExpandIT;
+  const u64 rfirst = r0 + rel0;
+  if (rfirst >= rend) return;
+  const u32 cnt = (u32)min<u64>(kExpandIT, rend - rfirst);
+  u32 mi = (u32)last_le<u32>(s_rel, nm, rel0);
+  uint4 m = s_m[mi];
+  const u64 t = mi == 0 ? rfirst - base0 : (u64)(rel0 - s_rel[mi]);
+  u32 i1, i2;
+  if (t < (1ull << 32)) {
+    const u32 tt = (u32)t;
+    i1 = tt / m.w;
+    i2 = tt - i1 * m.w;
+  } else {
+    const u64 q = t / m.w;
+    i1 = (u32)q;
+    i2 = (u32)(t - q * m.w);
+  }
+  KT key[kExpandIT];
+  float wt[kExpandIT];
 #pragma unroll
   for (int j = 0; j < kExpandIT; ++j) {
-    const u64 r = r0 + (u64)j * kExpandNT + threadIdx.x;
-    if (r >= rend) continue;
-    const u32 rel = (u32)(r - r0);
-    const u32 mi = (u32)last_le<u32>(s_rel, nm, rel);
-    const uint4 m = s_m[mi];
-    const u64 t = mi == 0 ? r - base0 : (u64)(rel - s_rel[mi]);
-    u64 i1, i2;
-    if (t < (1ull << 32)) {
-      const u32 tt = (u32)t, q = tt / m.w;
-      i1 = q;
-      i2 = tt - q * m.w;
-    } else {
-      i1 = t / m.w;
-      i2 = t - i1 * m.w;
+    key[j] = 0;
+    wt[j] = 0.f;
+    if ((u32)j < cnt) {
+      const uint2 A1 = arcs1[m.x + i1];
+      const uint2 A2 = arcs2[m.y + i2];
+      key[j] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
+      wt[j] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
+      if (++i2 == m.w) {
+        i2 = 0;
+        if (++i1 == m.z && (u32)j + 1 < cnt) {
+          i1 = 0;
+          m = s_m[++mi];
+        }
+      }
     }
-    const uint2 A1 = arcs1[m.x + i1];
-    const uint2 A2 = arcs2[m.y + i2];
-    rec_key[r] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
-    rec_w[r] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
+  }
+  if (cnt == kExpandIT) {
+    store_record_row(rec_key + rfirst, key);
+    float4 *wp = reinterpret_cast<float4 *>(rec_w + rfirst);
+    wp[0] = make_float4(wt[0], wt[1], wt[2], wt[3]);
+    wp[1] = make_float4(wt[4], wt[5], wt[6], wt[7]);
+  } else {
+    for (u32 j = 0; j < cnt; ++j) {
+      rec_key[rfirst + j] = key[j];
+      rec_w[rfirst + j] = wt[j];
+    }
   }
 }
 

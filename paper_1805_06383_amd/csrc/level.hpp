@@ -92,11 +92,12 @@ struct MergeArgs {
   u64 hmask;
   u32 *newlist;
   u64 newcap;
-  uint4 *temp;     // [R] merged arcs (slot, a, c, weight bits)
+  uint4 *temp;     // [R] merged runs: (source, key lo, key hi, weight bits) from the
+                   // merge, then (slot, a, c, weight bits) after launch_emit_runs
   u64 *tstart;     // [nsrc] first temp slot of each source's merged arcs (0 if none)
   u64 *mend;       // [nsrc] one past its last slot (0 if none)
   u64 window;      // W: tile t takes the sources starting in [t W, (t + 1) W)
-  u32 *tile_src;   // [ceil(R / W) + 1] scratch: first source of each tile
+  uint4 *tiles;    // [ceil(R / W)] scratch: tile descriptors
   Status *st;
   // multi-block path
   u32 *big;        // [nbig] level-local source indices
@@ -124,6 +125,9 @@ void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff
                     u32 lo, u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
                     float *ow, u32 *err, hipStream_t s);
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s);
+// Visited-table inserts and label lookups for every merged arc of the level
+// (aoff: exclusive scan of the merged counts, aoff[nsrc] = total).
+void launch_emit_runs(const MergeArgs &a, const u64 *aoff, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
 void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);

@@ -31,7 +31,6 @@ constexpr int NT = kMergeNT;
 constexpr int IT = kMergeIT;
 constexpr int C = kMergeCap;
 constexpr int NW = NT / kWave;
-constexpr int kEmitBatch = 2;  // items whose emission lookups are overlapped
 
 inline unsigned grid1(u64 n, int nt = 256) {
   return (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(n, nt), 1u << 20));
@@ -245,20 +244,17 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
     wkey[j] = r < a.R ? rk[r] : KT(0);
     wwt[j] = r < a.R ? a.rec_w[r] : 0.f;
   }
-  const u32 s0 = a.tile_src[tile];
-  u32 s1 = a.tile_src[tile + 1];
-  // a multi-block source can only be the last one starting in the window
-  if (s1 > s0 && a.roff[s1] - a.roff[s1 - 1] > kMergeSmall) --s1;
+  const uint4 td = a.tiles[tile];
+  const u32 s0 = td.x, s1 = td.y;
   if (s0 >= s1) return;
-  const u64 rb = a.roff[s0];
-  const u64 span = a.roff[s1] - rb;
-  if (span > (u64)C || rb < tstart || rb + span > tstart + C) {
+  const u64 rb = tstart + td.z;
+  if (td.w > (u32)C || (u64)td.z + td.w > (u64)C) {
     if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
     return;
   }
-  const u32 n = (u32)span;
+  const u32 n = td.w;
   if (n == 0) return;
-  const u32 off = (u32)(rb - tstart);  // window position of tile element 0
+  const u32 off = td.z;  // window position of tile element 0
 
   // 1. mark the first record of every non-empty source with its index + 1
   u32 *s_mark = reinterpret_cast<u32 *>(s_keys);
@@ -445,43 +441,32 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
   }
   __syncthreads();
   const u64 keymask = (1ull << a.key_bits) - 1;
-  for (u32 r0 = 0; r0 < nruns; r0 += NT * kEmitBatch) {
-    bool act[kEmitBatch];
-    u32 u_[kEmitBatch];
-    u64 key_[kEmitBatch], tpos[kEmitBatch];
-    float wt[kEmitBatch];
-#pragma unroll
-    for (int i = 0; i < kEmitBatch; ++i) {
-      const u32 r = r0 + i * NT + threadIdx.x;
-      act[i] = r < nruns;
-      u_[i] = 0;
-      key_[i] = 0;
-      tpos[i] = 0;
-      wt[i] = 0.f;
-      if (!act[i]) continue;
-      const u64 sk = s_keys[blocked_slot(s_runpos[r])];
-      const u64 seg = sk >> segshift;
-      key_[i] = (sk >> kIdxBits) & keymask;
-      u_[i] = s_segsrc[seg];
-      tpos[i] = rb + r;
-      wt[i] = s_runsum[r];
-      const bool first = r == 0 || (s_keys[blocked_slot(s_runpos[r - 1])] >> segshift) != seg;
-      const bool last =
-          r == nruns - 1 || (s_keys[blocked_slot(s_runpos[r + 1])] >> segshift) != seg;
-      if (first) a.tstart[u_[i]] = rb + r;
-      if (last) a.mend[u_[i]] = rb + r + 1;
-    }
-    emit_batch<kEmitBatch>(a, act, u_, key_, tpos, wt);
+  for (u32 r = threadIdx.x; r < nruns; r += NT) {
+    const u64 sk = s_keys[blocked_slot(s_runpos[r])];
+    const u64 seg = sk >> segshift;
+    const u64 key = (sk >> kIdxBits) & keymask;
+    const u32 u = s_segsrc[seg];
+    a.temp[rb + r] = make_uint4(u, (u32)key, (u32)(key >> 32), __float_as_uint(s_runsum[r]));
+    const bool first = r == 0 || (s_keys[blocked_slot(s_runpos[r - 1])] >> segshift) != seg;
+    const bool last =
+        r == nruns - 1 || (s_keys[blocked_slot(s_runpos[r + 1])] >> segshift) != seg;
+    if (first) a.tstart[u] = rb + r;
+    if (last) a.mend[u] = rb + r + 1;
   }
 }
 
-// Per merge tile t, the first source whose records start at or after
-// min(t * W, R), for t in [0, ntiles].
-__global__ void k_tile_sources(const u64 *roff, u32 nsrc, u64 R, u64 W, u64 ntiles,
-                               u32 *tile_src) {
-  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t <= ntiles; t += (u64)gridDim.x * blockDim.x) {
-    const u64 x = min(t * W, R);
-    tile_src[t] = (u32)min(lower_bound_dev<u64>(roff, (u64)nsrc + 1, x), (u64)nsrc);
+// Descriptor of merge tile t: the small sources whose first record falls in
+// [t W, (t + 1) W) -- (first source, one past the last, window offset of the
+// first record, number of records).
+__global__ void k_tile_sources(const u64 *roff, u32 nsrc, u64 R, u64 W, u64 ntiles, uint4 *tiles) {
+  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t < ntiles; t += (u64)gridDim.x * blockDim.x) {
+    const u64 tstart = t * W;
+    const u32 s0 = (u32)min(lower_bound_dev<u64>(roff, (u64)nsrc + 1, tstart), (u64)nsrc);
+    u32 s1 = (u32)min(lower_bound_dev<u64>(roff, (u64)nsrc + 1, min(tstart + W, R)), (u64)nsrc);
+    // a multi-block source can only be the last one starting in the window
+    if (s1 > s0 && roff[s1] - roff[s1 - 1] > kMergeSmall) --s1;
+    const u64 rb = roff[s0];
+    tiles[t] = make_uint4(s0, s1, (u32)(rb - min(rb, tstart)), (u32)(roff[s1] - rb));
   }
 }
 
@@ -521,30 +506,52 @@ __global__ void k_run_heads(const u64 *keys, u64 n, u32 *flags) {
 __global__ void k_big_reduce(MergeArgs a, const u64 *bigoff, u64 RB, const u64 *skey,
                              const u32 *sval, const u32 *flags, const u32 *ridx) {
   const u64 g = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  bool act[1] = {false};
-  u32 u[1] = {0};
-  u64 key[1] = {0}, tpos[1] = {0};
-  float wt[1] = {0.f};
-  if (g < RB && flags[g]) {
-    const u64 mk = skey[g];
-    const u32 i = (u32)(mk >> a.key_bits);
-    double acc = 0.0;
-    u64 q = g;
-    while (q < RB && skey[q] == mk) {
-      acc += (double)__uint_as_float(sval[q]);
-      ++q;
-    }
-    u[0] = a.big[i];
-    const u64 local = ridx[g] - ridx[bigoff[i]];
-    const u64 base = a.roff[u[0]];
-    if (g == bigoff[i]) a.tstart[u[0]] = base;
-    if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mend[u[0]] = base + local + 1;
-    key[0] = mk & ((1ull << a.key_bits) - 1);
-    tpos[0] = base + local;
-    wt[0] = (float)acc;
-    act[0] = true;
+  if (g >= RB || !flags[g]) return;
+  const u64 mk = skey[g];
+  const u32 i = (u32)(mk >> a.key_bits);
+  double acc = 0.0;
+  u64 q = g;
+  while (q < RB && skey[q] == mk) {
+    acc += (double)__uint_as_float(sval[q]);
+    ++q;
   }
-  emit_batch<1>(a, act, u, key, tpos, wt);
+  const u32 u = a.big[i];
+  const u64 local = ridx[g] - ridx[bigoff[i]];
+  const u64 base = a.roff[u];
+  if (g == bigoff[i]) a.tstart[u] = base;
+  if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mend[u] = base + local + 1;
+  const u64 key = mk & ((1ull << a.key_bits) - 1);
+  a.temp[base + local] = make_uint4(u, (u32)key, (u32)(key >> 32), __float_as_uint((float)acc));
+}
+
+// Merged arcs of the level, one per thread (grid-stride, wave-uniform trip
+// count): the run record (source, part-rank key, weight) at its temp slot
+// becomes (slot, a, c, weight) -- part ranks mapped back to (r1, a) and
+// (r2, c), the target pair inserted in the visited table, new pairs listed.
+// Separate from the merge so that these dependent lookups run at full
+// occupancy.
+__global__ __launch_bounds__(256) void k_emit_runs(MergeArgs a, const u64 *aoff) {
+  const u64 M = aoff[a.nsrc];
+  const u64 lane = lane_id();
+  const u64 wave0 = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const u64 nwaves = (u64)gridDim.x * blockDim.x / kWave;
+  for (u64 base = wave0 * kWave; base < M; base += nwaves * kWave) {
+    const u64 k = base + lane;
+    bool act[1] = {k < M};
+    u32 uu[1] = {0};
+    u64 key[1] = {0}, tpos[1] = {0};
+    float wt[1] = {0.f};
+    if (act[0]) {
+      const u32 u = (u32)last_le<u64>(aoff, a.nsrc, k);
+      const u64 t = a.tstart[u] + (k - aoff[u]);
+      const uint4 rec = a.temp[t];
+      uu[0] = rec.x;
+      key[0] = (u64)rec.y | ((u64)rec.z << 32);
+      tpos[0] = t;
+      wt[0] = __uint_as_float(rec.w);
+    }
+    emit_batch<1>(a, act, uu, key, tpos, wt);
+  }
 }
 
 // Merged arcs per source from where its runs start and end in temp.
@@ -645,8 +652,8 @@ void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s) {
   if (a.R == 0) return;
   const u64 g = ceil_div(a.R, a.window);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
-  hipLaunchKernelGGL(k_tile_sources, dim3(grid1(g + 1)), dim3(256), 0, s, a.roff, a.nsrc, a.R,
-                     a.window, g, a.tile_src);
+  hipLaunchKernelGGL(k_tile_sources, dim3(grid1(g)), dim3(256), 0, s, a.roff, a.nsrc, a.R,
+                     a.window, g, a.tiles);
   if (wide_keys)
     hipLaunchKernelGGL((k_merge_tiles<u64>), dim3((unsigned)g), dim3(NT), 0, s, a);
   else
@@ -715,6 +722,10 @@ void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff
   if (!M) return;
   hipLaunchKernelGGL(k_compact, dim3(grid1(M)), dim3(256), 0, s, temp, R, tstart, aoff, nsrc, lo,
                      M, hvals, osrc, odst, oil, ool, ow, err);
+}
+
+void launch_emit_runs(const MergeArgs &a, const u64 *aoff, hipStream_t s) {
+  hipLaunchKernelGGL(k_emit_runs, dim3(2048), dim3(256), 0, s, a, aoff);
 }
 
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s) {
