@@ -77,19 +77,23 @@ def recorded_traffic(kernel: str, workload: str):
         return None
 
 
-def algorithmic_bytes(st: dict, R: int, merged: int) -> dict:
-    """Bytes each of the two dominant kernels must move, per compose call.
+def algorithmic_bytes(st: dict, R: int) -> dict:
+    """Bytes each of the three tile kernels must move, per compose call.
 
-    write kernel: every unmerged record written once (key + float32 weight)
-      plus one 24-byte match descriptor read per matched (source, symbol);
-    merge kernel: every record of a tile-merged source read once, every
-      merged run written once (16 bytes: source, part-rank key, weight).
+    write (k_expand): every unmerged record written once (key + float32
+      weight) plus one 24-byte match descriptor read per matched
+      (source, symbol);
+    merge (k_merge_dense) and sort (k_merge_tiles): every record of the tiles
+      each merges read once, every merged run it produces written once
+      (16 bytes: source, part-rank key, weight).
     """
     rec = st["record_key_bytes"] + 4
     tile_records = R - st["total_big_records"]
+    dense = st["total_dense_records"]
     return {
         "write": R * rec + st["total_matches"] * 24,
-        "merge": tile_records * rec + merged * 16,
+        "merge": dense * rec + st["total_dense_runs"] * 16,
+        "sort": (tile_records - dense) * rec + st["total_sort_runs"] * 16,
     }
 
 
@@ -159,18 +163,23 @@ def main():
     post_rate = merged * args.steps / secs
 
     st = last.stats
-    ab = algorithmic_bytes(st, R, merged)
+    ab = algorithmic_bytes(st, R)
     kern = {}
-    for name, ms_key, n_key in (("write", "ms_write_kernel", "write_launches"),
-                                ("merge", "ms_merge_kernel", "merge_launches")):
+    for name, kernel, ms_key, n_key in (("write", "k_expand", "ms_write_kernel", "write_launches"),
+                                        ("merge", "k_merge_dense", "ms_merge_kernel", "merge_launches"),
+                                        ("sort", "k_merge_listed" if st["merge_launches"]
+                                         else "k_merge_tiles", "ms_sort_kernel", "sort_launches")):
         ms = sums[ms_key] / args.steps
         launches = max(1, st[n_key])
         gbs = ab[name] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
-        kern[name] = {"ms_per_step": ms, "launches_per_step": st[n_key],
+        kern[name] = {"kernel": kernel, "ms_per_step": ms, "launches_per_step": st[n_key],
                       "avg_launch_ms": ms / launches, "bytes_per_step": ab[name],
                       "bytes_per_launch": ab[name] / launches, "GBps": gbs}
-    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
-    kname = {"write": "k_expand", "merge": "k_merge_tiles"}[dom]
+    both_ms = sum(k["ms_per_step"] for k in kern.values())
+    kern["expand+merge"] = {"ms_per_step": both_ms, "bytes_per_step": sum(ab.values()),
+                            "GBps": sum(ab.values()) / (both_ms * 1e-3) / 1e9 if both_ms else 0.0}
+    dom = max(ab, key=lambda k: kern[k]["ms_per_step"])
+    kname = kern[dom]["kernel"]
     roof = {"bound": "hbm", "kernel": kname,
             "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": kern[dom]["GBps"] / HBM_PEAK_GBS,

@@ -133,13 +133,19 @@ typedef struct fstc_stats {
   double ms_merge;            /* segmented sort + reduce + visited inserts  */
   double ms_assign;           /* id assignment + result append              */
   double ms_write_kernel;     /* arc-pair write kernel alone, all levels    */
-  double ms_merge_kernel;     /* merge-tile kernel alone, all levels        */
+  double ms_merge_kernel;     /* dense-table merge kernel alone, all levels */
   uint32_t write_launches;    /* launches of the arc-pair write kernel      */
-  uint32_t merge_launches;    /* launches of the merge-tile kernel          */
+  uint32_t merge_launches;    /* launches of the dense-table merge kernel   */
   uint64_t total_matches;     /* matched (source, inner symbol) pairs       */
   uint64_t total_big_records; /* records merged by the multi-block path     */
   uint32_t record_key_bytes;  /* 4 or 8: key width of an unmerged record    */
   uint32_t key_bits;          /* part-rank bits of a record key             */
+  double ms_sort_kernel;      /* sorting merge-tile kernel alone            */
+  uint32_t sort_launches;     /* launches of the sorting merge-tile kernel  */
+  uint32_t reserved1;
+  uint64_t total_dense_records; /* records merged through the dense table   */
+  uint64_t total_dense_runs;  /* merged arcs the dense table produced        */
+  uint64_t total_sort_runs;   /* merged arcs the sorting tiles produced      */
 } fstc_stats;
 
 /*

@@ -114,7 +114,9 @@ const char *device_error_text(u32 e) {
   return "device index check failed";
 }
 
-enum Phase { kCsr, kCount, kExpand, kMerge, kAssign, kWriteKernel, kMergeKernel, kNumPhases };
+enum Phase {
+  kCsr, kCount, kExpand, kMerge, kAssign, kWriteKernel, kMergeKernel, kSortKernel, kNumPhases
+};
 
 // HIP-event timing of the phases on the call's stream (only with stats).
 struct Timer {
@@ -247,13 +249,14 @@ void Composer::run(fstc_result *out) {
   u64 n_states = 1, arcs = 0, premerge = 0;
   u32 lo = 0, hi = 1, depth = 0, new_levels = 0, expanded_levels = 0;
   u64 max_frontier = 0, max_level_pre = 0, big_total = 0, total_matches = 0, big_records = 0;
-  u32 write_launches = 0, merge_launches = 0;
+  u32 write_launches = 0, merge_launches = 0, sort_launches = 0;
+  u64 dense_records = 0, dense_runs = 0, sort_runs = 0;
 
   Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
   Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
       bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
       stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A), tiles_e(&A), tiles_m(&A), tstart(&A),
-      mend(&A);
+      mend(&A), sortlist(&A);
 
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
@@ -296,7 +299,9 @@ void Composer::run(fstc_result *out) {
     // merge window: as wide as the largest small source allows (see level.hpp)
     const u64 max_small = std::max<u32>(1, hs->st.max_small);
     const u64 window = nbig ? kMergeSmall : (u64)kMergeCap - max_small + 1;
-    tiles_m.ensure(ceil_div(R, window) * sizeof(uint4));
+    const u64 ntiles = ceil_div(R, window);
+    tiles_m.ensure(ntiles * sizeof(uint4));
+    sortlist.ensure(ntiles * 4);
     const u64 newcap = std::min<u64>(R, pairspace - n_states);
     newlist.ensure(std::max<u64>(newcap, 1) * 4);
 
@@ -354,16 +359,25 @@ void Composer::run(fstc_result *out) {
     ma.newcap = newcap;
     ma.temp = temp.as<uint4>();
     ma.tiles = tiles_m.as<uint4>();
+    ma.sortlist = sortlist.as<u32>();
+    ma.ntiles = ntiles;
     ma.window = window;
     ma.tstart = tstart.as<u64>();
     ma.mend = mend.as<u64>();
     ma.st = dst;
     ma.big = big.as<u32>();
+    launch_tile_sources(ma, s);
     T.end(kMerge);
+    if (key_bits <= kDenseKeyBits) {
+      T.begin();
+      launch_merge_dense(ma, s);
+      T.end(kMergeKernel);
+      ++merge_launches;
+    }
     T.begin();
-    launch_merge_tiles(ma, wide_keys, s);
-    T.end(kMergeKernel);
-    ++merge_launches;
+    launch_merge_sort(ma, wide_keys, s);
+    T.end(kSortKernel);
+    ++sort_launches;
     T.begin();
     if (nbig) {
       bigcnt.ensure((u64)nbig * 8);
@@ -383,6 +397,9 @@ void Composer::run(fstc_result *out) {
     sync_status();
     const u32 nnew = hs->st.nnew;
     const u64 merged = hs->st.merged;
+    dense_records += hs->st.dense_records;
+    dense_runs += hs->st.dense_runs;
+    sort_runs += hs->st.sort_runs;
     if (n_states + nnew > state_limit)
       throw Error(FSTC_ERR_CAPACITY, "reachable states exceed the state limit");
     if (o.max_arcs && arcs + merged > o.max_arcs)
@@ -456,6 +473,11 @@ void Composer::run(fstc_result *out) {
     stats->ms_merge_kernel = ms[kMergeKernel];
     stats->write_launches = write_launches;
     stats->merge_launches = merge_launches;
+    stats->ms_sort_kernel = ms[kSortKernel];
+    stats->sort_launches = sort_launches;
+    stats->total_dense_records = dense_records;
+    stats->total_dense_runs = dense_runs;
+    stats->total_sort_runs = sort_runs;
     stats->total_matches = total_matches;
     stats->total_big_records = big_records;
     stats->record_key_bytes = (u32)rec_bytes;
@@ -469,7 +491,7 @@ void Composer::run(fstc_result *out) {
     stats->ms_csr = ms[kCsr];
     stats->ms_count = ms[kCount];
     stats->ms_expand = ms[kExpand] + ms[kWriteKernel];
-    stats->ms_merge = ms[kMerge] + ms[kMergeKernel];
+    stats->ms_merge = ms[kMerge] + ms[kMergeKernel] + ms[kSortKernel];
     stats->ms_assign = ms[kAssign];
     stats->ms_total =
         std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();

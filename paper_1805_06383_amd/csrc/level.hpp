@@ -29,7 +29,11 @@ struct Status {
   u32 nwide, nheavy, nbig, nnew;
   u32 err;      // kErr* bits, sticky for the whole call
   u32 max_small;  // largest record count of a source merged by the tiles
-  u32 pad[2];
+  u64 dense_records;  // records of the tiles merged through a dense table
+  u64 dense_runs;     // merged arcs those tiles produced
+  u64 sort_runs;      // merged arcs of the tiles merged by sorting
+  u32 nsort;          // tiles k_merge_dense left to the sort kernel
+  u32 pad;
 };
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
@@ -49,6 +53,12 @@ constexpr int kMergeCap = kMergeNT * kMergeIT;
 constexpr u64 kMergeSmall = kMergeCap / 2;
 constexpr int kIdxBits = 12;  // log2(kMergeCap)
 constexpr int kMaxKeyBits = 64 - 2 * kIdxBits;  // 40: part-rank bits of both sides
+
+// A tile whose sources and keys span at most kDenseCap (source, key) pairs
+// ((s1 - s0) << key_bits <= kDenseCap) is merged through a table indexed by
+// that pair instead of a sort; this needs key_bits <= kDenseKeyBits.
+constexpr u32 kDenseCap = 2048;
+constexpr int kDenseKeyBits = 11;  // log2(kDenseCap)
 
 // Arc-pair write pass: 256 threads x 8 records per workgroup.
 constexpr int kExpandNT = 256;
@@ -97,14 +107,21 @@ struct MergeArgs {
   u64 *tstart;     // [nsrc] first temp slot of each source's merged arcs (0 if none)
   u64 *mend;       // [nsrc] one past its last slot (0 if none)
   u64 window;      // W: tile t takes the sources starting in [t W, (t + 1) W)
-  uint4 *tiles;    // [ceil(R / W)] scratch: tile descriptors
+  uint4 *tiles;    // [ntiles = ceil(R / W)] scratch: tile descriptors
+  u32 *sortlist;   // [ntiles] scratch: tiles left to the sort kernel
+  u64 ntiles;
   Status *st;
   // multi-block path
   u32 *big;        // [nbig] level-local source indices
 };
 
 void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStream_t s);
-void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s);
+// Tile descriptors of the level (a.tiles), then the two tile merges: the
+// dense-table kernel (only when a.key_bits <= kDenseKeyBits) and the sort
+// kernel, which takes every tile the dense kernel did not merge.
+void launch_tile_sources(const MergeArgs &a, hipStream_t s);
+void launch_merge_dense(const MergeArgs &a, hipStream_t s);
+void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s);
 // Multi-block merge of the nbig sources listed in a.big; bigoff has nbig + 1
 // entries (exclusive scan of their record counts, total RB).
 void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s);

@@ -80,6 +80,18 @@ __device__ __forceinline__ u32 blocked_slot(u32 p) {
   return (p & ~(u32)(kWave * IT - 1)) | ((p % IT) * kWave) | ((p / IT) % kWave);
 }
 
+// Tiles that the dense-table kernel takes (see k_merge_dense); it flags in
+// the descriptor (kRerouted) a tile it leaves to the sort kernel.
+constexpr u32 kRerouted = 0x80000000u;
+constexpr u64 kListedGrid = 2048;  // workgroups walking the list of tiles left to sort
+constexpr u32 kDenseEPT = kDenseCap / NT;  // table entries per thread when listing runs
+static_assert(kDenseCap % NT == 0 && (1u << kDenseKeyBits) == kDenseCap, "dense table shape");
+
+__device__ __forceinline__ bool dense_tile(const uint4 &td, int key_bits) {
+  return td.x < td.y && key_bits <= kDenseKeyBits &&
+         ((u64)(td.y - td.x) << key_bits) <= (u64)kDenseCap;
+}
+
 // Exclusive prefix over the waves of the block of one value per wave (taken
 // from any lane); *total receives the block total.  All threads must call it.
 __device__ __forceinline__ u32 block_offset(u32 wave_value, u32 *s_tmp, u32 *total) {
@@ -214,46 +226,51 @@ __device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)
   }
 }
 
-template <class KT>
-__global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
-  __shared__ u64 s_keys[C];
-  __shared__ float s_w[C];
-  __shared__ u32 s_segsrc[C];
-  __shared__ u32 s_cnt[NW * 256];
-  __shared__ u32 s_base[256];
-  __shared__ u32 s_tmp[NW];
-  __shared__ double s_wsum[NW];
-  __shared__ u32 s_wflag[NW];
+// LDS of the sorting tile merge.
+struct SortLds {
+  u64 keys[C];
+  float w[C];
+  u32 segsrc[C];
+  u32 cnt[NW * 256];
+  u32 base[256];
+  u32 tmp[NW];
+  double wsum[NW];
+  u32 wflag[NW];
+};
 
+// Sorting merge of tile `tile` by the whole block.
+template <class KT>
+__device__ __forceinline__ void merge_sort_tile(const MergeArgs &a, u32 tile, SortLds &L) {
+  u64 *s_keys = L.keys;
+  float *s_w = L.w;
+  u32 *s_segsrc = L.segsrc, *s_cnt = L.cnt, *s_base = L.base, *s_tmp = L.tmp;
+  double *s_wsum = L.wsum;
+  u32 *s_wflag = L.wflag;
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
-  // XCD-aware tile order: workgroups are dealt round-robin to the 8 XCDs, so
-  // give each XCD a contiguous run of tiles; neighbouring tiles share half of
-  // their record window, which then stays in that XCD's L2.
-  const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
   const u64 tstart = (u64)tile * a.window;
-  // A tile's records lie in [tstart, tstart + kMergeCap): its sources start
-  // before tstart + W and each has at most kMergeCap - W + 1 records.  Load
-  // that range now, before the bounds are known, so the loads overlap the
-  // bound lookups.
-  const KT *rk = static_cast<const KT *>(a.rec_key);
+  const uint4 td = a.tiles[tile];
+  const u32 s0 = td.x, s1 = td.y;
+  if (s0 >= s1) return;
+  if (dense_tile(td, a.key_bits) && !(td.w & kRerouted)) return;  // merged by k_merge_dense
+  const u32 n = td.w & ~kRerouted;
+  const u64 rb = tstart + td.z;
+  if (n > (u32)C || (u64)td.z + n > (u64)C) {
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
+    return;
+  }
+  if (n == 0) return;
+  // the tile's records, at window positions [td.z, td.z + n) of [tstart, tstart + kMergeCap)
+  const KT *rk = static_cast<const KT *>(a.rec_key) + tstart;
+  const float *rwin = a.rec_w + tstart;
   KT wkey[IT];
   float wwt[IT];
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const u64 r = tstart + w * (kWave * IT) + j * kWave + lane;
-    wkey[j] = r < a.R ? rk[r] : KT(0);
-    wwt[j] = r < a.R ? a.rec_w[r] : 0.f;
+    const u32 wpos = w * (kWave * IT) + j * kWave + lane;
+    const bool in = wpos >= td.z && wpos - td.z < n;
+    wkey[j] = in ? rk[wpos] : KT(0);
+    wwt[j] = in ? rwin[wpos] : 0.f;
   }
-  const uint4 td = a.tiles[tile];
-  const u32 s0 = td.x, s1 = td.y;
-  if (s0 >= s1) return;
-  const u64 rb = tstart + td.z;
-  if (td.w > (u32)C || (u64)td.z + td.w > (u64)C) {
-    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
-    return;
-  }
-  const u32 n = td.w;
-  if (n == 0) return;
   const u32 off = td.z;  // window position of tile element 0
 
   // 1. mark the first record of every non-empty source with its index + 1
@@ -453,6 +470,225 @@ __global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
     if (first) a.tstart[u] = rb + r;
     if (last) a.mend[u] = rb + r + 1;
   }
+  if (threadIdx.x == 0) atomicAdd((unsigned long long *)&a.st->sort_runs, (unsigned long long)nruns);
+}
+
+// Every tile of the level, one per workgroup.  XCD-aware tile order:
+// workgroups are dealt round-robin to the 8 XCDs, so each XCD gets a
+// contiguous run of tiles, whose record windows then stay in its L2.
+template <class KT>
+__global__ __launch_bounds__(NT, 4) void k_merge_tiles(MergeArgs a) {
+  __shared__ SortLds L;
+  merge_sort_tile<KT>(a, xcd_tile(blockIdx.x, gridDim.x), L);
+}
+
+// The tiles k_merge_dense listed in a.sortlist (a.st->nsort of them); a
+// fixed grid walks the list.
+template <class KT>
+__global__ __launch_bounds__(NT, 4) void k_merge_listed(MergeArgs a) {
+  __shared__ SortLds L;
+  const u32 nsort = __hip_atomic_load(&a.st->nsort, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (u32 i = blockIdx.x; i < nsort; i += gridDim.x) {
+    merge_sort_tile<KT>(a, a.sortlist[i], L);
+    __syncthreads();  // LDS reused by the next tile
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Dense-table merge: a tile whose sources and keys span at most kDenseCap
+// (source, key) pairs needs no sort.  Entry (segment, key) of an LDS table,
+// segment = rank of the source among the tile's non-empty sources, collects
+// the records with that key.  Sums are exact-order-independent: each entry
+// adds its products as 64-bit two's-complement integers in units of
+// 2^(E - 177), E the largest biased exponent among them (pass 1 takes the
+// maximum, pass 2 adds).  A product of biased exponent be and significand m
+// (24 bits with the hidden bit) becomes floor(+-m * 2^27 / 2^(E - be)), so
+// every term is below 2^51 in magnitude, a sum of 4096 stays below 2^63, and
+// the result does not depend on the order of the atomic adds; each term loses
+// at most one unit, 2^-50 of the entry's largest term.  Entries present in
+// the tile become runs in (segment, key) order, the order of the sort path.
+// A tile holding an infinite or NaN weight is left to the sort kernel
+// (descriptor flag kRerouted).
+__device__ __forceinline__ void list_for_sort(const MergeArgs &a, u32 tile) {
+  const u32 i = atomicAdd(&a.st->nsort, 1u);
+  if (i < a.ntiles) a.sortlist[i] = tile;
+}
+
+__global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
+  __shared__ unsigned long long s_sum[kDenseCap];
+  __shared__ u32 s_exp[kDenseCap];  // 0: entry absent, else largest biased exponent + 1
+  __shared__ u32 s_segsrc[kDenseCap];
+  __shared__ u16 s_runseg[kDenseCap];
+  __shared__ u32 s_bits[C / 32];  // bit e: tile element e starts a source
+  __shared__ u32 s_pre[C / 32];   // set bits in the words before
+  __shared__ u32 s_tmp[NW];
+
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
+  const uint4 td = a.tiles[tile];
+  if (td.x >= td.y || td.w == 0) return;  // no small source starts in this window
+  if (!dense_tile(td, a.key_bits)) {
+    if (threadIdx.x == 0) list_for_sort(a, tile);
+    return;
+  }
+  const u32 n = td.w, off = td.z;
+  if (n > (u32)C || off > (u32)C - n) {
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
+    return;
+  }
+  const u64 rb = (u64)tile * a.window + off;  // first record of the tile
+  // 1. source starts -> bitmap -> segment of every element
+  if (threadIdx.x < C / 32) s_bits[threadIdx.x] = 0;
+  // a dense tile has at most kDenseCap sources: thread t takes sources
+  // s0 + t + k*NT, k < kDenseEPT, and keeps their start (or kNoStart)
+  constexpr u32 kNoStart = 0xffffffffu;
+  u32 start[kDenseEPT];
+  u64 r0[kDenseEPT], r1[kDenseEPT];
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k) {
+    r0[k] = r1[k] = 0;
+    if (td.x + k * NT < td.y) {  // uniform; loads at clamped sources, no waits here
+      const u32 u = min(td.x + threadIdx.x + k * NT, td.y - 1);
+      r0[k] = a.roff[u];
+      r1[k] = a.roff[u + 1];
+    }
+  }
+  // items: tile element e = w*512 + j*64 + lane, present when e < n (a
+  // prefix of the thread's items).  Every item loads, at min(e, n - 1), so
+  // that no load waits on a branch.
+  const u32 *rk = static_cast<const u32 *>(a.rec_key) + rb;
+  const float *rw = a.rec_w + rb;
+  const u32 e0 = w * (kWave * IT) + lane;
+  u32 key[IT];
+  float wt[IT];
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = min(e0 + j * kWave, n - 1);
+    key[j] = rk[e];
+    wt[j] = rw[e];
+  }
+  __syncthreads();  // s_bits cleared
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k)
+    start[k] = (td.x + threadIdx.x + k * NT < td.y && r1[k] != r0[k]) ? (u32)(r0[k] - rb) : kNoStart;
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k)
+    if (start[k] != kNoStart) atomicOr(&s_bits[start[k] >> 5], 1u << (start[k] & 31));
+  __syncthreads();
+  if (w == 0) {
+    const u32 c0 = __popc(s_bits[2 * lane]), c1 = __popc(s_bits[2 * lane + 1]);
+    const u32 inc = wave_inclusive_sum(c0 + c1);
+    s_pre[2 * lane] = inc - c0 - c1;
+    s_pre[2 * lane + 1] = inc - c1;
+  }
+  __syncthreads();
+  if (!(s_bits[0] & 1u)) {  // impossible: element 0 starts a source
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  const u32 nseg = s_pre[C / 32 - 1] + __popc(s_bits[C / 32 - 1]);
+  const int kb = a.key_bits;
+  const u32 tsize = nseg << kb;
+  auto seg_of = [&](u32 e) {
+    return s_pre[e >> 5] + __popc(s_bits[e >> 5] & ((2u << (e & 31)) - 1u)) - 1u;
+  };
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k)
+    if (start[k] != kNoStart) s_segsrc[seg_of(start[k])] = td.x + threadIdx.x + k * NT;
+  for (u32 i = threadIdx.x; i < tsize; i += NT) {
+    s_sum[i] = 0;
+    s_exp[i] = 0;
+  }
+  // biased exponent of a weight, denormals and zero counted as 1
+  auto bexp = [](float x) { return max((__float_as_uint(x) >> 23) & 0xffu, 1u); };
+  constexpr u32 kNone = 0xffffffffu;  // table index of an absent item
+  u32 idx[IT];
+  u32 nonfinite = 0;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = e0 + j * kWave;
+    const u32 ix = (seg_of(min(e, n - 1)) << kb) | (key[j] & ((1u << kb) - 1u));
+    idx[j] = e < n ? ix : kNone;
+    nonfinite |= (e < n && bexp(wt[j]) == 0xffu) ? 1u : 0u;
+  }
+  if (__syncthreads_or(nonfinite)) {
+    if (threadIdx.x == 0) {
+      a.tiles[tile].w = n | kRerouted;
+      list_for_sort(a, tile);
+    }
+    return;
+  }
+
+  // 2. largest exponent per entry.  A thread's items with equal entries
+  //    (64 elements apart) are combined first: one LDS atomic per run of
+  //    equal consecutive items.
+  {
+    u32 m = 0;
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const bool start = j == 0 || idx[j] != idx[j - 1];
+      const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
+      const u32 be = bexp(wt[j]);
+      m = start ? be : max(m, be);
+      if (end) atomicMax(&s_exp[idx[j]], m + 1);
+    }
+  }
+  __syncthreads();
+  // 3. fixed-point sums, combined the same way
+  {
+    long long acc = 0;
+    u32 E = 0;
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const bool start = j == 0 || idx[j] != idx[j - 1];
+      const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
+      const u32 ex = s_exp[idx[j] != kNone ? idx[j] : 0u] - 1u;
+      E = start ? ex : E;
+      const u32 bits = __float_as_uint(wt[j]);
+      const u32 mag = (bits & 0x7fffffu) | (((bits >> 23) & 0xffu) ? 0x800000u : 0u);
+      const int ms = (bits >> 31) ? -(int)mag : (int)mag;
+      const long long term = ((long long)ms * (1ll << 27)) >> min(E - bexp(wt[j]), 63u);
+      acc = (start ? 0ll : acc) + term;
+      if (end) atomicAdd(&s_sum[idx[j]], (unsigned long long)acc);
+    }
+  }
+  __syncthreads();
+
+  // 4. present entries -> runs rb + r in entry order; thread t lists entries
+  //    t*kDenseEPT .. t*kDenseEPT + kDenseEPT - 1
+  u32 pmask = 0;
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k) {
+    const u32 i = threadIdx.x * kDenseEPT + k;
+    if (i < tsize && s_exp[i] != 0) pmask |= 1u << k;
+  }
+  const u32 pc = __popc(pmask);
+  const u32 pinc = wave_inclusive_sum(pc);
+  u32 nruns;
+  u32 r = block_offset(__shfl(pinc, kWave - 1, kWave), s_tmp, &nruns) + pinc - pc;
+  const u32 kmask = (1u << kb) - 1u;
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k) {
+    if (!((pmask >> k) & 1u)) continue;
+    const u32 i = threadIdx.x * kDenseEPT + k;
+    const int E = (int)s_exp[i] - 1;
+    const double v = ldexp((double)(long long)s_sum[i], E - 177);
+    const u32 seg = i >> kb;
+    a.temp[rb + r] = make_uint4(s_segsrc[seg], i & kmask, 0u, __float_as_uint((float)v));
+    s_runseg[r] = (u16)seg;
+    ++r;
+  }
+  __syncthreads();
+  for (u32 q = threadIdx.x; q < nruns; q += NT) {
+    const u32 seg = s_runseg[q];
+    const u32 u = s_segsrc[seg];
+    if (q == 0 || s_runseg[q - 1] != seg) a.tstart[u] = rb + q;
+    if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
+  }
+  if (threadIdx.x == 0) {
+    atomicAdd((unsigned long long *)&a.st->dense_records, (unsigned long long)n);
+    atomicAdd((unsigned long long *)&a.st->dense_runs, (unsigned long long)nruns);
+  }
 }
 
 // Descriptor of merge tile t: the small sources whose first record falls in
@@ -639,6 +875,8 @@ __global__ void k_reset_level(Status *st) {
   st->R = st->M = st->merged = st->RB = 0;
   st->nwide = st->nheavy = st->nbig = st->nnew = 0;
   st->max_small = 0;
+  st->dense_records = st->dense_runs = st->sort_runs = 0;
+  st->nsort = 0;
 }
 
 }  // namespace
@@ -648,16 +886,39 @@ void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStre
                      nsrc, big, st);
 }
 
-void launch_merge_tiles(const MergeArgs &a, bool wide_keys, hipStream_t s) {
-  if (a.R == 0) return;
+static u64 merge_grid(const MergeArgs &a) {
   const u64 g = ceil_div(a.R, a.window);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
+  return g;
+}
+
+void launch_tile_sources(const MergeArgs &a, hipStream_t s) {
+  if (a.R == 0) return;
+  const u64 g = merge_grid(a);
   hipLaunchKernelGGL(k_tile_sources, dim3(grid1(g)), dim3(256), 0, s, a.roff, a.nsrc, a.R,
                      a.window, g, a.tiles);
-  if (wide_keys)
+}
+
+void launch_merge_dense(const MergeArgs &a, hipStream_t s) {
+  if (a.R == 0 || a.key_bits > kDenseKeyBits) return;
+  hipLaunchKernelGGL(k_merge_dense, dim3((unsigned)merge_grid(a)), dim3(NT), 0, s, a);
+}
+
+void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s) {
+  if (a.R == 0) return;
+  const u64 g = merge_grid(a);
+  if (a.key_bits <= kDenseKeyBits) {
+    // after k_merge_dense: only the tiles it listed, walked by a fixed grid
+    const unsigned gl = (unsigned)std::min<u64>(g, kListedGrid);
+    if (wide_keys)
+      hipLaunchKernelGGL((k_merge_listed<u64>), dim3(gl), dim3(NT), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_merge_listed<u32>), dim3(gl), dim3(NT), 0, s, a);
+  } else if (wide_keys) {
     hipLaunchKernelGGL((k_merge_tiles<u64>), dim3((unsigned)g), dim3(NT), 0, s, a);
-  else
+  } else {
     hipLaunchKernelGGL((k_merge_tiles<u32>), dim3((unsigned)g), dim3(NT), 0, s, a);
+  }
 }
 
 void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s) {

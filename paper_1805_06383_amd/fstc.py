@@ -71,7 +71,10 @@ class FstcStats(ctypes.Structure):
                 ("ms_write_kernel", ctypes.c_double), ("ms_merge_kernel", ctypes.c_double),
                 ("write_launches", _u32), ("merge_launches", _u32),
                 ("total_matches", _u64), ("total_big_records", _u64),
-                ("record_key_bytes", _u32), ("key_bits", _u32)]
+                ("record_key_bytes", _u32), ("key_bits", _u32),
+                ("ms_sort_kernel", ctypes.c_double), ("sort_launches", _u32), ("reserved1", _u32),
+                ("total_dense_records", _u64), ("total_dense_runs", _u64),
+                ("total_sort_runs", _u64)]
 
 
 EXPORTS = ("fstc_compose", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",

@@ -183,6 +183,93 @@ def test_zero_weights_are_kept(fstc):
     compare(run_gpu(fstc, m1, m2), oracle.compose(m1, m2), "zero weights", rtol=RTOL)
 
 
+def with_weights(m, w):
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, m.src, m.dst, m.ilabel,
+                 m.olabel, np.asarray(w, np.float32), m.final)
+
+
+def signed_wide(rng, n, lo=-75, hi=40):
+    """Weights of random sign with exponents uniform on [lo, hi]: products span
+    denormals to 2^80 and sums cancel."""
+    e = rng.integers(lo, hi + 1, size=n)
+    sgn = rng.choice([-1.0, 1.0], size=n)
+    return (sgn * np.ldexp(1.0 + rng.random(n), e)).astype(np.float32)
+
+
+def compare_signed(fstc, m1, m2, what, **kw):
+    """Exact structure; each merged weight within 1e-5 of the sum of the
+    magnitudes of its terms (the composition of the absolute-weight inputs,
+    which has the same arcs), plus one float32 denormal step."""
+    g = run_gpu(fstc, m1, m2, **kw)
+    ref = oracle.compose(m1, m2, **kw)
+    mag = oracle.compose(with_weights(m1, np.abs(m1.weight)), with_weights(m2, np.abs(m2.weight)),
+                         **kw)
+    G, Rf, Mg = canon_of(g), canon_of(ref), canon_of(mag)
+    assert_same(G, Rf, rtol=np.inf, what=what)
+    assert np.array_equal(Mg.keys, Rf.keys)
+    err = np.abs(G.w.astype(np.float64) - Rf.w.astype(np.float64))
+    bound = 1e-5 * Mg.w.astype(np.float64) + 2.0**-149
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {int(bad.sum())} weights off, e.g. got {G.w[bad][0]!r} "
+                           f"ref {Rf.w[bad][0]!r} magnitude {Mg.w[bad][0]!r}")
+    assert g.num_premerge == ref.num_premerge
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_signed_wide_range_weights(fstc, seed):
+    """Cancelling sums, denormal and huge products through the tile merge."""
+    from test_oracle_pins import tiny_pair
+    rng = np.random.default_rng(500 + seed)
+    if seed < 8:
+        m1, m2 = tiny_pair(seed)
+    else:
+        m1, m2 = W.config1(seed)
+    m1 = with_weights(m1, signed_wide(rng, m1.num_arcs))
+    m2 = with_weights(m2, signed_wide(rng, m2.num_arcs))
+    compare_signed(fstc, m1, m2, f"signed seed {seed}")
+
+
+@pytest.mark.parametrize("cfg,cap", [(4, 2), (2, 2)])
+def test_signed_weights_workloads(fstc, cfg, cap):
+    """Signed weights on a workload with a small per-source key space (many
+    records per merged arc) and on one with a large key space."""
+    m1, m2 = W.make_config(cfg, 0)
+    rng = np.random.default_rng(77)
+    m1 = with_weights(m1, signed_wide(rng, m1.num_arcs, -30, 30))
+    m2 = with_weights(m2, signed_wide(rng, m2.num_arcs, -30, 30))
+    compare_signed(fstc, m1, m2, f"signed config{cfg} cap {cap}", max_levels=cap)
+
+
+def test_signed_matrix_product(fstc):
+    """Signed weights through the multi-block merge (one source)."""
+    rng = np.random.default_rng(9)
+    A = signed_wide(rng, 40 * 300, -20, 20).reshape(40, 300)
+    B = signed_wide(rng, 300 * 7, -20, 20).reshape(300, 7)
+    g = run_gpu(fstc, W.one_state_dense(A), W.one_state_dense(B))
+    P = A.astype(np.float64) @ B.astype(np.float64)
+    M = np.abs(A).astype(np.float64) @ np.abs(B).astype(np.float64)
+    err = np.abs(g.w.astype(np.float64) - P[g.a, g.c])
+    assert np.all(err <= 1e-5 * M[g.a, g.c] + 2.0**-149)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_infinite_weights(fstc, seed):
+    """Infinite products make infinite sums (positive weights: no inf - inf)."""
+    from test_oracle_pins import tiny_pair
+    m1, m2 = tiny_pair(seed + 20)
+    if m1.num_arcs == 0:
+        m1, m2 = W.config1(seed)
+    w = m1.weight.copy()
+    w[::5] = np.inf
+    m1 = with_weights(m1, w)
+    g = canon_of(run_gpu(fstc, m1, m2))
+    ref = canon_of(oracle.compose(m1, m2))
+    assert_same(g, ref, rtol=np.inf, what=f"inf seed {seed}")
+    assert np.array_equal(np.isinf(g.w), np.isinf(ref.w))
+    fin = np.isfinite(ref.w)
+    np.testing.assert_allclose(g.w[fin], ref.w[fin], rtol=RTOL)
+
+
 def test_config3_full(fstc):
     m1, m2 = W.config3(0)
     g = run_gpu(fstc, m1, m2)
