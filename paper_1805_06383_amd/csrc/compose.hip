@@ -206,9 +206,10 @@ void Composer::run(fstc_result *out) {
   if (!o.alloc) tune_default_pool();
   hs = staging();
 
-  Buf stb(&A), cntb(&A);
+  Buf stb(&A), cntb(&A), tstb(&A);
   dst = (Status *)stb.ensure(sizeof(Status));
   u64 *dcounts = (u64 *)cntb.ensure(8 * sizeof(u64));
+  u64 *tstat = (u64 *)tstb.ensure(kStatWords * sizeof(u64));
   fill_u32((u32 *)dst, 0, sizeof(Status) / 4, s);
 
   // (a0) device layout of both inputs
@@ -271,7 +272,7 @@ void Composer::run(fstc_result *out) {
     stmp.ensure(scan_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
-    launch_reset_level(dst, s);
+    launch_reset_level(dst, tstat, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
                  dst, nullptr, nullptr};
@@ -360,6 +361,7 @@ void Composer::run(fstc_result *out) {
     ma.temp = temp.as<uint4>();
     ma.tiles = tiles_m.as<uint4>();
     ma.sortlist = sortlist.as<u32>();
+    ma.tstat = tstat;
     ma.ntiles = ntiles;
     ma.window = window;
     ma.tstart = tstart.as<u64>();
@@ -392,7 +394,7 @@ void Composer::run(fstc_result *out) {
     launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
     exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
     launch_emit_runs(ma, aoff.as<u64>(), s);
-    launch_merged_total(aoff.as<u64>() + nsrc, dst, s);
+    launch_merged_total(aoff.as<u64>() + nsrc, dst, tstat, s);
     T.end(kMerge);
     sync_status();
     const u32 nnew = hs->st.nnew;

@@ -92,6 +92,12 @@ __device__ __forceinline__ bool dense_tile(const uint4 &td, int key_bits) {
          ((u64)(td.y - td.x) << key_bits) <= (u64)kDenseCap;
 }
 
+// Adds v to per-level counter f in the slot of this workgroup.
+__device__ __forceinline__ void add_stat(const MergeArgs &a, StatField f, u32 v) {
+  atomicAdd((unsigned long long *)&a.tstat[(blockIdx.x % kStatSlots) * kStatStride + f],
+            (unsigned long long)v);
+}
+
 // Exclusive prefix over the waves of the block of one value per wave (taken
 // from any lane); *total receives the block total.  All threads must call it.
 __device__ __forceinline__ u32 block_offset(u32 wave_value, u32 *s_tmp, u32 *total) {
@@ -470,7 +476,7 @@ __device__ __forceinline__ void merge_sort_tile(const MergeArgs &a, u32 tile, So
     if (first) a.tstart[u] = rb + r;
     if (last) a.mend[u] = rb + r + 1;
   }
-  if (threadIdx.x == 0) atomicAdd((unsigned long long *)&a.st->sort_runs, (unsigned long long)nruns);
+  if (threadIdx.x == 0) add_stat(a, kStatSortRuns, nruns);
 }
 
 // Every tile of the level, one per workgroup.  XCD-aware tile order:
@@ -686,8 +692,8 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
     if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
   }
   if (threadIdx.x == 0) {
-    atomicAdd((unsigned long long *)&a.st->dense_records, (unsigned long long)n);
-    atomicAdd((unsigned long long *)&a.st->dense_runs, (unsigned long long)nruns);
+    add_stat(a, kStatDenseRecords, n);
+    add_stat(a, kStatDenseRuns, nruns);
   }
 }
 
@@ -869,14 +875,31 @@ __global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st) {
   st->M = *mt;
 }
 
-__global__ void k_merged_total(const u64 *at, Status *st) { st->merged = *at; }
+// one wave: level total of merged arcs and of the per-tile counter slots
+__global__ void k_merged_total(const u64 *at, Status *st, const u64 *tstat) {
+  const u32 lane = lane_id();
+  const u64 *slot = tstat + (size_t)lane * kStatStride;
+  u64 v[3] = {slot[kStatDenseRecords], slot[kStatDenseRuns], slot[kStatSortRuns]};
+#pragma unroll
+  for (int f = 0; f < 3; ++f)
+    for (int d = kWave / 2; d > 0; d >>= 1) v[f] += __shfl_xor(v[f], d, kWave);
+  if (lane == 0) {
+    st->merged = *at;
+    st->dense_records = v[0];
+    st->dense_runs = v[1];
+    st->sort_runs = v[2];
+  }
+}
 
-__global__ void k_reset_level(Status *st) {
-  st->R = st->M = st->merged = st->RB = 0;
-  st->nwide = st->nheavy = st->nbig = st->nnew = 0;
-  st->max_small = 0;
-  st->dense_records = st->dense_runs = st->sort_runs = 0;
-  st->nsort = 0;
+__global__ void k_reset_level(Status *st, u64 *tstat) {
+  for (u32 i = threadIdx.x; i < kStatWords; i += blockDim.x) tstat[i] = 0;
+  if (threadIdx.x == 0) {
+    st->R = st->M = st->merged = st->RB = 0;
+    st->nwide = st->nheavy = st->nbig = st->nnew = 0;
+    st->max_small = 0;
+    st->dense_records = st->dense_runs = st->sort_runs = 0;
+    st->nsort = 0;
+  }
 }
 
 }  // namespace
@@ -1004,12 +1027,13 @@ void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hip
   hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st);
 }
 
-void launch_merged_total(const u64 *a_total, Status *st, hipStream_t s) {
-  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1), 0, s, a_total, st);
+void launch_merged_total(const u64 *a_total, Status *st, const u64 *tstat, hipStream_t s) {
+  static_assert(kStatSlots == kWave, "one lane per counter slot");
+  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(kWave), 0, s, a_total, st, tstat);
 }
 
-void launch_reset_level(Status *st, hipStream_t s) {
-  hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(1), 0, s, st);
+void launch_reset_level(Status *st, u64 *tstat, hipStream_t s) {
+  hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(256), 0, s, st, tstat);
 }
 
 }  // namespace fstc
