@@ -296,7 +296,7 @@ void Composer::run(fstc_result *out) {
     rkey.ensure(R * rec_bytes);
     rw.ensure(R * 4);
     temp.ensure(R * sizeof(uint4));
-    tiles_e.ensure((ceil_div(R, kExpandTile) + 1) * 8);
+    tiles_e.ensure(ceil_div(R, kExpandTile) * sizeof(ExpandTile));
     // merge window: as wide as the largest small source allows (see level.hpp)
     const u64 max_small = std::max<u32>(1, hs->st.max_small);
     const u64 window = nbig ? kMergeSmall : (u64)kMergeCap - max_small + 1;
@@ -330,7 +330,7 @@ void Composer::run(fstc_result *out) {
     T.end(kExpand);
     T.begin();
     launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
-                  rkey.p, rw.as<float>(), tiles_e.as<u64>(), &dst->err, s);
+                  rkey.p, rw.as<float>(), tiles_e.as<ExpandTile>(), &dst->err, s);
     T.end(kWriteKernel);
     ++write_launches;
     total_matches += M;

@@ -254,15 +254,13 @@ __global__ __launch_bounds__(kHeavyNT) void k_emit_heavy(LevelArgs a) {
 }
 
 // 8 consecutive record keys with 16-byte stores (p is 32-byte aligned).
-__device__ __forceinline__ void store_record_row(u32 *p, const u32 (&k)[8]) {
-  uint4 *q = reinterpret_cast<uint4 *>(p);
-  q[0] = make_uint4(k[0], k[1], k[2], k[3]);
-  q[1] = make_uint4(k[4], k[5], k[6], k[7]);
+__device__ __forceinline__ void store_record_row(u32 *p, const u32 (&k)[4]) {
+  *reinterpret_cast<uint4 *>(p) = make_uint4(k[0], k[1], k[2], k[3]);
 }
-__device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[8]) {
+__device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[4]) {
   ulonglong2 *q = reinterpret_cast<ulonglong2 *>(p);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) q[i] = make_ulonglong2(k[2 * i], k[2 * i + 1]);
+  q[0] = make_ulonglong2(k[0], k[1]);
+  q[1] = make_ulonglong2(k[2], k[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -270,32 +268,29 @@ __device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[8]) {
 // the matches overlapping the window are staged in LDS; each thread finds the
 // match of its first record by binary search there, takes
 // (i, j) = divmod(offset, n2) to select the M1 and M2 arcs, and steps through
-// its 8 consecutive records.  Record = (part1 << b2 | part2, p1 * p2).
+// its 4 consecutive records.  Record = (part1 << b2 | part2, p1 * p2).
 template <class KT>
 __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const u64 *mrbase, u64 M,
                                                       u64 R, const uint2 *arcs1,
                                                       const uint2 *arcs2, int b2, KT *rec_key,
-                                                      float *rec_w, const u64 *tile_lb, u32 *err) {
+                                                      float *rec_w, const ExpandTile *tiles,
+                                                      u32 *err) {
   __shared__ u32 s_rel[kExpandTile];
   __shared__ uint4 s_m[kExpandTile];
   const u64 r0 = (u64)blockIdx.x * kExpandTile;
   const u64 rend = min(r0 + kExpandTile, R);
-  // matches overlapping [r0, rend): the last one starting at or before r0
-  // through the last one starting before rend
-  const u64 lb0 = tile_lb[blockIdx.x], lb1 = tile_lb[blockIdx.x + 1];
-  const u64 k0 = (lb0 < M && mrbase[lb0] == r0) ? lb0 : lb0 - 1;
-  const u64 nm = lb1 - k0;
-  if (lb1 == 0 || lb1 <= k0 || nm > kExpandTile) {  // impossible: each match has >= 1 record
+  const ExpandTile ti = tiles[blockIdx.x];
+  const u64 k0 = ti.k0, nm = ti.kend - ti.k0;
+  if (ti.kend <= k0 || ti.kend > M || nm > kExpandTile) {  // impossible: each match has >= 1 record
     if (threadIdx.x == 0) set_error(err, kErrBounds);
     return;
   }
-  const u64 base0 = mrbase[k0];
   for (u32 i = threadIdx.x; i < nm; i += kExpandNT) {
     s_rel[i] = i == 0 ? 0u : (u32)(mrbase[k0 + i] - r0);
     s_m[i] = match[k0 + i];
   }
   __syncthreads();
-  // thread t writes the consecutive records r0 + 8t .. r0 + 8t + 7: one
+  // thread t writes the consecutive records r0 + 4t .. r0 + 4t + 3: one
   // search and one division, then (i1, i2) advance through the match
   const u32 rel0 = threadIdx.x * kExpandIT;
   const u64 rfirst = r0 + rel0;
@@ -303,7 +298,7 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   const u32 cnt = (u32)min<u64>(kExpandIT, rend - rfirst);
   u32 mi = (u32)last_le<u32>(s_rel, nm, rel0);
   uint4 m = s_m[mi];
-  const u64 t = mi == 0 ? rfirst - base0 : (u64)(rel0 - s_rel[mi]);
+  const u64 t = mi == 0 ? rfirst - ti.base0 : (u64)(rel0 - s_rel[mi]);
   u32 i1, i2;
   if (t < (1ull << 32)) {
     const u32 tt = (u32)t;
@@ -336,9 +331,7 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   }
   if (cnt == kExpandIT) {
     store_record_row(rec_key + rfirst, key);
-    float4 *wp = reinterpret_cast<float4 *>(rec_w + rfirst);
-    wp[0] = make_float4(wt[0], wt[1], wt[2], wt[3]);
-    wp[1] = make_float4(wt[4], wt[5], wt[6], wt[7]);
+    *reinterpret_cast<float4 *>(rec_w + rfirst) = make_float4(wt[0], wt[1], wt[2], wt[3]);
   } else {
     for (u32 j = 0; j < cnt; ++j) {
       rec_key[rfirst + j] = key[j];
@@ -347,10 +340,13 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   }
 }
 
-// tile_lb[t] = first match whose first record is >= min(t * kExpandTile, R).
-__global__ void k_tile_matches(const u64 *mrbase, u64 M, u64 R, u64 ntiles, u64 *tile_lb) {
-  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t <= ntiles; t += (u64)gridDim.x * blockDim.x)
-    tile_lb[t] = lower_bound_dev<u64>(mrbase, M, min(t * kExpandTile, R));
+__global__ void k_tile_matches(const u64 *mrbase, u64 M, u64 R, u64 ntiles, ExpandTile *tiles) {
+  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t < ntiles; t += (u64)gridDim.x * blockDim.x) {
+    const u64 r0 = t * kExpandTile;
+    const u64 k0 = last_le<u64>(mrbase, M, r0);
+    tiles[t] = ExpandTile{k0, lower_bound_dev<u64>(mrbase, M, min(r0 + kExpandTile, R)),
+                          mrbase[k0], 0};
+  }
 }
 
 }  // namespace
@@ -371,18 +367,18 @@ void launch_emit(const LevelArgs &a, hipStream_t s) {
 
 void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,
                    const CsrView &c2, int b2, bool wide_keys, void *rec_key, float *rec_w,
-                   u64 *tile_lb, u32 *err, hipStream_t s) {
+                   ExpandTile *tiles, u32 *err, hipStream_t s) {
   if (R == 0) return;
   const u64 g = ceil_div(R, kExpandTile);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
-  const unsigned gs = (unsigned)std::min<u64>(ceil_div(g + 1, 256), 1u << 20);
-  hipLaunchKernelGGL(k_tile_matches, dim3(gs), dim3(256), 0, s, mrbase, M, R, g, tile_lb);
+  const unsigned gs = (unsigned)std::min<u64>(ceil_div(g, 256), 1u << 20);
+  hipLaunchKernelGGL(k_tile_matches, dim3(gs), dim3(256), 0, s, mrbase, M, R, g, tiles);
   if (wide_keys)
     hipLaunchKernelGGL((k_expand<u64>), dim3((unsigned)g), dim3(kExpandNT), 0, s, match, mrbase,
-                       M, R, c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, tile_lb, err);
+                       M, R, c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, tiles, err);
   else
     hipLaunchKernelGGL((k_expand<u32>), dim3((unsigned)g), dim3(kExpandNT), 0, s, match, mrbase,
-                       M, R, c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, tile_lb, err);
+                       M, R, c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, tiles, err);
 }
 
 }  // namespace fstc

@@ -68,10 +68,17 @@ constexpr int kMaxKeyBits = 64 - 2 * kIdxBits;  // 40: part-rank bits of both si
 constexpr u32 kDenseCap = 2048;
 constexpr int kDenseKeyBits = 11;  // log2(kDenseCap)
 
-// Arc-pair write pass: 256 threads x 8 records per workgroup.
-constexpr int kExpandNT = 256;
-constexpr int kExpandIT = 8;
+// Arc-pair write pass: 512 threads x 4 records per workgroup.
+constexpr int kExpandNT = 512;
+constexpr int kExpandIT = 4;
 constexpr u64 kExpandTile = kExpandNT * kExpandIT;
+
+// Matches overlapping write tile t (records [t kExpandTile, ...)): k0 = the
+// last match starting at or before the tile, kend = the first match starting
+// at or after its end, base0 = first record of match k0.
+struct ExpandTile {
+  u64 k0, kend, base0, pad;
+};
 
 struct LevelArgs {
   CsrView c1, c2;
@@ -91,10 +98,10 @@ void launch_count(const LevelArgs &a, hipStream_t s);
 void launch_emit(const LevelArgs &a, hipStream_t s);
 // Writes R records: key = (part1 << b2) | part2 (u32 when key_bits <= 32,
 // else u64), weight = p1 * p2.
-// tile_lb: scratch of ceil(R / kExpandTile) + 1 u64.
+// tiles: scratch of ceil(R / kExpandTile) ExpandTile.
 void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,
                    const CsrView &c2, int b2, bool wide_keys, void *rec_key, float *rec_w,
-                   u64 *tile_lb, u32 *err, hipStream_t s);
+                   ExpandTile *tiles, u32 *err, hipStream_t s);
 
 struct MergeArgs {
   const void *rec_key;
