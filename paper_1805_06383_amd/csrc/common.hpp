@@ -181,6 +181,8 @@ __device__ __forceinline__ int bits_for_dev(u32 v) { return v ? 32 - __clz(v) : 
 
 // ---------------------------------------------------------------------------
 // Launch helpers shared by the translation units.
+// Compute units of the current device (queried once per device).
+int compute_units();
 void fill_u32(u32 *p, u32 v, u64 n, hipStream_t s);
 void fill_u64(u64 *p, u64 v, u64 n, hipStream_t s);
 

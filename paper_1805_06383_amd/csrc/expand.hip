@@ -254,88 +254,105 @@ __global__ __launch_bounds__(kHeavyNT) void k_emit_heavy(LevelArgs a) {
 }
 
 // 8 consecutive record keys with 16-byte stores (p is 32-byte aligned).
-__device__ __forceinline__ void store_record_row(u32 *p, const u32 (&k)[4]) {
-  *reinterpret_cast<uint4 *>(p) = make_uint4(k[0], k[1], k[2], k[3]);
+__device__ __forceinline__ void store_record_row(u32 *p, const u32 (&k)[8]) {
+  uint4 *q = reinterpret_cast<uint4 *>(p);
+  q[0] = make_uint4(k[0], k[1], k[2], k[3]);
+  q[1] = make_uint4(k[4], k[5], k[6], k[7]);
 }
-__device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[4]) {
+__device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[8]) {
   ulonglong2 *q = reinterpret_cast<ulonglong2 *>(p);
-  q[0] = make_ulonglong2(k[0], k[1]);
-  q[1] = make_ulonglong2(k[2], k[3]);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) q[i] = make_ulonglong2(k[2 * i], k[2 * i + 1]);
 }
 
 // ---------------------------------------------------------------------------
-// Arc-pair write pass.  Workgroup b produces records [b*2048, (b+1)*2048):
-// the matches overlapping the window are staged in LDS; each thread finds the
-// match of its first record by binary search there, takes
+// Arc-pair write pass.  Workgroup b produces records [b*4096, (b+1)*4096),
+// write tiles 2b and 2b + 1: the matches overlapping them are staged in LDS
+// (both tiles at once when they fit, else one tile after the other); each
+// thread finds the match of its first record by binary search there, takes
 // (i, j) = divmod(offset, n2) to select the M1 and M2 arcs, and steps through
-// its 4 consecutive records.  Record = (part1 << b2 | part2, p1 * p2).
+// its 8 consecutive records.  Record = (part1 << b2 | part2, p1 * p2).
 template <class KT>
 __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const u64 *mrbase, u64 M,
                                                       u64 R, const uint2 *arcs1,
                                                       const uint2 *arcs2, int b2, KT *rec_key,
                                                       float *rec_w, const ExpandTile *tiles,
-                                                      u32 *err) {
+                                                      u64 ntiles, u32 *err) {
   __shared__ u32 s_rel[kExpandTile];
   __shared__ uint4 s_m[kExpandTile];
-  const u64 r0 = (u64)blockIdx.x * kExpandTile;
-  const u64 rend = min(r0 + kExpandTile, R);
-  const ExpandTile ti = tiles[blockIdx.x];
-  const u64 k0 = ti.k0, nm = ti.kend - ti.k0;
-  if (ti.kend <= k0 || ti.kend > M || nm > kExpandTile) {  // impossible: each match has >= 1 record
-    if (threadIdx.x == 0) set_error(err, kErrBounds);
-    return;
-  }
-  for (u32 i = threadIdx.x; i < nm; i += kExpandNT) {
-    s_rel[i] = i == 0 ? 0u : (u32)(mrbase[k0 + i] - r0);
-    s_m[i] = match[k0 + i];
-  }
-  __syncthreads();
-  // thread t writes the consecutive records r0 + 4t .. r0 + 4t + 3: one
-  // search and one division, then (i1, i2) advance through the match
-  const u32 rel0 = threadIdx.x * kExpandIT;
-  const u64 rfirst = r0 + rel0;
-  if (rfirst >= rend) return;
-  const u32 cnt = (u32)min<u64>(kExpandIT, rend - rfirst);
-  u32 mi = (u32)last_le<u32>(s_rel, nm, rel0);
-  uint4 m = s_m[mi];
-  const u64 t = mi == 0 ? rfirst - ti.base0 : (u64)(rel0 - s_rel[mi]);
-  u32 i1, i2;
-  if (t < (1ull << 32)) {
-    const u32 tt = (u32)t;
-    i1 = tt / m.w;
-    i2 = tt - i1 * m.w;
-  } else {
-    const u64 q = t / m.w;
-    i1 = (u32)q;
-    i2 = (u32)(t - q * m.w);
-  }
-  KT key[kExpandIT];
-  float wt[kExpandIT];
+  constexpr u32 kPer = kExpandTile / kExpandIT;  // threads per write tile
+  const u64 g0 = (u64)blockIdx.x * kExpandGroup;
+  const u64 ng = min(kExpandGroup, ntiles - g0);
+  const u64 r0 = g0 * kExpandTile;
+  const ExpandTile ta = tiles[g0], tb = tiles[g0 + ng - 1];
+  // one staging for the whole group when its matches fit, else per tile
+  const bool one = tb.kend - ta.k0 <= kExpandTile;
+  const u32 passes = one ? 1u : (u32)ng;
+  const u32 rel0 = threadIdx.x * kExpandIT;  // first record of this thread, from r0
+  for (u32 pass = 0; pass < passes; ++pass) {
+    const ExpandTile ti = one ? ExpandTile{ta.k0, tb.kend, ta.base0, 0} : (pass ? tb : ta);
+    const u64 rs = one ? r0 : r0 + pass * kExpandTile;  // record origin of s_rel
+    const u64 k0 = ti.k0, nm = ti.kend - ti.k0;
+    if (ti.kend <= k0 || ti.kend > M || nm > kExpandTile) {  // impossible: >= 1 record per match
+      if (threadIdx.x == 0) set_error(err, kErrBounds);
+      return;
+    }
+    if (pass) __syncthreads();  // previous tile's LDS fully read
+    for (u32 i = threadIdx.x; i < nm; i += kExpandNT) {
+      s_rel[i] = i == 0 ? 0u : (u32)(mrbase[k0 + i] - rs);
+      s_m[i] = match[k0 + i];
+    }
+    __syncthreads();
+    // thread t writes the consecutive records r0 + 8t .. r0 + 8t + 7: one
+    // search and one division, then (i1, i2) advance through the match
+    if (!one && threadIdx.x / kPer != pass) continue;
+    const u64 rfirst = r0 + rel0;
+    if (rfirst >= R) continue;
+    const u32 cnt = (u32)min<u64>(kExpandIT, R - rfirst);
+    const u32 rel = (u32)(rfirst - rs);
+    u32 mi = (u32)last_le<u32>(s_rel, nm, rel);
+    uint4 m = s_m[mi];
+    const u64 t = mi == 0 ? rfirst - ti.base0 : (u64)(rel - s_rel[mi]);
+    u32 i1, i2;
+    if (t < (1ull << 32)) {
+      const u32 tt = (u32)t;
+      i1 = tt / m.w;
+      i2 = tt - i1 * m.w;
+    } else {
+      const u64 q = t / m.w;
+      i1 = (u32)q;
+      i2 = (u32)(t - q * m.w);
+    }
+    KT key[kExpandIT];
+    float wt[kExpandIT];
 #pragma unroll
-  for (int j = 0; j < kExpandIT; ++j) {
-    key[j] = 0;
-    wt[j] = 0.f;
-    if ((u32)j < cnt) {
-      const uint2 A1 = arcs1[m.x + i1];
-      const uint2 A2 = arcs2[m.y + i2];
-      key[j] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
-      wt[j] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
-      if (++i2 == m.w) {
-        i2 = 0;
-        if (++i1 == m.z && (u32)j + 1 < cnt) {
-          i1 = 0;
-          m = s_m[++mi];
+    for (int j = 0; j < kExpandIT; ++j) {
+      key[j] = 0;
+      wt[j] = 0.f;
+      if ((u32)j < cnt) {
+        const uint2 A1 = arcs1[m.x + i1];
+        const uint2 A2 = arcs2[m.y + i2];
+        key[j] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
+        wt[j] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
+        if (++i2 == m.w) {
+          i2 = 0;
+          if (++i1 == m.z && (u32)j + 1 < cnt) {
+            i1 = 0;
+            m = s_m[++mi];
+          }
         }
       }
     }
-  }
-  if (cnt == kExpandIT) {
-    store_record_row(rec_key + rfirst, key);
-    *reinterpret_cast<float4 *>(rec_w + rfirst) = make_float4(wt[0], wt[1], wt[2], wt[3]);
-  } else {
-    for (u32 j = 0; j < cnt; ++j) {
-      rec_key[rfirst + j] = key[j];
-      rec_w[rfirst + j] = wt[j];
+    if (cnt == kExpandIT) {
+      store_record_row(rec_key + rfirst, key);
+      float4 *wp = reinterpret_cast<float4 *>(rec_w + rfirst);
+      wp[0] = make_float4(wt[0], wt[1], wt[2], wt[3]);
+      wp[1] = make_float4(wt[4], wt[5], wt[6], wt[7]);
+    } else {
+      for (u32 j = 0; j < cnt; ++j) {
+        rec_key[rfirst + j] = key[j];
+        rec_w[rfirst + j] = wt[j];
+      }
     }
   }
 }
@@ -373,12 +390,13 @@ void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const Cs
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
   const unsigned gs = (unsigned)std::min<u64>(ceil_div(g, 256), 1u << 20);
   hipLaunchKernelGGL(k_tile_matches, dim3(gs), dim3(256), 0, s, mrbase, M, R, g, tiles);
+  const unsigned gw = (unsigned)ceil_div(g, kExpandGroup);
   if (wide_keys)
-    hipLaunchKernelGGL((k_expand<u64>), dim3((unsigned)g), dim3(kExpandNT), 0, s, match, mrbase,
-                       M, R, c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, tiles, err);
+    hipLaunchKernelGGL((k_expand<u64>), dim3(gw), dim3(kExpandNT), 0, s, match, mrbase, M, R,
+                       c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, tiles, g, err);
   else
-    hipLaunchKernelGGL((k_expand<u32>), dim3((unsigned)g), dim3(kExpandNT), 0, s, match, mrbase,
-                       M, R, c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, tiles, err);
+    hipLaunchKernelGGL((k_expand<u32>), dim3(gw), dim3(kExpandNT), 0, s, match, mrbase, M, R,
+                       c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, tiles, g, err);
 }
 
 }  // namespace fstc

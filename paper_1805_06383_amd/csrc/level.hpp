@@ -68,10 +68,13 @@ constexpr int kMaxKeyBits = 64 - 2 * kIdxBits;  // 40: part-rank bits of both si
 constexpr u32 kDenseCap = 2048;
 constexpr int kDenseKeyBits = 11;  // log2(kDenseCap)
 
-// Arc-pair write pass: 512 threads x 4 records per workgroup.
+// Arc-pair write pass: 512 threads x 8 records per workgroup, which covers
+// kExpandGroup write tiles of kExpandTile records (the LDS staging capacity
+// for match descriptors).
 constexpr int kExpandNT = 512;
-constexpr int kExpandIT = 4;
-constexpr u64 kExpandTile = kExpandNT * kExpandIT;
+constexpr int kExpandIT = 8;
+constexpr u64 kExpandTile = 2048;
+constexpr u64 kExpandGroup = kExpandNT * kExpandIT / kExpandTile;
 
 // Matches overlapping write tile t (records [t kExpandTile, ...)): k0 = the
 // last match starting at or before the tile, kend = the first match starting

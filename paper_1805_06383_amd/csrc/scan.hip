@@ -6,6 +6,8 @@
 // "Updating frontier and visited set").  Reduce-then-scan: one pass reduces
 // tiles of 4096 elements, the tile sums are scanned recursively, and a second
 // pass scans each tile with its offset.  A single tile is one launch.
+#include <atomic>
+
 #include "common.hpp"
 
 namespace fstc {
@@ -104,6 +106,20 @@ void scan_impl(const TI *in, TO *out, u64 n, TO *temp, hipStream_t s) {
 }
 
 }  // namespace
+
+int compute_units() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  FSTC_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) dev = 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    FSTC_HIP(hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev));
+    n = std::max(n, 1);
+    cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 void fill_u32(u32 *p, u32 v, u64 n, hipStream_t s) {
   if (!n) return;
