@@ -254,24 +254,42 @@ __global__ __launch_bounds__(kHeavyNT) void k_emit_heavy(LevelArgs a) {
 }
 
 // 8 consecutive record keys with 16-byte stores (p is 32-byte aligned).
-__device__ __forceinline__ void store_record_row(u32 *p, const u32 (&k)[8]) {
-  uint4 *q = reinterpret_cast<uint4 *>(p);
-  q[0] = make_uint4(k[0], k[1], k[2], k[3]);
-  q[1] = make_uint4(k[4], k[5], k[6], k[7]);
+// A lane writes kRun consecutive records per run; the lanes of a wave write
+// consecutive runs, so every vector store of a wave covers one contiguous
+// span (64 * 16 bytes for u32 keys and for weights).
+constexpr int kRun = 4;
+constexpr int kRuns = kExpandIT / kRun;  // runs per thread
+static_assert(kExpandIT % kRun == 0, "whole runs per thread");
+
+// Records are written once and read once by the merge, long after they
+// have left the caches at the sizes that matter: streaming stores.
+typedef u32 u32x4 __attribute__((ext_vector_type(4)));
+typedef u64 u64x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void store_run(u32 *p, const u32 (&k)[kRun]) {
+  const u32x4 v = {k[0], k[1], k[2], k[3]};
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p));
 }
-__device__ __forceinline__ void store_record_row(u64 *p, const u64 (&k)[8]) {
-  ulonglong2 *q = reinterpret_cast<ulonglong2 *>(p);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) q[i] = make_ulonglong2(k[2 * i], k[2 * i + 1]);
+__device__ __forceinline__ void store_run(u64 *p, const u64 (&k)[kRun]) {
+  const u64x2 v0 = {k[0], k[1]}, v1 = {k[2], k[3]};
+  __builtin_nontemporal_store(v0, reinterpret_cast<u64x2 *>(p));
+  __builtin_nontemporal_store(v1, reinterpret_cast<u64x2 *>(p) + 1);
+}
+__device__ __forceinline__ void store_run(float *p, const float (&w)[kRun]) {
+  const f32x4 v = {w[0], w[1], w[2], w[3]};
+  __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(p));
 }
 
 // ---------------------------------------------------------------------------
-// Arc-pair write pass.  Workgroup b produces records [b*4096, (b+1)*4096),
-// write tiles 2b and 2b + 1: the matches overlapping them are staged in LDS
-// (both tiles at once when they fit, else one tile after the other); each
-// thread finds the match of its first record by binary search there, takes
-// (i, j) = divmod(offset, n2) to select the M1 and M2 arcs, and steps through
-// its 8 consecutive records.  Record = (part1 << b2 | part2, p1 * p2).
+// Arc-pair write pass.  Workgroup b produces the records of write tiles
+// kExpandGroup*b .. kExpandGroup*(b+1) - 1: the matches overlapping them are
+// staged in LDS (all tiles at once when they fit, else one tile after the
+// other).  Wave w writes the wave span [w*64*kExpandIT, (w+1)*64*kExpandIT)
+// of the group as kRuns passes of 64 lanes x kRun consecutive records; for
+// each run a lane finds the match of its first record by binary search in
+// LDS, takes (i, j) = divmod(offset, n2) to select the M1 and M2 arcs, and
+// steps through the run.  Record = (part1 << b2 | part2, p1 * p2).
 template <class KT>
 __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const u64 *mrbase, u64 M,
                                                       u64 R, const uint2 *arcs1,
@@ -280,7 +298,9 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
                                                       u64 ntiles, u32 *err) {
   __shared__ u32 s_rel[kExpandTile];
   __shared__ uint4 s_m[kExpandTile];
-  constexpr u32 kPer = kExpandTile / kExpandIT;  // threads per write tile
+  constexpr u32 kSpan = kWave * kExpandIT;                      // records per wave
+  constexpr u32 kWavesPerTile = (u32)(kExpandTile / kSpan);
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u64 g0 = (u64)blockIdx.x * kExpandGroup;
   const u64 ng = min(kExpandGroup, ntiles - g0);
   const u64 r0 = g0 * kExpandTile;
@@ -288,9 +308,8 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   // one staging for the whole group when its matches fit, else per tile
   const bool one = tb.kend - ta.k0 <= kExpandTile;
   const u32 passes = one ? 1u : (u32)ng;
-  const u32 rel0 = threadIdx.x * kExpandIT;  // first record of this thread, from r0
   for (u32 pass = 0; pass < passes; ++pass) {
-    const ExpandTile ti = one ? ExpandTile{ta.k0, tb.kend, ta.base0, 0} : (pass ? tb : ta);
+    const ExpandTile ti = one ? ExpandTile{ta.k0, tb.kend, ta.base0, 0} : tiles[g0 + pass];
     const u64 rs = one ? r0 : r0 + pass * kExpandTile;  // record origin of s_rel
     const u64 k0 = ti.k0, nm = ti.kend - ti.k0;
     if (ti.kend <= k0 || ti.kend > M || nm > kExpandTile) {  // impossible: >= 1 record per match
@@ -303,55 +322,54 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
       s_m[i] = match[k0 + i];
     }
     __syncthreads();
-    // thread t writes the consecutive records r0 + 8t .. r0 + 8t + 7: one
-    // search and one division, then (i1, i2) advance through the match
-    if (!one && threadIdx.x / kPer != pass) continue;
-    const u64 rfirst = r0 + rel0;
-    if (rfirst >= R) continue;
-    const u32 cnt = (u32)min<u64>(kExpandIT, R - rfirst);
-    const u32 rel = (u32)(rfirst - rs);
-    u32 mi = (u32)last_le<u32>(s_rel, nm, rel);
-    uint4 m = s_m[mi];
-    const u64 t = mi == 0 ? rfirst - ti.base0 : (u64)(rel - s_rel[mi]);
-    u32 i1, i2;
-    if (t < (1ull << 32)) {
-      const u32 tt = (u32)t;
-      i1 = tt / m.w;
-      i2 = tt - i1 * m.w;
-    } else {
-      const u64 q = t / m.w;
-      i1 = (u32)q;
-      i2 = (u32)(t - q * m.w);
-    }
-    KT key[kExpandIT];
-    float wt[kExpandIT];
+    if (!one && w / kWavesPerTile != pass) continue;
 #pragma unroll
-    for (int j = 0; j < kExpandIT; ++j) {
-      key[j] = 0;
-      wt[j] = 0.f;
-      if ((u32)j < cnt) {
-        const uint2 A1 = arcs1[m.x + i1];
-        const uint2 A2 = arcs2[m.y + i2];
-        key[j] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
-        wt[j] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
-        if (++i2 == m.w) {
-          i2 = 0;
-          if (++i1 == m.z && (u32)j + 1 < cnt) {
-            i1 = 0;
-            m = s_m[++mi];
+    for (int h = 0; h < kRuns; ++h) {
+      const u64 rfirst = r0 + w * kSpan + h * (kWave * kRun) + lane * kRun;
+      if (rfirst >= R) break;
+      const u32 cnt = (u32)min<u64>(kRun, R - rfirst);
+      const u32 rel = (u32)(rfirst - rs);
+      u32 mi = (u32)last_le<u32>(s_rel, nm, rel);
+      uint4 m = s_m[mi];
+      const u64 t = mi == 0 ? rfirst - ti.base0 : (u64)(rel - s_rel[mi]);
+      u32 i1, i2;
+      if (t < (1ull << 32)) {
+        const u32 tt = (u32)t;
+        i1 = tt / m.w;
+        i2 = tt - i1 * m.w;
+      } else {
+        const u64 q = t / m.w;
+        i1 = (u32)q;
+        i2 = (u32)(t - q * m.w);
+      }
+      KT key[kRun];
+      float wt[kRun];
+#pragma unroll
+      for (int j = 0; j < kRun; ++j) {
+        key[j] = 0;
+        wt[j] = 0.f;
+        if ((u32)j < cnt) {
+          const uint2 A1 = arcs1[m.x + i1];
+          const uint2 A2 = arcs2[m.y + i2];
+          key[j] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
+          wt[j] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
+          if (++i2 == m.w) {
+            i2 = 0;
+            if (++i1 == m.z && (u32)j + 1 < cnt) {
+              i1 = 0;
+              m = s_m[++mi];
+            }
           }
         }
       }
-    }
-    if (cnt == kExpandIT) {
-      store_record_row(rec_key + rfirst, key);
-      float4 *wp = reinterpret_cast<float4 *>(rec_w + rfirst);
-      wp[0] = make_float4(wt[0], wt[1], wt[2], wt[3]);
-      wp[1] = make_float4(wt[4], wt[5], wt[6], wt[7]);
-    } else {
-      for (u32 j = 0; j < cnt; ++j) {
-        rec_key[rfirst + j] = key[j];
-        rec_w[rfirst + j] = wt[j];
+      if (cnt == kRun) {
+        store_run(rec_key + rfirst, key);
+        store_run(rec_w + rfirst, wt);
+      } else {
+        for (u32 j = 0; j < cnt; ++j) {
+          rec_key[rfirst + j] = key[j];
+          rec_w[rfirst + j] = wt[j];
+        }
       }
     }
   }

@@ -570,8 +570,8 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
     const u32 e = min(e0 + j * kWave, n - 1);
-    key[j] = rk[e];
-    wt[j] = rw[e];
+    key[j] = __builtin_nontemporal_load(rk + e);  // read once: streaming loads
+    wt[j] = __builtin_nontemporal_load(rw + e);
   }
   __syncthreads();  // s_bits cleared
 #pragma unroll
