@@ -29,6 +29,10 @@ enum : u32 {
 };
 
 constexpr u64 kEmptyKey = ~0ull;
+// Set in a merged arc's visited-table slot when its insert claimed the slot
+// (visited-table capacity is at most 2^31 slots).
+constexpr u32 kNewFlag = 0x80000000u;
+constexpr u64 kMaxHashCap = 1ull << 31;
 
 // ---------------------------------------------------------------------------
 // Host-side error plumbing (exceptions stay inside the library).

@@ -240,7 +240,8 @@ void Composer::run(fstc_result *out) {
   Buf sq1b(&A), sq2b(&A), hkb(&A), hvb(&A);
   sq1b.ensure(1024 * 4);
   sq2b.ensure(1024 * 4);
-  u64 hcap = next_pow2(std::max<u64>(4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1)));
+  u64 hcap = std::min<u64>(kMaxHashCap, next_pow2(std::max<u64>(
+                                           4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1))));
   hkb.ensure(hcap * 8);
   hvb.ensure(hcap * 4);
   fill_u64(hkb.as<u64>(), kEmptyKey, hcap, s);
@@ -257,7 +258,7 @@ void Composer::run(fstc_result *out) {
   Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
       bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
       stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A), tiles_e(&A), tiles_m(&A), tstart(&A),
-      mend(&A), sortlist(&A);
+      mend(&A), sortlist(&A), tile_runs(&A), wcnt(&A), woff(&A), wtmp(&A);
 
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
@@ -303,12 +304,14 @@ void Composer::run(fstc_result *out) {
     const u64 ntiles = ceil_div(R, window);
     tiles_m.ensure(ntiles * sizeof(uint4));
     sortlist.ensure(ntiles * 4);
+    tile_runs.ensure(ntiles * 4);
     const u64 newcap = std::min<u64>(R, pairspace - n_states);
     newlist.ensure(std::max<u64>(newcap, 1) * 4);
 
     // visited table: keep the load factor at most 1/2 for every pair this
     // level could add
-    const u64 need = 2 * (n_states + newcap);
+    // (at most kMaxHashCap slots: an insert into a full table reports it)
+    const u64 need = std::min<u64>(2 * (n_states + newcap), kMaxHashCap);
     if (need > hcap) {
       const u64 ncap = next_pow2(need);
       Buf nk(&A), nv(&A);
@@ -339,6 +342,7 @@ void Composer::run(fstc_result *out) {
     T.begin();
     fill_u64(tstart.as<u64>(), 0, nsrc, s);
     fill_u64(mend.as<u64>(), 0, nsrc, s);
+    fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
     MergeArgs ma{};
     ma.rec_key = rkey.p;
     ma.rec_w = rw.as<float>();
@@ -361,6 +365,7 @@ void Composer::run(fstc_result *out) {
     ma.temp = temp.as<uint4>();
     ma.tiles = tiles_m.as<uint4>();
     ma.sortlist = sortlist.as<u32>();
+    ma.tile_runs = tile_runs.as<u32>();
     ma.tstat = tstat;
     ma.ntiles = ntiles;
     ma.window = window;
@@ -381,19 +386,28 @@ void Composer::run(fstc_result *out) {
     T.end(kSortKernel);
     ++sort_launches;
     T.begin();
+    u64 RB = 0;
     if (nbig) {
       bigcnt.ensure((u64)nbig * 8);
       bigoff.ensure(((u64)nbig + 1) * 8);
       launch_big_counts(roff.as<u64>(), big.as<u32>(), nbig, bigcnt.as<u64>(), s);
       exclusive_scan(bigcnt.as<u64>(), bigoff.as<u64>(), nbig, stmp.p, s);
       read_words(bigoff.as<u64>() + nbig, 1);
-      const u64 RB = hs->words[0];
+      RB = hs->words[0];
       big_records += RB;
       merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, A, s);
     }
     launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
     exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
-    launch_emit_runs(ma, aoff.as<u64>(), s);
+    launch_emit_tiles(ma, s);
+    {
+      const u64 nw = newlist_waves(ma, RB);
+      wcnt.ensure(nw * 4);
+      woff.ensure((nw + 1) * 8);
+      wtmp.ensure(scan_temp_bytes(nw));
+      launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
+                     woff.as<u64>(), wtmp.p, s);
+    }
     launch_merged_total(aoff.as<u64>() + nsrc, dst, tstat, s);
     T.end(kMerge);
     sync_status();

@@ -128,6 +128,7 @@ struct MergeArgs {
   u64 *tstat;      // [kStatWords] per-tile counter slots
   uint4 *tiles;    // [ntiles = ceil(R / W)] scratch: tile descriptors
   u32 *sortlist;   // [ntiles] scratch: tiles left to the sort kernel
+  u32 *tile_runs;  // [ntiles] merged runs each tile wrote (zero-filled before the merge)
   u64 ntiles;
   Status *st;
   // multi-block path
@@ -161,9 +162,15 @@ void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff
                     u32 lo, u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
                     float *ow, u32 *err, hipStream_t s);
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s);
-// Visited-table inserts and label lookups for every merged arc of the level
-// (aoff: exclusive scan of the merged counts, aoff[nsrc] = total).
-void launch_emit_runs(const MergeArgs &a, const u64 *aoff, hipStream_t s);
+// Visited-table inserts and label lookups for every merged arc of the
+// tile-merged sources (merge_big does its own).
+void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
+// New-state list of the level from the claimed-slot flags (st->nnew = its
+// length).  wcnt: newlist_waves(a, RB) u32; woff: that + 1 u64; scan_tmp:
+// scan_temp_bytes(newlist_waves(a, RB)) bytes.
+u64 newlist_waves(const MergeArgs &a, u64 RB);
+void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
+                    void *scan_tmp, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
 void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);

@@ -195,9 +195,10 @@ __device__ __forceinline__ void hash_insert_batch(u64 *keys, u64 mask, const u64
 }
 
 // Merged arcs of B runs: part ranks back to (r1, a) and (r2, c), the target
-// pair inserted in the visited table, (slot, a, c, weight) written to
-// temp[tpos], and new pairs appended to the new-state list.  Every lane of the
-// wave must call it.
+// pair inserted in the visited table, and (slot, a, c, weight) written to
+// temp[tpos], with kNewFlag set in the slot when this insert claimed it (the
+// new-state list is built from these flags by k_newlist, without a shared
+// counter).
 template <int B>
 __device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)[B],
                                            const u32 (&u)[B], const u64 (&key)[B],
@@ -226,10 +227,10 @@ __device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)
   bool is_new[B];
   hash_insert_batch<B>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
 #pragma unroll
-  for (int i = 0; i < B; ++i) {
-    if (act[i]) a.temp[tpos[i]] = make_uint4(slot[i], P1[i].y, P2[i].y, __float_as_uint(w[i]));
-    wave_append(is_new[i], slot[i], a.newlist, &a.st->nnew, a.newcap, &a.st->err, kErrNewList);
-  }
+  for (int i = 0; i < B; ++i)
+    if (act[i])
+      a.temp[tpos[i]] = make_uint4(slot[i] | (is_new[i] ? kNewFlag : 0u), P1[i].y, P2[i].y,
+                                   __float_as_uint(w[i]));
 }
 
 // LDS of the sorting tile merge.
@@ -476,7 +477,10 @@ __device__ __forceinline__ void merge_sort_tile(const MergeArgs &a, u32 tile, So
     if (first) a.tstart[u] = rb + r;
     if (last) a.mend[u] = rb + r + 1;
   }
-  if (threadIdx.x == 0) add_stat(a, kStatSortRuns, nruns);
+  if (threadIdx.x == 0) {
+    a.tile_runs[tile] = nruns;
+    add_stat(a, kStatSortRuns, nruns);
+  }
 }
 
 // Every tile of the level, one per workgroup.  XCD-aware tile order:
@@ -692,6 +696,7 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
     if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
   }
   if (threadIdx.x == 0) {
+    a.tile_runs[tile] = nruns;
     add_stat(a, kStatDenseRecords, n);
     add_stat(a, kStatDenseRuns, nruns);
   }
@@ -745,47 +750,57 @@ __global__ void k_run_heads(const u64 *keys, u64 n, u32 *flags) {
   if (g < n) flags[g] = (g == 0 || keys[g] != keys[g - 1]) ? 1u : 0u;
 }
 
+// One thread per run head of the sorted multi-block records: sums the run
+// and emits the merged arc (visited-table insert included, see emit_batch).
 __global__ void k_big_reduce(MergeArgs a, const u64 *bigoff, u64 RB, const u64 *skey,
                              const u32 *sval, const u32 *flags, const u32 *ridx) {
   const u64 g = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= RB || !flags[g]) return;
-  const u64 mk = skey[g];
-  const u32 i = (u32)(mk >> a.key_bits);
-  double acc = 0.0;
-  u64 q = g;
-  while (q < RB && skey[q] == mk) {
-    acc += (double)__uint_as_float(sval[q]);
-    ++q;
+  bool act[1] = {g < RB && flags[g] != 0};
+  u32 uu[1] = {0};
+  u64 key[1] = {0}, tpos[1] = {0};
+  float wt[1] = {0.f};
+  if (act[0]) {
+    const u64 mk = skey[g];
+    const u32 i = (u32)(mk >> a.key_bits);
+    double acc = 0.0;
+    u64 q = g;
+    while (q < RB && skey[q] == mk) {
+      acc += (double)__uint_as_float(sval[q]);
+      ++q;
+    }
+    const u32 u = a.big[i];
+    const u64 local = ridx[g] - ridx[bigoff[i]];
+    const u64 base = a.roff[u];
+    if (g == bigoff[i]) a.tstart[u] = base;
+    if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mend[u] = base + local + 1;
+    uu[0] = u;
+    key[0] = mk & ((1ull << a.key_bits) - 1);
+    tpos[0] = base + local;
+    wt[0] = (float)acc;
   }
-  const u32 u = a.big[i];
-  const u64 local = ridx[g] - ridx[bigoff[i]];
-  const u64 base = a.roff[u];
-  if (g == bigoff[i]) a.tstart[u] = base;
-  if (q == RB || (u32)(skey[q] >> a.key_bits) != i) a.mend[u] = base + local + 1;
-  const u64 key = mk & ((1ull << a.key_bits) - 1);
-  a.temp[base + local] = make_uint4(u, (u32)key, (u32)(key >> 32), __float_as_uint((float)acc));
+  emit_batch<1>(a, act, uu, key, tpos, wt);
 }
 
-// Merged arcs of the level, one per thread (grid-stride, wave-uniform trip
-// count): the run record (source, part-rank key, weight) at its temp slot
-// becomes (slot, a, c, weight) -- part ranks mapped back to (r1, a) and
-// (r2, c), the target pair inserted in the visited table, new pairs listed.
-// Separate from the merge so that these dependent lookups run at full
-// occupancy.
-__global__ __launch_bounds__(256) void k_emit_runs(MergeArgs a, const u64 *aoff) {
-  const u64 M = aoff[a.nsrc];
-  const u64 lane = lane_id();
-  const u64 wave0 = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
-  const u64 nwaves = (u64)gridDim.x * blockDim.x / kWave;
-  for (u64 base = wave0 * kWave; base < M; base += nwaves * kWave) {
-    const u64 k = base + lane;
-    bool act[1] = {k < M};
+// Merged arcs of the tile-merged sources, one wave per merge tile (the tile
+// kernels left tile_runs[t] runs at temp[t W + off, ...)): each run record
+// (source, part-rank key, weight) becomes (slot, a, c, weight) -- part ranks
+// mapped back to (r1, a) and (r2, c), the target pair inserted in the
+// visited table, new pairs listed.  Separate from the merge so that these
+// dependent lookups run at full occupancy.
+__global__ __launch_bounds__(256) void k_emit_tiles(MergeArgs a) {
+  const u32 lane = lane_id();
+  const u64 tile = (u64)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (tile >= a.ntiles) return;
+  const u32 nr = a.tile_runs[tile];
+  if (nr == 0) return;
+  const u64 rb = tile * a.window + a.tiles[tile].z;
+  for (u32 r0 = 0; r0 < nr; r0 += kWave) {
+    bool act[1] = {r0 + lane < nr};
     u32 uu[1] = {0};
     u64 key[1] = {0}, tpos[1] = {0};
     float wt[1] = {0.f};
     if (act[0]) {
-      const u32 u = (u32)last_le<u64>(aoff, a.nsrc, k);
-      const u64 t = a.tstart[u] + (k - aoff[u]);
+      const u64 t = rb + r0 + lane;
       const uint4 rec = a.temp[t];
       uu[0] = rec.x;
       key[0] = (u64)rec.y | ((u64)rec.z << 32);
@@ -795,6 +810,58 @@ __global__ __launch_bounds__(256) void k_emit_runs(MergeArgs a, const u64 *aoff)
     emit_batch<1>(a, act, uu, key, tpos, wt);
   }
 }
+
+// New-state list without a shared counter: wave w either walks the runs of
+// merge tile w (w < ntiles) or 64 positions of the multi-block record space
+// (runs of multi-block source i sit at temp[roff[big[i]] + p - bigoff[i]]
+// while below mend).  Pass 0 counts the flagged (claimed) slots per wave into
+// wcnt; pass 1 writes them to newlist at woff[w] (exclusive scan of wcnt) in
+// wave order.
+template <int PASS>
+__global__ __launch_bounds__(256) void k_newlist(MergeArgs a, const u64 *bigoff, u32 nbig, u64 RB,
+                                                 u64 nbigw, u32 *wcnt, const u64 *woff) {
+  const u32 lane = lane_id();
+  const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  if (wv >= a.ntiles + nbigw) return;
+  const u64 base = PASS ? woff[wv] : 0;
+  u32 cnt = 0;
+  auto take = [&](bool f, u32 slot) {
+    const u64 m = __ballot(f);
+    if (PASS && f) {
+      const u64 pos = base + cnt + count_below(m);
+      if (pos < a.newcap) a.newlist[pos] = slot;
+      else set_error(&a.st->err, kErrNewList);
+    }
+    cnt += (u32)__popcll(m);
+  };
+  if (wv < a.ntiles) {
+    const u32 nr = a.tile_runs[wv];
+    if (nr == 0) {
+      if (!PASS && lane == 0) wcnt[wv] = 0;
+      return;
+    }
+    const u64 rb = wv * a.window + a.tiles[wv].z;
+    for (u32 r0 = 0; r0 < nr; r0 += kWave) {
+      u32 x = 0;
+      if (r0 + lane < nr) x = a.temp[rb + r0 + lane].x;
+      take((x & kNewFlag) != 0, x & ~kNewFlag);
+    }
+  } else {
+    const u64 p = (wv - a.ntiles) * kWave + lane;
+    u32 x = 0;
+    if (p < RB) {
+      const u32 i = (u32)last_le<u64>(bigoff, nbig, p);
+      const u32 u = a.big[i];
+      const u64 t = a.roff[u] + (p - bigoff[i]);
+      if (t < a.mend[u]) x = a.temp[t].x;
+    }
+    take((x & kNewFlag) != 0, x & ~kNewFlag);
+  }
+  if (!PASS && lane == 0) wcnt[wv] = cnt;
+}
+
+// Level total of new states (end of the exclusive scan of the per-wave counts).
+__global__ void k_new_total(const u64 *total, Status *st) { st->nnew = (u32)min<u64>(*total, 0xffffffffull); }
 
 // Merged arcs per source from where its runs start and end in temp.
 __global__ void k_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount) {
@@ -857,7 +924,7 @@ __global__ void k_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64
     }
     const uint4 rec = temp[t];
     osrc[k] = lo + u;
-    odst[k] = hvals[rec.x];
+    odst[k] = hvals[rec.x & ~kNewFlag];
     oil[k] = rec.y;
     ool[k] = rec.z;
     ow[k] = __uint_as_float(rec.w);
@@ -1008,8 +1075,25 @@ void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff
                      M, hvals, osrc, odst, oil, ool, ow, err);
 }
 
-void launch_emit_runs(const MergeArgs &a, const u64 *aoff, hipStream_t s) {
-  hipLaunchKernelGGL(k_emit_runs, dim3(2048), dim3(256), 0, s, a, aoff);
+u64 newlist_waves(const MergeArgs &a, u64 RB) { return a.ntiles + ceil_div(RB, kWave); }
+
+void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
+                    void *scan_tmp, hipStream_t s) {
+  const u64 nbigw = ceil_div(RB, kWave);
+  const u64 nw = a.ntiles + nbigw;
+  const unsigned g = (unsigned)ceil_div(nw, 256 / kWave);
+  hipLaunchKernelGGL(k_newlist<0>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
+                     (const u64 *)nullptr);
+  exclusive_scan(wcnt, woff, nw, scan_tmp, s);
+  hipLaunchKernelGGL(k_newlist<1>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
+                     (const u64 *)woff);
+  hipLaunchKernelGGL(k_new_total, dim3(1), dim3(1), 0, s, (const u64 *)(woff + nw), a.st);
+}
+
+void launch_emit_tiles(const MergeArgs &a, hipStream_t s) {
+  if (a.R == 0) return;
+  hipLaunchKernelGGL(k_emit_tiles, dim3((unsigned)ceil_div(a.ntiles, 256 / kWave)), dim3(256), 0, s,
+                     a);
 }
 
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s) {
