@@ -84,6 +84,7 @@ __device__ __forceinline__ u32 blocked_slot(u32 p) {
 // the descriptor (kRerouted) a tile it leaves to the sort kernel.
 constexpr u32 kRerouted = 0x80000000u;
 constexpr u64 kListedGrid = 2048;  // workgroups walking the list of tiles left to sort
+constexpr int kEmitBatch = 4;      // runs per lane in flight when a tile has many
 constexpr u32 kDenseEPT = kDenseCap / NT;  // table entries per thread when listing runs
 static_assert(kDenseCap % NT == 0 && (1u << kDenseKeyBits) == kDenseCap, "dense table shape");
 
@@ -781,33 +782,57 @@ __global__ void k_big_reduce(MergeArgs a, const u64 *bigoff, u64 RB, const u64 *
   emit_batch<1>(a, act, uu, key, tpos, wt);
 }
 
-// Merged arcs of the tile-merged sources, one wave per merge tile (the tile
+// Wave k of the wpt waves sharing a tile: the tile's runs at temp[rb ...] in
+// chunks of 64 B (chunks k, k + wpt, ...), B per lane at a time (lane l takes
+// runs r0 + l + 64 i, i < B).  Wave-uniform trip count.
+template <int B>
+__device__ __forceinline__ void emit_tile_runs(const MergeArgs &a, u64 rb, u32 nr, u32 lane, u32 k,
+                                               u32 wpt) {
+  for (u32 r0 = k * B * kWave; r0 < nr; r0 += wpt * B * kWave) {
+    bool act[B];
+    u32 uu[B];
+    u64 key[B], tpos[B];
+    float wt[B];
+#pragma unroll
+    for (int i = 0; i < B; ++i) {
+      const u32 r = r0 + i * kWave + lane;
+      act[i] = r < nr;
+      uu[i] = 0;
+      key[i] = 0;
+      tpos[i] = 0;
+      wt[i] = 0.f;
+      if (act[i]) {
+        const u64 t = rb + r;
+        const uint4 rec = a.temp[t];
+        uu[i] = rec.x;
+        key[i] = (u64)rec.y | ((u64)rec.z << 32);
+        tpos[i] = t;
+        wt[i] = __uint_as_float(rec.w);
+      }
+    }
+    emit_batch<B>(a, act, uu, key, tpos, wt);
+  }
+}
+
+// Merged arcs of the tile-merged sources, wpt waves per merge tile (the tile
 // kernels left tile_runs[t] runs at temp[t W + off, ...)): each run record
 // (source, part-rank key, weight) becomes (slot, a, c, weight) -- part ranks
 // mapped back to (r1, a) and (r2, c), the target pair inserted in the
-// visited table, new pairs listed.  Separate from the merge so that these
-// dependent lookups run at full occupancy.
-__global__ __launch_bounds__(256) void k_emit_tiles(MergeArgs a) {
+// visited table, kNewFlag set on claimed slots.  Separate from the merge so
+// that these dependent lookups run at full occupancy.
+__global__ __launch_bounds__(256) void k_emit_tiles(MergeArgs a, u32 wpt) {
   const u32 lane = lane_id();
-  const u64 tile = (u64)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  const u64 gw = (u64)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  const u64 tile = gw / wpt;
+  const u32 k = (u32)(gw % wpt);
   if (tile >= a.ntiles) return;
   const u32 nr = a.tile_runs[tile];
-  if (nr == 0) return;
+  if (k * kWave >= nr) return;
   const u64 rb = tile * a.window + a.tiles[tile].z;
-  for (u32 r0 = 0; r0 < nr; r0 += kWave) {
-    bool act[1] = {r0 + lane < nr};
-    u32 uu[1] = {0};
-    u64 key[1] = {0}, tpos[1] = {0};
-    float wt[1] = {0.f};
-    if (act[0]) {
-      const u64 t = rb + r0 + lane;
-      const uint4 rec = a.temp[t];
-      uu[0] = rec.x;
-      key[0] = (u64)rec.y | ((u64)rec.z << 32);
-      tpos[0] = t;
-      wt[0] = __uint_as_float(rec.w);
-    }
-    emit_batch<1>(a, act, uu, key, tpos, wt);
+  if (nr <= wpt * kWave) {
+    emit_tile_runs<1>(a, rb, nr, lane, k, wpt);
+  } else {
+    emit_tile_runs<kEmitBatch>(a, rb, nr, lane, k, wpt);  // several lookups in flight per lane
   }
 }
 
@@ -1092,8 +1117,12 @@ void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32
 
 void launch_emit_tiles(const MergeArgs &a, hipStream_t s) {
   if (a.R == 0) return;
-  hipLaunchKernelGGL(k_emit_tiles, dim3((unsigned)ceil_div(a.ntiles, 256 / kWave)), dim3(256), 0, s,
-                     a);
+  // waves per tile: enough waves in all to fill the chip even when a level
+  // has few tiles (each tile holds at most kMergeCap runs)
+  const u64 target = (u64)compute_units() * 128;
+  const u32 wpt = (u32)std::min<u64>(kMergeCap / kWave, std::max<u64>(1, ceil_div(target, a.ntiles)));
+  hipLaunchKernelGGL(k_emit_tiles, dim3((unsigned)ceil_div(a.ntiles * wpt, 256 / kWave)), dim3(256),
+                     0, s, a, wpt);
 }
 
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s) {
