@@ -253,53 +253,79 @@ __global__ __launch_bounds__(kHeavyNT) void k_emit_heavy(LevelArgs a) {
   }
 }
 
-// 8 consecutive record keys with 16-byte stores (p is 32-byte aligned).
-// A lane writes kRun consecutive records per run; the lanes of a wave write
-// consecutive runs, so every vector store of a wave covers one contiguous
-// span (64 * 16 bytes for u32 keys and for weights).
-constexpr int kRun = 4;
-constexpr int kRuns = kExpandIT / kRun;  // runs per thread
-static_assert(kExpandIT % kRun == 0, "whole runs per thread");
-
 // Records are written once and read once by the merge, long after they
-// have left the caches at the sizes that matter: streaming stores.
+// have left the caches at the sizes that matter: streaming stores of kRun
+// consecutive records per lane (the lanes of a wave write consecutive runs,
+// so every pair of vector stores of a wave covers one contiguous span).
+constexpr int kRun = kExpandIT;
 typedef u32 u32x4 __attribute__((ext_vector_type(4)));
 typedef u64 u64x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void store_run(u32 *p, const u32 (&k)[kRun]) {
-  const u32x4 v = {k[0], k[1], k[2], k[3]};
-  __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p));
+#pragma unroll
+  for (int i = 0; i < kRun; i += 4) {
+    const u32x4 v = {k[i], k[i + 1], k[i + 2], k[i + 3]};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(p + i));
+  }
 }
 __device__ __forceinline__ void store_run(u64 *p, const u64 (&k)[kRun]) {
-  const u64x2 v0 = {k[0], k[1]}, v1 = {k[2], k[3]};
-  __builtin_nontemporal_store(v0, reinterpret_cast<u64x2 *>(p));
-  __builtin_nontemporal_store(v1, reinterpret_cast<u64x2 *>(p) + 1);
+#pragma unroll
+  for (int i = 0; i < kRun; i += 2) {
+    const u64x2 v = {k[i], k[i + 1]};
+    __builtin_nontemporal_store(v, reinterpret_cast<u64x2 *>(p + i));
+  }
 }
 __device__ __forceinline__ void store_run(float *p, const float (&w)[kRun]) {
-  const f32x4 v = {w[0], w[1], w[2], w[3]};
-  __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(p));
+#pragma unroll
+  for (int i = 0; i < kRun; i += 4) {
+    const f32x4 v = {w[i], w[i + 1], w[i + 2], w[i + 3]};
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(p + i));
+  }
+}
+
+// Arc j of a CSR arc array.  With NARROW, j < 2^29 and the byte offset is a
+// 32-bit value added to the array base (one address operation per load).
+template <bool NARROW>
+__device__ __forceinline__ uint2 load_arc(const uint2 *arcs, u32 j) {
+  if (NARROW) return *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(arcs) + (j << 3));
+  return arcs[j];
 }
 
 // ---------------------------------------------------------------------------
 // Arc-pair write pass.  Workgroup b produces the records of write tiles
 // kExpandGroup*b .. kExpandGroup*(b+1) - 1: the matches overlapping them are
 // staged in LDS (all tiles at once when they fit, else one tile after the
-// other).  Wave w writes the wave span [w*64*kExpandIT, (w+1)*64*kExpandIT)
-// of the group as kRuns passes of 64 lanes x kRun consecutive records; for
-// each run a lane finds the match of its first record by binary search in
-// LDS, takes (i, j) = divmod(offset, n2) to select the M1 and M2 arcs, and
-// steps through the run.  Record = (part1 << b2 | part2, p1 * p2).
-template <class KT>
+// other) with a bitmap of their first records, so that the match holding a
+// record is a prefix popcount away.  Lane l of wave w writes the run of kRun
+// consecutive records starting at w*64*kRun + l*kRun of the group: it finds
+// the match of the run's first record, its offset t in the match gives
+// (i, j) = divmod(t, n2) (M1 arc i, M2 arc j of the match), and the next
+// records step through the match and into the following ones.  All arc
+// loads of the run are issued before any is used, and the records are
+// stored last, so loads are not queued behind the wave's own stores.
+// Record = (part1 << b2 | part2, p1 * p2).
+constexpr u32 kSpanRecs = kExpandNT * kExpandIT;  // records per workgroup
+constexpr u32 kSpanWords = kSpanRecs / 32;         // bitmap words
+static_assert(kSpanWords == 2 * kWave, "two bitmap words per lane of one wave");
+static_assert(kExpandTile % kExpandNT == 0, "whole staging rounds");
+static_assert(kRun % 4 == 0, "runs of whole 16-byte stores");
+
+template <class KT, bool NARROW>
 __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const u64 *mrbase, u64 M,
                                                       u64 R, const uint2 *arcs1,
                                                       const uint2 *arcs2, int b2, KT *rec_key,
                                                       float *rec_w, const ExpandTile *tiles,
                                                       u64 ntiles, u32 *err) {
-  __shared__ u32 s_rel[kExpandTile];
-  __shared__ uint4 s_m[kExpandTile];
-  constexpr u32 kSpan = kWave * kExpandIT;                      // records per wave
+  __shared__ u32 s_rel[kExpandTile + 1];  // first record of each match, relative; sentinel
+  __shared__ u32 s_a1[kExpandTile];       // first M1 arc of the match
+  __shared__ u32 s_a2[kExpandTile];       // first M2 arc
+  __shared__ u32 s_n2[kExpandTile];       // M2 arcs of the match
+  __shared__ u32 s_bits[kSpanWords];      // bit r: a match starts at relative record r
+  __shared__ u32 s_pre[kSpanWords];       // set bits in the words before
+  constexpr u32 kSpan = kWave * kRun;     // records per wave
   constexpr u32 kWavesPerTile = (u32)(kExpandTile / kSpan);
+  constexpr int kStage = (int)(kExpandTile / kExpandNT);
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u64 g0 = (u64)blockIdx.x * kExpandGroup;
   const u64 ng = min(kExpandGroup, ntiles - g0);
@@ -317,56 +343,101 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
       return;
     }
     if (pass) __syncthreads();  // previous tile's LDS fully read
-    for (u32 i = threadIdx.x; i < nm; i += kExpandNT) {
-      s_rel[i] = i == 0 ? 0u : (u32)(mrbase[k0 + i] - rs);
-      s_m[i] = match[k0 + i];
+    if (threadIdx.x < kSpanWords) s_bits[threadIdx.x] = 0;
+    if (threadIdx.x == 0) s_rel[nm] = 0xffffffffu;  // no record reaches it
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+      if ((u64)q * kExpandNT >= nm) break;  // uniform
+      const u32 i = threadIdx.x + q * kExpandNT;
+      const u64 k = k0 + min<u64>(i, nm - 1);  // in bounds
+      const u64 rb = mrbase[k];
+      const uint4 mm = match[k];
+      if (i < nm) {
+        // matches start inside the staged span, match k0 at or before it
+        const u32 rel = i == 0 ? 0u : (u32)(rb - rs);
+        s_rel[i] = rel;
+        s_a1[i] = mm.x;
+        s_a2[i] = mm.y;
+        s_n2[i] = mm.w;
+        atomicOr(&s_bits[rel >> 5], 1u << (rel & 31));
+      }
+    }
+    __syncthreads();
+    if (w == 0) {
+      const u32 c0 = __popc(s_bits[2 * lane]), c1 = __popc(s_bits[2 * lane + 1]);
+      const u32 inc = wave_inclusive_sum(c0 + c1);
+      s_pre[2 * lane] = inc - c0 - c1;
+      s_pre[2 * lane + 1] = inc - c1;
     }
     __syncthreads();
     if (!one && w / kWavesPerTile != pass) continue;
+
+    // 1. M1 / M2 arc index of every record of the run (in bounds even for
+    //    records past R: those repeat the run's first record, whose match is
+    //    match 0 when the run is empty)
+    const u64 rfirst = r0 + w * kSpan + lane * kRun;
+    const u32 cnt = rfirst < R ? (u32)min<u64>(kRun, R - rfirst) : 0u;
+    u32 p = cnt ? (u32)(rfirst - rs) : 0u;
+    const u32 wd = p >> 5;
+    u32 mi = s_pre[wd] + __popc(s_bits[wd] & ((2u << (p & 31)) - 1u)) - 1u;
+    u32 a1 = s_a1[mi], a2 = s_a2[mi], n2 = s_n2[mi], nxt = s_rel[mi + 1];
+    const u64 t = !cnt ? 0 : mi == 0 ? rfirst - ti.base0 : (u64)(p - s_rel[mi]);
+    u32 i1, i2;
+    if (t < (1ull << 32)) {
+      const u32 tt = (u32)t;
+      i1 = tt / n2;
+      i2 = tt - i1 * n2;
+    } else {
+      const u64 q = t / n2;
+      i1 = (u32)q;
+      i2 = (u32)(t - q * n2);
+    }
+    u32 ix1[kRun], ix2[kRun];
+    ix1[0] = a1 + i1;
+    ix2[0] = a2 + i2;
 #pragma unroll
-    for (int h = 0; h < kRuns; ++h) {
-      const u64 rfirst = r0 + w * kSpan + h * (kWave * kRun) + lane * kRun;
-      if (rfirst >= R) break;
-      const u32 cnt = (u32)min<u64>(kRun, R - rfirst);
-      const u32 rel = (u32)(rfirst - rs);
-      u32 mi = (u32)last_le<u32>(s_rel, nm, rel);
-      uint4 m = s_m[mi];
-      const u64 t = mi == 0 ? rfirst - ti.base0 : (u64)(rel - s_rel[mi]);
-      u32 i1, i2;
-      if (t < (1ull << 32)) {
-        const u32 tt = (u32)t;
-        i1 = tt / m.w;
-        i2 = tt - i1 * m.w;
-      } else {
-        const u64 q = t / m.w;
-        i1 = (u32)q;
-        i2 = (u32)(t - q * m.w);
+    for (int j = 1; j < kRun; ++j) {
+      ++p;
+      ++i2;
+      const bool wrap = i2 == n2;
+      i2 = wrap ? 0u : i2;
+      i1 += wrap ? 1u : 0u;
+      if (p == nxt && (u32)j < cnt) {  // record j opens the next match
+        ++mi;
+        a1 = s_a1[mi];
+        a2 = s_a2[mi];
+        n2 = s_n2[mi];
+        nxt = s_rel[mi + 1];
+        i1 = i2 = 0;
       }
-      KT key[kRun];
-      float wt[kRun];
+      const bool v = (u32)j < cnt;
+      ix1[j] = v ? a1 + i1 : ix1[0];
+      ix2[j] = v ? a2 + i2 : ix2[0];
+    }
+    // 2. every arc load of the run in flight at once
+    uint2 A1[kRun], A2[kRun];
+#pragma unroll
+    for (int j = 0; j < kRun; ++j) {
+      A1[j] = load_arc<NARROW>(arcs1, ix1[j]);
+      A2[j] = load_arc<NARROW>(arcs2, ix2[j]);
+    }
+    // 3. records, stored last (both branches use every loaded arc, so the
+    //    loads stay ahead of them)
+    KT key[kRun];
+    float wt[kRun];
+#pragma unroll
+    for (int j = 0; j < kRun; ++j) {
+      key[j] = (KT)(((u64)A1[j].x << b2) | (u64)A2[j].x);
+      wt[j] = __uint_as_float(A1[j].y) * __uint_as_float(A2[j].y);
+    }
+    if (cnt == (u32)kRun) {
+      store_run(rec_key + rfirst, key);
+      store_run(rec_w + rfirst, wt);
+    } else {
 #pragma unroll
       for (int j = 0; j < kRun; ++j) {
-        key[j] = 0;
-        wt[j] = 0.f;
         if ((u32)j < cnt) {
-          const uint2 A1 = arcs1[m.x + i1];
-          const uint2 A2 = arcs2[m.y + i2];
-          key[j] = (KT)(((u64)A1.x << b2) | (u64)A2.x);
-          wt[j] = __uint_as_float(A1.y) * __uint_as_float(A2.y);
-          if (++i2 == m.w) {
-            i2 = 0;
-            if (++i1 == m.z && (u32)j + 1 < cnt) {
-              i1 = 0;
-              m = s_m[++mi];
-            }
-          }
-        }
-      }
-      if (cnt == kRun) {
-        store_run(rec_key + rfirst, key);
-        store_run(rec_w + rfirst, wt);
-      } else {
-        for (u32 j = 0; j < cnt; ++j) {
           rec_key[rfirst + j] = key[j];
           rec_w[rfirst + j] = wt[j];
         }
@@ -409,12 +480,18 @@ void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const Cs
   const unsigned gs = (unsigned)std::min<u64>(ceil_div(g, 256), 1u << 20);
   hipLaunchKernelGGL(k_tile_matches, dim3(gs), dim3(256), 0, s, mrbase, M, R, g, tiles);
   const unsigned gw = (unsigned)ceil_div(g, kExpandGroup);
-  if (wide_keys)
-    hipLaunchKernelGGL((k_expand<u64>), dim3(gw), dim3(kExpandNT), 0, s, match, mrbase, M, R,
-                       c1.arcs, c2.arcs, b2, (u64 *)rec_key, rec_w, tiles, g, err);
-  else
-    hipLaunchKernelGGL((k_expand<u32>), dim3(gw), dim3(kExpandNT), 0, s, match, mrbase, M, R,
-                       c1.arcs, c2.arcs, b2, (u32 *)rec_key, rec_w, tiles, g, err);
+  // 32-bit byte offsets into the arc arrays when both hold fewer than 2^29 arcs
+  const bool narrow = std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29);
+  auto go = [&](auto kt, auto nar) {
+    using KT = decltype(kt);
+    hipLaunchKernelGGL((k_expand<KT, decltype(nar)::value>), dim3(gw), dim3(kExpandNT), 0, s, match,
+                       mrbase, M, R, c1.arcs, c2.arcs, b2, (KT *)rec_key, rec_w, tiles, g, err);
+  };
+  if (wide_keys) {
+    if (narrow) go(u64{}, std::true_type{}); else go(u64{}, std::false_type{});
+  } else {
+    if (narrow) go(u32{}, std::true_type{}); else go(u32{}, std::false_type{});
+  }
 }
 
 }  // namespace fstc

@@ -14,10 +14,11 @@ struct CsrView {
   const uint2 *arcs;
   const u32 *part_base;
   const uint2 *parts;
+  u64 num_arcs;
 };
 
 inline CsrView view(const Csr &c) {
-  return CsrView{c.row, c.seg_sym, c.seg_off, c.arcs, c.part_base, c.parts};
+  return CsrView{c.row, c.seg_sym, c.seg_off, c.arcs, c.part_base, c.parts, c.num_arcs};
 }
 
 // Host-visible per-level counters (one D2H copy per synchronisation).
