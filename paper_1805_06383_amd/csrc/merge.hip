@@ -86,6 +86,7 @@ constexpr u32 kRerouted = 0x80000000u;
 constexpr u64 kListedGrid = 2048;  // workgroups walking the list of tiles left to sort
 constexpr int kEmitBatch = 4;      // runs per lane in flight when a tile has many
 constexpr u32 kDenseEPT = kDenseCap / NT;  // table entries per thread when listing runs
+constexpr u32 kExactSpan = 26;  // binades of a tile summed exactly in 64-bit fixed point
 static_assert(kDenseCap % NT == 0 && (1u << kDenseKeyBits) == kDenseCap, "dense table shape");
 
 __device__ __forceinline__ bool dense_tile(const uint4 &td, int key_bits) {
@@ -516,7 +517,10 @@ __global__ __launch_bounds__(NT, 4) void k_merge_listed(MergeArgs a) {
 // (24 bits with the hidden bit) becomes floor(+-m * 2^27 / 2^(E - be)), so
 // every term is below 2^51 in magnitude, a sum of 4096 stays below 2^63, and
 // the result does not depend on the order of the atomic adds; each term loses
-// at most one unit, 2^-50 of the entry's largest term.  Entries present in
+// at most one unit, 2^-50 of the entry's largest term.  When all nonzero
+// weights of the tile lie within kExactSpan binades of the smallest one
+// (exponent Emin), the first pass is skipped: every term is m * 2^(be - Emin)
+// exactly, in units of 2^(Emin - 150), and each sum is exact.  Entries present in
 // the tile become runs in (segment, key) order, the order of the sort path.
 // A tile holding an infinite or NaN weight is left to the sort kernel
 // (descriptor flag kRerouted).
@@ -533,6 +537,7 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
   __shared__ u32 s_bits[C / 32];  // bit e: tile element e starts a source
   __shared__ u32 s_pre[C / 32];   // set bits in the words before
   __shared__ u32 s_tmp[NW];
+  __shared__ u32 s_emin, s_emax, s_nonfinite;  // over the tile's nonzero weights
 
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
@@ -550,6 +555,11 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
   const u64 rb = (u64)tile * a.window + off;  // first record of the tile
   // 1. source starts -> bitmap -> segment of every element
   if (threadIdx.x < C / 32) s_bits[threadIdx.x] = 0;
+  if (threadIdx.x == 0) {
+    s_emin = 0xffu;
+    s_emax = 0;
+    s_nonfinite = 0;
+  }
   // a dense tile has at most kDenseCap sources: thread t takes sources
   // s0 + t + k*NT, k < kDenseEPT, and keeps their start (or kNoStart)
   constexpr u32 kNoStart = 0xffffffffu;
@@ -612,55 +622,120 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
   }
   // biased exponent of a weight, denormals and zero counted as 1
   auto bexp = [](float x) { return max((__float_as_uint(x) >> 23) & 0xffu, 1u); };
+  // significand with the hidden bit, signed
+  auto sig = [](float x) {
+    const u32 bits = __float_as_uint(x);
+    const u32 mag = (bits & 0x7fffffu) | (((bits >> 23) & 0xffu) ? 0x800000u : 0u);
+    return (bits >> 31) ? -(int)mag : (int)mag;
+  };
   constexpr u32 kNone = 0xffffffffu;  // table index of an absent item
+  // Item j of every lane of the wave lies in the element row
+  // [w*512 + j*64, +64), two bitmap words: the segment of the lane's element
+  // is the row's prefix count plus the starts at or below its lane (mbcnt).
   u32 idx[IT];
-  u32 nonfinite = 0;
+  u32 nonfinite = 0, emin = 0xffu, emax = 0;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
     const u32 e = e0 + j * kWave;
-    const u32 ix = (seg_of(min(e, n - 1)) << kb) | (key[j] & ((1u << kb) - 1u));
-    idx[j] = e < n ? ix : kNone;
-    nonfinite |= (e < n && bexp(wt[j]) == 0xffu) ? 1u : 0u;
+    const u32 wd = (w * (kWave * IT) + j * kWave) >> 5;  // uniform
+    const u32 lo = __builtin_amdgcn_readfirstlane(s_bits[wd]);
+    const u32 hi = __builtin_amdgcn_readfirstlane(s_bits[wd + 1]);
+    const u32 pre = __builtin_amdgcn_readfirstlane(s_pre[wd]);
+    const u32 below = __builtin_amdgcn_mbcnt_hi(hi, __builtin_amdgcn_mbcnt_lo(lo, 0u));
+    const u32 own = (u32)((((u64)hi << 32 | lo) >> lane) & 1u);
+    const u32 seg = pre + below + own - 1u;  // elements past n: never used
+    idx[j] = e < n ? (seg << kb) | (key[j] & ((1u << kb) - 1u)) : kNone;
+    const u32 bits = __float_as_uint(wt[j]);
+    const u32 be = bexp(wt[j]);
+    const bool live = e < n && (bits & 0x7fffffffu) != 0;
+    nonfinite |= (e < n && be == 0xffu) ? 1u : 0u;
+    emin = live ? min(emin, be) : emin;
+    emax = live ? max(emax, be) : emax;
   }
-  if (__syncthreads_or(nonfinite)) {
+  // (nonfinite, 255 - emin) packed: the lexicographic maximum is right for
+  // both (emin only matters when no lane saw a non-finite weight)
+  const u32 packed = wave_max((nonfinite << 8) | (0xffu - emin));
+  emax = wave_max(emax);
+  if (lane == 0) {
+    atomicMin(&s_emin, 0xffu - (packed & 0xffu));
+    atomicMax(&s_emax, emax);
+    if (packed >> 8) s_nonfinite = 1;
+  }
+  __syncthreads();
+  if (s_nonfinite) {
     if (threadIdx.x == 0) {
       a.tiles[tile].w = n | kRerouted;
       list_for_sort(a, tile);
     }
     return;
   }
-
-  // 2. largest exponent per entry.  A thread's items with equal entries
-  //    (64 elements apart) are combined first: one LDS atomic per run of
-  //    equal consecutive items.
-  {
-    u32 m = 0;
+  const u32 Emin = s_emin, Emax = s_emax;
+  // a thread whose items all hold one entry (or none) flushes once
+  bool one_run = true;
+#pragma unroll
+  for (int j = 1; j < IT; ++j) one_run = one_run && (idx[j] == idx[0] || idx[j] == kNone);
+  if (Emax <= Emin + kExactSpan) {
+    // 2'. every nonzero weight of the tile within 2^kExactSpan binades: terms
+    //     m * 2^(be - Emin) are exact in 64 bits and so are their sums (all
+    //     below 2^(24 + kExactSpan + 12)); entry scale 2^(Emin - 150) is
+    //     recorded as s_exp = Emin + 28 (E - 177 = Emin - 150 below).
+    long long term[IT];
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
-      const bool start = j == 0 || idx[j] != idx[j - 1];
-      const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
       const u32 be = bexp(wt[j]);
-      m = start ? be : max(m, be);
-      if (end) atomicMax(&s_exp[idx[j]], m + 1);
+      term[j] = idx[j] == kNone ? 0ll : (long long)sig(wt[j]) << (be > Emin ? be - Emin : 0u);
     }
-  }
-  __syncthreads();
-  // 3. fixed-point sums, combined the same way
-  {
-    long long acc = 0;
-    u32 E = 0;
+    if (one_run) {
+      long long acc = 0;
 #pragma unroll
-    for (int j = 0; j < IT; ++j) {
-      const bool start = j == 0 || idx[j] != idx[j - 1];
-      const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
-      const u32 ex = s_exp[idx[j] != kNone ? idx[j] : 0u] - 1u;
-      E = start ? ex : E;
-      const u32 bits = __float_as_uint(wt[j]);
-      const u32 mag = (bits & 0x7fffffu) | (((bits >> 23) & 0xffu) ? 0x800000u : 0u);
-      const int ms = (bits >> 31) ? -(int)mag : (int)mag;
-      const long long term = ((long long)ms * (1ll << 27)) >> min(E - bexp(wt[j]), 63u);
-      acc = (start ? 0ll : acc) + term;
-      if (end) atomicAdd(&s_sum[idx[j]], (unsigned long long)acc);
+      for (int j = 0; j < IT; ++j) acc += term[j];
+      if (idx[0] != kNone) {
+        atomicAdd(&s_sum[idx[0]], (unsigned long long)acc);
+        s_exp[idx[0]] = Emin + 28;
+      }
+    } else {
+      long long acc = 0;
+#pragma unroll
+      for (int j = 0; j < IT; ++j) {
+        const bool start = j == 0 || idx[j] != idx[j - 1];
+        const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
+        acc = (start ? 0ll : acc) + term[j];
+        if (end) {
+          atomicAdd(&s_sum[idx[j]], (unsigned long long)acc);
+          s_exp[idx[j]] = Emin + 28;
+        }
+      }
+    }
+  } else {
+    // 2. largest exponent per entry.  A thread's items with equal entries
+    //    (64 elements apart) are combined first: one LDS atomic per run of
+    //    equal consecutive items.
+    {
+      u32 m = 0;
+#pragma unroll
+      for (int j = 0; j < IT; ++j) {
+        const bool start = j == 0 || idx[j] != idx[j - 1];
+        const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
+        const u32 be = bexp(wt[j]);
+        m = start ? be : max(m, be);
+        if (end) atomicMax(&s_exp[idx[j]], m + 1);
+      }
+    }
+    __syncthreads();
+    // 3. fixed-point sums, combined the same way
+    {
+      long long acc = 0;
+      u32 E = 0;
+#pragma unroll
+      for (int j = 0; j < IT; ++j) {
+        const bool start = j == 0 || idx[j] != idx[j - 1];
+        const bool end = idx[j] != kNone && (j == IT - 1 || idx[j + 1] != idx[j]);
+        const u32 ex = s_exp[idx[j] != kNone ? idx[j] : 0u] - 1u;
+        E = start ? ex : E;
+        const long long term = ((long long)sig(wt[j]) * (1ll << 27)) >> min(E - bexp(wt[j]), 63u);
+        acc = (start ? 0ll : acc) + term;
+        if (end) atomicAdd(&s_sum[idx[j]], (unsigned long long)acc);
+      }
     }
   }
   __syncthreads();
