@@ -258,7 +258,7 @@ void Composer::run(fstc_result *out) {
   Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
       bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
       stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A), tiles_e(&A), tiles_m(&A), tstart(&A),
-      mend(&A), sortlist(&A), tile_runs(&A), wcnt(&A), woff(&A), wtmp(&A);
+      mend(&A), sortlist(&A), tile_runs(&A), wcnt(&A), woff(&A), wtmp(&A), runsrc(&A);
 
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
@@ -297,6 +297,7 @@ void Composer::run(fstc_result *out) {
     rkey.ensure(R * rec_bytes);
     rw.ensure(R * 4);
     temp.ensure(R * sizeof(uint4));
+    runsrc.ensure(R * 4);
     tiles_e.ensure(ceil_div(R, kExpandTile) * sizeof(ExpandTile));
     // merge window: as wide as the largest small source allows (see level.hpp)
     const u64 max_small = std::max<u32>(1, hs->st.max_small);
@@ -363,6 +364,7 @@ void Composer::run(fstc_result *out) {
     ma.newlist = newlist.as<u32>();
     ma.newcap = newcap;
     ma.temp = temp.as<uint4>();
+    ma.runsrc = runsrc.as<u32>();
     ma.tiles = tiles_m.as<uint4>();
     ma.sortlist = sortlist.as<u32>();
     ma.tile_runs = tile_runs.as<u32>();
@@ -446,10 +448,9 @@ void Composer::run(fstc_result *out) {
       oil.grow_keep(na * 4, arcs * 4);
       ool.grow_keep(na * 4, arcs * 4);
       ow.grow_keep(na * 4, arcs * 4);
-      launch_compact(temp.as<uint4>(), R, tstart.as<u64>(), aoff.as<u64>(), nsrc, lo, merged,
-                     hvb.as<u32>(), osrc.as<u32>() + arcs, odst.as<u32>() + arcs,
-                     oil.as<u32>() + arcs, ool.as<u32>() + arcs, ow.as<float>() + arcs,
-                     &dst->err, s);
+      launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc.as<u32>() + arcs,
+                     odst.as<u32>() + arcs, oil.as<u32>() + arcs, ool.as<u32>() + arcs,
+                     ow.as<float>() + arcs, s);
     }
     T.end(kAssign);
     arcs += merged;

@@ -123,6 +123,8 @@ struct MergeArgs {
   u64 newcap;
   uint4 *temp;     // [R] merged runs: (source, key lo, key hi, weight bits) from the
                    // merge, then (slot, a, c, weight bits) after launch_emit_runs
+  u32 *runsrc;     // [R] level-local source of the merged run at each temp slot
+                   // (written with the visited-table insert)
   u64 *tstart;     // [nsrc] first temp slot of each source's merged arcs (0 if none)
   u64 *mend;       // [nsrc] one past its last slot (0 if none)
   u64 window;      // W: tile t takes the sources starting in [t W, (t + 1) W)
@@ -158,10 +160,13 @@ void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *
                    u32 *sq2, hipStream_t s);
 void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
                     u32 *vals, hipStream_t s);
-// Level merged arc k of source u is temp[tstart[u] + k - aoff[u]].
-void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff, u32 nsrc,
-                    u32 lo, u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool,
-                    float *ow, u32 *err, hipStream_t s);
+// Result append of the level's merged arcs: the runs of merge tile t go to
+// output positions aoff[first source of t] + r, those of multi-block source u
+// to aoff[u] + r (aoff: exclusive scan of merged arcs per source), so the
+// output stays grouped by source id.  dst ids come from hvals.
+// M: merged arcs of the level (the output arrays' length from osrc on).
+void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const u32 *hvals,
+                    u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s);
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s);
 // Visited-table inserts and label lookups for every merged arc of the
 // tile-merged sources (merge_big does its own).

@@ -229,10 +229,13 @@ __device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)
   bool is_new[B];
   hash_insert_batch<B>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
 #pragma unroll
-  for (int i = 0; i < B; ++i)
-    if (act[i])
+  for (int i = 0; i < B; ++i) {
+    if (act[i]) {
       a.temp[tpos[i]] = make_uint4(slot[i] | (is_new[i] ? kNewFlag : 0u), P1[i].y, P2[i].y,
                                    __float_as_uint(w[i]));
+      a.runsrc[tpos[i]] = u[i];
+    }
+  }
 }
 
 // LDS of the sorting tile merge.
@@ -1012,18 +1015,36 @@ __global__ void k_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq
   vals[i] = slot;
 }
 
-__global__ void k_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff, u32 nsrc,
-                          u32 lo, u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil,
-                          u32 *ool, float *ow, u32 *err) {
-  for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < M; k += (u64)gridDim.x * blockDim.x) {
-    const u32 u = (u32)last_le<u64>(aoff, nsrc, k);
-    const u64 t = tstart[u] + (k - aoff[u]);
-    if (t >= R) {
-      set_error(err, kErrBounds);
-      continue;
-    }
-    const uint4 rec = temp[t];
-    osrc[k] = lo + u;
+// Wave per segment of merged runs: merge tile i (i < ntiles) or multi-block
+// source big[i - ntiles]; lanes copy consecutive runs.
+__global__ __launch_bounds__(256) void k_compact(MergeArgs a, const u64 *aoff, u32 nbig, u64 M,
+                                                 const u32 *hvals, u32 *osrc, u32 *odst,
+                                                 u32 *oil, u32 *ool, float *ow) {
+  const u32 lane = lane_id();
+  const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  if (wv >= a.ntiles + nbig) return;
+  u64 tbase, obase;
+  u32 cnt;
+  if (wv < a.ntiles) {
+    cnt = a.tile_runs[wv];
+    if (cnt == 0) return;
+    const uint4 td = a.tiles[wv];
+    tbase = wv * a.window + td.z;
+    obase = aoff[td.x];
+  } else {
+    const u32 u = a.big[wv - a.ntiles];
+    tbase = a.tstart[u];
+    cnt = (u32)(a.mend[u] - tbase);
+    obase = aoff[u];
+  }
+  if (tbase + cnt > a.R || obase + cnt > M) {  // impossible: counts agree with aoff
+    if (lane == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  for (u32 r = lane; r < cnt; r += kWave) {
+    const uint4 rec = a.temp[tbase + r];
+    const u64 k = obase + r;
+    osrc[k] = a.lo + a.runsrc[tbase + r];
     odst[k] = hvals[rec.x & ~kNewFlag];
     oil[k] = rec.y;
     ool[k] = rec.z;
@@ -1167,12 +1188,12 @@ void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64
                      nnew, hkeys, bq2, keys, vals);
 }
 
-void launch_compact(const uint4 *temp, u64 R, const u64 *tstart, const u64 *aoff, u32 nsrc, u32 lo,
-                    u64 M, const u32 *hvals, u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow,
-                    u32 *err, hipStream_t s) {
-  if (!M) return;
-  hipLaunchKernelGGL(k_compact, dim3(grid1(M)), dim3(256), 0, s, temp, R, tstart, aoff, nsrc, lo,
-                     M, hvals, osrc, odst, oil, ool, ow, err);
+void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const u32 *hvals,
+                    u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s) {
+  const u64 nw = a.ntiles + nbig;
+  if (!nw || !M) return;
+  hipLaunchKernelGGL(k_compact, dim3((unsigned)ceil_div(nw, 256 / kWave)), dim3(256), 0, s, a, aoff,
+                     nbig, M, hvals, osrc, odst, oil, ool, ow);
 }
 
 u64 newlist_waves(const MergeArgs &a, u64 RB) { return a.ntiles + ceil_div(RB, kWave); }
