@@ -276,12 +276,11 @@ void Composer::run(fstc_result *out) {
     launch_reset_level(dst, tstat, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
-                 dst, nullptr, nullptr};
+                 dst, nullptr, nullptr, big.as<u32>()};
     T.begin();
     launch_count(la, s);
     exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
     exclusive_scan(mc.as<u32>(), moff.as<u64>(), nsrc, stmp.p, s);
-    launch_collect_big(roff.as<u64>(), nsrc, big.as<u32>(), dst, s);
     launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, s);
     T.end(kCount);
     sync_status();

@@ -75,18 +75,30 @@ __device__ __forceinline__ Ranges source_ranges(const LevelArgs &a, u32 u) {
 __device__ __forceinline__ u32 seg_len(const u32 *seg_off, u32 s) { return seg_off[s + 1] - seg_off[s]; }
 
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_count_small(LevelArgs a) {
+// Sources of more than kMergeSmall unmerged arcs are merged by the
+// multi-block path (a.big); the largest count among the others sizes the
+// merge window (st->max_small).  Both are gathered by the count kernels.
+constexpr int kCountNT = 256;
+
+// Thread per source: joins the short ones, lists the others for the
+// wavefront / workgroup joins.  List appends and the window maximum are
+// aggregated per workgroup in LDS: one device atomic per list per block.
+__global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
+  __shared__ u32 s_n[3], s_base[3], s_max;
+  const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  bool wide = false, heavy = false;
+  if (threadIdx.x < 3) s_n[threadIdx.x] = 0;
+  if (threadIdx.x == 0) s_max = 0;
+  bool pred[3] = {false, false, false};  // wide, heavy, big
+  u64 cnt = 0;
   if (u < a.nsrc) {
     const Ranges r = source_ranges(a, (u32)u);
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
     if (mn > kHeavyMin) {
-      heavy = true;
+      pred[1] = true;
     } else if (mn > kWideMin) {
-      wide = true;
+      pred[0] = true;
     } else {
-      u64 cnt = 0;
       u32 mc = 0;
       intersect_serial(a.c1.seg_sym, r.b1, r.e1, a.c2.seg_sym, r.b2, r.e2, [&](u32 s1, u32 s2) {
         cnt += (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2);
@@ -94,10 +106,51 @@ __global__ __launch_bounds__(256) void k_count_small(LevelArgs a) {
       });
       a.cnt[u] = cnt;
       a.mc[u] = mc;
+      pred[2] = cnt > kMergeSmall;
     }
   }
-  wave_append(wide, (u32)u, a.wide, &a.st->nwide);
-  wave_append(heavy, (u32)u, a.heavy, &a.st->nheavy);
+  const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
+  __syncthreads();
+  u64 m[3];
+  u32 woff[3];
+#pragma unroll
+  for (int l = 0; l < 3; ++l) {
+    m[l] = __ballot(pred[l]);
+    woff[l] = 0;
+    if (m[l]) {
+      const u32 leader = __ffsll((unsigned long long)m[l]) - 1;
+      if (lane == leader) woff[l] = atomicAdd(&s_n[l], (u32)__popcll(m[l]));
+      woff[l] = __shfl(woff[l], leader, kWave);
+    }
+  }
+  if (lane == 0 && small_max) atomicMax(&s_max, small_max);
+  __syncthreads();
+  u32 *const counters[3] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig};
+  if (threadIdx.x < 3 && s_n[threadIdx.x]) s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
+  if (threadIdx.x == 3 && s_max) atomicMax(&a.st->max_small, s_max);
+  __syncthreads();
+  u32 *const lists[3] = {a.wide, a.heavy, a.big};
+#pragma unroll
+  for (int l = 0; l < 3; ++l)
+    if (pred[l]) lists[l][s_base[l] + woff[l] + count_below(m[l])] = (u32)u;
+}
+
+// Big-source append and window maximum of one joined source (lane 0 of the
+// joining wave or thread 0 of the joining block): big sources are rare, the
+// maximum is kept in `run_max` and published once per block.
+__device__ __forceinline__ void note_count(const LevelArgs &a, u32 u, u64 cnt, u32 &run_max) {
+  if (cnt > kMergeSmall) a.big[atomicAdd(&a.st->nbig, 1u)] = u;
+  else run_max = max(run_max, (u32)cnt);
+}
+
+template <int NT>
+__device__ __forceinline__ void publish_max(const LevelArgs &a, u32 run_max, u32 *s_max) {
+  if (threadIdx.x == 0) *s_max = 0;
+  __syncthreads();
+  run_max = wave_max(run_max);
+  if (lane_id() == 0 && run_max) atomicMax(s_max, run_max);
+  __syncthreads();
+  if (threadIdx.x == 0 && *s_max) atomicMax(&a.st->max_small, *s_max);
 }
 
 // One lane's share of a cooperative join: element idx of the shorter list.
@@ -127,6 +180,8 @@ __device__ __forceinline__ Hit probe_one(const LevelArgs &a, const Ranges &r, bo
 
 // Wavefront per source (grid-stride over the wide list).
 __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
+  __shared__ u32 s_max;
+  u32 run_max = 0;
   const u32 lane = lane_id();
   const u32 gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const u32 nw = gridDim.x * blockDim.x / kWave;
@@ -150,8 +205,10 @@ __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
     if (lane == 0) {
       a.cnt[u] = cnt;
       a.mc[u] = mc;
+      note_count(a, u, cnt, run_max);
     }
   }
+  publish_max<256>(a, run_max, &s_max);
 }
 
 // Workgroup per source (grid-stride over the heavy list).
@@ -160,6 +217,8 @@ constexpr int kHeavyNT = 512;
 __global__ __launch_bounds__(kHeavyNT) void k_count_heavy(LevelArgs a) {
   __shared__ u64 s64[kHeavyNT / kWave];
   __shared__ u32 s32[kHeavyNT / kWave];
+  __shared__ u32 s_max;
+  u32 run_max = 0;
   const u32 n = a.st->nheavy;
   for (u32 i = blockIdx.x; i < n; i += gridDim.x) {
     const u32 u = a.heavy[i];
@@ -180,8 +239,10 @@ __global__ __launch_bounds__(kHeavyNT) void k_count_heavy(LevelArgs a) {
     if (threadIdx.x == 0) {
       a.cnt[u] = cnt;
       a.mc[u] = mc;
+      note_count(a, u, cnt, run_max);
     }
   }
+  publish_max<kHeavyNT>(a, run_max, &s_max);
 }
 
 // ---------------------------------------------------------------------------
@@ -458,8 +519,8 @@ __global__ void k_tile_matches(const u64 *mrbase, u64 M, u64 R, u64 ntiles, Expa
 }  // namespace
 
 void launch_count(const LevelArgs &a, hipStream_t s) {
-  const unsigned g = (unsigned)ceil_div(a.nsrc, 256);
-  hipLaunchKernelGGL(k_count_small, dim3(g), dim3(256), 0, s, a);
+  const unsigned g = (unsigned)ceil_div(a.nsrc, kCountNT);
+  hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
   hipLaunchKernelGGL(k_count_wide, dim3(2048), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_count_heavy, dim3(512), dim3(kHeavyNT), 0, s, a);
 }

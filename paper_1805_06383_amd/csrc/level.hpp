@@ -96,6 +96,7 @@ struct LevelArgs {
   Status *st;
   uint4 *match;          // [M] (M1 arc start, M2 arc start, n1, n2)
   u64 *mrbase;           // [M] first record of each match
+  u32 *big;              // [nsrc] sources for the multi-block merge (st->nbig)
 };
 
 void launch_count(const LevelArgs &a, hipStream_t s);
@@ -138,7 +139,6 @@ struct MergeArgs {
   u32 *big;        // [nbig] level-local source indices
 };
 
-void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStream_t s);
 // Tile descriptors of the level (a.tiles), then the two tile merges: the
 // dense-table kernel (only when a.key_bits <= kDenseKeyBits) and the sort
 // kernel, which takes every tile the dense kernel did not merge.

@@ -798,15 +798,6 @@ __global__ void k_tile_sources(const u64 *roff, u32 nsrc, u64 R, u64 W, u64 ntil
 
 // ---------------------------------------------------------------------------
 // Multi-block path for sources of more than kMergeSmall records.
-__global__ void k_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st) {
-  const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  const u64 c = u < nsrc ? roff[u + 1] - roff[u] : 0;
-  const bool is_big = c > kMergeSmall;
-  wave_append(is_big, (u32)u, big, &st->nbig);
-  const u32 m = wave_max((u32)(is_big ? 0 : c));
-  if (lane_id() == 0 && m) atomicMax(&st->max_small, m);
-}
-
 __global__ void k_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt) {
   const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < nbig) bigcnt[i] = roff[big[i] + 1] - roff[big[i]];
@@ -1091,11 +1082,6 @@ __global__ void k_reset_level(Status *st, u64 *tstat) {
 }
 
 }  // namespace
-
-void launch_collect_big(const u64 *roff, u32 nsrc, u32 *big, Status *st, hipStream_t s) {
-  hipLaunchKernelGGL(k_collect_big, dim3((unsigned)ceil_div(nsrc, 256)), dim3(256), 0, s, roff,
-                     nsrc, big, st);
-}
 
 static u64 merge_grid(const MergeArgs &a) {
   const u64 g = ceil_div(a.R, a.window);
