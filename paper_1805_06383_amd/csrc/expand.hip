@@ -178,6 +178,46 @@ __device__ __forceinline__ Hit probe_one(const LevelArgs &a, const Ranges &r, bo
   return h;
 }
 
+// Wave-cooperative probe of short-list elements base + lane against the
+// longer list, both sorted with distinct symbols: 64-symbol chunks of the
+// longer list are loaded into the lanes (one coalesced load each) and
+// searched by a 6-step binary search over lane shuffles.  `lp` is the first
+// chunk start of the longer list that can still match; it only moves
+// forward, so the next call (the next 64 short elements) resumes there.
+// All arguments but idx-dependent ones are wave-uniform.
+__device__ __forceinline__ Hit wave_probe(const LevelArgs &a, const Ranges &r, bool one_short,
+                                          u32 base, u32 es, u32 &lp) {
+  const u32 *ssym = one_short ? a.c1.seg_sym : a.c2.seg_sym;
+  const u32 *lsym = one_short ? a.c2.seg_sym : a.c1.seg_sym;
+  const u32 le = one_short ? r.e2 : r.e1;
+  const u32 lane = lane_id();
+  const u32 idx = base + lane;
+  const bool valid = idx < es;
+  const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
+  const u32 smax = __shfl(sym, (int)(min(es - base, (u32)kWave) - 1), kWave);
+  u32 fpos = 0xffffffffu;
+  for (u32 c = lp; c < le; c += kWave) {
+    const u32 len = min(le - c, (u32)kWave);
+    const u32 lv = lane < len ? lsym[c + lane] : 0xffffffffu;
+    if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past the short chunk
+    u32 pos = 0;  // elements of the chunk below sym (at most 63: then lane 63 decides)
+#pragma unroll
+    for (u32 step = kWave / 2; step; step >>= 1) {
+      const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
+      pos = v < sym ? pos + step : pos;
+    }
+    const u32 at = __shfl(lv, (int)pos, kWave);
+    if (valid && at == sym) fpos = c + pos;
+    if (__shfl(lv, (int)(len - 1), kWave) >= smax) {  // later short symbols start in this chunk
+      lp = c;
+      break;
+    }
+    lp = c + kWave;
+  }
+  if (fpos == 0xffffffffu) return Hit{false, 0, 0};
+  return one_short ? Hit{true, idx, fpos} : Hit{true, fpos, idx};
+}
+
 // Wavefront per source (grid-stride over the wide list).
 __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
   __shared__ u32 s_max;
@@ -193,8 +233,9 @@ __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
     const u32 bs = one_short ? r.b1 : r.b2, es = one_short ? r.e1 : r.e2;
     u64 cnt = 0;
     u32 mc = 0;
+    u32 lp = one_short ? r.b2 : r.b1;
     for (u32 base = bs; base < es; base += kWave) {
-      const Hit h = probe_one(a, r, one_short, base + lane);
+      const Hit h = wave_probe(a, r, one_short, base, es, lp);
       if (h.found) {
         cnt += (u64)seg_len(a.c1.seg_off, h.s1) * seg_len(a.c2.seg_off, h.s2);
         ++mc;
@@ -277,8 +318,9 @@ __global__ __launch_bounds__(256) void k_emit_wide(LevelArgs a) {
     const bool one_short = (r.e1 - r.b1) <= (r.e2 - r.b2);
     const u32 bs = one_short ? r.b1 : r.b2, es = one_short ? r.e1 : r.e2;
     u64 k = a.moff[u], rb = a.roff[u];
+    u32 lp = one_short ? r.b2 : r.b1;
     for (u32 base = bs; base < es; base += kWave) {
-      const Hit h = probe_one(a, r, one_short, base + lane);
+      const Hit h = wave_probe(a, r, one_short, base, es, lp);
       const u64 prod = h.found ? (u64)seg_len(a.c1.seg_off, h.s1) * seg_len(a.c2.seg_off, h.s2) : 0;
       const u64 fm = __ballot(h.found);
       const u64 incl = wave_inclusive_sum(prod);
