@@ -29,6 +29,9 @@
 //   * Optional level cap L > 0: only pairs at BFS depth < L are expanded; pairs
 //     at depth L are kept as states without outgoing arcs.
 //   * Merging never crosses sources (the per-source reduction of Algorithm 2).
+//   * Without reduction (§4, the comparison of Table 2 against Table 3): every
+//     joined arc pair is its own composed arc with weight fl32(p1 * p2); the
+//     reachable states are the same.
 //
 // The merge per source uses an ordered map keyed by (r1, r2, a, c); the pair
 // to id map is an ordered map; nothing here is tuned for speed.
@@ -149,7 +152,26 @@ uint64_t expand_pair(const Lookup &L1, const Lookup &L2, uint32_t q1, uint32_t q
   return joined;
 }
 
-int compose(const oracle_fst *m1, const oracle_fst *m2, uint32_t max_levels, Result &res) {
+// All composed arcs leaving (q1, q2) without reduction: the same two nested
+// loops, each joined pair appended as it is found.
+struct Joined { uint32_t r1, r2, a, c; float w; };
+void expand_pair_unreduced(const Lookup &L1, const Lookup &L2, uint32_t q1, uint32_t q2,
+                           std::vector<Joined> &out) {
+  const oracle_fst *m1 = L1.m, *m2 = L2.m;
+  auto r1 = L1.out(q1);
+  for (const uint32_t *p = r1.first; p != r1.second; ++p) {
+    const uint32_t e1 = *p;
+    auto r2 = L2.out_reading(q2, m1->olabel[e1]);
+    for (const uint32_t *s = r2.first; s != r2.second; ++s) {
+      const uint32_t e2 = *s;
+      out.push_back({m1->dst[e1], m2->dst[e2], m1->ilabel[e1], m2->olabel[e2],
+                     m1->weight[e1] * m2->weight[e2]});
+    }
+  }
+}
+
+int compose(const oracle_fst *m1, const oracle_fst *m2, uint32_t max_levels, bool reduce,
+            Result &res) {
   if (!valid(m1) || !valid(m2)) return ORACLE_INVALID;
   if (m1->num_osyms != m2->num_isyms) return ORACLE_ALPHABET;
   const auto t0 = std::chrono::steady_clock::now();
@@ -168,6 +190,27 @@ int compose(const oracle_fst *m1, const oracle_fst *m2, uint32_t max_levels, Res
     A.pop_front();
     if (max_levels > 0 && res.depth[u] >= max_levels) continue;
     const auto q = res.pairs[u];
+    if (!reduce) {
+      std::vector<Joined> out;
+      expand_pair_unreduced(L1, L2, q.first, q.second, out);
+      res.premerge += out.size();
+      for (const Joined &j : out) {
+        const auto v = std::make_pair(j.r1, j.r2);
+        auto it = id.find(v);
+        uint32_t vid;
+        if (it == id.end()) {
+          vid = (uint32_t)res.pairs.size();
+          id.emplace(v, vid);
+          res.pairs.push_back(v);
+          res.depth.push_back(res.depth[u] + 1);
+          A.push_back(vid);
+        } else {
+          vid = it->second;
+        }
+        res.arcs.push_back({u, vid, j.a, j.c, j.w});
+      }
+      continue;
+    }
     std::map<ArcKey, double> acc;
     res.premerge += expand_pair(L1, L2, q.first, q.second, acc);
     for (const auto &kv : acc) {
@@ -210,7 +253,23 @@ int oracle_compose(const oracle_fst *m1, const oracle_fst *m2, uint32_t max_leve
   if (!handle) return ORACLE_INVALID;
   *handle = nullptr;
   Result *r = new Result();
-  const int rc = compose(m1, m2, max_levels, *r);
+  const int rc = compose(m1, m2, max_levels, true, *r);
+  if (rc != ORACLE_OK) {
+    delete r;
+    return rc;
+  }
+  *handle = r;
+  return ORACLE_OK;
+}
+
+// The same search without reduction: every joined arc pair is an arc of the
+// result (arcs of a source in join order).
+int oracle_compose_unreduced(const oracle_fst *m1, const oracle_fst *m2, uint32_t max_levels,
+                             void **handle) {
+  if (!handle) return ORACLE_INVALID;
+  *handle = nullptr;
+  Result *r = new Result();
+  const int rc = compose(m1, m2, max_levels, false, *r);
   if (rc != ORACLE_OK) {
     delete r;
     return rc;
@@ -266,7 +325,7 @@ int oracle_expand_pairs(const oracle_fst *m1, const oracle_fst *m2, uint64_t n,
   return ORACLE_OK;
 }
 
-// out[0..3] = number of states, merged arcs, joined (unmerged) arc pairs, BFS layers.
+// out[0..3] = number of states, arcs (merged unless unreduced), joined arc pairs, BFS layers.
 void oracle_counts(const void *handle, uint64_t *out) {
   const Result *r = static_cast<const Result *>(handle);
   out[0] = r->pairs.size();

@@ -67,6 +67,9 @@ def _load(path: Path | None = None) -> ctypes.CDLL:
     lib.oracle_compose.argtypes = [ctypes.POINTER(_Fst), ctypes.POINTER(_Fst), u32,
                                    ctypes.POINTER(vp)]
     lib.oracle_compose.restype = ctypes.c_int
+    lib.oracle_compose_unreduced.argtypes = [ctypes.POINTER(_Fst), ctypes.POINTER(_Fst), u32,
+                                             ctypes.POINTER(vp)]
+    lib.oracle_compose_unreduced.restype = ctypes.c_int
     lib.oracle_expand_pairs.argtypes = [ctypes.POINTER(_Fst), ctypes.POINTER(_Fst), u64,
                                         vp, vp, ctypes.POINTER(vp)]
     lib.oracle_expand_pairs.restype = ctypes.c_int
@@ -139,13 +142,17 @@ def _collect(lib, h) -> OracleResult:
     return OracleResult(q1, q2, fin, dep, src, dst, a, c, w, int(counts[2]), int(counts[3]), secs)
 
 
-def compose(m1, m2, max_levels: int = 0, lib_path: Path | None = None) -> OracleResult:
-    """Reachable composition m1 o m2 (max_levels = 0: no level cap)."""
+def compose(m1, m2, max_levels: int = 0, lib_path: Path | None = None,
+            reduce: bool = True) -> OracleResult:
+    """Reachable composition m1 o m2 (max_levels = 0: no level cap).  With
+    reduce=False every joined arc pair is its own arc (no merging of identical
+    arcs, the setting of the paper's Table 2)."""
     lib = _load(lib_path)
     s1, k1 = _as_struct(m1)
     s2, k2 = _as_struct(m2)
     h = ctypes.c_void_p()
-    rc = lib.oracle_compose(ctypes.byref(s1), ctypes.byref(s2), int(max_levels), ctypes.byref(h))
+    fn = lib.oracle_compose if reduce else lib.oracle_compose_unreduced
+    rc = fn(ctypes.byref(s1), ctypes.byref(s2), int(max_levels), ctypes.byref(h))
     del k1, k2
     if rc != 0:
         raise OracleError(_ERRORS.get(rc, f"oracle error {rc}"))

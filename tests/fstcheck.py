@@ -174,3 +174,83 @@ def path_weights(T, start, end_vec, length):
         nv = np.einsum("XYq,xyqr->XxYyr", v, T)
         v = nv.reshape(v.shape[0] * nin, v.shape[1] * nout, n)
     return v @ end_vec
+
+
+# ---------------------------------------------------------------------------
+# Composition without reduction (every joined arc pair is an arc)
+# ---------------------------------------------------------------------------
+
+def brute_force_unreduced(m1, m2, max_levels: int = 0) -> Plain:
+    """All-pairs join over Q1 x Q2 without merging identical arcs, trimmed to
+    the arcs of reachable, expanded pairs (textbook BFS on the pair graph).
+    Each arc keeps its own float32 product."""
+    by_in = defaultdict(list)
+    for e2 in range(m2.num_arcs):
+        by_in[int(m2.ilabel[e2])].append(e2)
+    joined = []
+    for e1 in range(m1.num_arcs):
+        for e2 in by_in.get(int(m1.olabel[e1]), ()):
+            joined.append(((int(m1.src[e1]), int(m2.src[e2])), (int(m1.dst[e1]), int(m2.dst[e2])),
+                           int(m1.ilabel[e1]), int(m2.olabel[e2]),
+                           np.float32(m1.weight[e1]) * np.float32(m2.weight[e2])))
+    succ = defaultdict(set)
+    for u, v, _, _, _ in joined:
+        succ[u].add(v)
+    s = (int(m1.start), int(m2.start))
+    depth = {s: 0}
+    dq = deque([s])
+    while dq:
+        u = dq.popleft()
+        if max_levels and depth[u] >= max_levels:
+            continue
+        for v in sorted(succ.get(u, ())):
+            if v not in depth:
+                depth[v] = depth[u] + 1
+                dq.append(v)
+    states = sorted(depth)
+    sid = {p: i for i, p in enumerate(states)}
+    expanded = {p for p, d in depth.items() if not max_levels or d < max_levels}
+    arcs = [j for j in joined if j[0] in expanded]
+    q1 = np.array([p[0] for p in states], np.uint32)
+    q2 = np.array([p[1] for p in states], np.uint32)
+    fin = np.array([int(m1.final[p[0]] and m2.final[p[1]]) for p in states], np.uint8)
+    return Plain(q1, q2, fin, np.array([sid[j[0]] for j in arcs], np.int64),
+                 np.array([sid[j[1]] for j in arcs], np.int64),
+                 np.array([j[2] for j in arcs], np.uint32), np.array([j[3] for j in arcs], np.uint32),
+                 np.array([j[4] for j in arcs], np.float32))
+
+
+@dataclass
+class Multiset:
+    states: np.ndarray   # [n, 2] sorted (q1, q2)
+    finals: np.ndarray   # accept flag per sorted state
+    rows: np.ndarray     # [m, 7] sorted (src q1, src q2, dst q1, dst q2, a, c, weight bits)
+
+
+def multiset_of(res) -> Multiset:
+    """Canonical form of a result whose arcs are a multiset: state ids replaced
+    by their pairs, arcs (with their weight bits) in sorted order."""
+    q1 = np.asarray(res.q1, np.int64)
+    q2 = np.asarray(res.q2, np.int64)
+    order = np.lexsort((q2, q1))
+    states = np.stack([q1[order], q2[order]], 1)
+    finals = np.asarray(res.final, np.uint8)[order]
+    src = np.asarray(res.src, np.int64)
+    dst = np.asarray(res.dst, np.int64)
+    wbits = np.asarray(res.w, np.float32).view(np.uint32).astype(np.int64)
+    rows = np.stack([q1[src], q2[src], q1[dst], q2[dst], np.asarray(res.a, np.int64),
+                     np.asarray(res.c, np.int64), wbits], 1) if len(src) else np.zeros((0, 7), np.int64)
+    rows = rows[np.lexsort(rows.T[::-1])] if len(rows) else rows
+    return Multiset(states, finals, rows)
+
+
+def assert_same_multiset(got: Multiset, ref: Multiset, what: str = ""):
+    """Identical states, accept flags and arc multisets, weights bit for bit
+    (each weight is one float32 product on both sides)."""
+    assert np.array_equal(got.states, ref.states), f"{what}: state sets differ"
+    assert np.array_equal(got.finals, ref.finals), f"{what}: accept flags differ"
+    assert got.rows.shape == ref.rows.shape, f"{what}: {len(got.rows)} arcs vs {len(ref.rows)}"
+    if not np.array_equal(got.rows, ref.rows):
+        i = int(np.argmax(np.any(got.rows != ref.rows, axis=1)))
+        raise AssertionError(f"{what}: arc multisets differ, first at sorted row {i}: "
+                             f"{got.rows[i]} vs {ref.rows[i]}")

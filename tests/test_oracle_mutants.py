@@ -108,3 +108,63 @@ def test_mutant_is_caught(name, mutant_dir):
     subprocess.run(["g++", *CXXFLAGS, "-o", str(out), str(src)], check=True)
     failed = run_pins(out)
     assert failed, f"planted mistake {name} passed every pin"
+
+
+# Planted mistakes in the composition without reduction; caught by its own
+# pins (brute force without merging, the one-state closed form).
+MUTANTS_UNREDUCED = {
+    # product with one factor dropped
+    "unreduced_dropped_factor": ("m1->weight[e1] * m2->weight[e2]});",
+                                 "m1->weight[e1] * 1.0f});"),
+    # identical arcs merged after all
+    "unreduced_merges": ("    if (!reduce) {", "    if (false) {"),
+    # every arc points back at its source
+    "unreduced_self_target": ("res.arcs.push_back({u, vid, j.a, j.c, j.w});",
+                              "res.arcs.push_back({u, u, j.a, j.c, j.w});"),
+    # output label from M2's input side
+    "unreduced_wrong_output": ("m1->ilabel[e1], m2->olabel[e2],\n", "m1->ilabel[e1], m2->ilabel[e2],\n"),
+}
+
+
+def run_pins_unreduced(lib):
+    from fstcheck import assert_same_multiset, brute_force_unreduced, multiset_of
+    failed = set()
+    for seed in range(12):
+        m1, m2 = _tiny(seed)
+        try:
+            got = oracle.compose(m1, m2, lib_path=lib, reduce=False)
+            assert_same_multiset(multiset_of(got), multiset_of(brute_force_unreduced(m1, m2)))
+        except (AssertionError, IndexError, ValueError):
+            failed.add("brute_force_unreduced")
+    rng = np.random.default_rng(6)
+    A = W.random_weights(rng, 12).reshape(3, 4)
+    B = W.random_weights(rng, 8).reshape(4, 2)
+    try:
+        r = oracle.compose(W.one_state_dense(A), W.one_state_dense(B), lib_path=lib, reduce=False)
+        assert r.num_arcs == 24
+        a, b, c = np.meshgrid(np.arange(3), np.arange(4), np.arange(2), indexing="ij")
+        want = np.stack([a.ravel(), c.ravel(), (A[a, b].astype(np.float32) * B[b, c].astype(
+            np.float32)).ravel().view(np.uint32)], 1).astype(np.int64)
+        have = np.stack([r.a, r.c, r.w.view(np.uint32)], 1).astype(np.int64)
+        assert np.array_equal(have[np.lexsort(have.T[::-1])], want[np.lexsort(want.T[::-1])])
+    except (AssertionError, IndexError, ValueError):
+        failed.add("closed_form_unreduced")
+    return failed
+
+
+def test_unmutated_copy_passes_unreduced(mutant_dir):
+    out = mutant_dir / "liboracle_clean_u.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(out), SRC], check=True)
+    assert run_pins_unreduced(out) == set()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_UNREDUCED))
+def test_unreduced_mutant_is_caught(name, mutant_dir):
+    old, new = MUTANTS_UNREDUCED[name]
+    text = open(SRC).read()
+    assert text.count(old) >= 1, f"mutation site for {name} not found"
+    src = mutant_dir / f"{name}.cpp"
+    src.write_text(text.replace(old, new))
+    out = mutant_dir / f"lib{name}.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(out), str(src)], check=True)
+    assert run_pins_unreduced(out), f"planted mistake {name} passed every pin"
