@@ -95,6 +95,14 @@ typedef struct fstc_opts {
   fstc_alloc_fn alloc;        /* NULL: hipMallocAsync                      */
   fstc_free_fn free;
   void *alloc_ctx;
+  uint32_t no_reduction;      /* nonzero: no merging of identical arcs --
+                                 every joined arc pair is an arc of the
+                                 result with weight p1 * p2 (the setting the
+                                 paper compares against in section 4, Table 2);
+                                 the states are the same, num_arcs equals
+                                 num_premerge_arcs and arcs keep no order
+                                 within a source                          */
+  uint32_t reserved;
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the

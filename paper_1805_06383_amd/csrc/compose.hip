@@ -258,7 +258,8 @@ void Composer::run(fstc_result *out) {
   Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
       bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
       stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A), tiles_e(&A), tiles_m(&A), tstart(&A),
-      mend(&A), sortlist(&A), tile_runs(&A), wcnt(&A), woff(&A), wtmp(&A), runsrc(&A);
+      mend(&A), sortlist(&A), tile_runs(&A), wcnt(&A), woff(&A), wtmp(&A), runsrc(&A),
+      newbits(&A);
 
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
@@ -295,8 +296,10 @@ void Composer::run(fstc_result *out) {
     mrbase.ensure(M * 8);
     rkey.ensure(R * rec_bytes);
     rw.ensure(R * 4);
-    temp.ensure(R * sizeof(uint4));
-    runsrc.ensure(R * 4);
+    if (!o.no_reduction) {
+      temp.ensure(R * sizeof(uint4));
+      runsrc.ensure(R * 4);
+    }
     tiles_e.ensure(ceil_div(R, kExpandTile) * sizeof(ExpandTile));
     // merge window: as wide as the largest small source allows (see level.hpp)
     const u64 max_small = std::max<u32>(1, hs->st.max_small);
@@ -338,11 +341,8 @@ void Composer::run(fstc_result *out) {
     ++write_launches;
     total_matches += M;
 
-    // (a6) merge identical arcs, claim new pairs
-    T.begin();
-    fill_u64(tstart.as<u64>(), 0, nsrc, s);
-    fill_u64(mend.as<u64>(), 0, nsrc, s);
-    fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
+    // (a6) merge identical arcs, claim new pairs (or, without reduction,
+    // keep every record as an arc)
     MergeArgs ma{};
     ma.rec_key = rkey.p;
     ma.rec_w = rw.as<float>();
@@ -374,52 +374,86 @@ void Composer::run(fstc_result *out) {
     ma.mend = mend.as<u64>();
     ma.st = dst;
     ma.big = big.as<u32>();
-    launch_tile_sources(ma, s);
-    T.end(kMerge);
-    if (key_bits <= kDenseKeyBits) {
-      T.begin();
-      launch_merge_dense(ma, s);
-      T.end(kMergeKernel);
-      ++merge_launches;
-    }
-    T.begin();
-    launch_merge_sort(ma, wide_keys, s);
-    T.end(kSortKernel);
-    ++sort_launches;
-    T.begin();
     u64 RB = 0;
-    if (nbig) {
-      bigcnt.ensure((u64)nbig * 8);
-      bigoff.ensure(((u64)nbig + 1) * 8);
-      launch_big_counts(roff.as<u64>(), big.as<u32>(), nbig, bigcnt.as<u64>(), s);
-      exclusive_scan(bigcnt.as<u64>(), bigoff.as<u64>(), nbig, stmp.p, s);
-      read_words(bigoff.as<u64>() + nbig, 1);
-      RB = hs->words[0];
-      big_records += RB;
-      merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, A, s);
-    }
-    launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
-    exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
-    launch_emit_tiles(ma, s);
-    {
-      const u64 nw = newlist_waves(ma, RB);
+    u32 nnew = 0;
+    u64 merged = 0;
+    if (!o.no_reduction) {
+      T.begin();
+      fill_u64(tstart.as<u64>(), 0, nsrc, s);
+      fill_u64(mend.as<u64>(), 0, nsrc, s);
+      fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
+      launch_tile_sources(ma, s);
+      T.end(kMerge);
+      if (key_bits <= kDenseKeyBits) {
+        T.begin();
+        launch_merge_dense(ma, s);
+        T.end(kMergeKernel);
+        ++merge_launches;
+      }
+      T.begin();
+      launch_merge_sort(ma, wide_keys, s);
+      T.end(kSortKernel);
+      ++sort_launches;
+      T.begin();
+      if (nbig) {
+        bigcnt.ensure((u64)nbig * 8);
+        bigoff.ensure(((u64)nbig + 1) * 8);
+        launch_big_counts(roff.as<u64>(), big.as<u32>(), nbig, bigcnt.as<u64>(), s);
+        exclusive_scan(bigcnt.as<u64>(), bigoff.as<u64>(), nbig, stmp.p, s);
+        read_words(bigoff.as<u64>() + nbig, 1);
+        RB = hs->words[0];
+        big_records += RB;
+        merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, A, s);
+      }
+      launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
+      exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
+      launch_emit_tiles(ma, s);
+      {
+        const u64 nw = newlist_waves(ma, RB);
+        wcnt.ensure(nw * 4);
+        woff.ensure((nw + 1) * 8);
+        wtmp.ensure(scan_temp_bytes(nw));
+        launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
+                       woff.as<u64>(), wtmp.p, s);
+      }
+      launch_merged_total(aoff.as<u64>() + nsrc, dst, tstat, s);
+      T.end(kMerge);
+      sync_status();
+
+      nnew = hs->st.nnew;
+      merged = hs->st.merged;
+      dense_records += hs->st.dense_records;
+      dense_runs += hs->st.dense_runs;
+      sort_runs += hs->st.sort_runs;
+    } else {
+      if (o.max_arcs && arcs + R > o.max_arcs)
+        throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");
+      const u64 na = arcs + R;
+      osrc.grow_keep(na * 4, arcs * 4);
+      odst.grow_keep(na * 4, arcs * 4);
+      oil.grow_keep(na * 4, arcs * 4);
+      ool.grow_keep(na * 4, arcs * 4);
+      ow.grow_keep(na * 4, arcs * 4);
+      T.begin();
+      const u64 nwords = hcap / 32;
+      newbits.ensure(nwords * 4);
+      fill_u32(newbits.as<u32>(), 0, nwords, s);
+      launch_unreduced(ma, wide_keys, newbits.as<u32>(), osrc.as<u32>() + arcs, odst.as<u32>() + arcs,
+                       oil.as<u32>() + arcs, ool.as<u32>() + arcs, ow.as<float>() + arcs, s);
+      const u64 nw = bitlist_waves(nwords);
       wcnt.ensure(nw * 4);
       woff.ensure((nw + 1) * 8);
       wtmp.ensure(scan_temp_bytes(nw));
-      launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
-                     woff.as<u64>(), wtmp.p, s);
+      launch_bitlist(newbits.as<u32>(), nwords, newlist.as<u32>(), newcap, wcnt.as<u32>(),
+                     woff.as<u64>(), wtmp.p, dst, s);
+      T.end(kMerge);
+      sync_status();
+      nnew = hs->st.nnew;
+      merged = R;
     }
-    launch_merged_total(aoff.as<u64>() + nsrc, dst, tstat, s);
-    T.end(kMerge);
-    sync_status();
-    const u32 nnew = hs->st.nnew;
-    const u64 merged = hs->st.merged;
-    dense_records += hs->st.dense_records;
-    dense_runs += hs->st.dense_runs;
-    sort_runs += hs->st.sort_runs;
     if (n_states + nnew > state_limit)
       throw Error(FSTC_ERR_CAPACITY, "reachable states exceed the state limit");
-    if (o.max_arcs && arcs + merged > o.max_arcs)
+    if (!o.no_reduction && o.max_arcs && arcs + merged > o.max_arcs)
       throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");
 
     // (a5) ids for the new pairs; (a7) append the level's arcs
@@ -440,7 +474,9 @@ void Composer::run(fstc_result *out) {
     }
     launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), sq1b.as<u32>(),
                   sq2b.as<u32>(), s);
-    if (merged) {
+    if (o.no_reduction) {
+      launch_fix_dst(odst.as<u32>() + arcs, merged, hvb.as<u32>(), s);
+    } else if (merged) {
       const u64 na = arcs + merged;
       osrc.grow_keep(na * 4, arcs * 4);
       odst.grow_keep(na * 4, arcs * 4);

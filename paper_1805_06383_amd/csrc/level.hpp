@@ -177,6 +177,20 @@ void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
 u64 newlist_waves(const MergeArgs &a, u64 RB);
 void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
                     void *scan_tmp, hipStream_t s);
+// Composition without reduction: every record of the level becomes an arc
+// (osrc.. at [0, R)), its target pair claimed in the visited table and each
+// new claim flagged in `newbits` (one bit per table slot, cleared by the
+// caller); odst receives table slots until launch_fix_dst maps them to ids.
+void launch_unreduced(const MergeArgs &a, bool wide_keys, u32 *newbits, u32 *osrc, u32 *odst,
+                      u32 *oil, u32 *ool, float *ow, hipStream_t s);
+// New-state list from the claim bitmap, in slot order (st->nnew = its
+// length).  wcnt: bitlist_waves(nwords) u32; woff: that + 1 u64; scan_tmp:
+// scan_temp_bytes(bitlist_waves(nwords)) bytes.
+u64 bitlist_waves(u64 nwords);
+void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, u64 *woff,
+                    void *scan_tmp, Status *st, hipStream_t s);
+// dst[k] = hvals[dst[k]] for k < n.
+void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
 void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);

@@ -964,6 +964,90 @@ __global__ void k_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcou
 }
 
 // ---------------------------------------------------------------------------
+// Composition without reduction (every joined arc pair is an arc).  Wave per
+// kUnredB * 64 consecutive records, lane-striped: a record's source by a
+// binary search within the sources of the wave's first and last record; its
+// part ranks back to (r1, a) and (r2, c); the target pair claimed in the
+// visited table (new claims set a bit of newbits, so the new-state list
+// needs no shared counter); the arc written with the table slot as target.
+constexpr int kUnredB = 4;
+
+template <class KT>
+__global__ __launch_bounds__(256) void k_unreduced(MergeArgs a, u32 *newbits, u32 *osrc,
+                                                   u32 *odst, u32 *oil, u32 *ool, float *ow) {
+  const u32 lane = lane_id();
+  const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const u64 wb = wv * (u64)(kWave * kUnredB);
+  if (wb >= a.R) return;
+  const u64 we = min(wb + (u64)(kWave * kUnredB), a.R);
+  u32 ul = 0;
+  if (lane < 2) ul = (u32)last_le<u64>(a.roff, a.nsrc, lane == 0 ? wb : we - 1);
+  const u32 u0 = __shfl(ul, 0, kWave), u1 = __shfl(ul, 1, kWave);
+  const KT *rk = static_cast<const KT *>(a.rec_key);
+  bool act[kUnredB];
+  u32 uu[kUnredB], slot[kUnredB];
+  u64 hk[kUnredB], r[kUnredB];
+  uint2 P1[kUnredB], P2[kUnredB];
+  float wt[kUnredB];
+  bool is_new[kUnredB];
+#pragma unroll
+  for (int i = 0; i < kUnredB; ++i) {
+    r[i] = wb + (u64)i * kWave + lane;
+    act[i] = r[i] < we;
+    const u64 rr = act[i] ? r[i] : wb;
+    uu[i] = u0 + (u32)last_le<u64>(a.roff + u0, (u64)(u1 - u0) + 1, rr);
+    const u64 key = (u64)rk[rr];
+    wt[i] = a.rec_w[rr];
+    const u32 q1 = a.sq1[a.lo + uu[i]], q2 = a.sq2[a.lo + uu[i]];
+    P1[i] = a.parts1[a.pbase1[q1] + (u32)(key >> a.b2)];
+    P2[i] = a.parts2[a.pbase2[q2] + (u32)(key & ((1ull << a.b2) - 1))];
+    hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
+  }
+  hash_insert_batch<kUnredB>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
+#pragma unroll
+  for (int i = 0; i < kUnredB; ++i) {
+    if (!act[i]) continue;
+    if (is_new[i]) atomicOr(&newbits[slot[i] >> 5], 1u << (slot[i] & 31));
+    osrc[r[i]] = a.lo + uu[i];
+    odst[r[i]] = slot[i];
+    oil[r[i]] = P1[i].y;
+    ool[r[i]] = P2[i].y;
+    ow[r[i]] = wt[i];
+  }
+}
+
+// Set bits of a bitmap as a list of bit indices in increasing order: wave w
+// takes words [64 w, 64 w + 64); pass 0 counts, pass 1 writes at woff[w].
+template <int PASS>
+__global__ __launch_bounds__(256) void k_bitlist(const u32 *bits, u64 nwords, u32 *wcnt,
+                                                 const u64 *woff, u32 *list, u64 cap, Status *st) {
+  const u32 lane = lane_id();
+  const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const u64 i = wv * kWave + lane;
+  if (wv * kWave >= nwords) return;
+  u32 word = i < nwords ? bits[i] : 0u;
+  const u32 c = __popc(word);
+  const u32 incl = wave_inclusive_sum(c);
+  if (!PASS) {
+    if (lane == kWave - 1) wcnt[wv] = incl;
+    return;
+  }
+  u64 pos = woff[wv] + incl - c;
+  while (word) {
+    const u32 b = __ffs(word) - 1;
+    word &= word - 1;
+    if (pos < cap) list[pos] = (u32)(i * 32 + b);
+    else set_error(&st->err, kErrNewList);
+    ++pos;
+  }
+}
+
+__global__ void k_fix_dst(u32 *dst, u64 n, const u32 *hvals) {
+  for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (u64)gridDim.x * blockDim.x)
+    dst[k] = hvals[dst[k]];
+}
+
+// ---------------------------------------------------------------------------
 __global__ void k_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1,
                                u32 *sq2, u32 *err) {
   bool is_new;
@@ -1146,6 +1230,37 @@ void merge_big(const MergeArgs &a, bool wide_keys, u32 nbig, const u64 *bigoff, 
   exclusive_scan(flags.as<u32>(), ridx.as<u32>(), RB, tmp.p, s);
   hipLaunchKernelGGL(k_big_reduce, dim3(g), dim3(256), 0, s, a, bigoff, RB, skey.as<u64>(),
                      sval.as<u32>(), flags.as<u32>(), ridx.as<u32>());
+}
+
+void launch_unreduced(const MergeArgs &a, bool wide_keys, u32 *newbits, u32 *osrc, u32 *odst,
+                      u32 *oil, u32 *ool, float *ow, hipStream_t s) {
+  if (a.R == 0) return;
+  const u64 nw = ceil_div(a.R, (u64)kWave * kUnredB);
+  const unsigned g = (unsigned)ceil_div(nw, 256 / kWave);
+  if (ceil_div(nw, 256 / kWave) >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
+  if (wide_keys)
+    hipLaunchKernelGGL(k_unreduced<u64>, dim3(g), dim3(256), 0, s, a, newbits, osrc, odst, oil, ool, ow);
+  else
+    hipLaunchKernelGGL(k_unreduced<u32>, dim3(g), dim3(256), 0, s, a, newbits, osrc, odst, oil, ool, ow);
+}
+
+u64 bitlist_waves(u64 nwords) { return ceil_div(std::max<u64>(nwords, 1), kWave); }
+
+void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, u64 *woff,
+                    void *scan_tmp, Status *st, hipStream_t s) {
+  const u64 nw = bitlist_waves(nwords);
+  const unsigned g = (unsigned)ceil_div(nw, 256 / kWave);
+  hipLaunchKernelGGL(k_bitlist<0>, dim3(g), dim3(256), 0, s, bits, nwords, wcnt, (const u64 *)nullptr,
+                     list, cap, st);
+  exclusive_scan(wcnt, woff, nw, scan_tmp, s);
+  hipLaunchKernelGGL(k_bitlist<1>, dim3(g), dim3(256), 0, s, bits, nwords, wcnt, (const u64 *)woff,
+                     list, cap, st);
+  hipLaunchKernelGGL(k_new_total, dim3(1), dim3(1), 0, s, (const u64 *)(woff + nw), st);
+}
+
+void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s) {
+  if (!n) return;
+  hipLaunchKernelGGL(k_fix_dst, dim3(grid1(n)), dim3(256), 0, s, dst, n, hvals);
 }
 
 void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1, u32 *sq2,
