@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--oracle-levels", type=int, default=0,
                     help="depth cap of the CPU-oracle sample (0: the whole workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-reduction", action="store_true",
+                    help="compose without merging identical arcs (every joined arc pair is an "
+                         "arc; the setting of the paper's Table 2)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB three times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -97,9 +100,9 @@ def algorithmic_bytes(st: dict, R: int) -> dict:
     }
 
 
-def cpu_baseline(m1, m2, levels: int) -> dict:
+def cpu_baseline(m1, m2, levels: int, reduce: bool = True) -> dict:
     import oracle
-    r = oracle.compose(m1, m2, max_levels=levels)
+    r = oracle.compose(m1, m2, max_levels=levels, reduce=reduce)
     return {
         "value": r.num_premerge / r.seconds,
         "unit": "arcs/s",
@@ -107,7 +110,7 @@ def cpu_baseline(m1, m2, levels: int) -> dict:
         "kind": "oracle",
         "sample": ((f"same workload with the breadth-first search capped at depth {levels}: "
                     if levels else "the whole workload: ") +
-                   f"{r.num_premerge} unmerged / {r.num_arcs} merged arcs, "
+                   f"{r.num_premerge} unmerged / {r.num_arcs} output arcs, "
                    f"{r.num_states} states, {r.seconds:.2f} s on 1 of {os.cpu_count()} host "
                    f"cores ({platform.processor() or platform.machine()}); value = unmerged arcs/s"),
         "post_merge_value": r.num_arcs / r.seconds,
@@ -142,7 +145,8 @@ def main():
     torch.cuda.synchronize()
 
     def step():
-        return fstc.fstc_compose(m1, m2, max_levels=args.max_levels)
+        return fstc.fstc_compose(m1, m2, max_levels=args.max_levels,
+                                 reduce=not args.no_reduction)
 
     for _ in range(args.warmup):
         r = step()
@@ -201,7 +205,9 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"config {args.config}: {WORKLOAD_NAMES[args.config]}, seed {args.seed}"
-                        + (f", depth cap {args.max_levels}" if args.max_levels else ""),
+                        + (f", depth cap {args.max_levels}" if args.max_levels else "")
+                        + (", without reduction (every joined arc pair kept)"
+                           if args.no_reduction else ""),
             "states": last.num_states,
             "premerge_arcs": R,
             "merged_arcs": merged,
@@ -215,7 +221,7 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels)
+        out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels, not args.no_reduction)
     print(json.dumps(out), flush=True)
 
 
