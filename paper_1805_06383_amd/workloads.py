@@ -246,10 +246,16 @@ def config4(seed: int = 0, nq: int = 1000, m: int = 64, nsym: int = 64,
 
 def config5(seed: int = 0, nq: int = 1_000_000, na: int = 20_000_000,
             alpha: float = 2.1, dmin: int = 4, dmax: int = 10_000,
-            ng: int = 100_000, nouter: int = 10_000, final_frac: float = 0.01):
+            ng: int = 100_000, nouter: int = 10_000, final_frac: float = 0.01,
+            hub_start: bool = True):
     """Large pair: power-law out-degree P(d) ~ d**-alpha on [dmin, dmax],
     adjusted uniformly to exactly ``na`` arcs; uniform targets; inner symbols
-    Zipf(1.0) over ``ng``; outer symbols uniform over ``nouter``; 1% accept."""
+    Zipf(1.0) over ``ng``; outer symbols uniform over ``nouter``; 1% accept.
+    The start state 0 is a state of largest out-degree (its label is swapped
+    with that state's), as the start of a language-model-like transducer is
+    its busiest state; with a typical start the two start states would share
+    no inner symbol and the composition would stop at one state.  With
+    hub_start=False state 0 keeps its generated arcs."""
     rng = np.random.default_rng(1000 * 5 + seed)
     dvals = np.arange(dmin, dmax + 1, dtype=np.float64)
     pd = dvals ** (-alpha)
@@ -266,6 +272,12 @@ def config5(seed: int = 0, nq: int = 1_000_000, na: int = 20_000_000,
         perm = rng.permutation(na)
         src = src[perm]
         dst = rng.integers(0, nq, na)
+        hub = int(np.argmax(np.bincount(src, minlength=nq)))
+        if hub and hub_start:  # relabel: the busiest state becomes state 0
+            relabel = np.arange(nq, dtype=np.int64)
+            relabel[[0, hub]] = [hub, 0]
+            src = relabel[src].astype(np.uint32)
+            dst = relabel[dst]
         inner = _zipf(rng, ng, 1.0, na)
         outer = rng.integers(0, nouter, na)
         w = random_weights(rng, na)

@@ -296,11 +296,35 @@ def test_config2_capped(fstc, cap):
 
 
 def test_config5_scaled(fstc):
-    m1, m2 = W.config5(0, nq=20_000, na=400_000, ng=2_000, nouter=200)
-    for cap in (2, 3):
+    """Scaled power-law pair (20k states, 400k arcs each, degrees up to 1000,
+    start states the busiest ones): full parity up to depth 3 (2.8M arcs)."""
+    m1, m2 = W.config5(0, nq=20_000, na=400_000, dmax=1000, ng=2_000, nouter=200)
+    for cap in (1, 2, 3):
         g = run_gpu(fstc, m1, m2, max_levels=cap)
         check_structure(g, m1, m2)
         compare(g, oracle.compose(m1, m2, max_levels=cap), f"config5 scaled cap {cap}")
+
+
+_CFG5 = {}
+
+
+def config5_full():
+    """The full-size power-law pair (1M states, 20M arcs each), generated once."""
+    if not _CFG5:
+        _CFG5["m"] = W.config5(0)
+    return _CFG5["m"]
+
+
+@pytest.mark.timeout(600)
+def test_config5_full_cap2(fstc):
+    """Full-size power-law pair capped at depth 2: 5M states, the root a
+    948k-arc source on the multi-block merge path; full parity."""
+    m1, m2 = config5_full()
+    g = run_gpu(fstc, m1, m2, max_levels=2)
+    check_structure(g, m1, m2)
+    ref = oracle.compose(m1, m2, max_levels=2)
+    compare(g, ref, "config5 full cap 2")
+    _CFG5["cap2_states"] = ref.num_states
 
 
 def sampled_sources(fstc, g, m1, m2, k, seed):
@@ -357,6 +381,23 @@ def test_config4_full_sampled(fstc):
     assert np.array_equal(got, ref_states)
     assert g.num_premerge == 1024 * g.num_states  # every state expands 64 x 4 x 4
     sampled_sources(fstc, g, m1, m2, 300, seed=4)
+
+
+@pytest.mark.timeout(600)
+def test_config5_full_cap4_sampled(fstc):
+    """Full-size power-law pair capped at depth 4 (about 1e8 joined arc
+    pairs): structure, the depth <= 2 states as the first ids (the cap-2
+    result), and 300 sampled sources against the oracle's expansion."""
+    m1, m2 = config5_full()
+    g = run_gpu(fstc, m1, m2, max_levels=4)
+    check_structure(g, m1, m2)
+    g2 = run_gpu(fstc, m1, m2, max_levels=2)
+    n2 = g2.num_states
+    a = np.sort(g.q1[:n2].astype(np.uint64) << np.uint64(32) | g.q2[:n2])
+    b = np.sort(g2.q1.astype(np.uint64) << np.uint64(32) | g2.q2)
+    assert np.array_equal(a, b), "depth <= 2 states differ from the cap-2 run"
+    assert g.num_premerge > 5 * g2.num_premerge
+    sampled_sources(fstc, g, m1, m2, 300, seed=5)
 
 
 @pytest.mark.timeout(600)

@@ -73,4 +73,9 @@ def test_config5_scaled_shape():
         assert m.num_arcs == 400_000
         deg = np.bincount(m.src, minlength=m.num_states)
         assert deg.max() > 200  # heavy tail
+        assert deg[0] == deg.max()  # the start is a busiest state
         assert int(m.final.sum()) == 200
+    p1, p2 = W.config5(0, nq=20_000, na=400_000, ng=2_000, nouter=200, hub_start=False)
+    # the relabelling only swaps state 0 with the busiest state
+    assert np.array_equal(np.sort(np.bincount(p1.src, minlength=20_000)),
+                          np.sort(np.bincount(m1.src, minlength=20_000)))
