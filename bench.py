@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--no-reduction", action="store_true",
                     help="compose without merging identical arcs (every joined arc pair is an "
                          "arc; the setting of the paper's Table 2)")
+    ap.add_argument("--paper-pair", default="",
+                    help="SIZE-TARGET, e.g. 15k-de: instead of --config, the bigram-LM x "
+                         "translation-model pair German -> English -> TARGET at a Table 1 size")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB three times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -139,7 +142,17 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3}), file=sys.stderr, flush=True)
         del a_, b_
-    h1, h2 = W.make_config(args.config, args.seed)
+    if args.paper_pair:
+        size, target = args.paper_pair.split("-")
+        h1, h2 = W.paper_pair(size, target, args.seed)
+        workload = (f"bigram-LM x translation-model pair, Table 1 size {size}, German -> English "
+                    f"-> {target} ({h1.num_states} / {h2.num_states} states, {h1.num_arcs} / "
+                    f"{h2.num_arcs} arcs), seed {args.seed}")
+        traffic_key = None
+    else:
+        h1, h2 = W.make_config(args.config, args.seed)
+        workload = f"config {args.config}: {WORKLOAD_NAMES[args.config]}, seed {args.seed}"
+        traffic_key = "config%d" % args.config
     m1 = fstc.DeviceFST.from_host(h1, dev)
     m2 = fstc.DeviceFST.from_host(h2, dev)
     torch.cuda.synchronize()
@@ -187,8 +200,9 @@ def main():
     roof = {"bound": "hbm", "kernel": kname,
             "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": kern[dom]["GBps"] / HBM_PEAK_GBS,
-            "traffic": (recorded_traffic(kname, f"config{args.config}")
-                        if not args.max_levels else None)}
+            "traffic": (recorded_traffic(kname, traffic_key)
+                        if traffic_key and not args.max_levels and not args.no_reduction
+                        else None)}
 
     out = {
         "metric": METRIC,
@@ -204,7 +218,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"config {args.config}: {WORKLOAD_NAMES[args.config]}, seed {args.seed}"
+            "workload": workload
                         + (f", depth cap {args.max_levels}" if args.max_levels else "")
                         + (", without reduction (every joined arc pair kept)"
                            if args.no_reduction else ""),

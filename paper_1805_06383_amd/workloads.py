@@ -33,7 +33,7 @@ import numpy as np
 __all__ = [
     "FST", "random_weights", "tiny_random", "config1", "config2", "config3",
     "config4", "config5", "make_config", "identity", "one_state_dense",
-    "CONFIG_NAMES",
+    "CONFIG_NAMES", "PAPER_SHAPES", "lm_tm", "paper_pair",
 ]
 
 CONFIG_NAMES = {
@@ -287,6 +287,94 @@ def config5(seed: int = 0, nq: int = 1_000_000, na: int = 20_000_000,
         return FST(nq, 0, ng, nouter, src, dst, inner, outer, w, fin, name=name)
 
     return one(True, "cfg5.M1"), one(False, "cfg5.M2")
+
+
+# ---------------------------------------------------------------------------
+# Transducers shaped like the paper's own (§4.1, Figure 3): a bigram language
+# model over the output language pre-composed with a one-state translation
+# model, so that a state is the last output word (plus a sentence-start
+# state) and an arc e' -f:e-> e reads a source word f that translates to the
+# output word e.  Sizes follow Table 1, reading its "Transitions" column as
+# |Q|^2 (so |Q| = sqrt(Transitions)) and "Nonzero" as the number of arcs.
+# The Europarl-trained models themselves are not available; every statistic
+# below (Zipf word frequencies, successor counts, translation counts, weights)
+# is drawn synthetically.
+PAPER_SHAPES = {  # size -> language pair -> (states, arcs)
+    "1k": {"de-en": (4658, 16_500), "en-de": (3507, 15_400), "en-es": (3536, 15_500),
+           "en-it": (3619, 16_300)},
+    "10k": {"de-en": (19849, 114_000), "en-de": (11747, 93_900), "en-es": (11619, 93_300),
+            "en-it": (11958, 97_200)},
+    "15k": {"de-en": (25179, 158_000), "en-de": (14177, 126_000), "en-es": (13964, 125_000),
+            "en-it": (14457, 131_000)},
+}
+
+
+def lm_tm(rng: np.random.Generator, v_in: int, v_out: int, n_arcs: int,
+          final_frac: float = 0.3, name: str = "") -> FST:
+    """Bigram-LM x one-state-TM transducer from v_in source words to v_out
+    output words with exactly n_arcs arcs.
+
+    State 0 is the sentence start, state 1 + e the context "last output word
+    was e".  Output words have Zipf(1.0) frequencies; each has 1 + Poisson(1)
+    distinct translations drawn by Zipf(1.0) over the source words.  Each
+    context has a successor set of output words (the sentence start a large
+    one, a word context one growing with the word's frequency), drawn by
+    frequency; every (context, successor e, translation f of e) is an arc
+    context -f:e-> 1 + e with weight P(e | context) * P(f | e), both factors
+    normalised random weights.  The arc list is then cut or topped up
+    uniformly to exactly n_arcs."""
+    nq = v_out + 1
+    # translations of every output word
+    ntr = 1 + rng.poisson(1.0, v_out)
+    tr_word = np.repeat(np.arange(v_out), ntr)
+    tr_src = _zipf(rng, v_in, 1.0, int(ntr.sum()))
+    tr_p = random_weights(rng, len(tr_word)).astype(np.float64)
+    tr_p /= np.bincount(tr_word, weights=tr_p, minlength=v_out)[tr_word]
+    # successor sets: about n_arcs / mean(translations) (context, word) pairs
+    n_bigrams = int(np.ceil(n_arcs / ntr.mean()))
+    rank_w = 1.0 / np.arange(1, v_out + 1)  # Zipf(1.0) frequency of word ranks
+    ctx_w = np.r_[0.05 * rank_w.sum(), rank_w]  # the sentence start: about 5% of contexts
+    ctx = rng.choice(nq, size=n_bigrams, p=ctx_w / ctx_w.sum())
+    nxt = _zipf(rng, v_out, 1.0, n_bigrams)
+    bg = np.unique(np.stack([ctx, nxt], 1), axis=0)
+    bg_p = random_weights(rng, len(bg)).astype(np.float64)
+    bg_p /= np.bincount(bg[:, 0], weights=bg_p, minlength=nq)[bg[:, 0]]
+    # arcs = bigram x translation of its word
+    order = np.argsort(tr_word, kind="stable")
+    first = np.r_[0, np.cumsum(ntr)]
+    cnt = ntr[bg[:, 1]]
+    rep = np.repeat(np.arange(len(bg)), cnt)
+    k = np.arange(len(rep)) - np.repeat(np.cumsum(cnt) - cnt, cnt)  # translation index
+    t = order[first[bg[rep, 1]] + k]
+    src = bg[rep, 0]
+    out = bg[rep, 1]
+    w = (bg_p[rep] * tr_p[t]).astype(np.float32)
+    inp = tr_src[t]
+    if len(src) > n_arcs:
+        keep = np.sort(rng.choice(len(src), size=n_arcs, replace=False))
+        src, out, inp, w = src[keep], out[keep], inp[keep], w[keep]
+    elif len(src) < n_arcs:
+        extra = rng.integers(0, len(src), n_arcs - len(src))
+        src, out, inp, w = (np.r_[src, src[extra]], np.r_[out, out[extra]],
+                            np.r_[inp, inp[extra]], np.r_[w, w[extra]])
+    return FST(nq, 0, v_in, v_out, src, 1 + out, inp, out, w, _finals(rng, nq, final_frac),
+               name=name)
+
+
+def paper_pair(size: str = "1k", target: str = "de", seed: int = 0):
+    """(M1, M2) = (German-to-English, English-to-target) transducers of the
+    paper's experiment at one of its three training sizes (Table 1), for the
+    composition German -> target.  M1's output alphabet is M2's input
+    alphabet (the English words)."""
+    shapes = PAPER_SHAPES[size]
+    q_en, arcs1 = shapes["de-en"]
+    q_de = shapes["en-de"][0]
+    q_t, arcs2 = shapes[f"en-{target}"]
+    rng = np.random.default_rng(6000 + 100 * list(PAPER_SHAPES).index(size)
+                                + 10 * ["de", "es", "it"].index(target) + seed)
+    m1 = lm_tm(rng, q_de - 1, q_en - 1, arcs1, name=f"{size}.de-en")
+    m2 = lm_tm(rng, q_en - 1, q_t - 1, arcs2, name=f"{size}.en-{target}")
+    return m1, m2
 
 
 def make_config(cfg: int, seed: int = 0):

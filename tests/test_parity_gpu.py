@@ -295,6 +295,19 @@ def test_config2_capped(fstc, cap):
     compare(g, oracle.compose(m1, m2, max_levels=cap), f"config2 cap {cap}")
 
 
+@pytest.mark.parametrize("size", ["1k", "10k", "15k"])
+@pytest.mark.parametrize("target", ["de", "es", "it"])
+def test_paper_pairs(fstc, size, target):
+    """Bigram-LM x one-state-TM pairs shaped like the paper's experiment
+    (German -> English -> target, Table 1 sizes): full parity."""
+    m1, m2 = W.paper_pair(size, target)
+    g = run_gpu(fstc, m1, m2)
+    check_structure(g, m1, m2)
+    ref = oracle.compose(m1, m2)
+    compare(g, ref, f"paper pair {size} {target}")
+    ids_follow_depth(g, ref)
+
+
 def test_config5_scaled(fstc):
     """Scaled power-law pair (20k states, 400k arcs each, degrees up to 1000,
     start states the busiest ones): full parity up to depth 3 (2.8M arcs)."""

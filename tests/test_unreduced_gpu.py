@@ -77,6 +77,12 @@ def test_unreduced_workloads(fstc, cfg, cap):
     compare(fstc, m1, m2, f"config{cfg} cap {cap}", max_levels=cap)
 
 
+@pytest.mark.parametrize("size,target", [("1k", "de"), ("15k", "it")])
+def test_unreduced_paper_pairs(fstc, size, target):
+    m1, m2 = W.paper_pair(size, target)
+    compare(fstc, m1, m2, f"paper pair {size} {target}")
+
+
 def test_unreduced_degenerate(fstc):
     rng = np.random.default_rng(4)
     empty1 = W.tiny_random(rng, 3, 2, 2, 0)

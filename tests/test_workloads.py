@@ -1,5 +1,6 @@
 """Shape checks of the seeded synthetic workloads (no GPU)."""
 import numpy as np
+import pytest
 
 from paper_1805_06383_amd import workloads as W
 
@@ -79,3 +80,22 @@ def test_config5_scaled_shape():
     # the relabelling only swaps state 0 with the busiest state
     assert np.array_equal(np.sort(np.bincount(p1.src, minlength=20_000)),
                           np.sort(np.bincount(m1.src, minlength=20_000)))
+
+
+@pytest.mark.parametrize("size", ["1k", "10k", "15k"])
+@pytest.mark.parametrize("target", ["de", "es", "it"])
+def test_paper_pair_shape(size, target):
+    """Bigram-LM x one-state-TM pairs at the sizes of Table 1."""
+    m1, m2 = W.paper_pair(size, target)
+    for m in (m1, m2):
+        _check(m)
+        # an arc's target is the state of its output word (state 0: sentence start)
+        assert np.array_equal(m.dst, 1 + m.olabel)
+        assert m.num_states == m.num_osyms + 1
+    shapes = W.PAPER_SHAPES[size]
+    assert (m1.num_states, m1.num_arcs) == shapes["de-en"]
+    assert (m2.num_states, m2.num_arcs) == shapes[f"en-{target}"]
+    assert m1.num_osyms == m2.num_isyms  # English words join the two
+    assert m1.num_isyms == shapes["en-de"][0] - 1  # German source words
+    # sparse as in Table 1: arcs are a small fraction of |Q|^2
+    assert m1.num_arcs < 0.01 * m1.num_states ** 2
