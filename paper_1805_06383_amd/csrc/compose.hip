@@ -69,6 +69,35 @@ void *Buf::grow_keep(size_t bytes, size_t used) {
   return p;
 }
 
+void *Arena::take(size_t bytes) {
+  bytes = std::max<size_t>(256, (bytes + 255) & ~(size_t)255);
+  if (chunks.empty() || used + bytes > chunks.back().cap) {
+    const size_t c = std::max<size_t>(bytes, chunks.empty() ? (size_t)1 << 20 : 2 * chunks.back().cap);
+    chunks.push_back({static_cast<char *>(A->alloc(c)), c});
+    used = 0;
+  }
+  void *p = chunks.back().p + used;
+  used += bytes;
+  return p;
+}
+
+void Arena::reset() {
+  ++epoch;
+  if (chunks.size() > 1) {
+    size_t total = 0;
+    for (auto &c : chunks) total += c.cap;
+    release();
+    chunks.push_back({static_cast<char *>(A->alloc(total)), total});
+  }
+  used = 0;
+}
+
+void Arena::release() {
+  for (auto &c : chunks) A->free(c.p, c.cap);
+  chunks.clear();
+  used = 0;
+}
+
 namespace {
 
 thread_local std::string g_detail;
@@ -218,8 +247,12 @@ void Composer::run(fstc_result *out) {
   alloc_csr(m1, A, cb1, c1);
   alloc_csr(m2, A, cb2, c2);
   T.begin();
-  build_csr(m1, true, A, c1, dcounts + 0, &dst->err, s);
-  build_csr(m2, false, A, c2, dcounts + 3, &dst->err, s);
+  {
+    Arena csr_tmp(&A);
+    build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
+    csr_tmp.reset();
+    build_csr(m2, false, csr_tmp, c2, dcounts + 3, &dst->err, s);
+  }
   T.end(kCsr);
   sync_status();
   read_words(dcounts, 6);
@@ -255,16 +288,22 @@ void Composer::run(fstc_result *out) {
   u64 dense_records = 0, dense_runs = 0, sort_runs = 0;
 
   Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
-  Buf cnt(&A), mc(&A), roff(&A), moff(&A), mcount(&A), aoff(&A), wide(&A), heavy(&A), big(&A),
-      bigcnt(&A), bigoff(&A), match(&A), mrbase(&A), rkey(&A), rw(&A), temp(&A), newlist(&A),
-      stmp(&A), dk(&A), dv(&A), dka(&A), dva(&A), dtmp(&A), tiles_e(&A), tiles_m(&A), tstart(&A),
-      mend(&A), sortlist(&A), tile_runs(&A), wcnt(&A), woff(&A), wtmp(&A), runsrc(&A),
-      newbits(&A);
+  // per-level temporaries, carved from one arena reset at every level
+  Arena level_tmp(&A);
+  Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
+      aoff(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
+      rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
+      dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
+      tiles_e(&level_tmp), tiles_m(&level_tmp), tstart(&level_tmp), mend(&level_tmp),
+      sortlist(&level_tmp), tile_runs(&level_tmp), wcnt(&level_tmp), woff(&level_tmp),
+      wtmp(&level_tmp), runsrc(&level_tmp), newbits(&level_tmp);
 
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
     const u32 nsrc = hi - lo;
     if (nsrc == 0) break;
+    level_tmp.reset();
     ++expanded_levels;
     max_frontier = std::max<u64>(max_frontier, nsrc);
     const u64 np1 = (u64)nsrc + 1;
@@ -403,7 +442,7 @@ void Composer::run(fstc_result *out) {
         read_words(bigoff.as<u64>() + nbig, 1);
         RB = hs->words[0];
         big_records += RB;
-        merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, A, s);
+        merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, level_tmp, s);
       }
       launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
       exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
@@ -670,7 +709,10 @@ int fstc_build_csr(const fstc_fst *m, int by_output, hipStream_t stream, uint32_
     u64 *d_counts = (u64 *)dc.ensure(3 * 8);
     u32 *d_err = (u32 *)de.ensure(4);
     fill_u32(d_err, 0, 1, stream);
-    build_csr(*m, by_output != 0, A, c, d_counts, d_err, stream);
+    {
+      Arena tmp(&A);
+      build_csr(*m, by_output != 0, tmp, c, d_counts, d_err, stream);
+    }
     if (n) {
       const unsigned g = (unsigned)std::min<u64>(ceil_div(n, 256), 1u << 16);
       hipLaunchKernelGGL(k_split_uint2, dim3(g), dim3(256), 0, stream, c.arcs, n, arc_part,

@@ -128,7 +128,7 @@ void alloc_csr(const fstc_fst &m, Allocator &A, Buf *b, Csr &c) {
   c.parts = (uint2 *)b[5].ensure(std::max<u64>(n, 1) * sizeof(uint2));
 }
 
-void build_csr(const fstc_fst &m, bool by_output, Allocator &A, const Csr &c, u64 *d_counts,
+void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d_counts,
                u32 *d_err, hipStream_t s) {
   check_csr_ranges(m, by_output);
   const u64 n = m.num_arcs;
@@ -146,8 +146,8 @@ void build_csr(const fstc_fst &m, bool by_output, Allocator &A, const Csr &c, u6
   const int bi = (int)bits_for(ninner ? ninner - 1 : 0);
   const int bo = (int)bits_for(nouter ? nouter - 1 : 0);
 
-  Buf kp(&A), kc(&A), v1(&A), v2(&A), kalt(&A), valt(&A), flags(&A), ex(&A), apg(&A),
-      pstate(&A), sstate(&A), tmp(&A);
+  Tmp kp(&T), kc(&T), v1(&T), v2(&T), kalt(&T), valt(&T), flags(&T), ex(&T), apg(&T),
+      pstate(&T), sstate(&T), tmp(&T);
   kp.ensure(n * 8); kc.ensure(n * 8); v1.ensure(n * 4); v2.ensure(n * 4);
   kalt.ensure(n * 8); valt.ensure(n * 4);
   flags.ensure(n * 4); ex.ensure((n + 1) * 4); apg.ensure(n * 4);

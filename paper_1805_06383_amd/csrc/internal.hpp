@@ -1,6 +1,8 @@
 // Internal interfaces between the translation units of libfstc.
 #pragma once
 
+#include <vector>
+
 #include "common.hpp"
 
 namespace fstc {
@@ -52,6 +54,50 @@ struct Buf {
   }
 };
 
+// Bump allocator for temporaries that die together (one breadth-first level,
+// one CSR build): takes from its last chunk and adds a chunk at least twice
+// as large when that is full; reset() frees every chunk and, when there were
+// several, keeps one as large as all of them, so that after the first rounds
+// a round costs no allocator call.  Frees are stream ordered (like Buf), so
+// a reset while kernels still read the old chunks is safe.
+struct Arena {
+  Allocator *A = nullptr;
+  struct Chunk {
+    char *p;
+    size_t cap;
+  };
+  std::vector<Chunk> chunks;
+  size_t used = 0;
+  u64 epoch = 0;  // incremented by reset(): handles from older rounds are stale
+
+  explicit Arena(Allocator *a) : A(a) {}
+  Arena(const Arena &) = delete;
+  Arena &operator=(const Arena &) = delete;
+  ~Arena() { release(); }
+  void *take(size_t bytes);
+  void reset();
+  void release();
+};
+
+// A buffer of the current round of an Arena, with Buf's interface.
+struct Tmp {
+  Arena *T = nullptr;
+  void *p = nullptr;
+  u64 epoch = 0;
+
+  explicit Tmp(Arena *t) : T(t) {}
+  void *ensure(size_t bytes) {
+    p = T->take(bytes);
+    epoch = T->epoch;
+    return p;
+  }
+  template <class X>
+  X *as() const {
+    if (p && epoch != T->epoch) throw Error(FSTC_ERR_INTERNAL, "stale arena buffer");
+    return static_cast<X *>(p);
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Two-level (state, inner symbol) layout of one input transducer.
 struct Csr {
@@ -67,7 +113,7 @@ struct Csr {
 
 // Device counters written by the CSR build: [0] segments, [1] parts,
 // [2] max parts of one state.
-void build_csr(const fstc_fst &m, bool by_output, Allocator &A, const Csr &out, u64 *d_counts,
+void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &out, u64 *d_counts,
                u32 *d_err, hipStream_t s);
 
 // Checks the packing limits of build_csr for one transducer; throws

@@ -149,7 +149,7 @@ void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s);
 // entries (exclusive scan of their record counts, total RB).
 void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s);
 void merge_big(const MergeArgs &a, bool wide_keys, u32 nbig, const u64 *bigoff, u64 RB,
-               Allocator &A, hipStream_t s);
+               Arena &T, hipStream_t s);
 
 void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1, u32 *sq2,
                          u32 *err, hipStream_t s);

@@ -1208,9 +1208,9 @@ void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, h
 }
 
 void merge_big(const MergeArgs &a, bool wide_keys, u32 nbig, const u64 *bigoff, u64 RB,
-               Allocator &A, hipStream_t s) {
+               Arena &T, hipStream_t s) {
   if (nbig == 0 || RB == 0) return;
-  Buf skey(&A), sval(&A), kalt(&A), valt(&A), flags(&A), ridx(&A), tmp(&A);
+  Tmp skey(&T), sval(&T), kalt(&T), valt(&T), flags(&T), ridx(&T), tmp(&T);
   skey.ensure(RB * 8); sval.ensure(RB * 4); kalt.ensure(RB * 8); valt.ensure(RB * 4);
   flags.ensure(RB * 4); ridx.ensure((RB + 1) * 4);
   tmp.ensure(std::max(radix_temp_bytes(RB), scan_temp_bytes(RB)));
