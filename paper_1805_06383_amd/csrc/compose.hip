@@ -316,7 +316,7 @@ void Composer::run(fstc_result *out) {
     launch_reset_level(dst, tstat, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
-                 dst, nullptr, nullptr, big.as<u32>()};
+                 dst, nullptr, nullptr, nullptr, big.as<u32>()};
     T.begin();
     launch_count(la, s);
     exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
@@ -370,6 +370,7 @@ void Composer::run(fstc_result *out) {
     // (a4) match descriptors and the arc-pair write pass
     la.match = match.as<uint4>();
     la.mrbase = mrbase.as<u64>();
+    la.tiles = tiles_e.as<ExpandTile>();
     T.begin();
     launch_emit(la, s);
     T.end(kExpand);

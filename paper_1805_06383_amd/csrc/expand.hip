@@ -292,6 +292,10 @@ __device__ __forceinline__ void put_match(const LevelArgs &a, u64 k, u32 s1, u32
   const u32 a2 = a.c2.seg_off[s2], n2 = a.c2.seg_off[s2 + 1] - a2;
   a.match[k] = make_uint4(a1, a2, n1, n2);
   a.mrbase[k] = rbase;
+  // entries of the write tiles whose first record lies in this match
+  const u64 end = rbase + (u64)n1 * n2;
+  for (u64 t = (rbase + kExpandTile - 1) / kExpandTile; t * kExpandTile < end; ++t)
+    a.tiles[t] = ExpandTile{k, rbase};
 }
 
 __global__ __launch_bounds__(256) void k_emit_small(LevelArgs a) {
@@ -433,15 +437,23 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   const u64 g0 = (u64)blockIdx.x * kExpandGroup;
   const u64 ng = min(kExpandGroup, ntiles - g0);
   const u64 r0 = g0 * kExpandTile;
-  const ExpandTile ta = tiles[g0], tb = tiles[g0 + ng - 1];
+  // matches of tile t: k0(t) .. kend(t) - 1
+  auto kend_of = [&](u64 t) -> u64 {
+    if (t + 1 >= ntiles) return M;
+    const ExpandTile nx = tiles[t + 1];
+    return nx.base0 == (t + 1) * kExpandTile ? nx.k0 : nx.k0 + 1;
+  };
+  const ExpandTile ta = tiles[g0];
+  const u64 gend = kend_of(g0 + ng - 1);
   // one staging for the whole group when its matches fit, else per tile
-  const bool one = tb.kend - ta.k0 <= kExpandTile;
+  const bool one = gend - ta.k0 <= kExpandTile;
   const u32 passes = one ? 1u : (u32)ng;
   for (u32 pass = 0; pass < passes; ++pass) {
-    const ExpandTile ti = one ? ExpandTile{ta.k0, tb.kend, ta.base0, 0} : tiles[g0 + pass];
+    const ExpandTile ti = one ? ta : tiles[g0 + pass];
+    const u64 kend = one ? gend : kend_of(g0 + pass);
     const u64 rs = one ? r0 : r0 + pass * kExpandTile;  // record origin of s_rel
-    const u64 k0 = ti.k0, nm = ti.kend - ti.k0;
-    if (ti.kend <= k0 || ti.kend > M || nm > kExpandTile) {  // impossible: >= 1 record per match
+    const u64 k0 = ti.k0, nm = kend - ti.k0;
+    if (kend <= k0 || kend > M || nm > kExpandTile) {  // impossible: >= 1 record per match
       if (threadIdx.x == 0) set_error(err, kErrBounds);
       return;
     }
@@ -549,15 +561,6 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
   }
 }
 
-__global__ void k_tile_matches(const u64 *mrbase, u64 M, u64 R, u64 ntiles, ExpandTile *tiles) {
-  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t < ntiles; t += (u64)gridDim.x * blockDim.x) {
-    const u64 r0 = t * kExpandTile;
-    const u64 k0 = last_le<u64>(mrbase, M, r0);
-    tiles[t] = ExpandTile{k0, lower_bound_dev<u64>(mrbase, M, min(r0 + kExpandTile, R)),
-                          mrbase[k0], 0};
-  }
-}
-
 }  // namespace
 
 void launch_count(const LevelArgs &a, hipStream_t s) {
@@ -580,8 +583,6 @@ void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const Cs
   if (R == 0) return;
   const u64 g = ceil_div(R, kExpandTile);
   if (g >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "level too large for one launch");
-  const unsigned gs = (unsigned)std::min<u64>(ceil_div(g, 256), 1u << 20);
-  hipLaunchKernelGGL(k_tile_matches, dim3(gs), dim3(256), 0, s, mrbase, M, R, g, tiles);
   const unsigned gw = (unsigned)ceil_div(g, kExpandGroup);
   // 32-bit byte offsets into the arc arrays when both hold fewer than 2^29 arcs
   const bool narrow = std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29);

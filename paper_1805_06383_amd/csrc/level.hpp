@@ -77,11 +77,14 @@ constexpr int kExpandIT = 8;
 constexpr u64 kExpandTile = 2048;
 constexpr u64 kExpandGroup = kExpandNT * kExpandIT / kExpandTile;
 
-// Matches overlapping write tile t (records [t kExpandTile, ...)): k0 = the
-// last match starting at or before the tile, kend = the first match starting
-// at or after its end, base0 = first record of match k0.
+// Write tile t holds records [t kExpandTile, (t + 1) kExpandTile): k0 = the
+// match holding its first record, base0 = that match's first record.  The
+// emit kernels write the entries of the tiles whose first record falls in a
+// match they emit; the matches of tile t are k0(t) .. kend(t) - 1, kend(t)
+// following from entry t + 1 (k0(t + 1), plus one unless that match starts
+// exactly at the tile boundary; M for the last tile).
 struct ExpandTile {
-  u64 k0, kend, base0, pad;
+  u64 k0, base0;
 };
 
 struct LevelArgs {
@@ -96,6 +99,7 @@ struct LevelArgs {
   Status *st;
   uint4 *match;          // [M] (M1 arc start, M2 arc start, n1, n2)
   u64 *mrbase;           // [M] first record of each match
+  ExpandTile *tiles;     // [ceil(R / kExpandTile)] write-tile entries
   u32 *big;              // [nsrc] sources for the multi-block merge (st->nbig)
 };
 
@@ -103,7 +107,7 @@ void launch_count(const LevelArgs &a, hipStream_t s);
 void launch_emit(const LevelArgs &a, hipStream_t s);
 // Writes R records: key = (part1 << b2) | part2 (u32 when key_bits <= 32,
 // else u64), weight = p1 * p2.
-// tiles: scratch of ceil(R / kExpandTile) ExpandTile.
+// tiles: the ceil(R / kExpandTile) write-tile entries written by launch_emit.
 void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,
                    const CsrView &c2, int b2, bool wide_keys, void *rec_key, float *rec_w,
                    ExpandTile *tiles, u32 *err, hipStream_t s);
