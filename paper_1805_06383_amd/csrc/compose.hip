@@ -235,10 +235,9 @@ void Composer::run(fstc_result *out) {
   if (!o.alloc) tune_default_pool();
   hs = staging();
 
-  Buf stb(&A), cntb(&A), tstb(&A);
+  Buf stb(&A), cntb(&A);
   dst = (Status *)stb.ensure(sizeof(Status));
   u64 *dcounts = (u64 *)cntb.ensure(8 * sizeof(u64));
-  u64 *tstat = (u64 *)tstb.ensure(kStatWords * sizeof(u64));
   fill_u32((u32 *)dst, 0, sizeof(Status) / 4, s);
 
   // (a0) device layout of both inputs
@@ -313,7 +312,7 @@ void Composer::run(fstc_result *out) {
     stmp.ensure(scan_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
-    launch_reset_level(dst, tstat, s);
+    launch_reset_level(dst, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
                  dst, nullptr, nullptr, nullptr, big.as<u32>()};
@@ -407,7 +406,6 @@ void Composer::run(fstc_result *out) {
     ma.tiles = tiles_m.as<uint4>();
     ma.sortlist = sortlist.as<u32>();
     ma.tile_runs = tile_runs.as<u32>();
-    ma.tstat = tstat;
     ma.ntiles = ntiles;
     ma.window = window;
     ma.tstart = tstart.as<u64>();
@@ -456,7 +454,7 @@ void Composer::run(fstc_result *out) {
         launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
                        woff.as<u64>(), wtmp.p, s);
       }
-      launch_merged_total(aoff.as<u64>() + nsrc, dst, tstat, s);
+      launch_merged_total(aoff.as<u64>() + nsrc, ma, s);
       T.end(kMerge);
       sync_status();
 

@@ -37,14 +37,6 @@ struct Status {
   u32 pad;
 };
 
-// Per-tile counters are added into kStatSlots slots, one 128-byte line each
-// (a device-scope atomic on one shared address per tile serialises the
-// whole merge), and summed into Status once per level.
-constexpr int kStatSlots = 64;
-constexpr int kStatStride = 16;  // u64 per slot
-enum StatField { kStatDenseRecords, kStatDenseRuns, kStatSortRuns };
-constexpr size_t kStatWords = (size_t)kStatSlots * kStatStride;
-
 // A source whose shorter segment list is longer than kWideMin is joined by a
 // wavefront, longer than kHeavyMin by a workgroup; others by one thread.
 constexpr u32 kWideMin = 24;
@@ -133,7 +125,6 @@ struct MergeArgs {
   u64 *tstart;     // [nsrc] first temp slot of each source's merged arcs (0 if none)
   u64 *mend;       // [nsrc] one past its last slot (0 if none)
   u64 window;      // W: tile t takes the sources starting in [t W, (t + 1) W)
-  u64 *tstat;      // [kStatWords] per-tile counter slots
   uint4 *tiles;    // [ntiles = ceil(R / W)] scratch: tile descriptors
   u32 *sortlist;   // [ntiles] scratch: tiles left to the sort kernel
   u32 *tile_runs;  // [ntiles] merged runs each tile wrote (zero-filled before the merge)
@@ -198,8 +189,8 @@ void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
 void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);
-// Also sums the per-tile counter slots into st.
-void launch_merged_total(const u64 *a_total, Status *st, const u64 *tstat, hipStream_t s);
-void launch_reset_level(Status *st, u64 *tstat, hipStream_t s);
+// Level total of merged arcs, plus the dense / sort tile statistics of st.
+void launch_merged_total(const u64 *a_total, const MergeArgs &a, hipStream_t s);
+void launch_reset_level(Status *st, hipStream_t s);
 
 }  // namespace fstc

@@ -94,12 +94,6 @@ __device__ __forceinline__ bool dense_tile(const uint4 &td, int key_bits) {
          ((u64)(td.y - td.x) << key_bits) <= (u64)kDenseCap;
 }
 
-// Adds v to per-level counter f in the slot of this workgroup.
-__device__ __forceinline__ void add_stat(const MergeArgs &a, StatField f, u32 v) {
-  atomicAdd((unsigned long long *)&a.tstat[(blockIdx.x % kStatSlots) * kStatStride + f],
-            (unsigned long long)v);
-}
-
 // Exclusive prefix over the waves of the block of one value per wave (taken
 // from any lane); *total receives the block total.  All threads must call it.
 __device__ __forceinline__ u32 block_offset(u32 wave_value, u32 *s_tmp, u32 *total) {
@@ -482,10 +476,7 @@ __device__ __forceinline__ void merge_sort_tile(const MergeArgs &a, u32 tile, So
     if (first) a.tstart[u] = rb + r;
     if (last) a.mend[u] = rb + r + 1;
   }
-  if (threadIdx.x == 0) {
-    a.tile_runs[tile] = nruns;
-    add_stat(a, kStatSortRuns, nruns);
-  }
+  if (threadIdx.x == 0) a.tile_runs[tile] = nruns;
 }
 
 // Every tile of the level, one per workgroup.  XCD-aware tile order:
@@ -774,11 +765,7 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
     if (q == 0 || s_runseg[q - 1] != seg) a.tstart[u] = rb + q;
     if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
   }
-  if (threadIdx.x == 0) {
-    a.tile_runs[tile] = nruns;
-    add_stat(a, kStatDenseRecords, n);
-    add_stat(a, kStatDenseRuns, nruns);
-  }
+  if (threadIdx.x == 0) a.tile_runs[tile] = nruns;
 }
 
 // Descriptor of merge tile t: the small sources whose first record falls in
@@ -1138,24 +1125,41 @@ __global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st) {
   st->M = *mt;
 }
 
-// one wave: level total of merged arcs and of the per-tile counter slots
-__global__ void k_merged_total(const u64 *at, Status *st, const u64 *tstat) {
-  const u32 lane = lane_id();
-  const u64 *slot = tstat + (size_t)lane * kStatStride;
-  u64 v[3] = {slot[kStatDenseRecords], slot[kStatDenseRuns], slot[kStatSortRuns]};
-#pragma unroll
-  for (int f = 0; f < 3; ++f)
-    for (int d = kWave / 2; d > 0; d >>= 1) v[f] += __shfl_xor(v[f], d, kWave);
-  if (lane == 0) {
-    st->merged = *at;
-    st->dense_records = v[0];
-    st->dense_runs = v[1];
-    st->sort_runs = v[2];
+// Level totals after the merge: merged arcs (end of the scan of merged arcs
+// per source), and, over the merge tiles, the records and runs of the tiles
+// the dense-table kernel merged and the runs of those the sort kernel merged.
+__global__ __launch_bounds__(256) void k_merged_total(const u64 *at, Status *st, MergeArgs a) {
+  __shared__ u64 s_v[3][256 / kWave];
+  u64 v[3] = {0, 0, 0};
+  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t < a.ntiles; t += (u64)gridDim.x * blockDim.x) {
+    const uint4 td = a.tiles[t];
+    const u32 runs = a.tile_runs[t];
+    if (td.x < td.y && dense_tile(td, a.key_bits) && !(td.w & kRerouted)) {
+      v[0] += td.w;
+      v[1] += runs;
+    } else {
+      v[2] += runs;
+    }
   }
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+#pragma unroll
+  for (int f = 0; f < 3; ++f) {
+    v[f] = wave_sum(v[f]);
+    if (lane == 0) s_v[f][w] = v[f];
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    u64 t = 0;
+    for (int i = 0; i < 256 / kWave; ++i) t += s_v[threadIdx.x][i];
+    if (t) {
+      u64 *dst = threadIdx.x == 0 ? &st->dense_records : threadIdx.x == 1 ? &st->dense_runs : &st->sort_runs;
+      atomicAdd((unsigned long long *)dst, (unsigned long long)t);
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) st->merged = *at;
 }
 
-__global__ void k_reset_level(Status *st, u64 *tstat) {
-  for (u32 i = threadIdx.x; i < kStatWords; i += blockDim.x) tstat[i] = 0;
+__global__ void k_reset_level(Status *st) {
   if (threadIdx.x == 0) {
     st->R = st->M = st->merged = st->RB = 0;
     st->nwide = st->nheavy = st->nbig = st->nnew = 0;
@@ -1337,13 +1341,13 @@ void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hip
   hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st);
 }
 
-void launch_merged_total(const u64 *a_total, Status *st, const u64 *tstat, hipStream_t s) {
-  static_assert(kStatSlots == kWave, "one lane per counter slot");
-  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(kWave), 0, s, a_total, st, tstat);
+void launch_merged_total(const u64 *a_total, const MergeArgs &a, hipStream_t s) {
+  const unsigned g = (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(a.ntiles, 256), 64));
+  hipLaunchKernelGGL(k_merged_total, dim3(g), dim3(256), 0, s, a_total, a.st, a);
 }
 
-void launch_reset_level(Status *st, u64 *tstat, hipStream_t s) {
-  hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(256), 0, s, st, tstat);
+void launch_reset_level(Status *st, hipStream_t s) {
+  hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(1), 0, s, st);
 }
 
 }  // namespace fstc
