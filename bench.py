@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--no-reduction", action="store_true",
                     help="compose without merging identical arcs (every joined arc pair is an "
                          "arc; the setting of the paper's Table 2)")
+    ap.add_argument("--fused", action="store_true",
+                    help="fused expand + merge: tiles merge their composed arcs without "
+                         "writing them first (opts.fused_merge)")
     ap.add_argument("--paper-pair", default="",
                     help="SIZE-TARGET, e.g. 15k-de: instead of --config, the bigram-LM x "
                          "translation-model pair German -> English -> TARGET at a Table 1 size")
@@ -159,7 +162,7 @@ def main():
 
     def step():
         return fstc.fstc_compose(m1, m2, max_levels=args.max_levels,
-                                 reduce=not args.no_reduction)
+                                 reduce=not args.no_reduction, fused=args.fused)
 
     for _ in range(args.warmup):
         r = step()
@@ -221,7 +224,8 @@ def main():
             "workload": workload
                         + (f", depth cap {args.max_levels}" if args.max_levels else "")
                         + (", without reduction (every joined arc pair kept)"
-                           if args.no_reduction else ""),
+                           if args.no_reduction else "")
+                        + (", fused expand + merge" if args.fused else ""),
             "states": last.num_states,
             "premerge_arcs": R,
             "merged_arcs": merged,

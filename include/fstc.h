@@ -102,7 +102,13 @@ typedef struct fstc_opts {
                                  the states are the same, num_arcs equals
                                  num_premerge_arcs and arcs keep no order
                                  within a source                          */
-  uint32_t reserved;
+  uint32_t fused_merge;       /* nonzero: on levels whose sources all fit a
+                                 merge tile and whose keys fit the dense
+                                 table, generate each tile's composed arcs
+                                 inside the merge (section 5's direction of
+                                 keeping intermediate data on chip) instead
+                                 of writing and re-reading them; same
+                                 result                                   */
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the
@@ -150,7 +156,7 @@ typedef struct fstc_stats {
   uint32_t key_bits;          /* part-rank bits of a record key             */
   double ms_sort_kernel;      /* sorting merge-tile kernel alone            */
   uint32_t sort_launches;     /* launches of the sorting merge-tile kernel  */
-  uint32_t reserved1;
+  uint32_t fused_levels;      /* levels merged by the fused kernel         */
   uint64_t total_dense_records; /* records merged through the dense table   */
   uint64_t total_dense_runs;  /* merged arcs the dense table produced        */
   uint64_t total_sort_runs;   /* merged arcs the sorting tiles produced      */

@@ -283,7 +283,7 @@ void Composer::run(fstc_result *out) {
   u64 n_states = 1, arcs = 0, premerge = 0;
   u32 lo = 0, hi = 1, depth = 0, new_levels = 0, expanded_levels = 0;
   u64 max_frontier = 0, max_level_pre = 0, big_total = 0, total_matches = 0, big_records = 0;
-  u32 write_launches = 0, merge_launches = 0, sort_launches = 0;
+  u32 write_launches = 0, merge_launches = 0, sort_launches = 0, fused_levels = 0;
   u64 dense_records = 0, dense_runs = 0, sort_runs = 0;
 
   Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
@@ -373,11 +373,15 @@ void Composer::run(fstc_result *out) {
     T.begin();
     launch_emit(la, s);
     T.end(kExpand);
-    T.begin();
-    launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
-                  rkey.p, rw.as<float>(), tiles_e.as<ExpandTile>(), &dst->err, s);
-    T.end(kWriteKernel);
-    ++write_launches;
+    // fused levels generate each tile's records inside the merge instead
+    const bool fuse = o.fused_merge && !o.no_reduction && key_bits <= kDenseKeyBits && nbig == 0;
+    if (!fuse) {
+      T.begin();
+      launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
+                    rkey.p, rw.as<float>(), tiles_e.as<ExpandTile>(), &dst->err, s);
+      T.end(kWriteKernel);
+      ++write_launches;
+    }
     total_matches += M;
 
     // (a6) merge identical arcs, claim new pairs (or, without reduction,
@@ -412,6 +416,11 @@ void Composer::run(fstc_result *out) {
     ma.mend = mend.as<u64>();
     ma.st = dst;
     ma.big = big.as<u32>();
+    ma.match = match.as<uint4>();
+    ma.mrbase = mrbase.as<u64>();
+    ma.moff = moff.as<u64>();
+    ma.arcs1 = c1.arcs;
+    ma.arcs2 = c2.arcs;
     u64 RB = 0;
     u32 nnew = 0;
     u64 merged = 0;
@@ -422,7 +431,13 @@ void Composer::run(fstc_result *out) {
       fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
       launch_tile_sources(ma, s);
       T.end(kMerge);
-      if (key_bits <= kDenseKeyBits) {
+      if (fuse) {
+        T.begin();
+        launch_fuse_merge(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+        T.end(kMergeKernel);
+        ++merge_launches;
+        ++fused_levels;
+      } else if (key_bits <= kDenseKeyBits) {
         T.begin();
         launch_merge_dense(ma, s);
         T.end(kMergeKernel);
@@ -565,6 +580,7 @@ void Composer::run(fstc_result *out) {
     stats->merge_launches = merge_launches;
     stats->ms_sort_kernel = ms[kSortKernel];
     stats->sort_launches = sort_launches;
+    stats->fused_levels = fused_levels;
     stats->total_dense_records = dense_records;
     stats->total_dense_runs = dense_runs;
     stats->total_sort_runs = sort_runs;

@@ -132,6 +132,11 @@ struct MergeArgs {
   Status *st;
   // multi-block path
   u32 *big;        // [nbig] level-local source indices
+  // fused expand + merge: the level's matches instead of its records
+  const uint4 *match;   // [M] (M1 arc start, M2 arc start, n1, n2)
+  const u64 *mrbase;    // [M] first record of each match
+  const u64 *moff;      // [nsrc + 1] first match of each source
+  const uint2 *arcs1, *arcs2;  // CSR arcs (part rank, weight bits)
 };
 
 // Tile descriptors of the level (a.tiles), then the two tile merges: the
@@ -140,6 +145,10 @@ struct MergeArgs {
 void launch_tile_sources(const MergeArgs &a, hipStream_t s);
 void launch_merge_dense(const MergeArgs &a, hipStream_t s);
 void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s);
+// Fused expand + merge of every tile (in place of launch_expand and
+// launch_merge_dense; needs key_bits <= kDenseKeyBits, no multi-block
+// sources, 32-bit record keys).  narrow: both arc arrays below 2^29 arcs.
+void launch_fuse_merge(const MergeArgs &a, bool narrow, hipStream_t s);
 // Multi-block merge of the nbig sources listed in a.big; bigoff has nbig + 1
 // entries (exclusive scan of their record counts, total RB).
 void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s);

@@ -523,29 +523,70 @@ __device__ __forceinline__ void list_for_sort(const MergeArgs &a, u32 tile) {
   if (i < a.ntiles) a.sortlist[i] = tile;
 }
 
-__global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
-  __shared__ unsigned long long s_sum[kDenseCap];
-  __shared__ u32 s_exp[kDenseCap];  // 0: entry absent, else largest biased exponent + 1
-  __shared__ u32 s_segsrc[kDenseCap];
-  __shared__ u16 s_runseg[kDenseCap];
-  __shared__ u32 s_bits[C / 32];  // bit e: tile element e starts a source
-  __shared__ u32 s_pre[C / 32];   // set bits in the words before
-  __shared__ u32 s_tmp[NW];
-  __shared__ u32 s_emin, s_emax, s_nonfinite;  // over the tile's nonzero weights
+// LDS of the dense-table merge.
+struct DenseLds {
+  unsigned long long sum[kDenseCap];
+  u32 exp[kDenseCap];  // 0: entry absent, else largest biased exponent + 1
+  u32 segsrc[kDenseCap];
+  u16 runseg[kDenseCap];
+  u32 bits[C / 32];  // bit e: tile element e starts a source
+  u32 pre[C / 32];   // set bits in the words before
+  u32 tmp[NW];
+  u32 emin, emax, nonfinite;  // over the tile's nonzero weights
+};
 
+// A tile's inputs to the dense merge: the record offsets of its first
+// sources (thread t: sources s0 + t + k*NT) and its records (item j of lane
+// l of wave w: tile element w*512 + j*64 + l, at min(e, n - 1)).
+struct DenseRecs {
+  u64 r0[kDenseEPT], r1[kDenseEPT];
+  u32 key[IT];
+  float wt[IT];
+};
+
+// Tiles the dense-table merge takes (as far as its descriptor tells).
+__device__ __forceinline__ bool dense_ok(const MergeArgs &a, const uint4 &td) {
+  return td.x < td.y && td.w != 0 && dense_tile(td, a.key_bits) && td.w <= (u32)C &&
+         td.z <= (u32)C - td.w;
+}
+
+__device__ __forceinline__ void dense_load_offsets(const MergeArgs &a, const uint4 &td,
+                                                   DenseRecs &in) {
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k) {
+    in.r0[k] = in.r1[k] = 0;
+    if (td.x + k * NT < td.y) {  // uniform; loads at clamped sources
+      const u32 u = min(td.x + threadIdx.x + k * NT, td.y - 1);
+      in.r0[k] = a.roff[u];
+      in.r1[k] = a.roff[u + 1];
+    }
+  }
+}
+
+__device__ __forceinline__ void dense_load_records(const MergeArgs &a, u32 tile, const uint4 &td,
+                                                   DenseRecs &in) {
+  const u32 n = td.w;
+  const u64 rb = (u64)tile * a.window + td.z;
+  const u32 *rk = static_cast<const u32 *>(a.rec_key) + rb;
+  const float *rw = a.rec_w + rb;
+  const u32 e0 = (threadIdx.x / kWave) * (kWave * IT) + lane_id();
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = min(e0 + j * kWave, n - 1);
+    in.key[j] = __builtin_nontemporal_load(rk + e);  // read once: streaming loads
+    in.wt[j] = __builtin_nontemporal_load(rw + e);
+  }
+}
+
+// Dense-table merge of tile `tile` (dense_ok) from its inputs `in`.
+__device__ __forceinline__ void dense_merge_tile(const MergeArgs &a, u32 tile, const uint4 td,
+                                                 const DenseRecs &in, DenseLds &L) {
+  unsigned long long *s_sum = L.sum;
+  u32 *s_exp = L.exp, *s_segsrc = L.segsrc, *s_bits = L.bits, *s_pre = L.pre, *s_tmp = L.tmp;
+  u16 *s_runseg = L.runseg;
+  u32 &s_emin = L.emin, &s_emax = L.emax, &s_nonfinite = L.nonfinite;
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
-  const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
-  const uint4 td = a.tiles[tile];
-  if (td.x >= td.y || td.w == 0) return;  // no small source starts in this window
-  if (!dense_tile(td, a.key_bits)) {
-    if (threadIdx.x == 0) list_for_sort(a, tile);
-    return;
-  }
   const u32 n = td.w, off = td.z;
-  if (n > (u32)C || off > (u32)C - n) {
-    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
-    return;
-  }
   const u64 rb = (u64)tile * a.window + off;  // first record of the tile
   // 1. source starts -> bitmap -> segment of every element
   if (threadIdx.x < C / 32) s_bits[threadIdx.x] = 0;
@@ -558,30 +599,10 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
   // s0 + t + k*NT, k < kDenseEPT, and keeps their start (or kNoStart)
   constexpr u32 kNoStart = 0xffffffffu;
   u32 start[kDenseEPT];
-  u64 r0[kDenseEPT], r1[kDenseEPT];
-#pragma unroll
-  for (u32 k = 0; k < kDenseEPT; ++k) {
-    r0[k] = r1[k] = 0;
-    if (td.x + k * NT < td.y) {  // uniform; loads at clamped sources, no waits here
-      const u32 u = min(td.x + threadIdx.x + k * NT, td.y - 1);
-      r0[k] = a.roff[u];
-      r1[k] = a.roff[u + 1];
-    }
-  }
-  // items: tile element e = w*512 + j*64 + lane, present when e < n (a
-  // prefix of the thread's items).  Every item loads, at min(e, n - 1), so
-  // that no load waits on a branch.
-  const u32 *rk = static_cast<const u32 *>(a.rec_key) + rb;
-  const float *rw = a.rec_w + rb;
+  const u64 *r0 = in.r0, *r1 = in.r1;
+  const u32 *key = in.key;
+  const float *wt = in.wt;
   const u32 e0 = w * (kWave * IT) + lane;
-  u32 key[IT];
-  float wt[IT];
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    const u32 e = min(e0 + j * kWave, n - 1);
-    key[j] = __builtin_nontemporal_load(rk + e);  // read once: streaming loads
-    wt[j] = __builtin_nontemporal_load(rw + e);
-  }
   __syncthreads();  // s_bits cleared
 #pragma unroll
   for (u32 k = 0; k < kDenseEPT; ++k)
@@ -766,6 +787,175 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
     if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
   }
   if (threadIdx.x == 0) a.tile_runs[tile] = nruns;
+}
+
+
+__global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
+  __shared__ DenseLds L;
+  const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
+  const uint4 td = a.tiles[tile];
+  if (td.x >= td.y || td.w == 0) return;  // no small source starts in this window
+  if (!dense_tile(td, a.key_bits)) {
+    if (threadIdx.x == 0) list_for_sort(a, tile);
+    return;
+  }
+  if (td.w > (u32)C || td.z > (u32)C - td.w) {
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
+    return;
+  }
+  DenseRecs in;
+  dense_load_offsets(a, td, in);
+  dense_load_records(a, tile, td, in);
+  dense_merge_tile(a, tile, td, in, L);
+}
+
+
+// ---------------------------------------------------------------------------
+// Fused expand + merge (the records of a tile never leave the chip).  The
+// matches of the tile's sources (moff[s0] .. moff[s1]) are staged in chunks
+// of kFuseChunk in LDS -- first element in the tile, first M1 and M2 arc, n2,
+// and a bitmap of match starts -- and thread t produces the 8 consecutive
+// tile elements from 8 t of the chunk's span the way the write pass does:
+// the element's match by prefix popcount, (i, j) = divmod(offset, n2) for its
+// M1 and M2 arc, then stepping; all arc loads of the run before any use.
+// Keys and weights go to LDS at their element positions, and the dense merge
+// reads them back in its striped order.  A tile the dense table cannot take
+// writes its records to the record arrays instead and is left to the sort
+// kernel.
+constexpr int kFuseChunk = 512;
+constexpr int kFuseRun = 8;
+static_assert(kFuseRun * NT == C, "one run per thread covers a tile");
+
+struct FuseLds {
+  u32 rel[kFuseChunk + 1];  // first element of each staged match; the chunk's end
+  u32 a1[kFuseChunk], a2[kFuseChunk], n2[kFuseChunk];
+  u32 mbits[C / 32], mpre[C / 32];  // match starts among the tile's elements
+  u16 key[C];                        // dense keys fit 11 bits
+  float w[C];
+};
+
+union FuseDenseLds {
+  FuseLds f;
+  DenseLds d;
+};
+
+template <bool NARROW>
+__device__ __forceinline__ uint2 fuse_arc(const uint2 *arcs, u32 j) {
+  if (NARROW) return *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(arcs) + (j << 3));
+  return arcs[j];
+}
+
+template <bool NARROW>
+__global__ __launch_bounds__(NT, 8) void k_fuse_merge(MergeArgs a) {
+  __shared__ FuseDenseLds U;
+  FuseLds &F = U.f;
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u32 tile = xcd_tile(blockIdx.x, gridDim.x);
+  const uint4 td = a.tiles[tile];
+  if (td.x >= td.y || td.w == 0) return;  // no small source starts in this window
+  const u32 n = td.w;
+  if (n > (u32)C || td.z > (u32)C - n) {
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrTileSize);
+    return;
+  }
+  const bool dense = dense_tile(td, a.key_bits);
+  const u64 rb = (u64)tile * a.window + td.z;  // first record of the tile
+  DenseRecs in;
+  if (dense) dense_load_offsets(a, td, in);
+  const u64 ka = a.moff[td.x], kz = a.moff[td.y];
+  for (u64 kc = ka; kc < kz; kc += kFuseChunk) {
+    const u32 nm = (u32)min<u64>(kFuseChunk, kz - kc);
+    if (kc != ka) __syncthreads();  // previous chunk's LDS fully read
+    if (threadIdx.x < C / 32) F.mbits[threadIdx.x] = 0;
+    __syncthreads();
+    for (u32 i = threadIdx.x; i <= nm; i += NT) {
+      // element of match kc + i (i == nm: where the chunk ends)
+      const u64 k = kc + i;
+      const u32 rel = k < kz ? (u32)(a.mrbase[k] - rb) : n;
+      F.rel[i] = rel;
+      if (i < nm) {
+        const uint4 m = a.match[k];
+        F.a1[i] = m.x;
+        F.a2[i] = m.y;
+        F.n2[i] = m.w;
+        atomicOr(&F.mbits[rel >> 5], 1u << (rel & 31));
+      }
+    }
+    __syncthreads();
+    if (w == 0) {
+      const u32 c0 = __popc(F.mbits[2 * lane]), c1 = __popc(F.mbits[2 * lane + 1]);
+      const u32 inc = wave_inclusive_sum(c0 + c1);
+      F.mpre[2 * lane] = inc - c0 - c1;
+      F.mpre[2 * lane + 1] = inc - c1;
+    }
+    __syncthreads();
+    const u32 cs = F.rel[0], ce = F.rel[nm];  // the chunk's elements
+    const u32 p0 = cs + kFuseRun * threadIdx.x;
+    if (p0 < ce && ce <= n) {
+      const u32 cnt = min((u32)kFuseRun, ce - p0);
+      u32 p = p0;
+      const u32 wd = p >> 5;
+      u32 mi = F.mpre[wd] + __popc(F.mbits[wd] & ((2u << (p & 31)) - 1u)) - 1u;
+      u32 a1 = F.a1[mi], a2 = F.a2[mi], n2 = F.n2[mi], nxt = F.rel[mi + 1];
+      const u32 t = p - F.rel[mi];
+      u32 i1 = t / n2, i2 = t - (t / n2) * n2;
+      u32 ix1[kFuseRun], ix2[kFuseRun];
+      ix1[0] = a1 + i1;
+      ix2[0] = a2 + i2;
+#pragma unroll
+      for (int j = 1; j < kFuseRun; ++j) {
+        ++p;
+        ++i2;
+        const bool wrap = i2 == n2;
+        i2 = wrap ? 0u : i2;
+        i1 += wrap ? 1u : 0u;
+        if (p == nxt && (u32)j < cnt) {  // element j opens the next match
+          ++mi;
+          a1 = F.a1[mi];
+          a2 = F.a2[mi];
+          n2 = F.n2[mi];
+          nxt = F.rel[mi + 1];
+          i1 = i2 = 0;
+        }
+        const bool v = (u32)j < cnt;
+        ix1[j] = v ? a1 + i1 : ix1[0];
+        ix2[j] = v ? a2 + i2 : ix2[0];
+      }
+      uint2 A1[kFuseRun], A2[kFuseRun];
+#pragma unroll
+      for (int j = 0; j < kFuseRun; ++j) {
+        A1[j] = fuse_arc<NARROW>(a.arcs1, ix1[j]);
+        A2[j] = fuse_arc<NARROW>(a.arcs2, ix2[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < kFuseRun; ++j) {
+        if ((u32)j >= cnt) continue;
+        const u32 key = (A1[j].x << a.b2) | A2[j].x;
+        const float wt = __uint_as_float(A1[j].y) * __uint_as_float(A2[j].y);
+        if (dense) {
+          F.key[p0 + j] = (u16)key;
+          F.w[p0 + j] = wt;
+        } else {
+          static_cast<u32 *>(const_cast<void *>(a.rec_key))[rb + p0 + j] = key;
+          const_cast<float *>(a.rec_w)[rb + p0 + j] = wt;
+        }
+      }
+    }
+  }
+  if (!dense) {
+    if (threadIdx.x == 0) list_for_sort(a, tile);
+    return;
+  }
+  __syncthreads();  // every element generated
+  const u32 e0 = w * (kWave * IT) + lane;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 e = min(e0 + j * kWave, n - 1);
+    in.key[j] = F.key[e];
+    in.wt[j] = F.w[e];
+  }
+  __syncthreads();  // the merge reuses the LDS
+  dense_merge_tile(a, tile, td, in, U.d);
 }
 
 // Descriptor of merge tile t: the small sources whose first record falls in
@@ -1187,6 +1377,14 @@ void launch_tile_sources(const MergeArgs &a, hipStream_t s) {
 void launch_merge_dense(const MergeArgs &a, hipStream_t s) {
   if (a.R == 0 || a.key_bits > kDenseKeyBits) return;
   hipLaunchKernelGGL(k_merge_dense, dim3((unsigned)merge_grid(a)), dim3(NT), 0, s, a);
+}
+
+void launch_fuse_merge(const MergeArgs &a, bool narrow, hipStream_t s) {
+  if (a.R == 0) return;
+  if (narrow)
+    hipLaunchKernelGGL(k_fuse_merge<true>, dim3((unsigned)merge_grid(a)), dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_fuse_merge<false>, dim3((unsigned)merge_grid(a)), dim3(NT), 0, s, a);
 }
 
 void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s) {

@@ -1,0 +1,121 @@
+"""Fused expand + merge (opts.fused_merge) on the GPU, through the C ABI.
+
+The fused kernel generates each merge tile's composed arcs on chip from the
+same match descriptors and CSR arcs, with the same float32 products, and
+merges them with the same dense-table merge; tiles the dense table cannot take
+are written out and sorted as before.  So with deterministic ids (within a
+depth, ordered by (q1, q2); otherwise the order follows which visited-table
+insert wins) a fused composition must equal the unfused one bit for bit (ids,
+arc order and weights), and both equal the oracle to the parity bar.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from fstcheck import assert_same, canon_of
+from paper_1805_06383_amd import workloads as W
+from test_oracle_pins import tiny_pair
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fstc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1805_06383_amd import fstc as F
+    F.load_library()
+    return F
+
+
+FIELDS = ("q1", "q2", "final", "src", "dst", "a", "c", "w")
+
+
+def same_bits(x, y, what):
+    for f in FIELDS:
+        a, b = getattr(x, f), getattr(y, f)
+        assert a.shape == b.shape and np.array_equal(a.view(np.uint8), b.view(np.uint8)), \
+            f"{what}: field {f} differs between fused and unfused"
+    assert x.num_premerge == y.num_premerge
+
+
+def fused_vs_unfused(F, m1, m2, what, **kw):
+    fu = F.compose(m1, m2, fused=True, deterministic_ids=True, **kw)
+    un = F.compose(m1, m2, fused=False, deterministic_ids=True, **kw)
+    same_bits(fu.to_host(), un.to_host(), what)
+    return fu
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_fused_tiny(fstc, seed):
+    m1, m2 = tiny_pair(seed)
+    g = fused_vs_unfused(fstc, m1, m2, f"tiny {seed}").to_host()
+    assert_same(canon_of(g), canon_of(oracle.compose(m1, m2)), what=f"tiny {seed}")
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_fused_config1(fstc, seed):
+    m1, m2 = W.config1(seed)
+    g = fused_vs_unfused(fstc, m1, m2, f"config1 {seed}").to_host()
+    assert_same(canon_of(g), canon_of(oracle.compose(m1, m2)), what=f"config1 {seed}")
+
+
+@pytest.mark.parametrize("cfg,cap", [(4, 3), (2, 3), (3, 0)])
+def test_fused_workloads_oracle(fstc, cfg, cap):
+    m1, m2 = W.make_config(cfg, 0)
+    g = fused_vs_unfused(fstc, m1, m2, f"config{cfg} cap {cap}", max_levels=cap).to_host()
+    assert_same(canon_of(g), canon_of(oracle.compose(m1, m2, max_levels=cap)),
+                what=f"config{cfg} cap {cap}")
+
+
+@pytest.mark.parametrize("size,target", [("1k", "de"), ("15k", "es")])
+def test_fused_paper_pairs(fstc, size, target):
+    m1, m2 = W.paper_pair(size, target)
+    g = fused_vs_unfused(fstc, m1, m2, f"paper {size} {target}").to_host()
+    assert_same(canon_of(g), canon_of(oracle.compose(m1, m2)), what=f"paper {size} {target}")
+
+
+@pytest.mark.timeout(300)
+def test_fused_config4_full(fstc):
+    """Full HMM-like workload: every level is fused (one dense tile kind),
+    bit-identical to the unfused composition."""
+    m1, m2 = W.config4(0)
+    fu = fused_vs_unfused(fstc, m1, m2, "config4 full")
+    assert fu.stats["fused_levels"] >= 9 and fu.stats["write_launches"] == 0
+
+
+@pytest.mark.timeout(600)
+def test_fused_config2_full(fstc):
+    """Medium sparse pair in full: its keys need more bits than the dense
+    table takes, so no level is fused and the result is the unfused one."""
+    m1, m2 = W.config2(0)
+    fu = fused_vs_unfused(fstc, m1, m2, "config2 full")
+    assert fu.stats["fused_levels"] == 0
+
+
+def test_fused_tiles_left_to_sort(fstc):
+    """Fused levels whose tiles hold too many sources for the dense table:
+    those tiles' arcs are written out and merged by the sort kernel."""
+    seen = 0
+    for seed in range(200):
+        m1, m2 = W.config1(seed)
+        fu = fstc.compose(m1, m2, fused=True)
+        if fu.stats["fused_levels"] and fu.stats["total_sort_runs"]:
+            fused_vs_unfused(fstc, m1, m2, f"config1 {seed}")
+            assert_same(canon_of(fu.to_host()), canon_of(oracle.compose(m1, m2)),
+                        what=f"config1 {seed}")
+            seen += 1
+            if seen == 5:
+                break
+    assert seen > 0, "no config-1 seed fused a level with sorted tiles"
+
+
+def test_fused_signed_weights(fstc):
+    """Signed, wide-range weights: the exact tile sums match the unfused run."""
+    from test_parity_gpu import signed_wide, with_weights
+    m1, m2 = W.config4(0)
+    rng = np.random.default_rng(78)
+    m1 = with_weights(m1, signed_wide(rng, m1.num_arcs, -30, 30))
+    m2 = with_weights(m2, signed_wide(rng, m2.num_arcs, -30, 30))
+    fused_vs_unfused(fstc, m1, m2, "signed config4 cap 2", max_levels=2)
