@@ -60,7 +60,8 @@ void *Buf::ensure(size_t bytes) {
 
 void *Buf::grow_keep(size_t bytes, size_t used) {
   if (bytes <= cap && p) return p;
-  const size_t c = std::max<size_t>(std::max<size_t>(256, (bytes + 255) & ~(size_t)255), 2 * cap);
+  const size_t c = std::max<size_t>(std::max<size_t>(kMinGrow * 4, (bytes + 255) & ~(size_t)255),
+                                    2 * cap);
   void *q = A->alloc(c);
   if (used && p) FSTC_HIP(hipMemcpyAsync(q, p, used, hipMemcpyDeviceToDevice, A->stream));
   release();
@@ -270,8 +271,10 @@ void Composer::run(fstc_result *out) {
   u64 state_limit = std::min<u64>(pairspace, 0xffffffffull);
   if (o.max_states) state_limit = std::min<u64>(state_limit, o.max_states);
   Buf sq1b(&A), sq2b(&A), hkb(&A), hvb(&A);
-  sq1b.ensure(1024 * 4);
-  sq2b.ensure(1024 * 4);
+  // state and result arrays start at kMinGrow entries, so that small
+  // compositions never grow them
+  sq1b.ensure(kMinGrow * 4);
+  sq2b.ensure(kMinGrow * 4);
   u64 hcap = std::min<u64>(kMaxHashCap, next_pow2(std::max<u64>(
                                            4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1))));
   hkb.ensure(hcap * 8);
@@ -371,7 +374,7 @@ void Composer::run(fstc_result *out) {
     la.mrbase = mrbase.as<u64>();
     la.tiles = tiles_e.as<ExpandTile>();
     T.begin();
-    launch_emit(la, s);
+    launch_emit(la, hs->st.nwide, hs->st.nheavy, s);
     T.end(kExpand);
     // fused levels generate each tile's records inside the merge instead
     const bool fuse = o.fused_merge && !o.no_reduction && key_bits <= kDenseKeyBits && nbig == 0;

@@ -563,18 +563,24 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
 
 }  // namespace
 
+// Grids of the wavefront and workgroup joins: at most one wave (block) per
+// listed source, whose number is bounded by the frontier before the count
+// and known exactly after it.
+static unsigned wide_grid(u64 n) { return (unsigned)std::min<u64>(2048, ceil_div(n, 256 / kWave)); }
+static unsigned heavy_grid(u64 n) { return (unsigned)std::min<u64>(512, n); }
+
 void launch_count(const LevelArgs &a, hipStream_t s) {
   const unsigned g = (unsigned)ceil_div(a.nsrc, kCountNT);
   hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
-  hipLaunchKernelGGL(k_count_wide, dim3(2048), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_count_heavy, dim3(512), dim3(kHeavyNT), 0, s, a);
+  hipLaunchKernelGGL(k_count_wide, dim3(wide_grid(a.nsrc)), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_count_heavy, dim3(heavy_grid(a.nsrc)), dim3(kHeavyNT), 0, s, a);
 }
 
-void launch_emit(const LevelArgs &a, hipStream_t s) {
+void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s) {
   const unsigned g = (unsigned)ceil_div(a.nsrc, 256);
   hipLaunchKernelGGL(k_emit_small, dim3(g), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_emit_wide, dim3(2048), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_emit_heavy, dim3(512), dim3(kHeavyNT), 0, s, a);
+  if (nwide) hipLaunchKernelGGL(k_emit_wide, dim3(wide_grid(nwide)), dim3(256), 0, s, a);
+  if (nheavy) hipLaunchKernelGGL(k_emit_heavy, dim3(heavy_grid(nheavy)), dim3(kHeavyNT), 0, s, a);
 }
 
 void launch_expand(const uint4 *match, const u64 *mrbase, u64 M, u64 R, const CsrView &c1,

@@ -21,6 +21,9 @@ struct Allocator {
   void free(void *p, size_t bytes);
 };
 
+// Smallest capacity (in 4-byte entries) of a buffer grown with grow_keep.
+constexpr size_t kMinGrow = (size_t)1 << 18;
+
 // Grow-only device buffer owned by a compose call.
 struct Buf {
   Allocator *A = nullptr;

@@ -96,7 +96,8 @@ struct LevelArgs {
 };
 
 void launch_count(const LevelArgs &a, hipStream_t s);
-void launch_emit(const LevelArgs &a, hipStream_t s);
+// nwide / nheavy: the list lengths the count kernels produced (st->nwide, nheavy).
+void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s);
 // Writes R records: key = (part1 << b2) | part2 (u32 when key_bits <= 32,
 // else u64), weight = p1 * p2.
 // tiles: the ceil(R / kExpandTile) write-tile entries written by launch_emit.
