@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--fused", action="store_true",
                     help="fused expand + merge: tiles merge their composed arcs without "
                          "writing them first (opts.fused_merge)")
+    ap.add_argument("--no-product", action="store_true",
+                    help="send every source through written records (opts.no_product_merge): "
+                         "the paper's count / write / sort-and-reduce path")
     ap.add_argument("--paper-pair", default="",
                     help="SIZE-TARGET, e.g. 15k-de: instead of --config, the bigram-LM x "
                          "translation-model pair German -> English -> TARGET at a Table 1 size")
@@ -162,7 +165,8 @@ def main():
 
     def step():
         return fstc.fstc_compose(m1, m2, max_levels=args.max_levels,
-                                 reduce=not args.no_reduction, fused=args.fused)
+                                 reduce=not args.no_reduction, fused=args.fused,
+                                 product=not args.no_product)
 
     for _ in range(args.warmup):
         r = step()
@@ -196,6 +200,11 @@ def main():
                       "avg_launch_ms": ms / launches, "bytes_per_step": ab[name],
                       "bytes_per_launch": ab[name] / launches, "GBps": gbs}
     both_ms = sum(k["ms_per_step"] for k in kern.values())
+    kern["product"] = {"kernel": "k_prod_sources",
+                       "ms_per_step": sums["ms_product_kernel"] / args.steps,
+                       "launches_per_step": st["product_launches"],
+                       "sources_per_step": st["total_product_sources"],
+                       "joined_pairs_per_step": st["total_product_records"]}
     kern["expand+merge"] = {"ms_per_step": both_ms, "bytes_per_step": sum(ab.values()),
                             "GBps": sum(ab.values()) / (both_ms * 1e-3) / 1e9 if both_ms else 0.0}
     dom = max(ab, key=lambda k: kern[k]["ms_per_step"])
@@ -225,7 +234,8 @@ def main():
                         + (f", depth cap {args.max_levels}" if args.max_levels else "")
                         + (", without reduction (every joined arc pair kept)"
                            if args.no_reduction else "")
-                        + (", fused expand + merge" if args.fused else ""),
+                        + (", fused expand + merge" if args.fused else "")
+                        + (", no product merge" if args.no_product else ""),
             "states": last.num_states,
             "premerge_arcs": R,
             "merged_arcs": merged,

@@ -109,6 +109,18 @@ typedef struct fstc_opts {
                                  keeping intermediate data on chip) instead
                                  of writing and re-reading them; same
                                  result                                   */
+  uint32_t no_product_merge;  /* nonzero: every source goes through written
+                                 records (count, write, sort/table merge) as
+                                 the paper describes.  0: a source whose two
+                                 states have few (target, outer symbol)
+                                 pairs, whose arcs fill their (pair, inner
+                                 symbol) cells densely and at most once
+                                 each, is merged by one wavefront from its
+                                 two arc matrices (sum over matched symbols
+                                 of float32 products, added in float64),
+                                 without records.  Same states and arcs;
+                                 weights agree to float64 rounding        */
+  uint32_t reserved;
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the
@@ -160,6 +172,12 @@ typedef struct fstc_stats {
   uint64_t total_dense_records; /* records merged through the dense table   */
   uint64_t total_dense_runs;  /* merged arcs the dense table produced        */
   uint64_t total_sort_runs;   /* merged arcs the sorting tiles produced      */
+  uint64_t total_product_records; /* joined arc pairs merged by the product
+                                     merge (never written as records)         */
+  uint64_t total_product_sources; /* sources merged by the product merge      */
+  double ms_product_kernel;   /* product-merge kernel alone, all levels      */
+  uint32_t product_launches;  /* launches of the product-merge kernel        */
+  uint32_t reserved0;
 } fstc_stats;
 
 /*

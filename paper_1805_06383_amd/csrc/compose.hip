@@ -145,7 +145,8 @@ const char *device_error_text(u32 e) {
 }
 
 enum Phase {
-  kCsr, kCount, kExpand, kMerge, kAssign, kWriteKernel, kMergeKernel, kSortKernel, kNumPhases
+  kCsr, kCount, kExpand, kMerge, kAssign, kWriteKernel, kMergeKernel, kSortKernel,
+  kProductKernel, kNumPhases
 };
 
 // HIP-event timing of the phases on the call's stream (only with stats).
@@ -242,16 +243,23 @@ void Composer::run(fstc_result *out) {
   fill_u32((u32 *)dst, 0, sizeof(Status) / 4, s);
 
   // (a0) device layout of both inputs
-  Buf cb1[7], cb2[7];
+  Buf cb1[7], cb2[7], cf1(&A), cf2(&A);
   Csr c1, c2;
   alloc_csr(m1, A, cb1, c1);
   alloc_csr(m2, A, cb2, c2);
+  c1.cell_flag = (u32 *)cf1.ensure(std::max<u64>(m1.num_states, 1) * 4);
+  c2.cell_flag = (u32 *)cf2.ensure(std::max<u64>(m2.num_states, 1) * 4);
+  const bool product = !o.no_reduction && !o.no_product_merge;
   T.begin();
   {
     Arena csr_tmp(&A);
     build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
     csr_tmp.reset();
     build_csr(m2, false, csr_tmp, c2, dcounts + 3, &dst->err, s);
+    if (product) {
+      build_cell_flags(c1, c1.cell_flag, s);
+      build_cell_flags(c2, c2.cell_flag, s);
+    }
   }
   T.end(kCsr);
   sync_status();
@@ -287,13 +295,14 @@ void Composer::run(fstc_result *out) {
   u32 lo = 0, hi = 1, depth = 0, new_levels = 0, expanded_levels = 0;
   u64 max_frontier = 0, max_level_pre = 0, big_total = 0, total_matches = 0, big_records = 0;
   u32 write_launches = 0, merge_launches = 0, sort_launches = 0, fused_levels = 0;
-  u64 dense_records = 0, dense_runs = 0, sort_runs = 0;
+  u64 dense_records = 0, dense_runs = 0, sort_runs = 0, product_records = 0, product_sources = 0;
+  u32 product_launches = 0;
 
   Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
-      aoff(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      aoff(&level_tmp), pk(&level_tmp), poff(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -312,13 +321,14 @@ void Composer::run(fstc_result *out) {
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
     mcount.ensure(np1 * 4); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
+    pk.ensure(np1 * 4); poff.ensure(np1 * 8);
     stmp.ensure(scan_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
     launch_reset_level(dst, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
-                 dst, nullptr, nullptr, nullptr, big.as<u32>()};
+                 dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), product ? 1u : 0u};
     T.begin();
     launch_count(la, s);
     exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
@@ -327,10 +337,14 @@ void Composer::run(fstc_result *out) {
     T.end(kCount);
     sync_status();
     const u64 R = hs->st.R, M = hs->st.M;
-    const u32 nbig = hs->st.nbig;
-    if (R == 0) break;  // no arc leaves this level: no new states either
-    premerge += R;
-    max_level_pre = std::max(max_level_pre, R);
+    const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
+    if (nprod) exclusive_scan(pk.as<u32>(), poff.as<u64>(), nsrc, stmp.p, s);
+    const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
+    if (R == 0 && nprod == 0) break;  // no arc leaves this level: no new states either
+    premerge += R + hs->st.prod_records;
+    max_level_pre = std::max(max_level_pre, R + hs->st.prod_records);
+    product_records += hs->st.prod_records;
+    product_sources += nprod;
     big_total += nbig;
 
     match.ensure(M * sizeof(uint4));
@@ -338,8 +352,8 @@ void Composer::run(fstc_result *out) {
     rkey.ensure(R * rec_bytes);
     rw.ensure(R * 4);
     if (!o.no_reduction) {
-      temp.ensure(R * sizeof(uint4));
-      runsrc.ensure(R * 4);
+      temp.ensure((R + prodpos) * sizeof(uint4));
+      runsrc.ensure((R + prodpos) * 4);
     }
     tiles_e.ensure(ceil_div(R, kExpandTile) * sizeof(ExpandTile));
     // merge window: as wide as the largest small source allows (see level.hpp)
@@ -349,7 +363,7 @@ void Composer::run(fstc_result *out) {
     tiles_m.ensure(ntiles * sizeof(uint4));
     sortlist.ensure(ntiles * 4);
     tile_runs.ensure(ntiles * 4);
-    const u64 newcap = std::min<u64>(R, pairspace - n_states);
+    const u64 newcap = std::min<u64>(R + prodpos, pairspace - n_states);
     newlist.ensure(std::max<u64>(newcap, 1) * 4);
 
     // visited table: keep the load factor at most 1/2 for every pair this
@@ -424,6 +438,15 @@ void Composer::run(fstc_result *out) {
     ma.moff = moff.as<u64>();
     ma.arcs1 = c1.arcs;
     ma.arcs2 = c2.arcs;
+    ma.pk = pk.as<u32>();
+    ma.poff = poff.as<u64>();
+    ma.prodpos = prodpos;
+    ma.row1 = c1.row;
+    ma.seg_sym1 = c1.seg_sym;
+    ma.seg_off1 = c1.seg_off;
+    ma.row2 = c2.row;
+    ma.seg_sym2 = c2.seg_sym;
+    ma.seg_off2 = c2.seg_off;
     u64 RB = 0;
     u32 nnew = 0;
     u64 merged = 0;
@@ -460,6 +483,14 @@ void Composer::run(fstc_result *out) {
         RB = hs->words[0];
         big_records += RB;
         merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, level_tmp, s);
+      }
+      if (nprod) {
+        T.end(kMerge);
+        T.begin();
+        launch_prod_sources(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+        T.end(kProductKernel);
+        ++product_launches;
+        T.begin();
       }
       launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
       exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
@@ -539,9 +570,14 @@ void Composer::run(fstc_result *out) {
       oil.grow_keep(na * 4, arcs * 4);
       ool.grow_keep(na * 4, arcs * 4);
       ow.grow_keep(na * 4, arcs * 4);
-      launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc.as<u32>() + arcs,
-                     odst.as<u32>() + arcs, oil.as<u32>() + arcs, ool.as<u32>() + arcs,
-                     ow.as<float>() + arcs, s);
+      if (nprod)  // product-merge sources interleave with the tiles' sources
+        launch_compact_sources(ma, aoff.as<u64>(), merged, hvb.as<u32>(), osrc.as<u32>() + arcs,
+                               odst.as<u32>() + arcs, oil.as<u32>() + arcs,
+                               ool.as<u32>() + arcs, ow.as<float>() + arcs, s);
+      else
+        launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc.as<u32>() + arcs,
+                       odst.as<u32>() + arcs, oil.as<u32>() + arcs, ool.as<u32>() + arcs,
+                       ow.as<float>() + arcs, s);
     }
     T.end(kAssign);
     arcs += merged;
@@ -586,6 +622,10 @@ void Composer::run(fstc_result *out) {
     stats->fused_levels = fused_levels;
     stats->total_dense_records = dense_records;
     stats->total_dense_runs = dense_runs;
+    stats->total_product_records = product_records;
+    stats->total_product_sources = product_sources;
+    stats->ms_product_kernel = ms[kProductKernel];
+    stats->product_launches = product_launches;
     stats->total_sort_runs = sort_runs;
     stats->total_matches = total_matches;
     stats->total_big_records = big_records;
@@ -600,7 +640,7 @@ void Composer::run(fstc_result *out) {
     stats->ms_csr = ms[kCsr];
     stats->ms_count = ms[kCount];
     stats->ms_expand = ms[kExpand] + ms[kWriteKernel];
-    stats->ms_merge = ms[kMerge] + ms[kMergeKernel] + ms[kSortKernel];
+    stats->ms_merge = ms[kMerge] + ms[kMergeKernel] + ms[kSortKernel] + ms[kProductKernel];
     stats->ms_assign = ms[kAssign];
     stats->ms_total =
         std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();

@@ -94,6 +94,32 @@ __global__ void k_segments(const u64 *kc, const u32 *perm, const u32 *flags, con
 
 __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 
+// Wave per state; lane l checks segments row[q] + l, + 64, ...: a segment
+// of more arcs than kProdParts, or whose arcs' parts are not all distinct
+// (a 64-bit mask of the parts), flags the state.
+__global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *arcs,
+                             const u32 *part_base, u32 nq, u32 *flag) {
+  const u32 lane = lane_id();
+  const u64 nw = (u64)gridDim.x * blockDim.x / kWave;
+  for (u64 q = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
+    bool bad = part_base[q + 1] - part_base[q] > kProdParts;
+    if (!bad) {
+      for (u32 sg = row[q] + lane; sg < row[q + 1]; sg += kWave) {
+        const u32 a0 = seg_off[sg], n = seg_off[sg + 1] - a0;
+        if (n > kProdParts) {
+          bad = true;
+          continue;
+        }
+        u64 m = 0;
+        for (u32 i = 0; i < n; ++i) m |= 1ull << (arcs[a0 + i].x & 63u);
+        bad |= (u32)__popcll(m) != n;
+      }
+    }
+    const bool any = __ballot(bad) != 0;
+    if (lane == 0) flag[q] = any ? 1u : 0u;
+  }
+}
+
 // a[i] = v for i in [*count, n).
 __global__ void k_fill_tail(u32 *a, const u32 *count, u64 n, u32 v) {
   const u64 c = *count;
@@ -102,6 +128,13 @@ __global__ void k_fill_tail(u32 *a, const u32 *count, u64 n, u32 v) {
 }
 
 }  // namespace
+
+void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s) {
+  if (!c.num_states) return;
+  const unsigned g = (unsigned)std::min<u64>(ceil_div(c.num_states, kNT / kWave), 1u << 16);
+  hipLaunchKernelGGL(k_cell_flags, dim3(g), dim3(kNT), 0, s, c.row, c.seg_off, c.arcs,
+                     c.part_base, c.num_states, cell_flag);
+}
 
 void check_csr_ranges(const fstc_fst &m, bool by_output) {
   if (m.num_arcs >= (1ull << 32))

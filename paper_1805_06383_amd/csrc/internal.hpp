@@ -112,12 +112,21 @@ struct Csr {
   uint2 *arcs = nullptr;     // [num_arcs] (part rank within state, weight bits)
   u32 *part_base = nullptr;  // [num_states + 1]
   uint2 *parts = nullptr;    // [num_arcs] (target, outer symbol)
+  u32 *cell_flag = nullptr;  // [num_states] see build_cell_flags (compose only)
 };
 
 // Device counters written by the CSR build: [0] segments, [1] parts,
 // [2] max parts of one state.
 void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &out, u64 *d_counts,
                u32 *d_err, hipStream_t s);
+
+// Largest part count of a state the product merge takes (level.hpp).
+constexpr u32 kProdParts = 64;
+
+// cell_flag[q] = 1 when state q has more than kProdParts parts or two arcs
+// with the same part and inner symbol (parallel arcs with equal labels and
+// target), else 0.
+void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s);
 
 // Checks the packing limits of build_csr for one transducer; throws
 // Error(FSTC_ERR_RANGE) when a key does not fit 64 bits.

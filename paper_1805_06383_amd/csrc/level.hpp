@@ -15,10 +15,12 @@ struct CsrView {
   const u32 *part_base;
   const uint2 *parts;
   u64 num_arcs;
+  const u32 *cell_flag;  // [num_states] nonzero: the state cannot take the product merge
 };
 
 inline CsrView view(const Csr &c) {
-  return CsrView{c.row, c.seg_sym, c.seg_off, c.arcs, c.part_base, c.parts, c.num_arcs};
+  return CsrView{c.row, c.seg_sym, c.seg_off, c.arcs, c.part_base, c.parts, c.num_arcs,
+                 c.cell_flag};
 }
 
 // Host-visible per-level counters (one D2H copy per synchronisation).
@@ -34,8 +36,20 @@ struct Status {
   u64 dense_runs;     // merged arcs those tiles produced
   u64 sort_runs;      // merged arcs of the tiles merged by sorting
   u32 nsort;          // tiles k_merge_dense left to the sort kernel
-  u32 pad;
+  u32 nprod;          // sources of the product merge
+  u64 prod_records;   // their joined arc pairs (not written as records)
+  u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
 };
+
+// Product merge (merge.hip, k_prod_sources).  A source (q1, q2) whose states
+// have at most kProdParts parts each, whose (p1, p2) table has at most
+// kProdEntries entries, whose two arc matrices (P1 x G and G x P2 cells for
+// G matched inner symbols) fit kProdCells, whose matrices hold at least half
+// of their cells' products as joined arc pairs, and whose states have no two
+// arcs in one (part, inner symbol) cell, is merged by one wavefront from its
+// staged matrices instead of through records.
+constexpr u32 kProdEntries = 64;
+constexpr u32 kProdCells = 1024;
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
 // wavefront, longer than kHeavyMin by a workgroup; others by one thread.
@@ -93,6 +107,8 @@ struct LevelArgs {
   u64 *mrbase;           // [M] first record of each match
   ExpandTile *tiles;     // [ceil(R / kExpandTile)] write-tile entries
   u32 *big;              // [nsrc] sources for the multi-block merge (st->nbig)
+  u32 *pk;               // [nsrc] table entries of a product-merge source, else 0
+  u32 prod;              // nonzero: sources may take the product merge
 };
 
 void launch_count(const LevelArgs &a, hipStream_t s);
@@ -138,6 +154,12 @@ struct MergeArgs {
   const u64 *mrbase;    // [M] first record of each match
   const u64 *moff;      // [nsrc + 1] first match of each source
   const uint2 *arcs1, *arcs2;  // CSR arcs (part rank, weight bits)
+  // product merge: the sources with pk[u] != 0 own temp slots
+  // R + poff[u] .. R + poff[u] + pk[u] - 1 (prodpos slots in all)
+  const u32 *pk;
+  const u64 *poff;
+  u64 prodpos;
+  const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;
 };
 
 // Tile descriptors of the level (a.tiles), then the two tile merges: the
@@ -150,6 +172,10 @@ void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s);
 // launch_merge_dense; needs key_bits <= kDenseKeyBits, no multi-block
 // sources, 32-bit record keys).  narrow: both arc arrays below 2^29 arcs.
 void launch_fuse_merge(const MergeArgs &a, bool narrow, hipStream_t s);
+// Product merge of the sources with a.pk[u] != 0: their merged arcs, with
+// visited-table inserts, at temp[R + poff[u] ...) and tstart / mend.
+// narrow: both arc arrays below 2^29 arcs.
+void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s);
 // Multi-block merge of the nbig sources listed in a.big; bigoff has nbig + 1
 // entries (exclusive scan of their record counts, total RB).
 void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s);
@@ -172,12 +198,17 @@ void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64
 // M: merged arcs of the level (the output arrays' length from osrc on).
 void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const u32 *hvals,
                     u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s);
+// Result append source by source (tstart[u] .. mend[u] - 1 to aoff[u] ...):
+// the form used when product-merge sources sit between tile-merged ones.
+void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,
+                            u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s);
 void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s);
 // Visited-table inserts and label lookups for every merged arc of the
 // tile-merged sources (merge_big does its own).
 void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
-// New-state list of the level from the claimed-slot flags (st->nnew = its
-// length).  wcnt: newlist_waves(a, RB) u32; woff: that + 1 u64; scan_tmp:
+// New-state list of the level from the claimed-slot flags of the tile runs,
+// the multi-block runs and the product-merge slots (st->nnew = its length).
+// wcnt: newlist_waves(a, RB) u32; woff: that + 1 u64; scan_tmp:
 // scan_temp_bytes(newlist_waves(a, RB)) bytes.
 u64 newlist_waves(const MergeArgs &a, u64 RB);
 void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,

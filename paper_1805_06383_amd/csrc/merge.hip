@@ -523,6 +523,16 @@ __device__ __forceinline__ void list_for_sort(const MergeArgs &a, u32 tile) {
   if (i < a.ntiles) a.sortlist[i] = tile;
 }
 
+// Biased exponent of a weight, denormals and zero counted as 1.
+__device__ __forceinline__ u32 fx_bexp(float x) { return max((__float_as_uint(x) >> 23) & 0xffu, 1u); }
+
+// Significand of a weight with the hidden bit, signed.
+__device__ __forceinline__ int fx_sig(float x) {
+  const u32 bits = __float_as_uint(x);
+  const u32 mag = (bits & 0x7fffffu) | (((bits >> 23) & 0xffu) ? 0x800000u : 0u);
+  return (bits >> 31) ? -(int)mag : (int)mag;
+}
+
 // LDS of the dense-table merge.
 struct DenseLds {
   unsigned long long sum[kDenseCap];
@@ -578,12 +588,52 @@ __device__ __forceinline__ void dense_load_records(const MergeArgs &a, u32 tile,
   }
 }
 
+// Present entries of the dense table (s_exp != 0) of tile `tile` -> runs
+// rb + r in entry order (entry i = segment << kb | key), with the source
+// ranges tstart / mend and the tile's run count.  Thread t lists entries
+// t*kDenseEPT .. t*kDenseEPT + kDenseEPT - 1 of the first tsize.
+__device__ __forceinline__ void dense_list_runs(const MergeArgs &a, u32 tile, u64 rb, u32 tsize,
+                                                int kb, DenseLds &L) {
+  unsigned long long *s_sum = L.sum;
+  u32 *s_exp = L.exp, *s_segsrc = L.segsrc, *s_tmp = L.tmp;
+  u16 *s_runseg = L.runseg;
+  u32 pmask = 0;
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k) {
+    const u32 i = threadIdx.x * kDenseEPT + k;
+    if (i < tsize && s_exp[i] != 0) pmask |= 1u << k;
+  }
+  const u32 pc = __popc(pmask);
+  const u32 pinc = wave_inclusive_sum(pc);
+  u32 nruns;
+  u32 r = block_offset(__shfl(pinc, kWave - 1, kWave), s_tmp, &nruns) + pinc - pc;
+  const u32 kmask = (1u << kb) - 1u;
+#pragma unroll
+  for (u32 k = 0; k < kDenseEPT; ++k) {
+    if (!((pmask >> k) & 1u)) continue;
+    const u32 i = threadIdx.x * kDenseEPT + k;
+    const int E = (int)s_exp[i] - 1;
+    const double v = ldexp((double)(long long)s_sum[i], E - 177);
+    const u32 seg = i >> kb;
+    a.temp[rb + r] = make_uint4(s_segsrc[seg], i & kmask, 0u, __float_as_uint((float)v));
+    s_runseg[r] = (u16)seg;
+    ++r;
+  }
+  __syncthreads();
+  for (u32 q = threadIdx.x; q < nruns; q += NT) {
+    const u32 seg = s_runseg[q];
+    const u32 u = s_segsrc[seg];
+    if (q == 0 || s_runseg[q - 1] != seg) a.tstart[u] = rb + q;
+    if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
+  }
+  if (threadIdx.x == 0) a.tile_runs[tile] = nruns;
+}
+
 // Dense-table merge of tile `tile` (dense_ok) from its inputs `in`.
 __device__ __forceinline__ void dense_merge_tile(const MergeArgs &a, u32 tile, const uint4 td,
                                                  const DenseRecs &in, DenseLds &L) {
   unsigned long long *s_sum = L.sum;
-  u32 *s_exp = L.exp, *s_segsrc = L.segsrc, *s_bits = L.bits, *s_pre = L.pre, *s_tmp = L.tmp;
-  u16 *s_runseg = L.runseg;
+  u32 *s_exp = L.exp, *s_segsrc = L.segsrc, *s_bits = L.bits, *s_pre = L.pre;
   u32 &s_emin = L.emin, &s_emax = L.emax, &s_nonfinite = L.nonfinite;
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u32 n = td.w, off = td.z;
@@ -635,14 +685,8 @@ __device__ __forceinline__ void dense_merge_tile(const MergeArgs &a, u32 tile, c
     s_sum[i] = 0;
     s_exp[i] = 0;
   }
-  // biased exponent of a weight, denormals and zero counted as 1
-  auto bexp = [](float x) { return max((__float_as_uint(x) >> 23) & 0xffu, 1u); };
-  // significand with the hidden bit, signed
-  auto sig = [](float x) {
-    const u32 bits = __float_as_uint(x);
-    const u32 mag = (bits & 0x7fffffu) | (((bits >> 23) & 0xffu) ? 0x800000u : 0u);
-    return (bits >> 31) ? -(int)mag : (int)mag;
-  };
+  auto bexp = fx_bexp;
+  auto sig = fx_sig;
   constexpr u32 kNone = 0xffffffffu;  // table index of an absent item
   // Item j of every lane of the wave lies in the element row
   // [w*512 + j*64, +64), two bitmap words: the segment of the lane's element
@@ -755,38 +799,7 @@ __device__ __forceinline__ void dense_merge_tile(const MergeArgs &a, u32 tile, c
   }
   __syncthreads();
 
-  // 4. present entries -> runs rb + r in entry order; thread t lists entries
-  //    t*kDenseEPT .. t*kDenseEPT + kDenseEPT - 1
-  u32 pmask = 0;
-#pragma unroll
-  for (u32 k = 0; k < kDenseEPT; ++k) {
-    const u32 i = threadIdx.x * kDenseEPT + k;
-    if (i < tsize && s_exp[i] != 0) pmask |= 1u << k;
-  }
-  const u32 pc = __popc(pmask);
-  const u32 pinc = wave_inclusive_sum(pc);
-  u32 nruns;
-  u32 r = block_offset(__shfl(pinc, kWave - 1, kWave), s_tmp, &nruns) + pinc - pc;
-  const u32 kmask = (1u << kb) - 1u;
-#pragma unroll
-  for (u32 k = 0; k < kDenseEPT; ++k) {
-    if (!((pmask >> k) & 1u)) continue;
-    const u32 i = threadIdx.x * kDenseEPT + k;
-    const int E = (int)s_exp[i] - 1;
-    const double v = ldexp((double)(long long)s_sum[i], E - 177);
-    const u32 seg = i >> kb;
-    a.temp[rb + r] = make_uint4(s_segsrc[seg], i & kmask, 0u, __float_as_uint((float)v));
-    s_runseg[r] = (u16)seg;
-    ++r;
-  }
-  __syncthreads();
-  for (u32 q = threadIdx.x; q < nruns; q += NT) {
-    const u32 seg = s_runseg[q];
-    const u32 u = s_segsrc[seg];
-    if (q == 0 || s_runseg[q - 1] != seg) a.tstart[u] = rb + q;
-    if (q == nruns - 1 || s_runseg[q + 1] != seg) a.mend[u] = rb + q + 1;
-  }
-  if (threadIdx.x == 0) a.tile_runs[tile] = nruns;
+  dense_list_runs(a, tile, rb, tsize, kb, L);
 }
 
 
@@ -809,6 +822,188 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
   dense_merge_tile(a, tile, td, in, L);
 }
 
+
+// ---------------------------------------------------------------------------
+// Product merge, wavefront per source (level.hpp: which sources take it).
+// For a source (q1, q2) with matched inner symbols g (the symbols q1 writes
+// and q2 reads), every joined arc pair is a term w1(p1, g) * w2(g, p2): the
+// weight of q1's arc with part p1 and symbol g times that of q2's arc with
+// symbol g and part p2, keyed (p1, p2).  With at most one arc per (part,
+// symbol) cell, the merged weight of key (p1, p2) is the sum over g alone.
+// The wave
+//   1. joins the two symbol lists (64 symbols of the shorter list per step,
+//      searched in 64-symbol chunks of the longer one held in lanes) and
+//      stages each matched symbol's arcs as cells of an M1 matrix (p1, g)
+//      and an M2 matrix (g, p2) in its own LDS, every cell loaded once;
+//   2. gives each table entry q = 64 / pow2ceil(P1 P2) lanes, lane c of the
+//      entry adding the terms of g = c, c + q, ...: each term the float32
+//      product the record would carry, added in float64 in increasing g,
+//      then the q partial sums combined by a fixed butterfly (the same sum
+//      on every run);
+//   3. emits every entry with at least one term as a merged arc (visited-
+//      table insert, label lookups, see emit_batch) at temp slot R + poff[u]
+//      + r in entry order, and marks the rest of its slots empty.
+// No LDS is shared between waves, so no workgroup barrier is needed.
+constexpr int kProdNT = 256;
+constexpr int kProdWaves = kProdNT / kWave;
+constexpr int kProdBatch = 4;  // arcs per side loaded at once when staging
+
+template <bool NARROW>
+__device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
+  if (NARROW) return *reinterpret_cast<const uint2 *>(reinterpret_cast<const char *>(arcs) + (j << 3));
+  return arcs[j];
+}
+
+template <bool NARROW>
+__global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
+  __shared__ u32 s_val[kProdWaves][kProdCells];        // cell weights (bits)
+  __shared__ u32 s_cell[kProdWaves][kProdCells / 32];  // bit c: cell c holds an arc
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u64 u = (u64)blockIdx.x * kProdWaves + w;
+  if (u >= a.nsrc) return;  // whole wave
+  const u32 K = a.pk[u];
+  if (K == 0) return;  // whole wave: record path
+  u32 *val = s_val[w], *cell = s_cell[w];
+  const u32 sid = a.lo + (u32)u;
+  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
+  const u32 P1 = a.pbase1[q1 + 1] - a.pbase1[q1], P2 = a.pbase2[q2 + 1] - a.pbase2[q2];
+  const u32 b1 = a.row1[q1], e1 = a.row1[q1 + 1], b2 = a.row2[q2], e2 = a.row2[q2 + 1];
+  if (P1 * P2 != K || K > kProdEntries) {  // impossible: the count kernel checked both
+    if (lane == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  // M1 cell (p1, g) at p1 GS + g, M2 cell (g, p2) at P1 GS + g P2 + p2
+  const u32 GS = kProdCells / (P1 + P2);
+  if (lane < kProdCells / 32) cell[lane] = 0;
+
+  // 1. join + staging
+  const bool one_short = (e1 - b1) <= (e2 - b2);
+  const u32 *ssym = one_short ? a.seg_sym1 : a.seg_sym2;
+  const u32 *lsym = one_short ? a.seg_sym2 : a.seg_sym1;
+  const u32 bs = one_short ? b1 : b2, es = one_short ? e1 : e2;
+  const u32 le = one_short ? e2 : e1;
+  u32 lp = one_short ? b2 : b1;  // first chunk of the longer list that can still match
+  u32 G = 0;
+  bool bad = false;
+  __builtin_amdgcn_wave_barrier();
+  for (u32 base = bs; base < es; base += kWave) {
+    const u32 idx = base + lane;
+    const bool valid = idx < es;
+    const u32 sym = valid ? ssym[idx] : 0xffffffffu;
+    const u32 smax = __shfl(sym, (int)(min(es - base, (u32)kWave) - 1), kWave);
+    u32 fpos = 0xffffffffu;
+    for (u32 c = lp; c < le; c += kWave) {
+      const u32 len = min(le - c, (u32)kWave);
+      const u32 lv = lane < len ? lsym[c + lane] : 0xffffffffu;
+      if (__shfl(lv, 0, kWave) > smax) break;
+      u32 pos = 0;
+#pragma unroll
+      for (u32 step = kWave / 2; step; step >>= 1) {
+        const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
+        pos = v < sym ? pos + step : pos;
+      }
+      const u32 at = __shfl(lv, (int)pos, kWave);
+      if (valid && at == sym) fpos = c + pos;
+      if (__shfl(lv, (int)(len - 1), kWave) >= smax) {
+        lp = c;
+        break;
+      }
+      lp = c + kWave;
+    }
+    const bool found = fpos != 0xffffffffu;
+    const u64 fm = __ballot(found);
+    if (found) {
+      const u32 s1 = one_short ? idx : fpos, s2 = one_short ? fpos : idx;
+      const u32 g = G + count_below(fm);
+      const u32 a1 = a.seg_off1[s1], n1 = a.seg_off1[s1 + 1] - a1;
+      const u32 a2 = a.seg_off2[s2], n2 = a.seg_off2[s2 + 1] - a2;
+      if (g >= GS) {  // impossible: the count kernel bounded (P1 + P2) G
+        bad = true;
+      } else {
+        for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
+          uint2 x1[kProdBatch], x2[kProdBatch];
+#pragma unroll
+          for (int k = 0; k < kProdBatch; ++k) {
+            const u32 i = i0 + (u32)k;
+            x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(0, 0);
+            x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(0, 0);
+          }
+#pragma unroll
+          for (int k = 0; k < kProdBatch; ++k) {
+            const u32 i = i0 + (u32)k;
+            if (i < n1) {
+              if (x1[k].x < P1) {
+                const u32 cc = x1[k].x * GS + g;
+                val[cc] = x1[k].y;
+                atomicOr(&cell[cc >> 5], 1u << (cc & 31));
+              } else {
+                bad = true;
+              }
+            }
+            if (i < n2) {
+              if (x2[k].x < P2) {
+                const u32 cc = P1 * GS + g * P2 + x2[k].x;
+                val[cc] = x2[k].y;
+                atomicOr(&cell[cc >> 5], 1u << (cc & 31));
+              } else {
+                bad = true;
+              }
+            }
+          }
+        }
+      }
+    }
+    G += (u32)__popcll(fm);
+  }
+  if (__ballot(bad)) {
+    if (lane == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+  // 2. entry sums
+  u32 q = kWave;
+  while (q > 1 && (kWave / q) < K) q >>= 1;  // q = 64 / pow2ceil(K)
+  const u32 e = lane / q, c = lane % q;
+  const bool act = e < K;
+  const u32 p1 = act ? e / P2 : 0, p2 = act ? e - (e / P2) * P2 : 0;
+  double acc = 0.0;
+  u32 any = 0;
+  if (act) {
+    const u32 ca = p1 * GS, cb = P1 * GS + p2;
+    for (u32 g = c; g < G; g += q) {
+      const u32 ia = ca + g, ib = cb + g * P2;
+      if ((cell[ia >> 5] >> (ia & 31)) & (cell[ib >> 5] >> (ib & 31)) & 1u) {
+        const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
+        acc += (double)t;
+        any = 1;
+      }
+    }
+  }
+  for (u32 d = 1; d < q; d <<= 1) {
+    acc += __shfl_xor(acc, (int)d, kWave);
+    any |= (u32)__shfl_xor((int)any, (int)d, kWave);
+  }
+
+  // 3. merged arcs in entry order
+  const bool run = act && c == 0 && any;
+  const u64 rm = __ballot(run);
+  const u32 nr = (u32)__popcll(rm);
+  const u64 base = a.R + a.poff[u];
+  bool act1[1] = {run};
+  u32 uu[1] = {(u32)u};
+  u64 key[1] = {((u64)p1 << a.b2) | p2};
+  u64 tpos[1] = {base + count_below(rm)};
+  float wt[1] = {(float)acc};
+  emit_batch<1>(a, act1, uu, key, tpos, wt);
+  if (lane >= nr && lane < K) a.temp[base + lane] = make_uint4(0, 0, 0, 0);  // empty slot
+  if (lane == 0) {
+    a.tstart[u] = base;
+    a.mend[u] = base + nr;
+  }
+}
 
 // ---------------------------------------------------------------------------
 // Fused expand + merge (the records of a tile never leave the chip).  The
@@ -846,7 +1041,7 @@ __device__ __forceinline__ uint2 fuse_arc(const uint2 *arcs, u32 j) {
 }
 
 template <bool NARROW>
-__global__ __launch_bounds__(NT, 8) void k_fuse_merge(MergeArgs a) {
+__global__ __launch_bounds__(NT, 6) void k_fuse_merge(MergeArgs a) {
   __shared__ FuseDenseLds U;
   FuseLds &F = U.f;
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
@@ -948,11 +1143,27 @@ __global__ __launch_bounds__(NT, 8) void k_fuse_merge(MergeArgs a) {
   }
   __syncthreads();  // every element generated
   const u32 e0 = w * (kWave * IT) + lane;
+  bool nonfinite = false;
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
     const u32 e = min(e0 + j * kWave, n - 1);
     in.key[j] = F.key[e];
     in.wt[j] = F.w[e];
+    nonfinite |= ((__float_as_uint(in.wt[j]) >> 23) & 0xffu) == 0xffu;
+  }
+  // a non-finite weight sends the tile to the sort kernel, which reads the
+  // records from HBM: write them there first
+  if (__syncthreads_or(nonfinite)) {
+    u32 *rk = static_cast<u32 *>(const_cast<void *>(a.rec_key)) + rb;
+    float *rw = const_cast<float *>(a.rec_w) + rb;
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 e = e0 + j * kWave;
+      if (e < n) {
+        rk[e] = in.key[j];
+        rw[e] = in.wt[j];
+      }
+    }
   }
   __syncthreads();  // the merge reuses the LDS
   dense_merge_tile(a, tile, td, in, U.d);
@@ -1083,9 +1294,10 @@ __global__ __launch_bounds__(256) void k_emit_tiles(MergeArgs a, u32 wpt) {
 }
 
 // New-state list without a shared counter: wave w either walks the runs of
-// merge tile w (w < ntiles) or 64 positions of the multi-block record space
+// merge tile w (w < ntiles), or 64 positions of the multi-block record space
 // (runs of multi-block source i sit at temp[roff[big[i]] + p - bigoff[i]]
-// while below mend).  Pass 0 counts the flagged (claimed) slots per wave into
+// while below mend), or 64 product-merge slots temp[R + p] (empty slots
+// carry no flag).  Pass 0 counts the flagged (claimed) slots per wave into
 // wcnt; pass 1 writes them to newlist at woff[w] (exclusive scan of wcnt) in
 // wave order.
 template <int PASS>
@@ -1093,7 +1305,7 @@ __global__ __launch_bounds__(256) void k_newlist(MergeArgs a, const u64 *bigoff,
                                                  u64 nbigw, u32 *wcnt, const u64 *woff) {
   const u32 lane = lane_id();
   const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
-  if (wv >= a.ntiles + nbigw) return;
+  if (wv >= a.ntiles + nbigw + (a.prodpos + kWave - 1) / kWave) return;
   const u64 base = PASS ? woff[wv] : 0;
   u32 cnt = 0;
   auto take = [&](bool f, u32 slot) {
@@ -1117,6 +1329,10 @@ __global__ __launch_bounds__(256) void k_newlist(MergeArgs a, const u64 *bigoff,
       if (r0 + lane < nr) x = a.temp[rb + r0 + lane].x;
       take((x & kNewFlag) != 0, x & ~kNewFlag);
     }
+  } else if (wv >= a.ntiles + nbigw) {
+    const u64 p = (wv - a.ntiles - nbigw) * kWave + lane;
+    const u32 x = p < a.prodpos ? a.temp[a.R + p].x : 0u;
+    take((x & kNewFlag) != 0, x & ~kNewFlag);
   } else {
     const u64 p = (wv - a.ntiles) * kWave + lane;
     u32 x = 0;
@@ -1304,6 +1520,31 @@ __global__ __launch_bounds__(256) void k_compact(MergeArgs a, const u64 *aoff, u
   }
 }
 
+// Result append source by source: 16 lanes per source.
+__global__ __launch_bounds__(256) void k_compact_sources(MergeArgs a, const u64 *aoff, u64 M,
+                                                         const u32 *hvals, u32 *osrc, u32 *odst,
+                                                         u32 *oil, u32 *ool, float *ow) {
+  const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  const u64 u = t / 16;
+  const u32 j = (u32)(t % 16);
+  if (u >= a.nsrc) return;
+  const u64 tb = a.tstart[u], n = a.mend[u] - tb, ob = aoff[u];
+  if (n == 0) return;
+  if (tb + n > a.R + a.prodpos || ob + n > M) {  // impossible: counts agree with aoff
+    if (j == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  for (u64 r = j; r < n; r += 16) {
+    const uint4 rec = a.temp[tb + r];
+    const u64 k = ob + r;
+    osrc[k] = a.lo + (u32)u;
+    odst[k] = hvals[rec.x & ~kNewFlag];
+    oil[k] = rec.y;
+    ool[k] = rec.z;
+    ow[k] = __uint_as_float(rec.w);
+  }
+}
+
 __global__ void k_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1,
                          const uint8_t *f2, uint8_t *fin) {
   for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x)
@@ -1355,6 +1596,8 @@ __global__ void k_reset_level(Status *st) {
     st->nwide = st->nheavy = st->nbig = st->nnew = 0;
     st->max_small = 0;
     st->dense_records = st->dense_runs = st->sort_runs = 0;
+    st->nprod = 0;
+    st->prod_records = st->prod_entries = 0;
     st->nsort = 0;
   }
 }
@@ -1460,6 +1703,22 @@ void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, 
   hipLaunchKernelGGL(k_new_total, dim3(1), dim3(1), 0, s, (const u64 *)(woff + nw), st);
 }
 
+void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s) {
+  if (!a.nsrc) return;
+  const unsigned g = (unsigned)ceil_div(a.nsrc, kProdWaves);
+  if (narrow)
+    hipLaunchKernelGGL(k_prod_sources<true>, dim3(g), dim3(kProdNT), 0, s, a);
+  else
+    hipLaunchKernelGGL(k_prod_sources<false>, dim3(g), dim3(kProdNT), 0, s, a);
+}
+
+void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,
+                            u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s) {
+  if (!a.nsrc || !M) return;
+  hipLaunchKernelGGL(k_compact_sources, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256),
+                     0, s, a, aoff, M, hvals, osrc, odst, oil, ool, ow);
+}
+
 void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s) {
   if (!n) return;
   hipLaunchKernelGGL(k_fix_dst, dim3(grid1(n)), dim3(256), 0, s, dst, n, hvals);
@@ -1499,12 +1758,15 @@ void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const 
                      nbig, M, hvals, osrc, odst, oil, ool, ow);
 }
 
-u64 newlist_waves(const MergeArgs &a, u64 RB) { return a.ntiles + ceil_div(RB, kWave); }
+u64 newlist_waves(const MergeArgs &a, u64 RB) {
+  return a.ntiles + ceil_div(RB, kWave) + ceil_div(a.prodpos, (u64)kWave);
+}
 
 void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
                     void *scan_tmp, hipStream_t s) {
   const u64 nbigw = ceil_div(RB, kWave);
-  const u64 nw = a.ntiles + nbigw;
+  const u64 nw = newlist_waves(a, RB);
+  if (nw == 0) return;  // st->nnew stays 0
   const unsigned g = (unsigned)ceil_div(nw, 256 / kWave);
   hipLaunchKernelGGL(k_newlist<0>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
                      (const u64 *)nullptr);

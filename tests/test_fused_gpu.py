@@ -3,7 +3,8 @@
 The fused kernel generates each merge tile's composed arcs on chip from the
 same match descriptors and CSR arcs, with the same float32 products, and
 merges them with the same dense-table merge; tiles the dense table cannot take
-are written out and sorted as before.  So with deterministic ids (within a
+are written out and sorted as before.  Sources of the product merge take the
+same kernel either way.  So with deterministic ids (within a
 depth, ordered by (q1, q2); otherwise the order follows which visited-table
 insert wins) a fused composition must equal the unfused one bit for bit (ids,
 arc order and weights), and both equal the oracle to the parity bar.
@@ -83,6 +84,10 @@ def test_fused_config4_full(fstc):
     m1, m2 = W.config4(0)
     fu = fused_vs_unfused(fstc, m1, m2, "config4 full")
     assert fu.stats["fused_levels"] >= 9 and fu.stats["write_launches"] == 0
+    # nearly every source is merged from its staged arc matrices
+    assert fu.stats["total_product_records"] >= 0.9 * fu.num_premerge_arcs
+    fr = fused_vs_unfused(fstc, m1, m2, "config4 full, records only", product=False)
+    assert fr.stats["write_launches"] == 0 and fr.stats["total_product_records"] == 0
 
 
 @pytest.mark.timeout(600)
@@ -119,3 +124,26 @@ def test_fused_signed_weights(fstc):
     m1 = with_weights(m1, signed_wide(rng, m1.num_arcs, -30, 30))
     m2 = with_weights(m2, signed_wide(rng, m2.num_arcs, -30, 30))
     fused_vs_unfused(fstc, m1, m2, "signed config4 cap 2", max_levels=2)
+
+
+def with_weights(m, w):
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, m.src, m.dst, m.ilabel,
+                 m.olabel, np.asarray(w, np.float32), m.final)
+
+
+def test_fused_infinite_weights(fstc):
+    """Infinite weights on the record path: a fused tile with a non-finite
+    product writes its records out for the sort kernel, as the unfused path
+    does."""
+    m1, m2 = W.config4(0)
+    w = m1.weight.copy()
+    w[::997] = np.inf
+    m1 = with_weights(m1, w)
+    fu = fused_vs_unfused(fstc, m1, m2, "config4 inf cap 3", max_levels=3, product=False)
+    assert fu.stats["total_sort_runs"] > 0
+    g = canon_of(fu.to_host())
+    ref = canon_of(oracle.compose(m1, m2, max_levels=3))
+    assert_same(g, ref, rtol=np.inf, what="config4 inf cap 3")
+    assert np.array_equal(np.isinf(g.w), np.isinf(ref.w))
+    fin = np.isfinite(ref.w)
+    np.testing.assert_allclose(g.w[fin], ref.w[fin], rtol=1e-5)

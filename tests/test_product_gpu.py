@@ -1,0 +1,168 @@
+"""Product merge (the default; opts.no_product_merge turns it off) on the GPU,
+through the C ABI.
+
+A source whose two states have few (target, outer symbol) parts and whose
+arcs fill their (part, inner symbol) cells densely, at most once each, is
+merged by one wavefront from its two staged arc matrices: the merged weight
+of (p1, p2) is the sum over matched inner symbols g of the float32 products
+w1(p1, g) * w2(g, p2) -- exactly the joined arc pairs the record path writes
+-- added in float64.  The states, arcs and arc order must equal those of the
+record path and of the oracle; weights meet the parity bar (and agree with
+the record path to float64 rounding).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from fstcheck import assert_same, canon_of
+from paper_1805_06383_amd import workloads as W
+from test_oracle_pins import tiny_pair
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def fstc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1805_06383_amd import fstc as F
+    F.load_library()
+    return F
+
+
+def with_weights(m, w):
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, m.src, m.dst, m.ilabel,
+                 m.olabel, np.asarray(w, np.float32), m.final)
+
+
+FIELDS = ("q1", "q2", "final", "src", "dst", "a", "c")
+
+
+def product_vs_records(F, m1, m2, what, rtol=1e-6, **kw):
+    """Deterministic ids: identical states, arcs and order with and without
+    the product merge; weights within rtol of each other."""
+    pr = F.compose(m1, m2, product=True, deterministic_ids=True, **kw)
+    rc = F.compose(m1, m2, product=False, deterministic_ids=True, **kw)
+    x, y = pr.to_host(), rc.to_host()
+    for f in FIELDS:
+        a, b = getattr(x, f), getattr(y, f)
+        assert a.shape == b.shape and np.array_equal(a, b), f"{what}: field {f} differs"
+    assert x.num_premerge == y.num_premerge, what
+    assert rc.stats["total_product_records"] == 0
+    np.testing.assert_allclose(x.w, y.w, rtol=rtol, err_msg=what)
+    return pr
+
+
+@pytest.mark.parametrize("cap", [1, 2, 3])
+def test_product_config4_caps(fstc, cap):
+    m1, m2 = W.config4(0)
+    pr = product_vs_records(fstc, m1, m2, f"config4 cap {cap}", max_levels=cap)
+    st = pr.stats
+    assert st["product_launches"] >= 1
+    assert st["total_product_records"] == pr.num_premerge_arcs  # every source qualifies
+    assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2, max_levels=cap)),
+                rtol=RTOL, what=f"config4 cap {cap}")
+
+
+@pytest.mark.parametrize("seed", range(1, 4))
+def test_product_config4_seeds(fstc, seed):
+    m1, m2 = W.config4(seed, nq=300)
+    pr = product_vs_records(fstc, m1, m2, f"config4 nq 300 seed {seed}")
+    assert pr.stats["total_product_sources"] > 0
+    assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2)), rtol=RTOL,
+                what=f"config4 nq 300 seed {seed}")
+
+
+def duplicate_slot(m, every, inner_is_output):
+    """Config-4 transducer whose states q % every == 0 carry slot 1 with the
+    (outer symbol, target) of slot 0: two arcs in one (part, inner symbol)
+    cell, which keeps those states out of the product merge."""
+    slots, nq = 4, m.num_states
+    per = m.num_arcs // nq  # m * slots arcs per state, slot fastest
+    dst, il, ol = m.dst.copy(), m.ilabel.copy(), m.olabel.copy()
+    outer = il if inner_is_output else ol
+    for q in range(0, nq, every):
+        base = q * per + np.arange(0, per, slots)
+        dst[base + 1] = dst[base]
+        outer[base + 1] = outer[base]
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, m.src, dst, il, ol, m.weight,
+                 m.final)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_product_mixed_with_records(fstc, fused):
+    """States with parallel arcs in one cell go through records while their
+    neighbours take the product merge: both kinds interleave within every
+    level (and within merge tiles), and the result is assembled source by
+    source."""
+    m1, m2 = W.config4(0)
+    m1 = duplicate_slot(m1, 3, True)
+    m2 = duplicate_slot(m2, 5, False)
+    pr = product_vs_records(fstc, m1, m2, "config4 shared cells cap 3", max_levels=3,
+                            fused=fused)
+    st = pr.stats
+    assert 0 < st["total_product_records"] < pr.num_premerge_arcs
+    assert st["total_dense_records"] > 0
+    assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2, max_levels=3)),
+                rtol=RTOL, what="config4 shared cells cap 3")
+
+
+def test_product_signed_weights(fstc):
+    """Signed weights over a wide range: cancelling float64 sums stay within
+    1e-5 of the magnitude sum (the parity bar for signed weights)."""
+    from test_parity_gpu import compare_signed, signed_wide
+    m1, m2 = W.config4(0)
+    rng = np.random.default_rng(79)
+    m1 = with_weights(m1, signed_wide(rng, m1.num_arcs, -30, 30))
+    m2 = with_weights(m2, signed_wide(rng, m2.num_arcs, -30, 30))
+    compare_signed(fstc, m1, m2, "signed config4 cap 2 (product)", max_levels=2)
+
+
+def test_product_infinite_weights(fstc):
+    """Infinite products make infinite sums, as in the oracle's float64 sums."""
+    m1, m2 = W.config4(0)
+    w = m1.weight.copy()
+    w[::997] = np.inf
+    m1 = with_weights(m1, w)
+    g = fstc.compose(m1, m2, max_levels=3)
+    assert g.stats["total_product_records"] > 0
+    gc = canon_of(g.to_host())
+    ref = canon_of(oracle.compose(m1, m2, max_levels=3))
+    assert_same(gc, ref, rtol=np.inf, what="config4 inf cap 3")
+    assert np.array_equal(np.isinf(gc.w), np.isinf(ref.w))
+    fin = np.isfinite(ref.w)
+    np.testing.assert_allclose(gc.w[fin], ref.w[fin], rtol=RTOL)
+
+
+def test_product_matrix_product(fstc):
+    """One-state transducers: the composition is the matrix product A B; with
+    4 x 16 parts on a 40-symbol inner alphabet the single source qualifies."""
+    rng = np.random.default_rng(12)
+    A = W.random_weights(rng, 4 * 40).reshape(4, 40)
+    B = W.random_weights(rng, 40 * 16).reshape(40, 16)
+    g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B)).to_host()
+    assert g.num_premerge == 4 * 40 * 16
+    P = A.astype(np.float64) @ B.astype(np.float64)
+    np.testing.assert_allclose(g.w.astype(np.float64), P[g.a, g.c], rtol=RTOL)
+    assert len(g.w) == 64
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_product_tiny_and_config1(fstc, seed):
+    """Small random pairs (some sources qualify, most do not): same result
+    with and without the product merge, equal to the oracle."""
+    m1, m2 = tiny_pair(seed) if seed < 15 else W.config1(seed)
+    pr = product_vs_records(fstc, m1, m2, f"seed {seed}")
+    assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2)), rtol=RTOL,
+                what=f"seed {seed}")
+
+
+@pytest.mark.parametrize("size,target", [("1k", "de"), ("15k", "it")])
+def test_product_paper_pairs(fstc, size, target):
+    m1, m2 = W.paper_pair(size, target)
+    pr = product_vs_records(fstc, m1, m2, f"paper {size} {target}")
+    assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2)), rtol=RTOL,
+                what=f"paper {size} {target}")
