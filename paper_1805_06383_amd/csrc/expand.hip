@@ -80,71 +80,17 @@ __device__ __forceinline__ u32 seg_len(const u32 *seg_off, u32 s) { return seg_o
 // merge window (st->max_small).  Both are gathered by the count kernels.
 constexpr int kCountNT = 256;
 
-// Table entries P1 P2 of source u if it takes the product merge (level.hpp:
-// cnt joined arc pairs over mc matched inner symbols), else 0.
-__device__ __forceinline__ u32 product_entries(const LevelArgs &a, u32 u, u64 cnt, u32 mc) {
-  if (!a.prod || cnt == 0) return 0;
-  const u32 sid = a.lo + u;
-  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
-  if (a.c1.cell_flag[q1] | a.c2.cell_flag[q2]) return 0;
-  // flags clear: both part counts are at most kProdParts
-  const u32 p1 = a.c1.part_base[q1 + 1] - a.c1.part_base[q1];
-  const u32 p2 = a.c2.part_base[q2 + 1] - a.c2.part_base[q2];
-  const u32 k = p1 * p2;
-  if (k == 0 || k > kProdEntries || (u64)(p1 + p2) * mc > kProdCells || (u64)k * mc > 2 * cnt)
-    return 0;
-  return k;
-}
-
-// Per-workgroup totals of the product-merge sources a thread classified,
-// added to st->nprod / prod_records / prod_entries with one atomic each.
-// All threads of the block must call it.
-template <int NT>
-__device__ __forceinline__ void publish_prod(const LevelArgs &a, u32 n, u64 rec, u64 ent,
-                                             unsigned long long *s_p) {
-  if (threadIdx.x < 3) s_p[threadIdx.x] = 0;
-  __syncthreads();
-  n = wave_sum(n);
-  rec = wave_sum(rec);
-  ent = wave_sum(ent);
-  if (lane_id() == 0 && n) {
-    atomicAdd(&s_p[0], (unsigned long long)n);
-    atomicAdd(&s_p[1], (unsigned long long)rec);
-    atomicAdd(&s_p[2], (unsigned long long)ent);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0 && s_p[0]) {
-    atomicAdd(&a.st->nprod, (u32)s_p[0]);
-    atomicAdd((unsigned long long *)&a.st->prod_records, s_p[1]);
-    atomicAdd((unsigned long long *)&a.st->prod_entries, s_p[2]);
-  }
-}
-
-// Writes the counts of a joined source: a product-merge source gets no
-// records and no matches (the record path skips it) and its entry count in
-// pk; returns the entry count (0: record path).
-__device__ __forceinline__ u32 put_count(const LevelArgs &a, u32 u, u64 cnt, u32 mc) {
-  const u32 k = product_entries(a, u, cnt, mc);
-  a.pk[u] = k;
-  a.cnt[u] = k ? 0 : cnt;
-  a.mc[u] = k ? 0 : mc;
-  return k;
-}
-
 // Thread per source: joins the short ones, lists the others for the
 // wavefront / workgroup joins.  List appends and the window maximum are
 // aggregated per workgroup in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   __shared__ u32 s_n[3], s_base[3], s_max;
-  __shared__ unsigned long long s_p[3];
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (threadIdx.x < 3) s_n[threadIdx.x] = 0;
   if (threadIdx.x == 0) s_max = 0;
   bool pred[3] = {false, false, false};  // wide, heavy, big
   u64 cnt = 0;
-  u32 pk = 0;
-  u64 prec = 0;
   if (u < a.nsrc) {
     const Ranges r = source_ranges(a, (u32)u);
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
@@ -158,15 +104,11 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
         cnt += (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2);
         ++mc;
       });
-      pk = put_count(a, (u32)u, cnt, mc);
-      if (pk) {
-        prec = cnt;
-        cnt = 0;
-      }
+      a.cnt[u] = cnt;
+      a.mc[u] = mc;
       pred[2] = cnt > kMergeSmall;
     }
   }
-  publish_prod<kCountNT>(a, pk ? 1u : 0u, prec, pk, s_p);
   const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
   __syncthreads();
   u64 m[3];
@@ -279,9 +221,7 @@ __device__ __forceinline__ Hit wave_probe(const LevelArgs &a, const Ranges &r, b
 // Wavefront per source (grid-stride over the wide list).
 __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
   __shared__ u32 s_max;
-  __shared__ unsigned long long s_p[3];
-  u32 run_max = 0, pn = 0;
-  u64 prec = 0, pent = 0;
+  u32 run_max = 0;
   const u32 lane = lane_id();
   const u32 gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const u32 nw = gridDim.x * blockDim.x / kWave;
@@ -304,18 +244,12 @@ __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
     cnt = wave_sum(cnt);
     mc = wave_sum(mc);
     if (lane == 0) {
-      const u32 k = put_count(a, u, cnt, mc);
-      if (k) {
-        pn += 1;
-        prec += cnt;
-        pent += k;
-      } else {
-        note_count(a, u, cnt, run_max);
-      }
+      a.cnt[u] = cnt;
+      a.mc[u] = mc;
+      note_count(a, u, cnt, run_max);
     }
   }
   publish_max<256>(a, run_max, &s_max);
-  publish_prod<256>(a, pn, prec, pent, s_p);
 }
 
 // Workgroup per source (grid-stride over the heavy list).
@@ -325,9 +259,7 @@ __global__ __launch_bounds__(kHeavyNT) void k_count_heavy(LevelArgs a) {
   __shared__ u64 s64[kHeavyNT / kWave];
   __shared__ u32 s32[kHeavyNT / kWave];
   __shared__ u32 s_max;
-  __shared__ unsigned long long s_p[3];
-  u32 run_max = 0, pn = 0;
-  u64 prec = 0, pent = 0;
+  u32 run_max = 0;
   const u32 n = a.st->nheavy;
   for (u32 i = blockIdx.x; i < n; i += gridDim.x) {
     const u32 u = a.heavy[i];
@@ -346,18 +278,59 @@ __global__ __launch_bounds__(kHeavyNT) void k_count_heavy(LevelArgs a) {
     cnt = block_sum<kHeavyNT, u64>(cnt, s64);
     mc = block_sum<kHeavyNT, u32>(mc, s32);
     if (threadIdx.x == 0) {
-      const u32 k = put_count(a, u, cnt, mc);
-      if (k) {
-        pn += 1;
-        prec += cnt;
-        pent += k;
-      } else {
-        note_count(a, u, cnt, run_max);
-      }
+      a.cnt[u] = cnt;
+      a.mc[u] = mc;
+      note_count(a, u, cnt, run_max);
     }
   }
   publish_max<kHeavyNT>(a, run_max, &s_max);
-  publish_prod<kHeavyNT>(a, pn, prec, pent, s_p);
+}
+
+// ---------------------------------------------------------------------------
+// Product-merge selection (level.hpp), thread per source, after the joins
+// are counted: a selected source keeps its entry count P1 P2 in pk and gets
+// no records and no matches, so the record path skips it.  Sources the
+// multi-block path listed (more than kMergeSmall records) stay there.
+// Totals go to st->nprod / prod_records / prod_entries, one atomic each per
+// workgroup.
+__global__ __launch_bounds__(kCountNT) void k_classify(LevelArgs a) {
+  __shared__ unsigned long long s_p[3];
+  const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  if (threadIdx.x < 3) s_p[threadIdx.x] = 0;
+  u32 k = 0;
+  u64 cnt = 0;
+  if (u < a.nsrc) {
+    cnt = a.cnt[u];
+    if (a.prod && cnt >= kProdMinRecords && cnt <= kMergeSmall) {
+      const u32 sid = a.lo + (u32)u;
+      const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
+      const u32 p1 = a.c1.part_base[q1 + 1] - a.c1.part_base[q1];
+      const u32 p2 = a.c2.part_base[q2 + 1] - a.c2.part_base[q2];
+      const u32 l1 = a.c1.row[q1 + 1] - a.c1.row[q1], l2 = a.c2.row[q2 + 1] - a.c2.row[q2];
+      const bool ok = (a.c1.cell_flag[q1] | a.c2.cell_flag[q2]) == 0 && p1 + p2 <= kProdRowSum &&
+                      min(l1, l2) <= (u32)kWave && cnt >= (u64)p1 * p2;
+      k = ok ? p1 * p2 : 0;
+    }
+    a.pk[u] = k;
+    if (k) {
+      a.cnt[u] = 0;
+      a.mc[u] = 0;
+    }
+  }
+  __syncthreads();
+  const u32 n = wave_sum(k ? 1u : 0u);
+  const u64 rec = wave_sum(k ? cnt : 0ull), ent = wave_sum((u64)k);
+  if (lane_id() == 0 && n) {
+    atomicAdd(&s_p[0], (unsigned long long)n);
+    atomicAdd(&s_p[1], (unsigned long long)rec);
+    atomicAdd(&s_p[2], (unsigned long long)ent);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0 && s_p[0]) {
+    atomicAdd(&a.st->nprod, (u32)s_p[0]);
+    atomicAdd((unsigned long long *)&a.st->prod_records, s_p[1]);
+    atomicAdd((unsigned long long *)&a.st->prod_entries, s_p[2]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -651,6 +624,7 @@ void launch_count(const LevelArgs &a, hipStream_t s) {
   hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
   hipLaunchKernelGGL(k_count_wide, dim3(wide_grid(a.nsrc)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_count_heavy, dim3(heavy_grid(a.nsrc)), dim3(kHeavyNT), 0, s, a);
+  hipLaunchKernelGGL(k_classify, dim3(g), dim3(kCountNT), 0, s, a);
 }
 
 void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s) {

@@ -41,15 +41,14 @@ struct Status {
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
 };
 
-// Product merge (merge.hip, k_prod_sources).  A source (q1, q2) whose states
-// have at most kProdParts parts each, whose (p1, p2) table has at most
-// kProdEntries entries, whose two arc matrices (P1 x G and G x P2 cells for
-// G matched inner symbols) fit kProdCells, whose matrices hold at least half
-// of their cells' products as joined arc pairs, and whose states have no two
-// arcs in one (part, inner symbol) cell, is merged by one wavefront from its
-// staged matrices instead of through records.
-constexpr u32 kProdEntries = 64;
-constexpr u32 kProdCells = 1024;
+// Product merge (merge.hip, k_prod_sources).  A source (q1, q2) is merged
+// by one wavefront from its staged arc matrices instead of through records
+// when its states have P1 + P2 <= kProdRowSum parts in all, the shorter of
+// its two inner-symbol lists has at most 64 symbols, neither state has two
+// arcs in one (part, inner symbol) cell, and it has at least
+// max(kProdMinRecords, P1 P2) and at most kMergeSmall joined arc pairs.
+constexpr u32 kProdRowSum = 16;
+constexpr u32 kProdMinRecords = 64;
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
 // wavefront, longer than kHeavyMin by a workgroup; others by one thread.

@@ -195,6 +195,30 @@ __device__ __forceinline__ void hash_insert_batch(u64 *keys, u64 mask, const u64
 // temp[tpos], with kNewFlag set in the slot when this insert claimed it (the
 // new-state list is built from these flags by k_newlist, without a shared
 // counter).
+// The part pairs of B merged arcs -> visited-table insert of the target pair
+// (r1, r2) and the run record (slot | kNewFlag if claimed, a, c, weight) at
+// temp[tpos], source u at runsrc[tpos].
+template <int B>
+__device__ __forceinline__ void emit_parts(const MergeArgs &a, const bool (&act)[B],
+                                           const u32 (&u)[B], const uint2 (&P1)[B],
+                                           const uint2 (&P2)[B], const u64 (&tpos)[B],
+                                           const float (&w)[B]) {
+  u64 hk[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
+  u32 slot[B];
+  bool is_new[B];
+  hash_insert_batch<B>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    if (act[i]) {
+      a.temp[tpos[i]] = make_uint4(slot[i] | (is_new[i] ? kNewFlag : 0u), P1[i].y, P2[i].y,
+                                   __float_as_uint(w[i]));
+      a.runsrc[tpos[i]] = u[i];
+    }
+  }
+}
+
 template <int B>
 __device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)[B],
                                            const u32 (&u)[B], const u64 (&key)[B],
@@ -212,24 +236,12 @@ __device__ __forceinline__ void emit_batch(const MergeArgs &a, const bool (&act)
     pb2[i] = act[i] ? a.pbase2[q2[i]] : 0;
   }
   uint2 P1[B], P2[B];
-  u64 hk[B];
 #pragma unroll
   for (int i = 0; i < B; ++i) {
     P1[i] = act[i] ? a.parts1[pb1[i] + (u32)(key[i] >> a.b2)] : make_uint2(0, 0);
     P2[i] = act[i] ? a.parts2[pb2[i] + (u32)(key[i] & ((1ull << a.b2) - 1))] : make_uint2(0, 0);
-    hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
   }
-  u32 slot[B];
-  bool is_new[B];
-  hash_insert_batch<B>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
-#pragma unroll
-  for (int i = 0; i < B; ++i) {
-    if (act[i]) {
-      a.temp[tpos[i]] = make_uint4(slot[i] | (is_new[i] ? kNewFlag : 0u), P1[i].y, P2[i].y,
-                                   __float_as_uint(w[i]));
-      a.runsrc[tpos[i]] = u[i];
-    }
-  }
+  emit_parts<B>(a, act, u, P1, P2, tpos, w);
 }
 
 // LDS of the sorting tile merge.
@@ -825,28 +837,29 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
 
 // ---------------------------------------------------------------------------
 // Product merge, wavefront per source (level.hpp: which sources take it).
-// For a source (q1, q2) with matched inner symbols g (the symbols q1 writes
-// and q2 reads), every joined arc pair is a term w1(p1, g) * w2(g, p2): the
-// weight of q1's arc with part p1 and symbol g times that of q2's arc with
-// symbol g and part p2, keyed (p1, p2).  With at most one arc per (part,
-// symbol) cell, the merged weight of key (p1, p2) is the sum over g alone.
-// The wave
-//   1. joins the two symbol lists (64 symbols of the shorter list per step,
-//      searched in 64-symbol chunks of the longer one held in lanes) and
-//      stages each matched symbol's arcs as cells of an M1 matrix (p1, g)
-//      and an M2 matrix (g, p2) in its own LDS, every cell loaded once;
-//   2. gives each table entry q = 64 / pow2ceil(P1 P2) lanes, lane c of the
-//      entry adding the terms of g = c, c + q, ...: each term the float32
-//      product the record would carry, added in float64 in increasing g,
-//      then the q partial sums combined by a fixed butterfly (the same sum
-//      on every run);
-//   3. emits every entry with at least one term as a merged arc (visited-
-//      table insert, label lookups, see emit_batch) at temp slot R + poff[u]
-//      + r in entry order, and marks the rest of its slots empty.
+// For a source (q1, q2) every joined arc pair is a term w1(p1, g) w2(g, p2):
+// the weight of q1's arc with part p1 and inner symbol g times that of q2's
+// arc with symbol g and part p2, keyed (p1, p2).  With at most one arc per
+// (part, symbol) cell, the merged weight of key (p1, p2) is a sum over g
+// alone.  Lane g of the wave takes symbol g of the shorter list (at most 64):
+//   1. it finds the symbol in the longer list (64-symbol chunks held in
+//      lanes, searched by shuffles), loads both segments' arcs and writes
+//      their weights to the cells (g, p1) and (g, p2) of two matrices in the
+//      wave's own LDS, every cell loaded once; a ballot per part gives the
+//      64-bit mask of the symbols where that part has an arc;
+//   2. each table entry (p1, p2) gets q = 64 / pow2ceil(P1 P2) lanes; lane c
+//      of the entry visits the symbols g = c mod q set in mask1(p1) &
+//      mask2(p2) -- exactly the entry's joined arc pairs -- adding the
+//      float32 product a record would carry, in float64, in increasing g;
+//      the q partial sums are combined by a fixed butterfly;
+//   3. every entry with a term becomes a merged arc (visited-table insert,
+//      labels from the parts, see emit_parts) at temp slot R + poff[u] + r in
+//      entry order; the entry's other slots are marked empty.
 // No LDS is shared between waves, so no workgroup barrier is needed.
 constexpr int kProdNT = 256;
 constexpr int kProdWaves = kProdNT / kWave;
-constexpr int kProdBatch = 4;  // arcs per side loaded at once when staging
+constexpr u32 kProdCells = kProdRowSum * kWave;  // both matrices, 64 symbols
+constexpr int kProdBatch = 4;                     // arcs per side loaded at once
 
 template <bool NARROW>
 __device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
@@ -856,108 +869,94 @@ __device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
 
 template <bool NARROW>
 __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
-  __shared__ u32 s_val[kProdWaves][kProdCells];        // cell weights (bits)
-  __shared__ u32 s_cell[kProdWaves][kProdCells / 32];  // bit c: cell c holds an arc
+  __shared__ u32 s_val[kProdWaves][kProdCells];  // weight bits: M1 (g, p1), then M2 (g, p2)
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u64 u = (u64)blockIdx.x * kProdWaves + w;
   if (u >= a.nsrc) return;  // whole wave
-  const u32 K = a.pk[u];
-  if (K == 0) return;  // whole wave: record path
-  u32 *val = s_val[w], *cell = s_cell[w];
   const u32 sid = a.lo + (u32)u;
-  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
-  const u32 P1 = a.pbase1[q1 + 1] - a.pbase1[q1], P2 = a.pbase2[q2 + 1] - a.pbase2[q2];
+  const u32 K = a.pk[u];
+  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];  // loaded with pk
+  if (K == 0) return;  // whole wave: record path
+  u32 *val = s_val[w];
+  const u32 pb1 = a.pbase1[q1], P1 = a.pbase1[q1 + 1] - pb1;
+  const u32 pb2 = a.pbase2[q2], P2 = a.pbase2[q2 + 1] - pb2;
   const u32 b1 = a.row1[q1], e1 = a.row1[q1 + 1], b2 = a.row2[q2], e2 = a.row2[q2 + 1];
-  if (P1 * P2 != K || K > kProdEntries) {  // impossible: the count kernel checked both
+  const bool one_short = (e1 - b1) <= (e2 - b2);
+  const u32 bs = one_short ? b1 : b2, es = one_short ? e1 : e2;
+  if (P1 * P2 != K || P1 + P2 > kProdRowSum || es <= bs || es - bs > (u32)kWave) {
+    // impossible: k_classify checked all three
     if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
   }
-  // M1 cell (p1, g) at p1 GS + g, M2 cell (g, p2) at P1 GS + g P2 + p2
-  const u32 GS = kProdCells / (P1 + P2);
-  if (lane < kProdCells / 32) cell[lane] = 0;
-
-  // 1. join + staging
-  const bool one_short = (e1 - b1) <= (e2 - b2);
   const u32 *ssym = one_short ? a.seg_sym1 : a.seg_sym2;
   const u32 *lsym = one_short ? a.seg_sym2 : a.seg_sym1;
-  const u32 bs = one_short ? b1 : b2, es = one_short ? e1 : e2;
   const u32 le = one_short ? e2 : e1;
-  u32 lp = one_short ? b2 : b1;  // first chunk of the longer list that can still match
-  u32 G = 0;
-  bool bad = false;
-  __builtin_amdgcn_wave_barrier();
-  for (u32 base = bs; base < es; base += kWave) {
-    const u32 idx = base + lane;
-    const bool valid = idx < es;
-    const u32 sym = valid ? ssym[idx] : 0xffffffffu;
-    const u32 smax = __shfl(sym, (int)(min(es - base, (u32)kWave) - 1), kWave);
-    u32 fpos = 0xffffffffu;
-    for (u32 c = lp; c < le; c += kWave) {
-      const u32 len = min(le - c, (u32)kWave);
-      const u32 lv = lane < len ? lsym[c + lane] : 0xffffffffu;
-      if (__shfl(lv, 0, kWave) > smax) break;
-      u32 pos = 0;
+
+  // 1. join, staging, part masks
+  const u32 idx = bs + lane;
+  const bool valid = idx < es;
+  const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
+  const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
+  u32 fpos = 0xffffffffu;
+  for (u32 c = one_short ? b2 : b1; c < le; c += kWave) {
+    const u32 len = min(le - c, (u32)kWave);
+    const u32 lv = lane < len ? lsym[c + lane] : 0xffffffffu;
+    if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
+    u32 pos = 0;  // elements of the chunk below sym
 #pragma unroll
-      for (u32 step = kWave / 2; step; step >>= 1) {
-        const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
-        pos = v < sym ? pos + step : pos;
-      }
-      const u32 at = __shfl(lv, (int)pos, kWave);
-      if (valid && at == sym) fpos = c + pos;
-      if (__shfl(lv, (int)(len - 1), kWave) >= smax) {
-        lp = c;
-        break;
-      }
-      lp = c + kWave;
+    for (u32 step = kWave / 2; step; step >>= 1) {
+      const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
+      pos = v < sym ? pos + step : pos;
     }
-    const bool found = fpos != 0xffffffffu;
-    const u64 fm = __ballot(found);
-    if (found) {
-      const u32 s1 = one_short ? idx : fpos, s2 = one_short ? fpos : idx;
-      const u32 g = G + count_below(fm);
-      const u32 a1 = a.seg_off1[s1], n1 = a.seg_off1[s1 + 1] - a1;
-      const u32 a2 = a.seg_off2[s2], n2 = a.seg_off2[s2 + 1] - a2;
-      if (g >= GS) {  // impossible: the count kernel bounded (P1 + P2) G
-        bad = true;
-      } else {
-        for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
-          uint2 x1[kProdBatch], x2[kProdBatch];
+    const u32 at = __shfl(lv, (int)pos, kWave);
+    if (valid && at == sym) fpos = c + pos;
+    if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
+  }
+  u64 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol
+  bool bad = false;
+  if (fpos != 0xffffffffu) {
+    const u32 s1 = one_short ? idx : fpos, s2 = one_short ? fpos : idx;
+    const u32 a1 = a.seg_off1[s1], n1 = a.seg_off1[s1 + 1] - a1;
+    const u32 a2 = a.seg_off2[s2], n2 = a.seg_off2[s2 + 1] - a2;
+    for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
+      uint2 x1[kProdBatch], x2[kProdBatch];
 #pragma unroll
-          for (int k = 0; k < kProdBatch; ++k) {
-            const u32 i = i0 + (u32)k;
-            x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(0, 0);
-            x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(0, 0);
-          }
+      for (int k = 0; k < kProdBatch; ++k) {
+        const u32 i = i0 + (u32)k;
+        x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(kProdRowSum, 0);
+        x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(kProdRowSum, 0);
+      }
 #pragma unroll
-          for (int k = 0; k < kProdBatch; ++k) {
-            const u32 i = i0 + (u32)k;
-            if (i < n1) {
-              if (x1[k].x < P1) {
-                const u32 cc = x1[k].x * GS + g;
-                val[cc] = x1[k].y;
-                atomicOr(&cell[cc >> 5], 1u << (cc & 31));
-              } else {
-                bad = true;
-              }
-            }
-            if (i < n2) {
-              if (x2[k].x < P2) {
-                const u32 cc = P1 * GS + g * P2 + x2[k].x;
-                val[cc] = x2[k].y;
-                atomicOr(&cell[cc >> 5], 1u << (cc & 31));
-              } else {
-                bad = true;
-              }
-            }
-          }
+      for (int k = 0; k < kProdBatch; ++k) {
+        // parts below P; the padding part kProdRowSum marks no arc
+        if (x1[k].x < P1) {
+          val[lane * P1 + x1[k].x] = x1[k].y;
+          pm1 |= 1ull << x1[k].x;
+        } else {
+          bad |= x1[k].x != kProdRowSum;
+        }
+        if (x2[k].x < P2) {
+          val[kWave * P1 + lane * P2 + x2[k].x] = x2[k].y;
+          pm2 |= 1ull << x2[k].x;
+        } else {
+          bad |= x2[k].x != kProdRowSum;
         }
       }
     }
-    G += (u32)__popcll(fm);
   }
-  if (__ballot(bad)) {
+  if (__ballot(bad)) {  // impossible: parts are below the state's part count
     if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
+  }
+  // lane p holds the symbol mask of M1 part p in ma, of M2 part p in mb
+  u64 ma = 0, mb = 0;
+  for (u32 p = 0; p < P1; ++p) {
+    const u64 m = __ballot((pm1 >> p) & 1ull);
+    ma = lane == p ? m : ma;
+  }
+  for (u32 p = 0; p < P2; ++p) {
+    const u64 m = __ballot((pm2 >> p) & 1ull);
+    mb = lane == p ? m : mb;
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -969,35 +968,31 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const u32 e = lane / q, c = lane % q;
   const bool act = e < K;
   const u32 p1 = act ? e / P2 : 0, p2 = act ? e - (e / P2) * P2 : 0;
+  const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
+  u64 lanes_c = 0;  // symbols c, c + q, ...
+  for (u32 g = c; g < (u32)kWave; g += q) lanes_c |= 1ull << g;
+  u64 todo = act ? (m & lanes_c) : 0;
   double acc = 0.0;
-  u32 any = 0;
-  if (act) {
-    const u32 ca = p1 * GS, cb = P1 * GS + p2;
-    for (u32 g = c; g < G; g += q) {
-      const u32 ia = ca + g, ib = cb + g * P2;
-      if ((cell[ia >> 5] >> (ia & 31)) & (cell[ib >> 5] >> (ib & 31)) & 1u) {
-        const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
-        acc += (double)t;
-        any = 1;
-      }
-    }
+  while (todo) {
+    const u32 g = (u32)__builtin_ctzll(todo);
+    todo &= todo - 1;
+    const float t = __uint_as_float(val[g * P1 + p1]) * __uint_as_float(val[kWave * P1 + g * P2 + p2]);
+    acc += (double)t;
   }
-  for (u32 d = 1; d < q; d <<= 1) {
-    acc += __shfl_xor(acc, (int)d, kWave);
-    any |= (u32)__shfl_xor((int)any, (int)d, kWave);
-  }
+  for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
 
   // 3. merged arcs in entry order
-  const bool run = act && c == 0 && any;
+  const bool run = act && c == 0 && m != 0;
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
   const u64 base = a.R + a.poff[u];
   bool act1[1] = {run};
   u32 uu[1] = {(u32)u};
-  u64 key[1] = {((u64)p1 << a.b2) | p2};
+  uint2 P1v[1] = {run ? a.parts1[pb1 + p1] : make_uint2(0, 0)};
+  uint2 P2v[1] = {run ? a.parts2[pb2 + p2] : make_uint2(0, 0)};
   u64 tpos[1] = {base + count_below(rm)};
   float wt[1] = {(float)acc};
-  emit_batch<1>(a, act1, uu, key, tpos, wt);
+  emit_parts<1>(a, act1, uu, P1v, P2v, tpos, wt);
   if (lane >= nr && lane < K) a.temp[base + lane] = make_uint4(0, 0, 0, 0);  // empty slot
   if (lane == 0) {
     a.tstart[u] = base;
