@@ -302,7 +302,7 @@ void Composer::run(fstc_result *out) {
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
-      aoff(&level_tmp), pk(&level_tmp), poff(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      aoff(&level_tmp), pk(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -321,14 +321,15 @@ void Composer::run(fstc_result *out) {
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
     mcount.ensure(np1 * 4); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
-    pk.ensure(np1 * 4); poff.ensure(np1 * 8);
+    pk.ensure(np1 * 4); poff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     stmp.ensure(scan_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
     launch_reset_level(dst, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
-                 dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), product ? 1u : 0u};
+                 dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), phdr.as<uint4>(),
+                 product ? 1u : 0u};
     T.begin();
     launch_count(la, s);
     exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
@@ -439,6 +440,7 @@ void Composer::run(fstc_result *out) {
     ma.arcs1 = c1.arcs;
     ma.arcs2 = c2.arcs;
     ma.pk = pk.as<u32>();
+    ma.phdr = phdr.as<uint4>();
     ma.poff = poff.as<u64>();
     ma.prodpos = prodpos;
     ma.row1 = c1.row;

@@ -310,6 +310,10 @@ __global__ __launch_bounds__(kCountNT) void k_classify(LevelArgs a) {
       const bool ok = (a.c1.cell_flag[q1] | a.c2.cell_flag[q2]) == 0 && p1 + p2 <= kProdRowSum &&
                       min(l1, l2) <= (u32)kWave && cnt >= (u64)p1 * p2;
       k = ok ? p1 * p2 : 0;
+      if (k) {
+        a.phdr[2 * u] = make_uint4(a.c1.part_base[q1], a.c2.part_base[q2], p1 | (p2 << 16), 0u);
+        a.phdr[2 * u + 1] = make_uint4(a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]);
+      }
     }
     a.pk[u] = k;
     if (k) {

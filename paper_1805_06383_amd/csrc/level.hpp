@@ -107,8 +107,13 @@ struct LevelArgs {
   ExpandTile *tiles;     // [ceil(R / kExpandTile)] write-tile entries
   u32 *big;              // [nsrc] sources for the multi-block merge (st->nbig)
   u32 *pk;               // [nsrc] table entries of a product-merge source, else 0
+  uint4 *phdr;           // [2 nsrc] product-merge source header (see ProdHeader)
   u32 prod;              // nonzero: sources may take the product merge
 };
+
+// Written by the selection for a product-merge source u at phdr[2u], [2u+1]:
+// (M1 part base, M2 part base, P1 | P2 << 16, unused), (M1 segment range
+// begin, end, M2 segment range begin, end).
 
 void launch_count(const LevelArgs &a, hipStream_t s);
 // nwide / nheavy: the list lengths the count kernels produced (st->nwide, nheavy).
@@ -156,6 +161,7 @@ struct MergeArgs {
   // product merge: the sources with pk[u] != 0 own temp slots
   // R + poff[u] .. R + poff[u] + pk[u] - 1 (prodpos slots in all)
   const u32 *pk;
+  const uint4 *phdr;
   const u64 *poff;
   u64 prodpos;
   const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;

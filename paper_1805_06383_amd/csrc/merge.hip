@@ -869,25 +869,40 @@ __device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
 
 template <bool NARROW>
 __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
-  __shared__ u32 s_val[kProdWaves][kProdCells];  // weight bits: M1 (g, p1), then M2 (g, p2)
-  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  __shared__ u32 s_val[kProdWaves][kProdCells + 1];  // M1 (g, p1), M2 (g, p2); a spare cell
+  // everything about the source is wave-uniform: scalar registers
+  auto uni = [](u32 x) { return (u32)__builtin_amdgcn_readfirstlane((int)x); };
+  const u32 lane = lane_id(), w = uni(threadIdx.x / kWave);
   const u64 u = (u64)blockIdx.x * kProdWaves + w;
   if (u >= a.nsrc) return;  // whole wave
-  const u32 sid = a.lo + (u32)u;
-  const u32 K = a.pk[u];
-  const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];  // loaded with pk
+  const u32 K = uni(a.pk[u]);
+  const uint4 h0 = a.phdr[2 * u], h1 = a.phdr[2 * u + 1];  // loaded with pk, used if K != 0
   if (K == 0) return;  // whole wave: record path
   u32 *val = s_val[w];
-  const u32 pb1 = a.pbase1[q1], P1 = a.pbase1[q1 + 1] - pb1;
-  const u32 pb2 = a.pbase2[q2], P2 = a.pbase2[q2 + 1] - pb2;
-  const u32 b1 = a.row1[q1], e1 = a.row1[q1 + 1], b2 = a.row2[q2], e2 = a.row2[q2 + 1];
+  const u32 pb1 = uni(h0.x), pb2 = uni(h0.y), P1 = uni(h0.z & 0xffffu), P2 = uni(h0.z >> 16);
+  const u32 b1 = uni(h1.x), e1 = uni(h1.y), b2 = uni(h1.z), e2 = uni(h1.w);
   const bool one_short = (e1 - b1) <= (e2 - b2);
   const u32 bs = one_short ? b1 : b2, es = one_short ? e1 : e2;
   if (P1 * P2 != K || P1 + P2 > kProdRowSum || es <= bs || es - bs > (u32)kWave) {
-    // impossible: k_classify checked all three
+    // impossible: the selection checked all of it
     if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
   }
+  // this lane's table entry (q lanes per entry), its labels and the first
+  // visited-table probe of its target pair, all issued before the join
+  u32 q = kWave;
+  while (q > 1 && (kWave / q) < K) q >>= 1;  // q = 64 / pow2ceil(K)
+  const u32 e = lane / q, c = lane % q;
+  const bool act = e < K;
+  const u32 p1 = act ? e / P2 : 0, p2 = act ? e - (e / P2) * P2 : 0;
+  const bool owner = act && c == 0;
+  const uint2 L1 = owner ? a.parts1[pb1 + p1] : make_uint2(0, 0);
+  const uint2 L2 = owner ? a.parts2[pb2 + p2] : make_uint2(0, 0);
+  const u64 hk = ((u64)L1.x << 32) | (u64)L2.x;
+  u64 hslot = mix64(hk) & a.hmask;
+  u64 hcur = owner ? __hip_atomic_load(&a.hkeys[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
+                   : 0ull;
+
   const u32 *ssym = one_short ? a.seg_sym1 : a.seg_sym2;
   const u32 *lsym = one_short ? a.seg_sym2 : a.seg_sym1;
   const u32 le = one_short ? e2 : e1;
@@ -898,9 +913,9 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
   const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
   u32 fpos = 0xffffffffu;
-  for (u32 c = one_short ? b2 : b1; c < le; c += kWave) {
-    const u32 len = min(le - c, (u32)kWave);
-    const u32 lv = lane < len ? lsym[c + lane] : 0xffffffffu;
+  for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
+    const u32 len = min(le - cb, (u32)kWave);
+    const u32 lv = lane < len ? lsym[cb + lane] : 0xffffffffu;
     if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
     u32 pos = 0;  // elements of the chunk below sym
 #pragma unroll
@@ -909,10 +924,10 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
       pos = v < sym ? pos + step : pos;
     }
     const u32 at = __shfl(lv, (int)pos, kWave);
-    if (valid && at == sym) fpos = c + pos;
+    if (valid && at == sym) fpos = cb + pos;
     if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
   }
-  u64 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol
+  u32 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol (parts < 16)
   bool bad = false;
   if (fpos != 0xffffffffu) {
     const u32 s1 = one_short ? idx : fpos, s2 = one_short ? fpos : idx;
@@ -928,19 +943,14 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < kProdBatch; ++k) {
-        // parts below P; the padding part kProdRowSum marks no arc
-        if (x1[k].x < P1) {
-          val[lane * P1 + x1[k].x] = x1[k].y;
-          pm1 |= 1ull << x1[k].x;
-        } else {
-          bad |= x1[k].x != kProdRowSum;
-        }
-        if (x2[k].x < P2) {
-          val[kWave * P1 + lane * P2 + x2[k].x] = x2[k].y;
-          pm2 |= 1ull << x2[k].x;
-        } else {
-          bad |= x2[k].x != kProdRowSum;
-        }
+        // parts are below P; the padding part kProdRowSum marks no arc and
+        // writes the spare cell
+        const bool v1 = x1[k].x < P1, v2 = x2[k].x < P2;
+        val[v1 ? lane * P1 + x1[k].x : kProdCells] = x1[k].y;
+        val[v2 ? kWave * P1 + lane * P2 + x2[k].x : kProdCells] = x2[k].y;
+        pm1 |= v1 ? 1u << x1[k].x : 0u;
+        pm2 |= v2 ? 1u << x2[k].x : 0u;
+        bad |= (!v1 && x1[k].x != kProdRowSum) || (!v2 && x2[k].x != kProdRowSum);
       }
     }
   }
@@ -951,48 +961,68 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   // lane p holds the symbol mask of M1 part p in ma, of M2 part p in mb
   u64 ma = 0, mb = 0;
   for (u32 p = 0; p < P1; ++p) {
-    const u64 m = __ballot((pm1 >> p) & 1ull);
+    const u64 m = __ballot((pm1 >> p) & 1u);
     ma = lane == p ? m : ma;
   }
   for (u32 p = 0; p < P2; ++p) {
-    const u64 m = __ballot((pm2 >> p) & 1ull);
+    const u64 m = __ballot((pm2 >> p) & 1u);
     mb = lane == p ? m : mb;
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  // 2. entry sums
-  u32 q = kWave;
-  while (q > 1 && (kWave / q) < K) q >>= 1;  // q = 64 / pow2ceil(K)
-  const u32 e = lane / q, c = lane % q;
-  const bool act = e < K;
-  const u32 p1 = act ? e / P2 : 0, p2 = act ? e - (e / P2) * P2 : 0;
+  // 2. entry sums: lane c of the entry adds the terms of g = c, c + q, ...
+  //    (bit j of mm: symbol c + j q is one of the entry's terms)
   const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
-  u64 lanes_c = 0;  // symbols c, c + q, ...
-  for (u32 g = c; g < (u32)kWave; g += q) lanes_c |= 1ull << g;
-  u64 todo = act ? (m & lanes_c) : 0;
+  u64 mm = act ? m >> c : 0;
+  const u32 qs = q < (u32)kWave ? q : 0u;  // q = 64: a single symbol per lane
+  u32 ia = c * P1 + p1, ib = kWave * P1 + c * P2 + p2;
+  const u32 da = q * P1, db = q * P2;
   double acc = 0.0;
-  while (todo) {
-    const u32 g = (u32)__builtin_ctzll(todo);
-    todo &= todo - 1;
-    const float t = __uint_as_float(val[g * P1 + p1]) * __uint_as_float(val[kWave * P1 + g * P2 + p2]);
-    acc += (double)t;
+  while (mm) {  // at most 64 / q steps: every step drops q bits (all, when q = 64)
+    const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
+    acc += (mm & 1u) ? (double)t : 0.0;
+    mm = qs ? mm >> qs : 0ull;
+    ia += da;
+    ib += db;
   }
   for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
 
-  // 3. merged arcs in entry order
-  const bool run = act && c == 0 && m != 0;
+  // 3. merged arcs in entry order: the visited-table insert resumes from
+  //    the probe loaded above
+  const bool run = owner && m != 0;
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
   const u64 base = a.R + a.poff[u];
-  bool act1[1] = {run};
-  u32 uu[1] = {(u32)u};
-  uint2 P1v[1] = {run ? a.parts1[pb1 + p1] : make_uint2(0, 0)};
-  uint2 P2v[1] = {run ? a.parts2[pb2 + p2] : make_uint2(0, 0)};
-  u64 tpos[1] = {base + count_below(rm)};
-  float wt[1] = {(float)acc};
-  emit_parts<1>(a, act1, uu, P1v, P2v, tpos, wt);
+  if (run) {
+    u32 slot = 0;
+    bool is_new = false, done = false;
+    for (u64 probe = 0; probe <= a.hmask && !done; ++probe) {
+      if (probe) {
+        hslot = (hslot + 1) & a.hmask;
+        hcur = __hip_atomic_load(&a.hkeys[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+      if (hcur == kEmptyKey) {
+        hcur = atomicCAS((unsigned long long *)&a.hkeys[hslot], (unsigned long long)kEmptyKey,
+                         (unsigned long long)hk);
+        if (hcur == kEmptyKey) {
+          is_new = true;
+          done = true;
+          slot = (u32)hslot;
+          continue;
+        }
+      }
+      if (hcur == hk) {
+        done = true;
+        slot = (u32)hslot;
+      }
+    }
+    if (!done) set_error(&a.st->err, kErrHashFull);
+    const u64 t = base + count_below(rm);
+    a.temp[t] = make_uint4(slot | (is_new ? kNewFlag : 0u), L1.y, L2.y, __float_as_uint((float)acc));
+    a.runsrc[t] = (u32)u;
+  }
   if (lane >= nr && lane < K) a.temp[base + lane] = make_uint4(0, 0, 0, 0);  // empty slot
   if (lane == 0) {
     a.tstart[u] = base;

@@ -168,3 +168,23 @@ def test_product_paper_pairs(fstc, size, target):
     pr = product_vs_records(fstc, m1, m2, f"paper {size} {target}")
     assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2)), rtol=RTOL,
                 what=f"paper {size} {target}")
+
+
+@pytest.mark.parametrize("with_inf", [False, True])
+def test_product_single_entry(fstc, with_inf):
+    """P1 = P2 = 1 on 64 inner symbols: one table entry, all 64 lanes on it
+    (one symbol each); with an infinite weight the masked sum runs."""
+    rng = np.random.default_rng(21)
+    A = W.random_weights(rng, 64).reshape(1, 64)
+    B = W.random_weights(rng, 64).reshape(64, 1)
+    if with_inf:
+        A[0, 17] = np.inf
+    g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B))
+    assert g.stats["total_product_sources"] == 1
+    g = g.to_host()
+    assert g.num_premerge == 64 and len(g.w) == 1
+    ref = oracle.compose(W.one_state_dense(A), W.one_state_dense(B))
+    if with_inf:
+        assert np.isinf(g.w[0]) and np.isinf(ref.w[0])
+    else:
+        np.testing.assert_allclose(g.w, ref.w, rtol=RTOL)
