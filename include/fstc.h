@@ -139,7 +139,9 @@ typedef struct fstc_result {
   uint32_t *ilabel;           /* [num_arcs] input symbol (from Sigma)       */
   uint32_t *olabel;           /* [num_arcs] output symbol (from Delta)      */
   float *weight;              /* [num_arcs] merged weight                   */
-  void *alloc_ptr[8];         /* allocation records, for release only       */
+  void *alloc_ptr[8];         /* allocation records, for release only (the
+                                 arrays may share allocations: the five arc
+                                 arrays are columns of one)               */
   size_t alloc_bytes[8];
 } fstc_result;
 

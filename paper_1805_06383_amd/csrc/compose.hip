@@ -150,21 +150,33 @@ enum Phase {
 };
 
 // HIP-event timing of the phases on the call's stream (only with stats).
+// Phase timing with HIP events on the call's stream.  Events are created
+// once per thread and reused by later calls (creating them costs more than a
+// short level), and a span that begins where the previous one ended shares
+// that event.
 struct Timer {
   hipStream_t s = nullptr;
   bool on = false;
-  std::vector<hipEvent_t> pool;
   std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> spans;
   hipEvent_t open = nullptr;
   size_t used = 0;
 
+  int device = -1;
+  // events belong to the device current at their creation: one pool per device
+  static std::vector<hipEvent_t> &pool(int dev) {
+    static thread_local std::vector<std::vector<hipEvent_t>> p;
+    if ((int)p.size() <= dev) p.resize(dev + 1);
+    return p[dev];
+  }
   hipEvent_t get() {
-    if (used == pool.size()) {
+    if (device < 0) FSTC_HIP(hipGetDevice(&device));
+    auto &p = pool(device);
+    if (used == p.size()) {
       hipEvent_t e;
       FSTC_HIP(hipEventCreate(&e));
-      pool.push_back(e);
+      p.push_back(e);
     }
-    return pool[used++];
+    return p[used++];
   }
   void begin() {
     if (!on) return;
@@ -176,16 +188,40 @@ struct Timer {
     hipEvent_t e = get();
     FSTC_HIP(hipEventRecord(e, s));
     spans.push_back({phase, {open, e}});
+    open = e;
   }
+  // end(phase) and begin() at once: the next span starts at this boundary
+  // (only where nothing is enqueued in between)
+  void chain(int phase) { end(phase); }
   void totals(double *ms) {
     for (auto &sp : spans) {
       float t = 0.f;
       if (hipEventElapsedTime(&t, sp.second.first, sp.second.second) == hipSuccess) ms[sp.first] += t;
     }
   }
-  ~Timer() {
-    for (auto e : pool) (void)hipEventDestroy(e);
+};
+
+// The five result columns (src, dst, ilabel, olabel, weight; 4 bytes each)
+// in one grow-only buffer: column i at byte i * cap * 4.  Growth is one
+// allocation and one strided copy of the rows kept.
+struct ArcCols {
+  Buf b;
+  u64 cap = 0;  // entries per column
+  hipStream_t s = nullptr;
+
+  explicit ArcCols(Allocator *A, hipStream_t st) : b(A), s(st) {}
+  void grow(u64 need, u64 used) {
+    if (need <= cap && b.p) return;
+    const u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), 2 * cap);
+    Buf nb(b.A);
+    nb.ensure(5 * nc * 4);
+    if (used && b.p)
+      FSTC_HIP(hipMemcpy2DAsync(nb.p, nc * 4, b.p, cap * 4, used * 4, 5, hipMemcpyDeviceToDevice, s));
+    std::swap(b.p, nb.p);
+    std::swap(b.cap, nb.cap);
+    cap = nc;
   }
+  u32 *col(int i) { return reinterpret_cast<u32 *>(static_cast<char *>(b.p) + (size_t)i * cap * 4); }
 };
 
 struct Composer {
@@ -196,6 +232,7 @@ struct Composer {
   Allocator A;
   Timer T;
   Staging *hs = nullptr;
+  Status *hs_dev = nullptr;  // hs->st as the device sees it
   Status *dst = nullptr;
   u32 nsyncs = 0;
 
@@ -222,6 +259,18 @@ struct Composer {
     }
   }
 
+  // the counters a kernel already copied to hs->st (launch_level_totals,
+  // launch_merged_total)
+  void sync_published() {
+    FSTC_HIP(hipGetLastError());
+    FSTC_HIP(hipStreamSynchronize(s));
+    ++nsyncs;
+    if (hs->st.err) {
+      throw Error((hs->st.err & kErrBadArc) ? FSTC_ERR_INVALID_ARG : FSTC_ERR_INTERNAL,
+                  device_error_text(hs->st.err));
+    }
+  }
+
   void read_words(const u64 *d, int n) {
     FSTC_HIP(hipGetLastError());
     FSTC_HIP(hipMemcpyAsync(hs->words, d, n * sizeof(u64), hipMemcpyDeviceToHost, s));
@@ -236,6 +285,7 @@ void Composer::run(fstc_result *out) {
   const auto t0 = std::chrono::steady_clock::now();
   if (!o.alloc) tune_default_pool();
   hs = staging();
+  FSTC_HIP(hipHostGetDevicePointer((void **)&hs_dev, hs, 0));
 
   Buf stb(&A), cntb(&A);
   dst = (Status *)stb.ensure(sizeof(Status));
@@ -298,7 +348,7 @@ void Composer::run(fstc_result *out) {
   u64 dense_records = 0, dense_runs = 0, sort_runs = 0, product_records = 0, product_sources = 0;
   u32 product_launches = 0;
 
-  Buf osrc(&A), odst(&A), oil(&A), ool(&A), ow(&A);
+  ArcCols out_arcs(&A, s);
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
@@ -334,9 +384,9 @@ void Composer::run(fstc_result *out) {
     launch_count(la, s);
     exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
     exclusive_scan(mc.as<u32>(), moff.as<u64>(), nsrc, stmp.p, s);
-    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, s);
+    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, hs_dev, s);
     T.end(kCount);
-    sync_status();
+    sync_published();
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
     if (nprod) exclusive_scan(pk.as<u32>(), poff.as<u64>(), nsrc, stmp.p, s);
@@ -390,15 +440,16 @@ void Composer::run(fstc_result *out) {
     la.tiles = tiles_e.as<ExpandTile>();
     T.begin();
     launch_emit(la, hs->st.nwide, hs->st.nheavy, s);
-    T.end(kExpand);
     // fused levels generate each tile's records inside the merge instead
     const bool fuse = o.fused_merge && !o.no_reduction && key_bits <= kDenseKeyBits && nbig == 0;
     if (!fuse) {
-      T.begin();
+      T.chain(kExpand);
       launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
                     rkey.p, rw.as<float>(), tiles_e.as<ExpandTile>(), &dst->err, s);
       T.end(kWriteKernel);
       ++write_launches;
+    } else {
+      T.end(kExpand);
     }
     total_matches += M;
 
@@ -458,24 +509,20 @@ void Composer::run(fstc_result *out) {
       fill_u64(mend.as<u64>(), 0, nsrc, s);
       fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
       launch_tile_sources(ma, s);
-      T.end(kMerge);
+      T.chain(kMerge);
       if (fuse) {
-        T.begin();
         launch_fuse_merge(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
-        T.end(kMergeKernel);
+        T.chain(kMergeKernel);
         ++merge_launches;
         ++fused_levels;
       } else if (key_bits <= kDenseKeyBits) {
-        T.begin();
         launch_merge_dense(ma, s);
-        T.end(kMergeKernel);
+        T.chain(kMergeKernel);
         ++merge_launches;
       }
-      T.begin();
       launch_merge_sort(ma, wide_keys, s);
-      T.end(kSortKernel);
+      T.chain(kSortKernel);
       ++sort_launches;
-      T.begin();
       if (nbig) {
         bigcnt.ensure((u64)nbig * 8);
         bigoff.ensure(((u64)nbig + 1) * 8);
@@ -487,12 +534,10 @@ void Composer::run(fstc_result *out) {
         merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, level_tmp, s);
       }
       if (nprod) {
-        T.end(kMerge);
-        T.begin();
+        T.chain(kMerge);
         launch_prod_sources(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
-        T.end(kProductKernel);
+        T.chain(kProductKernel);
         ++product_launches;
-        T.begin();
       }
       launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
       exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
@@ -505,9 +550,9 @@ void Composer::run(fstc_result *out) {
         launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
                        woff.as<u64>(), wtmp.p, s);
       }
-      launch_merged_total(aoff.as<u64>() + nsrc, ma, s);
+      launch_merged_total(aoff.as<u64>() + nsrc, ma, hs_dev, s);
       T.end(kMerge);
-      sync_status();
+      sync_published();
 
       nnew = hs->st.nnew;
       merged = hs->st.merged;
@@ -517,18 +562,16 @@ void Composer::run(fstc_result *out) {
     } else {
       if (o.max_arcs && arcs + R > o.max_arcs)
         throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");
-      const u64 na = arcs + R;
-      osrc.grow_keep(na * 4, arcs * 4);
-      odst.grow_keep(na * 4, arcs * 4);
-      oil.grow_keep(na * 4, arcs * 4);
-      ool.grow_keep(na * 4, arcs * 4);
-      ow.grow_keep(na * 4, arcs * 4);
+      out_arcs.grow(arcs + R, arcs);
+      u32 *osrc = out_arcs.col(0), *odst = out_arcs.col(1), *oil = out_arcs.col(2),
+          *ool = out_arcs.col(3);
+      float *ow = reinterpret_cast<float *>(out_arcs.col(4));
       T.begin();
       const u64 nwords = hcap / 32;
       newbits.ensure(nwords * 4);
       fill_u32(newbits.as<u32>(), 0, nwords, s);
-      launch_unreduced(ma, wide_keys, newbits.as<u32>(), osrc.as<u32>() + arcs, odst.as<u32>() + arcs,
-                       oil.as<u32>() + arcs, ool.as<u32>() + arcs, ow.as<float>() + arcs, s);
+      launch_unreduced(ma, wide_keys, newbits.as<u32>(), osrc + arcs, odst + arcs, oil + arcs,
+                       ool + arcs, ow + arcs, s);
       const u64 nw = bitlist_waves(nwords);
       wcnt.ensure(nw * 4);
       woff.ensure((nw + 1) * 8);
@@ -564,22 +607,18 @@ void Composer::run(fstc_result *out) {
     launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), sq1b.as<u32>(),
                   sq2b.as<u32>(), s);
     if (o.no_reduction) {
-      launch_fix_dst(odst.as<u32>() + arcs, merged, hvb.as<u32>(), s);
+      launch_fix_dst(out_arcs.col(1) + arcs, merged, hvb.as<u32>(), s);
     } else if (merged) {
-      const u64 na = arcs + merged;
-      osrc.grow_keep(na * 4, arcs * 4);
-      odst.grow_keep(na * 4, arcs * 4);
-      oil.grow_keep(na * 4, arcs * 4);
-      ool.grow_keep(na * 4, arcs * 4);
-      ow.grow_keep(na * 4, arcs * 4);
+      out_arcs.grow(arcs + merged, arcs);
+      u32 *osrc = out_arcs.col(0) + arcs, *odst = out_arcs.col(1) + arcs,
+          *oil = out_arcs.col(2) + arcs, *ool = out_arcs.col(3) + arcs;
+      float *ow = reinterpret_cast<float *>(out_arcs.col(4)) + arcs;
       if (nprod)  // product-merge sources interleave with the tiles' sources
-        launch_compact_sources(ma, aoff.as<u64>(), merged, hvb.as<u32>(), osrc.as<u32>() + arcs,
-                               odst.as<u32>() + arcs, oil.as<u32>() + arcs,
-                               ool.as<u32>() + arcs, ow.as<float>() + arcs, s);
+        launch_compact_sources(ma, aoff.as<u64>(), merged, hvb.as<u32>(), osrc, odst, oil, ool,
+                               ow, s);
       else
-        launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc.as<u32>() + arcs,
-                       odst.as<u32>() + arcs, oil.as<u32>() + arcs, ool.as<u32>() + arcs,
-                       ow.as<float>() + arcs, s);
+        launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc, odst, oil, ool, ow,
+                       s);
     }
     T.end(kAssign);
     arcs += merged;
@@ -601,16 +640,26 @@ void Composer::run(fstc_result *out) {
   out->num_arcs = arcs;
   out->num_premerge_arcs = premerge;
   out->num_levels = new_levels + 1;
-  Buf *keep[8] = {&sq1b, &sq2b, &finb, &osrc, &odst, &oil, &ool, &ow};
-  void **fields[8] = {(void **)&out->state_q1, (void **)&out->state_q2, (void **)&out->final,
-                      (void **)&out->src, (void **)&out->dst, (void **)&out->ilabel,
-                      (void **)&out->olabel, (void **)&out->weight};
-  for (int i = 0; i < 8; ++i) {
+  // states: one allocation per array; arcs: the five columns of one
+  // allocation (alloc_ptr[3]); alloc_ptr[4..7] stay NULL
+  Buf *keep[3] = {&sq1b, &sq2b, &finb};
+  void **fields[3] = {(void **)&out->state_q1, (void **)&out->state_q2, (void **)&out->final};
+  for (int i = 0; i < 3; ++i) {
     size_t b = 0;
     void *p = keep[i]->detach(&b);
     out->alloc_ptr[i] = p;
     out->alloc_bytes[i] = b;
     *fields[i] = p;
+  }
+  if (arcs) {
+    out->src = out_arcs.col(0);
+    out->dst = out_arcs.col(1);
+    out->ilabel = out_arcs.col(2);
+    out->olabel = out_arcs.col(3);
+    out->weight = reinterpret_cast<float *>(out_arcs.col(4));
+    size_t b = 0;
+    out->alloc_ptr[3] = out_arcs.b.detach(&b);
+    out->alloc_bytes[3] = b;
   }
   if (stats) {
     double ms[kNumPhases] = {};

@@ -234,9 +234,11 @@ void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, 
 void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
-void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s);
+// Both also copy *st to `host` (pinned memory the device can write).
+void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host,
+                         hipStream_t s);
 // Level total of merged arcs, plus the dense / sort tile statistics of st.
-void launch_merged_total(const u64 *a_total, const MergeArgs &a, hipStream_t s);
+void launch_merged_total(const u64 *a_total, const MergeArgs &a, Status *host, hipStream_t s);
 void launch_reset_level(Status *st, hipStream_t s);
 
 }  // namespace fstc

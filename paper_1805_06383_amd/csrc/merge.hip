@@ -1576,18 +1576,29 @@ __global__ void k_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f
     fin[i] = (f1[sq1[i]] != 0 && f2[sq2[i]] != 0) ? 1 : 0;
 }
 
-__global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st) {
+// Copies the level counters to host memory (pinned, device-visible), so the
+// host reads them after a stream synchronisation without a separate copy.
+__device__ __forceinline__ void publish(const Status *st, Status *host, u32 t, u32 nt) {
+  const u32 *src = reinterpret_cast<const u32 *>(st);
+  u32 *dst = reinterpret_cast<u32 *>(host);
+  for (u32 i = t; i < sizeof(Status) / 4; i += nt) dst[i] = src[i];
+}
+
+__global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st, Status *host) {
   st->R = *rt;
   st->M = *mt;
+  publish(st, host, 0, 1);
 }
 
 // Level totals after the merge: merged arcs (end of the scan of merged arcs
 // per source), and, over the merge tiles, the records and runs of the tiles
 // the dense-table kernel merged and the runs of those the sort kernel merged.
-__global__ __launch_bounds__(256) void k_merged_total(const u64 *at, Status *st, MergeArgs a) {
-  __shared__ u64 s_v[3][256 / kWave];
+// One workgroup: it also publishes the counters to host memory at the end.
+__global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, Status *st, MergeArgs a,
+                                                       Status *host) {
+  __shared__ u64 s_v[3][1024 / kWave];
   u64 v[3] = {0, 0, 0};
-  for (u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x; t < a.ntiles; t += (u64)gridDim.x * blockDim.x) {
+  for (u64 t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
     const uint4 td = a.tiles[t];
     const u32 runs = a.tile_runs[t];
     if (td.x < td.y && dense_tile(td, a.key_bits) && !(td.w & kRerouted)) {
@@ -1606,13 +1617,14 @@ __global__ __launch_bounds__(256) void k_merged_total(const u64 *at, Status *st,
   __syncthreads();
   if (threadIdx.x < 3) {
     u64 t = 0;
-    for (int i = 0; i < 256 / kWave; ++i) t += s_v[threadIdx.x][i];
-    if (t) {
-      u64 *dst = threadIdx.x == 0 ? &st->dense_records : threadIdx.x == 1 ? &st->dense_runs : &st->sort_runs;
-      atomicAdd((unsigned long long *)dst, (unsigned long long)t);
-    }
+    for (int i = 0; i < 1024 / kWave; ++i) t += s_v[threadIdx.x][i];
+    u64 *dst = threadIdx.x == 0 ? &st->dense_records : threadIdx.x == 1 ? &st->dense_runs : &st->sort_runs;
+    *dst += t;
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) st->merged = *at;
+  if (threadIdx.x == 3) st->merged = *at;
+  __syncthreads();
+  __threadfence();
+  publish(st, host, threadIdx.x, blockDim.x);
 }
 
 __global__ void k_reset_level(Status *st) {
@@ -1822,13 +1834,13 @@ void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, con
   hipLaunchKernelGGL(k_finals, dim3(grid1(n)), dim3(256), 0, s, sq1, sq2, n, f1, f2, fin);
 }
 
-void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, hipStream_t s) {
-  hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st);
+void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st, host);
 }
 
-void launch_merged_total(const u64 *a_total, const MergeArgs &a, hipStream_t s) {
-  const unsigned g = (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(a.ntiles, 256), 64));
-  hipLaunchKernelGGL(k_merged_total, dim3(g), dim3(256), 0, s, a_total, a.st, a);
+void launch_merged_total(const u64 *a_total, const MergeArgs &a, Status *host, hipStream_t s) {
+  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1024), 0, s, a_total, a.st, a, host);
 }
 
 void launch_reset_level(Status *st, hipStream_t s) {

@@ -294,15 +294,28 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
                           ctypes.byref(st) if want_stats else None)
     _check(rc)
     ns, na = int(res.num_states), int(res.num_arcs)
-    bufs = [alloc.take(res.alloc_ptr[i]) for i in range(8)]
+    owners = [(int(res.alloc_ptr[i]), alloc.take(res.alloc_ptr[i])) for i in range(8)
+              if res.alloc_ptr[i]]
     assert not alloc.live, f"library left {len(alloc.live)} temporaries allocated"
     i32, f32, u8 = torch.int32, torch.float32, torch.uint8
+
+    def view(ptr, n, dtype):
+        """Tensor of n elements at device address ptr, inside the allocation
+        that owns it (the result arrays may share allocations)."""
+        if not ptr or n == 0:
+            return torch.empty(0, dtype=dtype, device=device)
+        ptr = int(ptr)
+        for base, buf in owners:
+            if base <= ptr < base + buf.numel():
+                return _view(buf[ptr - base:], n, dtype, device)
+        raise RuntimeError("result array outside its recorded allocations")
+
     stats = {k: getattr(st, k) for k, _ in FstcStats._fields_} if want_stats else {}
     return Composed(ns, na, int(res.num_premerge_arcs), int(res.num_levels),
-                    _view(bufs[0], ns, i32, device), _view(bufs[1], ns, i32, device),
-                    _view(bufs[2], ns, u8, device), _view(bufs[3], na, i32, device),
-                    _view(bufs[4], na, i32, device), _view(bufs[5], na, i32, device),
-                    _view(bufs[6], na, i32, device), _view(bufs[7], na, f32, device), stats)
+                    view(res.state_q1, ns, i32), view(res.state_q2, ns, i32),
+                    view(res.final, ns, u8), view(res.src, na, i32), view(res.dst, na, i32),
+                    view(res.ilabel, na, i32), view(res.olabel, na, i32),
+                    view(res.weight, na, f32), stats)
 
 
 def fstc_result_release(result: FstcResult, opts: FstcOpts | None = None, stream=None):
