@@ -1,13 +1,18 @@
 """Throughput of reachable-state weighted FST composition on one MI355X.
 
 One step = one fstc_compose call over the whole workload (CSR build of both
-inputs, every breadth-first level: join count, arc-pair write, merge,
-visited-table insert, id assignment, result append), inputs already resident
-in HBM.  Prints one JSON line.
+inputs, every breadth-first level: join count, product merge or arc-pair
+write + merge, visited-table insert, id assignment, result append), inputs
+already resident in HBM.  Prints one JSON line.
 
 Default workload: the HMM-like dense-inner-alphabet pair (|Q1| = |Q2| = 1000,
 64 inner symbols, 4 (outer symbol, target) slots per state, 256 arcs per
 state, seed 0), the configuration the HBM-fraction target is stated on.
+
+The headline step is the library's default (product merge on).  Unless
+--no-record-path is given, the same workload is also timed with every source
+going through written records (opts.no_product_merge), and that step's
+expand + merge kernels and their HBM roofline are reported as "record_path".
 """
 from __future__ import annotations
 
@@ -25,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "composed arcs/sec (pre- and post-merge) + HBM GB/s fraction, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
+FP64_VECTOR_PEAK_TFLOPS = 78.6  # MI355X vector float64 (the product merge adds in float64)
 WORKLOAD_NAMES = {
     1: "tiny random pair: |Q|=200, |Sigma|=|Delta|=50, |Gamma|=100, 2,000 arcs each",
     2: "medium sparse pair: |Q|=10,000, 200,000 arcs each, inner Zipf(1.0) over 5,000, outer 2,000",
@@ -54,6 +60,8 @@ def parse():
     ap.add_argument("--no-product", action="store_true",
                     help="send every source through written records (opts.no_product_merge): "
                          "the paper's count / write / sort-and-reduce path")
+    ap.add_argument("--no-record-path", action="store_true",
+                    help="skip the second timing with the product merge off")
     ap.add_argument("--paper-pair", default="",
                     help="SIZE-TARGET, e.g. 15k-de: instead of --config, the bigram-LM x "
                          "translation-model pair German -> English -> TARGET at a Table 1 size")
@@ -89,6 +97,12 @@ def recorded_traffic(kernel: str, workload: str):
         return None
 
 
+def product_flops(st: dict) -> float:
+    """Float operations the product merge must do per compose: one float32
+    multiply and one float64 add per joined arc pair it merges."""
+    return 2.0 * st["total_product_records"]
+
+
 def algorithmic_bytes(st: dict, R: int) -> dict:
     """Bytes each of the three tile kernels must move, per compose call.
 
@@ -100,6 +114,7 @@ def algorithmic_bytes(st: dict, R: int) -> dict:
       (16 bytes: source, part-rank key, weight).
     """
     rec = st["record_key_bytes"] + 4
+    R = R - st["total_product_records"]  # joined pairs written as records
     tile_records = R - st["total_big_records"]
     dense = st["total_dense_records"]
     return {
@@ -163,58 +178,78 @@ def main():
     m2 = fstc.DeviceFST.from_host(h2, dev)
     torch.cuda.synchronize()
 
-    def step():
-        return fstc.fstc_compose(m1, m2, max_levels=args.max_levels,
-                                 reduce=not args.no_reduction, fused=args.fused,
-                                 product=not args.no_product)
+    def timed(product: bool):
+        """Warmup + K timed steps; returns (seconds, last result, summed stats)."""
+        def step():
+            return fstc.fstc_compose(m1, m2, max_levels=args.max_levels,
+                                     reduce=not args.no_reduction, fused=args.fused,
+                                     product=product)
+        for _ in range(args.warmup):
+            r = step()
+            del r
+        torch.cuda.synchronize()
+        sums = {}
+        last = None
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            last = step()
+            for k, v in last.stats.items():
+                sums[k] = sums.get(k, 0) + v
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0, last, sums
 
-    for _ in range(args.warmup):
-        r = step()
-        del r
-    torch.cuda.synchronize()
-    sums = {}
-    last = None
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        last = step()
-        for k, v in last.stats.items():
-            sums[k] = sums.get(k, 0) + v
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    secs = t1 - t0
+    def kernels_and_roofline(last, sums, traffic_key):
+        R = last.num_premerge_arcs
+        st = last.stats
+        ab = algorithmic_bytes(st, R)
+        kern = {}
+        for name, kernel, ms_key, n_key in (("write", "k_expand", "ms_write_kernel", "write_launches"),
+                                            ("merge", "k_merge_dense", "ms_merge_kernel", "merge_launches"),
+                                            ("sort", "k_merge_listed" if st["merge_launches"]
+                                             else "k_merge_tiles", "ms_sort_kernel", "sort_launches")):
+            ms = sums[ms_key] / args.steps
+            launches = max(1, st[n_key])
+            gbs = ab[name] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+            kern[name] = {"kernel": kernel, "ms_per_step": ms, "launches_per_step": st[n_key],
+                          "avg_launch_ms": ms / launches, "bytes_per_step": ab[name],
+                          "bytes_per_launch": ab[name] / launches, "GBps": gbs}
+        both_ms = sum(k["ms_per_step"] for k in kern.values())
+        kern["expand+merge"] = {"ms_per_step": both_ms, "bytes_per_step": sum(ab.values()),
+                                "GBps": sum(ab.values()) / (both_ms * 1e-3) / 1e9 if both_ms else 0.0}
+        pms = sums["ms_product_kernel"] / args.steps
+        pl = max(1, st["product_launches"])
+        pf = product_flops(st)
+        kern["product"] = {"kernel": "k_prod_sources", "ms_per_step": pms,
+                           "launches_per_step": st["product_launches"], "avg_launch_ms": pms / pl,
+                           "sources_per_step": st["total_product_sources"],
+                           "joined_pairs_per_step": st["total_product_records"],
+                           "flops_per_step": pf,
+                           "TFLOPps": pf / (pms * 1e-3) / 1e12 if pms > 0 else 0.0}
+        rec_ms = {k: kern[k]["ms_per_step"] for k in ab}
+        dom = max(rec_ms, key=rec_ms.get)
+        exact = traffic_key and not args.max_levels and not args.no_reduction
+        if pms > rec_ms[dom]:
+            # the product merge dominates: float64 adds, not HBM streams, are
+            # its arithmetic (its bound in practice is per-source latency)
+            roof = {"bound": "alu", "kernel": "k_prod_sources",
+                    "achieved": kern["product"]["TFLOPps"], "peak": FP64_VECTOR_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": kern["product"]["TFLOPps"] / FP64_VECTOR_PEAK_TFLOPS,
+                    "traffic": recorded_traffic("k_prod_sources", traffic_key) if exact else None}
+        else:
+            kname = kern[dom]["kernel"]
+            roof = {"bound": "hbm", "kernel": kname,
+                    "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": kern[dom]["GBps"] / HBM_PEAK_GBS,
+                    "traffic": recorded_traffic(kname, traffic_key) if exact else None}
+        return kern, roof
+
+    product = not args.no_product
+    secs, last, sums = timed(product)
     R, merged = last.num_premerge_arcs, last.num_arcs
     pre_rate = R * args.steps / secs
     post_rate = merged * args.steps / secs
-
-    st = last.stats
-    ab = algorithmic_bytes(st, R)
-    kern = {}
-    for name, kernel, ms_key, n_key in (("write", "k_expand", "ms_write_kernel", "write_launches"),
-                                        ("merge", "k_merge_dense", "ms_merge_kernel", "merge_launches"),
-                                        ("sort", "k_merge_listed" if st["merge_launches"]
-                                         else "k_merge_tiles", "ms_sort_kernel", "sort_launches")):
-        ms = sums[ms_key] / args.steps
-        launches = max(1, st[n_key])
-        gbs = ab[name] / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
-        kern[name] = {"kernel": kernel, "ms_per_step": ms, "launches_per_step": st[n_key],
-                      "avg_launch_ms": ms / launches, "bytes_per_step": ab[name],
-                      "bytes_per_launch": ab[name] / launches, "GBps": gbs}
-    both_ms = sum(k["ms_per_step"] for k in kern.values())
-    kern["product"] = {"kernel": "k_prod_sources",
-                       "ms_per_step": sums["ms_product_kernel"] / args.steps,
-                       "launches_per_step": st["product_launches"],
-                       "sources_per_step": st["total_product_sources"],
-                       "joined_pairs_per_step": st["total_product_records"]}
-    kern["expand+merge"] = {"ms_per_step": both_ms, "bytes_per_step": sum(ab.values()),
-                            "GBps": sum(ab.values()) / (both_ms * 1e-3) / 1e9 if both_ms else 0.0}
-    dom = max(ab, key=lambda k: kern[k]["ms_per_step"])
-    kname = kern[dom]["kernel"]
-    roof = {"bound": "hbm", "kernel": kname,
-            "achieved": kern[dom]["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": kern[dom]["GBps"] / HBM_PEAK_GBS,
-            "traffic": (recorded_traffic(kname, traffic_key)
-                        if traffic_key and not args.max_levels and not args.no_reduction
-                        else None)}
+    key = traffic_key if product else (traffic_key + "_records" if traffic_key else None)
+    kern, roof = kernels_and_roofline(last, sums, key)
 
     out = {
         "metric": METRIC,
@@ -248,6 +283,17 @@ def main():
         "kernels": kern,
         "roofline": roof,
     }
+    if product and not args.no_record_path and not args.no_reduction:
+        rsecs, rlast, rsums = timed(False)
+        rkern, rroof = kernels_and_roofline(rlast, rsums,
+                                            traffic_key + "_records" if traffic_key else None)
+        out["record_path"] = {
+            "what": "same workload, every source through written records (opts.no_product_merge)",
+            "value": rlast.num_premerge_arcs * args.steps / rsecs,
+            "ms_per_step": rsecs * 1e3 / args.steps,
+            "kernels": {k: rkern[k] for k in ("write", "merge", "sort", "expand+merge")},
+            "roofline": rroof,
+        }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels, not args.no_reduction)
     print(json.dumps(out), flush=True)
