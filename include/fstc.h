@@ -120,7 +120,11 @@ typedef struct fstc_opts {
                                  of float32 products, added in float64),
                                  without records.  Same states and arcs;
                                  weights agree to float64 rounding        */
-  uint32_t reserved;
+  uint32_t hash_visited;      /* nonzero: the visited set is always the hash
+                                 table of pair keys.  0: when |Q1| |Q2| is
+                                 at most 2^26 it is a dense array indexed by
+                                 q1 |Q2| + q2 (the paper's |Q1||Q2| table,
+                                 section 3.4), 4 bytes a pair; same result */
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the

@@ -32,7 +32,12 @@ constexpr u64 kEmptyKey = ~0ull;
 // Set in a merged arc's visited-table slot when its insert claimed the slot
 // (visited-table capacity is at most 2^31 slots).
 constexpr u32 kNewFlag = 0x80000000u;
+// Dense visited array entries (ids stay below both).
+constexpr u32 kUnvisited = 0xffffffffu;
+constexpr u32 kClaimed = 0xfffffffeu;
 constexpr u64 kMaxHashCap = 1ull << 31;
+// Largest pair space |Q1| |Q2| whose visited set is a dense array (4 bytes a pair).
+constexpr u64 kDensePairs = 1ull << 26;
 
 // ---------------------------------------------------------------------------
 // Host-side error plumbing (exceptions stay inside the library).

@@ -333,13 +333,23 @@ void Composer::run(fstc_result *out) {
   // compositions never grow them
   sq1b.ensure(kMinGrow * 4);
   sq2b.ensure(kMinGrow * 4);
-  u64 hcap = std::min<u64>(kMaxHashCap, next_pow2(std::max<u64>(
-                                           4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1))));
-  hkb.ensure(hcap * 8);
-  hvb.ensure(hcap * 4);
-  fill_u64(hkb.as<u64>(), kEmptyKey, hcap, s);
-  launch_insert_start(hkb.as<u64>(), hcap - 1, hvb.as<u32>(), m1.start, m2.start, sq1b.as<u32>(),
-                      sq2b.as<u32>(), &dst->err, s);
+  // visited set: a dense array over all pairs when there are at most
+  // kDensePairs of them (slot = q1 |Q2| + q2, no probing), else a hash table
+  const bool dense_vis = pairspace <= kDensePairs && !o.hash_visited;
+  const u32 vn2 = dense_vis ? m2.num_states : 0u;
+  u64 hcap = dense_vis ? pairspace
+                       : std::min<u64>(kMaxHashCap, next_pow2(std::max<u64>(
+                             4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1))));
+  if (dense_vis) {
+    hvb.ensure(hcap * 4);
+    fill_u32(hvb.as<u32>(), kUnvisited, hcap, s);
+  } else {
+    hkb.ensure(hcap * 8);
+    hvb.ensure(hcap * 4);
+    fill_u64(hkb.as<u64>(), kEmptyKey, hcap, s);
+  }
+  launch_insert_start(hkb.as<u64>(), hcap - 1, hvb.as<u32>(), vn2, m1.start, m2.start,
+                      sq1b.as<u32>(), sq2b.as<u32>(), &dst->err, s);
 
   u64 n_states = 1, arcs = 0, premerge = 0;
   u32 lo = 0, hi = 1, depth = 0, new_levels = 0, expanded_levels = 0;
@@ -421,7 +431,7 @@ void Composer::run(fstc_result *out) {
     // level could add
     // (at most kMaxHashCap slots: an insert into a full table reports it)
     const u64 need = std::min<u64>(2 * (n_states + newcap), kMaxHashCap);
-    if (need > hcap) {
+    if (!dense_vis && need > hcap) {
       const u64 ncap = next_pow2(need);
       Buf nk(&A), nv(&A);
       nk.ensure(ncap * 8);
@@ -472,6 +482,8 @@ void Composer::run(fstc_result *out) {
     ma.b2 = b2;
     ma.hkeys = hkb.as<u64>();
     ma.hmask = hcap - 1;
+    ma.vis = hvb.as<u32>();
+    ma.vn2 = vn2;
     ma.newlist = newlist.as<u32>();
     ma.newcap = newcap;
     ma.temp = temp.as<uint4>();
@@ -567,7 +579,7 @@ void Composer::run(fstc_result *out) {
           *ool = out_arcs.col(3);
       float *ow = reinterpret_cast<float *>(out_arcs.col(4));
       T.begin();
-      const u64 nwords = hcap / 32;
+      const u64 nwords = ceil_div(hcap, 32);
       newbits.ensure(nwords * 4);
       fill_u32(newbits.as<u32>(), 0, nwords, s);
       launch_unreduced(ma, wide_keys, newbits.as<u32>(), osrc + arcs, odst + arcs, oil + arcs,
@@ -599,12 +611,12 @@ void Composer::run(fstc_result *out) {
       dk.ensure((u64)nnew * 8); dv.ensure((u64)nnew * 4);
       dka.ensure((u64)nnew * 8); dva.ensure((u64)nnew * 4);
       dtmp.ensure(radix_temp_bytes(nnew));
-      launch_newkeys(newlist.as<u32>(), nnew, hkb.as<u64>(), bq2, dk.as<u64>(), dv.as<u32>(), s);
+      launch_newkeys(newlist.as<u32>(), nnew, hkb.as<u64>(), vn2, bq2, dk.as<u64>(), dv.as<u32>(), s);
       radix_sort_pairs(dk.as<u64>(), dv.as<u32>(), dka.as<u64>(), dva.as<u32>(), nnew, 0,
                        bq1 + bq2, dtmp.p, s);
       slots = dv.as<u32>();
     }
-    launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), sq1b.as<u32>(),
+    launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), vn2, sq1b.as<u32>(),
                   sq2b.as<u32>(), s);
     if (o.no_reduction) {
       launch_fix_dst(out_arcs.col(1) + arcs, merged, hvb.as<u32>(), s);

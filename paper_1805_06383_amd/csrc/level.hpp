@@ -135,8 +135,13 @@ struct MergeArgs {
   const u32 *pbase1, *pbase2;
   const uint2 *parts1, *parts2;
   int key_bits, b2;
+  // visited set: a hash table of pair keys (hkeys, hmask; ids by slot in
+  // vis) or, when vn2 != 0, a dense array vis[r1 vn2 + r2] (slot = pair
+  // index) holding kUnvisited, kClaimed or the pair's id
   u64 *hkeys;
   u64 hmask;
+  u32 *vis;
+  u32 vn2;
   u32 *newlist;
   u64 newcap;
   uint4 *temp;     // [R] merged runs: (source, key lo, key hi, weight bits) from the
@@ -187,14 +192,15 @@ void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, h
 void merge_big(const MergeArgs &a, bool wide_keys, u32 nbig, const u64 *bigoff, u64 RB,
                Arena &T, hipStream_t s);
 
-void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1, u32 *sq2,
-                         u32 *err, hipStream_t s);
+// vn2 != 0: dense visited array (MergeArgs), hkeys unused.
+void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 vn2, u32 s1, u32 s2, u32 *sq1,
+                         u32 *sq2, u32 *err, hipStream_t s);
 void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32 *nvals,
                    u64 nmask, u32 *err, hipStream_t s);
 // ids base .. base + nnew - 1 in new-list order (or the order in `order`).
-void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 *sq1,
-                   u32 *sq2, hipStream_t s);
-void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
+void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 vn2,
+                   u32 *sq1, u32 *sq2, hipStream_t s);
+void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, u32 vn2, int bq2, u64 *keys,
                     u32 *vals, hipStream_t s);
 // Result append of the level's merged arcs: the runs of merge tile t go to
 // output positions aoff[first source of t] + r, those of multi-block source u

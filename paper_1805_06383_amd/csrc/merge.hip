@@ -190,6 +190,32 @@ __device__ __forceinline__ void hash_insert_batch(u64 *keys, u64 mask, const u64
   set_error(err, kErrHashFull);
 }
 
+// Visited-set insert of B target pairs (key = r1 << 32 | r2): the hash
+// table, or the dense array when a.vn2 != 0 (slot = r1 vn2 + r2; a claim is
+// a CAS from kUnvisited to kClaimed, tried only when a plain read of the
+// entry still sees kUnvisited -- entries never return to it).
+template <int B>
+__device__ __forceinline__ void visit_batch(const MergeArgs &a, const u64 (&key)[B],
+                                            const bool (&act)[B], u32 (&slot)[B],
+                                            bool (&is_new)[B]) {
+  if (!a.vn2) {
+    hash_insert_batch<B>(a.hkeys, a.hmask, key, act, slot, is_new, &a.st->err);
+    return;
+  }
+  u32 cur[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    slot[i] = act[i] ? (u32)(key[i] >> 32) * a.vn2 + (u32)key[i] : 0u;
+    is_new[i] = false;
+    cur[i] = act[i] ? __hip_atomic_load(&a.vis[slot[i]], __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_WORKGROUP)
+                    : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < B; ++i)
+    if (act[i] && cur[i] == kUnvisited) is_new[i] = atomicCAS(&a.vis[slot[i]], kUnvisited, kClaimed) == kUnvisited;
+}
+
 // Merged arcs of B runs: part ranks back to (r1, a) and (r2, c), the target
 // pair inserted in the visited table, and (slot, a, c, weight) written to
 // temp[tpos], with kNewFlag set in the slot when this insert claimed it (the
@@ -208,7 +234,7 @@ __device__ __forceinline__ void emit_parts(const MergeArgs &a, const bool (&act)
   for (int i = 0; i < B; ++i) hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
   u32 slot[B];
   bool is_new[B];
-  hash_insert_batch<B>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
+  visit_batch<B>(a, hk, act, slot, is_new);
 #pragma unroll
   for (int i = 0; i < B; ++i) {
     if (act[i]) {
@@ -899,9 +925,11 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const uint2 L1 = owner ? a.parts1[pb1 + p1] : make_uint2(0, 0);
   const uint2 L2 = owner ? a.parts2[pb2 + p2] : make_uint2(0, 0);
   const u64 hk = ((u64)L1.x << 32) | (u64)L2.x;
-  u64 hslot = mix64(hk) & a.hmask;
-  u64 hcur = owner ? __hip_atomic_load(&a.hkeys[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
-                   : 0ull;
+  u64 hslot = a.vn2 ? (u64)L1.x * a.vn2 + L2.x : mix64(hk) & a.hmask;
+  u64 hcur = 0;
+  if (owner)
+    hcur = a.vn2 ? (u64)__hip_atomic_load(&a.vis[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
+                 : __hip_atomic_load(&a.hkeys[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 
   const u32 *ssym = one_short ? a.seg_sym1 : a.seg_sym2;
   const u32 *lsym = one_short ? a.seg_sym2 : a.seg_sym1;
@@ -995,7 +1023,15 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
   const u64 base = a.R + a.poff[u];
-  if (run) {
+  if (run && a.vn2) {
+    // dense array: the entry read above, then a claim if it was unvisited
+    const bool is_new = hcur == kUnvisited &&
+                        atomicCAS(&a.vis[hslot], kUnvisited, kClaimed) == kUnvisited;
+    const u64 t = base + count_below(rm);
+    a.temp[t] = make_uint4((u32)hslot | (is_new ? kNewFlag : 0u), L1.y, L2.y,
+                           __float_as_uint((float)acc));
+    a.runsrc[t] = (u32)u;
+  } else if (run) {
     u32 slot = 0;
     bool is_new = false, done = false;
     for (u64 probe = 0; probe <= a.hmask && !done; ++probe) {
@@ -1421,7 +1457,7 @@ __global__ __launch_bounds__(256) void k_unreduced(MergeArgs a, u32 *newbits, u3
     P2[i] = a.parts2[a.pbase2[q2] + (u32)(key & ((1ull << a.b2) - 1))];
     hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
   }
-  hash_insert_batch<kUnredB>(a.hkeys, a.hmask, hk, act, slot, is_new, &a.st->err);
+  visit_batch<kUnredB>(a, hk, act, slot, is_new);
 #pragma unroll
   for (int i = 0; i < kUnredB; ++i) {
     if (!act[i]) continue;
@@ -1466,10 +1502,10 @@ __global__ void k_fix_dst(u32 *dst, u64 n, const u32 *hvals) {
 }
 
 // ---------------------------------------------------------------------------
-__global__ void k_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1,
-                               u32 *sq2, u32 *err) {
+__global__ void k_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 vn2, u32 s1, u32 s2,
+                               u32 *sq1, u32 *sq2, u32 *err) {
   bool is_new;
-  const u32 slot = hash_insert(hkeys, hmask, ((u64)s1 << 32) | s2, is_new, err);
+  const u32 slot = vn2 ? s1 * vn2 + s2 : hash_insert(hkeys, hmask, ((u64)s1 << 32) | s2, is_new, err);
   hvals[slot] = 0;
   sq1[0] = s1;
   sq2[0] = s2;
@@ -1487,23 +1523,28 @@ __global__ void k_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkey
 }
 
 __global__ void k_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals,
-                         u32 *sq1, u32 *sq2) {
+                         u32 vn2, u32 *sq1, u32 *sq2) {
   const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= nnew) return;
   const u32 slot = slots[i];
   const u32 id = base + (u32)i;
   hvals[slot] = id;
-  const u64 k = hkeys[slot];
-  sq1[id] = (u32)(k >> 32);
-  sq2[id] = (u32)k;
+  if (vn2) {
+    sq1[id] = slot / vn2;
+    sq2[id] = slot % vn2;
+  } else {
+    const u64 k = hkeys[slot];
+    sq1[id] = (u32)(k >> 32);
+    sq2[id] = (u32)k;
+  }
 }
 
-__global__ void k_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
-                          u32 *vals) {
+__global__ void k_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, u32 vn2, int bq2,
+                          u64 *keys, u32 *vals) {
   const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= nnew) return;
   const u32 slot = newlist[i];
-  const u64 k = hkeys[slot];
+  const u64 k = vn2 ? ((u64)(slot / vn2) << 32) | (slot % vn2) : hkeys[slot];
   keys[i] = ((k >> 32) << bq2) | (k & 0xffffffffull);
   vals[i] = slot;
 }
@@ -1761,9 +1802,9 @@ void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s) {
   hipLaunchKernelGGL(k_fix_dst, dim3(grid1(n)), dim3(256), 0, s, dst, n, hvals);
 }
 
-void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 s1, u32 s2, u32 *sq1, u32 *sq2,
-                         u32 *err, hipStream_t s) {
-  hipLaunchKernelGGL(k_insert_start, dim3(1), dim3(1), 0, s, hkeys, hmask, hvals, s1, s2, sq1,
+void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 vn2, u32 s1, u32 s2, u32 *sq1,
+                         u32 *sq2, u32 *err, hipStream_t s) {
+  hipLaunchKernelGGL(k_insert_start, dim3(1), dim3(1), 0, s, hkeys, hmask, hvals, vn2, s1, s2, sq1,
                      sq2, err);
 }
 
@@ -1773,18 +1814,18 @@ void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32
                      nvals, nmask, err);
 }
 
-void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 *sq1,
-                   u32 *sq2, hipStream_t s) {
+void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 vn2,
+                   u32 *sq1, u32 *sq2, hipStream_t s) {
   if (!nnew) return;
   hipLaunchKernelGGL(k_assign, dim3((unsigned)ceil_div(nnew, 256)), dim3(256), 0, s, slots, nnew,
-                     base, hkeys, hvals, sq1, sq2);
+                     base, hkeys, hvals, vn2, sq1, sq2);
 }
 
-void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, int bq2, u64 *keys,
+void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, u32 vn2, int bq2, u64 *keys,
                     u32 *vals, hipStream_t s) {
   if (!nnew) return;
   hipLaunchKernelGGL(k_newkeys, dim3((unsigned)ceil_div(nnew, 256)), dim3(256), 0, s, newlist,
-                     nnew, hkeys, bq2, keys, vals);
+                     nnew, hkeys, vn2, bq2, keys, vals);
 }
 
 void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const u32 *hvals,
