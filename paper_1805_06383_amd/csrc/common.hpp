@@ -201,6 +201,11 @@ size_t scan_temp_bytes(u64 n);
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s);
 void exclusive_scan(const u32 *in, u64 *out, u64 n, void *temp, hipStream_t s);
 void exclusive_scan(const u32 *in, u32 *out, u64 n, void *temp, hipStream_t s);
+// Three exclusive scans of arrays of the same length at once (out_k has
+// n + 1 entries); `temp` must hold scan3_temp_bytes(n) bytes.
+size_t scan3_temp_bytes(u64 n);
+void exclusive_scan3(const u64 *in0, u64 *out0, const u32 *in1, u64 *out1, const u32 *in2,
+                     u64 *out2, u64 n, void *temp, hipStream_t s);
 
 // Stable LSD radix sort of (u64 key, u32 value) on key bits [lo, hi).
 // keys/vals hold the input; keys_alt/vals_alt are scratch of the same size;

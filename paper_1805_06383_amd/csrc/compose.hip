@@ -362,7 +362,7 @@ void Composer::run(fstc_result *out) {
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
-      aoff(&level_tmp), pk(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      aoff(&level_tmp), pk(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -382,24 +382,26 @@ void Composer::run(fstc_result *out) {
     mcount.ensure(np1 * 4); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
     pk.ensure(np1 * 4); poff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
-    stmp.ensure(scan_temp_bytes(np1));
+    wrange.ensure(np1 * sizeof(uint4));
+    stmp.ensure(scan3_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
     launch_reset_level(dst, s);
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
+                 wrange.as<uint4>(),
                  dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), phdr.as<uint4>(),
                  product ? 1u : 0u};
     T.begin();
     launch_count(la, s);
-    exclusive_scan(cnt.as<u64>(), roff.as<u64>(), nsrc, stmp.p, s);
-    exclusive_scan(mc.as<u32>(), moff.as<u64>(), nsrc, stmp.p, s);
+    // records, matches and product-merge entries per source
+    exclusive_scan3(cnt.as<u64>(), roff.as<u64>(), mc.as<u32>(), moff.as<u64>(), pk.as<u32>(),
+                    poff.as<u64>(), nsrc, stmp.p, s);
     launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, hs_dev, s);
     T.end(kCount);
     sync_published();
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
-    if (nprod) exclusive_scan(pk.as<u32>(), poff.as<u64>(), nsrc, stmp.p, s);
     const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
     if (R == 0 && nprod == 0) break;  // no arc leaves this level: no new states either
     premerge += R + hs->st.prod_records;

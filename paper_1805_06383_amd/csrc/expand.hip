@@ -91,8 +91,9 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   if (threadIdx.x == 0) s_max = 0;
   bool pred[3] = {false, false, false};  // wide, heavy, big
   u64 cnt = 0;
+  Ranges r{0, 0, 0, 0};
   if (u < a.nsrc) {
-    const Ranges r = source_ranges(a, (u32)u);
+    r = source_ranges(a, (u32)u);
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
     if (mn > kHeavyMin) {
       pred[1] = true;
@@ -131,8 +132,12 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   __syncthreads();
   u32 *const lists[3] = {a.wide, a.heavy, a.big};
 #pragma unroll
-  for (int l = 0; l < 3; ++l)
-    if (pred[l]) lists[l][s_base[l] + woff[l] + count_below(m[l])] = (u32)u;
+  for (int l = 0; l < 3; ++l) {
+    if (!pred[l]) continue;
+    const u32 pos = s_base[l] + woff[l] + count_below(m[l]);
+    lists[l][pos] = (u32)u;
+    if (l == 0) a.wrange[pos] = make_uint4(r.b1, r.e1, r.b2, r.e2);  // saves the wide join two loads
+  }
 }
 
 // Big-source append and window maximum of one joined source (lane 0 of the
@@ -228,7 +233,8 @@ __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
   const u32 n = a.st->nwide;
   for (u32 i = gw; i < n; i += nw) {
     const u32 u = a.wide[i];
-    const Ranges r = source_ranges(a, u);
+    const uint4 wr = a.wrange[i];
+    const Ranges r{wr.x, wr.y, wr.z, wr.w};
     const bool one_short = (r.e1 - r.b1) <= (r.e2 - r.b2);
     const u32 bs = one_short ? r.b1 : r.b2, es = one_short ? r.e1 : r.e2;
     u64 cnt = 0;
@@ -371,7 +377,8 @@ __global__ __launch_bounds__(256) void k_emit_wide(LevelArgs a) {
   for (u32 i = gw; i < n; i += nw) {
     const u32 u = a.wide[i];
     if (a.pk[u]) continue;  // product merge
-    const Ranges r = source_ranges(a, u);
+    const uint4 wr = a.wrange[i];
+    const Ranges r{wr.x, wr.y, wr.z, wr.w};
     const bool one_short = (r.e1 - r.b1) <= (r.e2 - r.b2);
     const u32 bs = one_short ? r.b1 : r.b2, es = one_short ? r.e1 : r.e2;
     u64 k = a.moff[u], rb = a.roff[u];
