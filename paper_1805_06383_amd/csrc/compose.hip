@@ -404,9 +404,8 @@ void Composer::run(fstc_result *out) {
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
     const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
     if (R == 0 && nprod == 0) break;  // no arc leaves this level: no new states either
-    premerge += R + hs->st.prod_records;
-    max_level_pre = std::max(max_level_pre, R + hs->st.prod_records);
-    product_records += hs->st.prod_records;
+    premerge += R;
+    max_level_pre = std::max(max_level_pre, R);
     product_sources += nprod;
     big_total += nbig;
 
@@ -506,6 +505,7 @@ void Composer::run(fstc_result *out) {
     ma.arcs2 = c2.arcs;
     ma.pk = pk.as<u32>();
     ma.phdr = phdr.as<uint4>();
+    ma.pcnt = cnt.as<u64>();  // product-merge sources have no records: their slots are free
     ma.poff = poff.as<u64>();
     ma.prodpos = prodpos;
     ma.row1 = c1.row;
@@ -553,7 +553,7 @@ void Composer::run(fstc_result *out) {
         T.chain(kProductKernel);
         ++product_launches;
       }
-      launch_mcount(tstart.as<u64>(), mend.as<u64>(), nsrc, mcount.as<u32>(), s);
+      launch_mcount(ma, mcount.as<u32>(), s);
       exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
       launch_emit_tiles(ma, s);
       {
@@ -570,6 +570,9 @@ void Composer::run(fstc_result *out) {
 
       nnew = hs->st.nnew;
       merged = hs->st.merged;
+      premerge += hs->st.prod_records;
+      product_records += hs->st.prod_records;
+      max_level_pre = std::max(max_level_pre, R + hs->st.prod_records);
       dense_records += hs->st.dense_records;
       dense_runs += hs->st.dense_runs;
       sort_runs += hs->st.sort_runs;

@@ -80,22 +80,49 @@ __device__ __forceinline__ u32 seg_len(const u32 *seg_off, u32 s) { return seg_o
 // merge window (st->max_small).  Both are gathered by the count kernels.
 constexpr int kCountNT = 256;
 
-// Thread per source: joins the short ones, lists the others for the
-// wavefront / workgroup joins.  List appends and the window maximum are
+// Product-merge selection of source u (level.hpp) from what the count
+// already loaded: table entries P1 P2 and the source header written to
+// phdr, or 0 (record path).  The cell flags are clear only for states of at
+// most kProdParts parts.
+__device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1, u32 q2,
+                                              const Ranges &r) {
+  if (a.c1.cell_flag[q1] | a.c2.cell_flag[q2]) return 0;
+  const u32 pb1 = a.c1.part_base[q1], p1 = a.c1.part_base[q1 + 1] - pb1;
+  const u32 pb2 = a.c2.part_base[q2], p2 = a.c2.part_base[q2 + 1] - pb2;
+  if (p1 == 0 || p2 == 0 || p1 + p2 > kProdRowSum) return 0;
+  a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16), 0u);
+  a.phdr[2 * u + 1] = make_uint4(r.b1, r.e1, r.b2, r.e2);
+  return p1 * p2;
+}
+
+// Thread per source: selects the product-merge sources (no records, no
+// matches; pk = their entry count), joins the other short ones, lists the
+// rest for the wavefront / workgroup joins.  List appends, the window
+// maximum and the product-merge totals (st->nprod, prod_entries) are
 // aggregated per workgroup in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   __shared__ u32 s_n[3], s_base[3], s_max;
+  __shared__ unsigned long long s_p[2];
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (threadIdx.x < 3) s_n[threadIdx.x] = 0;
+  if (threadIdx.x < 2) s_p[threadIdx.x] = 0;
   if (threadIdx.x == 0) s_max = 0;
   bool pred[3] = {false, false, false};  // wide, heavy, big
   u64 cnt = 0;
+  u32 pk = 0;
   Ranges r{0, 0, 0, 0};
   if (u < a.nsrc) {
-    r = source_ranges(a, (u32)u);
+    const u32 sid = a.lo + (u32)u;
+    const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
+    r = Ranges{a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]};
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
-    if (mn > kHeavyMin) {
+    if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r);
+    a.pk[u] = pk;
+    if (pk) {
+      a.cnt[u] = 0;
+      a.mc[u] = 0;
+    } else if (mn > kHeavyMin) {
       pred[1] = true;
     } else if (mn > kWideMin) {
       pred[0] = true;
@@ -111,6 +138,15 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     }
   }
   const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
+  {
+    const u32 np = wave_sum(pk ? 1u : 0u);
+    const u64 ne = wave_sum((u64)pk);
+    __syncthreads();  // s_p cleared
+    if (lane == 0 && np) {
+      atomicAdd(&s_p[0], (unsigned long long)np);
+      atomicAdd(&s_p[1], (unsigned long long)ne);
+    }
+  }
   __syncthreads();
   u64 m[3];
   u32 woff[3];
@@ -129,6 +165,10 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   u32 *const counters[3] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig};
   if (threadIdx.x < 3 && s_n[threadIdx.x]) s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
   if (threadIdx.x == 3 && s_max) atomicMax(&a.st->max_small, s_max);
+  if (threadIdx.x == 4 && s_p[0]) {
+    atomicAdd(&a.st->nprod, (u32)s_p[0]);
+    atomicAdd((unsigned long long *)&a.st->prod_entries, s_p[1]);
+  }
   __syncthreads();
   u32 *const lists[3] = {a.wide, a.heavy, a.big};
 #pragma unroll
@@ -290,57 +330,6 @@ __global__ __launch_bounds__(kHeavyNT) void k_count_heavy(LevelArgs a) {
     }
   }
   publish_max<kHeavyNT>(a, run_max, &s_max);
-}
-
-// ---------------------------------------------------------------------------
-// Product-merge selection (level.hpp), thread per source, after the joins
-// are counted: a selected source keeps its entry count P1 P2 in pk and gets
-// no records and no matches, so the record path skips it.  Sources the
-// multi-block path listed (more than kMergeSmall records) stay there.
-// Totals go to st->nprod / prod_records / prod_entries, one atomic each per
-// workgroup.
-__global__ __launch_bounds__(kCountNT) void k_classify(LevelArgs a) {
-  __shared__ unsigned long long s_p[3];
-  const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  if (threadIdx.x < 3) s_p[threadIdx.x] = 0;
-  u32 k = 0;
-  u64 cnt = 0;
-  if (u < a.nsrc) {
-    cnt = a.cnt[u];
-    if (a.prod && cnt >= kProdMinRecords && cnt <= kMergeSmall) {
-      const u32 sid = a.lo + (u32)u;
-      const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
-      const u32 p1 = a.c1.part_base[q1 + 1] - a.c1.part_base[q1];
-      const u32 p2 = a.c2.part_base[q2 + 1] - a.c2.part_base[q2];
-      const u32 l1 = a.c1.row[q1 + 1] - a.c1.row[q1], l2 = a.c2.row[q2 + 1] - a.c2.row[q2];
-      const bool ok = (a.c1.cell_flag[q1] | a.c2.cell_flag[q2]) == 0 && p1 + p2 <= kProdRowSum &&
-                      min(l1, l2) <= (u32)kWave && cnt >= (u64)p1 * p2;
-      k = ok ? p1 * p2 : 0;
-      if (k) {
-        a.phdr[2 * u] = make_uint4(a.c1.part_base[q1], a.c2.part_base[q2], p1 | (p2 << 16), 0u);
-        a.phdr[2 * u + 1] = make_uint4(a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]);
-      }
-    }
-    a.pk[u] = k;
-    if (k) {
-      a.cnt[u] = 0;
-      a.mc[u] = 0;
-    }
-  }
-  __syncthreads();
-  const u32 n = wave_sum(k ? 1u : 0u);
-  const u64 rec = wave_sum(k ? cnt : 0ull), ent = wave_sum((u64)k);
-  if (lane_id() == 0 && n) {
-    atomicAdd(&s_p[0], (unsigned long long)n);
-    atomicAdd(&s_p[1], (unsigned long long)rec);
-    atomicAdd(&s_p[2], (unsigned long long)ent);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0 && s_p[0]) {
-    atomicAdd(&a.st->nprod, (u32)s_p[0]);
-    atomicAdd((unsigned long long *)&a.st->prod_records, s_p[1]);
-    atomicAdd((unsigned long long *)&a.st->prod_entries, s_p[2]);
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -635,7 +624,6 @@ void launch_count(const LevelArgs &a, hipStream_t s) {
   hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
   hipLaunchKernelGGL(k_count_wide, dim3(wide_grid(a.nsrc)), dim3(256), 0, s, a);
   hipLaunchKernelGGL(k_count_heavy, dim3(heavy_grid(a.nsrc)), dim3(kHeavyNT), 0, s, a);
-  hipLaunchKernelGGL(k_classify, dim3(g), dim3(kCountNT), 0, s, a);
 }
 
 void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s) {

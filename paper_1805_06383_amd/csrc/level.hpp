@@ -44,11 +44,12 @@ struct Status {
 // Product merge (merge.hip, k_prod_sources).  A source (q1, q2) is merged
 // by one wavefront from its staged arc matrices instead of through records
 // when its states have P1 + P2 <= kProdRowSum parts in all, the shorter of
-// its two inner-symbol lists has at most 64 symbols, neither state has two
-// arcs in one (part, inner symbol) cell, and it has at least
-// max(kProdMinRecords, P1 P2) and at most kMergeSmall joined arc pairs.
+// its two inner-symbol lists has kProdMinSymbols to 64 symbols, and neither
+// state has two arcs in one (part, inner symbol) cell.  The count kernel
+// selects it from the list lengths and part counts alone; the product
+// kernel counts its joined pairs.
 constexpr u32 kProdRowSum = 16;
-constexpr u32 kProdMinRecords = 64;
+constexpr u32 kProdMinSymbols = 8;
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
 // wavefront, longer than kHeavyMin by a workgroup; others by one thread.
@@ -112,7 +113,7 @@ struct LevelArgs {
   u32 prod;              // nonzero: sources may take the product merge
 };
 
-// Written by the selection for a product-merge source u at phdr[2u], [2u+1]:
+// Written by the count kernel for a product-merge source u at phdr[2u], [2u+1]:
 // (M1 part base, M2 part base, P1 | P2 << 16, unused), (M1 segment range
 // begin, end, M2 segment range begin, end).
 
@@ -170,6 +171,7 @@ struct MergeArgs {
   const uint4 *phdr;
   const u64 *poff;
   u64 prodpos;
+  u64 *pcnt;  // [nsrc] joined arc pairs of each product-merge source (written by it)
   const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;
 };
 
@@ -214,7 +216,9 @@ void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const 
 // the form used when product-merge sources sit between tile-merged ones.
 void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,
                             u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s);
-void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s);
+// mcount[u] = mend[u] - tstart[u]; also adds the joined pairs of the
+// product-merge sources (a.pcnt where a.pk != 0) to st->prod_records.
+void launch_mcount(const MergeArgs &a, u32 *mcount, hipStream_t s);
 // Visited-table inserts and label lookups for every merged arc of the
 // tile-merged sources (merge_big does its own).
 void launch_emit_tiles(const MergeArgs &a, hipStream_t s);

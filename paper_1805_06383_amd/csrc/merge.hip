@@ -1018,10 +1018,12 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
 
   // 3. merged arcs in entry order: the visited-table insert resumes from
-  //    the probe loaded above
+  //    the probe loaded above; the source's joined pairs (the entries' terms)
+  //    go to pcnt[u]
   const bool run = owner && m != 0;
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
+  const u32 pairs = wave_sum(owner ? (u32)__popcll(m) : 0u);
   const u64 base = a.R + a.poff[u];
   if (run && a.vn2) {
     // dense array: the entry read above, then a claim if it was unvisited
@@ -1063,6 +1065,7 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   if (lane == 0) {
     a.tstart[u] = base;
     a.mend[u] = base + nr;
+    a.pcnt[u] = pairs;
   }
 }
 
@@ -1411,10 +1414,23 @@ __global__ __launch_bounds__(256) void k_newlist(MergeArgs a, const u64 *bigoff,
 // Level total of new states (end of the exclusive scan of the per-wave counts).
 __global__ void k_new_total(const u64 *total, Status *st) { st->nnew = (u32)min<u64>(*total, 0xffffffffull); }
 
-// Merged arcs per source from where its runs start and end in temp.
-__global__ void k_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount) {
+// Merged arcs per source from where its runs start and end in temp; the
+// joined pairs of the product-merge sources summed into st->prod_records
+// (one device atomic per workgroup).
+__global__ __launch_bounds__(256) void k_mcount(MergeArgs a, u32 *mcount) {
+  __shared__ unsigned long long s_sum;
+  if (threadIdx.x == 0) s_sum = 0;
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  if (u < nsrc) mcount[u] = (u32)(mend[u] - tstart[u]);
+  u64 v = 0;
+  if (u < a.nsrc) {
+    mcount[u] = (u32)(a.mend[u] - a.tstart[u]);
+    if (a.prodpos && a.pk[u]) v = a.pcnt[u];
+  }
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane_id() == 0 && v) atomicAdd(&s_sum, (unsigned long long)v);
+  __syncthreads();
+  if (threadIdx.x == 0 && s_sum) atomicAdd((unsigned long long *)&a.st->prod_records, s_sum);
 }
 
 // ---------------------------------------------------------------------------
@@ -1864,9 +1880,8 @@ void launch_emit_tiles(const MergeArgs &a, hipStream_t s) {
                      0, s, a, wpt);
 }
 
-void launch_mcount(const u64 *tstart, const u64 *mend, u32 nsrc, u32 *mcount, hipStream_t s) {
-  hipLaunchKernelGGL(k_mcount, dim3((unsigned)ceil_div(nsrc, 256)), dim3(256), 0, s, tstart, mend,
-                     nsrc, mcount);
+void launch_mcount(const MergeArgs &a, u32 *mcount, hipStream_t s) {
+  hipLaunchKernelGGL(k_mcount, dim3((unsigned)ceil_div(a.nsrc, 256)), dim3(256), 0, s, a, mcount);
 }
 
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
