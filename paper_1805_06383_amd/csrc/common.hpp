@@ -26,6 +26,7 @@ enum : u32 {
   kErrBounds = 4u,      // an internal index check failed
   kErrNewList = 8u,     // more new states than the new-state list holds
   kErrTileSize = 16u,   // a merge tile exceeded its LDS capacity
+  kErrScan = 32u,       // a single-pass scan waited too long for a predecessor tile
 };
 
 constexpr u64 kEmptyKey = ~0ull;
@@ -201,6 +202,21 @@ size_t scan_temp_bytes(u64 n);
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s);
 void exclusive_scan(const u32 *in, u64 *out, u64 n, void *temp, hipStream_t s);
 void exclusive_scan(const u32 *in, u32 *out, u64 n, void *temp, hipStream_t s);
+// Single-pass exclusive scans (decoupled look-back) of up to three arrays of
+// the same length n at once, one launch: in[k] holds u64 when wide[k], else
+// u32; out[k] has n + 1 entries (u64).  `state` is scan_lb_state_bytes(n)
+// bytes that no other code writes and that were zero-filled once when
+// allocated; `ctr` is a device word that is 0 before the call (the call
+// leaves it 0); scan failures set kErrScan in *err.
+struct ScanJob {
+  const void *in;
+  bool wide;
+  u64 *out;
+};
+size_t scan_lb_state_bytes(u64 n);
+void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
+                       hipStream_t s);
+
 // Three exclusive scans of arrays of the same length at once (out_k has
 // n + 1 entries); `temp` must hold scan3_temp_bytes(n) bytes.
 size_t scan3_temp_bytes(u64 n);

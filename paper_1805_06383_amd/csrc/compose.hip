@@ -141,6 +141,7 @@ const char *device_error_text(u32 e) {
   if (e & kErrHashFull) return "visited table full";
   if (e & kErrNewList) return "new-state list overflow";
   if (e & kErrTileSize) return "merge tile exceeded its capacity";
+  if (e & kErrScan) return "a single-pass scan timed out waiting for a predecessor tile";
   return "device index check failed";
 }
 
@@ -149,8 +150,7 @@ enum Phase {
   kProductKernel, kNumPhases
 };
 
-// HIP-event timing of the phases on the call's stream (only with stats).
-// Phase timing with HIP events on the call's stream.  Events are created
+// Phase timing with HIP events on the call's stream (only with stats).  Events are created
 // once per thread and reused by later calls (creating them costs more than a
 // short level), and a span that begins where the previous one ended shares
 // that event.
@@ -359,6 +359,17 @@ void Composer::run(fstc_result *out) {
   u32 product_launches = 0;
 
   ArcCols out_arcs(&A, s);
+  // single-pass scan state: zero-filled when (re)allocated, then written
+  // only by the scans
+  Buf lbstate(&A);
+  auto lb = [&](u64 n) {
+    const size_t b = scan_lb_state_bytes(n);
+    if (b > lbstate.cap) {
+      lbstate.ensure(std::max<size_t>(b, 2 * lbstate.cap));
+      fill_u32(lbstate.as<u32>(), 0, lbstate.cap / 4, s);
+    }
+    return lbstate.p;
+  };
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
@@ -395,8 +406,11 @@ void Composer::run(fstc_result *out) {
     T.begin();
     launch_count(la, s);
     // records, matches and product-merge entries per source
-    exclusive_scan3(cnt.as<u64>(), roff.as<u64>(), mc.as<u32>(), moff.as<u64>(), pk.as<u32>(),
-                    poff.as<u64>(), nsrc, stmp.p, s);
+    {
+      const ScanJob jobs[3] = {{cnt.p, true, roff.as<u64>()}, {mc.p, false, moff.as<u64>()},
+                               {pk.p, false, poff.as<u64>()}};
+      exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+    }
     launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, hs_dev, s);
     T.end(kCount);
     sync_published();
@@ -554,15 +568,17 @@ void Composer::run(fstc_result *out) {
         ++product_launches;
       }
       launch_mcount(ma, mcount.as<u32>(), s);
-      exclusive_scan(mcount.as<u32>(), aoff.as<u64>(), nsrc, stmp.p, s);
+      {
+        const ScanJob job{mcount.p, false, aoff.as<u64>()};
+        exclusive_scan_lb(&job, 1, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+      }
       launch_emit_tiles(ma, s);
       {
         const u64 nw = newlist_waves(ma, RB);
         wcnt.ensure(nw * 4);
         woff.ensure((nw + 1) * 8);
-        wtmp.ensure(scan_temp_bytes(nw));
         launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
-                       woff.as<u64>(), wtmp.p, s);
+                       woff.as<u64>(), lb(nw), s);
       }
       launch_merged_total(aoff.as<u64>() + nsrc, ma, hs_dev, s);
       T.end(kMerge);
@@ -884,10 +900,19 @@ int fstc_exclusive_scan_u64(const uint64_t *in, uint64_t *out, uint64_t n, hipSt
     Allocator A;
     A.stream = stream;
     tune_default_pool();
-    Buf tmp(&A);
-    tmp.ensure(scan_temp_bytes(n));
-    exclusive_scan(in, out, n, tmp.p, stream);
+    // single-pass scan: zero-filled state, a counter and an error word
+    Buf state(&A), words(&A);
+    state.ensure(scan_lb_state_bytes(n));
+    words.ensure(8);
+    fill_u32(state.as<u32>(), 0, state.cap / 4, stream);
+    fill_u32(words.as<u32>(), 0, 2, stream);
+    const ScanJob job{in, true, out};
+    exclusive_scan_lb(&job, 1, n, state.p, words.as<u32>(), words.as<u32>() + 1, stream);
+    Staging *hs = staging();
     FSTC_HIP(hipGetLastError());
+    FSTC_HIP(hipMemcpyAsync(&hs->st.err, words.as<u32>() + 1, 4, hipMemcpyDeviceToHost, stream));
+    FSTC_HIP(hipStreamSynchronize(stream));
+    if (hs->st.err) throw Error(FSTC_ERR_INTERNAL, device_error_text(hs->st.err));
   });
 }
 

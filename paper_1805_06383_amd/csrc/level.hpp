@@ -37,6 +37,7 @@ struct Status {
   u64 sort_runs;      // merged arcs of the tiles merged by sorting
   u32 nsort;          // tiles k_merge_dense left to the sort kernel
   u32 nprod;          // sources of the product merge
+  u32 scan_ctr;       // tile counter of the single-pass scans (0 between scans)
   u64 prod_records;   // their joined arc pairs (not written as records)
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
 };
@@ -226,9 +227,11 @@ void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
 // the multi-block runs and the product-merge slots (st->nnew = its length).
 // wcnt: newlist_waves(a, RB) u32; woff: that + 1 u64; scan_tmp:
 // scan_temp_bytes(newlist_waves(a, RB)) bytes.
+// scan_state: scan_lb_state_bytes(newlist_waves(a, RB)) bytes of single-pass
+// scan state (see exclusive_scan_lb).
 u64 newlist_waves(const MergeArgs &a, u64 RB);
 void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
-                    void *scan_tmp, hipStream_t s);
+                    void *scan_state, hipStream_t s);
 // Composition without reduction: every record of the level becomes an arc
 // (osrc.. at [0, R)), its target pair claimed in the visited table and each
 // new claim flagged in `newbits` (one bit per table slot, cleared by the

@@ -1857,14 +1857,15 @@ u64 newlist_waves(const MergeArgs &a, u64 RB) {
 }
 
 void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
-                    void *scan_tmp, hipStream_t s) {
+                    void *scan_state, hipStream_t s) {
   const u64 nbigw = ceil_div(RB, kWave);
   const u64 nw = newlist_waves(a, RB);
   if (nw == 0) return;  // st->nnew stays 0
   const unsigned g = (unsigned)ceil_div(nw, 256 / kWave);
   hipLaunchKernelGGL(k_newlist<0>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
                      (const u64 *)nullptr);
-  exclusive_scan(wcnt, woff, nw, scan_tmp, s);
+  const ScanJob job{wcnt, false, woff};
+  exclusive_scan_lb(&job, 1, nw, scan_state, &a.st->scan_ctr, &a.st->err, s);
   hipLaunchKernelGGL(k_newlist<1>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
                      (const u64 *)woff);
   hipLaunchKernelGGL(k_new_total, dim3(1), dim3(1), 0, s, (const u64 *)(woff + nw), a.st);

@@ -172,6 +172,144 @@ __global__ __launch_bounds__(kScanNT) void k_sums_scan3(const u64 *sums, u64 nb,
   }
 }
 
+// ---------------------------------------------------------------------------
+// Single-pass scan with decoupled look-back (Merrill & Garland, "Single-pass
+// Parallel Prefix Scan with Decoupled Look-back", 2016).  A workgroup takes
+// the next tile number from a counter, so every lower tile belongs to a
+// workgroup already running; it publishes its tile total ("aggregate"),
+// then wave 0 reads the states of the 64 tiles below it at once and adds
+// aggregates down to the nearest tile that has published its inclusive
+// prefix, publishes its own inclusive prefix, and the workgroup writes its
+// tile offset by that.  A state word is (epoch << 2 | kind): words of other
+// calls carry other epochs and count as not yet published.  Waits are
+// bounded (kLbSpins reads of a window): past that, kErrScan.
+constexpr int kLbNT = 256;
+constexpr int kLbIT = 8;
+constexpr int kLbTile = kLbNT * kLbIT;
+constexpr u32 kLbAgg = 1u, kLbIncl = 2u;
+constexpr u32 kLbSpins = 1u << 22;
+constexpr int kLbMax = 3;
+
+struct LbArgs {
+  const void *in[kLbMax];
+  u64 *out[kLbMax];
+  u32 wide;  // bit k: in[k] holds u64
+  u64 n;
+  u32 nb, epoch;
+  u32 *flags;   // [nb]
+  u64 *agg;     // [nb * kLbMax]
+  u64 *incl;    // [nb * kLbMax]
+  u32 *ctr, *err;
+};
+
+template <int K>
+__global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
+  __shared__ u32 s_t;
+  __shared__ u64 s_off[kLbMax];
+  __shared__ u64 scratch[kLbNT / kWave];
+  const u32 lane = lane_id();
+  if (threadIdx.x == 0) {
+    const u32 t = atomicAdd(p.ctr, 1u);
+    if (t == p.nb - 1) atomicExch(p.ctr, 0u);  // the last number is taken: ready for the next call
+    s_t = t;
+  }
+  __syncthreads();
+  const u32 t = s_t;
+  const u64 base = (u64)t * kLbTile + (u64)threadIdx.x * kLbIT;  // blocked: kLbIT per thread
+  u64 loc[K][kLbIT];
+  u64 ex[K], tot[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    u64 run = 0;
+#pragma unroll
+    for (int j = 0; j < kLbIT; ++j) {
+      const u64 i = base + j;
+      u64 x = 0;
+      if (i < p.n)
+        x = ((p.wide >> k) & 1u) ? static_cast<const u64 *>(p.in[k])[i]
+                                 : (u64) static_cast<const u32 *>(p.in[k])[i];
+      loc[k][j] = run;
+      run += x;
+    }
+    ex[k] = block_exclusive_sum<kLbNT, u64>(run, scratch, &tot[k]);
+    __syncthreads();  // scratch reused
+  }
+  if (threadIdx.x < (u32)kWave) {
+    u64 off[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) off[k] = 0;
+    if (t == 0) {
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) p.incl[k] = tot[k];
+        __hip_atomic_store(&p.flags[0], (p.epoch << 2) | kLbIncl, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    } else {
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) p.agg[(u64)t * kLbMax + k] = tot[k];
+        __hip_atomic_store(&p.flags[t], (p.epoch << 2) | kLbAgg, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+      long long hi = (long long)t - 1;  // nearest predecessor of the window
+      u32 spins = 0;
+      bool failed = false;
+      while (true) {
+        const long long j = hi - (long long)lane;
+        u32 f = (p.epoch << 2) | kLbIncl;  // below tile 0: an empty prefix
+        if (j >= 0)
+          f = __hip_atomic_load(&p.flags[j], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        const bool ready = (f >> 2) == p.epoch && (f & 3u) != 0;
+        const bool isp = ready && (f & 3u) == kLbIncl;
+        const u64 pm = __ballot(isp), rm = __ballot(ready);
+        const u32 lp = pm ? (u32)__builtin_ctzll(pm) : (u32)kWave;  // nearest inclusive prefix
+        const u64 need = lp < (u32)kWave ? (lp == 63 ? ~0ull : (2ull << lp) - 1ull) : ~0ull;
+        if ((rm & need) != need) {  // a tile in between has not published yet
+          if (++spins > kLbSpins) {
+            failed = true;
+            break;
+          }
+          continue;
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          u64 x = 0;
+          if (j >= 0 && (u32)lane < lp) x = p.agg[(u64)j * kLbMax + k];
+          else if (j >= 0 && (u32)lane == lp) x = p.incl[(u64)j * kLbMax + k];
+          off[k] += wave_sum(x);
+        }
+        if (lp < (u32)kWave) break;
+        hi -= kWave;
+      }
+      if (failed && lane == 0) atomicOr(p.err, kErrScan);
+      if (lane == 0) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) p.incl[(u64)t * kLbMax + k] = off[k] + tot[k];
+        __hip_atomic_store(&p.flags[t], (p.epoch << 2) | kLbIncl, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) {
+        s_off[k] = off[k];
+        if (t == p.nb - 1) p.out[k][p.n] = off[k] + tot[k];
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const u64 o = s_off[k] + ex[k];
+#pragma unroll
+    for (int j = 0; j < kLbIT; ++j) {
+      const u64 i = base + j;
+      if (i < p.n) p.out[k][i] = o + loc[k][j];
+    }
+  }
+}
+
 template <class TO>
 size_t temp_elems(u64 n) {
   size_t t = 0;
@@ -233,6 +371,39 @@ void fill_u64(u64 *p, u64 v, u64 n, hipStream_t s) {
 }
 
 size_t scan_temp_bytes(u64 n) { return temp_elems<u64>(n) * sizeof(u64) + 256; }
+
+size_t scan_lb_state_bytes(u64 n) {
+  const u64 nb = std::max<u64>(1, ceil_div(n, kLbTile));
+  return (size_t)nb * (4 + 2 * kLbMax * 8) + 256;
+}
+
+void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
+                       hipStream_t s) {
+  static std::atomic<u32> epochs{0};
+  const u64 nb = std::max<u64>(1, ceil_div(n, kLbTile));
+  if (nb >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "scan too large for one launch");
+  LbArgs p{};
+  p.wide = 0;
+  for (int i = 0; i < k; ++i) {
+    p.in[i] = jobs[i].in;
+    p.out[i] = jobs[i].out;
+    p.wide |= (jobs[i].wide ? 1u : 0u) << i;
+  }
+  p.n = n;
+  p.nb = (u32)nb;
+  u32 e = (epochs.fetch_add(1, std::memory_order_relaxed) + 1) & 0x3fffffffu;
+  p.epoch = e ? e : 1u;  // state words of zero-filled memory never match
+  char *b = static_cast<char *>(state);
+  p.agg = reinterpret_cast<u64 *>(b);
+  p.incl = p.agg + nb * kLbMax;
+  p.flags = reinterpret_cast<u32 *>(p.incl + nb * kLbMax);
+  p.ctr = ctr;
+  p.err = err;
+  const dim3 g((unsigned)nb), bl(kLbNT);
+  if (k == 1) hipLaunchKernelGGL(k_scan_lb<1>, g, bl, 0, s, p);
+  else if (k == 2) hipLaunchKernelGGL(k_scan_lb<2>, g, bl, 0, s, p);
+  else hipLaunchKernelGGL(k_scan_lb<3>, g, bl, 0, s, p);
+}
 
 size_t scan3_temp_bytes(u64 n) {
   return std::max<size_t>(6 * ceil_div(std::max<u64>(n, 1), kScanTile) * sizeof(u64) + 256,
