@@ -198,6 +198,12 @@ def main():
         torch.cuda.synchronize()
         return time.perf_counter() - t0, last, sums
 
+    def phase_times(product: bool):
+        r = fstc.fstc_compose(m1, m2, max_levels=args.max_levels, reduce=not args.no_reduction,
+                              fused=args.fused, product=product, phase_timing=True)
+        torch.cuda.synchronize()
+        return {k: r.stats[k] for k in ("ms_csr", "ms_count", "ms_expand", "ms_merge", "ms_assign")}
+
     def kernels_and_roofline(last, sums, traffic_key):
         R = last.num_premerge_arcs
         st = last.stats
@@ -278,8 +284,9 @@ def main():
             "input_sha256": [h1.digest()[:16], h2.digest()[:16]],
         },
         "post_merge_arcs_per_s": post_rate,
-        "phase_ms_per_step": {k: sums[k] / args.steps for k in
-                              ("ms_csr", "ms_count", "ms_expand", "ms_merge", "ms_assign")},
+        # one more, untimed step with an event at every phase boundary (the
+        # timed steps record events around the single-kernel phases only)
+        "phase_ms_untimed_step": phase_times(product),
         "kernels": kern,
         "roofline": roof,
     }

@@ -125,6 +125,15 @@ typedef struct fstc_opts {
                                  at most 2^26 it is a dense array indexed by
                                  q1 |Q2| + q2 (the paper's |Q1||Q2| table,
                                  section 3.4), 4 bytes a pair; same result */
+  uint32_t phase_timing;      /* with stats: nonzero times every phase
+                                 (ms_csr .. ms_assign) with HIP events at
+                                 each phase boundary.  0: only the kernels
+                                 behind ms_write_kernel, ms_merge_kernel,
+                                 ms_sort_kernel and ms_product_kernel are
+                                 timed, one event before and one after each
+                                 launch, and the phase times are 0 (every
+                                 event costs the stream a few microseconds) */
+  uint32_t reserved0;
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the
@@ -150,7 +159,7 @@ typedef struct fstc_result {
 } fstc_result;
 
 /* Per-call statistics (all optional to read). Times from HIP events on the
- * call's stream, in milliseconds. */
+ * call's stream, in milliseconds; the phase times need opts->phase_timing. */
 typedef struct fstc_stats {
   uint32_t num_levels;        /* breadth-first levels expanded              */
   uint32_t num_host_syncs;

@@ -109,10 +109,21 @@ struct Staging {
   u64 words[16];
 };
 
+// Coherent (fine-grained) pinned memory: the publishing kernels' stores
+// reach the host while they run, so the host can watch st.seq.
 Staging *staging() {
   thread_local Staging *p = nullptr;
-  if (!p) FSTC_HIP(hipHostMalloc((void **)&p, sizeof(Staging), hipHostMallocDefault));
+  if (!p) {
+    FSTC_HIP(hipHostMalloc((void **)&p, sizeof(Staging), hipHostMallocCoherent));
+    std::memset(p, 0, sizeof(Staging));
+  }
   return p;
+}
+
+// Publication numbers of this thread's staging block, never reused.
+u32 next_publication() {
+  thread_local u32 n = 0;
+  return ++n;
 }
 
 // Keep freed blocks of the default stream-ordered pool instead of returning
@@ -147,18 +158,24 @@ const char *device_error_text(u32 e) {
 
 enum Phase {
   kCsr, kCount, kExpand, kMerge, kAssign, kWriteKernel, kMergeKernel, kSortKernel,
-  kProductKernel, kNumPhases
+  kProductKernel, kNumPhases, kNone = -1
 };
 
-// Phase timing with HIP events on the call's stream (only with stats).  Events are created
-// once per thread and reused by later calls (creating them costs more than a
-// short level), and a span that begins where the previous one ended shares
-// that event.
+inline bool kernel_phase(int p) { return p >= kWriteKernel && p < kNumPhases; }
+
+// Timing with HIP events on the call's stream (only with stats).  T.at(p)
+// marks a boundary: the current span ends there and a span of phase p (or
+// none, kNone) begins.  With all phases on, every boundary records one event
+// shared by the two spans; otherwise only boundaries of the single-kernel
+// phases record one, so that a timed kernel costs two events.  Events are
+// created once per thread and device and reused by later calls.
 struct Timer {
   hipStream_t s = nullptr;
-  bool on = false;
+  bool on = false;   // stats wanted
+  bool all = false;  // every phase, not just the kernel phases
   std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> spans;
   hipEvent_t open = nullptr;
+  int cur = kNone;
   size_t used = 0;
 
   int device = -1;
@@ -178,21 +195,19 @@ struct Timer {
     }
     return p[used++];
   }
-  void begin() {
+  bool want(int p) const { return p != kNone && (all || kernel_phase(p)); }
+  void at(int next) {
     if (!on) return;
-    open = get();
-    FSTC_HIP(hipEventRecord(open, s));
+    if (want(cur) || want(next)) {
+      hipEvent_t e = get();
+      FSTC_HIP(hipEventRecord(e, s));
+      if (want(cur) && open) spans.push_back({cur, {open, e}});
+      open = want(next) ? e : nullptr;
+    } else {
+      open = nullptr;
+    }
+    cur = next;
   }
-  void end(int phase) {
-    if (!on) return;
-    hipEvent_t e = get();
-    FSTC_HIP(hipEventRecord(e, s));
-    spans.push_back({phase, {open, e}});
-    open = e;
-  }
-  // end(phase) and begin() at once: the next span starts at this boundary
-  // (only where nothing is enqueued in between)
-  void chain(int phase) { end(phase); }
   void totals(double *ms) {
     for (auto &sp : spans) {
       float t = 0.f;
@@ -246,6 +261,7 @@ struct Composer {
     A.stream = s;
     T.s = s;
     T.on = stats != nullptr;
+    T.all = o.phase_timing != 0;
   }
 
   void sync_status() {
@@ -259,11 +275,23 @@ struct Composer {
     }
   }
 
-  // the counters a kernel already copied to hs->st (launch_level_totals,
-  // launch_merged_total)
-  void sync_published() {
+  // Waits until a kernel has copied the counters to hs->st and then written
+  // publication number `seq` (launch_level_totals, launch_merged_total): a
+  // spin on that word, with a stream query every few thousand reads so that
+  // a failed or drained stream ends the wait.
+  void wait_published(u32 seq) {
     FSTC_HIP(hipGetLastError());
-    FSTC_HIP(hipStreamSynchronize(s));
+    for (u32 i = 1;; ++i) {
+      if (__atomic_load_n(&hs->st.seq, __ATOMIC_ACQUIRE) == seq) break;
+      if ((i & 4095u) == 0) {
+        const hipError_t q = hipStreamQuery(s);
+        if (q == hipErrorNotReady) continue;
+        FSTC_HIP(q);
+        if (__atomic_load_n(&hs->st.seq, __ATOMIC_ACQUIRE) == seq) break;
+        throw Error(FSTC_ERR_INTERNAL, "level counters were not published");
+      }
+      __builtin_ia32_pause();
+    }
     ++nsyncs;
     if (hs->st.err) {
       throw Error((hs->st.err & kErrBadArc) ? FSTC_ERR_INVALID_ARG : FSTC_ERR_INTERNAL,
@@ -300,7 +328,7 @@ void Composer::run(fstc_result *out) {
   c1.cell_flag = (u32 *)cf1.ensure(std::max<u64>(m1.num_states, 1) * 4);
   c2.cell_flag = (u32 *)cf2.ensure(std::max<u64>(m2.num_states, 1) * 4);
   const bool product = !o.no_reduction && !o.no_product_merge;
-  T.begin();
+  T.at(kCsr);
   {
     Arena csr_tmp(&A);
     build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
@@ -311,9 +339,9 @@ void Composer::run(fstc_result *out) {
       build_cell_flags(c2, c2.cell_flag, s);
     }
   }
-  T.end(kCsr);
+  T.at(kNone);
+  FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 6 * sizeof(u64), hipMemcpyDeviceToHost, s));
   sync_status();
-  read_words(dcounts, 6);
   const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
   const int b1 = (int)bits_for(maxp1 ? maxp1 - 1 : 0);
   const int b2 = (int)bits_for(maxp2 ? maxp2 - 1 : 0);
@@ -381,6 +409,7 @@ void Composer::run(fstc_result *out) {
       sortlist(&level_tmp), tile_runs(&level_tmp), wcnt(&level_tmp), woff(&level_tmp),
       wtmp(&level_tmp), runsrc(&level_tmp), newbits(&level_tmp);
 
+  bool status_clear = true;  // level counters of *dst all zero
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
     const u32 nsrc = hi - lo;
@@ -397,13 +426,14 @@ void Composer::run(fstc_result *out) {
     stmp.ensure(scan3_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
-    launch_reset_level(dst, s);
+    if (!status_clear) launch_reset_level(dst, s);
+    status_clear = false;
     LevelArgs la{view(c1), view(c2), sq1b.as<u32>(), sq2b.as<u32>(), lo, nsrc, cnt.as<u64>(),
                  mc.as<u32>(), roff.as<u64>(), moff.as<u64>(), wide.as<u32>(), heavy.as<u32>(),
                  wrange.as<uint4>(),
                  dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), phdr.as<uint4>(),
-                 product ? 1u : 0u};
-    T.begin();
+                 product ? 1u : 0u, tstart.as<u64>(), mend.as<u64>()};
+    T.at(kCount);
     launch_count(la, s);
     // records, matches and product-merge entries per source
     {
@@ -411,9 +441,10 @@ void Composer::run(fstc_result *out) {
                                {pk.p, false, poff.as<u64>()}};
       exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
     }
-    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, hs_dev, s);
-    T.end(kCount);
-    sync_published();
+    const u32 seq1 = next_publication();
+    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, hs_dev, seq1, s);
+    T.at(kNone);
+    wait_published(seq1);
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
     const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
@@ -463,19 +494,17 @@ void Composer::run(fstc_result *out) {
     la.match = match.as<uint4>();
     la.mrbase = mrbase.as<u64>();
     la.tiles = tiles_e.as<ExpandTile>();
-    T.begin();
-    launch_emit(la, hs->st.nwide, hs->st.nheavy, s);
+    T.at(kExpand);
+    if (M) launch_emit(la, hs->st.nwide, hs->st.nheavy, s);
     // fused levels generate each tile's records inside the merge instead
     const bool fuse = o.fused_merge && !o.no_reduction && key_bits <= kDenseKeyBits && nbig == 0;
-    if (!fuse) {
-      T.chain(kExpand);
+    if (!fuse && R) {
+      T.at(kWriteKernel);
       launch_expand(match.as<uint4>(), mrbase.as<u64>(), M, R, view(c1), view(c2), b2, wide_keys,
                     rkey.p, rw.as<float>(), tiles_e.as<ExpandTile>(), &dst->err, s);
-      T.end(kWriteKernel);
       ++write_launches;
-    } else {
-      T.end(kExpand);
     }
+    T.at(kNone);
     total_matches += M;
 
     // (a6) merge identical arcs, claim new pairs (or, without reduction,
@@ -532,25 +561,25 @@ void Composer::run(fstc_result *out) {
     u32 nnew = 0;
     u64 merged = 0;
     if (!o.no_reduction) {
-      T.begin();
-      fill_u64(tstart.as<u64>(), 0, nsrc, s);
-      fill_u64(mend.as<u64>(), 0, nsrc, s);
-      fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
-      launch_tile_sources(ma, s);
-      T.chain(kMerge);
-      if (fuse) {
-        launch_fuse_merge(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
-        T.chain(kMergeKernel);
-        ++merge_launches;
-        ++fused_levels;
-      } else if (key_bits <= kDenseKeyBits) {
-        launch_merge_dense(ma, s);
-        T.chain(kMergeKernel);
-        ++merge_launches;
+      T.at(kMerge);
+      if (R) {
+        fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
+        launch_tile_sources(ma, s);
+        if (fuse) {
+          T.at(kMergeKernel);
+          launch_fuse_merge(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+          ++merge_launches;
+          ++fused_levels;
+        } else if (key_bits <= kDenseKeyBits) {
+          T.at(kMergeKernel);
+          launch_merge_dense(ma, s);
+          ++merge_launches;
+        }
+        T.at(kSortKernel);
+        launch_merge_sort(ma, wide_keys, s);
+        ++sort_launches;
+        T.at(kMerge);
       }
-      launch_merge_sort(ma, wide_keys, s);
-      T.chain(kSortKernel);
-      ++sort_launches;
       if (nbig) {
         bigcnt.ensure((u64)nbig * 8);
         bigoff.ensure(((u64)nbig + 1) * 8);
@@ -562,9 +591,9 @@ void Composer::run(fstc_result *out) {
         merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, level_tmp, s);
       }
       if (nprod) {
-        T.chain(kMerge);
+        T.at(kProductKernel);
         launch_prod_sources(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
-        T.chain(kProductKernel);
+        T.at(kMerge);
         ++product_launches;
       }
       launch_mcount(ma, mcount.as<u32>(), s);
@@ -573,16 +602,16 @@ void Composer::run(fstc_result *out) {
         exclusive_scan_lb(&job, 1, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
       }
       launch_emit_tiles(ma, s);
-      {
-        const u64 nw = newlist_waves(ma, RB);
-        wcnt.ensure(nw * 4);
-        woff.ensure((nw + 1) * 8);
-        launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB, wcnt.as<u32>(),
-                       woff.as<u64>(), lb(nw), s);
-      }
-      launch_merged_total(aoff.as<u64>() + nsrc, ma, hs_dev, s);
-      T.end(kMerge);
-      sync_published();
+      const u64 nw = newlist_waves(ma, RB);
+      wcnt.ensure(nw * 4);
+      woff.ensure((nw + 1) * 8);
+      const u64 *new_total = launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB,
+                                            wcnt.as<u32>(), woff.as<u64>(), lb(nw), s);
+      const u32 seq2 = next_publication();
+      launch_merged_total(aoff.as<u64>() + nsrc, new_total, ma, hs_dev, seq2, s);
+      T.at(kNone);
+      wait_published(seq2);
+      status_clear = true;  // k_merged_total cleared the level counters
 
       nnew = hs->st.nnew;
       merged = hs->st.merged;
@@ -599,7 +628,7 @@ void Composer::run(fstc_result *out) {
       u32 *osrc = out_arcs.col(0), *odst = out_arcs.col(1), *oil = out_arcs.col(2),
           *ool = out_arcs.col(3);
       float *ow = reinterpret_cast<float *>(out_arcs.col(4));
-      T.begin();
+      T.at(kMerge);
       const u64 nwords = ceil_div(hcap, 32);
       newbits.ensure(nwords * 4);
       fill_u32(newbits.as<u32>(), 0, nwords, s);
@@ -611,7 +640,7 @@ void Composer::run(fstc_result *out) {
       wtmp.ensure(scan_temp_bytes(nw));
       launch_bitlist(newbits.as<u32>(), nwords, newlist.as<u32>(), newcap, wcnt.as<u32>(),
                      woff.as<u64>(), wtmp.p, dst, s);
-      T.end(kMerge);
+      T.at(kNone);
       sync_status();
       nnew = hs->st.nnew;
       merged = R;
@@ -622,7 +651,7 @@ void Composer::run(fstc_result *out) {
       throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");
 
     // (a5) ids for the new pairs; (a7) append the level's arcs
-    T.begin();
+    T.at(kAssign);
     const u64 ns_new = n_states + nnew;
     sq1b.grow_keep(ns_new * 4, n_states * 4);
     sq2b.grow_keep(ns_new * 4, n_states * 4);
@@ -653,7 +682,7 @@ void Composer::run(fstc_result *out) {
         launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc, odst, oil, ool, ow,
                        s);
     }
-    T.end(kAssign);
+    T.at(kNone);
     arcs += merged;
     n_states = ns_new;
     if (nnew) ++new_levels;
@@ -721,11 +750,13 @@ void Composer::run(fstc_result *out) {
     stats->max_level_premerge = max_level_pre;
     stats->big_sources = big_total;
     stats->hash_capacity = hcap;
-    stats->ms_csr = ms[kCsr];
-    stats->ms_count = ms[kCount];
-    stats->ms_expand = ms[kExpand] + ms[kWriteKernel];
-    stats->ms_merge = ms[kMerge] + ms[kMergeKernel] + ms[kSortKernel] + ms[kProductKernel];
-    stats->ms_assign = ms[kAssign];
+    if (T.all) {
+      stats->ms_csr = ms[kCsr];
+      stats->ms_count = ms[kCount];
+      stats->ms_expand = ms[kExpand] + ms[kWriteKernel];
+      stats->ms_merge = ms[kMerge] + ms[kMergeKernel] + ms[kSortKernel] + ms[kProductKernel];
+      stats->ms_assign = ms[kAssign];
+    }
     stats->ms_total =
         std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
   }

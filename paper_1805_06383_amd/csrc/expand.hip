@@ -115,6 +115,8 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   if (u < a.nsrc) {
     const u32 sid = a.lo + (u32)u;
     const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
+    a.tstart[u] = 0;
+    a.mend[u] = 0;
     r = Ranges{a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]};
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
     if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r);
@@ -263,13 +265,18 @@ __device__ __forceinline__ Hit wave_probe(const LevelArgs &a, const Ranges &r, b
   return one_short ? Hit{true, idx, fpos} : Hit{true, fpos, idx};
 }
 
-// Wavefront per source (grid-stride over the wide list).
-__global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
-  __shared__ u32 s_max;
-  u32 run_max = 0;
+// The joins of the listed sources, one launch of kListNT-thread blocks:
+// blocks [0, gw) take the wide list with a wavefront per source, the others
+// the heavy list with the whole block per source (both grid-stride over
+// their list, whose length the small-source kernel left in *st).
+constexpr int kListNT = 512;
+constexpr int kHeavyNT = kListNT;
+
+__device__ __forceinline__ void count_wide_sources(const LevelArgs &a, u32 blk, u32 nblk,
+                                                   u32 &run_max) {
   const u32 lane = lane_id();
-  const u32 gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
-  const u32 nw = gridDim.x * blockDim.x / kWave;
+  const u32 gw = (blk * kListNT + threadIdx.x) / kWave;
+  const u32 nw = nblk * kListNT / kWave;
   const u32 n = a.st->nwide;
   for (u32 i = gw; i < n; i += nw) {
     const u32 u = a.wide[i];
@@ -295,41 +302,45 @@ __global__ __launch_bounds__(256) void k_count_wide(LevelArgs a) {
       note_count(a, u, cnt, run_max);
     }
   }
-  publish_max<256>(a, run_max, &s_max);
 }
 
-// Workgroup per source (grid-stride over the heavy list).
-constexpr int kHeavyNT = 512;
-
-__global__ __launch_bounds__(kHeavyNT) void k_count_heavy(LevelArgs a) {
-  __shared__ u64 s64[kHeavyNT / kWave];
-  __shared__ u32 s32[kHeavyNT / kWave];
-  __shared__ u32 s_max;
-  u32 run_max = 0;
+__device__ __forceinline__ void count_heavy_sources(const LevelArgs &a, u32 blk, u32 nblk,
+                                                    u32 &run_max, u64 *s64, u32 *s32) {
   const u32 n = a.st->nheavy;
-  for (u32 i = blockIdx.x; i < n; i += gridDim.x) {
+  for (u32 i = blk; i < n; i += nblk) {
     const u32 u = a.heavy[i];
     const Ranges r = source_ranges(a, u);
     const bool one_short = (r.e1 - r.b1) <= (r.e2 - r.b2);
     const u32 bs = one_short ? r.b1 : r.b2, es = one_short ? r.e1 : r.e2;
     u64 cnt = 0;
     u32 mc = 0;
-    for (u32 base = bs; base < es; base += kHeavyNT) {
+    for (u32 base = bs; base < es; base += kListNT) {
       const Hit h = probe_one(a, r, one_short, base + threadIdx.x);
       if (h.found) {
         cnt += (u64)seg_len(a.c1.seg_off, h.s1) * seg_len(a.c2.seg_off, h.s2);
         ++mc;
       }
     }
-    cnt = block_sum<kHeavyNT, u64>(cnt, s64);
-    mc = block_sum<kHeavyNT, u32>(mc, s32);
+    cnt = block_sum<kListNT, u64>(cnt, s64);
+    mc = block_sum<kListNT, u32>(mc, s32);
     if (threadIdx.x == 0) {
       a.cnt[u] = cnt;
       a.mc[u] = mc;
       note_count(a, u, cnt, run_max);
     }
   }
-  publish_max<kHeavyNT>(a, run_max, &s_max);
+}
+
+__global__ __launch_bounds__(kListNT) void k_count_lists(LevelArgs a, u32 gw) {
+  __shared__ u64 s64[kListNT / kWave];
+  __shared__ u32 s32[kListNT / kWave];
+  __shared__ u32 s_max;
+  u32 run_max = 0;
+  if (blockIdx.x < gw)
+    count_wide_sources(a, blockIdx.x, gw, run_max);
+  else
+    count_heavy_sources(a, blockIdx.x - gw, gridDim.x - gw, run_max, s64, s32);
+  publish_max<kListNT>(a, run_max, &s_max);
 }
 
 // ---------------------------------------------------------------------------
@@ -622,8 +633,12 @@ static unsigned heavy_grid(u64 n) { return (unsigned)std::min<u64>(512, n); }
 void launch_count(const LevelArgs &a, hipStream_t s) {
   const unsigned g = (unsigned)ceil_div(a.nsrc, kCountNT);
   hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
-  hipLaunchKernelGGL(k_count_wide, dim3(wide_grid(a.nsrc)), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(k_count_heavy, dim3(heavy_grid(a.nsrc)), dim3(kHeavyNT), 0, s, a);
+  // wide: at most one wave per source (1024 blocks of 8 waves at most);
+  // heavy: one block per source (512 blocks at most)
+  const u64 n = a.nsrc;
+  const unsigned gw = (unsigned)std::min<u64>(1024, ceil_div(n, kListNT / kWave));
+  const unsigned gh = (unsigned)std::min<u64>(512, n);
+  hipLaunchKernelGGL(k_count_lists, dim3(gw + gh), dim3(kListNT), 0, s, a, gw);
 }
 
 void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s) {

@@ -38,6 +38,7 @@ struct Status {
   u32 nsort;          // tiles k_merge_dense left to the sort kernel
   u32 nprod;          // sources of the product merge
   u32 scan_ctr;       // tile counter of the single-pass scans (0 between scans)
+  u32 seq;            // host copy only: number of the last publication, written last
   u64 prod_records;   // their joined arc pairs (not written as records)
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
 };
@@ -112,6 +113,8 @@ struct LevelArgs {
   u32 *pk;               // [nsrc] table entries of a product-merge source, else 0
   uint4 *phdr;           // [2 nsrc] product-merge source header (see ProdHeader)
   u32 prod;              // nonzero: sources may take the product merge
+  u64 *tstart, *mend;    // [nsrc] the merge's first / end temp slot per source:
+                         // zeroed by the count kernel
 };
 
 // Written by the count kernel for a product-merge source u at phdr[2u], [2u+1]:
@@ -224,14 +227,15 @@ void launch_mcount(const MergeArgs &a, u32 *mcount, hipStream_t s);
 // tile-merged sources (merge_big does its own).
 void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
 // New-state list of the level from the claimed-slot flags of the tile runs,
-// the multi-block runs and the product-merge slots (st->nnew = its length).
-// wcnt: newlist_waves(a, RB) u32; woff: that + 1 u64; scan_tmp:
-// scan_temp_bytes(newlist_waves(a, RB)) bytes.
+// the multi-block runs and the product-merge slots.  Returns the device
+// address of its length (for launch_merged_total), or NULL when there is
+// nothing to list.
+// wcnt: newlist_waves(a, RB) u32; woff: that + 1 u64.
 // scan_state: scan_lb_state_bytes(newlist_waves(a, RB)) bytes of single-pass
 // scan state (see exclusive_scan_lb).
 u64 newlist_waves(const MergeArgs &a, u64 RB);
-void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
-                    void *scan_state, hipStream_t s);
+const u64 *launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt,
+                          u64 *woff, void *scan_state, hipStream_t s);
 // Composition without reduction: every record of the level becomes an arc
 // (osrc.. at [0, R)), its target pair claimed in the visited table and each
 // new claim flagged in `newbits` (one bit per table slot, cleared by the
@@ -248,11 +252,16 @@ void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, 
 void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
-// Both also copy *st to `host` (pinned memory the device can write).
-void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host,
+// Both also copy *st to `host` (pinned, coherent host memory the device can
+// write) and then set host->seq = seq, so that the host can wait for the
+// copy by watching that word.
+void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host, u32 seq,
                          hipStream_t s);
-// Level total of merged arcs, plus the dense / sort tile statistics of st.
-void launch_merged_total(const u64 *a_total, const MergeArgs &a, Status *host, hipStream_t s);
+// Level total of merged arcs, new pairs (*new_total, when not NULL) and the
+// dense / sort tile statistics of st; after publishing it clears the level
+// counters of *st for the next level (what launch_reset_level does).
+void launch_merged_total(const u64 *a_total, const u64 *new_total, const MergeArgs &a, Status *host,
+                         u32 seq, hipStream_t s);
 void launch_reset_level(Status *st, hipStream_t s);
 
 }  // namespace fstc

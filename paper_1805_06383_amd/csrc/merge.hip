@@ -1633,26 +1633,45 @@ __global__ void k_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f
     fin[i] = (f1[sq1[i]] != 0 && f2[sq2[i]] != 0) ? 1 : 0;
 }
 
-// Copies the level counters to host memory (pinned, device-visible), so the
-// host reads them after a stream synchronisation without a separate copy.
-__device__ __forceinline__ void publish(const Status *st, Status *host, u32 t, u32 nt) {
+// Copies the level counters to host memory (pinned, coherent, device-
+// visible), then, after a system-scope fence, the publication number: the
+// host waits for that word instead of a stream synchronisation.  Threads
+// t = 0 .. nt-1 of one workgroup call it together.
+__device__ __forceinline__ void publish(const Status *st, Status *host, u32 seq, u32 t, u32 nt) {
   const u32 *src = reinterpret_cast<const u32 *>(st);
   u32 *dst = reinterpret_cast<u32 *>(host);
-  for (u32 i = t; i < sizeof(Status) / 4; i += nt) dst[i] = src[i];
+  constexpr u32 kSeqWord = offsetof(Status, seq) / 4;
+  for (u32 i = t; i < sizeof(Status) / 4; i += nt)
+    if (i != kSeqWord) dst[i] = src[i];
+  __threadfence_system();
+  if (nt > 1) __syncthreads();
+  if (t == 0) __hip_atomic_store(&host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-__global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st, Status *host) {
+__device__ __forceinline__ void clear_level(Status *st) {
+  st->R = st->M = st->merged = st->RB = 0;
+  st->nwide = st->nheavy = st->nbig = st->nnew = 0;
+  st->max_small = 0;
+  st->dense_records = st->dense_runs = st->sort_runs = 0;
+  st->nprod = 0;
+  st->prod_records = st->prod_entries = 0;
+  st->nsort = 0;
+}
+
+__global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st, Status *host, u32 seq) {
   st->R = *rt;
   st->M = *mt;
-  publish(st, host, 0, 1);
+  publish(st, host, seq, 0, 1);
 }
 
 // Level totals after the merge: merged arcs (end of the scan of merged arcs
-// per source), and, over the merge tiles, the records and runs of the tiles
-// the dense-table kernel merged and the runs of those the sort kernel merged.
-// One workgroup: it also publishes the counters to host memory at the end.
-__global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, Status *st, MergeArgs a,
-                                                       Status *host) {
+// per source), new pairs (end of the scan of the new-pair lists), and, over
+// the merge tiles, the records and runs of the tiles the dense-table kernel
+// merged and the runs of those the sort kernel merged.  One workgroup: it
+// publishes the counters to host memory and then clears them for the next
+// level.
+__global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 *nt, Status *st,
+                                                       MergeArgs a, Status *host, u32 seq) {
   __shared__ u64 s_v[3][1024 / kWave];
   u64 v[3] = {0, 0, 0};
   for (u64 t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
@@ -1676,24 +1695,18 @@ __global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, Status *st
     u64 t = 0;
     for (int i = 0; i < 1024 / kWave; ++i) t += s_v[threadIdx.x][i];
     u64 *dst = threadIdx.x == 0 ? &st->dense_records : threadIdx.x == 1 ? &st->dense_runs : &st->sort_runs;
-    *dst += t;
+    *dst = t;
   }
   if (threadIdx.x == 3) st->merged = *at;
+  if (threadIdx.x == 4 && nt) st->nnew = (u32)min<u64>(*nt, 0xffffffffull);
   __syncthreads();
   __threadfence();
-  publish(st, host, threadIdx.x, blockDim.x);
+  publish(st, host, seq, threadIdx.x, blockDim.x);
+  if (threadIdx.x == 0) clear_level(st);
 }
 
 __global__ void k_reset_level(Status *st) {
-  if (threadIdx.x == 0) {
-    st->R = st->M = st->merged = st->RB = 0;
-    st->nwide = st->nheavy = st->nbig = st->nnew = 0;
-    st->max_small = 0;
-    st->dense_records = st->dense_runs = st->sort_runs = 0;
-    st->nprod = 0;
-    st->prod_records = st->prod_entries = 0;
-    st->nsort = 0;
-  }
+  if (threadIdx.x == 0) clear_level(st);
 }
 
 }  // namespace
@@ -1856,11 +1869,11 @@ u64 newlist_waves(const MergeArgs &a, u64 RB) {
   return a.ntiles + ceil_div(RB, kWave) + ceil_div(a.prodpos, (u64)kWave);
 }
 
-void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt, u64 *woff,
-                    void *scan_state, hipStream_t s) {
+const u64 *launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt,
+                          u64 *woff, void *scan_state, hipStream_t s) {
   const u64 nbigw = ceil_div(RB, kWave);
   const u64 nw = newlist_waves(a, RB);
-  if (nw == 0) return;  // st->nnew stays 0
+  if (nw == 0) return nullptr;  // no new pairs
   const unsigned g = (unsigned)ceil_div(nw, 256 / kWave);
   hipLaunchKernelGGL(k_newlist<0>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
                      (const u64 *)nullptr);
@@ -1868,7 +1881,7 @@ void launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32
   exclusive_scan_lb(&job, 1, nw, scan_state, &a.st->scan_ctr, &a.st->err, s);
   hipLaunchKernelGGL(k_newlist<1>, dim3(g), dim3(256), 0, s, a, bigoff, nbig, RB, nbigw, wcnt,
                      (const u64 *)woff);
-  hipLaunchKernelGGL(k_new_total, dim3(1), dim3(1), 0, s, (const u64 *)(woff + nw), a.st);
+  return woff + nw;
 }
 
 void launch_emit_tiles(const MergeArgs &a, hipStream_t s) {
@@ -1891,13 +1904,15 @@ void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, con
   hipLaunchKernelGGL(k_finals, dim3(grid1(n)), dim3(256), 0, s, sq1, sq2, n, f1, f2, fin);
 }
 
-void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host,
+void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host, u32 seq,
                          hipStream_t s) {
-  hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st, host);
+  hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st, host, seq);
 }
 
-void launch_merged_total(const u64 *a_total, const MergeArgs &a, Status *host, hipStream_t s) {
-  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1024), 0, s, a_total, a.st, a, host);
+void launch_merged_total(const u64 *a_total, const u64 *new_total, const MergeArgs &a, Status *host,
+                         u32 seq, hipStream_t s) {
+  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1024), 0, s, a_total, new_total, a.st, a, host,
+                     seq);
 }
 
 void launch_reset_level(Status *st, hipStream_t s) {

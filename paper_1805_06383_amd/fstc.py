@@ -53,7 +53,7 @@ class FstcOpts(ctypes.Structure):
     _fields_ = [("max_levels", _u32), ("deterministic_ids", _u32), ("max_states", _u64),
                 ("max_arcs", _u64), ("alloc", ALLOC_FN), ("free", FREE_FN), ("alloc_ctx", _vp),
                 ("no_reduction", _u32), ("fused_merge", _u32), ("no_product_merge", _u32),
-                ("hash_visited", _u32)]
+                ("hash_visited", _u32), ("phase_timing", _u32), ("reserved0", _u32)]
 
 
 class FstcResult(ctypes.Structure):
@@ -175,10 +175,12 @@ class TorchAllocator:
         return self.live.pop(int(ptr))
 
     def opts(self, max_levels=0, deterministic_ids=False, max_states=0, max_arcs=0,
-             reduce=True, fused=False, product=True, hash_visited=False) -> FstcOpts:
+             reduce=True, fused=False, product=True, hash_visited=False,
+             phase_timing=False) -> FstcOpts:
         return FstcOpts(int(max_levels), 1 if deterministic_ids else 0, int(max_states),
                         int(max_arcs), self._alloc, self._free, None, 0 if reduce else 1,
-                        1 if fused else 0, 0 if product else 1, 1 if hash_visited else 0)
+                        1 if fused else 0, 0 if product else 1, 1 if hash_visited else 0,
+                        1 if phase_timing else 0, 0)
 
 
 # ---------------------------------------------------------------------------
@@ -277,18 +279,20 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
                  deterministic_ids: bool = False, max_states: int = 0, max_arcs: int = 0,
                  stream=None, want_stats: bool = True, reduce: bool = True,
                  fused: bool = False, product: bool = True,
-                 hash_visited: bool = False) -> Composed:
+                 hash_visited: bool = False, phase_timing: bool = False) -> Composed:
     """Reachable composition m1 o m2 on the GPU (see fstc_compose in fstc.h).
     reduce=False keeps every joined arc pair as its own arc (opts.no_reduction);
     fused=True merges tiles without writing their composed arcs first
     (opts.fused_merge); product=False sends every source through written
     records (opts.no_product_merge); hash_visited=True keeps the visited set
-    in the hash table even for small pair spaces (opts.hash_visited)."""
+    in the hash table even for small pair spaces (opts.hash_visited);
+    phase_timing=True fills the per-phase times of the stats
+    (opts.phase_timing; the kernel times are always there)."""
     lib = load_library()
     device = m1.src.device if m1.num_arcs else m1.final.device
     alloc = TorchAllocator(device)
     opts = alloc.opts(max_levels, deterministic_ids, max_states, max_arcs, reduce, fused, product,
-                      hash_visited)
+                      hash_visited, phase_timing)
     s1, s2 = m1.struct(), m2.struct()
     res = FstcResult()
     st = FstcStats()

@@ -76,3 +76,23 @@ def test_default_allocator_round_trip(env, case):
     assert g.num_premerge == ref.num_premerge
     # arcs grouped by source id
     assert np.all(np.diff(g.src.astype(np.int64)) >= 0)
+
+
+def test_phase_timing(env):
+    """Without opts.phase_timing only the single-kernel spans are timed (the
+    phase times stay 0); with it every phase is; the result is the same."""
+    F, lib, hip = env
+    m1, m2 = W.config4(0)
+    d1, d2 = F.DeviceFST.from_host(m1, "cuda"), F.DeviceFST.from_host(m2, "cuda")
+    a = F.fstc_compose(d1, d2, max_levels=3)
+    b = F.fstc_compose(d1, d2, max_levels=3, phase_timing=True)
+    phases = ("ms_csr", "ms_count", "ms_expand", "ms_merge", "ms_assign")
+    assert all(a.stats[k] == 0 for k in phases)
+    assert all(b.stats[k] > 0 for k in ("ms_csr", "ms_count", "ms_merge", "ms_assign"))
+    for r in (a, b):
+        assert r.stats["product_launches"] == 3 and r.stats["ms_product_kernel"] > 0
+        assert r.stats["write_launches"] == 0  # every source of config 4 takes the product merge
+    assert b.stats["ms_merge"] >= b.stats["ms_product_kernel"]
+    x, y = a.to_host(), b.to_host()
+    assert x.num_states == y.num_states and len(x.src) == len(y.src)
+    assert_same(canon_of(x), canon_of(y), what="phase timing on / off")
