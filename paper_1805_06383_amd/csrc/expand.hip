@@ -95,6 +95,15 @@ __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1,
   return p1 * p2;
 }
 
+// True when source ranges r are joined by one thread (the rule beside
+// kWideMin); the count and emit kernels classify alike.
+__device__ __forceinline__ bool thread_join(const LevelArgs &a, const Ranges &r) {
+  const u32 n1 = r.e1 - r.b1, n2 = r.e2 - r.b2;
+  const u32 mn = min(n1, n2), mx = max(n1, n2);
+  if (mn > kWideMin) return false;
+  return a.nsrc >= kFewSources || mn * (32u - __clz(mx)) <= kSerialSteps;
+}
+
 // Thread per source: selects the product-merge sources (no records, no
 // matches; pk = their entry count), joins the other short ones, lists the
 // rest for the wavefront / workgroup joins.  List appends, the window
@@ -126,7 +135,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
       a.mc[u] = 0;
     } else if (mn > kHeavyMin) {
       pred[1] = true;
-    } else if (mn > kWideMin) {
+    } else if (!thread_join(a, r)) {
       pred[0] = true;
     } else {
       u32 mc = 0;
@@ -241,8 +250,21 @@ __device__ __forceinline__ Hit wave_probe(const LevelArgs &a, const Ranges &r, b
   const u32 idx = base + lane;
   const bool valid = idx < es;
   const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
-  const u32 smax = __shfl(sym, (int)(min(es - base, (u32)kWave) - 1), kWave);
+  const u32 last = min(es - base, (u32)kWave) - 1;
+  const u32 smax = __shfl(sym, (int)last, kWave);
   u32 fpos = 0xffffffffu;
+  if (le - lp > 4u * kWave) {
+    // a long remainder: each lane binary-searches its symbol (fewer
+    // dependent loads than walking the chunks)
+    u32 l = lp;
+    if (valid) {
+      l = lower_bound_u32(lsym, lp, le, sym);
+      if (l < le && lsym[l] == sym) fpos = l;
+    }
+    lp = __shfl(l, (int)last, kWave);  // later short symbols are above smax
+    if (fpos == 0xffffffffu) return Hit{false, 0, 0};
+    return one_short ? Hit{true, idx, fpos} : Hit{true, fpos, idx};
+  }
   for (u32 c = lp; c < le; c += kWave) {
     const u32 len = min(le - c, (u32)kWave);
     const u32 lv = lane < len ? lsym[c + lane] : 0xffffffffu;
@@ -360,7 +382,7 @@ __global__ __launch_bounds__(256) void k_emit_small(LevelArgs a) {
   if (u >= a.nsrc) return;
   if (a.pk[u]) return;  // product merge: no matches, no records
   const Ranges r = source_ranges(a, (u32)u);
-  if (min(r.e1 - r.b1, r.e2 - r.b2) > kWideMin) return;
+  if (!thread_join(a, r)) return;
   u64 k = a.moff[u], rb = a.roff[u];
   intersect_serial(a.c1.seg_sym, r.b1, r.e1, a.c2.seg_sym, r.b2, r.e2, [&](u32 s1, u32 s2) {
     put_match(a, k, s1, s2, rb);

@@ -54,9 +54,15 @@ constexpr u32 kProdRowSum = 16;
 constexpr u32 kProdMinSymbols = 8;
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
-// wavefront, longer than kHeavyMin by a workgroup; others by one thread.
+// wavefront, longer than kHeavyMin by a workgroup; others by one thread,
+// except on levels of fewer than kFewSources sources (too few threads to
+// hide a long chain of dependent loads), where a source whose serial join
+// takes more than kSerialSteps binary-search steps (shorter length x bits of
+// the longer length) goes to a wavefront too.
 constexpr u32 kWideMin = 24;
 constexpr u32 kHeavyMin = 2048;
+constexpr u32 kFewSources = 1u << 16;
+constexpr u32 kSerialSteps = 48;
 
 // Merge tiles: 512 threads x 8 items = 4096 records of LDS capacity.  Sources
 // of more than kMergeSmall records take the multi-block path.  A tile takes
