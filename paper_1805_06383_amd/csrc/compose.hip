@@ -82,6 +82,15 @@ void *Arena::take(size_t bytes) {
   return p;
 }
 
+void Arena::reserve(size_t bytes) {
+  if (used || bytes == 0) return;
+  size_t total = 0;
+  for (auto &c : chunks) total += c.cap;
+  if (total >= bytes) return;
+  release();
+  chunks.push_back({static_cast<char *>(A->alloc(bytes)), bytes});
+}
+
 void Arena::reset() {
   ++epoch;
   if (chunks.size() > 1) {
@@ -315,22 +324,22 @@ void Composer::run(fstc_result *out) {
   hs = staging();
   FSTC_HIP(hipHostGetDevicePointer((void **)&hs_dev, hs, 0));
 
-  Buf stb(&A), cntb(&A);
-  dst = (Status *)stb.ensure(sizeof(Status));
-  u64 *dcounts = (u64 *)cntb.ensure(8 * sizeof(u64));
+  static_assert(sizeof(Status) <= 256, "Status and the CSR counts share one allocation");
+  Buf stb(&A);
+  dst = (Status *)stb.ensure(256 + 8 * sizeof(u64));
+  u64 *dcounts = reinterpret_cast<u64 *>(reinterpret_cast<char *>(dst) + 256);
   fill_u32((u32 *)dst, 0, sizeof(Status) / 4, s);
 
   // (a0) device layout of both inputs
-  Buf cb1[7], cb2[7], cf1(&A), cf2(&A);
+  Buf cb1(&A), cb2(&A);
   Csr c1, c2;
-  alloc_csr(m1, A, cb1, c1);
-  alloc_csr(m2, A, cb2, c2);
-  c1.cell_flag = (u32 *)cf1.ensure(std::max<u64>(m1.num_states, 1) * 4);
-  c2.cell_flag = (u32 *)cf2.ensure(std::max<u64>(m2.num_states, 1) * 4);
+  alloc_csr(m1, cb1, c1);
+  alloc_csr(m2, cb2, c2);
   const bool product = !o.no_reduction && !o.no_product_merge;
   T.at(kCsr);
   {
     Arena csr_tmp(&A);
+    csr_tmp.reserve(std::max(csr_temp_bytes(m1), csr_temp_bytes(m2)));
     build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
     csr_tmp.reset();
     build_csr(m2, false, csr_tmp, c2, dcounts + 3, &dst->err, s);

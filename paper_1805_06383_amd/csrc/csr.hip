@@ -13,6 +13,9 @@
 // (target pair, input, output) is then fixed by the two parts it joins, so
 // the merge sorts short part-rank keys instead of full labels.
 #include "internal.hpp"
+#include "radix_rank.hpp"
+
+#include <initializer_list>
 
 namespace fstc {
 namespace {
@@ -127,6 +130,339 @@ __global__ void k_fill_tail(u32 *a, const u32 *count, u64 n, u32 v) {
     a[i] = v;
 }
 
+// ---------------------------------------------------------------------------
+// Per-state build.  After one stable sort of the arcs by source state, each
+// state's arcs (in input order) are sorted inside one workgroup: by
+// (target, outer symbol) to rank its parts, and stably by inner symbol to
+// lay out its segments.  A state's parts and segments are first written at
+// its own arc offset (a state has at most as many of each as arcs); a scan
+// of the per-state counts then gives part_base and row, and a last pass
+// moves them to their final places.  Same layout as the global sorts.
+
+// Size classes of the per-state build: groups of 16 and of 64 lanes of a
+// wavefront per state up to 16 and kWave arcs, then workgroups of 256
+// threads with 1 and 4 items per thread, and of 1024 threads with 8 items
+// per thread (several tiles per sort pass beyond 8192 arcs).
+constexpr int kLocClasses = 5;
+__host__ __device__ constexpr u32 loc_class(u32 d) {
+  return d <= 16u ? 0u : d <= (u32)kWave ? 1u : d <= 256u ? 2u : d <= 1024u ? 3u : 4u;
+}
+
+struct LocalArgs {
+  const u64 *skey;     // [n] source state of each position (sorted)
+  const u32 *order;    // [n] arc index at each position (input order within a state)
+  const u32 *abase;    // [nq + 1] first position of each state
+  const u32 *dst, *inner, *outer;
+  const float *w;
+  int bo, bp, bi;      // outer-symbol bits, part-key bits, inner-symbol bits
+  u64 *ka, *kb;        // [n] sort keys (two buffers)
+  u32 *ia, *ib;        // [n] element numbers within the state (two buffers)
+  u32 *part_of;        // [n] part rank of element i of a state at abase + i
+  uint2 *ptmp;         // [n] parts of a state at its arc offset
+  u32 *ssym, *soff;    // [n] segments of a state at its arc offset
+  uint2 *arcs;         // [n] the CSR arcs
+  u32 *pcnt, *scnt;    // [nq] parts / segments per state
+  u64 *maxp;           // largest part count
+};
+
+// Raises *m to v.  Same-address atomics serialise, so the current value is
+// read first and only a larger v issues one (a handful per launch).
+__device__ __forceinline__ void note_max(u64 *m, u64 v) {
+  if (v > __hip_atomic_load(m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+    atomicMax((unsigned long long *)m, (unsigned long long)v);
+}
+
+// Stable LSD sort of the d keys at a0 (8-bit digits, `bits` key bits) in
+// tiles of NT * IT elements; bucket bases come from a histogram over the
+// state when it spans more than one tile.  On return kin / iin hold the
+// sorted keys and element numbers.
+template <int NT, int IT>
+__device__ void local_sort(u64 *&kin, u32 *&iin, u64 *&kout, u32 *&iout, u32 a0, u32 d,
+                           int bits, u32 *s_cnt, u32 *s_base, u32 *s_tmp, u32 *s_run) {
+  constexpr u32 kTile = NT * IT;
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const bool multi = d > kTile;
+  for (int shift = 0; shift < bits; shift += 8) {
+    const int db = min(8, bits - shift);
+    const u32 mask = (1u << db) - 1u;
+    if (multi) {
+      if (threadIdx.x < 256) s_run[threadIdx.x] = 0;
+      __syncthreads();
+      for (u32 i = threadIdx.x; i < d; i += NT)
+        atomicAdd(&s_run[(u32)(kin[a0 + i] >> shift) & mask], 1u);
+      __syncthreads();
+      u32 tot;
+      const u32 ex = block_exclusive_sum<NT, u32>(threadIdx.x < 256 ? s_run[threadIdx.x] : 0u,
+                                                  s_tmp, &tot);
+      __syncthreads();
+      if (threadIdx.x < 256) s_run[threadIdx.x] = ex;
+      __syncthreads();
+    }
+    for (u32 t0 = 0; t0 < d; t0 += kTile) {
+      u64 key[IT];
+      u32 val[IT], dig[IT], rid[IT];
+      u32 valid = 0;
+#pragma unroll
+      for (int j = 0; j < IT; ++j) {
+        const u32 i = t0 + w * (kWave * IT) + j * kWave + lane;
+        const bool v = i < d;
+        valid |= (v ? 1u : 0u) << j;
+        key[j] = v ? kin[a0 + i] : 0;
+        val[j] = v ? iin[a0 + i] : 0;
+        dig[j] = (u32)(key[j] >> shift) & mask;
+      }
+      block_rank_digits<NT, IT>(dig, valid, db, rid, s_cnt, s_base, s_tmp);
+#pragma unroll
+      for (int j = 0; j < IT; ++j) {
+        if (!((valid >> j) & 1u)) continue;
+        const u32 pos = (multi ? s_run[dig[j]] : s_base[dig[j]]) + rid[j];
+        kout[a0 + pos] = key[j];
+        iout[a0 + pos] = val[j];
+      }
+      if (multi) {
+        __syncthreads();  // every s_run read of this tile is done
+        const u32 nv = min(d - t0, kTile);
+        const u32 t = threadIdx.x;
+        if (t < 256) s_run[t] += (t + 1 < 256u ? s_base[t + 1] : nv) - s_base[t];
+        __syncthreads();
+      }
+    }
+    __syncthreads();  // kout complete before it is read
+    u64 *tk = kin; kin = kout; kout = tk;
+    u32 *tv = iin; iin = iout; iout = tv;
+  }
+}
+
+// Run heads of the sorted keys at a0: calls f(i, run, is_head) for every
+// position i with its run number; returns the number of runs.
+template <int NT, class F>
+__device__ u32 local_runs(const u64 *k, u32 a0, u32 d, u32 *s_tmp, F &&f) {
+  u32 carry = 0;
+  for (u32 t0 = 0; t0 < d; t0 += NT) {
+    const u32 i = t0 + threadIdx.x;
+    const bool v = i < d;
+    const bool head = v && (i == 0 || k[a0 + i] != k[a0 + i - 1]);
+    u32 tot;
+    const u32 ex = block_exclusive_sum<NT, u32>(head ? 1u : 0u, s_tmp, &tot);
+    if (v) f(i, carry + ex + (head ? 1u : 0u) - 1u, head);
+    carry += tot;
+  }
+  return carry;
+}
+
+// One workgroup per listed state (grid-stride over the list).
+template <int NT, int IT>
+__global__ __launch_bounds__(NT) void k_state_local(LocalArgs a, const u32 *list,
+                                                    const u32 *list_len) {
+  __shared__ u32 s_cnt[(NT / kWave) * 256];
+  __shared__ u32 s_base[256];
+  __shared__ u32 s_run[256];
+  __shared__ u32 s_tmp[NT / kWave];
+  const u32 nlist = *list_len;
+  const u64 omask = a.bo ? ((1ull << a.bo) - 1) : 0;
+  for (u32 li = blockIdx.x; li < nlist; li += gridDim.x) {
+    const u32 q = list[li];
+    const u32 a0 = a.abase[q], d = a.abase[q + 1] - a0;
+    // parts: ranks of the distinct (target, outer) keys
+    for (u32 i = threadIdx.x; i < d; i += NT) {
+      const u32 e = a.order[a0 + i];
+      a.ka[a0 + i] = ((u64)a.dst[e] << a.bo) | a.outer[e];
+      a.ia[a0 + i] = i;
+    }
+    __syncthreads();
+    u64 *kin = a.ka, *kout = a.kb;
+    u32 *iin = a.ia, *iout = a.ib;
+    local_sort<NT, IT>(kin, iin, kout, iout, a0, d, a.bp, s_cnt, s_base, s_tmp, s_run);
+    const u32 np = local_runs<NT>(kin, a0, d, s_tmp, [&](u32 i, u32 r, bool head) {
+      a.part_of[a0 + iin[a0 + i]] = r;
+      if (head) {
+        const u64 k = kin[a0 + i];
+        a.ptmp[a0 + r] = make_uint2((u32)(k >> a.bo), (u32)(k & omask));
+      }
+    });
+    __syncthreads();  // part_of complete; sort buffers free
+    // segments: stable sort by inner symbol
+    for (u32 i = threadIdx.x; i < d; i += NT) {
+      a.ka[a0 + i] = a.inner[a.order[a0 + i]];
+      a.ia[a0 + i] = i;
+    }
+    __syncthreads();
+    kin = a.ka; kout = a.kb; iin = a.ia; iout = a.ib;
+    local_sort<NT, IT>(kin, iin, kout, iout, a0, d, a.bi, s_cnt, s_base, s_tmp, s_run);
+    const u32 ns = local_runs<NT>(kin, a0, d, s_tmp, [&](u32 i, u32 r, bool head) {
+      const u32 el = iin[a0 + i];
+      a.arcs[a0 + i] = make_uint2(a.part_of[a0 + el], __float_as_uint(a.w[a.order[a0 + el]]));
+      if (head) {
+        a.ssym[a0 + r] = (u32)kin[a0 + i];
+        a.soff[a0 + r] = a0 + i;
+      }
+    });
+    if (threadIdx.x == 0) {
+      a.pcnt[q] = np;
+      a.scnt[q] = ns;
+      note_max(a.maxp, np);
+    }
+    __syncthreads();  // shared arrays free for the next state
+  }
+}
+
+// Bitonic sort of one (key, element) pair per lane within each group of G
+// lanes, ascending by key and then element number (so equal keys keep their
+// element order).
+template <int G>
+__device__ __forceinline__ void group_sort(u64 &k, u32 &i) {
+  const u32 lane = lane_id();
+#pragma unroll
+  for (u32 size = 2; size <= (u32)G; size <<= 1) {
+#pragma unroll
+    for (u32 j = size >> 1; j > 0; j >>= 1) {
+      const u64 ok = __shfl_xor(k, (int)j, kWave);
+      const u32 oi = __shfl_xor(i, (int)j, kWave);
+      const bool up = (lane & size) == 0 || size == (u32)G;  // this run ascends
+      const bool low = (lane & j) == 0;                       // lower lane of the pair
+      const bool other_less = ok < k || (ok == k && oi < i);
+      if ((low == up) == other_less) {
+        k = ok;
+        i = oi;
+      }
+    }
+  }
+}
+
+// A group of G lanes per listed state of at most G arcs (group lane =
+// element): the same two sorts as k_state_local, in registers.
+template <int G>
+__global__ __launch_bounds__(256) void k_state_group(LocalArgs a, const u32 *list,
+                                                     const u32 *list_len) {
+  constexpr u32 kPer = kWave / G;  // states per wavefront
+  const u32 lane = lane_id(), gl = lane % G, gb = lane - gl;
+  const u64 gmask = (G == kWave) ? ~0ull : (((1ull << G) - 1) << gb);
+  const u32 nlist = *list_len;
+  const u64 omask = a.bo ? ((1ull << a.bo) - 1) : 0;
+  const u32 nw = gridDim.x * (blockDim.x / kWave);
+  for (u32 wi = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; wi * kPer < nlist;
+       wi += nw) {
+    const u32 li = wi * kPer + lane / G;
+    const u32 q = li < nlist ? list[li] : 0u;
+    const u32 a0 = li < nlist ? a.abase[q] : 0u;
+    const u32 d = li < nlist ? a.abase[q + 1] - a0 : 0u;
+    const bool v = gl < d;
+    const u32 e = v ? a.order[a0 + gl] : 0u;
+    // parts
+    u64 k = v ? (((u64)a.dst[e] << a.bo) | a.outer[e]) : ~0ull;
+    u32 el = gl;
+    group_sort<G>(k, el);
+    const u64 kprev = __shfl(k, (int)(lane ? lane - 1 : 0), kWave);
+    bool head = v && (gl == 0 || k != kprev);
+    u64 hm = __ballot(head) & gmask;
+    const u32 np = (u32)__popcll(hm);
+    const u32 prank = count_below(hm) + (head ? 1u : 0u) - 1u;  // rank of sorted lane
+    if (head) a.ptmp[a0 + prank] = make_uint2((u32)(k >> a.bo), (u32)(k & omask));
+    // element el receives its part rank (each group holds a permutation)
+    const u32 my_part = (u32)__builtin_amdgcn_ds_permute((int)((gb + el) * 4u), (int)prank);
+    // segments: by inner symbol, element order within equal symbols
+    k = v ? (u64)a.inner[e] : ~0ull;
+    el = gl;
+    group_sort<G>(k, el);
+    const u64 sprev = __shfl(k, (int)(lane ? lane - 1 : 0), kWave);
+    head = v && (gl == 0 || k != sprev);
+    hm = __ballot(head) & gmask;
+    const u32 srank = count_below(hm) + (head ? 1u : 0u) - 1u;
+    const u32 part = __shfl(my_part, (int)(gb + el), kWave);
+    const u32 ee = __shfl(e, (int)(gb + el), kWave);
+    if (v) {
+      a.arcs[a0 + gl] = make_uint2(part, __float_as_uint(a.w[ee]));
+      if (head) {
+        a.ssym[a0 + srank] = (u32)k;
+        a.soff[a0 + srank] = a0 + gl;
+      }
+    }
+    if (gl == 0 && d) {
+      a.pcnt[q] = np;
+      a.scnt[q] = (u32)__popcll(hm);
+      note_max(a.maxp, np);
+    }
+  }
+}
+
+// First position of every state in the sorted state keys; states with arcs
+// are listed for the per-state kernels by size class (lists[c nq ..],
+// loc_class); states without arcs get zero counts.
+__global__ __launch_bounds__(256) void k_state_lists(const u64 *skey, u64 n, u32 nq, u32 *abase,
+                                                     u32 *pcnt, u32 *scnt, u32 *lists,
+                                                     u32 *list_len) {
+  __shared__ u32 s_n[kLocClasses], s_base[kLocClasses];
+  const u32 lane = lane_id();
+  const u64 q = (u64)blockIdx.x * blockDim.x + threadIdx.x;  // one pass: nq + 1 threads
+  if (threadIdx.x < (u32)kLocClasses) s_n[threadIdx.x] = 0;
+  u32 d = 0;
+  if (q <= nq) {
+    const u64 lo = lower_bound_dev<u64>(skey, n, q);
+    abase[q] = (u32)lo;
+    if (q < nq) {
+      d = (u32)(lower_bound_dev<u64>(skey, n, q + 1) - lo);
+      if (d == 0) pcnt[q] = scnt[q] = 0;
+    }
+  }
+  __syncthreads();
+  // appends aggregated per wave, then per block: one device atomic per class
+  u64 m[kLocClasses];
+  u32 woff[kLocClasses];
+#pragma unroll
+  for (int l = 0; l < kLocClasses; ++l) {
+    m[l] = __ballot(d > 0 && loc_class(d) == (u32)l);
+    woff[l] = 0;
+    if (m[l]) {
+      const u32 leader = __ffsll((unsigned long long)m[l]) - 1;
+      if (lane == leader) woff[l] = atomicAdd(&s_n[l], (u32)__popcll(m[l]));
+      woff[l] = __shfl(woff[l], leader, kWave);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < (u32)kLocClasses && s_n[threadIdx.x])
+    s_base[threadIdx.x] = atomicAdd(&list_len[threadIdx.x], s_n[threadIdx.x]);
+  __syncthreads();
+  if (d > 0) {
+    const u32 l = loc_class(d);
+    lists[(u64)l * nq + s_base[l] + woff[l] + count_below(m[l])] = (u32)q;
+  }
+}
+
+// Moves each state's parts and segments from its arc offset to their final
+// places; the totals go to counts[0] (segments) and counts[1] (parts).
+__global__ void k_state_place(const u64 *skey, const u32 *abase, u64 n, u32 nq, const u32 *pcnt,
+                              const u32 *scnt, const u32 *part_base, const u32 *row,
+                              const uint2 *ptmp, const u32 *ssym, const u32 *soff, uint2 *parts,
+                              u32 *seg_sym, u32 *seg_off, u64 *counts) {
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
+    const u32 q = (u32)skey[i];
+    const u32 j = (u32)i - abase[q];
+    if (j < pcnt[q]) parts[part_base[q] + j] = ptmp[i];
+    if (j < scnt[q]) {
+      seg_sym[row[q] + j] = ssym[i];
+      seg_off[row[q] + j] = soff[i];
+    }
+    if (i == 0) {
+      seg_off[row[nq]] = (u32)n;
+      counts[0] = row[nq];
+      counts[1] = part_base[nq];
+    }
+  }
+}
+
+__global__ void k_csr_keys(const u32 *src, const u32 *dst, const u32 *il, const u32 *ol, u64 n,
+                           u32 nq, u32 nis, u32 nos, u64 *skey, u32 *order, u32 *err) {
+  for (u64 e = (u64)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (u64)gridDim.x * blockDim.x) {
+    u32 s = src[e];
+    if (s >= nq || dst[e] >= nq || il[e] >= nis || ol[e] >= nos) {
+      set_error(err, kErrBadArc);
+      s = 0;
+    }
+    skey[e] = s;
+    order[e] = (u32)e;
+  }
+}
+
 }  // namespace
 
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s) {
@@ -148,17 +484,131 @@ void check_csr_ranges(const fstc_fst &m, bool by_output) {
     throw Error(FSTC_ERR_RANGE, "state and symbol ids do not fit the 64-bit CSR sort keys");
 }
 
-void alloc_csr(const fstc_fst &m, Allocator &A, Buf *b, Csr &c) {
+void alloc_csr(const fstc_fst &m, Buf &b, Csr &c) {
   const u64 n = m.num_arcs, nq = m.num_states;
-  for (int i = 0; i < 7; ++i) b[i].A = &A;
+  const u64 n1 = std::max<u64>(n, 1);
+  const size_t sz[7] = {(nq + 1) * 4, n1 * 4, (n + 1) * 4, n1 * 8, (nq + 1) * 4, n1 * 8,
+                        std::max<u64>(nq, 1) * 4};
+  size_t off[7], total = 0;
+  for (int i = 0; i < 7; ++i) {
+    off[i] = total;
+    total += (sz[i] + 255) & ~(size_t)255;
+  }
+  char *p = static_cast<char *>(b.ensure(total));
   c.num_states = m.num_states;
   c.num_arcs = n;
-  c.row = (u32 *)b[0].ensure((nq + 1) * sizeof(u32));
-  c.seg_sym = (u32 *)b[1].ensure(std::max<u64>(n, 1) * sizeof(u32));
-  c.seg_off = (u32 *)b[2].ensure((n + 1) * sizeof(u32));
-  c.arcs = (uint2 *)b[3].ensure(std::max<u64>(n, 1) * sizeof(uint2));
-  c.part_base = (u32 *)b[4].ensure((nq + 1) * sizeof(u32));
-  c.parts = (uint2 *)b[5].ensure(std::max<u64>(n, 1) * sizeof(uint2));
+  c.row = (u32 *)(p + off[0]);
+  c.seg_sym = (u32 *)(p + off[1]);
+  c.seg_off = (u32 *)(p + off[2]);
+  c.arcs = (uint2 *)(p + off[3]);
+  c.part_base = (u32 *)(p + off[4]);
+  c.parts = (uint2 *)(p + off[5]);
+  c.cell_flag = (u32 *)(p + off[6]);
+}
+
+namespace {
+
+// The per-state build (see k_state_local) for transducers of at most
+// kLocMaxStates states whose arcs per state stay moderate on average; one
+// state with a very large share of the arcs goes through the global sorts.
+constexpr u32 kLocMaxStates = 1u << 17;
+constexpr u64 kLocMaxAvg = 1024;
+constexpr u64 kLocAnyArcs = 1u << 16;
+
+bool use_local_build(u64 n, u32 nq) {
+  return nq <= kLocMaxStates && (n <= kLocMaxAvg * nq || n <= kLocAnyArcs);
+}
+
+size_t arena_bytes(std::initializer_list<size_t> sizes) {
+  size_t t = 0;
+  for (size_t b : sizes) t += std::max<size_t>(256, (b + 255) & ~(size_t)255);
+  return t;
+}
+
+void build_csr_local(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d_counts,
+                     u32 *d_err, hipStream_t s, int bq, int bi, int bo) {
+  const u64 n = m.num_arcs;
+  const u32 nq = m.num_states;
+  Tmp skey(&T), order(&T), kalt(&T), valt(&T), kb(&T), ib(&T), part_of(&T), ptmp(&T), ssym(&T),
+      soff(&T), pcnt(&T), scnt(&T), abase(&T), lists(&T), ctl(&T), rtmp(&T);
+  skey.ensure(n * 8); order.ensure(n * 4); kalt.ensure(n * 8); valt.ensure(n * 4);
+  kb.ensure(n * 8); ib.ensure(n * 4); part_of.ensure(n * 4); ptmp.ensure(n * 8);
+  ssym.ensure(n * 4); soff.ensure(n * 4);
+  pcnt.ensure((u64)nq * 4); scnt.ensure((u64)nq * 4); abase.ensure(((u64)nq + 1) * 4);
+  lists.ensure(kLocClasses * (u64)nq * 4);
+  rtmp.ensure(radix_temp_bytes(n));
+  // control words (list lengths, scan counter) and the single-pass scan
+  // state, zero-filled together
+  constexpr size_t kCtl = 256;
+  const size_t lbb = scan_lb_state_bytes(nq);
+  ctl.ensure(kCtl + lbb);
+  fill_u32(ctl.as<u32>(), 0, (kCtl + lbb) / 4, s);
+  u32 *list_len = ctl.as<u32>(), *scan_ctr = list_len + kLocClasses;
+  void *lbstate = static_cast<char *>(ctl.p) + kCtl;
+
+  const unsigned g = grid_for(n);
+  hipLaunchKernelGGL(k_csr_keys, dim3(g), dim3(kNT), 0, s, m.src, m.dst, m.ilabel, m.olabel, n,
+                     nq, m.num_isyms, m.num_osyms, skey.as<u64>(), order.as<u32>(), d_err);
+  // stable: arcs of a state keep their input order
+  radix_sort_pairs(skey.as<u64>(), order.as<u32>(), kalt.as<u64>(), valt.as<u32>(), n, 0, bq,
+                   rtmp.p, s);
+  hipLaunchKernelGGL(k_state_lists, dim3((unsigned)ceil_div((u64)nq + 1, kNT)), dim3(kNT), 0, s,
+                     skey.as<u64>(), n, nq, abase.as<u32>(), pcnt.as<u32>(), scnt.as<u32>(),
+                     lists.as<u32>(), list_len);
+  LocalArgs a{};
+  a.skey = skey.as<u64>();
+  a.order = order.as<u32>();
+  a.abase = abase.as<u32>();
+  a.dst = m.dst;
+  a.inner = by_output ? m.olabel : m.ilabel;
+  a.outer = by_output ? m.ilabel : m.olabel;
+  a.w = m.weight;
+  a.bo = bo;
+  a.bp = bq + bo;
+  a.bi = bi;
+  a.ka = kalt.as<u64>();
+  a.kb = kb.as<u64>();
+  a.ia = valt.as<u32>();
+  a.ib = ib.as<u32>();
+  a.part_of = part_of.as<u32>();
+  a.ptmp = ptmp.as<uint2>();
+  a.ssym = ssym.as<u32>();
+  a.soff = soff.as<u32>();
+  a.arcs = c.arcs;
+  a.pcnt = pcnt.as<u32>();
+  a.scnt = scnt.as<u32>();
+  a.maxp = d_counts + 2;
+  // grids: at most one lane group (workgroup) per state of the list
+  const u32 *L = lists.as<u32>();
+  hipLaunchKernelGGL(k_state_group<16>, dim3((unsigned)std::min<u64>(ceil_div(nq, 16), 4096)),
+                     dim3(256), 0, s, a, L, list_len);
+  hipLaunchKernelGGL(k_state_group<64>, dim3((unsigned)std::min<u64>(ceil_div(nq, 4), 4096)),
+                     dim3(256), 0, s, a, L + nq, list_len + 1);
+  hipLaunchKernelGGL((k_state_local<256, 1>), dim3((unsigned)std::min<u64>(nq, 4096)), dim3(256),
+                     0, s, a, L + 2 * (u64)nq, list_len + 2);
+  hipLaunchKernelGGL((k_state_local<256, 4>), dim3((unsigned)std::min<u64>(nq, 2048)), dim3(256),
+                     0, s, a, L + 3 * (u64)nq, list_len + 3);
+  hipLaunchKernelGGL((k_state_local<1024, 8>), dim3((unsigned)std::min<u64>(nq, 512)), dim3(1024),
+                     0, s, a, L + 4 * (u64)nq, list_len + 4);
+  const ScanJob jobs[2] = {{pcnt.p, false, (u64 *)c.part_base, true},
+                           {scnt.p, false, (u64 *)c.row, true}};
+  exclusive_scan_lb(jobs, 2, nq, lbstate, scan_ctr, d_err, s);
+  hipLaunchKernelGGL(k_state_place, dim3(g), dim3(kNT), 0, s, skey.as<u64>(), abase.as<u32>(), n,
+                     nq, pcnt.as<u32>(), scnt.as<u32>(), c.part_base, c.row, ptmp.as<uint2>(),
+                     ssym.as<u32>(), soff.as<u32>(), c.parts, c.seg_sym, c.seg_off, d_counts);
+}
+
+}  // namespace
+
+size_t csr_temp_bytes(const fstc_fst &m) {
+  const u64 n = m.num_arcs, nq = m.num_states;
+  if (n == 0) return 0;
+  if (use_local_build(n, m.num_states))
+    return arena_bytes({n * 8, n * 4, n * 8, n * 4, n * 8, n * 4, n * 4, n * 8, n * 4, n * 4,
+                        nq * 4, nq * 4, (nq + 1) * 4, kLocClasses * nq * 4, radix_temp_bytes(n),
+                        256 + scan_lb_state_bytes(nq)});
+  return arena_bytes({n * 8, n * 8, n * 4, n * 4, n * 8, n * 4, n * 4, (n + 1) * 4, n * 4, n * 4,
+                      n * 4, std::max(radix_temp_bytes(n), scan_temp_bytes(n))});
 }
 
 void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d_counts,
@@ -178,6 +628,10 @@ void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d
   const u32 nouter = by_output ? m.num_isyms : m.num_osyms;
   const int bi = (int)bits_for(ninner ? ninner - 1 : 0);
   const int bo = (int)bits_for(nouter ? nouter - 1 : 0);
+  if (use_local_build(n, nq)) {
+    build_csr_local(m, by_output, T, c, d_counts, d_err, s, bq, bi, bo);
+    return;
+  }
 
   Tmp kp(&T), kc(&T), v1(&T), v2(&T), kalt(&T), valt(&T), flags(&T), ex(&T), apg(&T),
       pstate(&T), sstate(&T), tmp(&T);

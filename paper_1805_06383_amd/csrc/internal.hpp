@@ -78,6 +78,9 @@ struct Arena {
   Arena &operator=(const Arena &) = delete;
   ~Arena() { release(); }
   void *take(size_t bytes);
+  // Makes the next round's takes of up to `bytes` in all come from one
+  // allocation (call right after construction or reset()).
+  void reserve(size_t bytes);
   void reset();
   void release();
 };
@@ -132,7 +135,10 @@ void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s);
 // Error(FSTC_ERR_RANGE) when a key does not fit 64 bits.
 void check_csr_ranges(const fstc_fst &m, bool by_output);
 
-// Allocates the arrays of a Csr in `bufs` (7 buffers) and fills `out`.
-void alloc_csr(const fstc_fst &m, Allocator &A, Buf *bufs, Csr &out);
+// Allocates the arrays of a Csr (cell flags included) as parts of one
+// buffer and fills `out`.
+void alloc_csr(const fstc_fst &m, Buf &buf, Csr &out);
+// Arena bytes build_csr takes for m (either direction).
+size_t csr_temp_bytes(const fstc_fst &m);
 
 }  // namespace fstc

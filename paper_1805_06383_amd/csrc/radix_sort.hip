@@ -63,6 +63,27 @@ __global__ __launch_bounds__(kNT) void k_digit_scatter(const u64 *keys, const u3
   }
 }
 
+// Exclusive scan of a digit histogram of at most kScan1Max entries by one
+// workgroup (one launch instead of a multi-level scan): thread t scans
+// entries [t c, t c + c) with c = ceil(nh / kScan1NT).
+constexpr int kScan1NT = 1024;
+constexpr u64 kScan1Max = 1u << 16;
+
+__global__ __launch_bounds__(kScan1NT) void k_hist_scan1(const u32 *hist, u32 *offs, u32 nh) {
+  __shared__ u32 scratch[kScan1NT / kWave];
+  const u32 c = (nh + kScan1NT - 1) / kScan1NT;
+  const u32 b = threadIdx.x * c, e = min(nh, b + c);
+  u32 sum = 0;
+  for (u32 i = b; i < e; ++i) sum += hist[i];
+  u32 total;
+  u32 run = block_exclusive_sum<kScan1NT, u32>(sum, scratch, &total);
+  for (u32 i = b; i < e; ++i) {
+    const u32 v = hist[i];
+    offs[i] = run;
+    run += v;
+  }
+}
+
 }  // namespace
 
 size_t radix_temp_bytes(u64 n) {
@@ -85,7 +106,10 @@ void radix_sort_pairs(u64 *keys, u32 *vals, u64 *keys_alt, u32 *vals_alt, u64 n,
     const int bits = std::min(8, hi - shift);
     const u32 mask = (1u << bits) - 1u;
     hipLaunchKernelGGL(k_digit_hist, dim3(nb), dim3(kNT), 0, s, ki, n, shift, mask, hist, nb);
-    exclusive_scan(hist, offs, nh, scan_tmp, s);
+    if (nh <= kScan1Max)
+      hipLaunchKernelGGL(k_hist_scan1, dim3(1), dim3(kScan1NT), 0, s, hist, offs, (u32)nh);
+    else
+      exclusive_scan(hist, offs, nh, scan_tmp, s);
     hipLaunchKernelGGL(k_digit_scatter, dim3(nb), dim3(kNT), 0, s, ki, vi, ko, vo, n, shift,
                        bits, offs, nb);
     std::swap(ki, ko);

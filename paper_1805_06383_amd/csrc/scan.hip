@@ -193,7 +193,8 @@ constexpr int kLbMax = 3;
 struct LbArgs {
   const void *in[kLbMax];
   u64 *out[kLbMax];
-  u32 wide;  // bit k: in[k] holds u64
+  u32 wide;    // bit k: in[k] holds u64
+  u32 narrow;  // bit k: out[k] holds u32
   u64 n;
   u32 nb, epoch;
   u32 *flags;   // [nb]
@@ -201,6 +202,11 @@ struct LbArgs {
   u64 *incl;    // [nb * kLbMax]
   u32 *ctr, *err;
 };
+
+__device__ __forceinline__ void put_out(const LbArgs &p, int k, u64 i, u64 v) {
+  if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[i] = (u32)v;
+  else p.out[k][i] = v;
+}
 
 template <int K>
 __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
@@ -294,7 +300,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         s_off[k] = off[k];
-        if (t == p.nb - 1) p.out[k][p.n] = off[k] + tot[k];
+        if (t == p.nb - 1) put_out(p, k, p.n, off[k] + tot[k]);
       }
     }
   }
@@ -305,7 +311,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
 #pragma unroll
     for (int j = 0; j < kLbIT; ++j) {
       const u64 i = base + j;
-      if (i < p.n) p.out[k][i] = o + loc[k][j];
+      if (i < p.n) put_out(p, k, i, o + loc[k][j]);
     }
   }
 }
@@ -384,10 +390,12 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   if (nb >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "scan too large for one launch");
   LbArgs p{};
   p.wide = 0;
+  p.narrow = 0;
   for (int i = 0; i < k; ++i) {
     p.in[i] = jobs[i].in;
     p.out[i] = jobs[i].out;
     p.wide |= (jobs[i].wide ? 1u : 0u) << i;
+    p.narrow |= (jobs[i].narrow_out ? 1u : 0u) << i;
   }
   p.n = n;
   p.nb = (u32)nb;
