@@ -212,7 +212,9 @@ struct ScanJob {
   const void *in;
   bool wide;
   u64 *out;
-  bool narrow_out = false;  // out holds u32 (sums must fit)
+  bool narrow_out = false;    // out holds u32 (sums must fit)
+  const u64 *sub = nullptr;   // scans in[i] - sub[i] (in wide)
+  bool total_only = false;    // writes out[n] alone
 };
 size_t scan_lb_state_bytes(u64 n);
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,

@@ -409,7 +409,7 @@ void Composer::run(fstc_result *out) {
   };
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
-  Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), mcount(&level_tmp),
+  Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),
       aoff(&level_tmp), pk(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
@@ -428,7 +428,7 @@ void Composer::run(fstc_result *out) {
     max_frontier = std::max<u64>(max_frontier, nsrc);
     const u64 np1 = (u64)nsrc + 1;
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
-    mcount.ensure(np1 * 4); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
+    ptot.ensure(np1 * 8); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
     pk.ensure(np1 * 4); poff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     wrange.ensure(np1 * sizeof(uint4));
@@ -605,10 +605,14 @@ void Composer::run(fstc_result *out) {
         T.at(kMerge);
         ++product_launches;
       }
-      launch_mcount(ma, mcount.as<u32>(), s);
+      // merged arcs per source (mend - tstart) scanned into result offsets;
+      // the per-source joined pairs (records, or the product merge's terms)
+      // summed for the level's product-merge pairs
       {
-        const ScanJob job{mcount.p, false, aoff.as<u64>()};
-        exclusive_scan_lb(&job, 1, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+        ScanJob jobs[2] = {{mend.p, true, aoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()}};
+        jobs[0].sub = tstart.as<u64>();
+        jobs[1].total_only = true;
+        exclusive_scan_lb(jobs, 2, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
       }
       launch_emit_tiles(ma, s);
       const u64 nw = newlist_waves(ma, RB);
@@ -617,7 +621,8 @@ void Composer::run(fstc_result *out) {
       const u64 *new_total = launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB,
                                             wcnt.as<u32>(), woff.as<u64>(), lb(nw), s);
       const u32 seq2 = next_publication();
-      launch_merged_total(aoff.as<u64>() + nsrc, new_total, ma, hs_dev, seq2, s);
+      launch_merged_total(aoff.as<u64>() + nsrc, new_total, ptot.as<u64>() + nsrc, ma, hs_dev,
+                          seq2, s);
       T.at(kNone);
       wait_published(seq2);
       status_clear = true;  // k_merged_total cleared the level counters

@@ -226,9 +226,6 @@ void launch_compact(const MergeArgs &a, const u64 *aoff, u32 nbig, u64 M, const 
 // the form used when product-merge sources sit between tile-merged ones.
 void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,
                             u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s);
-// mcount[u] = mend[u] - tstart[u]; also adds the joined pairs of the
-// product-merge sources (a.pcnt where a.pk != 0) to st->prod_records.
-void launch_mcount(const MergeArgs &a, u32 *mcount, hipStream_t s);
 // Visited-table inserts and label lookups for every merged arc of the
 // tile-merged sources (merge_big does its own).
 void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
@@ -263,11 +260,13 @@ void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, con
 // copy by watching that word.
 void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host, u32 seq,
                          hipStream_t s);
-// Level total of merged arcs, new pairs (*new_total, when not NULL) and the
-// dense / sort tile statistics of st; after publishing it clears the level
-// counters of *st for the next level (what launch_reset_level does).
-void launch_merged_total(const u64 *a_total, const u64 *new_total, const MergeArgs &a, Status *host,
-                         u32 seq, hipStream_t s);
+// Level total of merged arcs, new pairs (*new_total, when not NULL), the
+// product merge's joined pairs (*pair_total: the sum of a.pcnt over the
+// level's sources, records included, less st->R) and the dense / sort tile
+// statistics of st; after publishing it clears the level counters of *st
+// for the next level (what launch_reset_level does).
+void launch_merged_total(const u64 *a_total, const u64 *new_total, const u64 *pair_total,
+                         const MergeArgs &a, Status *host, u32 seq, hipStream_t s);
 void launch_reset_level(Status *st, hipStream_t s);
 
 }  // namespace fstc

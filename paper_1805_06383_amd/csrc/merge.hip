@@ -933,17 +933,26 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
 
   const u32 *ssym = one_short ? a.seg_sym1 : a.seg_sym2;
   const u32 *lsym = one_short ? a.seg_sym2 : a.seg_sym1;
+  const u32 *soffs = one_short ? a.seg_off1 : a.seg_off2;
+  const u32 *loffs = one_short ? a.seg_off2 : a.seg_off1;
   const u32 le = one_short ? e2 : e1;
 
-  // 1. join, staging, part masks
+  // 1. join, staging, part masks.  Segment offsets are loaded with the
+  //    symbols (this lane's short-list segment; the long-list chunk's, handed
+  //    over by the lane that found the match), so the arc loads follow the
+  //    join without another round trip.
   const u32 idx = bs + lane;
   const bool valid = idx < es;
   const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
+  const u32 sa = valid ? soffs[idx] : 0u, sn = valid ? soffs[idx + 1] - sa : 0u;
   const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
-  u32 fpos = 0xffffffffu;
+  bool found = false;
+  u32 la = 0, ln = 0;
   for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
     const u32 len = min(le - cb, (u32)kWave);
-    const u32 lv = lane < len ? lsym[cb + lane] : 0xffffffffu;
+    const bool in = lane < len;
+    const u32 lv = in ? lsym[cb + lane] : 0xffffffffu;
+    const u32 lo0 = in ? loffs[cb + lane] : 0u, lo1 = in ? loffs[cb + lane + 1] : 0u;
     if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
     u32 pos = 0;  // elements of the chunk below sym
 #pragma unroll
@@ -952,15 +961,19 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
       pos = v < sym ? pos + step : pos;
     }
     const u32 at = __shfl(lv, (int)pos, kWave);
-    if (valid && at == sym) fpos = cb + pos;
+    const u32 pa = __shfl(lo0, (int)pos, kWave), pe = __shfl(lo1, (int)pos, kWave);
+    if (valid && at == sym) {
+      found = true;
+      la = pa;
+      ln = pe - pa;
+    }
     if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
   }
   u32 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol (parts < 16)
   bool bad = false;
-  if (fpos != 0xffffffffu) {
-    const u32 s1 = one_short ? idx : fpos, s2 = one_short ? fpos : idx;
-    const u32 a1 = a.seg_off1[s1], n1 = a.seg_off1[s1 + 1] - a1;
-    const u32 a2 = a.seg_off2[s2], n2 = a.seg_off2[s2 + 1] - a2;
+  if (found) {
+    const u32 a1 = one_short ? sa : la, n1 = one_short ? sn : ln;
+    const u32 a2 = one_short ? la : sa, n2 = one_short ? ln : sn;
     for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
       uint2 x1[kProdBatch], x2[kProdBatch];
 #pragma unroll
@@ -1414,25 +1427,6 @@ __global__ __launch_bounds__(256) void k_newlist(MergeArgs a, const u64 *bigoff,
 // Level total of new states (end of the exclusive scan of the per-wave counts).
 __global__ void k_new_total(const u64 *total, Status *st) { st->nnew = (u32)min<u64>(*total, 0xffffffffull); }
 
-// Merged arcs per source from where its runs start and end in temp; the
-// joined pairs of the product-merge sources summed into st->prod_records
-// (one device atomic per workgroup).
-__global__ __launch_bounds__(256) void k_mcount(MergeArgs a, u32 *mcount) {
-  __shared__ unsigned long long s_sum;
-  if (threadIdx.x == 0) s_sum = 0;
-  const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  u64 v = 0;
-  if (u < a.nsrc) {
-    mcount[u] = (u32)(a.mend[u] - a.tstart[u]);
-    if (a.prodpos && a.pk[u]) v = a.pcnt[u];
-  }
-  v = wave_sum(v);
-  __syncthreads();
-  if (lane_id() == 0 && v) atomicAdd(&s_sum, (unsigned long long)v);
-  __syncthreads();
-  if (threadIdx.x == 0 && s_sum) atomicAdd((unsigned long long *)&a.st->prod_records, s_sum);
-}
-
 // ---------------------------------------------------------------------------
 // Composition without reduction (every joined arc pair is an arc).  Wave per
 // kUnredB * 64 consecutive records, lane-striped: a record's source by a
@@ -1665,13 +1659,15 @@ __global__ void k_level_totals(const u64 *rt, const u64 *mt, Status *st, Status 
 }
 
 // Level totals after the merge: merged arcs (end of the scan of merged arcs
-// per source), new pairs (end of the scan of the new-pair lists), and, over
-// the merge tiles, the records and runs of the tiles the dense-table kernel
-// merged and the runs of those the sort kernel merged.  One workgroup: it
-// publishes the counters to host memory and then clears them for the next
-// level.
-__global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 *nt, Status *st,
-                                                       MergeArgs a, Status *host, u32 seq) {
+// per source), new pairs (end of the scan of the new-pair lists), the
+// product merge's joined pairs (sum of the per-source joined pairs less the
+// level's records), and, over the merge tiles, the records and runs of the
+// tiles the dense-table kernel merged and the runs of those the sort kernel
+// merged.  One workgroup: it publishes the counters to host memory and then
+// clears them for the next level.
+__global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 *nt, const u64 *pt,
+                                                       Status *st, MergeArgs a, Status *host,
+                                                       u32 seq) {
   __shared__ u64 s_v[3][1024 / kWave];
   u64 v[3] = {0, 0, 0};
   for (u64 t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
@@ -1699,6 +1695,7 @@ __global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 
   }
   if (threadIdx.x == 3) st->merged = *at;
   if (threadIdx.x == 4 && nt) st->nnew = (u32)min<u64>(*nt, 0xffffffffull);
+  if (threadIdx.x == 5) st->prod_records = *pt - st->R;
   __syncthreads();
   __threadfence();
   publish(st, host, seq, threadIdx.x, blockDim.x);
@@ -1894,10 +1891,6 @@ void launch_emit_tiles(const MergeArgs &a, hipStream_t s) {
                      0, s, a, wpt);
 }
 
-void launch_mcount(const MergeArgs &a, u32 *mcount, hipStream_t s) {
-  hipLaunchKernelGGL(k_mcount, dim3((unsigned)ceil_div(a.nsrc, 256)), dim3(256), 0, s, a, mcount);
-}
-
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s) {
   if (!n) return;
@@ -1909,10 +1902,10 @@ void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Sta
   hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, st, host, seq);
 }
 
-void launch_merged_total(const u64 *a_total, const u64 *new_total, const MergeArgs &a, Status *host,
-                         u32 seq, hipStream_t s) {
-  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1024), 0, s, a_total, new_total, a.st, a, host,
-                     seq);
+void launch_merged_total(const u64 *a_total, const u64 *new_total, const u64 *pair_total,
+                         const MergeArgs &a, Status *host, u32 seq, hipStream_t s) {
+  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1024), 0, s, a_total, new_total, pair_total,
+                     a.st, a, host, seq);
 }
 
 void launch_reset_level(Status *st, hipStream_t s) {

@@ -195,6 +195,8 @@ struct LbArgs {
   u64 *out[kLbMax];
   u32 wide;    // bit k: in[k] holds u64
   u32 narrow;  // bit k: out[k] holds u32
+  u32 tonly;   // bit k: only out[k][n] is written
+  const u64 *sub[kLbMax];
   u64 n;
   u32 nb, epoch;
   u32 *flags;   // [nb]
@@ -231,9 +233,11 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
     for (int j = 0; j < kLbIT; ++j) {
       const u64 i = base + j;
       u64 x = 0;
-      if (i < p.n)
+      if (i < p.n) {
         x = ((p.wide >> k) & 1u) ? static_cast<const u64 *>(p.in[k])[i]
                                  : (u64) static_cast<const u32 *>(p.in[k])[i];
+        if (p.sub[k]) x -= p.sub[k][i];
+      }
       loc[k][j] = run;
       run += x;
     }
@@ -307,6 +311,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < K; ++k) {
+    if ((p.tonly >> k) & 1u) continue;
     const u64 o = s_off[k] + ex[k];
 #pragma unroll
     for (int j = 0; j < kLbIT; ++j) {
@@ -391,11 +396,14 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   LbArgs p{};
   p.wide = 0;
   p.narrow = 0;
+  p.tonly = 0;
   for (int i = 0; i < k; ++i) {
     p.in[i] = jobs[i].in;
     p.out[i] = jobs[i].out;
     p.wide |= (jobs[i].wide ? 1u : 0u) << i;
     p.narrow |= (jobs[i].narrow_out ? 1u : 0u) << i;
+    p.tonly |= (jobs[i].total_only ? 1u : 0u) << i;
+    p.sub[i] = jobs[i].sub;
   }
   p.n = n;
   p.nb = (u32)nb;
