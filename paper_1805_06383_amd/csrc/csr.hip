@@ -99,13 +99,17 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 
 // Wave per state; lane l checks segments row[q] + l, + 64, ...: a segment
 // of more arcs than kProdParts, or whose arcs' parts are not all distinct
-// (a 64-bit mask of the parts), flags the state.
+// (a 64-bit mask of the parts), flags the state (bit 0).  For the other
+// states the word also summarises the arcs' weights (kCellSpecial: a
+// non-finite or subnormal weight; the largest biased float32 exponent of a
+// nonzero weight at kCellEmaxShift, the smallest at kCellEminShift).
 __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *arcs,
                              const u32 *part_base, u32 nq, u32 *flag) {
   const u32 lane = lane_id();
   const u64 nw = (u64)gridDim.x * blockDim.x / kWave;
   for (u64 q = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
-    bool bad = part_base[q + 1] - part_base[q] > kProdParts;
+    bool bad = part_base[q + 1] - part_base[q] > kProdParts, special = false;
+    u32 emax = 0, emin = 255;
     if (!bad) {
       for (u32 sg = row[q] + lane; sg < row[q + 1]; sg += kWave) {
         const u32 a0 = seg_off[sg], n = seg_off[sg + 1] - a0;
@@ -114,12 +118,25 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
           continue;
         }
         u64 m = 0;
-        for (u32 i = 0; i < n; ++i) m |= 1ull << (arcs[a0 + i].x & 63u);
+        for (u32 i = 0; i < n; ++i) {
+          const uint2 x = arcs[a0 + i];
+          m |= 1ull << (x.x & 63u);
+          const u32 mag = x.y & 0x7fffffffu, e = mag >> 23;
+          special |= e == 255u || (e == 0u && mag != 0u);
+          if (mag) {
+            emax = max(emax, e);
+            emin = min(emin, e);
+          }
+        }
         bad |= (u32)__popcll(m) != n;
       }
     }
-    const bool any = __ballot(bad) != 0;
-    if (lane == 0) flag[q] = any ? 1u : 0u;
+    const bool any = __ballot(bad) != 0, spec = __ballot(special) != 0;
+    emax = wave_max(emax);
+    emin = 255u - wave_max(255u - emin);
+    if (lane == 0)
+      flag[q] = any ? kCellBad
+                    : (spec ? kCellSpecial : 0u) | (emax << kCellEmaxShift) | (emin << kCellEminShift);
   }
 }
 

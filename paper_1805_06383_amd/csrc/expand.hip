@@ -80,17 +80,33 @@ __device__ __forceinline__ u32 seg_len(const u32 *seg_off, u32 s) { return seg_o
 // merge window (st->max_small).  Both are gathered by the count kernels.
 constexpr int kCountNT = 256;
 
+// True when every product of a weight of the state summarised by f1 with
+// one of the state summarised by f2 (build_cell_flags) is a normal float32
+// number after rounding: no infinity or NaN, no subnormal operand,
+// |w1 w2| < 2^127 (biased exponents sum to at most 379) and
+// |w1 w2| >= 2^-126 for nonzero operands (they sum to at least 128).  Such
+// a product rounded to float32 is within 2^-24 of itself, relatively.
+__device__ __forceinline__ bool products_normal(u32 f1, u32 f2) {
+  if ((f1 | f2) & kCellSpecial) return false;
+  const u32 emax = ((f1 >> kCellEmaxShift) & 0xffu) + ((f2 >> kCellEmaxShift) & 0xffu);
+  const u32 emin = ((f1 >> kCellEminShift) & 0xffu) + ((f2 >> kCellEminShift) & 0xffu);
+  return emax <= 379u && emin >= 128u;
+}
+
 // Product-merge selection of source u (level.hpp) from what the count
 // already loaded: table entries P1 P2 and the source header written to
-// phdr, or 0 (record path).  The cell flags are clear only for states of at
-// most kProdParts parts.
+// phdr, or 0 (record path).  The header's last word selects the matrix-core
+// form (at most kProdMfmaParts parts per state, products_normal).  The
+// cells are single-arc only for states of at most kProdParts parts.
 __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1, u32 q2,
                                               const Ranges &r) {
-  if (a.c1.cell_flag[q1] | a.c2.cell_flag[q2]) return 0;
+  const u32 f1 = a.c1.cell_flag[q1], f2 = a.c2.cell_flag[q2];
+  if ((f1 | f2) & kCellBad) return 0;
   const u32 pb1 = a.c1.part_base[q1], p1 = a.c1.part_base[q1 + 1] - pb1;
   const u32 pb2 = a.c2.part_base[q2], p2 = a.c2.part_base[q2 + 1] - pb2;
   if (p1 == 0 || p2 == 0 || p1 + p2 > kProdRowSum) return 0;
-  a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16), 0u);
+  const bool mfma = p1 <= kProdMfmaParts && p2 <= kProdMfmaParts && products_normal(f1, f2);
+  a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16), mfma ? 1u : 0u);
   a.phdr[2 * u + 1] = make_uint4(r.b1, r.e1, r.b2, r.e2);
   return p1 * p2;
 }

@@ -126,9 +126,14 @@ void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &out, u64 
 // Largest part count of a state the product merge takes (level.hpp).
 constexpr u32 kProdParts = 64;
 
-// cell_flag[q] = 1 when state q has more than kProdParts parts or two arcs
-// with the same part and inner symbol (parallel arcs with equal labels and
-// target), else 0.
+// cell_flag[q] has bit kCellBad when state q has more than kProdParts parts
+// or two arcs with the same part and inner symbol (parallel arcs with equal
+// labels and target).  Otherwise it summarises the state's arc weights: bit
+// kCellSpecial when one is infinite, NaN or subnormal, and the largest and
+// smallest biased float32 exponents of its nonzero weights (0 and 255 in
+// those fields when it has none).
+constexpr u32 kCellBad = 1u, kCellSpecial = 2u;
+constexpr int kCellEmaxShift = 8, kCellEminShift = 16;
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s);
 
 // Checks the packing limits of build_csr for one transducer; throws

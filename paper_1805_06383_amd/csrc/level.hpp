@@ -52,6 +52,10 @@ struct Status {
 // kernel counts its joined pairs.
 constexpr u32 kProdRowSum = 16;
 constexpr u32 kProdMinSymbols = 8;
+// Sources whose states have at most kProdMfmaParts parts each and whose
+// weight products are normal float32 numbers (expand.hip, products_normal)
+// are summed on the matrix cores (merge.hip).
+constexpr u32 kProdMfmaParts = 4;
 
 // A source whose shorter segment list is longer than kWideMin is joined by a
 // wavefront, longer than kHeavyMin by a workgroup; others by one thread,

@@ -881,11 +881,34 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
 //   3. every entry with a term becomes a merged arc (visited-table insert,
 //      labels from the parts, see emit_parts) at temp slot R + poff[u] + r in
 //      entry order; the entry's other slots are marked empty.
+// Matrix-core form (the header's last word; P1, P2 <= kProdMfmaParts and
+// every product a normal float32 number, expand.hip): the cells are rows of
+// four (zero where a state has no arc) and step 2 is the 4 x 64 by 64 x 4
+// product of the two matrices, four v_mfma_f64_4x4x4f64.  Lane l supplies
+// row 16 t + l / 4, column l mod 4 of each matrix to product t; blocks
+// b = (l / 4) mod 4 of the result hold the sums over g = b mod 4, row
+// rotations within 16 lanes add them, and entry (p1, p2) ends in lane
+// 16 p1 + p2.  Its products are exact in float64, so the merged weight
+// differs from the float32-product sum by at most 2^-24 of the sum of the
+// terms' magnitudes (the selection's normal-range bound) before the
+// final rounding.
 // No LDS is shared between waves, so no workgroup barrier is needed.
 constexpr int kProdNT = 256;
 constexpr int kProdWaves = kProdNT / kWave;
 constexpr u32 kProdCells = kProdRowSum * kWave;  // both matrices, 64 symbols
+constexpr u32 kProdRow = kProdMfmaParts;         // cells per symbol, matrix-core form
 constexpr int kProdBatch = 4;                     // arcs per side loaded at once
+static_assert(2 * kProdRow * kWave <= kProdCells, "matrix-core cells fit the wave's LDS");
+
+// x from the lane 4 or 8 places before it (cyclically) in its row of 16.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const u64 b = (u64)__double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(u32)b, CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(u32)(b >> 32), CTRL, 0xf, 0xf, false);
+  return __longlong_as_double((long long)(((u64)(u32)hi << 32) | (u64)(u32)lo));
+}
+constexpr int kDppRowRor4 = 0x124, kDppRowRor8 = 0x128;
 
 template <bool NARROW>
 __device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
@@ -895,7 +918,8 @@ __device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
 
 template <bool NARROW>
 __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
-  __shared__ u32 s_val[kProdWaves][kProdCells + 1];  // M1 (g, p1), M2 (g, p2); a spare cell
+  // M1 (g, p1), M2 (g, p2); a spare cell; rows 16-byte aligned
+  __shared__ __align__(16) u32 s_val[kProdWaves][kProdCells + 4];
   // everything about the source is wave-uniform: scalar registers
   auto uni = [](u32 x) { return (u32)__builtin_amdgcn_readfirstlane((int)x); };
   const u32 lane = lane_id(), w = uni(threadIdx.x / kWave);
@@ -907,20 +931,36 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   u32 *val = s_val[w];
   const u32 pb1 = uni(h0.x), pb2 = uni(h0.y), P1 = uni(h0.z & 0xffffu), P2 = uni(h0.z >> 16);
   const u32 b1 = uni(h1.x), e1 = uni(h1.y), b2 = uni(h1.z), e2 = uni(h1.w);
+  const bool mf = uni(h0.w) != 0;  // matrix-core form
   const bool one_short = (e1 - b1) <= (e2 - b2);
   const u32 bs = one_short ? b1 : b2, es = one_short ? e1 : e2;
-  if (P1 * P2 != K || P1 + P2 > kProdRowSum || es <= bs || es - bs > (u32)kWave) {
+  if (P1 * P2 != K || P1 + P2 > kProdRowSum || es <= bs || es - bs > (u32)kWave ||
+      (mf && (P1 > kProdRow || P2 > kProdRow))) {
     // impossible: the selection checked all of it
     if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
   }
-  // this lane's table entry (q lanes per entry), its labels and the first
-  // visited-table probe of its target pair, all issued before the join
-  u32 q = kWave;
-  while (q > 1 && (kWave / q) < K) q >>= 1;  // q = 64 / pow2ceil(K)
-  const u32 e = lane / q, c = lane % q;
-  const bool act = e < K;
-  const u32 p1 = act ? e / P2 : 0, p2 = act ? e - (e / P2) * P2 : 0;
+  // this lane's table entry (q lanes per entry; lane 16 p1 + p2 alone in the
+  // matrix-core form), its labels and the first visited-table probe of its
+  // target pair, all issued before the join
+  u32 q = kWave, c = 0, p1 = 0, p2 = 0;
+  bool act;
+  if (mf) {
+    act = (lane >> 4) < P1 && (lane & 15u) < P2;
+    if (act) {
+      p1 = lane >> 4;
+      p2 = lane & 15u;
+    }
+  } else {
+    while (q > 1 && (kWave / q) < K) q >>= 1;  // q = 64 / pow2ceil(K)
+    const u32 e = lane / q;
+    c = lane % q;
+    act = e < K;
+    if (act) {
+      p1 = e / P2;
+      p2 = e - p1 * P2;
+    }
+  }
   const bool owner = act && c == 0;
   const uint2 L1 = owner ? a.parts1[pb1 + p1] : make_uint2(0, 0);
   const uint2 L2 = owner ? a.parts2[pb2 + p2] : make_uint2(0, 0);
@@ -971,6 +1011,12 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   }
   u32 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol (parts < 16)
   bool bad = false;
+  // cells per symbol row: P1 and P2, or rows of kProdRow cleared first
+  const u32 S1 = mf ? kProdRow : P1, S2 = mf ? kProdRow : P2;
+  if (mf) {
+    *reinterpret_cast<uint4 *>(&val[lane * kProdRow]) = make_uint4(0, 0, 0, 0);
+    *reinterpret_cast<uint4 *>(&val[(kWave + lane) * kProdRow]) = make_uint4(0, 0, 0, 0);
+  }
   if (found) {
     const u32 a1 = one_short ? sa : la, n1 = one_short ? sn : ln;
     const u32 a2 = one_short ? la : sa, n2 = one_short ? ln : sn;
@@ -987,8 +1033,8 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
         // parts are below P; the padding part kProdRowSum marks no arc and
         // writes the spare cell
         const bool v1 = x1[k].x < P1, v2 = x2[k].x < P2;
-        val[v1 ? lane * P1 + x1[k].x : kProdCells] = x1[k].y;
-        val[v2 ? kWave * P1 + lane * P2 + x2[k].x : kProdCells] = x2[k].y;
+        val[v1 ? lane * S1 + x1[k].x : kProdCells] = x1[k].y;
+        val[v2 ? kWave * S1 + lane * S2 + x2[k].x : kProdCells] = x2[k].y;
         pm1 |= v1 ? 1u << x1[k].x : 0u;
         pm2 |= v2 ? 1u << x2[k].x : 0u;
         bad |= (!v1 && x1[k].x != kProdRowSum) || (!v2 && x2[k].x != kProdRowSum);
@@ -1013,22 +1059,36 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  // 2. entry sums: lane c of the entry adds the terms of g = c, c + q, ...
-  //    (bit j of mm: symbol c + j q is one of the entry's terms)
+  // 2. entry sums
   const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
-  u64 mm = act ? m >> c : 0;
-  const u32 qs = q < (u32)kWave ? q : 0u;  // q = 64: a single symbol per lane
-  u32 ia = c * P1 + p1, ib = kWave * P1 + c * P2 + p2;
-  const u32 da = q * P1, db = q * P2;
   double acc = 0.0;
-  while (mm) {  // at most 64 / q steps: every step drops q bits (all, when q = 64)
-    const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
-    acc += (mm & 1u) ? (double)t : 0.0;
-    mm = qs ? mm >> qs : 0ull;
-    ia += da;
-    ib += db;
+  if (mf) {
+    // the 4 x 64 by 64 x 4 product on the matrix cores (see above)
+    double d = 0.0;
+#pragma unroll
+    for (u32 t = 0; t < 4; ++t) {
+      const double x = (double)__uint_as_float(val[t * kWave + lane]);
+      const double y = (double)__uint_as_float(val[(kProdRow + t) * kWave + lane]);
+      d = __builtin_amdgcn_mfma_f64_4x4x4f64(x, y, d, 0, 0, 0);
+    }
+    d += dpp_f64<kDppRowRor4>(d);
+    acc = d + dpp_f64<kDppRowRor8>(d);
+  } else {
+    // lane c of the entry adds the terms of g = c, c + q, ... (bit j of mm:
+    // symbol c + j q is one of the entry's terms)
+    u64 mm = act ? m >> c : 0;
+    const u32 qs = q < (u32)kWave ? q : 0u;  // q = 64: a single symbol per lane
+    u32 ia = c * P1 + p1, ib = kWave * P1 + c * P2 + p2;
+    const u32 da = q * P1, db = q * P2;
+    while (mm) {  // at most 64 / q steps: every step drops q bits (all, when q = 64)
+      const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
+      acc += (mm & 1u) ? (double)t : 0.0;
+      mm = qs ? mm >> qs : 0ull;
+      ia += da;
+      ib += db;
+    }
+    for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
   }
-  for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
 
   // 3. merged arcs in entry order: the visited-table insert resumes from
   //    the probe loaded above; the source's joined pairs (the entries' terms)
