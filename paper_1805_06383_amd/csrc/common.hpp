@@ -89,6 +89,32 @@ __device__ __forceinline__ T wave_sum(T x) {
   return x;
 }
 
+// Sum of x over the 64 lanes of a wave whose lanes are all active, returned
+// to every lane: window sums by DPP row shifts (lane 15 of each row of 16
+// ends with the row's sum), rows combined by the row broadcasts of lane 15
+// and lane 31, the total read from lane 63.  No LDS traffic.
+__device__ __forceinline__ u32 wave_total(u32 x) {
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return (u32)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// Bitwise OR of x over the 64 lanes of a wave whose lanes are all active,
+// returned to every lane (the pattern of wave_total).
+__device__ __forceinline__ u32 wave_or(u32 x) {
+  x |= (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x |= (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x |= (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x |= (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x |= (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x |= (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return (u32)__builtin_amdgcn_readlane((int)x, 63);
+}
+
 template <class T>
 __device__ __forceinline__ T wave_max(T x) {
 #pragma unroll

@@ -504,8 +504,8 @@ void check_csr_ranges(const fstc_fst &m, bool by_output) {
 void alloc_csr(const fstc_fst &m, Buf &b, Csr &c) {
   const u64 n = m.num_arcs, nq = m.num_states;
   const u64 n1 = std::max<u64>(n, 1);
-  const size_t sz[7] = {(nq + 1) * 4, n1 * 4, (n + 1) * 4, n1 * 8, (nq + 1) * 4, n1 * 8,
-                        std::max<u64>(nq, 1) * 4};
+  const size_t sz[7] = {(nq + 1) * 4, n1 * 4, (n + 1) * 4, (n + kArcTail) * 8, (nq + 1) * 4,
+                        n1 * 8, std::max<u64>(nq, 1) * 4};
   size_t off[7], total = 0;
   for (int i = 0; i < 7; ++i) {
     off[i] = total;

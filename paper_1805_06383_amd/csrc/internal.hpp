@@ -112,11 +112,16 @@ struct Csr {
   u32 *row = nullptr;        // [num_states + 1] -> segment index
   u32 *seg_sym = nullptr;    // [num_arcs] inner symbol of segment
   u32 *seg_off = nullptr;    // [num_arcs + 1] -> arc index
-  uint2 *arcs = nullptr;     // [num_arcs] (part rank within state, weight bits)
+  uint2 *arcs = nullptr;     // [num_arcs + kArcTail] (part rank within state, weight bits)
   u32 *part_base = nullptr;  // [num_states + 1]
   uint2 *parts = nullptr;    // [num_arcs] (target, outer symbol)
   u32 *cell_flag = nullptr;  // [num_states] see build_cell_flags (compose only)
 };
+
+// The arc array of a CSR built for composition (alloc_csr) has kArcTail
+// spare entries after its last arc, so that kArcTail consecutive arcs may be
+// loaded from any arc index (the values past the end are garbage).
+constexpr u32 kArcTail = 4;
 
 // Device counters written by the CSR build: [0] segments, [1] parts,
 // [2] max parts of one state.

@@ -898,6 +898,7 @@ constexpr int kProdWaves = kProdNT / kWave;
 constexpr u32 kProdCells = kProdRowSum * kWave;  // both matrices, 64 symbols
 constexpr u32 kProdRow = kProdMfmaParts;         // cells per symbol, matrix-core form
 constexpr int kProdBatch = 4;                     // arcs per side loaded at once
+static_assert(kProdBatch == (int)kProdRow, "one batch holds a matrix-core segment");
 static_assert(2 * kProdRow * kWave <= kProdCells, "matrix-core cells fit the wave's LDS");
 
 // x from the lane 4 or 8 places before it (cyclically) in its row of 16.
@@ -962,14 +963,18 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     }
   }
   const bool owner = act && c == 0;
-  const uint2 L1 = owner ? a.parts1[pb1 + p1] : make_uint2(0, 0);
-  const uint2 L2 = owner ? a.parts2[pb2 + p2] : make_uint2(0, 0);
+  // loaded by every lane, without a branch (the others load part 0 and the
+  // visited-table slot of that pair, in bounds); only owners use them
+  const uint2 L1 = a.parts1[pb1 + p1], L2 = a.parts2[pb2 + p2];
   const u64 hk = ((u64)L1.x << 32) | (u64)L2.x;
-  u64 hslot = a.vn2 ? (u64)L1.x * a.vn2 + L2.x : mix64(hk) & a.hmask;
-  u64 hcur = 0;
-  if (owner)
-    hcur = a.vn2 ? (u64)__hip_atomic_load(&a.vis[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)
-                 : __hip_atomic_load(&a.hkeys[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  u64 hslot, hcur;
+  if (a.vn2) {  // wave-uniform
+    hslot = (u64)L1.x * a.vn2 + L2.x;
+    hcur = __hip_atomic_load(&a.vis[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  } else {
+    hslot = mix64(hk) & a.hmask;
+    hcur = __hip_atomic_load(&a.hkeys[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
 
   const u32 *ssym = one_short ? a.seg_sym1 : a.seg_sym2;
   const u32 *lsym = one_short ? a.seg_sym2 : a.seg_sym1;
@@ -980,19 +985,31 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   // 1. join, staging, part masks.  Segment offsets are loaded with the
   //    symbols (this lane's short-list segment; the long-list chunk's, handed
   //    over by the lane that found the match), so the arc loads follow the
-  //    join without another round trip.
+  //    join without another round trip.  Loads are unconditional, from
+  //    indexes clamped into the lists, and their values selected after.
   const u32 idx = bs + lane;
   const bool valid = idx < es;
-  const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
-  const u32 sa = valid ? soffs[idx] : 0u, sn = valid ? soffs[idx + 1] - sa : 0u;
+  const u32 ic = valid ? idx : es - 1;
+  const u32 sym0 = ssym[ic], so0 = soffs[ic], so1 = soffs[ic + 1];
+  const u32 sym = valid ? sym0 : 0xffffffffu;  // labels are below 2^32 - 1
+  const u32 sa = valid ? so0 : 0u, sn = valid ? so1 - so0 : 0u;
   const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
+  const u64 vmask = __ballot(valid);
   bool found = false;
   u32 la = 0, ln = 0;
   for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
     const u32 len = min(le - cb, (u32)kWave);
     const bool in = lane < len;
-    const u32 lv = in ? lsym[cb + lane] : 0xffffffffu;
-    const u32 lo0 = in ? loffs[cb + lane] : 0u, lo1 = in ? loffs[cb + lane + 1] : 0u;
+    const u32 lc = cb + min(lane, len - 1);
+    const u32 lv0 = lsym[lc], lo00 = loffs[lc], lo10 = loffs[lc + 1];
+    const u32 lv = in ? lv0 : 0xffffffffu, lo0 = in ? lo00 : 0u, lo1 = in ? lo10 : 0u;
+    if (__ballot(valid && lv == sym) == vmask) {
+      // the chunk starts with the short list's symbols: lane i matches lane i
+      found = valid;
+      la = lo0;
+      ln = lo1 - lo0;
+      break;
+    }
     if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
     u32 pos = 0;  // elements of the chunk below sym
 #pragma unroll
@@ -1017,52 +1034,84 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     *reinterpret_cast<uint4 *>(&val[lane * kProdRow]) = make_uint4(0, 0, 0, 0);
     *reinterpret_cast<uint4 *>(&val[(kWave + lane) * kProdRow]) = make_uint4(0, 0, 0, 0);
   }
-  if (found) {
-    const u32 a1 = one_short ? sa : la, n1 = one_short ? sn : ln;
-    const u32 a2 = one_short ? la : sa, n2 = one_short ? ln : sn;
+  const u32 a1 = one_short ? sa : la, n1 = found ? (one_short ? sn : ln) : 0u;
+  const u32 a2 = one_short ? la : sa, n2 = found ? (one_short ? ln : sn) : 0u;
+  // arc k of each side is present when k < h (k in the batch); a present
+  // arc's part is below P (else the source is malformed); an absent one
+  // writes the spare cell
+  auto stage = [&](const uint2(&x1)[kProdBatch], const uint2(&x2)[kProdBatch], u32 h1, u32 h2) {
+#pragma unroll
+    for (int k = 0; k < kProdBatch; ++k) {
+      const bool in1 = (u32)k < h1, in2 = (u32)k < h2;
+      const bool v1 = in1 & (x1[k].x < P1), v2 = in2 & (x2[k].x < P2);
+      val[v1 ? lane * S1 + x1[k].x : kProdCells] = x1[k].y;
+      val[v2 ? kWave * S1 + lane * S2 + x2[k].x : kProdCells] = x2[k].y;
+      pm1 |= (v1 ? 1u : 0u) << x1[k].x;
+      pm2 |= (v2 ? 1u : 0u) << x2[k].x;
+      bad |= (in1 & !v1) | (in2 & !v2);  // bitwise: no short-circuit branches
+    }
+  };
+  if (mf) {
+    // at most kProdRow arcs per segment (single-arc cells): kProdRow
+    // consecutive arcs from the segment's first (arc 0 for a lane without a
+    // match; the arc arrays have kArcTail spare entries), those past the
+    // segment's end replaced by padding
+    static_assert(kProdBatch <= (int)kArcTail, "segment loads stay inside the arc arrays");
+    const u32 f1 = n1 ? a1 : 0u, f2 = n2 ? a2 : 0u;
+    uint2 x1[kProdBatch], x2[kProdBatch];
+#pragma unroll
+    for (int k = 0; k < kProdBatch; ++k) {
+      x1[k] = prod_arc<NARROW>(a.arcs1, f1 + (u32)k);
+      x2[k] = prod_arc<NARROW>(a.arcs2, f2 + (u32)k);
+    }
+    bad |= (n1 > kProdRow) | (n2 > kProdRow);
+    stage(x1, x2, n1, n2);
+  } else if (found) {
     for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
       uint2 x1[kProdBatch], x2[kProdBatch];
 #pragma unroll
       for (int k = 0; k < kProdBatch; ++k) {
         const u32 i = i0 + (u32)k;
-        x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(kProdRowSum, 0);
-        x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(kProdRowSum, 0);
+        x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(0, 0);
+        x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(0, 0);
       }
-#pragma unroll
-      for (int k = 0; k < kProdBatch; ++k) {
-        // parts are below P; the padding part kProdRowSum marks no arc and
-        // writes the spare cell
-        const bool v1 = x1[k].x < P1, v2 = x2[k].x < P2;
-        val[v1 ? lane * S1 + x1[k].x : kProdCells] = x1[k].y;
-        val[v2 ? kWave * S1 + lane * S2 + x2[k].x : kProdCells] = x2[k].y;
-        pm1 |= v1 ? 1u << x1[k].x : 0u;
-        pm2 |= v2 ? 1u << x2[k].x : 0u;
-        bad |= (!v1 && x1[k].x != kProdRowSum) || (!v2 && x2[k].x != kProdRowSum);
-      }
+      stage(x1, x2, n1 > i0 ? n1 - i0 : 0u, n2 > i0 ? n2 - i0 : 0u);
     }
   }
   if (__ballot(bad)) {  // impossible: parts are below the state's part count
     if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
   }
-  // lane p holds the symbol mask of M1 part p in ma, of M2 part p in mb
+  // symbol masks of the parts (bit g: symbol g has an arc of the part),
+  // outside the matrix-core form: lane p holds M1 part p's in ma, M2 part
+  // p's in mb
   u64 ma = 0, mb = 0;
-  for (u32 p = 0; p < P1; ++p) {
-    const u64 m = __ballot((pm1 >> p) & 1u);
-    ma = lane == p ? m : ma;
-  }
-  for (u32 p = 0; p < P2; ++p) {
-    const u64 m = __ballot((pm2 >> p) & 1u);
-    mb = lane == p ? m : mb;
+  if (!mf) {
+    for (u32 p = 0; p < P1; ++p) {
+      const u64 m = __ballot((pm1 >> p) & 1u);
+      ma = lane == p ? m : ma;
+    }
+    for (u32 p = 0; p < P2; ++p) {
+      const u64 m = __ballot((pm2 >> p) & 1u);
+      mb = lane == p ? m : mb;
+    }
   }
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-  // 2. entry sums
-  const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
+  // 2. entry sums; which entries have a term (the owner's `has`) and the
+  //    source's joined pairs
+  bool has;
+  u32 pairs;
   double acc = 0.0;
   if (mf) {
+    // bit 4 p1 + p2 of o: parts p1 and p2 both have an arc at this lane's
+    // symbol, a joined pair (the parts' bits spread 4 apart, times pm2)
+    const u32 sp = (pm1 & 1u) | ((pm1 & 2u) << 3) | ((pm1 & 4u) << 6) | ((pm1 & 8u) << 9);
+    const u32 o = pm2 * sp;
+    has = (wave_or(o) >> ((p1 << 2) | p2)) & 1u;
+    pairs = wave_total((u32)__popc(o));
     // the 4 x 64 by 64 x 4 product on the matrix cores (see above)
     double d = 0.0;
 #pragma unroll
@@ -1074,6 +1123,9 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     d += dpp_f64<kDppRowRor4>(d);
     acc = d + dpp_f64<kDppRowRor8>(d);
   } else {
+    const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
+    has = m != 0;
+    pairs = wave_total(owner ? (u32)__popcll(m) : 0u);
     // lane c of the entry adds the terms of g = c, c + q, ... (bit j of mm:
     // symbol c + j q is one of the entry's terms)
     u64 mm = act ? m >> c : 0;
@@ -1093,10 +1145,9 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   // 3. merged arcs in entry order: the visited-table insert resumes from
   //    the probe loaded above; the source's joined pairs (the entries' terms)
   //    go to pcnt[u]
-  const bool run = owner && m != 0;
+  const bool run = owner && has;
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
-  const u32 pairs = wave_sum(owner ? (u32)__popcll(m) : 0u);
   const u64 base = a.R + a.poff[u];
   if (run && a.vn2) {
     // dense array: the entry read above, then a claim if it was unvisited
