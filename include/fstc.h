@@ -193,6 +193,8 @@ typedef struct fstc_stats {
   double ms_product_kernel;   /* product-merge kernel alone, all levels      */
   uint32_t product_launches;  /* launches of the product-merge kernel        */
   uint32_t reserved0;
+  uint64_t total_product_mfma_sources; /* of those, sources whose sums ran on
+                                          the matrix cores (float64 MFMA)     */
 } fstc_stats;
 
 /*

@@ -58,10 +58,15 @@ void *Buf::ensure(size_t bytes) {
   return p;
 }
 
+// Growth factor of the grow-only arrays: 4 while they are small (fewer and
+// smaller copies of what they hold), 2 from kFastGrowBytes on.
+constexpr size_t kFastGrowBytes = size_t(1) << 28;
+inline size_t grown(size_t cap_bytes) { return cap_bytes * (cap_bytes < kFastGrowBytes ? 4 : 2); }
+
 void *Buf::grow_keep(size_t bytes, size_t used) {
   if (bytes <= cap && p) return p;
   const size_t c = std::max<size_t>(std::max<size_t>(kMinGrow * 4, (bytes + 255) & ~(size_t)255),
-                                    2 * cap);
+                                    grown(cap));
   void *q = A->alloc(c);
   if (used && p) FSTC_HIP(hipMemcpyAsync(q, p, used, hipMemcpyDeviceToDevice, A->stream));
   release();
@@ -236,7 +241,7 @@ struct ArcCols {
   explicit ArcCols(Allocator *A, hipStream_t st) : b(A), s(st) {}
   void grow(u64 need, u64 used) {
     if (need <= cap && b.p) return;
-    const u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), 2 * cap);
+    const u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), grown(5 * cap * 4) / 20);
     Buf nb(b.A);
     nb.ensure(5 * nc * 4);
     if (used && b.p)
@@ -394,6 +399,7 @@ void Composer::run(fstc_result *out) {
   u32 write_launches = 0, merge_launches = 0, sort_launches = 0, fused_levels = 0;
   u64 dense_records = 0, dense_runs = 0, sort_runs = 0, product_records = 0, product_sources = 0;
   u32 product_launches = 0;
+  u64 product_mfma_sources = 0;
 
   ArcCols out_arcs(&A, s);
   // single-pass scan state: zero-filled when (re)allocated, then written
@@ -461,6 +467,7 @@ void Composer::run(fstc_result *out) {
     premerge += R;
     max_level_pre = std::max(max_level_pre, R);
     product_sources += nprod;
+    product_mfma_sources += hs->st.nprod_mfma;
     big_total += nbig;
 
     match.ensure(M * sizeof(uint4));
@@ -753,6 +760,7 @@ void Composer::run(fstc_result *out) {
     stats->total_product_sources = product_sources;
     stats->ms_product_kernel = ms[kProductKernel];
     stats->product_launches = product_launches;
+    stats->total_product_mfma_sources = product_mfma_sources;
     stats->total_sort_runs = sort_runs;
     stats->total_matches = total_matches;
     stats->total_big_records = big_records;

@@ -99,13 +99,13 @@ __device__ __forceinline__ bool products_normal(u32 f1, u32 f2) {
 // form (at most kProdMfmaParts parts per state, products_normal).  The
 // cells are single-arc only for states of at most kProdParts parts.
 __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1, u32 q2,
-                                              const Ranges &r) {
+                                              const Ranges &r, bool &mfma) {
   const u32 f1 = a.c1.cell_flag[q1], f2 = a.c2.cell_flag[q2];
   if ((f1 | f2) & kCellBad) return 0;
   const u32 pb1 = a.c1.part_base[q1], p1 = a.c1.part_base[q1 + 1] - pb1;
   const u32 pb2 = a.c2.part_base[q2], p2 = a.c2.part_base[q2 + 1] - pb2;
   if (p1 == 0 || p2 == 0 || p1 + p2 > kProdRowSum) return 0;
-  const bool mfma = p1 <= kProdMfmaParts && p2 <= kProdMfmaParts && products_normal(f1, f2);
+  mfma = p1 <= kProdMfmaParts && p2 <= kProdMfmaParts && products_normal(f1, f2);
   a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16), mfma ? 1u : 0u);
   a.phdr[2 * u + 1] = make_uint4(r.b1, r.e1, r.b2, r.e2);
   return p1 * p2;
@@ -127,15 +127,16 @@ __device__ __forceinline__ bool thread_join(const LevelArgs &a, const Ranges &r)
 // aggregated per workgroup in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   __shared__ u32 s_n[3], s_base[3], s_max;
-  __shared__ unsigned long long s_p[2];
+  __shared__ unsigned long long s_p[3];
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (threadIdx.x < 3) s_n[threadIdx.x] = 0;
-  if (threadIdx.x < 2) s_p[threadIdx.x] = 0;
+  if (threadIdx.x < 3) s_p[threadIdx.x] = 0;
   if (threadIdx.x == 0) s_max = 0;
   bool pred[3] = {false, false, false};  // wide, heavy, big
   u64 cnt = 0;
   u32 pk = 0;
+  bool mf = false;
   Ranges r{0, 0, 0, 0};
   if (u < a.nsrc) {
     const u32 sid = a.lo + (u32)u;
@@ -144,7 +145,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     a.mend[u] = 0;
     r = Ranges{a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]};
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
-    if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r);
+    if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r, mf);
     a.pk[u] = pk;
     if (pk) {
       a.cnt[u] = 0;
@@ -168,10 +169,12 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   {
     const u32 np = wave_sum(pk ? 1u : 0u);
     const u64 ne = wave_sum((u64)pk);
+    const u32 nm = (u32)__popcll(__ballot(pk && mf));
     __syncthreads();  // s_p cleared
     if (lane == 0 && np) {
       atomicAdd(&s_p[0], (unsigned long long)np);
       atomicAdd(&s_p[1], (unsigned long long)ne);
+      atomicAdd(&s_p[2], (unsigned long long)nm);
     }
   }
   __syncthreads();
@@ -195,6 +198,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   if (threadIdx.x == 4 && s_p[0]) {
     atomicAdd(&a.st->nprod, (u32)s_p[0]);
     atomicAdd((unsigned long long *)&a.st->prod_entries, s_p[1]);
+    if (s_p[2]) atomicAdd(&a.st->nprod_mfma, (u32)s_p[2]);
   }
   __syncthreads();
   u32 *const lists[3] = {a.wide, a.heavy, a.big};

@@ -41,6 +41,8 @@ struct Status {
   u32 seq;            // host copy only: number of the last publication, written last
   u64 prod_records;   // their joined arc pairs (not written as records)
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
+  u32 nprod_mfma;     // product-merge sources summed on the matrix cores
+  u32 pad0;
 };
 
 // Product merge (merge.hip, k_prod_sources).  A source (q1, q2) is merged

@@ -1758,7 +1758,7 @@ __device__ __forceinline__ void clear_level(Status *st) {
   st->nwide = st->nheavy = st->nbig = st->nnew = 0;
   st->max_small = 0;
   st->dense_records = st->dense_runs = st->sort_runs = 0;
-  st->nprod = 0;
+  st->nprod = st->nprod_mfma = 0;
   st->prod_records = st->prod_entries = 0;
   st->nsort = 0;
 }

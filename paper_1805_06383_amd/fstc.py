@@ -78,7 +78,8 @@ class FstcStats(ctypes.Structure):
                 ("total_dense_records", _u64), ("total_dense_runs", _u64),
                 ("total_sort_runs", _u64), ("total_product_records", _u64),
                 ("total_product_sources", _u64), ("ms_product_kernel", ctypes.c_double),
-                ("product_launches", _u32), ("reserved0", _u32)]
+                ("product_launches", _u32), ("reserved0", _u32),
+                ("total_product_mfma_sources", _u64)]
 
 
 EXPORTS = ("fstc_compose", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",

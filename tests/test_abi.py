@@ -52,7 +52,37 @@ def test_struct_layouts_match_header(F):
     assert ctypes.sizeof(F.FstcFst) == 4 * 4 + 8 + 6 * 8
     assert ctypes.sizeof(F.FstcOpts) == 4 + 4 + 8 + 8 + 3 * 8 + 4 + 4 + 4 + 4 + 4 + 4
     assert ctypes.sizeof(F.FstcResult) == 3 * 8 + 4 + 4 + 8 * 8 + 8 * 8 + 8 * 8
-    assert ctypes.sizeof(F.FstcStats) == 4 + 4 + 4 * 8 + 8 * 8 + 4 + 4 + 8 + 8 + 4 + 4 + 8 + 4 + 4 + 5 * 8 + 8 + 4 + 4
+    assert ctypes.sizeof(F.FstcStats) == 4 + 4 + 4 * 8 + 8 * 8 + 4 + 4 + 8 + 8 + 4 + 4 + 8 + 4 + 4 + 5 * 8 + 8 + 4 + 4 + 8
+
+
+def test_struct_offsets_match_header(F, tmp_path):
+    """Every field of the binding's ctypes structs sits at the offset the C
+    header gives it (gcc, LP64), and the structs have the header's sizes."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("no gcc")
+    structs = {"fstc_fst": F.FstcFst, "fstc_opts": F.FstcOpts, "fstc_result": F.FstcResult,
+               "fstc_stats": F.FstcStats}
+    lines = ['#include "fstc.h"', "#include <stdio.h>", "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in cls._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(ROOT, "include")
+    r = subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", f"-I{inc}", "-I/opt/rocm/include",
+                        str(src), "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
+    for cname, cls in structs.items():
+        assert got[(cname, "size")] == ctypes.sizeof(cls), cname
+        for fname, _ in cls._fields_:
+            assert got[(cname, fname)] == getattr(cls, fname).offset, (cname, fname)
 
 
 def _fst(F, **kw):

@@ -63,6 +63,8 @@ def test_product_config4_caps(fstc, cap):
     st = pr.stats
     assert st["product_launches"] >= 1
     assert st["total_product_records"] == pr.num_premerge_arcs  # every source qualifies
+    # 4 parts per state, weights in (0, 1]: every source on the matrix cores
+    assert st["total_product_mfma_sources"] == st["total_product_sources"]
     assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2, max_levels=cap)),
                 rtol=RTOL, what=f"config4 cap {cap}")
 
@@ -145,6 +147,7 @@ def test_product_matrix_product(fstc):
     B = W.random_weights(rng, 40 * 12).reshape(40, 12)
     g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B))
     assert g.stats["total_product_sources"] == 1
+    assert g.stats["total_product_mfma_sources"] == 0  # 12 parts: the vector form
     g = g.to_host()
     assert g.num_premerge == 4 * 40 * 12
     P = A.astype(np.float64) @ B.astype(np.float64)
@@ -181,6 +184,8 @@ def test_product_single_entry(fstc, with_inf):
         A[0, 17] = np.inf
     g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B))
     assert g.stats["total_product_sources"] == 1
+    # an infinite weight keeps the source off the matrix cores
+    assert g.stats["total_product_mfma_sources"] == (0 if with_inf else 1)
     g = g.to_host()
     assert g.num_premerge == 64 and len(g.w) == 1
     ref = oracle.compose(W.one_state_dense(A), W.one_state_dense(B))
@@ -188,3 +193,38 @@ def test_product_single_entry(fstc, with_inf):
         assert np.isinf(g.w[0]) and np.isinf(ref.w[0])
     else:
         np.testing.assert_allclose(g.w, ref.w, rtol=RTOL)
+
+
+def scaled_states(m, every, e):
+    """m with the weights of the arcs leaving states q % every == 0 times 2^e."""
+    w = m.weight.astype(np.float64).copy()
+    w[m.src % every == 0] *= 2.0 ** e
+    return with_weights(m, w.astype(np.float32))
+
+
+@pytest.mark.parametrize("case", ["overflow", "subnormal"])
+def test_product_out_of_range_products(fstc, case):
+    """Sources whose float32 products would overflow or fall below the
+    normal range keep the float32-product (vector) form, where the oracle's
+    infinities and subnormal products are reproduced; the others run on the
+    matrix cores.  Every weight meets the parity bar (1e-5 relative, plus one
+    float32 subnormal step)."""
+    m1, m2 = W.config4(0)
+    if case == "overflow":
+        m1, m2 = scaled_states(m1, 3, 90), scaled_states(m2, 5, 45)
+    else:
+        m1, m2 = scaled_states(m1, 3, -100), scaled_states(m2, 5, -40)
+    g = fstc.compose(m1, m2, max_levels=3)
+    st = g.stats
+    assert 0 < st["total_product_mfma_sources"] < st["total_product_sources"]
+    gc = canon_of(g.to_host())
+    ref = canon_of(oracle.compose(m1, m2, max_levels=3))
+    assert_same(gc, ref, rtol=np.inf, what=f"config4 {case} cap 3")
+    assert np.array_equal(np.isinf(gc.w), np.isinf(ref.w))
+    if case == "overflow":
+        assert np.isinf(ref.w).any()
+    else:
+        assert (np.abs(ref.w) < np.finfo(np.float32).tiny).any()
+    fin = np.isfinite(ref.w)
+    err = np.abs(gc.w[fin].astype(np.float64) - ref.w[fin].astype(np.float64))
+    assert (err <= 1e-5 * np.abs(ref.w[fin].astype(np.float64)) + 2.0 ** -149).all()
