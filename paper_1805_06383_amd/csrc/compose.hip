@@ -416,7 +416,7 @@ void Composer::run(fstc_result *out) {
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),
-      aoff(&level_tmp), pk(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      aoff(&level_tmp), pk(&level_tmp), pflag(&level_tmp), ftot(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -436,7 +436,7 @@ void Composer::run(fstc_result *out) {
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
     ptot.ensure(np1 * 8); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
-    pk.ensure(np1 * 4); poff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
+    pk.ensure(np1 * 4); poff.ensure(np1 * 8); pflag.ensure(np1 * 8); ftot.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     wrange.ensure(np1 * sizeof(uint4));
     stmp.ensure(scan3_temp_bytes(np1));
 
@@ -448,16 +448,20 @@ void Composer::run(fstc_result *out) {
                  wrange.as<uint4>(),
                  dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), phdr.as<uint4>(),
                  product ? 1u : 0u, tstart.as<u64>(), mend.as<u64>()};
+    la.pflag = pflag.as<u64>();
     T.at(kCount);
     launch_count(la, s);
-    // records, matches and product-merge entries per source
+    // records, matches and product-merge entries per source; the product
+    // sources' flags summed
     {
-      const ScanJob jobs[3] = {{cnt.p, true, roff.as<u64>()}, {mc.p, false, moff.as<u64>()},
-                               {pk.p, false, poff.as<u64>()}};
-      exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+      ScanJob jobs[4] = {{cnt.p, true, roff.as<u64>()}, {mc.p, false, moff.as<u64>()},
+                         {pk.p, false, poff.as<u64>()}, {pflag.p, true, ftot.as<u64>()}};
+      jobs[3].total_only = true;
+      exclusive_scan_lb(jobs, 4, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
     }
     const u32 seq1 = next_publication();
-    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, dst, hs_dev, seq1, s);
+    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, poff.as<u64>() + nsrc,
+                        ftot.as<u64>() + nsrc, dst, hs_dev, seq1, s);
     T.at(kNone);
     wait_published(seq1);
     const u64 R = hs->st.R, M = hs->st.M;

@@ -121,17 +121,15 @@ __device__ __forceinline__ bool thread_join(const LevelArgs &a, const Ranges &r)
 }
 
 // Thread per source: selects the product-merge sources (no records, no
-// matches; pk = their entry count), joins the other short ones, lists the
-// rest for the wavefront / workgroup joins.  List appends, the window
-// maximum and the product-merge totals (st->nprod, prod_entries) are
-// aggregated per workgroup in LDS: one device atomic per list per block.
+// matches; pk = their entry count, pflag their flags for the level scan),
+// joins the other short ones, lists the rest for the wavefront / workgroup
+// joins.  List appends and the window maximum are aggregated per workgroup
+// in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   __shared__ u32 s_n[3], s_base[3], s_max;
-  __shared__ unsigned long long s_p[3];
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (threadIdx.x < 3) s_n[threadIdx.x] = 0;
-  if (threadIdx.x < 3) s_p[threadIdx.x] = 0;
   if (threadIdx.x == 0) s_max = 0;
   bool pred[3] = {false, false, false};  // wide, heavy, big
   u64 cnt = 0;
@@ -147,6 +145,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
     if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r, mf);
     a.pk[u] = pk;
+    a.pflag[u] = pk ? 1ull | ((u64)mf << 32) : 0ull;
     if (pk) {
       a.cnt[u] = 0;
       a.mc[u] = 0;
@@ -166,17 +165,6 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     }
   }
   const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
-  {
-    const u32 np = wave_sum(pk ? 1u : 0u);
-    const u64 ne = wave_sum((u64)pk);
-    const u32 nm = (u32)__popcll(__ballot(pk && mf));
-    __syncthreads();  // s_p cleared
-    if (lane == 0 && np) {
-      atomicAdd(&s_p[0], (unsigned long long)np);
-      atomicAdd(&s_p[1], (unsigned long long)ne);
-      atomicAdd(&s_p[2], (unsigned long long)nm);
-    }
-  }
   __syncthreads();
   u64 m[3];
   u32 woff[3];
@@ -195,11 +183,6 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   u32 *const counters[3] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig};
   if (threadIdx.x < 3 && s_n[threadIdx.x]) s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
   if (threadIdx.x == 3 && s_max) atomicMax(&a.st->max_small, s_max);
-  if (threadIdx.x == 4 && s_p[0]) {
-    atomicAdd(&a.st->nprod, (u32)s_p[0]);
-    atomicAdd((unsigned long long *)&a.st->prod_entries, s_p[1]);
-    if (s_p[2]) atomicAdd(&a.st->nprod_mfma, (u32)s_p[2]);
-  }
   __syncthreads();
   u32 *const lists[3] = {a.wide, a.heavy, a.big};
 #pragma unroll

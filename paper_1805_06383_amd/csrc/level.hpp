@@ -127,11 +127,13 @@ struct LevelArgs {
   u32 prod;              // nonzero: sources may take the product merge
   u64 *tstart, *mend;    // [nsrc] the merge's first / end temp slot per source:
                          // zeroed by the count kernel
+  u64 *pflag;            // [nsrc] 1 for a product-merge source, plus 2^32 when it
+                         // takes the matrix-core form (summed by the level scan)
 };
 
 // Written by the count kernel for a product-merge source u at phdr[2u], [2u+1]:
-// (M1 part base, M2 part base, P1 | P2 << 16, unused), (M1 segment range
-// begin, end, M2 segment range begin, end).
+// (M1 part base, M2 part base, P1 | P2 << 16, matrix-core form), (M1 segment
+// range begin, end, M2 segment range begin, end).
 
 void launch_count(const LevelArgs &a, hipStream_t s);
 // nwide / nheavy: the list lengths the count kernels produced (st->nwide, nheavy).
@@ -264,8 +266,11 @@ void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, con
 // Both also copy *st to `host` (pinned, coherent host memory the device can
 // write) and then set host->seq = seq, so that the host can wait for the
 // copy by watching that word.
-void launch_level_totals(const u64 *r_total, const u64 *m_total, Status *st, Status *host, u32 seq,
-                         hipStream_t s);
+// Level totals after the count scan: records *r_total, matches *m_total,
+// product-merge entries *p_total, and *f_total (the sum of pflag: product
+// sources in the low, matrix-core ones in the high 32 bits).
+void launch_level_totals(const u64 *r_total, const u64 *m_total, const u64 *p_total,
+                         const u64 *f_total, Status *st, Status *host, u32 seq, hipStream_t s);
 // Level total of merged arcs, new pairs (*new_total, when not NULL), the
 // product merge's joined pairs (*pair_total: the sum of a.pcnt over the
 // level's sources, records included, less st->R) and the dense / sort tile

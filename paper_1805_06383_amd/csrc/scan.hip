@@ -188,7 +188,7 @@ constexpr int kLbIT = 8;
 constexpr int kLbTile = kLbNT * kLbIT;
 constexpr u32 kLbAgg = 1u, kLbIncl = 2u;
 constexpr u32 kLbSpins = 1u << 22;
-constexpr int kLbMax = 3;
+constexpr int kLbMax = 4;
 
 struct LbArgs {
   const void *in[kLbMax];
@@ -418,7 +418,8 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   const dim3 g((unsigned)nb), bl(kLbNT);
   if (k == 1) hipLaunchKernelGGL(k_scan_lb<1>, g, bl, 0, s, p);
   else if (k == 2) hipLaunchKernelGGL(k_scan_lb<2>, g, bl, 0, s, p);
-  else hipLaunchKernelGGL(k_scan_lb<3>, g, bl, 0, s, p);
+  else if (k == 3) hipLaunchKernelGGL(k_scan_lb<3>, g, bl, 0, s, p);
+  else hipLaunchKernelGGL(k_scan_lb<4>, g, bl, 0, s, p);
 }
 
 size_t scan3_temp_bytes(u64 n) {
