@@ -1805,7 +1805,7 @@ __global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 
   __syncthreads();
   if (threadIdx.x < 3) {
     u64 t = 0;
-    for (int i = 0; i < 1024 / kWave; ++i) t += s_v[threadIdx.x][i];
+    for (u32 i = 0; i < blockDim.x / kWave; ++i) t += s_v[threadIdx.x][i];
     u64 *dst = threadIdx.x == 0 ? &st->dense_records : threadIdx.x == 1 ? &st->dense_runs : &st->sort_runs;
     *dst = t;
   }
@@ -2021,7 +2021,9 @@ void launch_level_totals(const u64 *r_total, const u64 *m_total, const u64 *p_to
 
 void launch_merged_total(const u64 *a_total, const u64 *new_total, const u64 *pair_total,
                          const MergeArgs &a, Status *host, u32 seq, hipStream_t s) {
-  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(1024), 0, s, a_total, new_total, pair_total,
+  // one wave unless there are many merge tiles to sum
+  const unsigned nt = a.ntiles > 4096 ? 1024 : kWave;
+  hipLaunchKernelGGL(k_merged_total, dim3(1), dim3(nt), 0, s, a_total, new_total, pair_total,
                      a.st, a, host, seq);
 }
 
