@@ -61,6 +61,9 @@ void *Buf::ensure(size_t bytes) {
 // Growth factor of the grow-only arrays: 4 while they are small (fewer and
 // smaller copies of what they hold), 2 from kFastGrowBytes on.
 constexpr size_t kFastGrowBytes = size_t(1) << 28;
+// Largest state or result arrays sized from the level's bounds (see the
+// early append in the level loop).
+constexpr u64 kEarlyBytes = u64(1) << 30;
 inline size_t grown(size_t cap_bytes) { return cap_bytes * (cap_bytes < kFastGrowBytes ? 4 : 2); }
 
 void *Buf::grow_keep(size_t bytes, size_t used) {
@@ -580,6 +583,26 @@ void Composer::run(fstc_result *out) {
     u64 RB = 0;
     u32 nnew = 0;
     u64 merged = 0;
+    // (a7) the level's merged arcs appended to the result: at most M of them
+    auto append = [&](u64 M) {
+      if (!M) return;
+      out_arcs.grow(arcs + M, arcs);
+      u32 *osrc = out_arcs.col(0) + arcs, *odst = out_arcs.col(1) + arcs,
+          *oil = out_arcs.col(2) + arcs, *ool = out_arcs.col(3) + arcs;
+      float *ow = reinterpret_cast<float *>(out_arcs.col(4)) + arcs;
+      if (nprod)  // product-merge sources interleave with the tiles' sources
+        launch_compact_sources(ma, aoff.as<u64>(), M, hvb.as<u32>(), osrc, odst, oil, ool, ow, s);
+      else
+        launch_compact(ma, aoff.as<u64>(), nbig, M, hvb.as<u32>(), osrc, odst, oil, ool, ow, s);
+    };
+    // Early append: when the capacities they need, bounded since the first
+    // synchronisation, are small, id assignment and the result append go to
+    // the stream before the host reads the level's totals, and the GPU runs
+    // them while the host waits (deterministic ids and an arc cap need the
+    // exact counts first).
+    const bool early = !o.no_reduction && !o.deterministic_ids && !o.max_arcs &&
+                       (n_states + newcap) * 8 <= kEarlyBytes &&
+                       (arcs + R + prodpos) * 20 <= kEarlyBytes;
     if (!o.no_reduction) {
       T.at(kMerge);
       if (R) {
@@ -634,6 +657,15 @@ void Composer::run(fstc_result *out) {
       const u32 seq2 = next_publication();
       launch_merged_total(aoff.as<u64>() + nsrc, new_total, ptot.as<u64>() + nsrc, ma, hs_dev,
                           seq2, s);
+      if (early) {
+        T.at(kAssign);
+        sq1b.grow_keep((n_states + newcap) * 4, n_states * 4);
+        sq2b.grow_keep((n_states + newcap) * 4, n_states * 4);
+        launch_assign_counted(newlist.as<u32>(), new_total, (u32)newcap, (u32)n_states,
+                              hkb.as<u64>(), hvb.as<u32>(), vn2, sq1b.as<u32>(), sq2b.as<u32>(),
+                              s);
+        append(R + prodpos);
+      }
       T.at(kNone);
       wait_published(seq2);
       status_clear = true;  // k_merged_total cleared the level counters
@@ -675,39 +707,32 @@ void Composer::run(fstc_result *out) {
     if (!o.no_reduction && o.max_arcs && arcs + merged > o.max_arcs)
       throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");
 
-    // (a5) ids for the new pairs; (a7) append the level's arcs
-    T.at(kAssign);
+    // (a5) ids for the new pairs; (a7) append the level's arcs (done above
+    // for an early append)
     const u64 ns_new = n_states + nnew;
-    sq1b.grow_keep(ns_new * 4, n_states * 4);
-    sq2b.grow_keep(ns_new * 4, n_states * 4);
-    const u32 *slots = newlist.as<u32>();
-    if (o.deterministic_ids && nnew > 1) {
-      const int bq1 = (int)bits_for(m1.num_states - 1), bq2 = (int)bits_for(m2.num_states - 1);
-      dk.ensure((u64)nnew * 8); dv.ensure((u64)nnew * 4);
-      dka.ensure((u64)nnew * 8); dva.ensure((u64)nnew * 4);
-      dtmp.ensure(radix_temp_bytes(nnew));
-      launch_newkeys(newlist.as<u32>(), nnew, hkb.as<u64>(), vn2, bq2, dk.as<u64>(), dv.as<u32>(), s);
-      radix_sort_pairs(dk.as<u64>(), dv.as<u32>(), dka.as<u64>(), dva.as<u32>(), nnew, 0,
-                       bq1 + bq2, dtmp.p, s);
-      slots = dv.as<u32>();
-    }
-    launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), vn2, sq1b.as<u32>(),
-                  sq2b.as<u32>(), s);
-    if (o.no_reduction) {
-      launch_fix_dst(out_arcs.col(1) + arcs, merged, hvb.as<u32>(), s);
-    } else if (merged) {
-      out_arcs.grow(arcs + merged, arcs);
-      u32 *osrc = out_arcs.col(0) + arcs, *odst = out_arcs.col(1) + arcs,
-          *oil = out_arcs.col(2) + arcs, *ool = out_arcs.col(3) + arcs;
-      float *ow = reinterpret_cast<float *>(out_arcs.col(4)) + arcs;
-      if (nprod)  // product-merge sources interleave with the tiles' sources
-        launch_compact_sources(ma, aoff.as<u64>(), merged, hvb.as<u32>(), osrc, odst, oil, ool,
-                               ow, s);
+    if (!early) {
+      T.at(kAssign);
+      sq1b.grow_keep(ns_new * 4, n_states * 4);
+      sq2b.grow_keep(ns_new * 4, n_states * 4);
+      const u32 *slots = newlist.as<u32>();
+      if (o.deterministic_ids && nnew > 1) {
+        const int bq1 = (int)bits_for(m1.num_states - 1), bq2 = (int)bits_for(m2.num_states - 1);
+        dk.ensure((u64)nnew * 8); dv.ensure((u64)nnew * 4);
+        dka.ensure((u64)nnew * 8); dva.ensure((u64)nnew * 4);
+        dtmp.ensure(radix_temp_bytes(nnew));
+        launch_newkeys(newlist.as<u32>(), nnew, hkb.as<u64>(), vn2, bq2, dk.as<u64>(), dv.as<u32>(), s);
+        radix_sort_pairs(dk.as<u64>(), dv.as<u32>(), dka.as<u64>(), dva.as<u32>(), nnew, 0,
+                         bq1 + bq2, dtmp.p, s);
+        slots = dv.as<u32>();
+      }
+      launch_assign(slots, nnew, (u32)n_states, hkb.as<u64>(), hvb.as<u32>(), vn2, sq1b.as<u32>(),
+                    sq2b.as<u32>(), s);
+      if (o.no_reduction)
+        launch_fix_dst(out_arcs.col(1) + arcs, merged, hvb.as<u32>(), s);
       else
-        launch_compact(ma, aoff.as<u64>(), nbig, merged, hvb.as<u32>(), osrc, odst, oil, ool, ow,
-                       s);
+        append(merged);
+      T.at(kNone);
     }
-    T.at(kNone);
     arcs += merged;
     n_states = ns_new;
     if (nnew) ++new_levels;

@@ -221,6 +221,11 @@ void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32
 // ids base .. base + nnew - 1 in new-list order (or the order in `order`).
 void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 vn2,
                    u32 *sq1, u32 *sq2, hipStream_t s);
+// The same for min(*count, cap) new pairs, the count read on the device
+// (the host need not know it yet); nothing when count is NULL.
+void launch_assign_counted(const u32 *slots, const u64 *count, u32 cap, u32 base,
+                           const u64 *hkeys, u32 *hvals, u32 vn2, u32 *sq1, u32 *sq2,
+                           hipStream_t s);
 void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, u32 vn2, int bq2, u64 *keys,
                     u32 *vals, hipStream_t s);
 // Result append of the level's merged arcs: the runs of merge tile t go to

@@ -1643,20 +1643,23 @@ __global__ void k_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkey
   }
 }
 
-__global__ void k_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals,
-                         u32 vn2, u32 *sq1, u32 *sq2) {
-  const u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= nnew) return;
-  const u32 slot = slots[i];
-  const u32 id = base + (u32)i;
-  hvals[slot] = id;
-  if (vn2) {
-    sq1[id] = slot / vn2;
-    sq2[id] = slot % vn2;
-  } else {
-    const u64 k = hkeys[slot];
-    sq1[id] = (u32)(k >> 32);
-    sq2[id] = (u32)k;
+// New pair i of the list gets id base + i: i < nnew, or i < min(*count,
+// nnew) when count is given (nnew is then the list's capacity).
+__global__ void k_assign(const u32 *slots, u32 nnew, const u64 *count, u32 base,
+                         const u64 *hkeys, u32 *hvals, u32 vn2, u32 *sq1, u32 *sq2) {
+  const u64 n = count ? min<u64>(*count, nnew) : nnew;
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
+    const u32 slot = slots[i];
+    const u32 id = base + (u32)i;
+    hvals[slot] = id;
+    if (vn2) {
+      sq1[id] = slot / vn2;
+      sq2[id] = slot % vn2;
+    } else {
+      const u64 k = hkeys[slot];
+      sq1[id] = (u32)(k >> 32);
+      sq2[id] = (u32)k;
+    }
   }
 }
 
@@ -1960,7 +1963,16 @@ void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *
                    u32 *sq1, u32 *sq2, hipStream_t s) {
   if (!nnew) return;
   hipLaunchKernelGGL(k_assign, dim3((unsigned)ceil_div(nnew, 256)), dim3(256), 0, s, slots, nnew,
-                     base, hkeys, hvals, vn2, sq1, sq2);
+                     (const u64 *)nullptr, base, hkeys, hvals, vn2, sq1, sq2);
+}
+
+void launch_assign_counted(const u32 *slots, const u64 *count, u32 cap, u32 base,
+                           const u64 *hkeys, u32 *hvals, u32 vn2, u32 *sq1, u32 *sq2,
+                           hipStream_t s) {
+  if (!count || !cap) return;
+  const unsigned g = (unsigned)std::min<u64>(ceil_div(cap, 256), 2048);
+  hipLaunchKernelGGL(k_assign, dim3(g), dim3(256), 0, s, slots, cap, count, base, hkeys, hvals,
+                     vn2, sq1, sq2);
 }
 
 void launch_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, u32 vn2, int bq2, u64 *keys,
