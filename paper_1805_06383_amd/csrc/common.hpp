@@ -103,6 +103,20 @@ __device__ __forceinline__ u32 wave_total(u32 x) {
   return (u32)__builtin_amdgcn_readlane((int)x, 63);
 }
 
+// Inclusive prefix sum of x over the 64 lanes of a wave whose lanes are all
+// active: prefixes within each row of 16 by DPP row shifts (zeros shifted
+// in), then the row totals carried by the broadcasts of lane 15 (to rows 1
+// and 3) and lane 31 (to rows 2 and 3).
+__device__ __forceinline__ u32 wave_inclusive_total(u32 x) {
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (u32)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 // Bitwise OR of x over the 64 lanes of a wave whose lanes are all active,
 // returned to every lane (the pattern of wave_total).
 __device__ __forceinline__ u32 wave_or(u32 x) {

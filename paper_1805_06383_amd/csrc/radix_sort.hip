@@ -64,23 +64,33 @@ __global__ __launch_bounds__(kNT) void k_digit_scatter(const u64 *keys, const u3
 }
 
 // Exclusive scan of a digit histogram of at most kScan1Max entries by one
-// workgroup (one launch instead of a multi-level scan): thread t scans
-// entries [t c, t c + c) with c = ceil(nh / kScan1NT).
+// workgroup (one launch instead of a multi-level scan).  Wave w owns the
+// entries [w S, w S + S), S a multiple of 64: it sums them in coalesced
+// 64-entry chunks, the waves' totals are combined in LDS, and a second pass
+// over the chunks writes each entry's offset from a DPP prefix sum plus the
+// running carry.
 constexpr int kScan1NT = 1024;
 constexpr u64 kScan1Max = 1u << 16;
 
 __global__ __launch_bounds__(kScan1NT) void k_hist_scan1(const u32 *hist, u32 *offs, u32 nh) {
-  __shared__ u32 scratch[kScan1NT / kWave];
-  const u32 c = (nh + kScan1NT - 1) / kScan1NT;
-  const u32 b = threadIdx.x * c, e = min(nh, b + c);
+  constexpr u32 kWaves = kScan1NT / kWave;
+  __shared__ u32 s_tot[kWaves];
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u32 seg = (nh + kWaves * kWave - 1) / (kWaves * kWave) * kWave;
+  const u32 b = min(nh, w * seg), e = min(nh, b + seg);
   u32 sum = 0;
-  for (u32 i = b; i < e; ++i) sum += hist[i];
-  u32 total;
-  u32 run = block_exclusive_sum<kScan1NT, u32>(sum, scratch, &total);
-  for (u32 i = b; i < e; ++i) {
-    const u32 v = hist[i];
-    offs[i] = run;
-    run += v;
+  for (u32 i = b + lane; i < e; i += kWave) sum += hist[i];
+  sum = wave_total(sum);
+  if (lane == 0) s_tot[w] = sum;
+  __syncthreads();
+  u32 carry = 0;
+  for (u32 k = 0; k < w; ++k) carry += s_tot[k];
+  for (u32 c = b; c < e; c += kWave) {  // wave-uniform bounds: every lane runs every chunk
+    const u32 i = c + lane;
+    const u32 v = i < e ? hist[i] : 0u;
+    const u32 incl = wave_inclusive_total(v);
+    if (i < e) offs[i] = carry + incl - v;
+    carry += (u32)__builtin_amdgcn_readlane((int)incl, kWave - 1);
   }
 }
 
