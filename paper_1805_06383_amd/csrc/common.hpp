@@ -255,10 +255,20 @@ struct ScanJob {
   bool narrow_out = false;    // out holds u32 (sums must fit)
   const u64 *sub = nullptr;   // scans in[i] - sub[i] (in wide)
   bool total_only = false;    // writes out[n] alone
+  u64 *total_to = nullptr;    // the total is also stored here
+};
+// After the last tile has stored the totals: `words` 32-bit words copied
+// from src to dst (host memory the device can write) except word seq_word,
+// a system-scope fence, then dst[seq_word] = seq (a publication the host
+// can wait for).
+struct ScanPublish {
+  const void *src;
+  void *dst;
+  u32 words, seq_word, seq;
 };
 size_t scan_lb_state_bytes(u64 n);
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
-                       hipStream_t s);
+                       hipStream_t s, const ScanPublish *pub = nullptr);
 
 // Three exclusive scans of arrays of the same length at once (out_k has
 // n + 1 entries); `temp` must hold scan3_temp_bytes(n) bytes.

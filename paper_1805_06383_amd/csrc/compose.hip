@@ -293,7 +293,7 @@ struct Composer {
   }
 
   // Waits until a kernel has copied the counters to hs->st and then written
-  // publication number `seq` (launch_level_totals, launch_merged_total): a
+  // publication number `seq` (the count scan's ScanPublish, launch_merged_total): a
   // spin on that word, with a stream query every few thousand reads so that
   // a failed or drained stream ends the wait.
   void wait_published(u32 seq) {
@@ -455,16 +455,21 @@ void Composer::run(fstc_result *out) {
     T.at(kCount);
     launch_count(la, s);
     // records, matches and product-merge entries per source; the product
-    // sources' flags summed
+    // sources' flags summed; the scan's last tile stores the level totals
+    // (R, M, product entries, product sources) and publishes the counters
+    const u32 seq1 = next_publication();
     {
       ScanJob jobs[4] = {{cnt.p, true, roff.as<u64>()}, {mc.p, false, moff.as<u64>()},
                          {pk.p, false, poff.as<u64>()}, {pflag.p, true, ftot.as<u64>()}};
       jobs[3].total_only = true;
-      exclusive_scan_lb(jobs, 4, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+      jobs[0].total_to = &dst->R;
+      jobs[1].total_to = &dst->M;
+      jobs[2].total_to = &dst->prod_entries;
+      jobs[3].total_to = reinterpret_cast<u64 *>(&dst->nprod);  // nprod, nprod_mfma
+      const ScanPublish pub{dst, hs_dev, (u32)(sizeof(Status) / 4), (u32)(offsetof(Status, seq) / 4),
+                            seq1};
+      exclusive_scan_lb(jobs, 4, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, &pub);
     }
-    const u32 seq1 = next_publication();
-    launch_level_totals(roff.as<u64>() + nsrc, moff.as<u64>() + nsrc, poff.as<u64>() + nsrc,
-                        ftot.as<u64>() + nsrc, dst, hs_dev, seq1, s);
     T.at(kNone);
     wait_published(seq1);
     const u64 R = hs->st.R, M = hs->st.M;

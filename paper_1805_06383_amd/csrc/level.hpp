@@ -36,14 +36,17 @@ struct Status {
   u64 dense_runs;     // merged arcs those tiles produced
   u64 sort_runs;      // merged arcs of the tiles merged by sorting
   u32 nsort;          // tiles k_merge_dense left to the sort kernel
-  u32 nprod;          // sources of the product merge
   u32 scan_ctr;       // tile counter of the single-pass scans (0 between scans)
   u32 seq;            // host copy only: number of the last publication, written last
+  u32 pad0;
+  u32 nprod;          // sources of the product merge       } one u64, the total of
+  u32 nprod_mfma;     // of those, summed on the matrix cores } the level's flag words
   u64 prod_records;   // their joined arc pairs (not written as records)
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
-  u32 nprod_mfma;     // product-merge sources summed on the matrix cores
-  u32 pad0;
 };
+static_assert(offsetof(Status, nprod) % 8 == 0 &&
+                  offsetof(Status, nprod_mfma) == offsetof(Status, nprod) + 4,
+              "the flag total is stored as one u64 over nprod, nprod_mfma");
 
 // Product merge (merge.hip, k_prod_sources).  A source (q1, q2) is merged
 // by one wavefront from its staged arc matrices instead of through records
@@ -268,14 +271,10 @@ void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, 
 void launch_fix_dst(u32 *dst, u64 n, const u32 *hvals, hipStream_t s);
 void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, const uint8_t *f2,
                    uint8_t *fin, hipStream_t s);
-// Both also copy *st to `host` (pinned, coherent host memory the device can
-// write) and then set host->seq = seq, so that the host can wait for the
-// copy by watching that word.
-// Level totals after the count scan: records *r_total, matches *m_total,
-// product-merge entries *p_total, and *f_total (the sum of pflag: product
-// sources in the low, matrix-core ones in the high 32 bits).
-void launch_level_totals(const u64 *r_total, const u64 *m_total, const u64 *p_total,
-                         const u64 *f_total, Status *st, Status *host, u32 seq, hipStream_t s);
+// It also copies *st to `host` (pinned, coherent host memory the device can
+// write) and then sets host->seq = seq, so that the host can wait for the
+// copy by watching that word (the count scan's last tile does the same
+// after the level's first phase, ScanPublish).
 // Level total of merged arcs, new pairs (*new_total, when not NULL), the
 // product merge's joined pairs (*pair_total: the sum of a.pcnt over the
 // level's sources, records included, less st->R) and the dense / sort tile

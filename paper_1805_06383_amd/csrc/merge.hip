@@ -1766,16 +1766,6 @@ __device__ __forceinline__ void clear_level(Status *st) {
   st->nsort = 0;
 }
 
-__global__ void k_level_totals(const u64 *rt, const u64 *mt, const u64 *pt, const u64 *ft,
-                               Status *st, Status *host, u32 seq) {
-  st->R = *rt;
-  st->M = *mt;
-  st->prod_entries = *pt;
-  const u64 f = *ft;
-  st->nprod = (u32)f;
-  st->nprod_mfma = (u32)(f >> 32);
-  publish(st, host, seq, 0, 1);
-}
 
 // Level totals after the merge: merged arcs (end of the scan of merged arcs
 // per source), new pairs (end of the scan of the new-pair lists), the
@@ -2025,11 +2015,6 @@ void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, con
   hipLaunchKernelGGL(k_finals, dim3(grid1(n)), dim3(256), 0, s, sq1, sq2, n, f1, f2, fin);
 }
 
-void launch_level_totals(const u64 *r_total, const u64 *m_total, const u64 *p_total,
-                         const u64 *f_total, Status *st, Status *host, u32 seq, hipStream_t s) {
-  hipLaunchKernelGGL(k_level_totals, dim3(1), dim3(1), 0, s, r_total, m_total, p_total, f_total,
-                     st, host, seq);
-}
 
 void launch_merged_total(const u64 *a_total, const u64 *new_total, const u64 *pair_total,
                          const MergeArgs &a, Status *host, u32 seq, hipStream_t s) {

@@ -197,6 +197,8 @@ struct LbArgs {
   u32 narrow;  // bit k: out[k] holds u32
   u32 tonly;   // bit k: only out[k][n] is written
   const u64 *sub[kLbMax];
+  u64 *total_to[kLbMax];
+  ScanPublish pub;  // pub.dst == NULL: none
   u64 n;
   u32 nb, epoch;
   u32 *flags;   // [nb]
@@ -304,7 +306,22 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         s_off[k] = off[k];
-        if (t == p.nb - 1) put_out(p, k, p.n, off[k] + tot[k]);
+        if (t == p.nb - 1) {
+          put_out(p, k, p.n, off[k] + tot[k]);
+          if (p.total_to[k]) *p.total_to[k] = off[k] + tot[k];
+        }
+      }
+      if (t == p.nb - 1 && p.pub.dst) {
+        // every other tile has published its inclusive prefix: the totals
+        // are final
+        const u32 *src = static_cast<const u32 *>(p.pub.src);
+        u32 *dst = static_cast<u32 *>(p.pub.dst);
+        __threadfence();
+        for (u32 i = 0; i < p.pub.words; ++i)
+          if (i != p.pub.seq_word) dst[i] = src[i];
+        __threadfence_system();
+        __hip_atomic_store(&dst[p.pub.seq_word], p.pub.seq, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_SYSTEM);
       }
     }
   }
@@ -389,7 +406,7 @@ size_t scan_lb_state_bytes(u64 n) {
 }
 
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
-                       hipStream_t s) {
+                       hipStream_t s, const ScanPublish *pub) {
   static std::atomic<u32> epochs{0};
   const u64 nb = std::max<u64>(1, ceil_div(n, kLbTile));
   if (nb >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "scan too large for one launch");
@@ -404,7 +421,9 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
     p.narrow |= (jobs[i].narrow_out ? 1u : 0u) << i;
     p.tonly |= (jobs[i].total_only ? 1u : 0u) << i;
     p.sub[i] = jobs[i].sub;
+    p.total_to[i] = jobs[i].total_to;
   }
+  if (pub) p.pub = *pub;
   p.n = n;
   p.nb = (u32)nb;
   u32 e = (epochs.fetch_add(1, std::memory_order_relaxed) + 1) & 0x3fffffffu;
