@@ -102,7 +102,9 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 // (a 64-bit mask of the parts), flags the state (bit 0).  For the other
 // states the word also summarises the arcs' weights (kCellSpecial: a
 // non-finite or subnormal weight; the largest biased float32 exponent of a
-// nonzero weight at kCellEmaxShift, the smallest at kCellEminShift).
+// nonzero weight at kCellEmaxShift, the smallest at kCellEminShift) and
+// marks a state of P parts, S segments and P S arcs kCellDense (no segment
+// has more than P arcs, so each has exactly P).
 __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *arcs,
                              const u32 *part_base, u32 nq, u32 *flag) {
   const u32 lane = lane_id();
@@ -134,9 +136,12 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
     const bool any = __ballot(bad) != 0, spec = __ballot(special) != 0;
     emax = wave_max(emax);
     emin = 255u - wave_max(255u - emin);
+    const u32 P = part_base[q + 1] - part_base[q], r0 = row[q], r1 = row[q + 1];
+    const bool dense = (u64)(seg_off[r1] - seg_off[r0]) == (u64)P * (r1 - r0);
     if (lane == 0)
       flag[q] = any ? kCellBad
-                    : (spec ? kCellSpecial : 0u) | (emax << kCellEmaxShift) | (emin << kCellEminShift);
+                    : (spec ? kCellSpecial : 0u) | (dense ? kCellDense : 0u) |
+                          (emax << kCellEmaxShift) | (emin << kCellEminShift);
   }
 }
 

@@ -95,9 +95,12 @@ __device__ __forceinline__ bool products_normal(u32 f1, u32 f2) {
 
 // Product-merge selection of source u (level.hpp) from what the count
 // already loaded: table entries P1 P2 and the source header written to
-// phdr, or 0 (record path).  The header's last word selects the matrix-core
-// form (at most kProdMfmaParts parts per state, products_normal).  The
-// cells are single-arc only for states of at most kProdParts parts.
+// phdr, or 0 (record path).  The header's last word holds the matrix-core
+// form (bit 0: at most kProdMfmaParts parts per state, products_normal) and
+// the aligned form (bit 1; both states kCellDense with symbol lists of one
+// length n, at bit 8): the second header word is then (M1 segment begin, its
+// first arc, M2 segment begin, its first arc).  The cells are single-arc
+// only for states of at most kProdParts parts.
 __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1, u32 q2,
                                               const Ranges &r, bool &mfma) {
   const u32 f1 = a.c1.cell_flag[q1], f2 = a.c2.cell_flag[q2];
@@ -106,8 +109,12 @@ __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1,
   const u32 pb2 = a.c2.part_base[q2], p2 = a.c2.part_base[q2 + 1] - pb2;
   if (p1 == 0 || p2 == 0 || p1 + p2 > kProdRowSum) return 0;
   mfma = p1 <= kProdMfmaParts && p2 <= kProdMfmaParts && products_normal(f1, f2);
-  a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16), mfma ? 1u : 0u);
-  a.phdr[2 * u + 1] = make_uint4(r.b1, r.e1, r.b2, r.e2);
+  const u32 n = r.e1 - r.b1;
+  const bool aligned = mfma && (f1 & f2 & kCellDense) && n == r.e2 - r.b2;
+  a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16),
+                             (mfma ? 1u : 0u) | (aligned ? 2u | (n << 8) : 0u));
+  a.phdr[2 * u + 1] = aligned ? make_uint4(r.b1, a.c1.seg_off[r.b1], r.b2, a.c2.seg_off[r.b2])
+                              : make_uint4(r.b1, r.e1, r.b2, r.e2);
   return p1 * p2;
 }
 

@@ -15,7 +15,7 @@ struct CsrView {
   const u32 *part_base;
   const uint2 *parts;
   u64 num_arcs;
-  const u32 *cell_flag;  // [num_states] nonzero: the state cannot take the product merge
+  const u32 *cell_flag;  // [num_states] build_cell_flags; kCellBad: no product merge
 };
 
 inline CsrView view(const Csr &c) {

@@ -931,12 +931,17 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   if (K == 0) return;  // whole wave: record path
   u32 *val = s_val[w];
   const u32 pb1 = uni(h0.x), pb2 = uni(h0.y), P1 = uni(h0.z & 0xffffu), P2 = uni(h0.z >> 16);
-  const u32 b1 = uni(h1.x), e1 = uni(h1.y), b2 = uni(h1.z), e2 = uni(h1.w);
-  const bool mf = uni(h0.w) != 0;  // matrix-core form
+  const u32 hf = uni(h0.w);
+  const bool mf = (hf & 1u) != 0;       // matrix-core form
+  const bool aligned = (hf & 2u) != 0;  // dense states, lists of one length na
+  const u32 na = hf >> 8;
+  const u32 b1 = uni(h1.x), b2 = uni(h1.z);
+  const u32 e1 = aligned ? b1 + na : uni(h1.y), e2 = aligned ? b2 + na : uni(h1.w);
+  const u32 ab1 = aligned ? uni(h1.y) : 0u, ab2 = aligned ? uni(h1.w) : 0u;  // first arcs
   const bool one_short = (e1 - b1) <= (e2 - b2);
   const u32 bs = one_short ? b1 : b2, es = one_short ? e1 : e2;
   if (P1 * P2 != K || P1 + P2 > kProdRowSum || es <= bs || es - bs > (u32)kWave ||
-      (mf && (P1 > kProdRow || P2 > kProdRow))) {
+      (mf && (P1 > kProdRow || P2 > kProdRow)) || (aligned && !mf)) {
     // impossible: the selection checked all of it
     if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
@@ -987,44 +992,64 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   //    over by the lane that found the match), so the arc loads follow the
   //    join without another round trip.  Loads are unconditional, from
   //    indexes clamped into the lists, and their values selected after.
-  const u32 idx = bs + lane;
-  const bool valid = idx < es;
-  const u32 ic = valid ? idx : es - 1;
-  const u32 sym0 = ssym[ic], so0 = soffs[ic], so1 = soffs[ic + 1];
-  const u32 sym = valid ? sym0 : 0xffffffffu;  // labels are below 2^32 - 1
-  const u32 sa = valid ? so0 : 0u, sn = valid ? so1 - so0 : 0u;
-  const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
-  const u64 vmask = __ballot(valid);
-  bool found = false;
-  u32 la = 0, ln = 0;
-  for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
-    const u32 len = min(le - cb, (u32)kWave);
-    const bool in = lane < len;
-    const u32 lc = cb + min(lane, len - 1);
-    const u32 lv0 = lsym[lc], lo00 = loffs[lc], lo10 = loffs[lc + 1];
-    const u32 lv = in ? lv0 : 0xffffffffu, lo0 = in ? lo00 : 0u, lo1 = in ? lo10 : 0u;
-    if (__ballot(valid && lv == sym) == vmask) {
-      // the chunk starts with the short list's symbols: lane i matches lane i
-      found = valid;
-      la = lo0;
-      ln = lo1 - lo0;
-      break;
-    }
-    if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
-    u32 pos = 0;  // elements of the chunk below sym
+  //    Aligned form: lane g takes symbol g of both lists, whose arcs are the
+  //    P1 (P2) consecutive ones from ab1 + P1 g (ab2 + P2 g); symbols and
+  //    arcs are loaded together and the arcs used once every lane's two
+  //    symbols agree (else the join below runs as for other sources).
+  bool found = false, staged = false;
+  u32 sa = 0, sn = 0, la = 0, ln = 0;
+  uint2 x1[kProdBatch], x2[kProdBatch];
+  if (aligned) {
+    const bool v = lane < na;
+    const u32 g = v ? lane : 0u;
+    const u32 s1 = a.seg_sym1[b1 + g], s2 = a.seg_sym2[b2 + g];
 #pragma unroll
-    for (u32 step = kWave / 2; step; step >>= 1) {
-      const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
-      pos = v < sym ? pos + step : pos;
+    for (int k = 0; k < kProdBatch; ++k) {
+      x1[k] = prod_arc<NARROW>(a.arcs1, ab1 + P1 * g + (u32)k);
+      x2[k] = prod_arc<NARROW>(a.arcs2, ab2 + P2 * g + (u32)k);
     }
-    const u32 at = __shfl(lv, (int)pos, kWave);
-    const u32 pa = __shfl(lo0, (int)pos, kWave), pe = __shfl(lo1, (int)pos, kWave);
-    if (valid && at == sym) {
-      found = true;
-      la = pa;
-      ln = pe - pa;
+    staged = __ballot(v && s1 == s2) == __ballot(v);
+    found = staged && v;
+  }
+  if (!staged) {
+    const u32 idx = bs + lane;
+    const bool valid = idx < es;
+    const u32 ic = valid ? idx : es - 1;
+    const u32 sym0 = ssym[ic], so0 = soffs[ic], so1 = soffs[ic + 1];
+    const u32 sym = valid ? sym0 : 0xffffffffu;  // labels are below 2^32 - 1
+    sa = valid ? so0 : 0u;
+    sn = valid ? so1 - so0 : 0u;
+    const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
+    const u64 vmask = __ballot(valid);
+    for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
+      const u32 len = min(le - cb, (u32)kWave);
+      const bool in = lane < len;
+      const u32 lc = cb + min(lane, len - 1);
+      const u32 lv0 = lsym[lc], lo00 = loffs[lc], lo10 = loffs[lc + 1];
+      const u32 lv = in ? lv0 : 0xffffffffu, lo0 = in ? lo00 : 0u, lo1 = in ? lo10 : 0u;
+      if (__ballot(valid && lv == sym) == vmask) {
+        // the chunk starts with the short list's symbols: lane i matches lane i
+        found = valid;
+        la = lo0;
+        ln = lo1 - lo0;
+        break;
+      }
+      if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
+      u32 pos = 0;  // elements of the chunk below sym
+  #pragma unroll
+      for (u32 step = kWave / 2; step; step >>= 1) {
+        const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
+        pos = v < sym ? pos + step : pos;
+      }
+      const u32 at = __shfl(lv, (int)pos, kWave);
+      const u32 pa = __shfl(lo0, (int)pos, kWave), pe = __shfl(lo1, (int)pos, kWave);
+      if (valid && at == sym) {
+        found = true;
+        la = pa;
+        ln = pe - pa;
+      }
+      if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
     }
-    if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
   }
   u32 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol (parts < 16)
   bool bad = false;
@@ -1034,8 +1059,9 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     *reinterpret_cast<uint4 *>(&val[lane * kProdRow]) = make_uint4(0, 0, 0, 0);
     *reinterpret_cast<uint4 *>(&val[(kWave + lane) * kProdRow]) = make_uint4(0, 0, 0, 0);
   }
-  const u32 a1 = one_short ? sa : la, n1 = found ? (one_short ? sn : ln) : 0u;
-  const u32 a2 = one_short ? la : sa, n2 = found ? (one_short ? ln : sn) : 0u;
+  const u32 a1 = one_short ? sa : la, a2 = one_short ? la : sa;
+  const u32 n1 = !found ? 0u : staged ? P1 : one_short ? sn : ln;
+  const u32 n2 = !found ? 0u : staged ? P2 : one_short ? ln : sn;
   // arc k of each side is present when k < h (k in the batch); a present
   // arc's part is below P (else the source is malformed); an absent one
   // writes the spare cell
@@ -1057,18 +1083,18 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     // match; the arc arrays have kArcTail spare entries), those past the
     // segment's end replaced by padding
     static_assert(kProdBatch <= (int)kArcTail, "segment loads stay inside the arc arrays");
-    const u32 f1 = n1 ? a1 : 0u, f2 = n2 ? a2 : 0u;
-    uint2 x1[kProdBatch], x2[kProdBatch];
+    if (!staged) {
+      const u32 f1 = n1 ? a1 : 0u, f2 = n2 ? a2 : 0u;
 #pragma unroll
-    for (int k = 0; k < kProdBatch; ++k) {
-      x1[k] = prod_arc<NARROW>(a.arcs1, f1 + (u32)k);
-      x2[k] = prod_arc<NARROW>(a.arcs2, f2 + (u32)k);
+      for (int k = 0; k < kProdBatch; ++k) {
+        x1[k] = prod_arc<NARROW>(a.arcs1, f1 + (u32)k);
+        x2[k] = prod_arc<NARROW>(a.arcs2, f2 + (u32)k);
+      }
     }
     bad |= (n1 > kProdRow) | (n2 > kProdRow);
     stage(x1, x2, n1, n2);
   } else if (found) {
     for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
-      uint2 x1[kProdBatch], x2[kProdBatch];
 #pragma unroll
       for (int k = 0; k < kProdBatch; ++k) {
         const u32 i = i0 + (u32)k;

@@ -228,3 +228,28 @@ def test_product_out_of_range_products(fstc, case):
     fin = np.isfinite(ref.w)
     err = np.abs(gc.w[fin].astype(np.float64) - ref.w[fin].astype(np.float64))
     assert (err <= 1e-5 * np.abs(ref.w[fin].astype(np.float64)) + 2.0 ** -149).all()
+
+
+def drop_inner(m, every, shift, inner_is_output):
+    """m without the arcs of states q % every == 0 whose inner symbol is
+    (q + shift) % 64: those states keep one arc per part in each remaining
+    segment (still dense) but miss one inner symbol."""
+    inner = m.olabel if inner_is_output else m.ilabel
+    keep = ~((m.src % every == 0) & (inner == (m.src + shift) % 64))
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, m.src[keep], m.dst[keep],
+                 m.ilabel[keep], m.olabel[keep], m.weight[keep], m.final)
+
+
+def test_product_aligned_lists_differ(fstc):
+    """Dense states whose symbol lists have one length but differ (each
+    misses another symbol): the aligned form's check fails and the source is
+    joined by search; sources whose lists agree take the aligned form.  Same
+    result as the record path and the oracle."""
+    m1, m2 = W.config4(0)
+    m1 = drop_inner(m1, 7, 0, True)
+    m2 = drop_inner(m2, 5, 1, False)
+    pr = product_vs_records(fstc, m1, m2, "config4 missing symbols cap 4", max_levels=4)
+    st = pr.stats
+    assert st["total_product_mfma_sources"] == st["total_product_sources"] > 0
+    assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2, max_levels=4)),
+                rtol=RTOL, what="config4 missing symbols cap 4")
