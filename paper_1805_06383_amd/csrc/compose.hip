@@ -419,7 +419,8 @@ void Composer::run(fstc_result *out) {
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),
-      aoff(&level_tmp), pk(&level_tmp), pflag(&level_tmp), ftot(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      aoff(&level_tmp), pk(&level_tmp), pflag(&level_tmp), ftot(&level_tmp), newc(&level_tmp),
+      newoff(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -439,7 +440,8 @@ void Composer::run(fstc_result *out) {
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
     ptot.ensure(np1 * 8); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
-    pk.ensure(np1 * 4); poff.ensure(np1 * 8); pflag.ensure(np1 * 8); ftot.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
+    pk.ensure(np1 * 4); poff.ensure(np1 * 8); pflag.ensure(np1 * 8); ftot.ensure(np1 * 8);
+    newc.ensure(np1 * 4); newoff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     wrange.ensure(np1 * sizeof(uint4));
     stmp.ensure(scan3_temp_bytes(np1));
 
@@ -452,6 +454,7 @@ void Composer::run(fstc_result *out) {
                  dst, nullptr, nullptr, nullptr, big.as<u32>(), pk.as<u32>(), phdr.as<uint4>(),
                  product ? 1u : 0u, tstart.as<u64>(), mend.as<u64>()};
     la.pflag = pflag.as<u64>();
+    la.newc = newc.as<u32>();
     T.at(kCount);
     launch_count(la, s);
     // records, matches and product-merge entries per source; the product
@@ -577,6 +580,7 @@ void Composer::run(fstc_result *out) {
     ma.pk = pk.as<u32>();
     ma.phdr = phdr.as<uint4>();
     ma.pcnt = cnt.as<u64>();  // product-merge sources have no records: their slots are free
+    ma.newc = newc.as<u32>();
     ma.poff = poff.as<u64>();
     ma.prodpos = prodpos;
     ma.row1 = c1.row;
@@ -647,18 +651,28 @@ void Composer::run(fstc_result *out) {
       // merged arcs per source (mend - tstart) scanned into result offsets;
       // the per-source joined pairs (records, or the product merge's terms)
       // summed for the level's product-merge pairs
+      // (on a level of product-merge sources alone, also the new pairs
+      // each source claimed, for the new-pair list)
+      const bool prod_only = R == 0;
       {
-        ScanJob jobs[2] = {{mend.p, true, aoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()}};
+        ScanJob jobs[3] = {{mend.p, true, aoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()},
+                           {newc.p, false, newoff.as<u64>()}};
         jobs[0].sub = tstart.as<u64>();
         jobs[1].total_only = true;
-        exclusive_scan_lb(jobs, 2, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+        exclusive_scan_lb(jobs, prod_only ? 3 : 2, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
       }
       launch_emit_tiles(ma, s);
-      const u64 nw = newlist_waves(ma, RB);
-      wcnt.ensure(nw * 4);
-      woff.ensure((nw + 1) * 8);
-      const u64 *new_total = launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB,
-                                            wcnt.as<u32>(), woff.as<u64>(), lb(nw), s);
+      const u64 *new_total = nullptr;
+      if (prod_only) {
+        launch_newlist_sources(ma, newoff.as<u64>(), s);
+        new_total = newoff.as<u64>() + nsrc;
+      } else {
+        const u64 nw = newlist_waves(ma, RB);
+        wcnt.ensure(nw * 4);
+        woff.ensure((nw + 1) * 8);
+        new_total = launch_newlist(ma, nbig ? bigoff.as<u64>() : nullptr, nbig, RB,
+                                   wcnt.as<u32>(), woff.as<u64>(), lb(nw), s);
+      }
       const u32 seq2 = next_publication();
       launch_merged_total(aoff.as<u64>() + nsrc, new_total, ptot.as<u64>() + nsrc, ma, hs_dev,
                           seq2, s);

@@ -148,6 +148,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     const u32 q1 = a.sq1[sid], q2 = a.sq2[sid];
     a.tstart[u] = 0;
     a.mend[u] = 0;
+    a.newc[u] = 0;
     r = Ranges{a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]};
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
     if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r, mf);

@@ -130,6 +130,8 @@ struct LevelArgs {
   u32 prod;              // nonzero: sources may take the product merge
   u64 *tstart, *mend;    // [nsrc] the merge's first / end temp slot per source:
                          // zeroed by the count kernel
+  u32 *newc;             // [nsrc] new pairs claimed per source: zeroed by the count
+                         // kernel, written by the product merge
   u64 *pflag;            // [nsrc] 1 for a product-merge source, plus 2^32 when it
                          // takes the matrix-core form (summed by the level scan)
 };
@@ -193,6 +195,7 @@ struct MergeArgs {
   const u64 *poff;
   u64 prodpos;
   u64 *pcnt;  // [nsrc] joined arc pairs of each product-merge source (written by it)
+  u32 *newc;  // [nsrc] new pairs each product-merge source claimed (written by it)
   const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;
 };
 
@@ -253,6 +256,11 @@ void launch_emit_tiles(const MergeArgs &a, hipStream_t s);
 // scan_state: scan_lb_state_bytes(newlist_waves(a, RB)) bytes of single-pass
 // scan state (see exclusive_scan_lb).
 u64 newlist_waves(const MergeArgs &a, u64 RB);
+// The same list for a level whose sources all took the product merge (no
+// records): newoff, the exclusive scan of a.newc, gives each source's first
+// list entry; 16 lanes per source with claims write its claimed slots in
+// temp order.
+void launch_newlist_sources(const MergeArgs &a, const u64 *newoff, hipStream_t s);
 const u64 *launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt,
                           u64 *woff, void *scan_state, hipStream_t s);
 // Composition without reduction: every record of the level becomes an arc

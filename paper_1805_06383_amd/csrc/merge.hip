@@ -1175,10 +1175,12 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
   const u64 base = a.R + a.poff[u];
+  bool claimed = false;  // this lane's entry claimed a new pair
   if (run && a.vn2) {
     // dense array: the entry read above, then a claim if it was unvisited
     const bool is_new = hcur == kUnvisited &&
                         atomicCAS(&a.vis[hslot], kUnvisited, kClaimed) == kUnvisited;
+    claimed = is_new;
     const u64 t = base + count_below(rm);
     a.temp[t] = make_uint4((u32)hslot | (is_new ? kNewFlag : 0u), L1.y, L2.y,
                            __float_as_uint((float)acc));
@@ -1210,12 +1212,15 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     const u64 t = base + count_below(rm);
     a.temp[t] = make_uint4(slot | (is_new ? kNewFlag : 0u), L1.y, L2.y, __float_as_uint((float)acc));
     a.runsrc[t] = (u32)u;
+    claimed = is_new;
   }
   if (lane >= nr && lane < K) a.temp[base + lane] = make_uint4(0, 0, 0, 0);  // empty slot
+  const u32 nclaim = (u32)__popcll(__ballot(claimed));
   if (lane == 0) {
     a.tstart[u] = base;
     a.mend[u] = base + nr;
     a.pcnt[u] = pairs;
+    a.newc[u] = nclaim;
   }
 }
 
@@ -1559,6 +1564,38 @@ __global__ __launch_bounds__(256) void k_newlist(MergeArgs a, const u64 *bigoff,
     take((x & kNewFlag) != 0, x & ~kNewFlag);
   }
   if (!PASS && lane == 0) wcnt[wv] = cnt;
+}
+
+// New-pair list of a level whose sources all took the product merge: 16
+// lanes per source (a source has at most 64 entries); a source with claims
+// writes the slots of its claimed entries, in temp order, from list entry
+// newoff[u].
+__global__ __launch_bounds__(256) void k_newlist_sources(MergeArgs a, const u64 *newoff) {
+  const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  const u64 u = t / 16;
+  const u32 j = (u32)(t % 16), lane = lane_id();
+  const u32 nc = u < a.nsrc ? a.newc[u] : 0u;
+  if (__ballot(nc != 0) == 0) return;  // whole wave
+  u64 base = 0, n = 0, o = 0;
+  if (nc) {
+    base = a.tstart[u];
+    n = a.mend[u] - base;
+    o = newoff[u];
+  }
+  const u64 gmask = 0xffffull << (lane & ~15u);  // this lane's group of 16
+  u32 done = 0;
+  for (u32 r0 = 0; r0 < (u32)kWave; r0 += 16) {
+    const u64 r = r0 + j;
+    const u32 x = (nc && r < n) ? a.temp[base + r].x : 0u;
+    const bool f = (x & kNewFlag) != 0;
+    const u64 m = __ballot(f) & gmask;
+    if (f) {
+      const u64 pos = o + done + count_below(m);
+      if (pos < a.newcap) a.newlist[pos] = x & ~kNewFlag;
+      else set_error(&a.st->err, kErrNewList);
+    }
+    done += (u32)__popcll(m);
+  }
 }
 
 // Level total of new states (end of the exclusive scan of the per-wave counts).
@@ -1949,6 +1986,12 @@ void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s) {
     hipLaunchKernelGGL(k_prod_sources<true>, dim3(g), dim3(kProdNT), 0, s, a);
   else
     hipLaunchKernelGGL(k_prod_sources<false>, dim3(g), dim3(kProdNT), 0, s, a);
+}
+
+void launch_newlist_sources(const MergeArgs &a, const u64 *newoff, hipStream_t s) {
+  if (!a.nsrc) return;
+  hipLaunchKernelGGL(k_newlist_sources, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256),
+                     0, s, a, newoff);
 }
 
 void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,
