@@ -33,6 +33,10 @@ constexpr u64 kEmptyKey = ~0ull;
 // Set in a merged arc's visited-table slot when its insert claimed the slot
 // (visited-table capacity is at most 2^31 slots).
 constexpr u32 kNewFlag = 0x80000000u;
+// A product-merge temp entry whose target already had an id (dense visited
+// array: ids and slots are below 2^26) holds that id with this flag instead
+// of the slot, so the result append needs no visited-array lookup.
+constexpr u32 kIdFlag = 0x40000000u;
 // Dense visited array entries (ids stay below both).
 constexpr u32 kUnvisited = 0xffffffffu;
 constexpr u32 kClaimed = 0xfffffffeu;

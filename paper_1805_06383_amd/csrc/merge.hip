@@ -1181,9 +1181,10 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     const bool is_new = hcur == kUnvisited &&
                         atomicCAS(&a.vis[hslot], kUnvisited, kClaimed) == kUnvisited;
     claimed = is_new;
+    const bool known = hcur < kClaimed;  // an id from an earlier level
     const u64 t = base + count_below(rm);
-    a.temp[t] = make_uint4((u32)hslot | (is_new ? kNewFlag : 0u), L1.y, L2.y,
-                           __float_as_uint((float)acc));
+    a.temp[t] = make_uint4(known ? ((u32)hcur | kIdFlag) : ((u32)hslot | (is_new ? kNewFlag : 0u)),
+                           L1.y, L2.y, __float_as_uint((float)acc));
     a.runsrc[t] = (u32)u;
   } else if (run) {
     u32 slot = 0;
@@ -1791,7 +1792,7 @@ __global__ __launch_bounds__(256) void k_compact_sources(MergeArgs a, const u64 
     const uint4 rec = a.temp[tb + r];
     const u64 k = ob + r;
     osrc[k] = a.lo + (u32)u;
-    odst[k] = hvals[rec.x & ~kNewFlag];
+    odst[k] = (rec.x & kIdFlag) ? rec.x & ~kIdFlag : hvals[rec.x & ~kNewFlag];
     oil[k] = rec.y;
     ool[k] = rec.z;
     ow[k] = __uint_as_float(rec.w);
