@@ -64,6 +64,8 @@ constexpr size_t kFastGrowBytes = size_t(1) << 28;
 // Largest state or result arrays sized from the level's bounds (see the
 // early append in the level loop).
 constexpr u64 kEarlyBytes = u64(1) << 30;
+// Largest temp (entries x 20 bytes) reserved for a speculative product merge.
+constexpr u64 kSpecBytes = u64(1) << 30;
 inline size_t grown(size_t cap_bytes) { return cap_bytes * (cap_bytes < kFastGrowBytes ? 4 : 2); }
 
 void *Buf::grow_keep(size_t bytes, size_t used) {
@@ -474,6 +476,49 @@ void Composer::run(fstc_result *out) {
       exclusive_scan_lb(jobs, 4, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, &pub);
     }
     T.at(kNone);
+    // Speculative product merge: with the dense visited array (no rehash
+    // between the count and the merge) the product kernel is launched
+    // before the host reads the level's counts, on temp slots reserved for
+    // every source's largest table; it reads the record count on the device
+    // and merges only when the level has no records -- the usual case where
+    // the product merge applies -- so the GPU works through the host's
+    // turnaround.  Otherwise it exits at once and the host launches it again
+    // after the synchronisation.
+    const u64 maxk = std::min<u64>(maxp1 * maxp2, 64);  // a source's table entries
+    const bool spec = product && dense_vis && (u64)nsrc * maxk * 20 <= kSpecBytes;
+    if (spec) {
+      temp.ensure((u64)nsrc * maxk * sizeof(uint4));
+      runsrc.ensure((u64)nsrc * maxk * 4);
+      MergeArgs pm{};  // the fields k_prod_sources reads
+      pm.R = 0;
+      pm.R_dev = roff.as<u64>() + nsrc;
+      pm.nsrc = nsrc;
+      pm.st = dst;
+      pm.pk = pk.as<u32>();
+      pm.phdr = phdr.as<uint4>();
+      pm.poff = poff.as<u64>();
+      pm.parts1 = c1.parts;
+      pm.parts2 = c2.parts;
+      pm.arcs1 = c1.arcs;
+      pm.arcs2 = c2.arcs;
+      pm.seg_sym1 = c1.seg_sym;
+      pm.seg_off1 = c1.seg_off;
+      pm.seg_sym2 = c2.seg_sym;
+      pm.seg_off2 = c2.seg_off;
+      pm.vis = hvb.as<u32>();
+      pm.vn2 = vn2;
+      pm.hkeys = hkb.as<u64>();
+      pm.hmask = hcap - 1;
+      pm.temp = temp.as<uint4>();
+      pm.runsrc = runsrc.as<u32>();
+      pm.tstart = tstart.as<u64>();
+      pm.mend = mend.as<u64>();
+      pm.pcnt = cnt.as<u64>();
+      pm.newc = newc.as<u32>();
+      T.at(kProductKernel);
+      launch_prod_sources(pm, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+      T.at(kNone);
+    }
     wait_published(seq1);
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
@@ -489,7 +534,9 @@ void Composer::run(fstc_result *out) {
     mrbase.ensure(M * 8);
     rkey.ensure(R * rec_bytes);
     rw.ensure(R * 4);
-    if (!o.no_reduction) {
+    // (every ensure takes new arena space: a speculative product merge that
+    // ran keeps the temp and runsrc it wrote)
+    if (!o.no_reduction && !(spec && R == 0)) {
       temp.ensure((R + prodpos) * sizeof(uint4));
       runsrc.ensure((R + prodpos) * 4);
     }
@@ -643,9 +690,11 @@ void Composer::run(fstc_result *out) {
         merge_big(ma, wide_keys, nbig, bigoff.as<u64>(), RB, level_tmp, s);
       }
       if (nprod) {
-        T.at(kProductKernel);
-        launch_prod_sources(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
-        T.at(kMerge);
+        if (!(spec && R == 0)) {  // (else the speculative launch merged them)
+          T.at(kProductKernel);
+          launch_prod_sources(ma, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+          T.at(kMerge);
+        }
         ++product_launches;
       }
       // merged arcs per source (mend - tstart) scanned into result offsets;

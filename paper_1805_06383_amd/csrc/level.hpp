@@ -196,6 +196,8 @@ struct MergeArgs {
   u64 prodpos;
   u64 *pcnt;  // [nsrc] joined arc pairs of each product-merge source (written by it)
   u32 *newc;  // [nsrc] new pairs each product-merge source claimed (written by it)
+  const u64 *R_dev;  // product merge launched before the host knew R: the level's
+                     // record count on the device (the kernel merges only if 0)
   const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;
 };
 

@@ -921,6 +921,9 @@ template <bool NARROW>
 __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   // M1 (g, p1), M2 (g, p2); a spare cell; rows 16-byte aligned
   __shared__ __align__(16) u32 s_val[kProdWaves][kProdCells + 4];
+  // launched before the host read the level's record count: nothing to do
+  // unless the level has no records (then a.R is 0)
+  if (a.R_dev && *a.R_dev != 0) return;
   // everything about the source is wave-uniform: scalar registers
   auto uni = [](u32 x) { return (u32)__builtin_amdgcn_readfirstlane((int)x); };
   const u32 lane = lane_id(), w = uni(threadIdx.x / kWave);
