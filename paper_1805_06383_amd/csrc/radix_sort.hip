@@ -78,19 +78,38 @@ __global__ __launch_bounds__(kScan1NT) void k_hist_scan1(const u32 *hist, u32 *o
   const u32 lane = lane_id(), w = threadIdx.x / kWave;
   const u32 seg = (nh + kWaves * kWave - 1) / (kWaves * kWave) * kWave;
   const u32 b = min(nh, w * seg), e = min(nh, b + seg);
+  // kBatch chunks' loads are issued before any of them is used
+  constexpr u32 kBatch = 8;
   u32 sum = 0;
-  for (u32 i = b + lane; i < e; i += kWave) sum += hist[i];
+  for (u32 c = b; c < e; c += kBatch * kWave) {
+    u32 v[kBatch];
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) {
+      const u32 i = c + q * kWave + lane;
+      v[q] = i < e ? hist[i] : 0u;
+    }
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) sum += v[q];
+  }
   sum = wave_total(sum);
   if (lane == 0) s_tot[w] = sum;
   __syncthreads();
   u32 carry = 0;
   for (u32 k = 0; k < w; ++k) carry += s_tot[k];
-  for (u32 c = b; c < e; c += kWave) {  // wave-uniform bounds: every lane runs every chunk
-    const u32 i = c + lane;
-    const u32 v = i < e ? hist[i] : 0u;
-    const u32 incl = wave_inclusive_total(v);
-    if (i < e) offs[i] = carry + incl - v;
-    carry += (u32)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+  for (u32 c = b; c < e; c += kBatch * kWave) {  // wave-uniform bounds: every lane runs every chunk
+    u32 v[kBatch];
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) {
+      const u32 i = c + q * kWave + lane;
+      v[q] = i < e ? hist[i] : 0u;
+    }
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) {
+      const u32 i = c + q * kWave + lane;
+      const u32 incl = wave_inclusive_total(v[q]);
+      if (i < e) offs[i] = carry + incl - v[q];
+      carry += (u32)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+    }
   }
 }
 
