@@ -891,7 +891,16 @@ __global__ __launch_bounds__(NT, 8) void k_merge_dense(MergeArgs a) {
 // 16 p1 + p2.  Its products are exact in float64, so the merged weight
 // differs from the float32-product sum by at most 2^-24 of the sum of the
 // terms' magnitudes (the selection's normal-range bound) before the
-// final rounding.
+// final rounding.  Entry presence and the joined pairs come from each
+// lane's outer product of its two part masks, reduced by DPP.
+// Aligned form (also in the header; both states dense, symbol lists of one
+// length): step 1's search is replaced by loading symbol g of both lists
+// with the arcs of segment g, found from the states' first arcs alone, and
+// checking afterwards that the lists agree (else step 1 runs as above).
+// A merged arc's temp entry holds the target's slot, with kNewFlag when
+// this entry claimed it, or, with the dense visited array, the target's id
+// with kIdFlag when it had one from an earlier level; the source's claims
+// go to newc[u] for the new-pair list.
 // No LDS is shared between waves, so no workgroup barrier is needed.
 constexpr int kProdNT = 256;
 constexpr int kProdWaves = kProdNT / kWave;
