@@ -274,12 +274,6 @@ size_t scan_lb_state_bytes(u64 n);
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
                        hipStream_t s, const ScanPublish *pub = nullptr);
 
-// Three exclusive scans of arrays of the same length at once (out_k has
-// n + 1 entries); `temp` must hold scan3_temp_bytes(n) bytes.
-size_t scan3_temp_bytes(u64 n);
-void exclusive_scan3(const u64 *in0, u64 *out0, const u32 *in1, u64 *out1, const u32 *in2,
-                     u64 *out2, u64 n, void *temp, hipStream_t s);
-
 // Stable LSD radix sort of (u64 key, u32 value) on key bits [lo, hi).
 // keys/vals hold the input; keys_alt/vals_alt are scratch of the same size;
 // `temp` must hold radix_temp_bytes(n) bytes.  The sorted data ends in

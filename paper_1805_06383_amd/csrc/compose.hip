@@ -445,7 +445,7 @@ void Composer::run(fstc_result *out) {
     pk.ensure(np1 * 4); poff.ensure(np1 * 8); pflag.ensure(np1 * 8); ftot.ensure(np1 * 8);
     newc.ensure(np1 * 4); newoff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     wrange.ensure(np1 * sizeof(uint4));
-    stmp.ensure(scan3_temp_bytes(np1));
+    stmp.ensure(scan_temp_bytes(np1));
 
     // (a2, a3) join counts and offsets
     if (!status_clear) launch_reset_level(dst, s);

@@ -73,105 +73,6 @@ __global__ __launch_bounds__(kScanNT) void k_tile_scan(const TI *in, TO *out, u6
   if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = off + total;
 }
 
-// Three arrays of one length scanned together (array 0 u64, arrays 1 and 2
-// u32, all into u64): the same tiles, one launch per pass for all three.
-struct Scan3 {
-  const u64 *in0;
-  const u32 *in1, *in2;
-  u64 *out0, *out1, *out2;
-};
-
-__device__ __forceinline__ u64 scan3_in(const Scan3 &p, int k, u64 i) {
-  return k == 0 ? p.in0[i] : k == 1 ? (u64)p.in1[i] : (u64)p.in2[i];
-}
-
-// tile_sums[k nb + b] = sum of tile b of array k
-__global__ __launch_bounds__(kScanNT) void k_tile_reduce3(Scan3 p, u64 n, u64 *tile_sums) {
-  __shared__ u64 scratch[kScanNT / kWave];
-  const u64 base = (u64)blockIdx.x * kScanTile;
-  for (int k = 0; k < 3; ++k) {
-    u64 s = 0;
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      const u64 i = base + (u64)j * kScanNT + threadIdx.x;
-      if (i < n) s += scan3_in(p, k, i);
-    }
-    s = block_sum<kScanNT, u64>(s, scratch);
-    if (threadIdx.x == 0) tile_sums[(u64)k * gridDim.x + blockIdx.x] = s;
-    __syncthreads();  // scratch reused
-  }
-}
-
-// Tile blockIdx.x of the three arrays, each offset by tile_offsets[k nb + b]
-// (or 0); the last tile writes out_k[n].
-__global__ __launch_bounds__(kScanNT) void k_tile_scan3(Scan3 p, u64 n, const u64 *tile_offsets) {
-  __shared__ u64 tile[kScanTile];
-  __shared__ u64 scratch[kScanNT / kWave];
-  const u64 base = (u64)blockIdx.x * kScanTile;
-  for (int k = 0; k < 3; ++k) {
-    u64 *out = k == 0 ? p.out0 : k == 1 ? p.out1 : p.out2;
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      const u64 i = base + (u64)j * kScanNT + threadIdx.x;
-      tile[j * kScanNT + threadIdx.x] = i < n ? scan3_in(p, k, i) : 0ull;
-    }
-    __syncthreads();
-    u64 local[kScanIT];
-    u64 run = 0;
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      local[j] = run;
-      run += tile[threadIdx.x * kScanIT + j];
-    }
-    u64 total;
-    const u64 excl = block_exclusive_sum<kScanNT, u64>(run, scratch, &total);
-    const u64 off = tile_offsets ? tile_offsets[(u64)k * gridDim.x + blockIdx.x] : 0ull;
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) tile[threadIdx.x * kScanIT + j] = local[j] + excl + off;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      const u64 i = base + (u64)j * kScanNT + threadIdx.x;
-      if (i < n) out[i] = tile[j * kScanNT + threadIdx.x];
-    }
-    if (blockIdx.x == gridDim.x - 1 && threadIdx.x == 0) out[n] = off + total;
-    __syncthreads();  // tile reused
-  }
-}
-
-// Exclusive scan of the nb tile sums of each array (nb <= kScanTile): one
-// workgroup, the three arrays in turn.
-__global__ __launch_bounds__(kScanNT) void k_sums_scan3(const u64 *sums, u64 nb, u64 *offs) {
-  __shared__ u64 tile[kScanTile];
-  __shared__ u64 scratch[kScanNT / kWave];
-  for (int k = 0; k < 3; ++k) {
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      const u64 i = (u64)j * kScanNT + threadIdx.x;
-      tile[j * kScanNT + threadIdx.x] = i < nb ? sums[(u64)k * nb + i] : 0ull;
-    }
-    __syncthreads();
-    u64 local[kScanIT];
-    u64 run = 0;
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      local[j] = run;
-      run += tile[threadIdx.x * kScanIT + j];
-    }
-    u64 total;
-    const u64 excl = block_exclusive_sum<kScanNT, u64>(run, scratch, &total);
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) tile[threadIdx.x * kScanIT + j] = local[j] + excl;
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kScanIT; ++j) {
-      const u64 i = (u64)j * kScanNT + threadIdx.x;
-      if (i < nb) offs[(u64)k * nb + i] = tile[j * kScanNT + threadIdx.x];
-    }
-    __syncthreads();
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Single-pass scan with decoupled look-back (Merrill & Garland, "Single-pass
 // Parallel Prefix Scan with Decoupled Look-back", 2016).  A workgroup takes
@@ -439,31 +340,6 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   else if (k == 2) hipLaunchKernelGGL(k_scan_lb<2>, g, bl, 0, s, p);
   else if (k == 3) hipLaunchKernelGGL(k_scan_lb<3>, g, bl, 0, s, p);
   else hipLaunchKernelGGL(k_scan_lb<4>, g, bl, 0, s, p);
-}
-
-size_t scan3_temp_bytes(u64 n) {
-  return std::max<size_t>(6 * ceil_div(std::max<u64>(n, 1), kScanTile) * sizeof(u64) + 256,
-                          scan_temp_bytes(n));
-}
-
-void exclusive_scan3(const u64 *in0, u64 *out0, const u32 *in1, u64 *out1, const u32 *in2,
-                     u64 *out2, u64 n, void *temp, hipStream_t s) {
-  const u64 nb = ceil_div(n, kScanTile);
-  if (n == 0 || nb > kScanTile) {  // empty, or too many tiles for one sums pass
-    exclusive_scan(in0, out0, n, temp, s);
-    exclusive_scan(in1, out1, n, temp, s);
-    exclusive_scan(in2, out2, n, temp, s);
-    return;
-  }
-  const Scan3 p{in0, in1, in2, out0, out1, out2};
-  if (nb == 1) {
-    hipLaunchKernelGGL(k_tile_scan3, dim3(1), dim3(kScanNT), 0, s, p, n, (const u64 *)nullptr);
-    return;
-  }
-  u64 *sums = static_cast<u64 *>(temp), *offs = sums + 3 * nb;
-  hipLaunchKernelGGL(k_tile_reduce3, dim3((unsigned)nb), dim3(kScanNT), 0, s, p, n, sums);
-  hipLaunchKernelGGL(k_sums_scan3, dim3(1), dim3(kScanNT), 0, s, (const u64 *)sums, nb, offs);
-  hipLaunchKernelGGL(k_tile_scan3, dim3((unsigned)nb), dim3(kScanNT), 0, s, p, n, (const u64 *)offs);
 }
 
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s) {
