@@ -69,7 +69,39 @@ def parse():
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB three times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--stream-mib", type=int, default=2048,
+                    help="size of each buffer of the STREAM-style probe of achievable HBM "
+                         "bandwidth (copy, write-only fill, read-only sum), timed before the "
+                         "workload; 0 skips it")
     return ap.parse_args()
+
+
+def stream_probe(dev, mib: int, reps: int = 5) -> dict:
+    """Achievable HBM bandwidth on this GPU with plain device kernels, timed
+    with events on the current stream: copy (read + write), fill (write
+    only) and a sum reduction (read only) of `mib` MiB buffers."""
+    import torch
+    n = (mib << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    out = {"buffer_bytes": n * 4, "reps": reps}
+    acc = torch.zeros((), dtype=torch.float32, device=dev)
+    for name, fn, nbytes in (("copy", lambda: b.copy_(a), 2 * n * 4),
+                             ("write", lambda: b.fill_(1.5), n * 4),
+                             ("read", lambda: torch.sum(a, out=acc), n * 4)):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[name + "_GBps"] = nbytes / (ms * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return out
 
 
 def kernel_source_digest(name: str) -> str:
@@ -155,6 +187,7 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    stream = stream_probe(dev, args.stream_mib) if args.stream_mib else None
     if args.copy_probe_mib:
         nbytes = args.copy_probe_mib << 20
         a_ = torch.empty(nbytes, dtype=torch.uint8, device=dev)
@@ -243,10 +276,17 @@ def main():
             # is the per-source chain of dependent loads
             on_mfma = st["total_product_mfma_sources"] == st["total_product_sources"]
             peak = FP64_MFMA_PEAK_TFLOPS if on_mfma else FP64_VECTOR_PEAK_TFLOPS
+            traffic = recorded_traffic("k_prod_sources", traffic_key) if exact else None
             roof = {"bound": "mfma" if on_mfma else "alu", "kernel": "k_prod_sources",
                     "achieved": kern["product"]["TFLOPps"], "peak": peak,
                     "unit": "TFLOP/s", "frac": kern["product"]["TFLOPps"] / peak,
-                    "traffic": recorded_traffic("k_prod_sources", traffic_key) if exact else None}
+                    "traffic": traffic,
+                    "limiter": "latency: each wave's chain of dependent loads (header, "
+                               "symbols and arcs, visited-array claim), not arithmetic"}
+            if traffic:
+                gbs = traffic / (kern["product"]["avg_launch_ms"] * 1e-3) / 1e9
+                roof["hbm_counter_GBps"] = gbs
+                roof["hbm_counter_frac"] = gbs / HBM_PEAK_GBS
         else:
             kname = kern[dom]["kernel"]
             roof = {"bound": "hbm", "kernel": kname,
@@ -307,6 +347,21 @@ def main():
             "kernels": {k: rkern[k] for k in ("write", "merge", "sort", "expand+merge")},
             "roofline": rroof,
         }
+        em = rkern["expand+merge"]
+    else:
+        em = kern["expand+merge"] if kern["expand+merge"]["ms_per_step"] else None
+    if em:
+        # the materialise-then-merge kernels (arc-pair write pass, tile merges)
+        # against the HBM peak and the probe's achievable bandwidth
+        out["expand_merge_hbm"] = {
+            "kernels": "k_expand + k_merge_dense + sort-tile merge",
+            "path": "record path (opts.no_product_merge)" if "record_path" in out else "this step",
+            "GBps": em["GBps"], "frac_of_peak": em["GBps"] / HBM_PEAK_GBS,
+            "frac_of_achievable": (em["GBps"] / stream["copy_GBps"]) if stream else None,
+            "bytes": "algorithmic: records written and read once (key + float32 weight), 24 B "
+                     "per match descriptor, 16 B per merged run written"}
+    if stream:
+        out["hbm_achievable"] = stream
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels, not args.no_reduction)
     print(json.dumps(out), flush=True)

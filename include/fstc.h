@@ -121,10 +121,14 @@ typedef struct fstc_opts {
                                  without records.  Same states and arcs;
                                  weights agree to float64 rounding        */
   uint32_t hash_visited;      /* nonzero: the visited set is always the hash
-                                 table of pair keys.  0: when |Q1| |Q2| is
-                                 at most 2^26 it is a dense array indexed by
-                                 q1 |Q2| + q2 (the paper's |Q1||Q2| table,
-                                 section 3.4), 4 bytes a pair; same result */
+                                 table of pair keys.  0: it is a dense array
+                                 indexed by q1 |Q2| + q2 (the paper's
+                                 |Q1||Q2| table, section 3.4), 4 bytes a
+                                 pair, when |Q1| |Q2| is at most 2^26, and
+                                 the hash table otherwise, moved into such
+                                 an array between two levels once the table
+                                 would need as many bytes as the array and
+                                 |Q1| |Q2| is at most 2^30; same result    */
   uint32_t phase_timing;      /* with stats: nonzero times every phase
                                  (ms_csr .. ms_assign) with HIP events at
                                  each phase boundary.  0: only the kernels
@@ -133,7 +137,12 @@ typedef struct fstc_opts {
                                  timed, one event before and one after each
                                  launch, and the phase times are 0 (every
                                  event costs the stream a few microseconds) */
-  uint32_t reserved0;
+  uint32_t hash_min_log2;     /* 0: the hash table of pair keys is sized by
+                                 the reachable pairs (load at most 1/2).
+                                 1..31: it has at least 2^hash_min_log2 slots
+                                 from the start (2^31 slots take 24 GiB);
+                                 for tests of large slot numbers.  Values
+                                 above 31 give FSTC_ERR_INVALID_ARG       */
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the
@@ -192,7 +201,10 @@ typedef struct fstc_stats {
   uint64_t total_product_sources; /* sources merged by the product merge      */
   double ms_product_kernel;   /* product-merge kernel alone, all levels      */
   uint32_t product_launches;  /* launches of the product-merge kernel        */
-  uint32_t reserved0;
+  uint32_t visited_form;      /* 0: hash table of pair keys throughout; 1:
+                                 dense |Q1||Q2| array from the start; 2: the
+                                 hash table moved into the dense array
+                                 between two levels                        */
   uint64_t total_product_mfma_sources; /* of those, sources whose sums ran on
                                           the matrix cores (float64 MFMA)     */
 } fstc_stats;

@@ -34,15 +34,20 @@ constexpr u64 kEmptyKey = ~0ull;
 // (visited-table capacity is at most 2^31 slots).
 constexpr u32 kNewFlag = 0x80000000u;
 // A product-merge temp entry whose target already had an id (dense visited
-// array: ids and slots are below 2^26) holds that id with this flag instead
-// of the slot, so the result append needs no visited-array lookup.
+// array only: ids and slots are below kDenseMaxPairs = 2^30) holds that id
+// with this flag instead of the slot, so the result append needs no
+// visited-array lookup.  Hash-table slots reach bit 30 and never carry it.
 constexpr u32 kIdFlag = 0x40000000u;
 // Dense visited array entries (ids stay below both).
 constexpr u32 kUnvisited = 0xffffffffu;
 constexpr u32 kClaimed = 0xfffffffeu;
 constexpr u64 kMaxHashCap = 1ull << 31;
-// Largest pair space |Q1| |Q2| whose visited set is a dense array (4 bytes a pair).
+// Largest pair space |Q1| |Q2| whose visited set is a dense array (4 bytes a
+// pair) from the start; up to kDenseMaxPairs the hash table is moved into
+// such an array once it would need as many bytes.
 constexpr u64 kDensePairs = 1ull << 26;
+constexpr u64 kDenseMaxPairs = 1ull << 30;
+static_assert(kDenseMaxPairs <= kIdFlag, "dense slots and ids stay below kIdFlag");
 
 // ---------------------------------------------------------------------------
 // Host-side error plumbing (exceptions stay inside the library).

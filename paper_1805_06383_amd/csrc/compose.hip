@@ -382,11 +382,14 @@ void Composer::run(fstc_result *out) {
   sq2b.ensure(kMinGrow * 4);
   // visited set: a dense array over all pairs when there are at most
   // kDensePairs of them (slot = q1 |Q2| + q2, no probing), else a hash table
-  const bool dense_vis = pairspace <= kDensePairs && !o.hash_visited;
-  const u32 vn2 = dense_vis ? m2.num_states : 0u;
+  // (moved into a dense array later when that is no larger, see below)
+  bool dense_vis = pairspace <= kDensePairs && !o.hash_visited;
+  u32 vn2 = dense_vis ? m2.num_states : 0u;
   u64 hcap = dense_vis ? pairspace
                        : std::min<u64>(kMaxHashCap, next_pow2(std::max<u64>(
                              4096, 2 * std::min<u64>(pairspace, m1.num_arcs + m2.num_arcs + 1))));
+  if (!dense_vis && o.hash_min_log2)
+    hcap = std::max<u64>(hcap, std::min<u64>(kMaxHashCap, 1ull << o.hash_min_log2));
   if (dense_vis) {
     hvb.ensure(hcap * 4);
     fill_u32(hvb.as<u32>(), kUnvisited, hcap, s);
@@ -405,6 +408,7 @@ void Composer::run(fstc_result *out) {
   u64 dense_records = 0, dense_runs = 0, sort_runs = 0, product_records = 0, product_sources = 0;
   u32 product_launches = 0;
   u64 product_mfma_sources = 0;
+  u32 vis_moves = 0;
 
   ArcCols out_arcs(&A, s);
   // single-pass scan state: zero-filled when (re)allocated, then written
@@ -555,7 +559,23 @@ void Composer::run(fstc_result *out) {
     // level could add
     // (at most kMaxHashCap slots: an insert into a full table reports it)
     const u64 need = std::min<u64>(2 * (n_states + newcap), kMaxHashCap);
-    if (!dense_vis && need > hcap) {
+    if (!dense_vis && need > hcap && !o.hash_visited && pairspace <= kDenseMaxPairs &&
+        next_pow2(need) * 12 >= pairspace * 4) {
+      // the grown table (8-byte keys, 4-byte ids) would be at least as large
+      // as the dense array over all pairs: move the visited set there (the
+      // level's inserts have not started; every state so far has its id)
+      Buf nv(&A);
+      nv.ensure(pairspace * 4);
+      fill_u32(nv.as<u32>(), kUnvisited, pairspace, s);
+      launch_states_to_dense(sq1b.as<u32>(), sq2b.as<u32>(), n_states, nv.as<u32>(),
+                             m2.num_states, s);
+      hkb.release();
+      std::swap(hvb.p, nv.p); std::swap(hvb.cap, nv.cap);
+      hcap = pairspace;
+      dense_vis = true;
+      vn2 = m2.num_states;
+      ++vis_moves;
+    } else if (!dense_vis && need > hcap) {
       const u64 ncap = next_pow2(need);
       Buf nk(&A), nv(&A);
       nk.ensure(ncap * 8);
@@ -869,6 +889,7 @@ void Composer::run(fstc_result *out) {
     stats->max_level_premerge = max_level_pre;
     stats->big_sources = big_total;
     stats->hash_capacity = hcap;
+    stats->visited_form = vis_moves ? 2u : dense_vis ? 1u : 0u;
     if (T.all) {
       stats->ms_csr = ms[kCsr];
       stats->ms_count = ms[kCount];
@@ -942,6 +963,8 @@ int fstc_compose(const fstc_fst *m1, const fstc_fst *m2, const fstc_opts *opts,
     return fail(FSTC_ERR_ALPHABET, "m1->num_osyms != m2->num_isyms");
   if (opts && ((opts->alloc == nullptr) != (opts->free == nullptr)))
     return fail(FSTC_ERR_INVALID_ARG, "opts->alloc and opts->free must be set together");
+  if (opts && opts->hash_min_log2 > 31)
+    return fail(FSTC_ERR_INVALID_ARG, "opts->hash_min_log2 must be at most 31");
   try {
     check_csr_ranges(*m1, true);
     check_csr_ranges(*m2, false);

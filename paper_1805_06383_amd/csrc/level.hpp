@@ -226,6 +226,10 @@ void launch_insert_start(u64 *hkeys, u64 hmask, u32 *hvals, u32 vn2, u32 s1, u32
                          u32 *sq2, u32 *err, hipStream_t s);
 void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32 *nvals,
                    u64 nmask, u32 *err, hipStream_t s);
+// Dense visited array vis (|Q1| |Q2| entries, already kUnvisited) from the
+// state arrays: vis[sq1[i] vn2 + sq2[i]] = i for every state id i < n.
+void launch_states_to_dense(const u32 *sq1, const u32 *sq2, u64 n, u32 *vis, u32 vn2,
+                            hipStream_t s);
 // ids base .. base + nnew - 1 in new-list order (or the order in `order`).
 void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 vn2,
                    u32 *sq1, u32 *sq2, hipStream_t s);

@@ -1719,6 +1719,13 @@ __global__ void k_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkey
   }
 }
 
+// The visited set moved from the hash table into the dense array vis
+// (filled with kUnvisited): state id i < n is stored at its pair's entry.
+__global__ void k_states_to_dense(const u32 *sq1, const u32 *sq2, u64 n, u32 *vis, u32 vn2) {
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x)
+    vis[(u64)sq1[i] * vn2 + sq2[i]] = (u32)i;
+}
+
 // New pair i of the list gets id base + i: i < nnew, or i < min(*count,
 // nnew) when count is given (nnew is then the list's capacity).
 __global__ void k_assign(const u32 *slots, u32 nnew, const u64 *count, u32 base,
@@ -1804,7 +1811,9 @@ __global__ __launch_bounds__(256) void k_compact_sources(MergeArgs a, const u64 
     const uint4 rec = a.temp[tb + r];
     const u64 k = ob + r;
     osrc[k] = a.lo + (u32)u;
-    odst[k] = (rec.x & kIdFlag) ? rec.x & ~kIdFlag : hvals[rec.x & ~kNewFlag];
+    // kIdFlag marks ids only with the dense array (slots and ids below 2^30
+    // there); hash-table slots use bit 30 themselves
+    odst[k] = (a.vn2 && (rec.x & kIdFlag)) ? rec.x & ~kIdFlag : hvals[rec.x & ~kNewFlag];
     oil[k] = rec.y;
     ool[k] = rec.z;
     ow[k] = __uint_as_float(rec.w);
@@ -2029,6 +2038,12 @@ void launch_rehash(const u64 *okeys, const u32 *ovals, u64 ocap, u64 *nkeys, u32
                    u64 nmask, u32 *err, hipStream_t s) {
   hipLaunchKernelGGL(k_rehash, dim3(grid1(ocap)), dim3(256), 0, s, okeys, ovals, ocap, nkeys,
                      nvals, nmask, err);
+}
+
+void launch_states_to_dense(const u32 *sq1, const u32 *sq2, u64 n, u32 *vis, u32 vn2,
+                            hipStream_t s) {
+  if (!n) return;
+  hipLaunchKernelGGL(k_states_to_dense, dim3(grid1(n)), dim3(256), 0, s, sq1, sq2, n, vis, vn2);
 }
 
 void launch_assign(const u32 *slots, u32 nnew, u32 base, const u64 *hkeys, u32 *hvals, u32 vn2,

@@ -396,3 +396,70 @@ def one_state_dense(W: np.ndarray, name: str = "dense") -> FST:
     a, b = a.ravel(), b.ravel()
     return FST(1, 0, na, nb, np.zeros(a.size), np.zeros(a.size), a, b,
                W[a, b], np.ones(1, dtype=np.uint8), name=name)
+
+
+def wide_parts_pair(seed: int = 0, nq: int = 2000, hub_parts: int = 70_000,
+                    small_arcs: int = 10, small_inner: int = 100, hub_dups: int = 5000):
+    """A pair whose start states each have more than 2^16 distinct
+    (target, outer symbol) pairs, so that a composed arc's two part ranks need
+    more than 32 bits together.
+
+    State 0 of M1 has ``hub_parts`` arcs k:k -> 1 + k mod (nq - 1) (outer
+    symbol k, inner symbol k); state 0 of M2 has arcs k:k -> 1 + 7k mod
+    (nq - 1).  The start pair joins them one to one.  Every other state has
+    ``small_arcs`` arcs with uniform targets (state 0 included), inner symbols
+    uniform over the first ``small_inner`` and outer symbols uniform, so that
+    later levels mix sources of the hub states with small ones.  The first
+    ``hub_dups`` hub arcs are listed twice (new weights), so that the start
+    pair's composed arcs merge in pairs.  30% of states accept."""
+    rng = np.random.default_rng(7000 + seed)
+    ng = hub_parts  # inner alphabet: the hub's symbols
+
+    def one(mult: int, inner_is_output: bool, name: str) -> FST:
+        k = np.r_[np.arange(hub_parts), np.arange(hub_dups)]
+        hsrc = np.zeros(len(k), np.int64)
+        hdst = 1 + (mult * k) % (nq - 1)
+        n = (nq - 1) * small_arcs
+        ssrc = np.repeat(np.arange(1, nq), small_arcs)
+        sdst = rng.integers(0, nq, n)
+        sinner = rng.integers(0, small_inner, n)
+        souter = rng.integers(0, hub_parts, n)
+        src = np.r_[hsrc, ssrc]
+        dst = np.r_[hdst, sdst]
+        inner = np.r_[k, sinner]
+        outer = np.r_[k, souter]
+        w = random_weights(rng, len(src))
+        fin = _finals(rng, nq, 0.3)
+        if inner_is_output:
+            return FST(nq, 0, hub_parts, ng, src, dst, outer, inner, w, fin, name=name)
+        return FST(nq, 0, ng, hub_parts, src, dst, inner, outer, w, fin, name=name)
+
+    return one(1, True, "wide.M1"), one(7, False, "wide.M2")
+
+
+def hub_pair(seed: int = 0, nq: int = 8250, hub: int = 2900, ninner: int = 8):
+    """A pair whose start states join on one inner symbol with ``hub`` arcs
+    each (distinct targets 1..hub, outer symbols uniform over 64), so the start
+    pair alone has hub^2 composed arcs to hub^2 distinct target pairs.  Every
+    other state has one arc with a uniform target, inner symbol uniform over
+    ``ninner`` and outer symbol uniform over 64.  With nq = 8250 the pair space
+    (6.8e7) is above 2^26 and the start pair's 8.4M targets are enough to make
+    the visited set's hash table outgrow a dense array of all pairs."""
+    rng = np.random.default_rng(8000 + seed)
+
+    def one(inner_is_output: bool, name: str) -> FST:
+        hsrc = np.zeros(hub, np.int64)
+        hdst = 1 + np.arange(hub)
+        hin = np.zeros(hub, np.int64)
+        ssrc = np.arange(1, nq)
+        sdst = rng.integers(0, nq, nq - 1)
+        sin = rng.integers(0, ninner, nq - 1)
+        src, dst, inner = np.r_[hsrc, ssrc], np.r_[hdst, sdst], np.r_[hin, sin]
+        outer = rng.integers(0, 64, len(src))
+        w = random_weights(rng, len(src))
+        fin = _finals(rng, nq, 0.2)
+        if inner_is_output:
+            return FST(nq, 0, 64, ninner, src, dst, outer, inner, w, fin, name=name)
+        return FST(nq, 0, ninner, 64, src, dst, inner, outer, w, fin, name=name)
+
+    return one(True, "hub.M1"), one(False, "hub.M2")

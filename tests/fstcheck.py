@@ -63,13 +63,32 @@ def assert_same(got: Canon, ref: Canon, rtol: float = 1e-5, what: str = ""):
     assert np.array_equal(got.finals, ref.finals), f"{what}: accept flags differ"
     assert got.keys.shape == ref.keys.shape, f"{what}: {len(got.keys)} arcs vs {len(ref.keys)}"
     assert np.array_equal(got.keys, ref.keys), f"{what}: arc key sets differ"
-    gw = got.w.astype(np.float64); rw = ref.w.astype(np.float64)
-    err = np.abs(gw - rw)
-    bad = err > rtol * np.abs(rw)
+    bad = ~weights_close(got.w, ref.w, rtol)
     if bad.any():
         i = int(np.argmax(bad))
         raise AssertionError(f"{what}: {int(bad.sum())} weights off, e.g. key {ref.keys[i]} "
-                             f"got {gw[i]!r} ref {rw[i]!r}")
+                             f"got {float(got.w[i])!r} ref {float(ref.w[i])!r}")
+
+
+def weights_close(got, ref, rtol, atol=0.0):
+    """Per element: a NaN reference needs a NaN, an infinite reference the
+    same infinity (sign included), a finite reference a finite weight within
+    rtol * |ref| + atol of it.  rtol = inf leaves finite weights unchecked but
+    still requires the NaN and infinity pattern to agree."""
+    gw = np.asarray(got, np.float64)
+    rw = np.asarray(ref, np.float64)
+    gn, rn = np.isnan(gw), np.isnan(rw)
+    gi, ri = np.isinf(gw), np.isinf(rw)
+    ok = (gn == rn) & (gi == ri)
+    ok &= ~ri | (gw == rw)
+    fin = ~(rn | ri)
+    if np.isinf(rtol):
+        ok &= ~fin | np.isfinite(gw)
+    else:
+        with np.errstate(invalid="ignore"):
+            within = np.abs(gw - rw) <= rtol * np.abs(rw) + atol
+        ok &= ~fin | within
+    return ok
 
 
 # ---------------------------------------------------------------------------
@@ -254,3 +273,57 @@ def assert_same_multiset(got: Multiset, ref: Multiset, what: str = ""):
         i = int(np.argmax(np.any(got.rows != ref.rows, axis=1)))
         raise AssertionError(f"{what}: arc multisets differ, first at sorted row {i}: "
                              f"{got.rows[i]} vs {ref.rows[i]}")
+
+
+# ---------------------------------------------------------------------------
+# Per-source expansion (no search): brute force over the arcs of two states
+# ---------------------------------------------------------------------------
+
+def brute_force_sources(m1, m2, q1s, q2s):
+    """Merged out-arcs of each source pair (q1s[i], q2s[i]) on its own, from
+    every pair of arcs leaving q1s[i] in M1 and q2s[i] in M2 that share the
+    inner symbol (§2 arc rule), identical (target pair, a, c) summed in
+    float64 over float32 products.  Numpy only.
+
+    Returns (rows, w, joined): rows [k, 7] int64 (batch index, src q1, src q2,
+    dst q1, dst q2, a, c) sorted, their weights (float32) and the number of
+    arc pairs joined per source."""
+    o1 = np.argsort(m1.src, kind="stable"); o2 = np.argsort(m2.src, kind="stable")
+    b1 = np.searchsorted(m1.src[o1], np.arange(m1.num_states + 1))
+    b2 = np.searchsorted(m2.src[o2], np.arange(m2.num_states + 1))
+    rows, ws, joined = [], [], []
+    for i, (q1, q2) in enumerate(zip(np.asarray(q1s, np.int64), np.asarray(q2s, np.int64))):
+        e1 = o1[b1[q1]:b1[q1 + 1]]
+        e2 = o2[b2[q2]:b2[q2 + 1]]
+        hit = m1.olabel[e1][:, None] == m2.ilabel[e2][None, :]
+        i1, i2 = np.nonzero(hit)
+        e1, e2 = e1[i1], e2[i2]
+        joined.append(len(e1))
+        if not len(e1):
+            continue
+        key = np.stack([m1.dst[e1], m2.dst[e2], m1.ilabel[e1], m2.olabel[e2]], 1).astype(np.int64)
+        prod = (m1.weight[e1] * m2.weight[e2]).astype(np.float32)
+        uk, inv = np.unique(key, axis=0, return_inverse=True)
+        acc = np.zeros(len(uk), np.float64)
+        np.add.at(acc, inv.ravel(), prod.astype(np.float64))
+        head = np.tile(np.array([i, q1, q2], np.int64), (len(uk), 1))
+        rows.append(np.concatenate([head, uk], 1))
+        ws.append(acc.astype(np.float32))
+    if not rows:
+        return np.zeros((0, 7), np.int64), np.zeros(0, np.float32), np.array(joined, np.int64)
+    rows = np.concatenate(rows); w = np.concatenate(ws)
+    order = np.lexsort(rows.T[::-1])
+    return rows[order], w[order], np.array(joined, np.int64)
+
+
+def source_rows(res, q1s, q2s):
+    """Rows (batch index, src q1, src q2, dst q1, dst q2, a, c) of a per-source
+    expansion result whose states 0..n-1 are the batch's sources, sorted,
+    with their weights."""
+    q1s = np.asarray(q1s, np.int64); q2s = np.asarray(q2s, np.int64)
+    src = np.asarray(res.src, np.int64); dst = np.asarray(res.dst, np.int64)
+    rows = np.stack([src, q1s[src], q2s[src], np.asarray(res.q1, np.int64)[dst],
+                     np.asarray(res.q2, np.int64)[dst], np.asarray(res.a, np.int64),
+                     np.asarray(res.c, np.int64)], 1) if len(src) else np.zeros((0, 7), np.int64)
+    order = np.lexsort(rows.T[::-1]) if len(rows) else np.zeros(0, np.int64)
+    return rows[order], np.asarray(res.w, np.float32)[order]

@@ -168,3 +168,65 @@ def test_unreduced_mutant_is_caught(name, mutant_dir):
     out = mutant_dir / f"lib{name}.so"
     subprocess.run(["g++", *CXXFLAGS, "-o", str(out), str(src)], check=True)
     assert run_pins_unreduced(out), f"planted mistake {name} passed every pin"
+
+
+# Planted mistakes in the per-source expansion (oracle_expand_pairs): its
+# batch assembly is its own code, so each slip there must fail one of its
+# pins (tests/test_oracle_expand.py's checks, run here on a few batches).
+MUTANTS_EXPAND = {
+    # the merge map survives from one source to the next
+    "expand_map_not_reset": ("    std::map<ArcKey, double> acc;\n    r->premerge",
+                             "    static std::map<ArcKey, double> acc;\n    r->premerge"),
+    # arcs carry the next batch index
+    "expand_src_off_by_one": ("r->arcs.push_back({(uint32_t)i, vid,",
+                              "r->arcs.push_back({(uint32_t)(i + 1 < n ? i + 1 : i), vid,"),
+    # targets numbered from 0, on top of the sources
+    "expand_targets_from_zero": ("vid = (uint32_t)r->pairs.size();",
+                                 "vid = (uint32_t)(r->pairs.size() - n);"),
+    # a target pair seen before gets a new id again
+    "expand_no_target_dedup": ("auto it = tid.find(v);", "auto it = tid.end();"),
+    # accept flags ignore M2
+    "expand_final_ignores_m2": ("&& m2->final[r->pairs[i].second]", "&& 1"),
+    # the joined count keeps only the last source
+    "expand_count_overwritten": ("r->premerge += expand_pair(", "r->premerge = expand_pair("),
+}
+
+
+def run_pins_expand(lib):
+    from test_oracle_expand import check_batch
+    failed = set()
+    cases = []
+    for seed in range(8):
+        m1, m2 = _tiny(100 + seed)
+        rng = np.random.default_rng(seed)
+        k = 6
+        cases.append((m1, m2, rng.integers(0, 4, k).astype(np.uint32),
+                      rng.integers(0, 4, k).astype(np.uint32)))
+    m1, m2 = W.config1(2)
+    rng = np.random.default_rng(3)
+    cases.append((m1, m2, rng.integers(0, 200, 30).astype(np.uint32),
+                  rng.integers(0, 200, 30).astype(np.uint32)))
+    for m1, m2, q1s, q2s in cases:
+        try:
+            check_batch(oracle.expand_pairs(m1, m2, q1s, q2s, lib_path=lib), m1, m2, q1s, q2s)
+        except (AssertionError, IndexError, ValueError):
+            failed.add("batch")
+    return failed
+
+
+def test_unmutated_copy_passes_expand(mutant_dir):
+    out = mutant_dir / "liboracle_clean_e.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(out), SRC], check=True)
+    assert run_pins_expand(out) == set()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_EXPAND))
+def test_expand_mutant_is_caught(name, mutant_dir):
+    old, new = MUTANTS_EXPAND[name]
+    text = open(SRC).read()
+    assert text.count(old) == 1, f"mutation site for {name} not found once"
+    src = mutant_dir / f"{name}.cpp"
+    src.write_text(text.replace(old, new))
+    out = mutant_dir / f"lib{name}.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(out), str(src)], check=True)
+    assert run_pins_expand(out), f"planted mistake {name} passed every pin"
