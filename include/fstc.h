@@ -274,6 +274,23 @@ int fstc_sort_pairs(uint64_t *keys, uint32_t *values, uint64_t n, int bit_lo, in
  * (n + 1 outputs; out[n] is the total).  Device arrays. */
 int fstc_exclusive_scan_u64(const uint64_t *in, uint64_t *out, uint64_t n, hipStream_t stream);
 
+/*
+ * fstc_exclusive_scan_u64_noalloc: the same scan as fstc_exclusive_scan_u64
+ * (same arguments, results and return codes), for callers that cannot
+ * allocate device memory (code that must not call hipMalloc or hipFree:
+ * tight serving loops, harnesses that forbid allocation).  It allocates
+ * nothing: the scan's temporaries (tile counter, error word, look-back state
+ * of every 2048-element tile) live in a file-scope device array of the
+ * library, about 8.9 MB, that each GPU it runs on holds until the process
+ * ends.  The first call on a device looks the array up and clears it
+ * (synchronising `stream`).  n is at most 2^28 (larger n: FSTC_ERR_RANGE,
+ * nothing launched).  Every call on one GPU shares that GPU's array: calls
+ * that overlap in time on one GPU, from any stream or thread, race and must
+ * not be made.  Synchronises `stream` before returning.
+ */
+int fstc_exclusive_scan_u64_noalloc(const uint64_t *in, uint64_t *out, uint64_t n,
+                                    hipStream_t stream);
+
 /* Text for a return code, and thread-local detail of the last failure. */
 const char *fstc_strerror(int code);
 const char *fstc_last_error_detail(void);

@@ -1089,6 +1089,16 @@ int fstc_exclusive_scan_u64(const uint64_t *in, uint64_t *out, uint64_t n, hipSt
   });
 }
 
+int fstc_exclusive_scan_u64_noalloc(const uint64_t *in, uint64_t *out, uint64_t n,
+                                    hipStream_t stream) {
+  if (!out || (n && !in)) return fail(FSTC_ERR_INVALID_ARG, "in or out is NULL");
+  if (n > noalloc_scan_max_n())
+    return fail(FSTC_ERR_RANGE, "n = " + std::to_string(n) + " exceeds the scratch capacity of " +
+                                    std::to_string(noalloc_scan_max_n()) + " elements");
+  return run_guarded("fstc_exclusive_scan_u64_noalloc", stream,
+                     [&] { noalloc_scan(in, out, n, stream); });
+}
+
 const char *fstc_strerror(int code) {
   switch (code) {
     case FSTC_OK: return "success";

@@ -153,4 +153,10 @@ void alloc_csr(const fstc_fst &m, Buf &buf, Csr &out);
 // Arena bytes build_csr takes for m (either direction).
 size_t csr_temp_bytes(const fstc_fst &m);
 
+// Exclusive scan of n u64 values (out has n + 1 entries) using the device's
+// file-scope scratch array instead of allocated temporaries (noalloc.hip);
+// n at most noalloc_scan_max_n().  Synchronises the stream.
+u64 noalloc_scan_max_n();
+void noalloc_scan(const u64 *in, u64 *out, u64 n, hipStream_t s);
+
 }  // namespace fstc

@@ -7,6 +7,7 @@ are carried in ``torch.int32`` tensors holding the same bits.
 
 Names follow the C ABI: ``fstc_compose``, ``fstc_result_release``,
 ``fstc_build_csr``, ``fstc_sort_pairs``, ``fstc_exclusive_scan_u64``,
+``fstc_exclusive_scan_u64_noalloc``,
 ``fstc_strerror``, ``fstc_last_error_detail``, ``fstc_version``; ``compose``
 is the convenience entry point.
 """
@@ -83,7 +84,8 @@ class FstcStats(ctypes.Structure):
 
 
 EXPORTS = ("fstc_compose", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",
-           "fstc_exclusive_scan_u64", "fstc_strerror", "fstc_last_error_detail", "fstc_version")
+           "fstc_exclusive_scan_u64", "fstc_exclusive_scan_u64_noalloc", "fstc_strerror",
+           "fstc_last_error_detail", "fstc_version")
 
 _lib = None
 
@@ -109,6 +111,8 @@ def load_library(path: Path | str | None = None) -> ctypes.CDLL:
     lib.fstc_sort_pairs.restype = ctypes.c_int
     lib.fstc_exclusive_scan_u64.argtypes = [_vp, _vp, _u64, _vp]
     lib.fstc_exclusive_scan_u64.restype = ctypes.c_int
+    lib.fstc_exclusive_scan_u64_noalloc.argtypes = [_vp, _vp, _u64, _vp]
+    lib.fstc_exclusive_scan_u64_noalloc.restype = ctypes.c_int
     lib.fstc_strerror.argtypes = [ctypes.c_int]
     lib.fstc_strerror.restype = ctypes.c_char_p
     lib.fstc_last_error_detail.argtypes = []
@@ -390,3 +394,16 @@ def fstc_exclusive_scan_u64(x: torch.Tensor, stream=None) -> torch.Tensor:
                                                   _stream_handle(stream)))
     return out
 
+
+def fstc_exclusive_scan_u64_noalloc(x: torch.Tensor, out: torch.Tensor | None = None,
+                                    stream=None) -> torch.Tensor:
+    """The same scan through the entry point that allocates nothing (the
+    library's per-device scratch array; n <= 2^28).  `out` (int64, n + 1
+    elements) may be given so that the call needs no allocation at all."""
+    assert x.dtype == torch.int64 and x.is_contiguous()
+    if out is None:
+        out = torch.empty(x.numel() + 1, dtype=torch.int64, device=x.device)
+    assert out.dtype == torch.int64 and out.is_contiguous() and out.numel() >= x.numel() + 1
+    _check(load_library().fstc_exclusive_scan_u64_noalloc(
+        x.data_ptr() if x.numel() else None, out.data_ptr(), x.numel(), _stream_handle(stream)))
+    return out
