@@ -88,7 +88,7 @@ def stream_probe(dev, mib: int, reps: int = 5) -> dict:
     acc = torch.zeros((), dtype=torch.float32, device=dev)
     for name, fn, nbytes in (("copy", lambda: b.copy_(a), 2 * n * 4),
                              ("write", lambda: b.fill_(1.5), n * 4),
-                             ("read", lambda: torch.sum(a, out=acc), n * 4)):
+                             ("read", lambda: torch.sum(a, dim=0, out=acc), n * 4)):
         fn()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

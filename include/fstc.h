@@ -207,6 +207,10 @@ typedef struct fstc_stats {
                                  between two levels                        */
   uint64_t total_product_mfma_sources; /* of those, sources whose sums ran on
                                           the matrix cores (float64 MFMA)     */
+  uint32_t direct_product_levels; /* levels of product-merge sources alone whose
+                                     merged arcs the product kernel wrote
+                                     straight into the result              */
+  uint32_t reserved1;
 } fstc_stats;
 
 /*
@@ -238,7 +242,8 @@ void fstc_result_release(fstc_result *r, const fstc_opts *opts, hipStream_t stre
  * uses it, built on the device (the paper sorts on the host).
  *
  * Arcs are grouped by source state, then by inner symbol (output symbol when
- * by_output != 0, as for M1; input symbol otherwise, as for M2).  Instead of
+ * by_output != 0, as for M1; input symbol otherwise, as for M2), then by
+ * part (below), then by input position.  Instead of
  * the dense offset array R[|Q| m + 1] of section 3.3, the layout is two-level:
  *   row[q] .. row[q+1]       segments of state q            [num_states+1]
  *   seg_sym[k]               inner symbol of segment k      [num_segments]

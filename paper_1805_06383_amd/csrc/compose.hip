@@ -408,7 +408,7 @@ void Composer::run(fstc_result *out) {
   u64 dense_records = 0, dense_runs = 0, sort_runs = 0, product_records = 0, product_sources = 0;
   u32 product_launches = 0;
   u64 product_mfma_sources = 0;
-  u32 vis_moves = 0;
+  u32 vis_moves = 0, direct_levels = 0;
 
   ArcCols out_arcs(&A, s);
   // single-pass scan state: zero-filled when (re)allocated, then written
@@ -490,6 +490,13 @@ void Composer::run(fstc_result *out) {
     // after the synchronisation.
     const u64 maxk = std::min<u64>(maxp1 * maxp2, 64);  // a source's table entries
     const bool spec = product && dense_vis && (u64)nsrc * maxk * 20 <= kSpecBytes;
+    // Direct product level: the speculative product kernel writes its merged
+    // arcs straight into the result (grown to hold every source's largest
+    // table first); when the level turns out to have records it writes
+    // nothing and the level takes the usual path.  Deterministic ids (a sort
+    // of the new pairs) and an arc cap keep the usual path.
+    const bool direct = spec && !o.deterministic_ids && !o.max_arcs &&
+                        (arcs + (u64)nsrc * maxk) * 20 <= kEarlyBytes;
     if (spec) {
       temp.ensure((u64)nsrc * maxk * sizeof(uint4));
       runsrc.ensure((u64)nsrc * maxk * 4);
@@ -497,6 +504,7 @@ void Composer::run(fstc_result *out) {
       pm.R = 0;
       pm.R_dev = roff.as<u64>() + nsrc;
       pm.nsrc = nsrc;
+      pm.lo = lo;
       pm.st = dst;
       pm.pk = pk.as<u32>();
       pm.phdr = phdr.as<uint4>();
@@ -519,6 +527,15 @@ void Composer::run(fstc_result *out) {
       pm.mend = mend.as<u64>();
       pm.pcnt = cnt.as<u64>();
       pm.newc = newc.as<u32>();
+      if (direct) {
+        out_arcs.grow(arcs + (u64)nsrc * maxk, arcs);
+        pm.out_src = out_arcs.col(0);
+        pm.out_dst = out_arcs.col(1);
+        pm.out_il = out_arcs.col(2);
+        pm.out_ol = out_arcs.col(3);
+        pm.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+        pm.out_base = arcs;
+      }
       T.at(kProductKernel);
       launch_prod_sources(pm, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
       T.at(kNone);
@@ -676,10 +693,54 @@ void Composer::run(fstc_result *out) {
     // the stream before the host reads the level's totals, and the GPU runs
     // them while the host waits (deterministic ids and an arc cap need the
     // exact counts first).
-    const bool early = !o.no_reduction && !o.deterministic_ids && !o.max_arcs &&
+    const bool direct_level = direct && R == 0;  // the speculative launch wrote the result
+    bool assigned = false;                        // ids and arcs of the level are in place
+    const bool early = !direct_level && !o.no_reduction && !o.deterministic_ids && !o.max_arcs &&
                        (n_states + newcap) * 8 <= kEarlyBytes &&
                        (arcs + R + prodpos) * 20 <= kEarlyBytes;
-    if (!o.no_reduction) {
+    if (direct_level) {
+      // the level's merged arcs are in the result at arcs + poff[u]: new
+      // pairs per source scanned into id offsets, joined pairs and merged
+      // arcs per source summed (the latter scanned too, for entries without
+      // a term), ids of the claimed entries, then the other new targets
+      ++product_launches;
+      T.at(kAssign);
+      {
+        ScanJob jobs[3] = {{newc.p, false, newoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()},
+                           {mend.p, true, aoff.as<u64>()}};
+        jobs[1].total_only = true;
+        jobs[2].sub = tstart.as<u64>();
+        exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+      }
+      ma.out_src = out_arcs.col(0);
+      ma.out_dst = out_arcs.col(1);
+      ma.out_il = out_arcs.col(2);
+      ma.out_ol = out_arcs.col(3);
+      ma.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+      ma.out_base = arcs;
+      sq1b.grow_keep((n_states + newcap) * 4, n_states * 4);
+      sq2b.grow_keep((n_states + newcap) * 4, n_states * 4);
+      launch_assign_direct(ma, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
+      const u32 seq2 = next_publication();
+      launch_merged_total(aoff.as<u64>() + nsrc, newoff.as<u64>() + nsrc, ptot.as<u64>() + nsrc, ma,
+                          hs_dev, seq2, s);
+      launch_fix_marked(ma, prodpos, s);
+      T.at(kNone);
+      wait_published(seq2);
+      status_clear = true;  // k_merged_total cleared the level counters
+      nnew = hs->st.nnew;
+      merged = hs->st.merged;
+      premerge += hs->st.prod_records;
+      product_records += hs->st.prod_records;
+      max_level_pre = std::max(max_level_pre, hs->st.prod_records);
+      if (merged < prodpos) {  // entries without a term leave holes: close them
+        Tmp rows(&level_tmp);
+        rows.ensure(prodpos * 20);
+        launch_close_holes(ma, aoff.as<u64>(), prodpos, rows.p, s);
+      }
+      assigned = true;
+      ++direct_levels;
+    } else if (!o.no_reduction) {
       T.at(kMerge);
       if (R) {
         fill_u32(tile_runs.as<u32>(), 0, ntiles, s);
@@ -798,7 +859,7 @@ void Composer::run(fstc_result *out) {
     // (a5) ids for the new pairs; (a7) append the level's arcs (done above
     // for an early append)
     const u64 ns_new = n_states + nnew;
-    if (!early) {
+    if (!early && !assigned) {
       T.at(kAssign);
       sq1b.grow_keep(ns_new * 4, n_states * 4);
       sq2b.grow_keep(ns_new * 4, n_states * 4);
@@ -890,6 +951,7 @@ void Composer::run(fstc_result *out) {
     stats->big_sources = big_total;
     stats->hash_capacity = hcap;
     stats->visited_form = vis_moves ? 2u : dense_vis ? 1u : 0u;
+    stats->direct_product_levels = direct_levels;
     if (T.all) {
       stats->ms_csr = ms[kCsr];
       stats->ms_count = ms[kCount];

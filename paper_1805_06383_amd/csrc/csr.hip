@@ -42,6 +42,16 @@ __global__ void k_csr_pack(const u32 *src, const u32 *dst, const u32 *il, const 
   }
 }
 
+// keys[i] = kc[perm[i]], vals[i] = perm[i]: the segment keys of the arcs in
+// part order.
+__global__ void k_gather_keys(const u64 *kc, const u32 *perm, u64 n, u64 *keys, u32 *vals) {
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
+    const u32 e = perm[i];
+    keys[i] = kc[e];
+    vals[i] = e;
+  }
+}
+
 __global__ void k_head_flags(const u64 *keys, u64 n, u32 *flags) {
   for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (u64)gridDim.x * blockDim.x)
     flags[k] = (k == 0 || keys[k] != keys[k - 1]) ? 1u : 0u;
@@ -104,13 +114,14 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 // non-finite or subnormal weight; the largest biased float32 exponent of a
 // nonzero weight at kCellEmaxShift, the smallest at kCellEminShift) and
 // marks a state of P parts, S segments and P S arcs kCellDense (no segment
-// has more than P arcs, so each has exactly P).
+// has more than P arcs, so each has exactly P), and kCellIdent as well when
+// arc i of every segment has part i.
 __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *arcs,
                              const u32 *part_base, u32 nq, u32 *flag) {
   const u32 lane = lane_id();
   const u64 nw = (u64)gridDim.x * blockDim.x / kWave;
   for (u64 q = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
-    bool bad = part_base[q + 1] - part_base[q] > kProdParts, special = false;
+    bool bad = part_base[q + 1] - part_base[q] > kProdParts, special = false, shuffled = false;
     u32 emax = 0, emin = 255;
     if (!bad) {
       for (u32 sg = row[q] + lane; sg < row[q + 1]; sg += kWave) {
@@ -123,6 +134,7 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
         for (u32 i = 0; i < n; ++i) {
           const uint2 x = arcs[a0 + i];
           m |= 1ull << (x.x & 63u);
+          shuffled |= x.x != i;
           const u32 mag = x.y & 0x7fffffffu, e = mag >> 23;
           special |= e == 255u || (e == 0u && mag != 0u);
           if (mag) {
@@ -134,6 +146,7 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
       }
     }
     const bool any = __ballot(bad) != 0, spec = __ballot(special) != 0;
+    const bool ident = __ballot(shuffled) == 0;
     emax = wave_max(emax);
     emin = 255u - wave_max(255u - emin);
     const u32 P = part_base[q + 1] - part_base[q], r0 = row[q], r1 = row[q + 1];
@@ -141,6 +154,7 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
     if (lane == 0)
       flag[q] = any ? kCellBad
                     : (spec ? kCellSpecial : 0u) | (dense ? kCellDense : 0u) |
+                          (dense && ident ? kCellIdent : 0u) |
                           (emax << kCellEmaxShift) | (emin << kCellEminShift);
   }
 }
@@ -155,8 +169,9 @@ __global__ void k_fill_tail(u32 *a, const u32 *count, u64 n, u32 v) {
 // ---------------------------------------------------------------------------
 // Per-state build.  After one stable sort of the arcs by source state, each
 // state's arcs (in input order) are sorted inside one workgroup: by
-// (target, outer symbol) to rank its parts, and stably by inner symbol to
-// lay out its segments.  A state's parts and segments are first written at
+// (target, outer symbol) to rank its parts, and then, in that part order,
+// stably by inner symbol to lay out its segments (so a segment's arcs are
+// ordered by part).  A state's parts and segments are first written at
 // its own arc offset (a state has at most as many of each as arcs); a scan
 // of the per-state counts then gives part_base and row, and a last pass
 // moves them to their final places.  Same layout as the global sorts.
@@ -302,14 +317,20 @@ __global__ __launch_bounds__(NT) void k_state_local(LocalArgs a, const u32 *list
         a.ptmp[a0 + r] = make_uint2((u32)(k >> a.bo), (u32)(k & omask));
       }
     });
-    __syncthreads();  // part_of complete; sort buffers free
-    // segments: stable sort by inner symbol
+    __syncthreads();  // part_of complete
+    // segments: stable sort by inner symbol of the elements in part order,
+    // so that the arcs of a segment are ordered by part (iin holds the
+    // elements in part order; kout / iout are free)
     for (u32 i = threadIdx.x; i < d; i += NT) {
-      a.ka[a0 + i] = a.inner[a.order[a0 + i]];
-      a.ia[a0 + i] = i;
+      const u32 el = iin[a0 + i];
+      kout[a0 + i] = a.inner[a.order[a0 + el]];
+      iout[a0 + i] = el;
     }
     __syncthreads();
-    kin = a.ka; kout = a.kb; iin = a.ia; iout = a.ib;
+    {
+      u64 *tk = kin; kin = kout; kout = tk;
+      u32 *tv = iin; iin = iout; iout = tv;
+    }
     local_sort<NT, IT>(kin, iin, kout, iout, a0, d, a.bi, s_cnt, s_base, s_tmp, s_run);
     const u32 ns = local_runs<NT>(kin, a0, d, s_tmp, [&](u32 i, u32 r, bool head) {
       const u32 el = iin[a0 + i];
@@ -382,10 +403,13 @@ __global__ __launch_bounds__(256) void k_state_group(LocalArgs a, const u32 *lis
     if (head) a.ptmp[a0 + prank] = make_uint2((u32)(k >> a.bo), (u32)(k & omask));
     // element el receives its part rank (each group holds a permutation)
     const u32 my_part = (u32)__builtin_amdgcn_ds_permute((int)((gb + el) * 4u), (int)prank);
-    // segments: by inner symbol, element order within equal symbols
+    // segments: by inner symbol, then part, then element (the arcs of a
+    // segment ordered by part); the element is the low 6 bits of the
+    // tie-break word
     k = v ? (u64)a.inner[e] : ~0ull;
-    el = gl;
+    el = (my_part << 6) | gl;
     group_sort<G>(k, el);
+    el &= 63u;
     const u64 sprev = __shfl(k, (int)(lane ? lane - 1 : 0), kWave);
     head = v && (gl == 0 || k != sprev);
     hm = __ballot(head) & gmask;
@@ -686,12 +710,15 @@ void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d
   hipLaunchKernelGGL(k_max_gap, dim3(grid_for(nq)), dim3(kNT), 0, s, c.part_base, nq,
                      d_counts + 2);
 
-  // segments: distinct (state, inner symbol) in sorted order
-  radix_sort_pairs(kc.as<u64>(), v2.as<u32>(), kalt.as<u64>(), valt.as<u32>(), n, 0, bq + bi,
+  // segments: distinct (state, inner symbol) in sorted order, the arcs of a
+  // segment ordered by part (the stable sort starts from the part order)
+  hipLaunchKernelGGL(k_gather_keys, dim3(g), dim3(kNT), 0, s, kc.as<u64>(), v1.as<u32>(), n,
+                     kalt.as<u64>(), valt.as<u32>());
+  radix_sort_pairs(kalt.as<u64>(), valt.as<u32>(), kc.as<u64>(), v2.as<u32>(), n, 0, bq + bi,
                    tmp.p, s);
-  hipLaunchKernelGGL(k_head_flags, dim3(g), dim3(kNT), 0, s, kc.as<u64>(), n, flags.as<u32>());
+  hipLaunchKernelGGL(k_head_flags, dim3(g), dim3(kNT), 0, s, kalt.as<u64>(), n, flags.as<u32>());
   exclusive_scan(flags.as<u32>(), ex.as<u32>(), n, tmp.p, s);
-  hipLaunchKernelGGL(k_segments, dim3(g), dim3(kNT), 0, s, kc.as<u64>(), v2.as<u32>(),
+  hipLaunchKernelGGL(k_segments, dim3(g), dim3(kNT), 0, s, kalt.as<u64>(), valt.as<u32>(),
                      flags.as<u32>(), ex.as<u32>(), n, bi, apg.as<u32>(), c.part_base,
                      m.weight, c.seg_sym, c.seg_off, sstate.as<u32>(), c.arcs);
   hipLaunchKernelGGL(k_copy_count, dim3(1), dim3(1), 0, s, ex.as<u32>() + n, d_counts + 0);

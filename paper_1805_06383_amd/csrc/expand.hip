@@ -99,7 +99,8 @@ __device__ __forceinline__ bool products_normal(u32 f1, u32 f2) {
 // form (bit 0: at most kProdMfmaParts parts per state, products_normal) and
 // the aligned form (bit 1; both states kCellDense with symbol lists of one
 // length n, at bit 8): the second header word is then (M1 segment begin, its
-// first arc, M2 segment begin, its first arc).  The cells are single-arc
+// first arc, M2 segment begin, its first arc).  Bit 2: aligned and both
+// states kCellIdent (the strided form of the product kernel).  The cells are single-arc
 // only for states of at most kProdParts parts.
 __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1, u32 q2,
                                               const Ranges &r, bool &mfma) {
@@ -111,8 +112,10 @@ __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1,
   mfma = p1 <= kProdMfmaParts && p2 <= kProdMfmaParts && products_normal(f1, f2);
   const u32 n = r.e1 - r.b1;
   const bool aligned = mfma && (f1 & f2 & kCellDense) && n == r.e2 - r.b2;
+  const bool strided = aligned && (f1 & f2 & kCellIdent);
   a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16),
-                             (mfma ? 1u : 0u) | (aligned ? 2u | (n << 8) : 0u));
+                             (mfma ? 1u : 0u) | (aligned ? 2u | (n << 8) : 0u) |
+                                 (strided ? 4u : 0u));
   a.phdr[2 * u + 1] = aligned ? make_uint4(r.b1, a.c1.seg_off[r.b1], r.b2, a.c2.seg_off[r.b2])
                               : make_uint4(r.b1, r.e1, r.b2, r.e2);
   return p1 * p2;

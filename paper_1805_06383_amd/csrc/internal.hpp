@@ -138,8 +138,10 @@ constexpr u32 kProdParts = 64;
 // smallest biased float32 exponents of its nonzero weights (0 and 255 in
 // those fields when it has none), and bit kCellDense when every one of its
 // segments holds exactly one arc per part (segment i's arcs are then the P
-// consecutive arcs from the state's first plus P i).
-constexpr u32 kCellBad = 1u, kCellSpecial = 2u, kCellDense = 4u;
+// consecutive arcs from the state's first plus P i), and kCellIdent besides
+// when, in every segment, arc j has part j (the per-state builds order a
+// segment's arcs by part).
+constexpr u32 kCellBad = 1u, kCellSpecial = 2u, kCellDense = 4u, kCellIdent = 8u;
 constexpr int kCellEmaxShift = 8, kCellEminShift = 16;
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s);
 

@@ -136,6 +136,11 @@ struct LevelArgs {
                          // takes the matrix-core form (summed by the level scan)
 };
 
+// Target column marks of a direct product level (MergeArgs::out_src), and
+// the source of an entry without a term.
+constexpr u32 kDstSlot = 0x80000000u, kDstClaim = 0x40000000u, kDstSlotMask = 0x3fffffffu;
+constexpr u32 kHoleSrc = 0xffffffffu;
+
 // Written by the count kernel for a product-merge source u at phdr[2u], [2u+1]:
 // (M1 part base, M2 part base, P1 | P2 << 16, matrix-core form), (M1 segment
 // range begin, end, M2 segment range begin, end).
@@ -198,6 +203,15 @@ struct MergeArgs {
   u32 *newc;  // [nsrc] new pairs each product-merge source claimed (written by it)
   const u64 *R_dev;  // product merge launched before the host knew R: the level's
                      // record count on the device (the kernel merges only if 0)
+  // direct product level (out_src != NULL; dense visited array only): the
+  // product kernel writes source u's merged arcs straight to the result
+  // columns at out_base + poff[u] + r instead of to temp, with the target
+  // column holding the id when the target had one, else its slot with
+  // kDstSlot (and kDstClaim when this entry claimed it); entries past the
+  // source's merged count get src = kHoleSrc
+  u32 *out_src, *out_dst, *out_il, *out_ol;
+  float *out_w;
+  u64 out_base;
   const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;
 };
 
@@ -267,6 +281,18 @@ u64 newlist_waves(const MergeArgs &a, u64 RB);
 // list entry; 16 lanes per source with claims write its claimed slots in
 // temp order.
 void launch_newlist_sources(const MergeArgs &a, const u64 *newoff, hipStream_t s);
+// Direct product level (see MergeArgs::out_src): ids base + newoff[u] + i for
+// the claimed entries of source u in entry order (visited array, state
+// arrays and the entries' target column), then every other marked target
+// replaced by its id from the visited array.
+void launch_assign_direct(const MergeArgs &a, const u64 *newoff, u32 base, u32 *sq1, u32 *sq2,
+                          hipStream_t s);
+void launch_fix_marked(const MergeArgs &a, u64 n, hipStream_t s);
+// Removes the entries without a term (src = kHoleSrc) from the n result rows
+// at out_base: source u's merged arcs move from out_base + poff[u] to
+// out_base + aoff[u] (aoff: exclusive scan of merged arcs per source), through
+// `tmp` (20 n bytes).
+void launch_close_holes(const MergeArgs &a, const u64 *aoff, u64 n, void *tmp, hipStream_t s);
 const u64 *launch_newlist(const MergeArgs &a, const u64 *bigoff, u32 nbig, u64 RB, u32 *wcnt,
                           u64 *woff, void *scan_state, hipStream_t s);
 // Composition without reduction: every record of the level becomes an arc

@@ -946,6 +946,7 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const u32 hf = uni(h0.w);
   const bool mf = (hf & 1u) != 0;       // matrix-core form
   const bool aligned = (hf & 2u) != 0;  // dense states, lists of one length na
+  const bool strided = (hf & 4u) != 0;  // aligned, segments ordered by part
   const u32 na = hf >> 8;
   const u32 b1 = uni(h1.x), b2 = uni(h1.z);
   const u32 e1 = aligned ? b1 + na : uni(h1.y), e2 = aligned ? b2 + na : uni(h1.w);
@@ -999,185 +1000,226 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const u32 *loffs = one_short ? a.seg_off2 : a.seg_off1;
   const u32 le = one_short ? e2 : e1;
 
-  // 1. join, staging, part masks.  Segment offsets are loaded with the
-  //    symbols (this lane's short-list segment; the long-list chunk's, handed
-  //    over by the lane that found the match), so the arc loads follow the
-  //    join without another round trip.  Loads are unconditional, from
-  //    indexes clamped into the lists, and their values selected after.
-  //    Aligned form: lane g takes symbol g of both lists, whose arcs are the
-  //    P1 (P2) consecutive ones from ab1 + P1 g (ab2 + P2 g); symbols and
-  //    arcs are loaded together and the arcs used once every lane's two
-  //    symbols agree (else the join below runs as for other sources).
-  bool found = false, staged = false;
-  u32 sa = 0, sn = 0, la = 0, ln = 0;
-  uint2 x1[kProdBatch], x2[kProdBatch];
-  if (aligned) {
-    const bool v = lane < na;
-    const u32 g = v ? lane : 0u;
-    const u32 s1 = a.seg_sym1[b1 + g], s2 = a.seg_sym2[b2 + g];
-#pragma unroll
-    for (int k = 0; k < kProdBatch; ++k) {
-      x1[k] = prod_arc<NARROW>(a.arcs1, ab1 + P1 * g + (u32)k);
-      x2[k] = prod_arc<NARROW>(a.arcs2, ab2 + P2 * g + (u32)k);
-    }
-    staged = __ballot(v && s1 == s2) == __ballot(v);
-    found = staged && v;
-  }
-  if (!staged) {
-    const u32 idx = bs + lane;
-    const bool valid = idx < es;
-    const u32 ic = valid ? idx : es - 1;
-    const u32 sym0 = ssym[ic], so0 = soffs[ic], so1 = soffs[ic + 1];
-    const u32 sym = valid ? sym0 : 0xffffffffu;  // labels are below 2^32 - 1
-    sa = valid ? so0 : 0u;
-    sn = valid ? so1 - so0 : 0u;
-    const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
-    const u64 vmask = __ballot(valid);
-    for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
-      const u32 len = min(le - cb, (u32)kWave);
-      const bool in = lane < len;
-      const u32 lc = cb + min(lane, len - 1);
-      const u32 lv0 = lsym[lc], lo00 = loffs[lc], lo10 = loffs[lc + 1];
-      const u32 lv = in ? lv0 : 0xffffffffu, lo0 = in ? lo00 : 0u, lo1 = in ? lo10 : 0u;
-      if (__ballot(valid && lv == sym) == vmask) {
-        // the chunk starts with the short list's symbols: lane i matches lane i
-        found = valid;
-        la = lo0;
-        ln = lo1 - lo0;
-        break;
-      }
-      if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
-      u32 pos = 0;  // elements of the chunk below sym
-  #pragma unroll
-      for (u32 step = kWave / 2; step; step >>= 1) {
-        const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
-        pos = v < sym ? pos + step : pos;
-      }
-      const u32 at = __shfl(lv, (int)pos, kWave);
-      const u32 pa = __shfl(lo0, (int)pos, kWave), pe = __shfl(lo1, (int)pos, kWave);
-      if (valid && at == sym) {
-        found = true;
-        la = pa;
-        ln = pe - pa;
-      }
-      if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
-    }
-  }
-  u32 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol (parts < 16)
-  bool bad = false;
-  // cells per symbol row: P1 and P2, or rows of kProdRow cleared first
-  const u32 S1 = mf ? kProdRow : P1, S2 = mf ? kProdRow : P2;
-  if (mf) {
-    *reinterpret_cast<uint4 *>(&val[lane * kProdRow]) = make_uint4(0, 0, 0, 0);
-    *reinterpret_cast<uint4 *>(&val[(kWave + lane) * kProdRow]) = make_uint4(0, 0, 0, 0);
-  }
-  const u32 a1 = one_short ? sa : la, a2 = one_short ? la : sa;
-  const u32 n1 = !found ? 0u : staged ? P1 : one_short ? sn : ln;
-  const u32 n2 = !found ? 0u : staged ? P2 : one_short ? ln : sn;
-  // arc k of each side is present when k < h (k in the batch); a present
-  // arc's part is below P (else the source is malformed); an absent one
-  // writes the spare cell
-  auto stage = [&](const uint2(&x1)[kProdBatch], const uint2(&x2)[kProdBatch], u32 h1, u32 h2) {
-#pragma unroll
-    for (int k = 0; k < kProdBatch; ++k) {
-      const bool in1 = (u32)k < h1, in2 = (u32)k < h2;
-      const bool v1 = in1 & (x1[k].x < P1), v2 = in2 & (x2[k].x < P2);
-      val[v1 ? lane * S1 + x1[k].x : kProdCells] = x1[k].y;
-      val[v2 ? kWave * S1 + lane * S2 + x2[k].x : kProdCells] = x2[k].y;
-      pm1 |= (v1 ? 1u : 0u) << x1[k].x;
-      pm2 |= (v2 ? 1u : 0u) << x2[k].x;
-      bad |= (in1 & !v1) | (in2 & !v2);  // bitwise: no short-circuit branches
-    }
-  };
-  if (mf) {
-    // at most kProdRow arcs per segment (single-arc cells): kProdRow
-    // consecutive arcs from the segment's first (arc 0 for a lane without a
-    // match; the arc arrays have kArcTail spare entries), those past the
-    // segment's end replaced by padding
-    static_assert(kProdBatch <= (int)kArcTail, "segment loads stay inside the arc arrays");
-    if (!staged) {
-      const u32 f1 = n1 ? a1 : 0u, f2 = n2 ? a2 : 0u;
-#pragma unroll
-      for (int k = 0; k < kProdBatch; ++k) {
-        x1[k] = prod_arc<NARROW>(a.arcs1, f1 + (u32)k);
-        x2[k] = prod_arc<NARROW>(a.arcs2, f2 + (u32)k);
-      }
-    }
-    bad |= (n1 > kProdRow) | (n2 > kProdRow);
-    stage(x1, x2, n1, n2);
-  } else if (found) {
-    for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
-#pragma unroll
-      for (int k = 0; k < kProdBatch; ++k) {
-        const u32 i = i0 + (u32)k;
-        x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(0, 0);
-        x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(0, 0);
-      }
-      stage(x1, x2, n1 > i0 ? n1 - i0 : 0u, n2 > i0 ? n2 - i0 : 0u);
-    }
-  }
-  if (__ballot(bad)) {  // impossible: parts are below the state's part count
-    if (lane == 0) set_error(&a.st->err, kErrBounds);
-    return;
-  }
-  // symbol masks of the parts (bit g: symbol g has an arc of the part),
-  // outside the matrix-core form: lane p holds M1 part p's in ma, M2 part
-  // p's in mb
-  u64 ma = 0, mb = 0;
-  if (!mf) {
-    for (u32 p = 0; p < P1; ++p) {
-      const u64 m = __ballot((pm1 >> p) & 1u);
-      ma = lane == p ? m : ma;
-    }
-    for (u32 p = 0; p < P2; ++p) {
-      const u64 m = __ballot((pm2 >> p) & 1u);
-      mb = lane == p ? m : mb;
-    }
-  }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-  // 2. entry sums; which entries have a term (the owner's `has`) and the
-  //    source's joined pairs
-  bool has;
-  u32 pairs;
+  // Strided form (both states' segments hold one arc per part, ordered by
+  // part, and the symbol lists have one length na): the matrix-core
+  // operands are loaded straight from the arc arrays -- instruction t, lane l
+  // takes symbol 16 t + l / 4, part l % 4, i.e. arc ab + P g + p, which for
+  // P = 4 is 64 consecutive arcs per instruction -- with no staging, no part
+  // masks and no entry presence test: every entry has na terms.  The lists
+  // are checked to agree (else the general join below runs).
+  bool has = false;
+  u32 pairs = 0;
   double acc = 0.0;
-  if (mf) {
-    // bit 4 p1 + p2 of o: parts p1 and p2 both have an arc at this lane's
-    // symbol, a joined pair (the parts' bits spread 4 apart, times pm2)
-    const u32 sp = (pm1 & 1u) | ((pm1 & 2u) << 3) | ((pm1 & 4u) << 6) | ((pm1 & 8u) << 9);
-    const u32 o = pm2 * sp;
-    has = (wave_or(o) >> ((p1 << 2) | p2)) & 1u;
-    pairs = wave_total((u32)__popc(o));
-    // the 4 x 64 by 64 x 4 product on the matrix cores (see above)
-    double d = 0.0;
+  bool summed = false;
+  if (strided) {
+    const bool v = lane < na;
+    const u32 g0 = v ? lane : 0u;
+    const u32 s1 = a.seg_sym1[b1 + g0], s2 = a.seg_sym2[b2 + g0];
+    const u32 pp = lane & 3u, gq = lane >> 2;
+    u32 w1[4], w2[4];
+    bool in1[4], in2[4];
 #pragma unroll
     for (u32 t = 0; t < 4; ++t) {
-      const double x = (double)__uint_as_float(val[t * kWave + lane]);
-      const double y = (double)__uint_as_float(val[(kProdRow + t) * kWave + lane]);
-      d = __builtin_amdgcn_mfma_f64_4x4x4f64(x, y, d, 0, 0, 0);
+      const u32 g = gq + 16u * t;
+      in1[t] = g < na && pp < P1;
+      in2[t] = g < na && pp < P2;
+      w1[t] = prod_arc<NARROW>(a.arcs1, in1[t] ? ab1 + P1 * g + pp : ab1).y;
+      w2[t] = prod_arc<NARROW>(a.arcs2, in2[t] ? ab2 + P2 * g + pp : ab2).y;
     }
-    d += dpp_f64<kDppRowRor4>(d);
-    acc = d + dpp_f64<kDppRowRor8>(d);
-  } else {
-    const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
-    has = m != 0;
-    pairs = wave_total(owner ? (u32)__popcll(m) : 0u);
-    // lane c of the entry adds the terms of g = c, c + q, ... (bit j of mm:
-    // symbol c + j q is one of the entry's terms)
-    u64 mm = act ? m >> c : 0;
-    const u32 qs = q < (u32)kWave ? q : 0u;  // q = 64: a single symbol per lane
-    u32 ia = c * P1 + p1, ib = kWave * P1 + c * P2 + p2;
-    const u32 da = q * P1, db = q * P2;
-    while (mm) {  // at most 64 / q steps: every step drops q bits (all, when q = 64)
-      const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
-      acc += (mm & 1u) ? (double)t : 0.0;
-      mm = qs ? mm >> qs : 0ull;
-      ia += da;
-      ib += db;
+    if (__ballot(v && s1 == s2) == __ballot(v)) {
+      double d = 0.0;
+#pragma unroll
+      for (u32 t = 0; t < 4; ++t) {
+        const double x = in1[t] ? (double)__uint_as_float(w1[t]) : 0.0;
+        const double y = in2[t] ? (double)__uint_as_float(w2[t]) : 0.0;
+        d = __builtin_amdgcn_mfma_f64_4x4x4f64(x, y, d, 0, 0, 0);
+      }
+      d += dpp_f64<kDppRowRor4>(d);
+      acc = d + dpp_f64<kDppRowRor8>(d);
+      has = true;
+      pairs = na * P1 * P2;
+      summed = true;
     }
-    for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
+  }
+  if (!summed) {
+    // 1. join, staging, part masks.  Segment offsets are loaded with the
+    //    symbols (this lane's short-list segment; the long-list chunk's, handed
+    //    over by the lane that found the match), so the arc loads follow the
+    //    join without another round trip.  Loads are unconditional, from
+    //    indexes clamped into the lists, and their values selected after.
+    //    Aligned form: lane g takes symbol g of both lists, whose arcs are the
+    //    P1 (P2) consecutive ones from ab1 + P1 g (ab2 + P2 g); symbols and
+    //    arcs are loaded together and the arcs used once every lane's two
+    //    symbols agree (else the join below runs as for other sources).
+    bool found = false, staged = false;
+    u32 sa = 0, sn = 0, la = 0, ln = 0;
+    uint2 x1[kProdBatch], x2[kProdBatch];
+    if (aligned) {
+      const bool v = lane < na;
+      const u32 g = v ? lane : 0u;
+      const u32 s1 = a.seg_sym1[b1 + g], s2 = a.seg_sym2[b2 + g];
+  #pragma unroll
+      for (int k = 0; k < kProdBatch; ++k) {
+        x1[k] = prod_arc<NARROW>(a.arcs1, ab1 + P1 * g + (u32)k);
+        x2[k] = prod_arc<NARROW>(a.arcs2, ab2 + P2 * g + (u32)k);
+      }
+      staged = __ballot(v && s1 == s2) == __ballot(v);
+      found = staged && v;
+    }
+    if (!staged) {
+      const u32 idx = bs + lane;
+      const bool valid = idx < es;
+      const u32 ic = valid ? idx : es - 1;
+      const u32 sym0 = ssym[ic], so0 = soffs[ic], so1 = soffs[ic + 1];
+      const u32 sym = valid ? sym0 : 0xffffffffu;  // labels are below 2^32 - 1
+      sa = valid ? so0 : 0u;
+      sn = valid ? so1 - so0 : 0u;
+      const u32 smax = __shfl(sym, (int)(es - bs - 1), kWave);
+      const u64 vmask = __ballot(valid);
+      for (u32 cb = one_short ? b2 : b1; cb < le; cb += kWave) {
+        const u32 len = min(le - cb, (u32)kWave);
+        const bool in = lane < len;
+        const u32 lc = cb + min(lane, len - 1);
+        const u32 lv0 = lsym[lc], lo00 = loffs[lc], lo10 = loffs[lc + 1];
+        const u32 lv = in ? lv0 : 0xffffffffu, lo0 = in ? lo00 : 0u, lo1 = in ? lo10 : 0u;
+        if (__ballot(valid && lv == sym) == vmask) {
+          // the chunk starts with the short list's symbols: lane i matches lane i
+          found = valid;
+          la = lo0;
+          ln = lo1 - lo0;
+          break;
+        }
+        if (__shfl(lv, 0, kWave) > smax) break;  // this chunk and later ones are past every symbol
+        u32 pos = 0;  // elements of the chunk below sym
+    #pragma unroll
+        for (u32 step = kWave / 2; step; step >>= 1) {
+          const u32 v = __shfl(lv, (int)(pos + step - 1), kWave);
+          pos = v < sym ? pos + step : pos;
+        }
+        const u32 at = __shfl(lv, (int)pos, kWave);
+        const u32 pa = __shfl(lo0, (int)pos, kWave), pe = __shfl(lo1, (int)pos, kWave);
+        if (valid && at == sym) {
+          found = true;
+          la = pa;
+          ln = pe - pa;
+        }
+        if (__shfl(lv, (int)(len - 1), kWave) >= smax) break;  // later chunks are past every symbol
+      }
+    }
+    u32 pm1 = 0, pm2 = 0;  // parts with an arc at this lane's symbol (parts < 16)
+    bool bad = false;
+    // cells per symbol row: P1 and P2, or rows of kProdRow cleared first
+    const u32 S1 = mf ? kProdRow : P1, S2 = mf ? kProdRow : P2;
+    if (mf) {
+      *reinterpret_cast<uint4 *>(&val[lane * kProdRow]) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4 *>(&val[(kWave + lane) * kProdRow]) = make_uint4(0, 0, 0, 0);
+    }
+    const u32 a1 = one_short ? sa : la, a2 = one_short ? la : sa;
+    const u32 n1 = !found ? 0u : staged ? P1 : one_short ? sn : ln;
+    const u32 n2 = !found ? 0u : staged ? P2 : one_short ? ln : sn;
+    // arc k of each side is present when k < h (k in the batch); a present
+    // arc's part is below P (else the source is malformed); an absent one
+    // writes the spare cell
+    auto stage = [&](const uint2(&x1)[kProdBatch], const uint2(&x2)[kProdBatch], u32 h1, u32 h2) {
+  #pragma unroll
+      for (int k = 0; k < kProdBatch; ++k) {
+        const bool in1 = (u32)k < h1, in2 = (u32)k < h2;
+        const bool v1 = in1 & (x1[k].x < P1), v2 = in2 & (x2[k].x < P2);
+        val[v1 ? lane * S1 + x1[k].x : kProdCells] = x1[k].y;
+        val[v2 ? kWave * S1 + lane * S2 + x2[k].x : kProdCells] = x2[k].y;
+        pm1 |= (v1 ? 1u : 0u) << x1[k].x;
+        pm2 |= (v2 ? 1u : 0u) << x2[k].x;
+        bad |= (in1 & !v1) | (in2 & !v2);  // bitwise: no short-circuit branches
+      }
+    };
+    if (mf) {
+      // at most kProdRow arcs per segment (single-arc cells): kProdRow
+      // consecutive arcs from the segment's first (arc 0 for a lane without a
+      // match; the arc arrays have kArcTail spare entries), those past the
+      // segment's end replaced by padding
+      static_assert(kProdBatch <= (int)kArcTail, "segment loads stay inside the arc arrays");
+      if (!staged) {
+        const u32 f1 = n1 ? a1 : 0u, f2 = n2 ? a2 : 0u;
+  #pragma unroll
+        for (int k = 0; k < kProdBatch; ++k) {
+          x1[k] = prod_arc<NARROW>(a.arcs1, f1 + (u32)k);
+          x2[k] = prod_arc<NARROW>(a.arcs2, f2 + (u32)k);
+        }
+      }
+      bad |= (n1 > kProdRow) | (n2 > kProdRow);
+      stage(x1, x2, n1, n2);
+    } else if (found) {
+      for (u32 i0 = 0; i0 < max(n1, n2); i0 += kProdBatch) {
+  #pragma unroll
+        for (int k = 0; k < kProdBatch; ++k) {
+          const u32 i = i0 + (u32)k;
+          x1[k] = i < n1 ? prod_arc<NARROW>(a.arcs1, a1 + i) : make_uint2(0, 0);
+          x2[k] = i < n2 ? prod_arc<NARROW>(a.arcs2, a2 + i) : make_uint2(0, 0);
+        }
+        stage(x1, x2, n1 > i0 ? n1 - i0 : 0u, n2 > i0 ? n2 - i0 : 0u);
+      }
+    }
+    if (__ballot(bad)) {  // impossible: parts are below the state's part count
+      if (lane == 0) set_error(&a.st->err, kErrBounds);
+      return;
+    }
+    // symbol masks of the parts (bit g: symbol g has an arc of the part),
+    // outside the matrix-core form: lane p holds M1 part p's in ma, M2 part
+    // p's in mb
+    u64 ma = 0, mb = 0;
+    if (!mf) {
+      for (u32 p = 0; p < P1; ++p) {
+        const u64 m = __ballot((pm1 >> p) & 1u);
+        ma = lane == p ? m : ma;
+      }
+      for (u32 p = 0; p < P2; ++p) {
+        const u64 m = __ballot((pm2 >> p) & 1u);
+        mb = lane == p ? m : mb;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // 2. entry sums; which entries have a term (the owner's `has`) and the
+    //    source's joined pairs
+    if (mf) {
+      // bit 4 p1 + p2 of o: parts p1 and p2 both have an arc at this lane's
+      // symbol, a joined pair (the parts' bits spread 4 apart, times pm2)
+      const u32 sp = (pm1 & 1u) | ((pm1 & 2u) << 3) | ((pm1 & 4u) << 6) | ((pm1 & 8u) << 9);
+      const u32 o = pm2 * sp;
+      has = (wave_or(o) >> ((p1 << 2) | p2)) & 1u;
+      pairs = wave_total((u32)__popc(o));
+      // the 4 x 64 by 64 x 4 product on the matrix cores (see above)
+      double d = 0.0;
+  #pragma unroll
+      for (u32 t = 0; t < 4; ++t) {
+        const double x = (double)__uint_as_float(val[t * kWave + lane]);
+        const double y = (double)__uint_as_float(val[(kProdRow + t) * kWave + lane]);
+        d = __builtin_amdgcn_mfma_f64_4x4x4f64(x, y, d, 0, 0, 0);
+      }
+      d += dpp_f64<kDppRowRor4>(d);
+      acc = d + dpp_f64<kDppRowRor8>(d);
+    } else {
+      const u64 m = __shfl(ma, (int)p1, kWave) & __shfl(mb, (int)p2, kWave);  // the entry's terms
+      has = m != 0;
+      pairs = wave_total(owner ? (u32)__popcll(m) : 0u);
+      // lane c of the entry adds the terms of g = c, c + q, ... (bit j of mm:
+      // symbol c + j q is one of the entry's terms)
+      u64 mm = act ? m >> c : 0;
+      const u32 qs = q < (u32)kWave ? q : 0u;  // q = 64: a single symbol per lane
+      u32 ia = c * P1 + p1, ib = kWave * P1 + c * P2 + p2;
+      const u32 da = q * P1, db = q * P2;
+      while (mm) {  // at most 64 / q steps: every step drops q bits (all, when q = 64)
+        const float t = __uint_as_float(val[ia]) * __uint_as_float(val[ib]);
+        acc += (mm & 1u) ? (double)t : 0.0;
+        mm = qs ? mm >> qs : 0ull;
+        ia += da;
+        ib += db;
+      }
+      for (u32 d = 1; d < q; d <<= 1) acc += __shfl_xor(acc, (int)d, kWave);
+    }
+
   }
 
   // 3. merged arcs in entry order: the visited-table insert resumes from
@@ -1186,7 +1228,13 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
   const bool run = owner && has;
   const u64 rm = __ballot(run);
   const u32 nr = (u32)__popcll(rm);
-  const u64 base = a.R + a.poff[u];
+  const u64 pu = a.poff[u];
+  const u64 base = a.R + pu;
+  const bool direct = a.out_src != nullptr;  // kernel-uniform
+  if (direct && !a.vn2) {  // impossible: direct levels have the dense array
+    if (lane == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
   bool claimed = false;  // this lane's entry claimed a new pair
   if (run && a.vn2) {
     // dense array: the entry read above, then a claim if it was unvisited
@@ -1194,10 +1242,20 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
                         atomicCAS(&a.vis[hslot], kUnvisited, kClaimed) == kUnvisited;
     claimed = is_new;
     const bool known = hcur < kClaimed;  // an id from an earlier level
-    const u64 t = base + count_below(rm);
-    a.temp[t] = make_uint4(known ? ((u32)hcur | kIdFlag) : ((u32)hslot | (is_new ? kNewFlag : 0u)),
-                           L1.y, L2.y, __float_as_uint((float)acc));
-    a.runsrc[t] = (u32)u;
+    if (direct) {
+      // the merged arc itself, at its place in the result
+      const u64 p = a.out_base + pu + count_below(rm);
+      a.out_src[p] = a.lo + (u32)u;
+      a.out_dst[p] = known ? (u32)hcur : ((u32)hslot | kDstSlot | (is_new ? kDstClaim : 0u));
+      a.out_il[p] = L1.y;
+      a.out_ol[p] = L2.y;
+      a.out_w[p] = (float)acc;
+    } else {
+      const u64 t = base + count_below(rm);
+      a.temp[t] = make_uint4(known ? ((u32)hcur | kIdFlag) : ((u32)hslot | (is_new ? kNewFlag : 0u)),
+                             L1.y, L2.y, __float_as_uint((float)acc));
+      a.runsrc[t] = (u32)u;
+    }
   } else if (run) {
     u32 slot = 0;
     bool is_new = false, done = false;
@@ -1227,7 +1285,14 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     a.runsrc[t] = (u32)u;
     claimed = is_new;
   }
-  if (lane >= nr && lane < K) a.temp[base + lane] = make_uint4(0, 0, 0, 0);  // empty slot
+  if (lane >= nr && lane < K) {  // an entry without a term
+    if (direct) {
+      a.out_src[a.out_base + pu + lane] = kHoleSrc;
+      a.out_dst[a.out_base + pu + lane] = 0u;
+    } else {
+      a.temp[base + lane] = make_uint4(0, 0, 0, 0);  // empty slot
+    }
+  }
   const u32 nclaim = (u32)__popcll(__ballot(claimed));
   if (lane == 0) {
     a.tstart[u] = base;
@@ -1609,6 +1674,86 @@ __global__ __launch_bounds__(256) void k_newlist_sources(MergeArgs a, const u64 
     }
     done += (u32)__popcll(m);
   }
+}
+
+// Direct product level: 16 lanes per source with claims; its claimed entries
+// (kDstClaim in the result's target column, entry order) get ids
+// base + newoff[u], + 1, ..., written to the visited array, the state
+// arrays and the target column.
+__global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *newoff, u32 base,
+                                                       u32 *sq1, u32 *sq2) {
+  const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  const u64 u = t / 16;
+  const u32 j = (u32)(t % 16), lane = lane_id();
+  const u32 nc = u < a.nsrc ? a.newc[u] : 0u;
+  if (__ballot(nc != 0) == 0) return;  // whole wave
+  u64 p0 = 0, n = 0, o = 0;
+  if (nc) {
+    p0 = a.out_base + a.poff[u];
+    n = a.mend[u] - a.tstart[u];
+    o = newoff[u];
+  }
+  const u64 gmask = 0xffffull << (lane & ~15u);  // this lane's group of 16
+  u32 done = 0;
+  for (u32 r0 = 0; r0 < (u32)kWave; r0 += 16) {
+    const u64 r = r0 + j;
+    const u32 x = (nc && r < n) ? a.out_dst[p0 + r] : 0u;
+    const bool f = (x & kDstClaim) != 0;
+    const u64 m = __ballot(f) & gmask;
+    if (f) {
+      const u32 slot = x & kDstSlotMask;
+      const u32 id = base + (u32)(o + done + count_below(m));
+      a.vis[slot] = id;
+      sq1[id] = slot / a.vn2;
+      sq2[id] = slot % a.vn2;
+      a.out_dst[p0 + r] = id;
+    }
+    done += (u32)__popcll(m);
+  }
+}
+
+// Direct product level, after k_assign_direct: targets still marked
+// kDstSlot (claimed by another source of the level) get their ids.
+__global__ void k_fix_marked(MergeArgs a, u64 n) {
+  u32 *dst = a.out_dst + a.out_base;
+  for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (u64)gridDim.x * blockDim.x) {
+    const u32 x = dst[k];
+    if (!(x & kDstSlot)) continue;
+    const u64 slot = x & kDstSlotMask;
+    if (slot > a.hmask) {  // impossible: slots index the visited array
+      set_error(&a.st->err, kErrBounds);
+      continue;
+    }
+    dst[k] = a.vis[slot];
+  }
+}
+
+// Direct product level with entries without a term: the n rows at out_base,
+// copied to tmp, go back without those entries (source u's arcs to
+// out_base + aoff[u]); 16 lanes per source.
+__global__ void k_copy_rows(const MergeArgs a, u64 n, u32 *tmp) {
+  const u32 *cols[5] = {a.out_src, a.out_dst, a.out_il, a.out_ol,
+                        reinterpret_cast<const u32 *>(a.out_w)};
+  for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (u64)gridDim.x * blockDim.x)
+#pragma unroll
+    for (int c = 0; c < 5; ++c) tmp[(u64)c * n + k] = cols[c][a.out_base + k];
+}
+
+__global__ __launch_bounds__(256) void k_close_holes(MergeArgs a, const u64 *aoff, u64 n,
+                                                     const u32 *tmp) {
+  const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+  const u64 u = t / 16;
+  const u32 j = (u32)(t % 16);
+  if (u >= a.nsrc) return;
+  const u64 from = a.poff[u], to = aoff[u], m = a.mend[u] - a.tstart[u];
+  if (from + m > n || to + m > n) {  // impossible: counts agree with the scans
+    if (j == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  u32 *cols[5] = {a.out_src, a.out_dst, a.out_il, a.out_ol, reinterpret_cast<u32 *>(a.out_w)};
+  for (u64 r = j; r < m; r += 16)
+#pragma unroll
+    for (int c = 0; c < 5; ++c) cols[c][a.out_base + to + r] = tmp[(u64)c * n + from + r];
 }
 
 // Level total of new states (end of the exclusive scan of the per-wave counts).
@@ -2014,6 +2159,25 @@ void launch_newlist_sources(const MergeArgs &a, const u64 *newoff, hipStream_t s
   if (!a.nsrc) return;
   hipLaunchKernelGGL(k_newlist_sources, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256),
                      0, s, a, newoff);
+}
+
+void launch_assign_direct(const MergeArgs &a, const u64 *newoff, u32 base, u32 *sq1, u32 *sq2,
+                          hipStream_t s) {
+  if (!a.nsrc) return;
+  hipLaunchKernelGGL(k_assign_direct, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256),
+                     0, s, a, newoff, base, sq1, sq2);
+}
+
+void launch_fix_marked(const MergeArgs &a, u64 n, hipStream_t s) {
+  if (!n) return;
+  hipLaunchKernelGGL(k_fix_marked, dim3(grid1(n)), dim3(256), 0, s, a, n);
+}
+
+void launch_close_holes(const MergeArgs &a, const u64 *aoff, u64 n, void *tmp, hipStream_t s) {
+  if (!n || !a.nsrc) return;
+  hipLaunchKernelGGL(k_copy_rows, dim3(grid1(n)), dim3(256), 0, s, a, n, static_cast<u32 *>(tmp));
+  hipLaunchKernelGGL(k_close_holes, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256), 0,
+                     s, a, aoff, n, static_cast<const u32 *>(tmp));
 }
 
 void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,

@@ -6,7 +6,7 @@
   rank of its (target, outer) among its state's parts;
 * segments: the distinct (state, inner symbol) pairs in increasing order;
   row[q] is the first segment of state q; arcs are ordered by (state, inner
-  symbol, input position), seg_off[k] is the first arc of segment k.
+  symbol, part, input position), seg_off[k] is the first arc of segment k.
 
 The shapes cover both builds of the library (the per-state build for
 transducers with moderate arcs per state, the global sorts otherwise), the
@@ -42,7 +42,7 @@ def csr_ref(m, by_output):
     inv = inv.reshape(-1)
     part_base = np.searchsorted(uniq[:, 0], np.arange(nq + 1)).astype(np.int64)
     arc_part = inv - part_base[src]
-    order = np.lexsort((np.arange(n), inner, src))
+    order = np.lexsort((np.arange(n), arc_part, inner, src))
     pairs = np.stack([src[order], inner[order]], axis=1)
     head = np.ones(n, bool)
     head[1:] = np.any(pairs[1:] != pairs[:-1], axis=1)

@@ -53,6 +53,14 @@ def product_vs_records(F, m1, m2, what, rtol=1e-6, **kw):
     assert x.num_premerge == y.num_premerge, what
     assert rc.stats["total_product_records"] == 0
     np.testing.assert_allclose(x.w, y.w, rtol=rtol, err_msg=what)
+    # ids in claim order (levels of product sources alone are then written
+    # straight into the result): the same composition, weights bit for bit
+    df = F.compose(m1, m2, product=True, **kw)
+    a, b = canon_of(df.to_host()), canon_of(x)
+    assert np.array_equal(a.states, b.states) and np.array_equal(a.finals, b.finals), what
+    assert np.array_equal(a.keys, b.keys), what
+    assert np.array_equal(a.w.view(np.uint32), b.w.view(np.uint32)), what
+    assert df.num_premerge_arcs == x.num_premerge, what
     return pr
 
 
@@ -253,3 +261,38 @@ def test_product_aligned_lists_differ(fstc):
     assert st["total_product_mfma_sources"] == st["total_product_sources"] > 0
     assert_same(canon_of(pr.to_host()), canon_of(oracle.compose(m1, m2, max_levels=4)),
                 rtol=RTOL, what="config4 missing symbols cap 4")
+
+
+def split_halves(m, inner_is_output, flip):
+    """m with the arcs of slots 0, 1 kept on inner symbols below 32 and those
+    of slots 2, 3 on symbols from 32 on (the reverse when flip): every state
+    keeps 4 parts, two arcs per segment."""
+    inner = (m.olabel if inner_is_output else m.ilabel).astype(np.int64)
+    slot = np.arange(m.num_arcs) % 4
+    low = (slot < 2) != flip
+    keep = np.where(low, inner < 32, inner >= 32)
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, m.src[keep], m.dst[keep],
+                 m.ilabel[keep], m.olabel[keep], m.weight[keep], m.final)
+
+
+@pytest.mark.parametrize("flip", [False, True])
+def test_product_entries_without_terms(fstc, flip):
+    """Every source is a product source whose table has entries without a
+    term (a part of M1 and a part of M2 sharing no inner symbol): on levels
+    of product sources alone the merged arcs are written straight into the
+    result, and the entries without a term leave gaps that are closed
+    afterwards.  Same result as the record path and the oracle."""
+    m1, m2 = W.config4(0, nq=300)
+    m1 = split_halves(m1, True, False)
+    m2 = split_halves(m2, False, flip)
+    pr = product_vs_records(fstc, m1, m2, f"config4 split halves flip={flip}", max_levels=4)
+    st = pr.stats
+    assert st["total_product_sources"] > 0
+    assert st["total_product_records"] == pr.num_premerge_arcs
+    g = pr.to_host()
+    # the levels of product sources alone were written straight to the result
+    assert fstc.compose(m1, m2, max_levels=4).stats["direct_product_levels"] >= 3
+    # fewer merged arcs than table entries: 8 of the 16 entries have terms
+    assert g.num_arcs < 16 * len(np.unique(g.src))
+    assert_same(canon_of(g), canon_of(oracle.compose(m1, m2, max_levels=4)), rtol=RTOL,
+                what=f"config4 split halves flip={flip}")
