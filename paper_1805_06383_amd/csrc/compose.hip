@@ -235,9 +235,46 @@ struct Timer {
   }
 };
 
+// Copies rows [0, used) of ncols columns of 4-byte entries, column i at
+// src + i * sstride (entries) to dst + i * dstride; 16-byte accesses (four
+// entries) when both strides are multiples of four and both bases 16-byte
+// aligned, single entries otherwise.
+__global__ void k_copy_columns(const u32 *src, u64 sstride, u32 *dst, u64 dstride, u64 used,
+                               u32 ncols, u32 vec) {
+  const u64 per = vec ? used / 4 : used;  // units per column
+  const u64 n = per * ncols;
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
+    const u64 c = i / per, k = i - c * per;
+    if (vec) {
+      *reinterpret_cast<uint4 *>(dst + c * dstride + 4 * k) =
+          *reinterpret_cast<const uint4 *>(src + c * sstride + 4 * k);
+    } else {
+      dst[c * dstride + k] = src[c * sstride + k];
+    }
+  }
+  // the last used % 4 entries of each column in the vector form
+  if (vec && blockIdx.x == 0 && threadIdx.x < ncols * 4u) {
+    const u32 c = threadIdx.x / 4, j = threadIdx.x % 4;
+    const u64 k = per * 4 + j;
+    if (k < used) dst[c * dstride + k] = src[c * sstride + k];
+  }
+}
+
+void copy_columns(const void *src, u64 sstride, void *dst, u64 dstride, u64 used, u32 ncols,
+                  hipStream_t s) {
+  if (!used) return;
+  const bool vec = sstride % 4 == 0 && dstride % 4 == 0 &&
+                   reinterpret_cast<uintptr_t>(src) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(dst) % 16 == 0;
+  const u64 units = (vec ? used / 4 : used) * ncols;
+  const unsigned g = (unsigned)std::max<u64>(1, std::min<u64>(ceil_div(units, 256), 8192));
+  hipLaunchKernelGGL(k_copy_columns, dim3(g), dim3(256), 0, s, static_cast<const u32 *>(src),
+                     sstride, static_cast<u32 *>(dst), dstride, used, ncols, vec ? 1u : 0u);
+}
+
 // The five result columns (src, dst, ilabel, olabel, weight; 4 bytes each)
 // in one grow-only buffer: column i at byte i * cap * 4.  Growth is one
-// allocation and one strided copy of the rows kept.
+// allocation and one copy kernel over the rows kept.
 struct ArcCols {
   Buf b;
   u64 cap = 0;  // entries per column
@@ -246,11 +283,11 @@ struct ArcCols {
   explicit ArcCols(Allocator *A, hipStream_t st) : b(A), s(st) {}
   void grow(u64 need, u64 used) {
     if (need <= cap && b.p) return;
-    const u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), grown(5 * cap * 4) / 20);
+    u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), grown(5 * cap * 4) / 20);
+    nc = (nc + 63) & ~63ull;  // columns 256-byte aligned
     Buf nb(b.A);
     nb.ensure(5 * nc * 4);
-    if (used && b.p)
-      FSTC_HIP(hipMemcpy2DAsync(nb.p, nc * 4, b.p, cap * 4, used * 4, 5, hipMemcpyDeviceToDevice, s));
+    if (used && b.p) copy_columns(b.p, cap, nb.p, nc, used, 5, s);
     std::swap(b.p, nb.p);
     std::swap(b.cap, nb.cap);
     cap = nc;

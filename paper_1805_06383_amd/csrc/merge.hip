@@ -1676,55 +1676,77 @@ __global__ __launch_bounds__(256) void k_newlist_sources(MergeArgs a, const u64 
   }
 }
 
-// Direct product level: 16 lanes per source with claims; its claimed entries
-// (kDstClaim in the result's target column, entry order) get ids
-// base + newoff[u], + 1, ..., written to the visited array, the state
-// arrays and the target column.
+// Direct product level: four lanes per source with claims; its claimed
+// entries (kDstClaim in the result's target column, entry order) get ids
+// base + newoff[u], + 1, ..., written to the visited array, the state arrays
+// and the target column.  Lane j of a group holds entries j, j + 4, ... (a
+// source has at most 64), all loaded before any is assigned.
 __global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *newoff, u32 base,
                                                        u32 *sq1, u32 *sq2) {
   const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  const u64 u = t / 16;
-  const u32 j = (u32)(t % 16), lane = lane_id();
+  const u64 u = t / 4;
+  const u32 j = (u32)(t % 4), lane = lane_id();
   const u32 nc = u < a.nsrc ? a.newc[u] : 0u;
   if (__ballot(nc != 0) == 0) return;  // whole wave
-  u64 p0 = 0, n = 0, o = 0;
+  u32 *d = a.out_dst;
+  u32 n = 0, id = 0;
   if (nc) {
-    p0 = a.out_base + a.poff[u];
-    n = a.mend[u] - a.tstart[u];
-    o = newoff[u];
+    d += a.out_base + a.poff[u];
+    n = (u32)(a.mend[u] - a.tstart[u]);
+    id = base + (u32)newoff[u];
   }
-  const u64 gmask = 0xffffull << (lane & ~15u);  // this lane's group of 16
-  u32 done = 0;
-  for (u32 r0 = 0; r0 < (u32)kWave; r0 += 16) {
-    const u64 r = r0 + j;
-    const u32 x = (nc && r < n) ? a.out_dst[p0 + r] : 0u;
-    const bool f = (x & kDstClaim) != 0;
+  u32 x[16];
+#pragma unroll
+  for (u32 k = 0; k < 16; ++k) {
+    const u32 r = 4 * k + j;
+    x[k] = (nc && r < n) ? d[r] : 0u;
+  }
+  const u64 gmask = 0xfull << (lane & ~3u);  // this lane's group of four
+#pragma unroll
+  for (u32 k = 0; k < 16; ++k) {
+    const bool f = (x[k] & kDstClaim) != 0;
     const u64 m = __ballot(f) & gmask;
     if (f) {
-      const u32 slot = x & kDstSlotMask;
-      const u32 id = base + (u32)(o + done + count_below(m));
-      a.vis[slot] = id;
-      sq1[id] = slot / a.vn2;
-      sq2[id] = slot % a.vn2;
-      a.out_dst[p0 + r] = id;
+      const u32 slot = x[k] & kDstSlotMask;
+      const u32 v = id + count_below(m);
+      a.vis[slot] = v;
+      sq1[v] = slot / a.vn2;
+      sq2[v] = slot % a.vn2;
+      d[4 * k + j] = v;
     }
-    done += (u32)__popcll(m);
+    id += (u32)__popcll(m);
   }
 }
 
 // Direct product level, after k_assign_direct: targets still marked
-// kDstSlot (claimed by another source of the level) get their ids.
+// kDstSlot (claimed by another source of the level) get their ids.  Four
+// entries per thread, 16-byte accesses after a head of at most three.
+__device__ __forceinline__ u32 fixed_target(const MergeArgs &a, u32 x) {
+  if (!(x & kDstSlot)) return x;
+  const u64 slot = x & kDstSlotMask;
+  if (slot > a.hmask) {  // impossible: slots index the visited array
+    set_error(&a.st->err, kErrBounds);
+    return x;
+  }
+  return a.vis[slot];
+}
+
 __global__ void k_fix_marked(MergeArgs a, u64 n) {
   u32 *dst = a.out_dst + a.out_base;
-  for (u64 k = (u64)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (u64)gridDim.x * blockDim.x) {
-    const u32 x = dst[k];
-    if (!(x & kDstSlot)) continue;
-    const u64 slot = x & kDstSlotMask;
-    if (slot > a.hmask) {  // impossible: slots index the visited array
-      set_error(&a.st->err, kErrBounds);
-      continue;
-    }
-    dst[k] = a.vis[slot];
+  const u64 head = std::min<u64>(n, (4u - ((u32)(reinterpret_cast<uintptr_t>(dst) >> 2) & 3u)) & 3u);
+  const u64 nv = (n - head) / 4;
+  uint4 *body = reinterpret_cast<uint4 *>(dst + head);
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < nv; i += (u64)gridDim.x * blockDim.x) {
+    const uint4 x = body[i];
+    if (!((x.x | x.y | x.z | x.w) & kDstSlot)) continue;
+    body[i] = make_uint4(fixed_target(a, x.x), fixed_target(a, x.y), fixed_target(a, x.z),
+                         fixed_target(a, x.w));
+  }
+  // the head and the last (n - head) % 4 entries
+  if (blockIdx.x == 0 && threadIdx.x < 8) {
+    const u64 k = threadIdx.x < 4 ? threadIdx.x : head + nv * 4 + (threadIdx.x - 4);
+    const bool mine = threadIdx.x < 4 ? k < head : k < n;
+    if (mine) dst[k] = fixed_target(a, dst[k]);
   }
 }
 
@@ -2164,13 +2186,13 @@ void launch_newlist_sources(const MergeArgs &a, const u64 *newoff, hipStream_t s
 void launch_assign_direct(const MergeArgs &a, const u64 *newoff, u32 base, u32 *sq1, u32 *sq2,
                           hipStream_t s) {
   if (!a.nsrc) return;
-  hipLaunchKernelGGL(k_assign_direct, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256),
-                     0, s, a, newoff, base, sq1, sq2);
+  hipLaunchKernelGGL(k_assign_direct, dim3((unsigned)ceil_div((u64)a.nsrc * 4, 256)), dim3(256), 0,
+                     s, a, newoff, base, sq1, sq2);
 }
 
 void launch_fix_marked(const MergeArgs &a, u64 n, hipStream_t s) {
   if (!n) return;
-  hipLaunchKernelGGL(k_fix_marked, dim3(grid1(n)), dim3(256), 0, s, a, n);
+  hipLaunchKernelGGL(k_fix_marked, dim3(grid1(ceil_div(n, 4) + 1)), dim3(256), 0, s, a, n);
 }
 
 void launch_close_holes(const MergeArgs &a, const u64 *aoff, u64 n, void *tmp, hipStream_t s) {

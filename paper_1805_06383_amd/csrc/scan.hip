@@ -119,13 +119,14 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __shared__ u64 s_off[kLbMax];
   __shared__ u64 scratch[kLbNT / kWave];
   const u32 lane = lane_id();
-  if (threadIdx.x == 0) {
+  // tile numbers from the counter (a single tile needs none)
+  if (threadIdx.x == 0 && p.nb > 1) {
     const u32 t = atomicAdd(p.ctr, 1u);
     if (t == p.nb - 1) atomicExch(p.ctr, 0u);  // the last number is taken: ready for the next call
     s_t = t;
   }
-  __syncthreads();
-  const u32 t = s_t;
+  if (p.nb > 1) __syncthreads();
+  const u32 t = p.nb > 1 ? s_t : 0u;
   const u64 base = (u64)t * kLbTile + (u64)threadIdx.x * kLbIT;  // blocked: kLbIT per thread
   u64 loc[K][kLbIT];
   u64 ex[K], tot[K];
@@ -152,7 +153,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
 #pragma unroll
     for (int k = 0; k < K; ++k) off[k] = 0;
     if (t == 0) {
-      if (lane == 0) {
+      if (lane == 0 && p.nb > 1) {  // a single tile has no successor reading it
 #pragma unroll
         for (int k = 0; k < K; ++k) p.incl[k] = tot[k];
         __hip_atomic_store(&p.flags[0], (p.epoch << 2) | kLbIncl, __ATOMIC_RELEASE,
@@ -212,18 +213,22 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
           if (p.total_to[k]) *p.total_to[k] = off[k] + tot[k];
         }
       }
-      if (t == p.nb - 1 && p.pub.dst) {
-        // every other tile has published its inclusive prefix: the totals
-        // are final
-        const u32 *src = static_cast<const u32 *>(p.pub.src);
-        u32 *dst = static_cast<u32 *>(p.pub.dst);
-        __threadfence();
-        for (u32 i = 0; i < p.pub.words; ++i)
-          if (i != p.pub.seq_word) dst[i] = src[i];
-        __threadfence_system();
+    }
+    if (t == p.nb - 1 && p.pub.dst) {
+      // every other tile has published its inclusive prefix: the totals
+      // are final.  Lane i copies word i (after lane 0's total stores are
+      // visible to the wave), then one lane writes the publication number
+      // once every lane's copy has completed.
+      const u32 *src = static_cast<const u32 *>(p.pub.src);
+      u32 *dst = static_cast<u32 *>(p.pub.dst);
+      __threadfence();
+      for (u32 i = lane; i < p.pub.words; i += kWave)
+        if (i != p.pub.seq_word) dst[i] = src[i];
+      __threadfence_system();
+      __builtin_amdgcn_wave_barrier();
+      if (lane == 0)
         __hip_atomic_store(&dst[p.pub.seq_word], p.pub.seq, __ATOMIC_RELEASE,
                            __HIP_MEMORY_SCOPE_SYSTEM);
-      }
     }
   }
   __syncthreads();
