@@ -463,7 +463,7 @@ void Composer::run(fstc_result *out) {
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),
       aoff(&level_tmp), pk(&level_tmp), pflag(&level_tmp), ftot(&level_tmp), newc(&level_tmp),
-      newoff(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      newoff(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), glist(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -482,7 +482,7 @@ void Composer::run(fstc_result *out) {
     const u64 np1 = (u64)nsrc + 1;
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
     ptot.ensure(np1 * 8); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
-    wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4);
+    wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4); glist.ensure(np1 * 4);
     pk.ensure(np1 * 4); poff.ensure(np1 * 8); pflag.ensure(np1 * 8); ftot.ensure(np1 * 8);
     newc.ensure(np1 * 4); newoff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     wrange.ensure(np1 * sizeof(uint4));
@@ -498,6 +498,11 @@ void Composer::run(fstc_result *out) {
                  product ? 1u : 0u, tstart.as<u64>(), mend.as<u64>()};
     la.pflag = pflag.as<u64>();
     la.newc = newc.as<u32>();
+    // strided product sources four per wave (dense visited array as of the
+    // count; a move to the dense array later in the level keeps them listed)
+    const bool quad = product && dense_vis;
+    la.quad = quad ? 1u : 0u;
+    la.glist = glist.as<u32>();
     T.at(kCount);
     launch_count(la, s);
     // records, matches and product-merge entries per source; the product
@@ -564,6 +569,8 @@ void Composer::run(fstc_result *out) {
       pm.mend = mend.as<u64>();
       pm.pcnt = cnt.as<u64>();
       pm.newc = newc.as<u32>();
+      pm.quad = la.quad;
+      pm.glist = glist.as<u32>();
       if (direct) {
         out_arcs.grow(arcs + (u64)nsrc * maxk, arcs);
         pm.out_src = out_arcs.col(0);
@@ -703,6 +710,8 @@ void Composer::run(fstc_result *out) {
     ma.pcnt = cnt.as<u64>();  // product-merge sources have no records: their slots are free
     ma.newc = newc.as<u32>();
     ma.poff = poff.as<u64>();
+    ma.quad = la.quad;
+    ma.glist = glist.as<u32>();
     ma.prodpos = prodpos;
     ma.row1 = c1.row;
     ma.seg_sym1 = c1.seg_sym;

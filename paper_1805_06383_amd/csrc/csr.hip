@@ -115,16 +115,20 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 // nonzero weight at kCellEmaxShift, the smallest at kCellEminShift) and
 // marks a state of P parts, S segments and P S arcs kCellDense (no segment
 // has more than P arcs, so each has exactly P), and kCellIdent as well when
-// arc i of every segment has part i.
-__global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *arcs,
-                             const u32 *part_base, u32 nq, u32 *flag) {
+// arc i of every segment has part i; kCellContig when its segment symbols
+// are consecutive (the first plus the segment index).
+__global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_off,
+                             const uint2 *arcs, const u32 *part_base, u32 nq, u32 *flag) {
   const u32 lane = lane_id();
   const u64 nw = (u64)gridDim.x * blockDim.x / kWave;
   for (u64 q = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
     bool bad = part_base[q + 1] - part_base[q] > kProdParts, special = false, shuffled = false;
+    bool gap = false;  // a symbol other than the first plus its segment index
     u32 emax = 0, emin = 255;
     if (!bad) {
+      const u32 sym0 = row[q] < row[q + 1] ? seg_sym[row[q]] : 0u;
       for (u32 sg = row[q] + lane; sg < row[q + 1]; sg += kWave) {
+        gap |= seg_sym[sg] != sym0 + (sg - row[q]);
         const u32 a0 = seg_off[sg], n = seg_off[sg + 1] - a0;
         if (n > kProdParts) {
           bad = true;
@@ -146,7 +150,7 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
       }
     }
     const bool any = __ballot(bad) != 0, spec = __ballot(special) != 0;
-    const bool ident = __ballot(shuffled) == 0;
+    const bool ident = __ballot(shuffled) == 0, contig = __ballot(gap) == 0;
     emax = wave_max(emax);
     emin = 255u - wave_max(255u - emin);
     const u32 P = part_base[q + 1] - part_base[q], r0 = row[q], r1 = row[q + 1];
@@ -154,7 +158,7 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_off, const uint2 *ar
     if (lane == 0)
       flag[q] = any ? kCellBad
                     : (spec ? kCellSpecial : 0u) | (dense ? kCellDense : 0u) |
-                          (dense && ident ? kCellIdent : 0u) |
+                          (dense && ident ? kCellIdent : 0u) | (contig ? kCellContig : 0u) |
                           (emax << kCellEmaxShift) | (emin << kCellEminShift);
   }
 }
@@ -514,7 +518,7 @@ __global__ void k_csr_keys(const u32 *src, const u32 *dst, const u32 *il, const 
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s) {
   if (!c.num_states) return;
   const unsigned g = (unsigned)std::min<u64>(ceil_div(c.num_states, kNT / kWave), 1u << 16);
-  hipLaunchKernelGGL(k_cell_flags, dim3(g), dim3(kNT), 0, s, c.row, c.seg_off, c.arcs,
+  hipLaunchKernelGGL(k_cell_flags, dim3(g), dim3(kNT), 0, s, c.row, c.seg_sym, c.seg_off, c.arcs,
                      c.part_base, c.num_states, cell_flag);
 }
 

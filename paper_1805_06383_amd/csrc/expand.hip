@@ -99,8 +99,10 @@ __device__ __forceinline__ bool products_normal(u32 f1, u32 f2) {
 // form (bit 0: at most kProdMfmaParts parts per state, products_normal) and
 // the aligned form (bit 1; both states kCellDense with symbol lists of one
 // length n, at bit 8): the second header word is then (M1 segment begin, its
-// first arc, M2 segment begin, its first arc).  Bit 2: aligned and both
-// states kCellIdent (the strided form of the product kernel).  The cells are single-arc
+// first arc, M2 segment begin, its first arc).  Bit 2: aligned, both states
+// kCellIdent and their symbol lists identical (kCellContig with one first
+// symbol): the strided form, merged four sources per wave with the dense
+// visited array (no symbol check there).  The cells are single-arc
 // only for states of at most kProdParts parts.
 __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1, u32 q2,
                                               const Ranges &r, bool &mfma) {
@@ -112,7 +114,10 @@ __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1,
   mfma = p1 <= kProdMfmaParts && p2 <= kProdMfmaParts && products_normal(f1, f2);
   const u32 n = r.e1 - r.b1;
   const bool aligned = mfma && (f1 & f2 & kCellDense) && n == r.e2 - r.b2;
-  const bool strided = aligned && (f1 & f2 & kCellIdent);
+  // strided: segments ordered by part on both sides and the two symbol
+  // lists identical (consecutive, same first symbol, same length)
+  const bool strided = aligned && (f1 & f2 & kCellIdent) && (f1 & f2 & kCellContig) &&
+                       a.c1.seg_sym[r.b1] == a.c2.seg_sym[r.b2];
   a.phdr[2 * u] = make_uint4(pb1, pb2, p1 | (p2 << 16),
                              (mfma ? 1u : 0u) | (aligned ? 2u | (n << 8) : 0u) |
                                  (strided ? 4u : 0u));
@@ -136,12 +141,12 @@ __device__ __forceinline__ bool thread_join(const LevelArgs &a, const Ranges &r)
 // joins.  List appends and the window maximum are aggregated per workgroup
 // in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
-  __shared__ u32 s_n[3], s_base[3], s_max;
+  __shared__ u32 s_n[4], s_base[4], s_max;
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  if (threadIdx.x < 3) s_n[threadIdx.x] = 0;
+  if (threadIdx.x < 4) s_n[threadIdx.x] = 0;
   if (threadIdx.x == 0) s_max = 0;
-  bool pred[3] = {false, false, false};  // wide, heavy, big
+  bool pred[4] = {false, false, false, false};  // wide, heavy, big, one-per-wave product
   u64 cnt = 0;
   u32 pk = 0;
   bool mf = false;
@@ -160,6 +165,8 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     if (pk) {
       a.cnt[u] = 0;
       a.mc[u] = 0;
+      // strided sources go to the four-source kernel when it runs
+      pred[3] = !(a.quad && (a.phdr[2 * u].w & 4u));
     } else if (mn > kHeavyMin) {
       pred[1] = true;
     } else if (!thread_join(a, r)) {
@@ -177,10 +184,10 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   }
   const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
   __syncthreads();
-  u64 m[3];
-  u32 woff[3];
+  u64 m[4];
+  u32 woff[4];
 #pragma unroll
-  for (int l = 0; l < 3; ++l) {
+  for (int l = 0; l < 4; ++l) {
     m[l] = __ballot(pred[l]);
     woff[l] = 0;
     if (m[l]) {
@@ -191,13 +198,13 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   }
   if (lane == 0 && small_max) atomicMax(&s_max, small_max);
   __syncthreads();
-  u32 *const counters[3] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig};
-  if (threadIdx.x < 3 && s_n[threadIdx.x]) s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
-  if (threadIdx.x == 3 && s_max) atomicMax(&a.st->max_small, s_max);
+  u32 *const counters[4] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig, &a.st->ngen};
+  if (threadIdx.x < 4 && s_n[threadIdx.x]) s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
+  if (threadIdx.x == 4 && s_max) atomicMax(&a.st->max_small, s_max);
   __syncthreads();
-  u32 *const lists[3] = {a.wide, a.heavy, a.big};
+  u32 *const lists[4] = {a.wide, a.heavy, a.big, a.glist};
 #pragma unroll
-  for (int l = 0; l < 3; ++l) {
+  for (int l = 0; l < 4; ++l) {
     if (!pred[l]) continue;
     const u32 pos = s_base[l] + woff[l] + count_below(m[l]);
     lists[l][pos] = (u32)u;

@@ -141,7 +141,9 @@ constexpr u32 kProdParts = 64;
 // consecutive arcs from the state's first plus P i), and kCellIdent besides
 // when, in every segment, arc j has part j (the per-state builds order a
 // segment's arcs by part).
-constexpr u32 kCellBad = 1u, kCellSpecial = 2u, kCellDense = 4u, kCellIdent = 8u;
+// kCellContig: the state's inner symbols are consecutive.
+constexpr u32 kCellBad = 1u, kCellSpecial = 2u, kCellDense = 4u, kCellIdent = 8u,
+              kCellContig = 16u;
 constexpr int kCellEmaxShift = 8, kCellEminShift = 16;
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s);
 

@@ -43,6 +43,8 @@ struct Status {
   u32 nprod_mfma;     // of those, summed on the matrix cores } the level's flag words
   u64 prod_records;   // their joined arc pairs (not written as records)
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
+  u32 ngen;           // product-merge sources listed for the one-per-wave kernel
+  u32 pad1;
 };
 static_assert(offsetof(Status, nprod) % 8 == 0 &&
                   offsetof(Status, nprod_mfma) == offsetof(Status, nprod) + 4,
@@ -134,6 +136,9 @@ struct LevelArgs {
                          // kernel, written by the product merge
   u64 *pflag;            // [nsrc] 1 for a product-merge source, plus 2^32 when it
                          // takes the matrix-core form (summed by the level scan)
+  u32 quad;              // nonzero: strided product sources go to the four-source
+                         // kernel (dense visited array), the others to glist
+  u32 *glist;            // [nsrc] product sources for the one-per-wave kernel (st->ngen)
 };
 
 // Target column marks of a direct product level (MergeArgs::out_src), and
@@ -203,6 +208,8 @@ struct MergeArgs {
   u32 *newc;  // [nsrc] new pairs each product-merge source claimed (written by it)
   const u64 *R_dev;  // product merge launched before the host knew R: the level's
                      // record count on the device (the kernel merges only if 0)
+  u32 quad;          // the strided product sources are merged four per wave
+  const u32 *glist;  // the other product sources (st->ngen of them)
   // direct product level (out_src != NULL; dense visited array only): the
   // product kernel writes source u's merged arcs straight to the result
   // columns at out_base + poff[u] + r instead of to temp, with the target
@@ -226,8 +233,10 @@ void launch_merge_sort(const MergeArgs &a, bool wide_keys, hipStream_t s);
 // sources, 32-bit record keys).  narrow: both arc arrays below 2^29 arcs.
 void launch_fuse_merge(const MergeArgs &a, bool narrow, hipStream_t s);
 // Product merge of the sources with a.pk[u] != 0: their merged arcs, with
-// visited-table inserts, at temp[R + poff[u] ...) and tstart / mend.
-// narrow: both arc arrays below 2^29 arcs.
+// visited-table inserts, at temp[R + poff[u] ...) (or the result, on a
+// direct level) and tstart / mend: with a.quad, the strided sources four per
+// wave and the listed ones (a.glist) one per wave; else every one of them
+// one per wave from the list.  narrow: both arc arrays below 2^29 arcs.
 void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s);
 // Multi-block merge of the nbig sources listed in a.big; bigoff has nbig + 1
 // entries (exclusive scan of their record counts, total RB).

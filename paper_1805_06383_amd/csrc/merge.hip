@@ -926,22 +926,15 @@ __device__ __forceinline__ uint2 prod_arc(const uint2 *arcs, u32 j) {
   return arcs[j];
 }
 
+__device__ __forceinline__ u32 uni(u32 x) { return (u32)__builtin_amdgcn_readfirstlane((int)x); }
+
+// One product source u (K table entries, header h0 h1) merged by the whole
+// wave; val is the wave's LDS cells.
 template <bool NARROW>
-__global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
-  // M1 (g, p1), M2 (g, p2); a spare cell; rows 16-byte aligned
-  __shared__ __align__(16) u32 s_val[kProdWaves][kProdCells + 4];
-  // launched before the host read the level's record count: nothing to do
-  // unless the level has no records (then a.R is 0)
-  if (a.R_dev && *a.R_dev != 0) return;
+__device__ __forceinline__ void prod_one(const MergeArgs &a, u64 u, u32 K, uint4 h0, uint4 h1,
+                                         u32 *val) {
   // everything about the source is wave-uniform: scalar registers
-  auto uni = [](u32 x) { return (u32)__builtin_amdgcn_readfirstlane((int)x); };
-  const u32 lane = lane_id(), w = uni(threadIdx.x / kWave);
-  const u64 u = (u64)blockIdx.x * kProdWaves + w;
-  if (u >= a.nsrc) return;  // whole wave
-  const u32 K = uni(a.pk[u]);
-  const uint4 h0 = a.phdr[2 * u], h1 = a.phdr[2 * u + 1];  // loaded with pk, used if K != 0
-  if (K == 0) return;  // whole wave: record path
-  u32 *val = s_val[w];
+  const u32 lane = lane_id();
   const u32 pb1 = uni(h0.x), pb2 = uni(h0.y), P1 = uni(h0.z & 0xffffu), P2 = uni(h0.z >> 16);
   const u32 hf = uni(h0.w);
   const bool mf = (hf & 1u) != 0;       // matrix-core form
@@ -1299,6 +1292,139 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
     a.mend[u] = base + nr;
     a.pcnt[u] = pairs;
     a.newc[u] = nclaim;
+  }
+}
+
+// The listed product sources (a.glist, st->ngen of them), one per wave: the
+// waves of the grid take list entries wave, wave + waves, ...  Launched
+// before the host knows the list length, so the grid is sized by the level.
+template <bool NARROW>
+__global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
+  // M1 (g, p1), M2 (g, p2); a spare cell; rows 16-byte aligned
+  __shared__ __align__(16) u32 s_val[kProdWaves][kProdCells + 4];
+  // launched before the host read the level's record count: nothing to do
+  // unless the level has no records (then a.R is 0)
+  if (a.R_dev && *a.R_dev != 0) return;
+  const u32 w = uni(threadIdx.x / kWave);
+  const u32 n = uni(__hip_atomic_load(&a.st->ngen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  const u32 nw = gridDim.x * kProdWaves;
+  for (u32 i = blockIdx.x * kProdWaves + w; i < n; i += nw) {
+    const u64 u = uni(a.glist[i]);
+    if (u >= a.nsrc) {  // impossible: the count kernel lists level sources
+      if (lane_id() == 0) set_error(&a.st->err, kErrBounds);
+      return;
+    }
+    const u32 K = uni(a.pk[u]);
+    const uint4 h0 = a.phdr[2 * u], h1 = a.phdr[2 * u + 1];
+    if (K == 0) continue;  // impossible: only product sources are listed
+    // the previous source's LDS reads are done before this one's writes
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    prod_one<NARROW>(a, u, K, h0, h1, s_val[w]);
+  }
+}
+
+// Strided product sources four per wave (dense visited array).  The
+// v_mfma_f64_4x4x4f64 instruction works on four independent 4 x 4 blocks;
+// block b = (l / 4) mod 4 takes source 4 (wave) + b.  For instruction t
+// lane l supplies, for its block's source, the weights of symbol
+// 4 t + l / 16, part l mod 4 of both states (zero past the source's parts
+// or symbols); after sixteen instructions (64 symbols) lane l holds entry
+// (l / 16, l mod 4) of its source, so every lane owns one entry and the
+// claims and stores of four sources run side by side.  Sums and entry
+// order are those of the one-per-wave kernel's matrix-core form.
+template <bool NARROW>
+__global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
+  if (a.R_dev && *a.R_dev != 0) return;
+  if (!a.vn2) {  // impossible: launched with the dense visited array only
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  const u32 lane = lane_id();
+  const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  const u32 b = (lane >> 2) & 3u;
+  const u64 u = wv * 4 + b;
+  const bool in = u < a.nsrc;
+  const u64 uc = in ? u : 0;
+  const u32 K = in ? a.pk[uc] : 0u;
+  const uint4 h0 = a.phdr[2 * uc], h1 = a.phdr[2 * uc + 1];
+  bool mine = K != 0 && (h0.w & 4u) != 0;
+  const u32 P1 = mine ? h0.z & 0xffffu : 0u, P2 = mine ? h0.z >> 16 : 0u;
+  const u32 na = mine ? h0.w >> 8 : 0u;
+  if (mine && (P1 * P2 != K || P1 > kProdRow || P2 > kProdRow || na == 0 || na > (u32)kWave)) {
+    set_error(&a.st->err, kErrBounds);  // impossible: the selection checked all of it
+    mine = false;
+  }
+  if (__ballot(mine) == 0) return;  // whole wave
+  const u32 pb1 = mine ? h0.x : 0u, pb2 = mine ? h0.y : 0u;
+  const u32 ab1 = mine ? h1.y : 0u, ab2 = mine ? h1.w : 0u;
+  const u32 p1 = lane >> 4, p2 = lane & 3u;
+  const bool own = mine && p1 < P1 && p2 < P2;
+  // the owned entry's parts and visited-array entry, issued first
+  const uint2 L1 = a.parts1[own ? pb1 + p1 : 0u], L2 = a.parts2[own ? pb2 + p2 : 0u];
+  const u64 hslot = own ? (u64)L1.x * a.vn2 + L2.x : 0;
+  const u32 hcur = __hip_atomic_load(&a.vis[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  const u64 pu = mine ? a.poff[u] : 0;
+  // the weight words of the operands (arc j's weight is word 2 j + 1)
+  const u32 *wt1 = reinterpret_cast<const u32 *>(a.arcs1) + 1;
+  const u32 *wt2 = reinterpret_cast<const u32 *>(a.arcs2) + 1;
+  const u32 q = lane & 3u, gk = lane >> 4;
+  u32 x1[16], x2[16];
+  u32 v1 = 0, v2 = 0;  // bit t: operand t present
+#pragma unroll
+  for (u32 t = 0; t < 16; ++t) {
+    const u32 g = 4u * t + gk;
+    const bool i1 = g < na && q < P1, i2 = g < na && q < P2;
+    v1 |= (i1 ? 1u : 0u) << t;
+    v2 |= (i2 ? 1u : 0u) << t;
+    const u32 j1 = i1 ? ab1 + P1 * g + q : 0u, j2 = i2 ? ab2 + P2 * g + q : 0u;
+    if (NARROW) {
+      x1[t] = *reinterpret_cast<const u32 *>(reinterpret_cast<const char *>(wt1) + (j1 << 3));
+      x2[t] = *reinterpret_cast<const u32 *>(reinterpret_cast<const char *>(wt2) + (j2 << 3));
+    } else {
+      x1[t] = wt1[2 * (u64)j1];
+      x2[t] = wt2[2 * (u64)j2];
+    }
+  }
+  double d = 0.0;
+#pragma unroll
+  for (u32 t = 0; t < 16; ++t) {
+    const double x = ((v1 >> t) & 1u) ? (double)__uint_as_float(x1[t]) : 0.0;
+    const double y = ((v2 >> t) & 1u) ? (double)__uint_as_float(x2[t]) : 0.0;
+    d = __builtin_amdgcn_mfma_f64_4x4x4f64(x, y, d, 0, 0, 0);
+  }
+  // merged arcs in entry order within each source (lane order within a
+  // block is (p1, p2) order); every entry has na terms
+  const u64 bmask = 0x000f000f000f000full << (4u * b);
+  const u64 rm = __ballot(own);
+  const u32 rank = count_below(rm & bmask);
+  bool claimed = false;
+  if (own) {
+    const bool is_new = hcur == kUnvisited &&
+                        atomicCAS(&a.vis[hslot], kUnvisited, kClaimed) == kUnvisited;
+    claimed = is_new;
+    const bool known = hcur < kClaimed;  // an id from an earlier level
+    if (a.out_src) {
+      const u64 p = a.out_base + pu + rank;
+      a.out_src[p] = a.lo + (u32)u;
+      a.out_dst[p] = known ? hcur : ((u32)hslot | kDstSlot | (is_new ? kDstClaim : 0u));
+      a.out_il[p] = L1.y;
+      a.out_ol[p] = L2.y;
+      a.out_w[p] = (float)d;
+    } else {
+      const u64 t = a.R + pu + rank;
+      a.temp[t] = make_uint4(known ? (hcur | kIdFlag) : ((u32)hslot | (is_new ? kNewFlag : 0u)),
+                             L1.y, L2.y, __float_as_uint((float)d));
+      a.runsrc[t] = (u32)u;
+    }
+  }
+  const u64 cm = __ballot(claimed);
+  if (mine && lane == 4u * b) {  // entry (0, 0) of the source
+    a.tstart[u] = a.R + pu;
+    a.mend[u] = a.R + pu + K;
+    a.pcnt[u] = (u64)na * K;
+    a.newc[u] = (u32)__popcll(cm & bmask);
   }
 }
 
@@ -2016,6 +2142,7 @@ __device__ __forceinline__ void clear_level(Status *st) {
   st->nprod = st->nprod_mfma = 0;
   st->prod_records = st->prod_entries = 0;
   st->nsort = 0;
+  st->ngen = 0;
 }
 
 
@@ -2170,7 +2297,15 @@ void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, 
 
 void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s) {
   if (!a.nsrc) return;
-  const unsigned g = (unsigned)ceil_div(a.nsrc, kProdWaves);
+  if (a.quad) {
+    const unsigned gq = (unsigned)ceil_div(ceil_div(a.nsrc, 4), 256 / kWave);
+    if (narrow) hipLaunchKernelGGL(k_prod_quad<true>, dim3(gq), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(k_prod_quad<false>, dim3(gq), dim3(256), 0, s, a);
+  }
+  // the listed sources: at most one wave per level source, and at most as
+  // many waves as the chip holds at once (they loop over the list)
+  const u64 waves = std::min<u64>(a.nsrc, (u64)compute_units() * 32);
+  const unsigned g = (unsigned)ceil_div(waves, kProdWaves);
   if (narrow)
     hipLaunchKernelGGL(k_prod_sources<true>, dim3(g), dim3(kProdNT), 0, s, a);
   else
