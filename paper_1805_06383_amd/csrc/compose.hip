@@ -463,7 +463,7 @@ void Composer::run(fstc_result *out) {
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),
       aoff(&level_tmp), pk(&level_tmp), pflag(&level_tmp), ftot(&level_tmp), newc(&level_tmp),
-      newoff(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), glist(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
+      newoff(&level_tmp), phdr(&level_tmp), poff(&level_tmp), wrange(&level_tmp), glist(&level_tmp), grp(&level_tmp), wide(&level_tmp), heavy(&level_tmp), big(&level_tmp),
       bigcnt(&level_tmp), bigoff(&level_tmp), match(&level_tmp), mrbase(&level_tmp),
       rkey(&level_tmp), rw(&level_tmp), temp(&level_tmp), newlist(&level_tmp), stmp(&level_tmp),
       dk(&level_tmp), dv(&level_tmp), dka(&level_tmp), dva(&level_tmp), dtmp(&level_tmp),
@@ -483,6 +483,7 @@ void Composer::run(fstc_result *out) {
     cnt.ensure(np1 * 8); mc.ensure(np1 * 4); roff.ensure(np1 * 8); moff.ensure(np1 * 8);
     ptot.ensure(np1 * 8); aoff.ensure(np1 * 8); tstart.ensure(np1 * 8); mend.ensure(np1 * 8);
     wide.ensure(np1 * 4); heavy.ensure(np1 * 4); big.ensure(np1 * 4); glist.ensure(np1 * 4);
+    grp.ensure(np1 * 4);
     pk.ensure(np1 * 4); poff.ensure(np1 * 8); pflag.ensure(np1 * 8); ftot.ensure(np1 * 8);
     newc.ensure(np1 * 4); newoff.ensure(np1 * 8); phdr.ensure(np1 * 2 * sizeof(uint4));
     wrange.ensure(np1 * sizeof(uint4));
@@ -503,6 +504,7 @@ void Composer::run(fstc_result *out) {
     const bool quad = product && dense_vis;
     la.quad = quad ? 1u : 0u;
     la.glist = glist.as<u32>();
+    la.grp = grp.as<u32>();
     T.at(kCount);
     launch_count(la, s);
     // records, matches and product-merge entries per source; the product
@@ -654,7 +656,7 @@ void Composer::run(fstc_result *out) {
     la.mrbase = mrbase.as<u64>();
     la.tiles = tiles_e.as<ExpandTile>();
     T.at(kExpand);
-    if (M) launch_emit(la, hs->st.nwide, hs->st.nheavy, s);
+    if (M) launch_emit(la, hs->st.nwide, hs->st.nheavy, hs->st.ngrp, s);
     // fused levels generate each tile's records inside the merge instead
     const bool fuse = o.fused_merge && !o.no_reduction && key_bits <= kDenseKeyBits && nbig == 0;
     if (!fuse && R) {

@@ -15,8 +15,9 @@
 //              level's composed arcs, whatever the fan-out of the sources
 //              inside it, so work is balanced across the chip and every
 //              store is coalesced.
-// Joins are done per thread, per wavefront or per workgroup depending on the
-// length of the shorter segment list (kWideMin / kHeavyMin).
+// Joins are done per thread, per 16-lane group, per wavefront or per
+// workgroup depending on the lengths of the two segment lists (the rules
+// beside kThreadSteps).
 #include "level.hpp"
 
 namespace fstc {
@@ -126,13 +127,16 @@ __device__ __forceinline__ u32 select_product(const LevelArgs &a, u32 u, u32 q1,
   return p1 * p2;
 }
 
-// True when source ranges r are joined by one thread (the rule beside
-// kWideMin); the count and emit kernels classify alike.
-__device__ __forceinline__ bool thread_join(const LevelArgs &a, const Ranges &r) {
+// How source ranges r are joined (the rules beside kThreadSteps; sources
+// of more than kHeavyMin symbols on the shorter list are classified before);
+// the count and emit kernels classify alike.
+enum : u32 { kJoinThread = 0, kJoinGroup = 1, kJoinWide = 2 };
+__device__ __forceinline__ u32 join_class(const Ranges &r) {
   const u32 n1 = r.e1 - r.b1, n2 = r.e2 - r.b2;
   const u32 mn = min(n1, n2), mx = max(n1, n2);
-  if (mn > kWideMin) return false;
-  return a.nsrc >= kFewSources || mn * (32u - __clz(mx)) <= kSerialSteps;
+  if (mn * (32u - __clz(mx)) <= kThreadSteps) return kJoinThread;
+  if (mn <= kGroupMax && mx <= kGroupLong) return kJoinGroup;
+  return kJoinWide;
 }
 
 // Thread per source: selects the product-merge sources (no records, no
@@ -141,12 +145,14 @@ __device__ __forceinline__ bool thread_join(const LevelArgs &a, const Ranges &r)
 // joins.  List appends and the window maximum are aggregated per workgroup
 // in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
-  __shared__ u32 s_n[4], s_base[4], s_max;
+  constexpr int kLists = 5;
+  __shared__ u32 s_n[kLists], s_base[kLists], s_max;
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  if (threadIdx.x < 4) s_n[threadIdx.x] = 0;
+  if (threadIdx.x < kLists) s_n[threadIdx.x] = 0;
   if (threadIdx.x == 0) s_max = 0;
-  bool pred[4] = {false, false, false, false};  // wide, heavy, big, one-per-wave product
+  // wide, heavy, big, one-per-wave product, 16-lane join
+  bool pred[kLists] = {false, false, false, false, false};
   u64 cnt = 0;
   u32 pk = 0;
   bool mf = false;
@@ -169,8 +175,10 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
       pred[3] = !(a.quad && (a.phdr[2 * u].w & 4u));
     } else if (mn > kHeavyMin) {
       pred[1] = true;
-    } else if (!thread_join(a, r)) {
+    } else if (join_class(r) == kJoinWide) {
       pred[0] = true;
+    } else if (join_class(r) == kJoinGroup) {
+      pred[4] = true;
     } else {
       u32 mc = 0;
       intersect_serial(a.c1.seg_sym, r.b1, r.e1, a.c2.seg_sym, r.b2, r.e2, [&](u32 s1, u32 s2) {
@@ -184,10 +192,10 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   }
   const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
   __syncthreads();
-  u64 m[4];
-  u32 woff[4];
+  u64 m[kLists];
+  u32 woff[kLists];
 #pragma unroll
-  for (int l = 0; l < 4; ++l) {
+  for (int l = 0; l < kLists; ++l) {
     m[l] = __ballot(pred[l]);
     woff[l] = 0;
     if (m[l]) {
@@ -198,13 +206,15 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   }
   if (lane == 0 && small_max) atomicMax(&s_max, small_max);
   __syncthreads();
-  u32 *const counters[4] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig, &a.st->ngen};
-  if (threadIdx.x < 4 && s_n[threadIdx.x]) s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
-  if (threadIdx.x == 4 && s_max) atomicMax(&a.st->max_small, s_max);
+  u32 *const counters[kLists] = {&a.st->nwide, &a.st->nheavy, &a.st->nbig, &a.st->ngen,
+                                 &a.st->ngrp};
+  if (threadIdx.x < kLists && s_n[threadIdx.x])
+    s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
+  if (threadIdx.x == kLists && s_max) atomicMax(&a.st->max_small, s_max);
   __syncthreads();
-  u32 *const lists[4] = {a.wide, a.heavy, a.big, a.glist};
+  u32 *const lists[kLists] = {a.wide, a.heavy, a.big, a.glist, a.grp};
 #pragma unroll
-  for (int l = 0; l < 4; ++l) {
+  for (int l = 0; l < kLists; ++l) {
     if (!pred[l]) continue;
     const u32 pos = s_base[l] + woff[l] + count_below(m[l]);
     lists[l][pos] = (u32)u;
@@ -374,15 +384,121 @@ __device__ __forceinline__ void count_heavy_sources(const LevelArgs &a, u32 blk,
   }
 }
 
-__global__ __launch_bounds__(kListNT) void k_count_lists(LevelArgs a, u32 gw) {
+// Join of one source by a group of kGroupLanes lanes (group-uniform
+// control flow; the group's lanes are all active): chunks of 16 symbols of
+// the shorter list, each searched by a 4-step binary search over lane
+// shuffles in 16-symbol chunks of the longer list, starting from the first
+// chunk that can still match (it only moves forward).  Calls f(s1, s2, m,
+// j) once per chunk of the shorter list, in increasing symbol order, with
+// (s1, s2) this lane's match (m: whether it has one) and j its group lane.
+template <class F>
+__device__ __forceinline__ void group_join(const LevelArgs &a, const Ranges &r, F &&f) {
+  constexpr int G = kGroupLanes;
+  const u32 j = lane_id() % G;
+  const bool one_short = (r.e1 - r.b1) <= (r.e2 - r.b2);
+  const u32 *ssym = one_short ? a.c1.seg_sym : a.c2.seg_sym;
+  const u32 *lsym = one_short ? a.c2.seg_sym : a.c1.seg_sym;
+  const u32 bs = one_short ? r.b1 : r.b2, es = one_short ? r.e1 : r.e2;
+  const u32 le = one_short ? r.e2 : r.e1;
+  u32 lp = one_short ? r.b2 : r.b1;
+  for (u32 base = bs; base < es; base += G) {
+    const u32 idx = base + j;
+    const bool valid = idx < es;
+    const u32 sym = valid ? ssym[idx] : 0xffffffffu;  // labels are below 2^32 - 1
+    const u32 last = min(es - base, (u32)G) - 1;
+    const u32 smax = __shfl(sym, (int)last, G);
+    u32 fpos = 0xffffffffu;
+    for (u32 c = lp; c < le; c += G) {
+      const u32 len = min(le - c, (u32)G);
+      const u32 lv = j < len ? lsym[c + j] : 0xffffffffu;
+      if (__shfl(lv, 0, G) > smax) break;  // this chunk and later ones are past the short chunk
+      u32 pos = 0;  // elements of the chunk below sym (at most 15)
+#pragma unroll
+      for (u32 step = G / 2; step; step >>= 1) {
+        const u32 v = __shfl(lv, (int)(pos + step - 1), G);
+        pos = v < sym ? pos + step : pos;
+      }
+      const u32 at = __shfl(lv, (int)pos, G);
+      if (valid && at == sym) fpos = c + pos;
+      if (__shfl(lv, (int)(len - 1), G) >= smax) {  // later short symbols start in this chunk
+        lp = c;
+        break;
+      }
+      lp = c + G;
+    }
+    const bool m = fpos != 0xffffffffu;
+    f(one_short ? idx : fpos, one_short ? fpos : idx, m, j);
+  }
+}
+
+// Sum over the kGroupLanes lanes of this lane's group.
+template <class T>
+__device__ __forceinline__ T group_sum(T x) {
+#pragma unroll
+  for (int d = kGroupLanes / 2; d > 0; d >>= 1) x += __shfl_xor(x, d, kGroupLanes);
+  return x;
+}
+
+// Inclusive prefix sum over the lanes of this lane's group.
+template <class T>
+__device__ __forceinline__ T group_inclusive_sum(T x) {
+  const u32 j = lane_id() % kGroupLanes;
+#pragma unroll
+  for (u32 d = 1; d < kGroupLanes; d <<= 1) {
+    const T y = __shfl_up(x, d, kGroupLanes);
+    if (j >= d) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ void count_group_sources(const LevelArgs &a, u32 blk, u32 nblk,
+                                                    u32 &run_max) {
+  constexpr u32 G = kGroupLanes;
+  const u32 gi = (blk * kListNT + threadIdx.x) / G;
+  const u32 ng = nblk * kListNT / G;
+  const u32 n = a.st->ngrp;
+  // every group of a wave runs the same number of rounds, so that the
+  // wave's lanes stay together; a group past the list idles
+  const u32 gw0 = gi - (threadIdx.x % kWave) / G;  // first group of this wave
+  for (u32 i0 = gw0; i0 < n; i0 += ng) {
+    const u32 i = i0 + (threadIdx.x % kWave) / G;
+    const bool have = i < n;
+    const u32 u = have ? a.grp[i] : 0u;
+    u64 cnt = 0;
+    u32 mc = 0;
+    if (have) {
+      const Ranges r = source_ranges(a, u);
+      group_join(a, r, [&](u32 s1, u32 s2, bool m, u32) {
+        if (m) {
+          cnt += (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2);
+          ++mc;
+        }
+      });
+    }
+    cnt = group_sum(cnt);
+    mc = group_sum(mc);
+    if (have && threadIdx.x % G == 0) {
+      a.cnt[u] = cnt;
+      a.mc[u] = mc;
+      note_count(a, u, cnt, run_max);
+    }
+  }
+}
+
+// The listed joins: blocks [0, gg) the 16-lane joins, [gg, gg + gw) the
+// wavefront joins, the rest the workgroup joins (each grid-stride over its
+// list).
+__global__ __launch_bounds__(kListNT) void k_count_lists(LevelArgs a, u32 gg, u32 gw) {
   __shared__ u64 s64[kListNT / kWave];
   __shared__ u32 s32[kListNT / kWave];
   __shared__ u32 s_max;
   u32 run_max = 0;
-  if (blockIdx.x < gw)
-    count_wide_sources(a, blockIdx.x, gw, run_max);
+  if (blockIdx.x < gg)
+    count_group_sources(a, blockIdx.x, gg, run_max);
+  else if (blockIdx.x < gg + gw)
+    count_wide_sources(a, blockIdx.x - gg, gw, run_max);
   else
-    count_heavy_sources(a, blockIdx.x - gw, gridDim.x - gw, run_max, s64, s32);
+    count_heavy_sources(a, blockIdx.x - gg - gw, gridDim.x - gg - gw, run_max, s64, s32);
   publish_max<kListNT>(a, run_max, &s_max);
 }
 
@@ -403,13 +519,40 @@ __global__ __launch_bounds__(256) void k_emit_small(LevelArgs a) {
   if (u >= a.nsrc) return;
   if (a.pk[u]) return;  // product merge: no matches, no records
   const Ranges r = source_ranges(a, (u32)u);
-  if (!thread_join(a, r)) return;
+  if (join_class(r) != kJoinThread) return;  // listed (heavy sources are never thread joins)
   u64 k = a.moff[u], rb = a.roff[u];
   intersect_serial(a.c1.seg_sym, r.b1, r.e1, a.c2.seg_sym, r.b2, r.e2, [&](u32 s1, u32 s2) {
     put_match(a, k, s1, s2, rb);
     rb += (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2);
     ++k;
   });
+}
+
+// The listed 16-lane joins: each group writes its source's match
+// descriptors in symbol order.
+__global__ __launch_bounds__(256) void k_emit_group(LevelArgs a) {
+  constexpr u32 G = kGroupLanes;
+  const u32 gi = (blockIdx.x * blockDim.x + threadIdx.x) / G;
+  const u32 ng = gridDim.x * blockDim.x / G;
+  const u32 n = a.st->ngrp;
+  const u32 gw0 = gi - (threadIdx.x % kWave) / G;  // first group of this wave
+  const u64 gmask = 0xffffull << (lane_id() & ~(G - 1));
+  for (u32 i0 = gw0; i0 < n; i0 += ng) {
+    const u32 i = i0 + (threadIdx.x % kWave) / G;
+    if (i >= n) continue;  // group-uniform; shuffles stay within groups
+    const u32 u = a.grp[i];  // never a product source
+    const Ranges r = source_ranges(a, u);
+    u64 k = a.moff[u], rb = a.roff[u];
+    group_join(a, r, [&](u32 s1, u32 s2, bool m, u32) {
+      const u64 prod = m ? (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2) : 0;
+      const u64 fm = __ballot(m) & gmask;
+      const u64 incl = group_inclusive_sum(prod);
+      const u64 total = __shfl(incl, (int)(G - 1), G);
+      if (m) put_match(a, k + count_below(fm), s1, s2, rb + incl - prod);
+      k += (u64)__popcll(fm);
+      rb += total;
+    });
+  }
 }
 
 __global__ __launch_bounds__(256) void k_emit_wide(LevelArgs a) {
@@ -676,17 +819,26 @@ static unsigned heavy_grid(u64 n) { return (unsigned)std::min<u64>(512, n); }
 void launch_count(const LevelArgs &a, hipStream_t s) {
   const unsigned g = (unsigned)ceil_div(a.nsrc, kCountNT);
   hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
-  // wide: at most one wave per source (1024 blocks of 8 waves at most);
-  // heavy: one block per source (512 blocks at most)
+  // 16-lane joins: at most one group per source, at most as many waves as
+  // the chip holds (they loop over the list); wide: at most one wave per
+  // source (1024 blocks of 8 waves at most); heavy: one block per source
+  // (512 blocks at most)
   const u64 n = a.nsrc;
+  const unsigned gg = (unsigned)std::min<u64>((u64)compute_units() * 4,
+                                              ceil_div(n, kListNT / kGroupLanes));
   const unsigned gw = (unsigned)std::min<u64>(1024, ceil_div(n, kListNT / kWave));
   const unsigned gh = (unsigned)std::min<u64>(512, n);
-  hipLaunchKernelGGL(k_count_lists, dim3(gw + gh), dim3(kListNT), 0, s, a, gw);
+  hipLaunchKernelGGL(k_count_lists, dim3(gg + gw + gh), dim3(kListNT), 0, s, a, gg, gw);
 }
 
-void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s) {
+void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, u32 ngrp, hipStream_t s) {
   const unsigned g = (unsigned)ceil_div(a.nsrc, 256);
   hipLaunchKernelGGL(k_emit_small, dim3(g), dim3(256), 0, s, a);
+  if (ngrp) {
+    const unsigned gg = (unsigned)std::min<u64>((u64)compute_units() * 8,
+                                                ceil_div((u64)ngrp, 256 / kGroupLanes));
+    hipLaunchKernelGGL(k_emit_group, dim3(gg), dim3(256), 0, s, a);
+  }
   if (nwide) hipLaunchKernelGGL(k_emit_wide, dim3(wide_grid(nwide)), dim3(256), 0, s, a);
   if (nheavy) hipLaunchKernelGGL(k_emit_heavy, dim3(heavy_grid(nheavy)), dim3(kHeavyNT), 0, s, a);
 }

@@ -44,7 +44,7 @@ struct Status {
   u64 prod_records;   // their joined arc pairs (not written as records)
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
   u32 ngen;           // product-merge sources listed for the one-per-wave kernel
-  u32 pad1;
+  u32 ngrp;           // sources listed for the 16-lane joins
 };
 static_assert(offsetof(Status, nprod) % 8 == 0 &&
                   offsetof(Status, nprod_mfma) == offsetof(Status, nprod) + 4,
@@ -64,16 +64,17 @@ constexpr u32 kProdMinSymbols = 8;
 // are summed on the matrix cores (merge.hip).
 constexpr u32 kProdMfmaParts = 4;
 
-// A source whose shorter segment list is longer than kWideMin is joined by a
-// wavefront, longer than kHeavyMin by a workgroup; others by one thread,
-// except on levels of fewer than kFewSources sources (too few threads to
-// hide a long chain of dependent loads), where a source whose serial join
-// takes more than kSerialSteps binary-search steps (shorter length x bits of
-// the longer length) goes to a wavefront too.
-constexpr u32 kWideMin = 24;
+// Joins: a source whose serial join takes at most kThreadSteps binary-search
+// steps (shorter length x bits of the longer length) is joined by one
+// thread; one whose shorter list has at most kGroupMax symbols and whose
+// longer one at most kGroupLong, by a group of kGroupLanes lanes; one whose
+// shorter list is longer than kHeavyMin, by a workgroup; the others by a
+// wavefront.
+constexpr u32 kThreadSteps = 12;
+constexpr u32 kGroupLanes = 16;
+constexpr u32 kGroupMax = 32;
+constexpr u32 kGroupLong = 512;
 constexpr u32 kHeavyMin = 2048;
-constexpr u32 kFewSources = 1u << 16;
-constexpr u32 kSerialSteps = 48;
 
 // Merge tiles: 512 threads x 8 items = 4096 records of LDS capacity.  Sources
 // of more than kMergeSmall records take the multi-block path.  A tile takes
@@ -139,6 +140,7 @@ struct LevelArgs {
   u32 quad;              // nonzero: strided product sources go to the four-source
                          // kernel (dense visited array), the others to glist
   u32 *glist;            // [nsrc] product sources for the one-per-wave kernel (st->ngen)
+  u32 *grp;              // [nsrc] sources for the 16-lane joins (st->ngrp)
 };
 
 // Target column marks of a direct product level (MergeArgs::out_src), and
@@ -151,8 +153,9 @@ constexpr u32 kHoleSrc = 0xffffffffu;
 // range begin, end, M2 segment range begin, end).
 
 void launch_count(const LevelArgs &a, hipStream_t s);
-// nwide / nheavy: the list lengths the count kernels produced (st->nwide, nheavy).
-void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, hipStream_t s);
+// nwide / nheavy / ngrp: the list lengths the count kernels produced
+// (st->nwide, nheavy, ngrp).
+void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, u32 ngrp, hipStream_t s);
 // Writes R records: key = (part1 << b2) | part2 (u32 when key_bits <= 32,
 // else u64), weight = p1 * p2.
 // tiles: the ceil(R / kExpandTile) write-tile entries written by launch_emit.

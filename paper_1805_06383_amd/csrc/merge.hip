@@ -2143,6 +2143,7 @@ __device__ __forceinline__ void clear_level(Status *st) {
   st->prod_records = st->prod_entries = 0;
   st->nsort = 0;
   st->ngen = 0;
+  st->ngrp = 0;
 }
 
 
