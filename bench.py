@@ -329,6 +329,7 @@ def main():
             "levels": last.num_levels,
             "input_sha256": [h1.digest()[:16], h2.digest()[:16]],
         },
+        "peak_device_GiB": last.stats["peak_device_bytes"] / 2**30,
         "post_merge_arcs_per_s": post_rate,
         # one more, untimed step with an event at every phase boundary (the
         # timed steps record events around the single-kernel phases only)

@@ -211,6 +211,9 @@ typedef struct fstc_stats {
                                      merged arcs the product kernel wrote
                                      straight into the result              */
   uint32_t reserved1;
+  uint64_t peak_device_bytes; /* largest amount of device memory the call held
+                                 from its allocator at one time (result
+                                 arrays and temporaries)                    */
 } fstc_stats;
 
 /*

@@ -80,15 +80,22 @@ void *Buf::grow_keep(size_t bytes, size_t used) {
   return p;
 }
 
+// A round that outgrows the arena adds a chunk as large as everything the
+// round has taken so far plus the request (so a round needs a logarithmic
+// number of chunks), and the next reset() folds the chunks into one
+// allocation of 1.5 times the largest round seen: the arena tracks what the
+// rounds use, not the sum of its chunks.
 void *Arena::take(size_t bytes) {
   bytes = std::max<size_t>(256, (bytes + 255) & ~(size_t)255);
   if (chunks.empty() || used + bytes > chunks.back().cap) {
-    const size_t c = std::max<size_t>(bytes, chunks.empty() ? (size_t)1 << 20 : 2 * chunks.back().cap);
+    const size_t c = std::max<size_t>((size_t)1 << 20, round_bytes + bytes);
     chunks.push_back({static_cast<char *>(A->alloc(c)), c});
     used = 0;
   }
   void *p = chunks.back().p + used;
   used += bytes;
+  round_bytes += bytes;
+  high = std::max(high, round_bytes);
   return p;
 }
 
@@ -104,18 +111,19 @@ void Arena::reserve(size_t bytes) {
 void Arena::reset() {
   ++epoch;
   if (chunks.size() > 1) {
-    size_t total = 0;
-    for (auto &c : chunks) total += c.cap;
+    const size_t c = ((high + high / 2) + 255) & ~(size_t)255;
     release();
-    chunks.push_back({static_cast<char *>(A->alloc(total)), total});
+    chunks.push_back({static_cast<char *>(A->alloc(c)), c});
   }
   used = 0;
+  round_bytes = 0;
 }
 
 void Arena::release() {
   for (auto &c : chunks) A->free(c.p, c.cap);
   chunks.clear();
   used = 0;
+  round_bytes = 0;
 }
 
 namespace {
@@ -1000,6 +1008,7 @@ void Composer::run(fstc_result *out) {
     stats->hash_capacity = hcap;
     stats->visited_form = vis_moves ? 2u : dense_vis ? 1u : 0u;
     stats->direct_product_levels = direct_levels;
+    stats->peak_device_bytes = A.peak_bytes;
     if (T.all) {
       stats->ms_csr = ms[kCsr];
       stats->ms_count = ms[kCount];

@@ -218,7 +218,9 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     if (!pred[l]) continue;
     const u32 pos = s_base[l] + woff[l] + count_below(m[l]);
     lists[l][pos] = (u32)u;
-    if (l == 0) a.wrange[pos] = make_uint4(r.b1, r.e1, r.b2, r.e2);  // saves the wide join two loads
+    // saves the listed joins two dependent loads
+    if (l == 0) a.wrange[pos] = make_uint4(r.b1, r.e1, r.b2, r.e2);
+    if (l == 4) a.wrange[a.nsrc - 1 - pos] = make_uint4(r.b1, r.e1, r.b2, r.e2);
   }
 }
 
@@ -467,7 +469,8 @@ __device__ __forceinline__ void count_group_sources(const LevelArgs &a, u32 blk,
     u64 cnt = 0;
     u32 mc = 0;
     if (have) {
-      const Ranges r = source_ranges(a, u);
+      const uint4 wr = a.wrange[a.nsrc - 1 - i];
+      const Ranges r{wr.x, wr.y, wr.z, wr.w};
       group_join(a, r, [&](u32 s1, u32 s2, bool m, u32) {
         if (m) {
           cnt += (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2);
@@ -541,7 +544,8 @@ __global__ __launch_bounds__(256) void k_emit_group(LevelArgs a) {
     const u32 i = i0 + (threadIdx.x % kWave) / G;
     if (i >= n) continue;  // group-uniform; shuffles stay within groups
     const u32 u = a.grp[i];  // never a product source
-    const Ranges r = source_ranges(a, u);
+    const uint4 wr = a.wrange[a.nsrc - 1 - i];
+    const Ranges r{wr.x, wr.y, wr.z, wr.w};
     u64 k = a.moff[u], rb = a.roff[u];
     group_join(a, r, [&](u32 s1, u32 s2, bool m, u32) {
       const u64 prod = m ? (u64)seg_len(a.c1.seg_off, s1) * seg_len(a.c2.seg_off, s2) : 0;

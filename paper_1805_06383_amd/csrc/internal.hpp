@@ -58,11 +58,12 @@ struct Buf {
 };
 
 // Bump allocator for temporaries that die together (one breadth-first level,
-// one CSR build): takes from its last chunk and adds a chunk at least twice
-// as large when that is full; reset() frees every chunk and, when there were
-// several, keeps one as large as all of them, so that after the first rounds
-// a round costs no allocator call.  Frees are stream ordered (like Buf), so
-// a reset while kernels still read the old chunks is safe.
+// one CSR build): takes from its last chunk and, when that is full, adds one
+// as large as the round's takes so far plus the request; reset() frees every
+// chunk and, when there were several, keeps one of 1.5 times the largest
+// round's takes, so that after the first rounds a round costs no allocator
+// call and the arena holds what the rounds use.  Frees are stream ordered
+// (like Buf), so a reset while kernels still read the old chunks is safe.
 struct Arena {
   Allocator *A = nullptr;
   struct Chunk {
@@ -70,7 +71,9 @@ struct Arena {
     size_t cap;
   };
   std::vector<Chunk> chunks;
-  size_t used = 0;
+  size_t used = 0;        // bytes taken from the last chunk
+  size_t round_bytes = 0;  // bytes taken in this round, all chunks
+  size_t high = 0;         // largest round_bytes of any round so far
   u64 epoch = 0;  // incremented by reset(): handles from older rounds are stale
 
   explicit Arena(Allocator *a) : A(a) {}

@@ -122,7 +122,8 @@ struct LevelArgs {
   const u64 *roff;       // [nsrc + 1] exclusive scan of cnt
   const u64 *moff;       // [nsrc + 1] exclusive scan of mc
   u32 *wide, *heavy;     // source lists for wavefront / workgroup joins
-  uint4 *wrange;         // [nsrc] segment ranges (b1, e1, b2, e2) of wide[i]
+  uint4 *wrange;         // [nsrc] segment ranges (b1, e1, b2, e2) of wide[i] at i, of
+                         // grp[i] at nsrc - 1 - i (the two lists hold at most nsrc)
   Status *st;
   uint4 *match;          // [M] (M1 arc start, M2 arc start, n1, n2)
   u64 *mrbase;           // [M] first record of each match

@@ -193,13 +193,17 @@ __device__ __forceinline__ void hash_insert_batch(u64 *keys, u64 mask, const u64
 // Visited-set insert of B target pairs (key = r1 << 32 | r2): the hash
 // table, or the dense array when a.vn2 != 0 (slot = r1 vn2 + r2; a claim is
 // a CAS from kUnvisited to kClaimed, tried only when a plain read of the
-// entry still sees kUnvisited -- entries never return to it).
+// entry still sees kUnvisited -- entries never return to it).  known[i]:
+// the pair's id when an earlier level gave it one and the dense array holds
+// it, else kUnvisited.
 template <int B>
 __device__ __forceinline__ void visit_batch(const MergeArgs &a, const u64 (&key)[B],
                                             const bool (&act)[B], u32 (&slot)[B],
-                                            bool (&is_new)[B]) {
+                                            bool (&is_new)[B], u32 (&known)[B]) {
   if (!a.vn2) {
     hash_insert_batch<B>(a.hkeys, a.hmask, key, act, slot, is_new, &a.st->err);
+#pragma unroll
+    for (int i = 0; i < B; ++i) known[i] = kUnvisited;
     return;
   }
   u32 cur[B];
@@ -212,18 +216,18 @@ __device__ __forceinline__ void visit_batch(const MergeArgs &a, const u64 (&key)
                     : 0u;
   }
 #pragma unroll
-  for (int i = 0; i < B; ++i)
+  for (int i = 0; i < B; ++i) {
+    known[i] = cur[i] < kClaimed ? cur[i] : kUnvisited;  // ids are below both markers
     if (act[i] && cur[i] == kUnvisited) is_new[i] = atomicCAS(&a.vis[slot[i]], kUnvisited, kClaimed) == kUnvisited;
+  }
 }
 
-// Merged arcs of B runs: part ranks back to (r1, a) and (r2, c), the target
-// pair inserted in the visited table, and (slot, a, c, weight) written to
-// temp[tpos], with kNewFlag set in the slot when this insert claimed it (the
-// new-state list is built from these flags by k_newlist, without a shared
-// counter).
 // The part pairs of B merged arcs -> visited-table insert of the target pair
 // (r1, r2) and the run record (slot | kNewFlag if claimed, a, c, weight) at
-// temp[tpos], source u at runsrc[tpos].
+// temp[tpos], source u at runsrc[tpos] (the new-state list is built from
+// these flags by k_newlist, without a shared counter).  A target that
+// already has an id in the dense array is recorded as id | kIdFlag, so the
+// result append needs no visited-array lookup for it.
 template <int B>
 __device__ __forceinline__ void emit_parts(const MergeArgs &a, const bool (&act)[B],
                                            const u32 (&u)[B], const uint2 (&P1)[B],
@@ -232,14 +236,15 @@ __device__ __forceinline__ void emit_parts(const MergeArgs &a, const bool (&act)
   u64 hk[B];
 #pragma unroll
   for (int i = 0; i < B; ++i) hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
-  u32 slot[B];
+  u32 slot[B], known[B];
   bool is_new[B];
-  visit_batch<B>(a, hk, act, slot, is_new);
+  visit_batch<B>(a, hk, act, slot, is_new, known);
 #pragma unroll
   for (int i = 0; i < B; ++i) {
     if (act[i]) {
-      a.temp[tpos[i]] = make_uint4(slot[i] | (is_new[i] ? kNewFlag : 0u), P1[i].y, P2[i].y,
-                                   __float_as_uint(w[i]));
+      const u32 x = known[i] != kUnvisited ? known[i] | kIdFlag
+                                           : slot[i] | (is_new[i] ? kNewFlag : 0u);
+      a.temp[tpos[i]] = make_uint4(x, P1[i].y, P2[i].y, __float_as_uint(w[i]));
       a.runsrc[tpos[i]] = u[i];
     }
   }
@@ -1934,6 +1939,7 @@ __global__ __launch_bounds__(256) void k_unreduced(MergeArgs a, u32 *newbits, u3
   uint2 P1[kUnredB], P2[kUnredB];
   float wt[kUnredB];
   bool is_new[kUnredB];
+  u32 known[kUnredB];  // unused: the result holds slots until the ids are known
 #pragma unroll
   for (int i = 0; i < kUnredB; ++i) {
     r[i] = wb + (u64)i * kWave + lane;
@@ -1947,7 +1953,7 @@ __global__ __launch_bounds__(256) void k_unreduced(MergeArgs a, u32 *newbits, u3
     P2[i] = a.parts2[a.pbase2[q2] + (u32)(key & ((1ull << a.b2) - 1))];
     hk[i] = ((u64)P1[i].x << 32) | (u64)P2[i].x;
   }
-  visit_batch<kUnredB>(a, hk, act, slot, is_new);
+  visit_batch<kUnredB>(a, hk, act, slot, is_new, known);
 #pragma unroll
   for (int i = 0; i < kUnredB; ++i) {
     if (!act[i]) continue;
@@ -2051,6 +2057,14 @@ __global__ void k_newkeys(const u32 *newlist, u32 nnew, const u64 *hkeys, u32 vn
 
 // Wave per segment of merged runs: merge tile i (i < ntiles) or multi-block
 // source big[i - ntiles]; lanes copy consecutive runs.
+// Target id of a merged arc's record word x: the id itself when it carries
+// kIdFlag (dense visited array only: its slots and ids are below 2^30, while
+// hash-table slots use bit 30 themselves), else the id the visited set now
+// holds at the slot.
+__device__ __forceinline__ u32 target_id(const MergeArgs &a, u32 x, const u32 *hvals) {
+  return (a.vn2 && (x & kIdFlag)) ? x & ~kIdFlag : hvals[x & ~kNewFlag];
+}
+
 __global__ __launch_bounds__(256) void k_compact(MergeArgs a, const u64 *aoff, u32 nbig, u64 M,
                                                  const u32 *hvals, u32 *osrc, u32 *odst,
                                                  u32 *oil, u32 *ool, float *ow) {
@@ -2079,37 +2093,59 @@ __global__ __launch_bounds__(256) void k_compact(MergeArgs a, const u64 *aoff, u
     const uint4 rec = a.temp[tbase + r];
     const u64 k = obase + r;
     osrc[k] = a.lo + a.runsrc[tbase + r];
-    odst[k] = hvals[rec.x & ~kNewFlag];
+    odst[k] = target_id(a, rec.x, hvals);
     oil[k] = rec.y;
     ool[k] = rec.z;
     ow[k] = __uint_as_float(rec.w);
   }
 }
 
-// Result append source by source: 16 lanes per source.
+// Result append, sources in consecutive groups of 64 per wave: their merged
+// arcs are consecutive in the result (aoff is the exclusive scan of the
+// per-source counts mend - tstart), so the wave walks the group's output
+// range 64 entries at a time, each lane finding its entry's source by a
+// binary search over the group's offsets held one per lane.
 __global__ __launch_bounds__(256) void k_compact_sources(MergeArgs a, const u64 *aoff, u64 M,
                                                          const u32 *hvals, u32 *osrc, u32 *odst,
                                                          u32 *oil, u32 *ool, float *ow) {
-  const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
-  const u64 u = t / 16;
-  const u32 j = (u32)(t % 16);
-  if (u >= a.nsrc) return;
-  const u64 tb = a.tstart[u], n = a.mend[u] - tb, ob = aoff[u];
-  if (n == 0) return;
-  if (tb + n > a.R + a.prodpos || ob + n > M) {  // impossible: counts agree with aoff
-    if (j == 0) set_error(&a.st->err, kErrBounds);
+  const u32 lane = lane_id();
+  const u64 u0 = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave * kWave;
+  if (u0 >= a.nsrc) return;
+  const u64 u = u0 + lane;
+  const bool in = u < a.nsrc;
+  const u64 tb = in ? a.tstart[u] : 0, n = in ? a.mend[u] - tb : 0;
+  const u64 ob = in ? aoff[u] : 0;
+  const u64 incl = wave_inclusive_sum(n);
+  const u64 rel = incl - n;  // this source's first entry, relative to the group's
+  const u64 total = __shfl(incl, kWave - 1, kWave);
+  const u64 ob0 = __shfl(ob, 0, kWave);
+  // impossible: counts agree with aoff and the temp ranges lie in temp
+  const bool bad = (in && (ob != ob0 + rel || tb + n > a.R + a.prodpos)) || ob0 + total > M;
+  if (__ballot(bad)) {
+    if (lane == 0) set_error(&a.st->err, kErrBounds);
     return;
   }
-  for (u64 r = j; r < n; r += 16) {
-    const uint4 rec = a.temp[tb + r];
-    const u64 k = ob + r;
-    osrc[k] = a.lo + (u32)u;
-    // kIdFlag marks ids only with the dense array (slots and ids below 2^30
-    // there); hash-table slots use bit 30 themselves
-    odst[k] = (a.vn2 && (rec.x & kIdFlag)) ? rec.x & ~kIdFlag : hvals[rec.x & ~kNewFlag];
-    oil[k] = rec.y;
-    ool[k] = rec.z;
-    ow[k] = __uint_as_float(rec.w);
+  for (u64 p0 = 0; p0 < total; p0 += kWave) {
+    const u64 p = p0 + lane;
+    // last lane whose source starts at or before p (sources without arcs
+    // share their start with the next one; the last of them is taken)
+    u32 s = 0;
+#pragma unroll
+    for (u32 step = kWave / 2; step; step >>= 1) {
+      const u64 r = __shfl(rel, (int)(s + step), kWave);
+      s = (s + step < (u32)kWave && r <= p) ? s + step : s;
+    }
+    const u64 rs = __shfl(rel, (int)s, kWave);
+    const u64 ts = __shfl(tb, (int)s, kWave);
+    if (p < total) {
+      const uint4 rec = a.temp[ts + (p - rs)];
+      const u64 k = ob0 + p;
+      osrc[k] = a.lo + (u32)(u0 + s);
+      odst[k] = target_id(a, rec.x, hvals);
+      oil[k] = rec.y;
+      ool[k] = rec.z;
+      ow[k] = __uint_as_float(rec.w);
+    }
   }
 }
 
@@ -2341,7 +2377,7 @@ void launch_close_holes(const MergeArgs &a, const u64 *aoff, u64 n, void *tmp, h
 void launch_compact_sources(const MergeArgs &a, const u64 *aoff, u64 M, const u32 *hvals,
                             u32 *osrc, u32 *odst, u32 *oil, u32 *ool, float *ow, hipStream_t s) {
   if (!a.nsrc || !M) return;
-  hipLaunchKernelGGL(k_compact_sources, dim3((unsigned)ceil_div((u64)a.nsrc * 16, 256)), dim3(256),
+  hipLaunchKernelGGL(k_compact_sources, dim3((unsigned)ceil_div((u64)a.nsrc, 256)), dim3(256),
                      0, s, a, aoff, M, hvals, osrc, odst, oil, ool, ow);
 }
 
