@@ -565,6 +565,8 @@ void Composer::run(fstc_result *out) {
       pm.parts2 = c2.parts;
       pm.arcs1 = c1.arcs;
       pm.arcs2 = c2.arcs;
+      pm.wts1 = c1.wts;
+      pm.wts2 = c2.wts;
       pm.seg_sym1 = c1.seg_sym;
       pm.seg_off1 = c1.seg_off;
       pm.seg_sym2 = c2.seg_sym;
@@ -715,6 +717,8 @@ void Composer::run(fstc_result *out) {
     ma.moff = moff.as<u64>();
     ma.arcs1 = c1.arcs;
     ma.arcs2 = c2.arcs;
+    ma.wts1 = c1.wts;
+    ma.wts2 = c2.wts;
     ma.pk = pk.as<u32>();
     ma.phdr = phdr.as<uint4>();
     ma.pcnt = cnt.as<u64>();  // product-merge sources have no records: their slots are free

@@ -117,6 +117,14 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 // has more than P arcs, so each has exactly P), and kCellIdent as well when
 // arc i of every segment has part i; kCellContig when its segment symbols
 // are consecutive (the first plus the segment index).
+// The arcs' weight words as an array of their own (the product merge's
+// operand loads then fetch weights alone), zeros after the last arc.
+__global__ void k_arc_weights(const uint2 *arcs, u64 n, u32 *wts) {
+  for (u64 j = (u64)blockIdx.x * blockDim.x + threadIdx.x; j < n + kArcTail;
+       j += (u64)gridDim.x * blockDim.x)
+    wts[j] = j < n ? arcs[j].y : 0u;
+}
+
 __global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_off,
                              const uint2 *arcs, const u32 *part_base, u32 nq, u32 *flag) {
   const u32 lane = lane_id();
@@ -516,6 +524,9 @@ __global__ void k_csr_keys(const u32 *src, const u32 *dst, const u32 *il, const 
 }  // namespace
 
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s) {
+  const u64 nw = c.num_arcs + kArcTail;
+  hipLaunchKernelGGL(k_arc_weights, dim3((unsigned)std::min<u64>(ceil_div(nw, kNT), 4096)),
+                     dim3(kNT), 0, s, c.arcs, c.num_arcs, c.wts);
   if (!c.num_states) return;
   const unsigned g = (unsigned)std::min<u64>(ceil_div(c.num_states, kNT / kWave), 1u << 16);
   hipLaunchKernelGGL(k_cell_flags, dim3(g), dim3(kNT), 0, s, c.row, c.seg_sym, c.seg_off, c.arcs,
@@ -537,10 +548,10 @@ void check_csr_ranges(const fstc_fst &m, bool by_output) {
 void alloc_csr(const fstc_fst &m, Buf &b, Csr &c) {
   const u64 n = m.num_arcs, nq = m.num_states;
   const u64 n1 = std::max<u64>(n, 1);
-  const size_t sz[7] = {(nq + 1) * 4, n1 * 4, (n + 1) * 4, (n + kArcTail) * 8, (nq + 1) * 4,
-                        n1 * 8, std::max<u64>(nq, 1) * 4};
-  size_t off[7], total = 0;
-  for (int i = 0; i < 7; ++i) {
+  const size_t sz[8] = {(nq + 1) * 4, n1 * 4, (n + 1) * 4, (n + kArcTail) * 8, (nq + 1) * 4,
+                        n1 * 8, std::max<u64>(nq, 1) * 4, (n + kArcTail) * 4};
+  size_t off[8], total = 0;
+  for (int i = 0; i < 8; ++i) {
     off[i] = total;
     total += (sz[i] + 255) & ~(size_t)255;
   }
@@ -554,6 +565,7 @@ void alloc_csr(const fstc_fst &m, Buf &b, Csr &c) {
   c.part_base = (u32 *)(p + off[4]);
   c.parts = (uint2 *)(p + off[5]);
   c.cell_flag = (u32 *)(p + off[6]);
+  c.wts = (u32 *)(p + off[7]);
 }
 
 namespace {

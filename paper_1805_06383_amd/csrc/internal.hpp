@@ -119,6 +119,8 @@ struct Csr {
   u32 *part_base = nullptr;  // [num_states + 1]
   uint2 *parts = nullptr;    // [num_arcs] (target, outer symbol)
   u32 *cell_flag = nullptr;  // [num_states] see build_cell_flags (compose only)
+  u32 *wts = nullptr;        // [num_arcs + kArcTail] arcs[j].y alone, zeros after the
+                             // last arc (compose only, build_cell_flags)
 };
 
 // The arc array of a CSR built for composition (alloc_csr) has kArcTail
@@ -148,6 +150,7 @@ constexpr u32 kProdParts = 64;
 constexpr u32 kCellBad = 1u, kCellSpecial = 2u, kCellDense = 4u, kCellIdent = 8u,
               kCellContig = 16u;
 constexpr int kCellEmaxShift = 8, kCellEminShift = 16;
+// Also fills c.wts.
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s);
 
 // Checks the packing limits of build_csr for one transducer; throws

@@ -202,6 +202,7 @@ struct MergeArgs {
   const u64 *mrbase;    // [M] first record of each match
   const u64 *moff;      // [nsrc + 1] first match of each source
   const uint2 *arcs1, *arcs2;  // CSR arcs (part rank, weight bits)
+  const u32 *wts1, *wts2;      // their weight words alone (Csr::wts)
   // product merge: the sources with pk[u] != 0 own temp slots
   // R + poff[u] .. R + poff[u] + pk[u] - 1 (prodpos slots in all)
   const u32 *pk;

@@ -1021,8 +1021,8 @@ __device__ __forceinline__ void prod_one(const MergeArgs &a, u64 u, u32 K, uint4
       const u32 g = gq + 16u * t;
       in1[t] = g < na && pp < P1;
       in2[t] = g < na && pp < P2;
-      w1[t] = prod_arc<NARROW>(a.arcs1, in1[t] ? ab1 + P1 * g + pp : ab1).y;
-      w2[t] = prod_arc<NARROW>(a.arcs2, in2[t] ? ab2 + P2 * g + pp : ab2).y;
+      w1[t] = a.wts1[in1[t] ? ab1 + P1 * g + pp : ab1];
+      w2[t] = a.wts2[in2[t] ? ab2 + P2 * g + pp : ab2];
     }
     if (__ballot(v && s1 == s2) == __ballot(v)) {
       double d = 0.0;
@@ -1371,9 +1371,6 @@ __global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
   const u64 hslot = own ? (u64)L1.x * a.vn2 + L2.x : 0;
   const u32 hcur = __hip_atomic_load(&a.vis[hslot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   const u64 pu = mine ? a.poff[u] : 0;
-  // the weight words of the operands (arc j's weight is word 2 j + 1)
-  const u32 *wt1 = reinterpret_cast<const u32 *>(a.arcs1) + 1;
-  const u32 *wt2 = reinterpret_cast<const u32 *>(a.arcs2) + 1;
   const u32 q = lane & 3u, gk = lane >> 4;
   u32 x1[16], x2[16];
   u32 v1 = 0, v2 = 0;  // bit t: operand t present
@@ -1384,13 +1381,8 @@ __global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
     v1 |= (i1 ? 1u : 0u) << t;
     v2 |= (i2 ? 1u : 0u) << t;
     const u32 j1 = i1 ? ab1 + P1 * g + q : 0u, j2 = i2 ? ab2 + P2 * g + q : 0u;
-    if (NARROW) {
-      x1[t] = *reinterpret_cast<const u32 *>(reinterpret_cast<const char *>(wt1) + (j1 << 3));
-      x2[t] = *reinterpret_cast<const u32 *>(reinterpret_cast<const char *>(wt2) + (j2 << 3));
-    } else {
-      x1[t] = wt1[2 * (u64)j1];
-      x2[t] = wt2[2 * (u64)j2];
-    }
+    x1[t] = a.wts1[j1];
+    x2[t] = a.wts2[j2];
   }
   double d = 0.0;
 #pragma unroll

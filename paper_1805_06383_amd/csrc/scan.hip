@@ -81,15 +81,24 @@ __global__ __launch_bounds__(kScanNT) void k_tile_scan(const TI *in, TO *out, u6
 // then wave 0 reads the states of the 64 tiles below it at once and adds
 // aggregates down to the nearest tile that has published its inclusive
 // prefix, publishes its own inclusive prefix, and the workgroup writes its
-// tile offset by that.  A state word is (epoch << 2 | kind): words of other
-// calls carry other epochs and count as not yet published.  Waits are
-// bounded (kLbSpins reads of a window): past that, kErrScan.
+// tile offset by that.
+//
+// Published values need no memory fences: every 64-bit state word carries
+// the call's epoch in its high half and one half of a value in its low half,
+// and is written and read with relaxed device-scope atomics, which the
+// chip's eight L2 caches keep coherent (a release store or acquire load
+// would instead write back or invalidate the whole L2 of an XCD, once per
+// tile).  A value is two such words; a reader takes it once both carry the
+// current epoch, so words of other calls never match and no word depends on
+// the order in which another becomes visible.  Waits are bounded (kLbSpins
+// reads of a window): past that, kErrScan.
 constexpr int kLbNT = 256;
 constexpr int kLbIT = 8;
 constexpr int kLbTile = kLbNT * kLbIT;
-constexpr u32 kLbAgg = 1u, kLbIncl = 2u;
 constexpr u32 kLbSpins = 1u << 22;
 constexpr int kLbMax = 4;
+// State words per tile: [kLbMax values][aggregate, inclusive][lo, hi].
+constexpr int kLbWords = kLbMax * 4;
 
 struct LbArgs {
   const void *in[kLbMax];
@@ -102,15 +111,22 @@ struct LbArgs {
   ScanPublish pub;  // pub.dst == NULL: none
   u64 n;
   u32 nb, epoch;
-  u32 *flags;   // [nb]
-  u64 *agg;     // [nb * kLbMax]
-  u64 *incl;    // [nb * kLbMax]
+  u64 *state;   // [nb * kLbWords]
   u32 *ctr, *err;
 };
 
 __device__ __forceinline__ void put_out(const LbArgs &p, int k, u64 i, u64 v) {
   if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[i] = (u32)v;
   else p.out[k][i] = v;
+}
+
+// Publishes value v of array k of tile t as its aggregate (which = 0) or
+// inclusive prefix (which = 1).
+__device__ __forceinline__ void lb_put(const LbArgs &p, u32 t, int k, int which, u64 v) {
+  u64 *w = p.state + (u64)t * kLbWords + k * 4 + which * 2;
+  const u64 tag = (u64)p.epoch << 32;
+  __hip_atomic_store(&w[0], tag | (v & 0xffffffffull), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(&w[1], tag | (v >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int K>
@@ -155,27 +171,38 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
     if (t == 0) {
       if (lane == 0 && p.nb > 1) {  // a single tile has no successor reading it
 #pragma unroll
-        for (int k = 0; k < K; ++k) p.incl[k] = tot[k];
-        __hip_atomic_store(&p.flags[0], (p.epoch << 2) | kLbIncl, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        for (int k = 0; k < K; ++k) lb_put(p, 0, k, 1, tot[k]);
       }
     } else {
       if (lane == 0) {
 #pragma unroll
-        for (int k = 0; k < K; ++k) p.agg[(u64)t * kLbMax + k] = tot[k];
-        __hip_atomic_store(&p.flags[t], (p.epoch << 2) | kLbAgg, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        for (int k = 0; k < K; ++k) lb_put(p, t, k, 0, tot[k]);
       }
       long long hi = (long long)t - 1;  // nearest predecessor of the window
       u32 spins = 0;
       bool failed = false;
       while (true) {
         const long long j = hi - (long long)lane;
-        u32 f = (p.epoch << 2) | kLbIncl;  // below tile 0: an empty prefix
-        if (j >= 0)
-          f = __hip_atomic_load(&p.flags[j], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-        const bool ready = (f >> 2) == p.epoch && (f & 3u) != 0;
-        const bool isp = ready && (f & 3u) == kLbIncl;
+        // lane's tile j: below tile 0, an empty inclusive prefix
+        bool isp = true, isa = true;
+        u64 av[K], iv[K];
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+          av[k] = 0;
+          iv[k] = 0;
+          if (j >= 0) {
+            const u64 *w = p.state + (u64)j * kLbWords + k * 4;
+            const u64 a0 = __hip_atomic_load(&w[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const u64 a1 = __hip_atomic_load(&w[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const u64 i0 = __hip_atomic_load(&w[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const u64 i1 = __hip_atomic_load(&w[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            isa = isa && (u32)(a0 >> 32) == p.epoch && (u32)(a1 >> 32) == p.epoch;
+            isp = isp && (u32)(i0 >> 32) == p.epoch && (u32)(i1 >> 32) == p.epoch;
+            av[k] = (a0 & 0xffffffffull) | (a1 << 32);
+            iv[k] = (i0 & 0xffffffffull) | (i1 << 32);
+          }
+        }
+        const bool ready = isp || isa;
         const u64 pm = __ballot(isp), rm = __ballot(ready);
         const u32 lp = pm ? (u32)__builtin_ctzll(pm) : (u32)kWave;  // nearest inclusive prefix
         const u64 need = lp < (u32)kWave ? (lp == 63 ? ~0ull : (2ull << lp) - 1ull) : ~0ull;
@@ -184,13 +211,14 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
             failed = true;
             break;
           }
+          __builtin_amdgcn_s_sleep(1);
           continue;
         }
 #pragma unroll
         for (int k = 0; k < K; ++k) {
           u64 x = 0;
-          if (j >= 0 && (u32)lane < lp) x = p.agg[(u64)j * kLbMax + k];
-          else if (j >= 0 && (u32)lane == lp) x = p.incl[(u64)j * kLbMax + k];
+          if (j >= 0 && (u32)lane < lp) x = av[k];
+          else if (j >= 0 && (u32)lane == lp) x = iv[k];
           off[k] += wave_sum(x);
         }
         if (lp < (u32)kWave) break;
@@ -199,9 +227,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
       if (failed && lane == 0) atomicOr(p.err, kErrScan);
       if (lane == 0) {
 #pragma unroll
-        for (int k = 0; k < K; ++k) p.incl[(u64)t * kLbMax + k] = off[k] + tot[k];
-        __hip_atomic_store(&p.flags[t], (p.epoch << 2) | kLbIncl, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        for (int k = 0; k < K; ++k) lb_put(p, t, k, 1, off[k] + tot[k]);
       }
     }
     if (lane == 0) {
@@ -308,7 +334,7 @@ size_t scan_temp_bytes(u64 n) { return temp_elems<u64>(n) * sizeof(u64) + 256; }
 
 size_t scan_lb_state_bytes(u64 n) {
   const u64 nb = std::max<u64>(1, ceil_div(n, kLbTile));
-  return (size_t)nb * (4 + 2 * kLbMax * 8) + 256;
+  return (size_t)nb * kLbWords * 8 + 256;
 }
 
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
@@ -332,12 +358,9 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   if (pub) p.pub = *pub;
   p.n = n;
   p.nb = (u32)nb;
-  u32 e = (epochs.fetch_add(1, std::memory_order_relaxed) + 1) & 0x3fffffffu;
+  u32 e = epochs.fetch_add(1, std::memory_order_relaxed) + 1;
   p.epoch = e ? e : 1u;  // state words of zero-filled memory never match
-  char *b = static_cast<char *>(state);
-  p.agg = reinterpret_cast<u64 *>(b);
-  p.incl = p.agg + nb * kLbMax;
-  p.flags = reinterpret_cast<u32 *>(p.incl + nb * kLbMax);
+  p.state = static_cast<u64 *>(state);
   p.ctr = ctr;
   p.err = err;
   const dim3 g((unsigned)nb), bl(kLbNT);
