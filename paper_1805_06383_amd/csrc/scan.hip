@@ -129,11 +129,21 @@ __device__ __forceinline__ void lb_put(const LbArgs &p, u32 t, int k, int which,
   __hip_atomic_store(&w[1], tag | (v >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int K>
+// LDS slot of tile element e: one u64 of padding every 32 elements keeps
+// both the striped (e = r * kLbNT + thread) and the blocked (e = thread *
+// kLbIT + j) accesses free of bank conflicts.
+__device__ __forceinline__ u32 lb_slot(u32 e) { return e + (e >> 5); }
+
+// STRIPED: loads and stores striped across the workgroup through LDS (full
+// coalescing, for scans of many tiles, where bandwidth counts); otherwise
+// each thread reads and writes its own elements (fewer registers and
+// barriers, for scans of few tiles, where the latency of one tile counts).
+template <int K, bool STRIPED>
 __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __shared__ u32 s_t;
   __shared__ u64 s_off[kLbMax];
   __shared__ u64 scratch[kLbNT / kWave];
+  __shared__ u64 s_x[STRIPED ? kLbTile + kLbTile / 32 : 1];  // one array of the tile, transposed
   const u32 lane = lane_id();
   // tile numbers from the counter (a single tile needs none)
   if (threadIdx.x == 0 && p.nb > 1) {
@@ -143,26 +153,42 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   }
   if (p.nb > 1) __syncthreads();
   const u32 t = p.nb > 1 ? s_t : 0u;
-  const u64 base = (u64)t * kLbTile + (u64)threadIdx.x * kLbIT;  // blocked: kLbIT per thread
+  const u64 tbase = (u64)t * kLbTile;
+  // thread i scans elements kLbIT i .. kLbIT i + kLbIT - 1 of the tile
+  // (blocked); loads and stores are striped across the workgroup and pass
+  // through s_x
   u64 loc[K][kLbIT];
   u64 ex[K], tot[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
+    const bool wide = (p.wide >> k) & 1u;
+    const u64 *sub = p.sub[k];
+    auto elem = [&](u64 i) {
+      u64 x = 0;
+      if (i < p.n) {
+        x = wide ? static_cast<const u64 *>(p.in[k])[i] : (u64) static_cast<const u32 *>(p.in[k])[i];
+        if (sub) x -= sub[i];
+      }
+      return x;
+    };
+    if (STRIPED) {
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r) {
+        const u32 e = (u32)r * kLbNT + threadIdx.x;
+        s_x[lb_slot(e)] = elem(tbase + e);
+      }
+      __syncthreads();
+    }
     u64 run = 0;
 #pragma unroll
     for (int j = 0; j < kLbIT; ++j) {
-      const u64 i = base + j;
-      u64 x = 0;
-      if (i < p.n) {
-        x = ((p.wide >> k) & 1u) ? static_cast<const u64 *>(p.in[k])[i]
-                                 : (u64) static_cast<const u32 *>(p.in[k])[i];
-        if (p.sub[k]) x -= p.sub[k][i];
-      }
+      const u32 e = threadIdx.x * kLbIT + j;
+      const u64 x = STRIPED ? s_x[lb_slot(e)] : elem(tbase + e);
       loc[k][j] = run;
       run += x;
     }
     ex[k] = block_exclusive_sum<kLbNT, u64>(run, scratch, &tot[k]);
-    __syncthreads();  // scratch reused
+    __syncthreads();  // scratch and s_x reused
   }
   if (threadIdx.x < (u32)kWave) {
     u64 off[K];
@@ -260,13 +286,26 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    if ((p.tonly >> k) & 1u) continue;
+    if ((p.tonly >> k) & 1u) continue;  // uniform
     const u64 o = s_off[k] + ex[k];
+    if (!STRIPED) {
 #pragma unroll
-    for (int j = 0; j < kLbIT; ++j) {
-      const u64 i = base + j;
-      if (i < p.n) put_out(p, k, i, o + loc[k][j]);
+      for (int j = 0; j < kLbIT; ++j) {
+        const u64 i = tbase + threadIdx.x * kLbIT + j;
+        if (i < p.n) put_out(p, k, i, o + loc[k][j]);
+      }
+      continue;
     }
+#pragma unroll
+    for (int j = 0; j < kLbIT; ++j) s_x[lb_slot(threadIdx.x * kLbIT + j)] = o + loc[k][j];
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kLbIT; ++r) {
+      const u32 e = (u32)r * kLbNT + threadIdx.x;
+      const u64 i = tbase + e;
+      if (i < p.n) put_out(p, k, i, s_x[lb_slot(e)]);
+    }
+    __syncthreads();
   }
 }
 
@@ -364,10 +403,18 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   p.ctr = ctr;
   p.err = err;
   const dim3 g((unsigned)nb), bl(kLbNT);
-  if (k == 1) hipLaunchKernelGGL(k_scan_lb<1>, g, bl, 0, s, p);
-  else if (k == 2) hipLaunchKernelGGL(k_scan_lb<2>, g, bl, 0, s, p);
-  else if (k == 3) hipLaunchKernelGGL(k_scan_lb<3>, g, bl, 0, s, p);
-  else hipLaunchKernelGGL(k_scan_lb<4>, g, bl, 0, s, p);
+  // striped once the tiles outnumber the compute units
+  if (nb > (u64)compute_units()) {
+    if (k == 1) hipLaunchKernelGGL((k_scan_lb<1, true>), g, bl, 0, s, p);
+    else if (k == 2) hipLaunchKernelGGL((k_scan_lb<2, true>), g, bl, 0, s, p);
+    else if (k == 3) hipLaunchKernelGGL((k_scan_lb<3, true>), g, bl, 0, s, p);
+    else hipLaunchKernelGGL((k_scan_lb<4, true>), g, bl, 0, s, p);
+  } else {
+    if (k == 1) hipLaunchKernelGGL((k_scan_lb<1, false>), g, bl, 0, s, p);
+    else if (k == 2) hipLaunchKernelGGL((k_scan_lb<2, false>), g, bl, 0, s, p);
+    else if (k == 3) hipLaunchKernelGGL((k_scan_lb<3, false>), g, bl, 0, s, p);
+    else hipLaunchKernelGGL((k_scan_lb<4, false>), g, bl, 0, s, p);
+  }
 }
 
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s) {
