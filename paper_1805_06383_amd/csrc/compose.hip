@@ -15,6 +15,7 @@
 // The host reads a few counters twice per level; everything else stays in
 // HBM.  Buffers are grow-only and come from the caller's allocator (PyTorch's
 // caching allocator in the Python binding) or hipMallocAsync.
+#include <array>
 #include <chrono>
 #include <cstring>
 #include <functional>
@@ -88,6 +89,7 @@ void *Buf::grow_keep(size_t bytes, size_t used) {
 void *Arena::take(size_t bytes) {
   bytes = std::max<size_t>(256, (bytes + 255) & ~(size_t)255);
   if (chunks.empty() || used + bytes > chunks.back().cap) {
+    if (fixed) throw Error(FSTC_ERR_INTERNAL, "fixed arena exhausted");
     const size_t c = std::max<size_t>((size_t)1 << 20, round_bytes + bytes);
     chunks.push_back({static_cast<char *>(A->alloc(c)), c});
     used = 0;
@@ -146,6 +148,40 @@ Staging *staging() {
   }
   return p;
 }
+
+// A second stream of this thread on the current device (default priority,
+// not blocking on the null stream), created at first use and kept for the
+// thread's lifetime, with one event for forking work onto it and one for
+// joining it back.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+SideStream &side_stream() {
+  thread_local std::array<SideStream, 64> ss{};
+  int dev = 0;
+  FSTC_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) throw Error(FSTC_ERR_INVALID_ARG, "device index too large");
+  SideStream &x = ss[dev];
+  if (!x.s) {
+    FSTC_HIP(hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking));
+    FSTC_HIP(hipEventCreateWithFlags(&x.fork, hipEventDisableTiming));
+    FSTC_HIP(hipEventCreateWithFlags(&x.join, hipEventDisableTiming));
+  }
+  return x;
+}
+
+// Makes `main` wait for everything queued on the side stream when it goes
+// out of scope, on every path (an exception included), so that frees
+// ordered on `main` come after the side stream's kernels.
+struct SideJoin {
+  hipStream_t main;
+  SideStream &side;
+  ~SideJoin() {
+    (void)hipEventRecord(side.join, side.s);
+    (void)hipStreamWaitEvent(main, side.join, 0);
+  }
+};
 
 // Publication numbers of this thread's staging block, never reused.
 u32 next_publication() {
@@ -393,15 +429,25 @@ void Composer::run(fstc_result *out) {
   const bool product = !o.no_reduction && !o.no_product_merge;
   T.at(kCsr);
   {
-    Arena csr_tmp(&A);
-    csr_tmp.reserve(std::max(csr_temp_bytes(m1), csr_temp_bytes(m2)));
+    // the two layouts are independent: M2's is built on a side stream
+    // while M1's is built on the call's stream (each of their kernels is
+    // short, so the two sequences overlap and fill each other's gaps); the
+    // side stream's temporaries are allocated up front, in stream order on
+    // `s` before the fork
+    check_csr_ranges(m1, true);
+    check_csr_ranges(m2, false);
+    Arena csr_tmp(&A), csr_tmp2(&A);
+    csr_tmp.reserve(csr_temp_bytes(m1));
+    csr_tmp2.reserve(csr_temp_bytes(m2));
+    csr_tmp2.fixed = true;
+    SideStream &side = side_stream();
+    FSTC_HIP(hipEventRecord(side.fork, s));
+    FSTC_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
+    SideJoin join{s, side};
+    build_csr(m2, false, csr_tmp2, c2, dcounts + 3, &dst->err, side.s);
+    if (product) build_cell_flags(c2, c2.cell_flag, side.s);
     build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
-    csr_tmp.reset();
-    build_csr(m2, false, csr_tmp, c2, dcounts + 3, &dst->err, s);
-    if (product) {
-      build_cell_flags(c1, c1.cell_flag, s);
-      build_cell_flags(c2, c2.cell_flag, s);
-    }
+    if (product) build_cell_flags(c1, c1.cell_flag, s);
   }
   T.at(kNone);
   FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 6 * sizeof(u64), hipMemcpyDeviceToHost, s));

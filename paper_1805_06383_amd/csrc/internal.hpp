@@ -75,6 +75,9 @@ struct Arena {
   size_t round_bytes = 0;  // bytes taken in this round, all chunks
   size_t high = 0;         // largest round_bytes of any round so far
   u64 epoch = 0;  // incremented by reset(): handles from older rounds are stale
+  // When set, a take that needs a new chunk throws instead (an arena whose
+  // memory another stream uses must not allocate on the owning stream then).
+  bool fixed = false;
 
   explicit Arena(Allocator *a) : A(a) {}
   Arena(const Arena &) = delete;
