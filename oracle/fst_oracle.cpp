@@ -33,6 +33,23 @@
 //     joined arc pair is its own composed arc with weight fl32(p1 * p2); the
 //     reachable states are the same.
 //
+//   * With epsilon transitions (the paper's §2 excludes them and names
+//     composition filters as the way to admit them): one label value eps
+//     stands for the empty string on every tape.  Composed states are
+//     triples (q1, q2, f) with the filter state f of the three-state epsilon
+//     filter of Mohri, Pereira and Riley (also Allauzen, Riley and Schalkwyk
+//     2009), which admits exactly one alignment of every pair of paths:
+//       - M1 arc with output b != eps and M2 arc with input b: both move,
+//         from any f, to f = 0;
+//       - M1 arc with output eps and M2 arc with input eps: both move, from
+//         f = 0 only, to f = 0;
+//       - M1 arc with output eps alone (M2 stays, the composed arc writes
+//         eps): from f = 0 or 2, to f = 2;
+//       - M2 arc with input eps alone (M1 stays, the composed arc reads
+//         eps): from f = 0 or 1, to f = 1.
+//     A single move's weight is that arc's weight; accept states are the
+//     triples with q1 in F1 and q2 in F2, whatever f.
+//
 // The merge per source uses an ordered map keyed by (r1, r2, a, c); the pair
 // to id map is an ordered map; nothing here is tuned for speed.
 //
@@ -65,6 +82,7 @@ enum { ORACLE_OK = 0, ORACLE_INVALID = 1, ORACLE_ALPHABET = 2 };
 
 struct Result {
   std::vector<std::pair<uint32_t, uint32_t>> pairs;  // id -> (q1, q2)
+  std::vector<uint8_t> filt;                          // id -> filter state (epsilon composition)
   std::vector<uint32_t> depth;                        // id -> BFS depth
   std::vector<uint8_t> final;                         // id -> accept
   struct Arc { uint32_t src, dst, a, c; float w; };
@@ -240,9 +258,125 @@ int compose(const oracle_fst *m1, const oracle_fst *m2, uint32_t max_levels, boo
   return ORACLE_OK;
 }
 
+// One composed move out of a triple: target triple, labels, weight.
+struct Move { uint32_t r1, r2; uint8_t f; uint32_t a, c; float w; };
+
+// Every move the epsilon filter allows out of (q1, q2, f), in the order M1's
+// arcs (with their matches), then M2's input-epsilon arcs alone.
+void eps_moves(const Lookup &L1, const Lookup &L2, uint32_t q1, uint32_t q2, uint8_t f,
+               uint32_t eps, std::vector<Move> &out) {
+  const oracle_fst *m1 = L1.m, *m2 = L2.m;
+  auto r1 = L1.out(q1);
+  for (const uint32_t *p = r1.first; p != r1.second; ++p) {
+    const uint32_t e1 = *p;
+    const uint32_t b = m1->olabel[e1];
+    if (b != eps || f == 0) {  // both move: on a symbol from any f, on eps from f = 0
+      auto r2 = L2.out_reading(q2, b);
+      for (const uint32_t *t = r2.first; t != r2.second; ++t) {
+        const uint32_t e2 = *t;
+        out.push_back({m1->dst[e1], m2->dst[e2], 0, m1->ilabel[e1], m2->olabel[e2],
+                       m1->weight[e1] * m2->weight[e2]});
+      }
+    }
+    if (b == eps && (f == 0 || f == 2))  // M1 alone on its output eps
+      out.push_back({m1->dst[e1], q2, 2, m1->ilabel[e1], eps, m1->weight[e1]});
+  }
+  if (f == 0 || f == 1) {  // M2 alone on its input eps
+    auto r2 = L2.out_reading(q2, eps);
+    for (const uint32_t *t = r2.first; t != r2.second; ++t) {
+      const uint32_t e2 = *t;
+      out.push_back({q1, m2->dst[e2], 1, eps, m2->olabel[e2], m2->weight[e2]});
+    }
+  }
+}
+
+// Breadth-first search over the triples reachable from (s1, s2, 0); with
+// reduce, moves of one source that agree in target triple and labels are
+// merged (float64 sum of their float32 weights, rounded once).
+int compose_eps(const oracle_fst *m1, const oracle_fst *m2, uint32_t eps, uint32_t max_levels,
+                bool reduce, Result &res) {
+  if (!valid(m1) || !valid(m2)) return ORACLE_INVALID;
+  if (m1->num_osyms != m2->num_isyms) return ORACLE_ALPHABET;
+  if (eps >= m1->num_isyms || eps >= m1->num_osyms || eps >= m2->num_osyms) return ORACLE_INVALID;
+  const auto t0 = std::chrono::steady_clock::now();
+  Lookup L1(m1), L2(m2);
+  using Triple = std::array<uint32_t, 3>;
+  std::map<Triple, uint32_t> id;
+  std::deque<uint32_t> A;
+  id[Triple{m1->start, m2->start, 0}] = 0;
+  res.pairs.push_back({m1->start, m2->start});
+  res.filt.push_back(0);
+  res.depth.push_back(0);
+  A.push_back(0);
+  auto number = [&](uint32_t u, const Move &mv) {
+    const Triple v{mv.r1, mv.r2, mv.f};
+    auto it = id.find(v);
+    if (it != id.end()) return it->second;
+    const uint32_t vid = (uint32_t)res.pairs.size();
+    id.emplace(v, vid);
+    res.pairs.push_back({mv.r1, mv.r2});
+    res.filt.push_back(mv.f);
+    res.depth.push_back(res.depth[u] + 1);
+    A.push_back(vid);
+    return vid;
+  };
+  while (!A.empty()) {
+    const uint32_t u = A.front();
+    A.pop_front();
+    if (max_levels > 0 && res.depth[u] >= max_levels) continue;
+    std::vector<Move> moves;
+    eps_moves(L1, L2, res.pairs[u].first, res.pairs[u].second, res.filt[u], eps, moves);
+    res.premerge += moves.size();
+    if (!reduce) {
+      for (const Move &mv : moves) res.arcs.push_back({u, number(u, mv), mv.a, mv.c, mv.w});
+      continue;
+    }
+    std::map<std::array<uint32_t, 5>, double> acc;  // (r1, r2, f, a, c)
+    for (const Move &mv : moves) acc[{mv.r1, mv.r2, mv.f, mv.a, mv.c}] += (double)mv.w;
+    for (const auto &kv : acc) {
+      const Move mv{kv.first[0], kv.first[1], (uint8_t)kv.first[2], kv.first[3], kv.first[4], 0.f};
+      res.arcs.push_back({u, number(u, mv), mv.a, mv.c, (float)kv.second});
+    }
+  }
+  res.final.resize(res.pairs.size());
+  uint32_t maxd = 0;
+  for (size_t i = 0; i < res.pairs.size(); ++i) {
+    res.final[i] = (m1->final[res.pairs[i].first] && m2->final[res.pairs[i].second]) ? 1 : 0;
+    maxd = std::max(maxd, res.depth[i]);
+  }
+  res.levels = maxd + 1;
+  res.seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  return ORACLE_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+// Composition with epsilon transitions: label eps is the empty string on all
+// four tapes (it must be a symbol of each alphabet); the composed states are
+// (q1, q2, filter state) triples (oracle_filter_states), reachable from
+// (start1, start2, 0).  reduce = 0 keeps every move as its own arc.  Returns
+// 0, 1 (invalid transducer or eps out of range) or 2 (alphabet mismatch).
+int oracle_compose_eps(const oracle_fst *m1, const oracle_fst *m2, uint32_t eps,
+                       uint32_t max_levels, int reduce, void **handle) {
+  if (!handle) return ORACLE_INVALID;
+  *handle = nullptr;
+  Result *r = new Result();
+  const int rc = compose_eps(m1, m2, eps, max_levels, reduce != 0, *r);
+  if (rc != ORACLE_OK) {
+    delete r;
+    return rc;
+  }
+  *handle = r;
+  return ORACLE_OK;
+}
+
+// Per state id: its filter state (0 for results of the other entry points).
+void oracle_filter_states(const void *handle, uint8_t *f) {
+  const Result *r = static_cast<const Result *>(handle);
+  for (size_t i = 0; i < r->pairs.size(); ++i) f[i] = i < r->filt.size() ? r->filt[i] : 0;
+}
 
 // Composes m1 with m2 over the pairs reachable from (start1, start2).
 // max_levels = 0 means no cap.  On success *handle owns the result (release

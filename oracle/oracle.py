@@ -83,6 +83,11 @@ def _load(path: Path | None = None) -> ctypes.CDLL:
     lib.oracle_arcs.restype = None
     lib.oracle_free.argtypes = [vp]
     lib.oracle_free.restype = None
+    lib.oracle_compose_eps.argtypes = [ctypes.POINTER(_Fst), ctypes.POINTER(_Fst), u32, u32,
+                                       ctypes.c_int, ctypes.POINTER(vp)]
+    lib.oracle_compose_eps.restype = ctypes.c_int
+    lib.oracle_filter_states.argtypes = [vp, vp]
+    lib.oracle_filter_states.restype = None
     _handle_cache[key] = lib
     return lib
 
@@ -113,6 +118,7 @@ class OracleResult:
     num_premerge: int
     levels: int
     seconds: float
+    f: np.ndarray | None = None  # filter state of each state (epsilon composition)
 
     @property
     def num_states(self) -> int:
@@ -126,10 +132,14 @@ class OracleResult:
 _ERRORS = {1: "invalid transducer", 2: "alphabet mismatch (|Gamma| of M1 output != M2 input)"}
 
 
-def _collect(lib, h) -> OracleResult:
+def _collect(lib, h, with_filter: bool = False) -> OracleResult:
     counts = np.zeros(4, np.uint64)
     lib.oracle_counts(h, counts.ctypes.data)
     ns, na = int(counts[0]), int(counts[1])
+    filt = None
+    if with_filter:
+        filt = np.empty(ns, np.uint8)
+        lib.oracle_filter_states(h, filt.ctypes.data)
     q1 = np.empty(ns, np.uint32); q2 = np.empty(ns, np.uint32)
     fin = np.empty(ns, np.uint8); dep = np.empty(ns, np.uint32)
     lib.oracle_states(h, q1.ctypes.data, q2.ctypes.data, fin.ctypes.data, dep.ctypes.data)
@@ -139,7 +149,8 @@ def _collect(lib, h) -> OracleResult:
                     w.ctypes.data)
     secs = lib.oracle_seconds(h)
     lib.oracle_free(h)
-    return OracleResult(q1, q2, fin, dep, src, dst, a, c, w, int(counts[2]), int(counts[3]), secs)
+    return OracleResult(q1, q2, fin, dep, src, dst, a, c, w, int(counts[2]), int(counts[3]), secs,
+                        filt)
 
 
 def compose(m1, m2, max_levels: int = 0, lib_path: Path | None = None,
@@ -173,3 +184,21 @@ def expand_pairs(m1, m2, q1s, q2s, lib_path: Path | None = None) -> OracleResult
     if rc != 0:
         raise OracleError(_ERRORS.get(rc, f"oracle error {rc}"))
     return _collect(lib, h)
+
+
+def compose_eps(m1, m2, eps: int, max_levels: int = 0, reduce: bool = True,
+                lib_path: Path | None = None) -> OracleResult:
+    """Composition with epsilon transitions (label ``eps`` is the empty string
+    on every tape) under the three-state epsilon filter: states are triples
+    (q1, q2, f) with ``f`` the filter state.  reduce=False keeps every move
+    as its own arc."""
+    lib = _load(lib_path)
+    s1, k1 = _as_struct(m1)
+    s2, k2 = _as_struct(m2)
+    h = ctypes.c_void_p()
+    rc = lib.oracle_compose_eps(ctypes.byref(s1), ctypes.byref(s2), int(eps), int(max_levels),
+                                1 if reduce else 0, ctypes.byref(h))
+    del k1, k2
+    if rc != 0:
+        raise OracleError(_ERRORS.get(rc, f"oracle error {rc}"))
+    return _collect(lib, h, with_filter=True)

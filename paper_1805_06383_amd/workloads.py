@@ -123,6 +123,43 @@ def tiny_random(rng: np.random.Generator, nq: int, nin: int, nout: int,
     )
 
 
+def eps_random(rng: np.random.Generator, nq: int, nin: int, nout: int, narcs: int,
+               eps_in: float, eps_out: float, final_frac: float = 0.3, acyclic: bool = False,
+               eps: int = 0) -> FST:
+    """Small FST whose labels are the empty-string label ``eps`` with
+    probability eps_in (input tape) and eps_out (output tape), else uniform
+    over the other symbols; with acyclic=True every arc goes from a lower to a
+    higher state (its paths are finite)."""
+    if acyclic:
+        src = rng.integers(0, nq - 1, narcs)
+        dst = src + 1 + (rng.random(narcs) * (nq - 1 - src)).astype(np.int64)
+    else:
+        src, dst = rng.integers(0, nq, narcs), rng.integers(0, nq, narcs)
+
+    def labels(n, size, p):
+        lab = rng.integers(0, size - 1, n)
+        lab = lab + (lab >= eps)  # uniform over the symbols other than eps
+        return np.where(rng.random(n) < p, eps, lab)
+
+    return FST(num_states=nq, start=0, num_isyms=nin, num_osyms=nout, src=src, dst=dst,
+               ilabel=labels(narcs, nin, eps_in), olabel=labels(narcs, nout, eps_out),
+               weight=random_weights(rng, narcs),
+               final=(rng.random(nq) < final_frac).astype(np.uint8),
+               name=f"eps(q={nq},arcs={narcs},in={eps_in},out={eps_out})")
+
+
+def eps_pair(seed: int = 0, nq: int = 200, narcs: int = 2000, nsym: int = 100,
+             nouter: int = 50, eps_inner: float = 0.1, eps_outer: float = 0.05):
+    """Config-1-shaped pair with the empty-string label 0 on every tape: M1's
+    outputs and M2's inputs are label 0 with probability eps_inner, the outer
+    tapes with probability eps_outer; other labels uniform."""
+    rng = np.random.default_rng(7000 + seed)
+    m1 = eps_random(rng, nq, nouter, nsym, narcs, eps_outer, eps_inner, final_frac=0.1)
+    m2 = eps_random(rng, nq, nsym, nouter, narcs, eps_inner, eps_outer, final_frac=0.1)
+    m1.name, m2.name = "eps.M1", "eps.M2"
+    return m1, m2
+
+
 def config1(seed: int = 0):
     """Tiny random pair: |Q|=200, |Sigma|=|Delta|=50, |Gamma|=100, 2,000 arcs
     each with uniform src, dst and labels, 10% accept states."""

@@ -39,6 +39,23 @@ MUTANTS = {
 }
 
 
+# planted mistakes in the epsilon filter (compose_eps)
+MUTANTS_EPS = {
+    # M2 may move alone after M1 moved alone: two orders of the same moves
+    "eps_both_orders": ("if (f == 0 || f == 1) {  // M2 alone", "if (true) {  // M2 alone"),
+    # both moving on the empty label is never taken
+    "eps_no_joint_move": ("if (b != eps || f == 0) {", "if (b != eps) {"),
+    # both moving on the empty label allowed from every filter state
+    "eps_joint_any_state": ("if (b != eps || f == 0) {", "if (true) {"),
+    # M1 alone returns to filter state 0
+    "eps_m1_alone_state": ("out.push_back({m1->dst[e1], q2, 2,", "out.push_back({m1->dst[e1], q2, 0,"),
+    # M2 alone carries weight one instead of its arc's
+    "eps_m2_alone_weight": ("m2->olabel[e2], m2->weight[e2]});", "m2->olabel[e2], 1.0f});"),
+    # M1 alone writes its input symbol instead of the empty string
+    "eps_m1_alone_label": ("m1->ilabel[e1], eps, m1->weight[e1]", "m1->ilabel[e1], m1->ilabel[e1], m1->weight[e1]"),
+}
+
+
 def _tiny(seed):
     rng = np.random.default_rng(seed)
     m1 = W.tiny_random(rng, 4, 2, 2, 12, final_frac=0.5)
@@ -230,3 +247,45 @@ def test_expand_mutant_is_caught(name, mutant_dir):
     out = mutant_dir / f"lib{name}.so"
     subprocess.run(["g++", *CXXFLAGS, "-o", str(out), str(src)], check=True)
     assert run_pins_expand(out), f"planted mistake {name} passed every pin"
+
+
+def run_pins_eps(lib):
+    """Names of the epsilon-composition pins failing for the library at lib."""
+    import test_oracle_eps as E
+    failed = set()
+    for seed in range(40):
+        m1, m2 = E.acyclic_pair(seed) if seed < 25 else E.acyclic_pair(
+            1000 + seed, eps_in=0.3, eps_inner=0.8, eps_out=0.3)
+        try:
+            r = oracle.compose_eps(m1, m2, E.EPS, lib_path=lib)
+            E.assert_relations_equal(E.result_relation(r), E.composed_relation(m1, m2))
+        except (AssertionError, IndexError, ValueError, KeyError):
+            failed.add("relation")
+    for name in ("test_one_output_eps_meets_one_input_eps", "test_two_output_eps_against_one_input_eps",
+                 "test_epsilon_then_symbol", "test_both_sides_empty_everywhere"):
+        fn = getattr(E, name)
+        saved = E.oracle.compose_eps
+        try:
+            E.oracle.compose_eps = lambda *a, **k: saved(*a, lib_path=lib, **k)
+            fn()
+        except (AssertionError, IndexError, ValueError, KeyError):
+            failed.add(name)
+        finally:
+            E.oracle.compose_eps = saved
+    return failed
+
+
+def test_eps_pins_pass_on_the_oracle():
+    assert run_pins_eps(None) == set()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_EPS))
+def test_eps_mutant_is_caught(tmp_path, name):
+    old, new = MUTANTS_EPS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site of {name} not unique"
+    mut = tmp_path / f"{name}.cpp"
+    mut.write_text(src.replace(old, new))
+    lib = tmp_path / f"lib{name}.so"
+    subprocess.run(["g++", *CXXFLAGS, "-o", str(lib), str(mut)], check=True)
+    assert run_pins_eps(lib), f"mutant {name} passes every epsilon pin"
