@@ -66,6 +66,10 @@ def parse():
     ap.add_argument("--paper-pair", default="",
                     help="SIZE-TARGET, e.g. 15k-de: instead of --config, the bigram-LM x "
                          "translation-model pair German -> English -> TARGET at a Table 1 size")
+    ap.add_argument("--eps-pair", action="store_true",
+                    help="instead of --config, a pair with the empty-string label 0 on every "
+                         "tape (2,000 states and 40,000 arcs per side, 5%% empty labels), "
+                         "composed under the three-state epsilon filter (fstc_compose_eps)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB three times "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -157,9 +161,12 @@ def algorithmic_bytes(st: dict, R: int) -> dict:
     }
 
 
-def cpu_baseline(m1, m2, levels: int, reduce: bool = True) -> dict:
+def cpu_baseline(m1, m2, levels: int, reduce: bool = True, eps: bool = False) -> dict:
     import oracle
-    r = oracle.compose(m1, m2, max_levels=levels, reduce=reduce)
+    if eps:
+        r = oracle.compose_eps(m1, m2, 0, max_levels=levels, reduce=reduce)
+    else:
+        r = oracle.compose(m1, m2, max_levels=levels, reduce=reduce)
     return {
         "value": r.num_premerge / r.seconds,
         "unit": "arcs/s",
@@ -197,7 +204,14 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": nbytes, "launches": 3}), file=sys.stderr, flush=True)
         del a_, b_
-    if args.paper_pair:
+    if args.eps_pair:
+        h1, h2 = W.eps_pair(11 + args.seed, nq=2000, narcs=40000, nsym=1000, nouter=500,
+                            eps_inner=0.05, eps_outer=0.05)
+        workload = ("pair with epsilon transitions: 2,000 states and 40,000 arcs per side, "
+                    "inner alphabet 1,000, outer 500, label 0 empty on 5% of each tape, "
+                    f"three-state epsilon filter, seed {11 + args.seed}")
+        traffic_key = None
+    elif args.paper_pair:
         size, target = args.paper_pair.split("-")
         h1, h2 = W.paper_pair(size, target, args.seed)
         workload = (f"bigram-LM x translation-model pair, Table 1 size {size}, German -> English "
@@ -215,6 +229,10 @@ def main():
     def timed(product: bool):
         """Warmup + K timed steps; returns (seconds, last result, summed stats)."""
         def step():
+            if args.eps_pair:
+                return fstc.fstc_compose_eps(m1, m2, 0, max_levels=args.max_levels,
+                                             reduce=not args.no_reduction, fused=args.fused,
+                                             product=product)
             return fstc.fstc_compose(m1, m2, max_levels=args.max_levels,
                                      reduce=not args.no_reduction, fused=args.fused,
                                      product=product)
@@ -233,6 +251,8 @@ def main():
         return time.perf_counter() - t0, last, sums
 
     def phase_times(product: bool):
+        if args.eps_pair:
+            return None  # the per-phase events cover one composition of the two
         r = fstc.fstc_compose(m1, m2, max_levels=args.max_levels, reduce=not args.no_reduction,
                               fused=args.fused, product=product, phase_timing=True)
         torch.cuda.synchronize()
@@ -367,7 +387,8 @@ def main():
     if stream:
         out["hbm_achievable"] = stream
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels, not args.no_reduction)
+        out["cpu_baseline"] = cpu_baseline(h1, h2, args.oracle_levels, not args.no_reduction,
+                                           args.eps_pair)
     print(json.dumps(out), flush=True)
 
 

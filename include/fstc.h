@@ -236,8 +236,54 @@ typedef struct fstc_stats {
 int fstc_compose(const fstc_fst *m1, const fstc_fst *m2, const fstc_opts *opts,
                  hipStream_t stream, fstc_result *out, fstc_stats *stats);
 
-/* Frees every buffer of a result obtained from fstc_compose with the same
- * opts (allocator) and zeroes *r.  Safe on a zeroed result. */
+/*
+ * fstc_compose_eps: M1∘M2 with epsilon transitions.  The paper admits no
+ * epsilon transitions (§2) and names composition filters as what admitting
+ * them takes; this entry point takes the three-state epsilon filter (Mohri,
+ * Pereira and Riley; Allauzen, Riley and Schalkwyk 2009), under which every
+ * pair of paths of M1 and M2 with matching middle strings is aligned exactly
+ * once, so that the result's weight on an (input, output) string pair is the
+ * sum over middle strings y of M1's weight on (input, y) times M2's on
+ * (y, output), the empty string removed.
+ *
+ *   eps            the label value that stands for the empty string on every
+ *                  tape; it must be a symbol of all four alphabets
+ *                  (eps < m1->num_isyms, m1->num_osyms = m2->num_isyms,
+ *                  m2->num_osyms; else FSTC_ERR_INVALID_ARG).
+ *   state_filter   may be NULL; receives a device array [num_states] of the
+ *                  filter state of each state, owned by the result (freed by
+ *                  fstc_result_release).
+ *   other arguments as for fstc_compose; opts->max_levels caps the depth in
+ *   moves of the composed search, the caps apply to the result.
+ *
+ * The result's states are triples (q1, q2, f): state_q1 / state_q2 hold q1 and
+ * q2, state_filter f, id 0 = (start1, start2, 0).  Its arcs (the moves the
+ * filter allows out of a triple, merged as fstc_compose merges unless
+ * opts->no_reduction):
+ *   - an M1 arc with output b != eps and an M2 arc with input b, from any f,
+ *     to f = 0: input and output labels of the two arcs, weight p1 * p2;
+ *   - an M1 arc with output eps and an M2 arc with input eps, from f = 0, to
+ *     f = 0, likewise;
+ *   - an M1 arc with output eps alone (M2 stays), from f = 0 or 2, to f = 2:
+ *     labels (M1 input, eps), weight p1;
+ *   - an M2 arc with input eps alone (M1 stays), from f = 0 or 1, to f = 1:
+ *     labels (eps, M2 output), weight p2.
+ * Accept states: q1 in F1 and q2 in F2, whatever f.  num_premerge_arcs counts
+ * the moves.  Triples from which no accepting state is reachable are kept
+ * (reachable states only, as fstc_compose).
+ *
+ * It runs as two epsilon-free compositions, (M1' ∘ F) ∘ M2', with the filter
+ * F a three-state transducer and M1', M2' relabelled copies of the inputs
+ * (output / input eps renamed, a weight-one loop per state); the first has
+ * at most 3 |Q1| states.  Needs num_arcs + num_states < 2^32 per input.
+ */
+int fstc_compose_eps(const fstc_fst *m1, const fstc_fst *m2, uint32_t eps,
+                     const fstc_opts *opts, hipStream_t stream, fstc_result *out,
+                     uint8_t **state_filter, fstc_stats *stats);
+
+/* Frees every buffer of a result obtained from fstc_compose (or
+ * fstc_compose_eps) with the same opts (allocator) and zeroes *r.  Safe on a
+ * zeroed result. */
 void fstc_result_release(fstc_result *r, const fstc_opts *opts, hipStream_t stream);
 
 /*

@@ -18,7 +18,7 @@ OBJDIR = HERE / "_build"
 LIB = HERE / "libfstc.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["scan.hip", "radix_sort.hip", "csr.hip", "expand.hip", "merge.hip", "compose.hip",
-           "noalloc.hip"]
+           "noalloc.hip", "eps.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",

@@ -1146,6 +1146,123 @@ int fstc_compose(const fstc_fst *m1, const fstc_fst *m2, const fstc_opts *opts,
   });
 }
 
+int fstc_compose_eps(const fstc_fst *m1, const fstc_fst *m2, uint32_t eps, const fstc_opts *opts,
+                     hipStream_t stream, fstc_result *out, uint8_t **state_filter,
+                     fstc_stats *stats) {
+  if (out) std::memset(out, 0, sizeof(*out));
+  if (state_filter) *state_filter = nullptr;
+  if (stats) std::memset(stats, 0, sizeof(*stats));
+  if (!out) return fail(FSTC_ERR_INVALID_ARG, "out is NULL");
+  int rc = check_fst(m1, "m1");
+  if (rc) return rc;
+  rc = check_fst(m2, "m2");
+  if (rc) return rc;
+  if (m1->num_osyms != m2->num_isyms)
+    return fail(FSTC_ERR_ALPHABET, "m1->num_osyms != m2->num_isyms");
+  if (eps >= m1->num_isyms || eps >= m1->num_osyms || eps >= m2->num_osyms)
+    return fail(FSTC_ERR_INVALID_ARG, "eps must be a symbol of every alphabet");
+  const u32 G = m1->num_osyms;  // E1 = G, E2 = G + 1 extend the inner alphabet
+  if (G > 0xfffffffdu) return fail(FSTC_ERR_RANGE, "inner alphabet too large for two more symbols");
+  if (m1->num_arcs + m1->num_states >= (1ull << 32) || m2->num_arcs + m2->num_states >= (1ull << 32))
+    return fail(FSTC_ERR_RANGE, "num_arcs + num_states must be below 2^32");
+  if (opts && ((opts->alloc == nullptr) != (opts->free == nullptr)))
+    return fail(FSTC_ERR_INVALID_ARG, "opts->alloc and opts->free must be set together");
+  if (opts && opts->hash_min_log2 > 31)
+    return fail(FSTC_ERR_INVALID_ARG, "opts->hash_min_log2 must be at most 31");
+  return run_guarded("fstc_compose_eps", stream, [&] {
+    const auto t0 = std::chrono::steady_clock::now();
+    Allocator A;
+    if (opts) {
+      A.fa = opts->alloc;
+      A.ff = opts->free;
+      A.ctx = opts->alloc_ctx;
+    } else {
+      tune_default_pool();
+    }
+    A.stream = stream;
+    // the relabelled inputs and the filter, five arrays each (4 B per arc
+    // and array) in one buffer per transducer, the filter's accept flags last
+    struct Side {
+      Buf b;
+      fstc_fst f{};
+      explicit Side(Allocator *a) : b(a) {}
+      void carve(u64 n, u32 nq, u32 start, u32 nin, u32 nout, const uint8_t *final) {
+        const u64 cols = (std::max<u64>(n, 1) + 63) & ~63ull;
+        char *p = static_cast<char *>(b.ensure(cols * 20 + 256));
+        f = fstc_fst{nq, start, nin, nout, n, (const u32 *)p, (const u32 *)(p + cols * 4),
+                     (const u32 *)(p + cols * 8), (const u32 *)(p + cols * 12),
+                     (const float *)(p + cols * 16), final ? final : (const uint8_t *)(p + cols * 20)};
+      }
+      u32 *col(int i) const { return const_cast<u32 *>(i == 0 ? f.src : i == 1 ? f.dst : i == 2 ? f.ilabel : f.olabel); }
+      float *w() const { return const_cast<float *>(f.weight); }
+    };
+    Side s1(&A), s2(&A), sf(&A);
+    s1.carve(m1->num_arcs + m1->num_states, m1->num_states, m1->start, m1->num_isyms, G + 2,
+             m1->final);
+    s2.carve(m2->num_arcs + m2->num_states, m2->num_states, m2->start, G + 2, m2->num_osyms,
+             m2->final);
+    sf.carve(3ull * (G - 1) + 5, 3, 0, G + 2, G + 2, nullptr);
+    build_eps_side(*m1, true, eps, G + 1, G, s1.col(0), s1.col(1), s1.col(2), s1.col(3), s1.w(),
+                   stream);
+    build_eps_side(*m2, false, eps, G, G + 1, s2.col(0), s2.col(1), s2.col(2), s2.col(3), s2.w(),
+                   stream);
+    build_eps_filter(G, eps, sf.col(0), sf.col(1), sf.col(2), sf.col(3), sf.w(),
+                     const_cast<uint8_t *>(sf.f.final), stream);
+    // M1' ∘ F: every joined pair is an arc (weights w1 * 1 exactly), the
+    // whole search (at most 3 |Q1| states)
+    fstc_opts oa{};
+    if (opts) oa = *opts;
+    oa.max_levels = 0;
+    oa.max_states = 0;
+    oa.max_arcs = 0;
+    oa.no_reduction = 1;
+    oa.fused_merge = 0;
+    oa.phase_timing = 0;
+    check_csr_ranges(s1.f, true);
+    check_csr_ranges(sf.f, false);
+    fstc_result ra{};
+    struct Release {
+      fstc_result *r;
+      Allocator *A;
+      bool armed = true;
+      ~Release() {
+        if (!armed) return;
+        for (int i = 0; i < 8; ++i)
+          if (r->alloc_ptr[i]) A->free(r->alloc_ptr[i], r->alloc_bytes[i]);
+        std::memset(r, 0, sizeof(*r));
+      }
+    };
+    Release ga{&ra, &A};
+    {
+      Composer c(s1.f, sf.f, &oa, stream, nullptr);
+      c.run(&ra);
+    }
+    // (M1' ∘ F) ∘ M2' with the caller's options; its start is id 0 = (s1, 0)
+    if (ra.num_states >= (1ull << 32)) throw Error(FSTC_ERR_RANGE, "filter composition too large");
+    const fstc_fst fa{(u32)ra.num_states, 0, m1->num_isyms, G + 2, ra.num_arcs, ra.src, ra.dst,
+                      ra.ilabel, ra.olabel, ra.weight, ra.final};
+    check_csr_ranges(fa, true);
+    check_csr_ranges(s2.f, false);
+    Release go{out, &A};
+    {
+      Composer c(fa, s2.f, opts, stream, stats);
+      c.run(out);
+    }
+    Buf fb(&A);
+    uint8_t *filt = static_cast<uint8_t *>(fb.ensure(std::max<u64>(out->num_states, 1)));
+    map_eps_states(out->state_q1, ra.state_q1, ra.state_q2, out->num_states, filt, stream);
+    FSTC_HIP(hipGetLastError());
+    size_t bytes = 0;
+    out->alloc_ptr[4] = fb.detach(&bytes);
+    out->alloc_bytes[4] = bytes;
+    if (state_filter) *state_filter = filt;
+    go.armed = false;
+    if (stats)
+      stats->ms_total =
+          std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0).count();
+  });
+}
+
 void fstc_result_release(fstc_result *r, const fstc_opts *opts, hipStream_t stream) {
   if (!r) return;
   Allocator A;

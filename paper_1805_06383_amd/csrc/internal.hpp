@@ -169,6 +169,21 @@ size_t csr_temp_bytes(const fstc_fst &m);
 // Exclusive scan of n u64 values (out has n + 1 entries) using the device's
 // file-scope scratch array instead of allocated temporaries (noalloc.hip);
 // n at most noalloc_scan_max_n().  Synchronises the stream.
+// Composition with epsilon transitions (eps.hip): the relabelled inputs and
+// the filter transducer of the filter composition (M1' ∘ F) ∘ M2', and the
+// map of its states back to (q1, q2, filter state).
+// M1' (by_output: output eps -> e_rename, loops eps:e_loop) or M2' (input
+// eps -> e_rename, loops e_loop:eps): num_arcs + num_states arcs.
+void build_eps_side(const fstc_fst &m, bool by_output, u32 eps, u32 e_rename, u32 e_loop,
+                    u32 *src, u32 *dst, u32 *il, u32 *ol, float *w, hipStream_t s);
+// F over nsym inner symbols (E1 = nsym, E2 = nsym + 1): 3 (nsym - 1) + 5 arcs,
+// 3 states, all accepting.
+void build_eps_filter(u32 nsym, u32 eps, u32 *src, u32 *dst, u32 *il, u32 *ol, float *w,
+                      uint8_t *final, hipStream_t s);
+// q1[i] (a state of M1' ∘ F) -> aq1[q1[i]]; filt[i] = af[q1[i]].
+void map_eps_states(u32 *q1, const u32 *aq1, const u32 *af, u64 n, uint8_t *filt,
+                    hipStream_t s);
+
 u64 noalloc_scan_max_n();
 void noalloc_scan(const u64 *in, u64 *out, u64 n, hipStream_t s);
 

@@ -84,7 +84,7 @@ class FstcStats(ctypes.Structure):
                 ("reserved1", _u32), ("peak_device_bytes", _u64)]
 
 
-EXPORTS = ("fstc_compose", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",
+EXPORTS = ("fstc_compose", "fstc_compose_eps", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",
            "fstc_exclusive_scan_u64", "fstc_exclusive_scan_u64_noalloc", "fstc_strerror",
            "fstc_last_error_detail", "fstc_version")
 
@@ -104,6 +104,10 @@ def load_library(path: Path | str | None = None) -> ctypes.CDLL:
                                  ctypes.POINTER(FstcOpts), _vp, ctypes.POINTER(FstcResult),
                                  ctypes.POINTER(FstcStats)]
     lib.fstc_compose.restype = ctypes.c_int
+    lib.fstc_compose_eps.argtypes = [ctypes.POINTER(FstcFst), ctypes.POINTER(FstcFst), _u32,
+                                     ctypes.POINTER(FstcOpts), _vp, ctypes.POINTER(FstcResult),
+                                     ctypes.POINTER(_vp), ctypes.POINTER(FstcStats)]
+    lib.fstc_compose_eps.restype = ctypes.c_int
     lib.fstc_result_release.argtypes = [ctypes.POINTER(FstcResult), ctypes.POINTER(FstcOpts), _vp]
     lib.fstc_result_release.restype = None
     lib.fstc_build_csr.argtypes = [ctypes.POINTER(FstcFst), ctypes.c_int, _vp] + [_vp] * 9
@@ -243,14 +247,18 @@ class Composed:
     olabel: torch.Tensor
     weight: torch.Tensor
     stats: dict = field(default_factory=dict)
+    state_filter: torch.Tensor | None = None  # uint8 filter state (fstc_compose_eps)
 
     def to_host(self):
-        """numpy view: q1, q2, final, src, dst, a, c, w (uint32 / float32)."""
+        """numpy view: q1, q2, final, src, dst, a, c, w (uint32 / float32),
+        and f (filter states) for a composition with epsilon transitions."""
         def u(t):
             return t.cpu().numpy().view(np.uint32)
         return HostComposed(u(self.state_q1), u(self.state_q2), self.final.cpu().numpy(),
                             u(self.src), u(self.dst), u(self.ilabel), u(self.olabel),
-                            self.weight.cpu().numpy(), self.num_premerge_arcs, self.num_levels)
+                            self.weight.cpu().numpy(), self.num_premerge_arcs, self.num_levels,
+                            None if self.state_filter is None
+                            else self.state_filter.cpu().numpy())
 
 
 @dataclass
@@ -265,6 +273,7 @@ class HostComposed:
     w: np.ndarray
     num_premerge: int
     levels: int
+    f: np.ndarray | None = None
 
     @property
     def num_states(self):
@@ -308,6 +317,35 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
                           _stream_handle(stream), ctypes.byref(res),
                           ctypes.byref(st) if want_stats else None)
     _check(rc)
+    return _wrap(res, st if want_stats else None, alloc, device)
+
+
+def fstc_compose_eps(m1: DeviceFST, m2: DeviceFST, eps: int, max_levels: int = 0,
+                     deterministic_ids: bool = False, max_states: int = 0, max_arcs: int = 0,
+                     stream=None, want_stats: bool = True, reduce: bool = True,
+                     fused: bool = False, product: bool = True,
+                     hash_visited: bool = False) -> Composed:
+    """Composition with epsilon transitions (see fstc_compose_eps in fstc.h):
+    label ``eps`` is the empty string on every tape; states are triples, the
+    filter state in ``state_filter``.  Options as for fstc_compose."""
+    lib = load_library()
+    device = m1.src.device if m1.num_arcs else m1.final.device
+    alloc = TorchAllocator(device)
+    opts = alloc.opts(max_levels, deterministic_ids, max_states, max_arcs, reduce, fused, product,
+                      hash_visited, False, 0)
+    s1, s2 = m1.struct(), m2.struct()
+    res = FstcResult()
+    st = FstcStats()
+    filt = _vp()
+    rc = lib.fstc_compose_eps(ctypes.byref(s1), ctypes.byref(s2), int(eps), ctypes.byref(opts),
+                              _stream_handle(stream), ctypes.byref(res), ctypes.byref(filt),
+                              ctypes.byref(st) if want_stats else None)
+    _check(rc)
+    return _wrap(res, st if want_stats else None, alloc, device, filt.value)
+
+
+def _wrap(res, st, alloc, device, filt_ptr=None) -> Composed:
+    """A result of the C ABI as tensors that own its allocations."""
     ns, na = int(res.num_states), int(res.num_arcs)
     owners = [(int(res.alloc_ptr[i]), alloc.take(res.alloc_ptr[i])) for i in range(8)
               if res.alloc_ptr[i]]
@@ -325,12 +363,13 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
                 return _view(buf[ptr - base:], n, dtype, device)
         raise RuntimeError("result array outside its recorded allocations")
 
-    stats = {k: getattr(st, k) for k, _ in FstcStats._fields_} if want_stats else {}
+    stats = {k: getattr(st, k) for k, _ in FstcStats._fields_} if st is not None else {}
     return Composed(ns, na, int(res.num_premerge_arcs), int(res.num_levels),
                     view(res.state_q1, ns, i32), view(res.state_q2, ns, i32),
                     view(res.final, ns, u8), view(res.src, na, i32), view(res.dst, na, i32),
                     view(res.ilabel, na, i32), view(res.olabel, na, i32),
-                    view(res.weight, na, f32), stats)
+                    view(res.weight, na, f32), stats,
+                    view(filt_ptr, ns, u8) if filt_ptr is not None else None)
 
 
 def fstc_result_release(result: FstcResult, opts: FstcOpts | None = None, stream=None):
@@ -348,6 +387,15 @@ def compose(m1, m2, device="cuda", **kw) -> Composed:
     if not isinstance(m2, DeviceFST):
         m2 = DeviceFST.from_host(m2, device)
     return fstc_compose(m1, m2, **kw)
+
+
+def compose_eps(m1, m2, eps: int, device="cuda", **kw) -> Composed:
+    """Host or device transducers in, device result out (epsilon transitions)."""
+    if not isinstance(m1, DeviceFST):
+        m1 = DeviceFST.from_host(m1, device)
+    if not isinstance(m2, DeviceFST):
+        m2 = DeviceFST.from_host(m2, device)
+    return fstc_compose_eps(m1, m2, eps, **kw)
 
 
 def fstc_build_csr(m: DeviceFST, by_output: bool, stream=None) -> dict:

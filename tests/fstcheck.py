@@ -47,6 +47,13 @@ def canon_of(res) -> Canon:
     return canon(res.q1, res.q2, res.final, res.src, res.dst, res.a, res.c, res.w)
 
 
+def canon_eps(res) -> Canon:
+    """Canonical form of a composition with epsilon transitions, whose states
+    are triples (q1, q2, f): the pair column q2 carries 3 q2 + f."""
+    q2f = np.asarray(res.q2, np.uint64) * 3 + np.asarray(res.f, np.uint64)
+    return canon(res.q1, q2f, res.final, res.src, res.dst, res.a, res.c, res.w)
+
+
 def unique_rows(x: np.ndarray) -> bool:
     if len(x) < 2:
         return True
@@ -261,6 +268,17 @@ def multiset_of(res) -> Multiset:
                      np.asarray(res.c, np.int64), wbits], 1) if len(src) else np.zeros((0, 7), np.int64)
     rows = rows[np.lexsort(rows.T[::-1])] if len(rows) else rows
     return Multiset(states, finals, rows)
+
+
+def multiset_eps(res) -> Multiset:
+    """multiset_of for a composition with epsilon transitions (3 q2 + f in the
+    q2 column)."""
+    class _R:
+        pass
+    r = _R()
+    r.q1, r.final, r.src, r.dst, r.a, r.c, r.w = res.q1, res.final, res.src, res.dst, res.a, res.c, res.w
+    r.q2 = np.asarray(res.q2, np.int64) * 3 + np.asarray(res.f, np.int64)
+    return multiset_of(r)
 
 
 def assert_same_multiset(got: Multiset, ref: Multiset, what: str = ""):
