@@ -276,8 +276,12 @@ struct ScanPublish {
   u32 words, seq_word, seq;
 };
 size_t scan_lb_state_bytes(u64 n);
+// skip_if (may be NULL): a device word read by every workgroup first; when it
+// is nonzero the scan does nothing at all (a scan enqueued before the host
+// knows whether it is needed).
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
-                       hipStream_t s, const ScanPublish *pub = nullptr);
+                       hipStream_t s, const ScanPublish *pub = nullptr,
+                       const u64 *skip_if = nullptr);
 
 // Stable LSD radix sort of (u64 key, u32 value) on key bits [lo, hi).
 // keys/vals hold the input; keys_alt/vals_alt are scratch of the same size;

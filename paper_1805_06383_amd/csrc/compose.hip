@@ -500,6 +500,9 @@ void Composer::run(fstc_result *out) {
   u32 product_launches = 0;
   u64 product_mfma_sources = 0;
   u32 vis_moves = 0, direct_levels = 0;
+  // the previous level was a direct product level (or none has run): the
+  // next one is enqueued whole before the host reads its counts
+  bool last_direct = true;
 
   ArcCols out_arcs(&A, s);
   // single-pass scan state: zero-filled when (re)allocated, then written
@@ -642,7 +645,51 @@ void Composer::run(fstc_result *out) {
       launch_prod_sources(pm, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
       T.at(kNone);
     }
-    wait_published(seq1);
+    // Direct level enqueued whole: after the product kernel, the scans, id
+    // assignment, totals and target fix-up of a direct level go to the stream
+    // too, each reading the level's record count on the device and doing
+    // nothing when it is not zero (k_merged_total then only publishes the
+    // count's totals); the host waits once, at that publication, sized by
+    // bounds: every source's largest table for the new pairs and arcs.
+    const bool ahead = direct && last_direct;
+    u32 seq_wait = seq1;
+    if (ahead) {
+      const u64 newcap_b = std::min<u64>((u64)nsrc * maxk, pairspace - n_states);
+      sq1b.grow_keep((n_states + newcap_b) * 4, n_states * 4);
+      sq2b.grow_keep((n_states + newcap_b) * 4, n_states * 4);
+      T.at(kAssign);
+      ScanJob jobs[3] = {{newc.p, false, newoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()},
+                         {mend.p, true, aoff.as<u64>()}};
+      jobs[1].total_only = true;
+      jobs[2].sub = tstart.as<u64>();
+      exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, nullptr,
+                        roff.as<u64>() + nsrc);
+      MergeArgs md{};  // the fields the direct-level kernels read
+      md.R_dev = roff.as<u64>() + nsrc;
+      md.nsrc = nsrc;
+      md.lo = lo;
+      md.st = dst;
+      md.newc = newc.as<u32>();
+      md.poff = poff.as<u64>();
+      md.tstart = tstart.as<u64>();
+      md.mend = mend.as<u64>();
+      md.vis = hvb.as<u32>();
+      md.vn2 = vn2;
+      md.hmask = hcap - 1;
+      md.out_src = out_arcs.col(0);
+      md.out_dst = out_arcs.col(1);
+      md.out_il = out_arcs.col(2);
+      md.out_ol = out_arcs.col(3);
+      md.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+      md.out_base = arcs;
+      launch_assign_direct(md, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
+      seq_wait = next_publication();
+      launch_merged_total(aoff.as<u64>() + nsrc, newoff.as<u64>() + nsrc, ptot.as<u64>() + nsrc, md,
+                          hs_dev, seq_wait, s);
+      launch_fix_marked(md, (u64)nsrc * maxk, s);
+      T.at(kNone);
+    }
+    wait_published(seq_wait);
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
     const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
@@ -804,7 +851,30 @@ void Composer::run(fstc_result *out) {
     const bool early = !direct_level && !o.no_reduction && !o.deterministic_ids && !o.max_arcs &&
                        (n_states + newcap) * 8 <= kEarlyBytes &&
                        (arcs + R + prodpos) * 20 <= kEarlyBytes;
-    if (direct_level) {
+    last_direct = direct_level;
+    if (direct_level && ahead) {
+      // everything ran before the wait: read the totals
+      ++product_launches;
+      status_clear = true;  // k_merged_total cleared the level counters
+      nnew = hs->st.nnew;
+      merged = hs->st.merged;
+      premerge += hs->st.prod_records;
+      product_records += hs->st.prod_records;
+      max_level_pre = std::max(max_level_pre, hs->st.prod_records);
+      if (merged < prodpos) {  // entries without a term leave holes: close them
+        ma.out_src = out_arcs.col(0);
+        ma.out_dst = out_arcs.col(1);
+        ma.out_il = out_arcs.col(2);
+        ma.out_ol = out_arcs.col(3);
+        ma.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+        ma.out_base = arcs;
+        Tmp rows(&level_tmp);
+        rows.ensure(prodpos * 20);
+        launch_close_holes(ma, aoff.as<u64>(), prodpos, rows.p, s);
+      }
+      assigned = true;
+      ++direct_levels;
+    } else if (direct_level) {
       // the level's merged arcs are in the result at arcs + poff[u]: new
       // pairs per source scanned into id offsets, joined pairs and merged
       // arcs per source summed (the latter scanned too, for entries without

@@ -1806,6 +1806,7 @@ __global__ __launch_bounds__(256) void k_newlist_sources(MergeArgs a, const u64 
 // source has at most 64), all loaded before any is assigned.
 __global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *newoff, u32 base,
                                                        u32 *sq1, u32 *sq2) {
+  if (a.R_dev && *a.R_dev != 0) return;  // enqueued ahead: the level has records
   const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   const u64 u = t / 4;
   const u32 j = (u32)(t % 4), lane = lane_id();
@@ -1855,6 +1856,11 @@ __device__ __forceinline__ u32 fixed_target(const MergeArgs &a, u32 x) {
 }
 
 __global__ void k_fix_marked(MergeArgs a, u64 n) {
+  if (a.R_dev) {  // enqueued ahead: n bounds the level's entries, whose count is the
+                  // total of the entry scan (the level counters are cleared by now)
+    if (*a.R_dev != 0) return;
+    n = min<u64>(n, a.poff[a.nsrc]);
+  }
   u32 *dst = a.out_dst + a.out_base;
   const u64 head = std::min<u64>(n, (4u - ((u32)(reinterpret_cast<uintptr_t>(dst) >> 2) & 3u)) & 3u);
   const u64 nv = (n - head) / 4;
@@ -2186,6 +2192,13 @@ __global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 
                                                        Status *st, MergeArgs a, Status *host,
                                                        u32 seq) {
   __shared__ u64 s_v[3][1024 / kWave];
+  if (a.R_dev && *a.R_dev != 0) {
+    // enqueued ahead of a level that turned out to have records: publish the
+    // level's counters as they are (the count's totals), change nothing
+    __threadfence();
+    publish(st, host, seq, threadIdx.x, blockDim.x);
+    return;
+  }
   u64 v[3] = {0, 0, 0};
   for (u64 t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
     const uint4 td = a.tiles[t];

@@ -113,6 +113,7 @@ struct LbArgs {
   u32 nb, epoch;
   u64 *state;   // [nb * kLbWords]
   u32 *ctr, *err;
+  const u64 *skip_if;  // nonzero *skip_if: nothing to do
 };
 
 __device__ __forceinline__ void put_out(const LbArgs &p, int k, u64 i, u64 v) {
@@ -145,6 +146,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __shared__ u64 scratch[kLbNT / kWave];
   __shared__ u64 s_x[STRIPED ? kLbTile + kLbTile / 32 : 1];  // one array of the tile, transposed
   const u32 lane = lane_id();
+  if (p.skip_if && *p.skip_if != 0) return;  // uniform: every workgroup leaves before the counter
   // tile numbers from the counter (a single tile needs none)
   if (threadIdx.x == 0 && p.nb > 1) {
     const u32 t = atomicAdd(p.ctr, 1u);
@@ -377,7 +379,7 @@ size_t scan_lb_state_bytes(u64 n) {
 }
 
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
-                       hipStream_t s, const ScanPublish *pub) {
+                       hipStream_t s, const ScanPublish *pub, const u64 *skip_if) {
   static std::atomic<u32> epochs{0};
   const u64 nb = std::max<u64>(1, ceil_div(n, kLbTile));
   if (nb >= (1ull << 31)) throw Error(FSTC_ERR_CAPACITY, "scan too large for one launch");
@@ -402,6 +404,7 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   p.state = static_cast<u64 *>(state);
   p.ctr = ctr;
   p.err = err;
+  p.skip_if = skip_if;
   const dim3 g((unsigned)nb), bl(kLbNT);
   // striped once the tiles outnumber the compute units
   if (nb > (u64)compute_units()) {
