@@ -318,7 +318,10 @@ void copy_columns(const void *src, u64 sstride, void *dst, u64 dstride, u64 used
 
 // The five result columns (src, dst, ilabel, olabel, weight; 4 bytes each)
 // in one grow-only buffer: column i at byte i * cap * 4.  Growth is one
-// allocation and one copy kernel over the rows kept.
+// allocation and one copy kernel over the rows kept, by at least 4x at every
+// size: the result grows fastest in the levels where the search widens, and
+// a smaller factor copies large results several times over (without
+// reduction at config 4, 2x growth copied 25 GB for a 19.7 GB result).
 struct ArcCols {
   Buf b;
   u64 cap = 0;  // entries per column
@@ -327,7 +330,7 @@ struct ArcCols {
   explicit ArcCols(Allocator *A, hipStream_t st) : b(A), s(st) {}
   void grow(u64 need, u64 used) {
     if (need <= cap && b.p) return;
-    u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), grown(5 * cap * 4) / 20);
+    u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), 4 * cap);
     nc = (nc + 63) & ~63ull;  // columns 256-byte aligned
     Buf nb(b.A);
     nb.ensure(5 * nc * 4);
@@ -427,6 +430,11 @@ void Composer::run(fstc_result *out) {
   alloc_csr(m1, cb1, c1);
   alloc_csr(m2, cb2, c2);
   const bool product = !o.no_reduction && !o.no_product_merge;
+  // without reduction, levels whose sources are all strided four-source
+  // product sources resolve each source's targets once and write its joined
+  // pairs from the two weight matrices (no records, no per-record probe)
+  const bool unred_prod = o.no_reduction && !o.no_product_merge && !o.deterministic_ids &&
+                          !o.max_arcs;
   T.at(kCsr);
   {
     // the two layouts are independent: M2's is built on a side stream
@@ -445,9 +453,9 @@ void Composer::run(fstc_result *out) {
     FSTC_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
     SideJoin join{s, side};
     build_csr(m2, false, csr_tmp2, c2, dcounts + 3, &dst->err, side.s);
-    if (product) build_cell_flags(c2, c2.cell_flag, side.s);
+    if (product || unred_prod) build_cell_flags(c2, c2.cell_flag, side.s);
     build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
-    if (product) build_cell_flags(c1, c1.cell_flag, s);
+    if (product || unred_prod) build_cell_flags(c1, c1.cell_flag, s);
   }
   T.at(kNone);
   FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 6 * sizeof(u64), hipMemcpyDeviceToHost, s));
@@ -558,17 +566,20 @@ void Composer::run(fstc_result *out) {
     la.newc = newc.as<u32>();
     // strided product sources four per wave (dense visited array as of the
     // count; a move to the dense array later in the level keeps them listed)
-    const bool quad = product && dense_vis;
+    const bool uprod = unred_prod && dense_vis;
+    const bool quad = (product || uprod) && dense_vis;
+    la.prod = (product || uprod) ? 1u : 0u;
+    la.unred = uprod ? 1u : 0u;
     la.quad = quad ? 1u : 0u;
     la.glist = glist.as<u32>();
     la.grp = grp.as<u32>();
-    T.at(kCount);
-    launch_count(la, s);
-    // records, matches and product-merge entries per source; the product
-    // sources' flags summed; the scan's last tile stores the level totals
-    // (R, M, product entries, product sources) and publishes the counters
-    const u32 seq1 = next_publication();
-    {
+    // count + level scan: records, matches and product-merge entries per
+    // source; the product sources' flags summed; the scan's last tile stores
+    // the level totals (R, M, product entries, product sources) and
+    // publishes the counters as publication `seq`
+    auto count_and_scan = [&](u32 seq) {
+      T.at(kCount);
+      launch_count(la, s);
       ScanJob jobs[4] = {{cnt.p, true, roff.as<u64>()}, {mc.p, false, moff.as<u64>()},
                          {pk.p, false, poff.as<u64>()}, {pflag.p, true, ftot.as<u64>()}};
       jobs[3].total_only = true;
@@ -577,10 +588,12 @@ void Composer::run(fstc_result *out) {
       jobs[2].total_to = &dst->prod_entries;
       jobs[3].total_to = reinterpret_cast<u64 *>(&dst->nprod);  // nprod, nprod_mfma
       const ScanPublish pub{dst, hs_dev, (u32)(sizeof(Status) / 4), (u32)(offsetof(Status, seq) / 4),
-                            seq1};
+                            seq};
       exclusive_scan_lb(jobs, 4, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, &pub);
-    }
-    T.at(kNone);
+      T.at(kNone);
+    };
+    const u32 seq1 = next_publication();
+    count_and_scan(seq1);
     // Speculative product merge: with the dense visited array (no rehash
     // between the count and the merge) the product kernel is launched
     // before the host reads the level's counts, on temp slots reserved for
@@ -690,6 +703,15 @@ void Composer::run(fstc_result *out) {
       T.at(kNone);
     }
     wait_published(seq_wait);
+    if (uprod && hs->st.nprod && hs->st.R) {
+      // without reduction a level takes the product form only whole: this
+      // one has other sources too, so every source goes through records
+      launch_reset_level(dst, s);
+      la.prod = la.unred = la.quad = 0u;
+      const u32 seq1b = next_publication();
+      count_and_scan(seq1b);
+      wait_published(seq1b);
+    }
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
     const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
@@ -1003,6 +1025,79 @@ void Composer::run(fstc_result *out) {
       dense_records += hs->st.dense_records;
       dense_runs += hs->st.dense_runs;
       sort_runs += hs->st.sort_runs;
+    } else if (nprod) {
+      // without reduction, every source a strided product source (R == 0):
+      // the four-source kernel resolves each source's targets into utab
+      // (claims marked), the claims are numbered and the marks fixed as on
+      // a direct level, then every joined pair is written from the two
+      // weight matrices
+      T.at(kMerge);
+      Tmp utab(&level_tmp);
+      utab.ensure(std::max<u64>(prodpos, 1) * 4);
+      MergeArgs pa{};
+      pa.nsrc = nsrc;
+      pa.lo = lo;
+      pa.st = dst;
+      pa.pk = pk.as<u32>();
+      pa.phdr = phdr.as<uint4>();
+      pa.poff = poff.as<u64>();
+      pa.parts1 = c1.parts;
+      pa.parts2 = c2.parts;
+      pa.arcs1 = c1.arcs;
+      pa.arcs2 = c2.arcs;
+      pa.wts1 = c1.wts;
+      pa.wts2 = c2.wts;
+      pa.seg_sym1 = c1.seg_sym;
+      pa.seg_off1 = c1.seg_off;
+      pa.seg_sym2 = c2.seg_sym;
+      pa.seg_off2 = c2.seg_off;
+      pa.vis = hvb.as<u32>();
+      pa.vn2 = vn2;
+      pa.hmask = hcap - 1;
+      pa.tstart = tstart.as<u64>();
+      pa.mend = mend.as<u64>();
+      pa.pcnt = cnt.as<u64>();
+      pa.newc = newc.as<u32>();
+      pa.quad = 1;
+      pa.glist = glist.as<u32>();
+      pa.utab = utab.as<u32>();
+      T.at(kProductKernel);
+      launch_prod_sources(pa, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+      ++product_launches;
+      T.at(kAssign);
+      {
+        ScanJob jobs[2] = {{newc.p, false, newoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()}};
+        exclusive_scan_lb(jobs, 2, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+      }
+      const u64 newcap_u = std::min<u64>(prodpos, pairspace - n_states);
+      sq1b.grow_keep((n_states + newcap_u) * 4, n_states * 4);
+      sq2b.grow_keep((n_states + newcap_u) * 4, n_states * 4);
+      pa.out_dst = utab.as<u32>();
+      pa.out_base = 0;
+      launch_assign_direct(pa, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
+      launch_fix_marked(pa, prodpos, s);
+      const u32 seq2 = next_publication();
+      launch_merged_total(ptot.as<u64>() + nsrc, newoff.as<u64>() + nsrc, ptot.as<u64>() + nsrc,
+                          pa, hs_dev, seq2, s);
+      T.at(kNone);
+      wait_published(seq2);
+      status_clear = true;  // k_merged_total cleared the level counters
+      nnew = hs->st.nnew;
+      merged = hs->st.merged;  // every joined pair is an arc
+      premerge += merged;
+      product_records += merged;
+      max_level_pre = std::max(max_level_pre, merged);
+      T.at(kMerge);
+      out_arcs.grow(arcs + merged, arcs);
+      pa.out_src = out_arcs.col(0);
+      pa.out_dst = out_arcs.col(1);
+      pa.out_il = out_arcs.col(2);
+      pa.out_ol = out_arcs.col(3);
+      pa.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+      pa.out_base = arcs;
+      launch_unreduced_product(pa, ptot.as<u64>(), s);
+      T.at(kNone);
+      assigned = true;
     } else {
       if (o.max_arcs && arcs + R > o.max_arcs)
         throw Error(FSTC_ERR_CAPACITY, "composed arcs exceed opts->max_arcs");

@@ -166,6 +166,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     r = Ranges{a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]};
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
     if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r, mf);
+    if (pk && a.unred && !(a.quad && (a.phdr[2 * u].w & 4u))) pk = 0;  // records
     a.pk[u] = pk;
     a.pflag[u] = pk ? 1ull | ((u64)mf << 32) : 0ull;
     if (pk) {

@@ -142,6 +142,8 @@ struct LevelArgs {
                          // kernel (dense visited array), the others to glist
   u32 *glist;            // [nsrc] product sources for the one-per-wave kernel (st->ngen)
   u32 *grp;              // [nsrc] sources for the 16-lane joins (st->ngrp)
+  u32 unred;             // composition without reduction: only strided sources with
+                         // the four-source kernel take the product form
 };
 
 // Target column marks of a direct product level (MergeArgs::out_src), and
@@ -225,7 +227,19 @@ struct MergeArgs {
   float *out_w;
   u64 out_base;
   const u32 *row1, *seg_sym1, *seg_off1, *row2, *seg_sym2, *seg_off2;
+  // composition without reduction, a level of strided product sources
+  // (utab != NULL): the four-source kernel resolves only the targets, entry
+  // r of source u at utab[poff[u] + r] marked like the target column of a
+  // direct level; launch_unreduced_product then writes every joined pair
+  u32 *utab;
 };
+
+// Composition without reduction, a level whose sources all took the
+// four-source form and whose targets utab holds as ids: source u's joined
+// pairs as arcs at out_base + off[u] .. (off: exclusive scan of the joined
+// pairs per source), entry (p1, p2) times symbol g at
+// (p1 P2 + p2) na + g, weight the float32 product of the two arc weights.
+void launch_unreduced_product(const MergeArgs &a, const u64 *off, hipStream_t s);
 
 // Tile descriptors of the level (a.tiles), then the two tile merges: the
 // dense-table kernel (only when a.key_bits <= kDenseKeyBits) and the sort

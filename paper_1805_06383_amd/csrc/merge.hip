@@ -1402,7 +1402,9 @@ __global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
                         atomicCAS(&a.vis[hslot], kUnvisited, kClaimed) == kUnvisited;
     claimed = is_new;
     const bool known = hcur < kClaimed;  // an id from an earlier level
-    if (a.out_src) {
+    if (a.utab) {
+      a.utab[pu + rank] = known ? hcur : ((u32)hslot | kDstSlot | (is_new ? kDstClaim : 0u));
+    } else if (a.out_src) {
       const u64 p = a.out_base + pu + rank;
       a.out_src[p] = a.lo + (u32)u;
       a.out_dst[p] = known ? hcur : ((u32)hslot | kDstSlot | (is_new ? kDstClaim : 0u));
@@ -1422,6 +1424,59 @@ __global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
     a.mend[u] = a.R + pu + K;
     a.pcnt[u] = (u64)na * K;
     a.newc[u] = (u32)__popcll(cm & bmask);
+  }
+}
+
+// Composition without reduction, a level of strided product sources whose
+// targets are resolved (utab holds ids): one wave per source, lane g for
+// symbol g, writes the na joined pairs of each entry (p1, p2) -- the float32
+// product of the M1 arc of part p1 and the M2 arc of part p2 at symbol g
+// -- with the entry's target and labels.
+__global__ __launch_bounds__(256) void k_unreduced_product(MergeArgs a, const u64 *off) {
+  const u32 lane = lane_id();
+  const u64 u = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+  if (u >= a.nsrc) return;
+  const u32 K = a.pk[u];
+  if (!K) return;
+  const uint4 h0 = a.phdr[2 * u], h1 = a.phdr[2 * u + 1];
+  const u32 P1 = h0.z & 0xffffu, P2 = h0.z >> 16, na = h0.w >> 8;
+  if (!(h0.w & 4u) || P1 * P2 != K || P1 > 4 || P2 > 4 || na > (u32)kWave) {
+    if (lane == 0) set_error(&a.st->err, kErrBounds);  // impossible: the selection checked it
+    return;
+  }
+  const u64 base = a.out_base + off[u];
+  const u32 *tab = a.utab + a.poff[u];
+  const u32 src = a.lo + (u32)u;
+  const bool g_ok = lane < na;
+  float w1[4], w2[4];
+#pragma unroll
+  for (u32 p = 0; p < 4; ++p) {
+    w1[p] = (g_ok && p < P1) ? __uint_as_float(a.wts1[h1.y + P1 * lane + p]) : 0.f;
+    w2[p] = (g_ok && p < P2) ? __uint_as_float(a.wts2[h1.w + P2 * lane + p]) : 0.f;
+  }
+#pragma unroll
+  for (u32 p1 = 0; p1 < 4; ++p1) {
+    if (p1 >= P1) break;
+    const u32 il = a.parts1[h0.x + p1].y;
+#pragma unroll
+    for (u32 p2 = 0; p2 < 4; ++p2) {
+      if (p2 >= P2) break;
+      const u32 e = p1 * P2 + p2;
+      const u32 t = tab[e];
+      if (t & kDstSlot) {  // impossible: every target was numbered before this kernel
+        if (lane == 0) set_error(&a.st->err, kErrBounds);
+        return;
+      }
+      const u32 ol = a.parts2[h0.y + p2].y;
+      if (g_ok) {
+        const u64 k = base + (u64)e * na + lane;
+        a.out_src[k] = src;
+        a.out_dst[k] = t;
+        a.out_il[k] = il;
+        a.out_ol[k] = ol;
+        a.out_w[k] = w1[p1] * w2[p2];
+      }
+    }
   }
 }
 
@@ -2365,6 +2420,12 @@ void launch_assign_direct(const MergeArgs &a, const u64 *newoff, u32 base, u32 *
   if (!a.nsrc) return;
   hipLaunchKernelGGL(k_assign_direct, dim3((unsigned)ceil_div((u64)a.nsrc * 4, 256)), dim3(256), 0,
                      s, a, newoff, base, sq1, sq2);
+}
+
+void launch_unreduced_product(const MergeArgs &a, const u64 *off, hipStream_t s) {
+  if (!a.nsrc) return;
+  hipLaunchKernelGGL(k_unreduced_product, dim3((unsigned)ceil_div((u64)a.nsrc * kWave, 256)),
+                     dim3(256), 0, s, a, off);
 }
 
 void launch_fix_marked(const MergeArgs &a, u64 n, hipStream_t s) {
