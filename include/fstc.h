@@ -143,6 +143,14 @@ typedef struct fstc_opts {
                                  from the start (2^31 slots take 24 GiB);
                                  for tests of large slot numbers.  Values
                                  above 31 give FSTC_ERR_INVALID_ARG       */
+  uint32_t no_small_levels;   /* nonzero: every level takes the per-level
+                                 kernels.  0: while a level has at most 512
+                                 pairs and 2,048 joined arc pairs, one
+                                 workgroup joins, merges, numbers the new
+                                 pairs (in (q1, q2) order) and appends the
+                                 arcs of it and of the levels after it in
+                                 one launch (composition with reduction only;
+                                 the result is the same composition)        */
 } fstc_opts;
 
 /* Composition result.  All arrays are device memory obtained from the
@@ -210,7 +218,8 @@ typedef struct fstc_stats {
   uint32_t direct_product_levels; /* levels of product-merge sources alone whose
                                      merged arcs the product kernel wrote
                                      straight into the result              */
-  uint32_t reserved1;
+  uint32_t small_levels;      /* levels done by the one-workgroup kernel
+                                 (opts.no_small_levels)                     */
   uint64_t peak_device_bytes; /* largest amount of device memory the call held
                                  from its allocator at one time (result
                                  arrays and temporaries)                    */

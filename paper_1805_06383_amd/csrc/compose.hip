@@ -537,10 +537,85 @@ void Composer::run(fstc_result *out) {
       wtmp(&level_tmp), runsrc(&level_tmp), newbits(&level_tmp);
 
   bool status_clear = true;  // level counters of *dst all zero
+  // small levels (level.hpp, k_small_levels): one workgroup runs them, and
+  // the levels after them, in one launch; a level it declines (too large,
+  // or a capacity it must not exceed) takes the per-level kernels
+  const bool small_ok = !o.no_reduction && !o.no_small_levels;
+  u32 small_skip_depth = ~0u;  // the depth the one-workgroup kernel declined last
+  u32 small_levels = 0;
+  Buf ssb(&A);
+  SmallState *ss_dev = small_ok ? static_cast<SmallState *>(ssb.ensure(sizeof(SmallState)))
+                                : nullptr;
+  static_assert(sizeof(SmallState) <= sizeof(Staging::words), "SmallState fits the staging words");
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
+    if (hi == lo) break;
+    if (small_ok && hi - lo <= kSmallSources && depth != small_skip_depth) {
+      constexpr u64 kSmallGrow = 1u << 16;  // room for this many states and arcs past the current
+      sq1b.grow_keep((n_states + kSmallGrow) * 4, n_states * 4);
+      sq2b.grow_keep((n_states + kSmallGrow) * 4, n_states * 4);
+      out_arcs.grow(arcs + kSmallGrow, arcs);
+      SmallArgs sa{};
+      sa.row1 = c1.row; sa.seg_sym1 = c1.seg_sym; sa.seg_off1 = c1.seg_off;
+      sa.part_base1 = c1.part_base; sa.arcs1 = c1.arcs; sa.parts1 = c1.parts;
+      sa.row2 = c2.row; sa.seg_sym2 = c2.seg_sym; sa.seg_off2 = c2.seg_off;
+      sa.part_base2 = c2.part_base; sa.arcs2 = c2.arcs; sa.parts2 = c2.parts;
+      sa.b2 = b2;
+      sa.key_bits = key_bits;
+      sa.va.vis = hvb.as<u32>();
+      sa.va.vn2 = vn2;
+      sa.va.hkeys = hkb.as<u64>();
+      sa.va.hmask = hcap - 1;
+      sa.va.st = dst;
+      sa.sq1 = sq1b.as<u32>();
+      sa.sq2 = sq2b.as<u32>();
+      sa.state_cap = std::min<u64>(state_limit, std::min(sq1b.cap, sq2b.cap) / 4);
+      if (!dense_vis) sa.state_cap = std::min<u64>(sa.state_cap, hcap / 2);  // load at most 1/2
+      sa.arc_cap = out_arcs.cap;
+      if (o.max_arcs) sa.arc_cap = std::min<u64>(sa.arc_cap, o.max_arcs);
+      sa.out_src = out_arcs.col(0);
+      sa.out_dst = out_arcs.col(1);
+      sa.out_il = out_arcs.col(2);
+      sa.out_ol = out_arcs.col(3);
+      sa.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+      sa.max_levels = o.max_levels;
+      sa.ss = ss_dev;
+      SmallState init{};
+      init.lo = lo;
+      init.hi = hi;
+      init.n_states = n_states;
+      init.arcs = arcs;
+      init.premerge = premerge;
+      init.depth = depth;
+      std::memcpy(hs->words, &init, sizeof init);
+      FSTC_HIP(hipMemcpyAsync(ss_dev, hs->words, sizeof init, hipMemcpyHostToDevice, s));
+      if (!status_clear) {
+        launch_reset_level(dst, s);
+        status_clear = true;
+      }
+      T.at(kCount);
+      launch_small_levels(sa, s);
+      T.at(kNone);
+      FSTC_HIP(hipMemcpyAsync(hs->words, ss_dev, sizeof(SmallState), hipMemcpyDeviceToHost, s));
+      sync_status();
+      SmallState out_st;
+      std::memcpy(&out_st, hs->words, sizeof out_st);
+      lo = (u32)out_st.lo;
+      hi = (u32)out_st.hi;
+      n_states = out_st.n_states;
+      arcs = out_st.arcs;
+      premerge = out_st.premerge;
+      depth = out_st.depth;
+      expanded_levels += out_st.levels;
+      new_levels += out_st.new_levels;
+      small_levels += out_st.levels;
+      max_frontier = std::max<u64>(max_frontier, out_st.max_frontier);
+      max_level_pre = std::max<u64>(max_level_pre, out_st.max_level_pre);
+      if (out_st.reason == kSmallDone) break;
+      if (out_st.reason == kSmallTooLarge || out_st.levels == 0) small_skip_depth = depth;
+      continue;  // larger capacities (a capacity stop after progress) or the per-level path
+    }
     const u32 nsrc = hi - lo;
-    if (nsrc == 0) break;
     level_tmp.reset();
     ++expanded_levels;
     max_frontier = std::max<u64>(max_frontier, nsrc);
@@ -1095,7 +1170,9 @@ void Composer::run(fstc_result *out) {
       pa.out_ol = out_arcs.col(3);
       pa.out_w = reinterpret_cast<float *>(out_arcs.col(4));
       pa.out_base = arcs;
+      T.at(kWriteKernel);  // the level's write pass: every joined pair to the result
       launch_unreduced_product(pa, ptot.as<u64>(), s);
+      ++write_launches;
       T.at(kNone);
       assigned = true;
     } else {
@@ -1224,6 +1301,7 @@ void Composer::run(fstc_result *out) {
     stats->visited_form = vis_moves ? 2u : dense_vis ? 1u : 0u;
     stats->direct_product_levels = direct_levels;
     stats->peak_device_bytes = A.peak_bytes;
+    stats->small_levels = small_levels;
     if (T.all) {
       stats->ms_csr = ms[kCsr];
       stats->ms_count = ms[kCount];

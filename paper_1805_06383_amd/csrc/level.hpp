@@ -234,6 +234,38 @@ struct MergeArgs {
   u32 *utab;
 };
 
+// Small levels in one workgroup (merge.hip, k_small_levels): while a level
+// has at most kSmallSources sources and kSmallRecords joined pairs, one
+// workgroup joins, sorts and merges its records in LDS, inserts the targets,
+// numbers the new pairs in (q1, q2) order and appends the merged arcs, then
+// goes on with the next level; it stops at the first level it cannot take
+// (too large, or a capacity below), at the depth cap, or when the search
+// ends, and leaves the loop state in *ss for the host.
+constexpr u32 kSmallSources = 512;
+constexpr u32 kSmallRecords = 2048;
+enum : u32 { kSmallTooLarge = 1, kSmallCapacity = 2, kSmallDone = 3 };
+struct SmallState {
+  u64 lo, hi, n_states, arcs, premerge;
+  u64 max_frontier, max_level_pre;
+  u32 depth, levels, new_levels, reason;
+};
+struct SmallArgs {
+  const u32 *row1, *seg_sym1, *seg_off1, *part_base1;
+  const uint2 *arcs1, *parts1;
+  const u32 *row2, *seg_sym2, *seg_off2, *part_base2;
+  const uint2 *arcs2, *parts2;
+  int b2, key_bits;
+  MergeArgs va;  // visited set: vis, vn2, hkeys, hmask, st
+  u32 *sq1, *sq2;
+  u64 state_cap;  // at most this many states after a level (arrays, hash load, caps)
+  u64 arc_cap;    // at most this many result arcs after a level
+  u32 *out_src, *out_dst, *out_il, *out_ol;
+  float *out_w;
+  u32 max_levels;
+  SmallState *ss;
+};
+void launch_small_levels(const SmallArgs &a, hipStream_t s);
+
 // Composition without reduction, a level whose sources all took the
 // four-source form and whose targets utab holds as ids: source u's joined
 // pairs as arcs at out_base + off[u] .. (off: exclusive scan of the joined

@@ -1481,6 +1481,237 @@ __global__ __launch_bounds__(256) void k_unreduced_product(MergeArgs a, const u6
 }
 
 // ---------------------------------------------------------------------------
+// Small levels in one workgroup (level.hpp, SmallArgs).  Per level:
+//   1. each source's joined pairs counted by a walk of its two symbol lists
+//      (thread per source), offsets by a workgroup scan;
+//   2. records (source index, part-rank key; float32 product) written to LDS;
+//   3. a bitonic sort of the records by key, then each run summed in float64
+//      by the thread that holds its head, merged arcs compacted in key order;
+//   4. capacities checked (before anything global changes), targets inserted
+//      in the visited set, the new pairs sorted by (q1, q2) and numbered
+//      after the existing states, then every merged arc appended with its
+//      target's id (read back from the visited set after a barrier).
+constexpr int kSmallNT = 1024;
+
+// Bitonic sort of key[0..n) (n a power of two, at most kSmallRecords) with
+// a 32-bit payload, by the whole workgroup; ends with a barrier.
+__device__ __forceinline__ void small_sort(u64 *key, u32 *val, u32 n) {
+  for (u32 k = 2; k <= n; k <<= 1) {
+    for (u32 j = k >> 1; j > 0; j >>= 1) {
+      for (u32 i = threadIdx.x; i < n; i += kSmallNT) {
+        const u32 ixj = i ^ j;
+        if (ixj > i) {
+          const bool up = (i & k) == 0;
+          const u64 x = key[i], y = key[ixj];
+          if ((x > y) == up) {
+            key[i] = y;
+            key[ixj] = x;
+            const u32 t = val[i];
+            val[i] = val[ixj];
+            val[ixj] = t;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Calls f(s1, s2) for every pair of segments with one symbol: s1 in
+// [b1, e1), s2 in [b2, e2), in increasing symbol order (the shorter list
+// walked, the longer one binary-searched from a moving lower bound).
+template <class F>
+__device__ __forceinline__ void small_join(const u32 *sym1, u32 b1, u32 e1, const u32 *sym2,
+                                           u32 b2, u32 e2, F &&f) {
+  const bool one = e1 - b1 <= e2 - b2;
+  const u32 *ss = one ? sym1 : sym2, *ls = one ? sym2 : sym1;
+  const u32 sb = one ? b1 : b2, se = one ? e1 : e2, le = one ? e2 : e1;
+  u32 lo = one ? b2 : b1;
+  for (u32 i = sb; i < se && lo < le; ++i) {
+    const u32 sym = ss[i];
+    u32 l = lo, h = le;
+    while (l < h) {
+      const u32 m = (l + h) >> 1;
+      if (ls[m] < sym) l = m + 1; else h = m;
+    }
+    if (l < le && ls[l] == sym) {
+      if (one) f(i, l); else f(l, i);
+      lo = l + 1;
+    } else {
+      lo = l;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
+  __shared__ u64 s_key[kSmallRecords];
+  __shared__ u32 s_val[kSmallRecords];  // record weights (bits), then claimed slots
+  __shared__ u64 m_key[kSmallRecords];
+  __shared__ float m_w[kSmallRecords];
+  __shared__ u32 m_x[kSmallRecords];    // target slot, kNewFlag when this insert claimed it
+  __shared__ u64 s_scr[kSmallNT / kWave];
+  const u32 t = threadIdx.x;
+  SmallState st = *a.ss;
+  st.levels = st.new_levels = 0;
+  st.reason = 0;
+  const u64 kmask = (1ull << a.key_bits) - 1, m2 = (1ull << a.b2) - 1;
+  while (true) {
+    const u64 nsrc = st.hi - st.lo;
+    if (nsrc == 0 || (a.max_levels && st.depth >= a.max_levels)) {
+      st.reason = kSmallDone;
+      break;
+    }
+    if (nsrc > kSmallSources) {
+      st.reason = kSmallTooLarge;
+      break;
+    }
+    // 1. joined pairs per source
+    u32 q1 = 0, q2 = 0, b1 = 0, e1 = 0, b2 = 0, e2 = 0;
+    u64 cnt = 0;
+    if (t < nsrc) {
+      q1 = a.sq1[st.lo + t];
+      q2 = a.sq2[st.lo + t];
+      b1 = a.row1[q1], e1 = a.row1[q1 + 1], b2 = a.row2[q2], e2 = a.row2[q2 + 1];
+      small_join(a.seg_sym1, b1, e1, a.seg_sym2, b2, e2, [&](u32 s1, u32 s2) {
+        cnt += (u64)(a.seg_off1[s1 + 1] - a.seg_off1[s1]) * (a.seg_off2[s2 + 1] - a.seg_off2[s2]);
+      });
+    }
+    u64 R;
+    const u64 off = block_exclusive_sum<kSmallNT, u64>(cnt, s_scr, &R);
+    if (R > kSmallRecords) {  // uniform: every thread has R
+      st.reason = kSmallTooLarge;
+      break;
+    }
+    if (R == 0) {  // no arc leaves this level: no new states either
+      st.reason = kSmallDone;
+      break;
+    }
+    // 2. records: key = source index, then the part-rank key
+    if (t < nsrc) {
+      u32 k = (u32)off;
+      small_join(a.seg_sym1, b1, e1, a.seg_sym2, b2, e2, [&](u32 s1, u32 s2) {
+        for (u32 i = a.seg_off1[s1]; i < a.seg_off1[s1 + 1]; ++i) {
+          const uint2 x1 = a.arcs1[i];
+          for (u32 j = a.seg_off2[s2]; j < a.seg_off2[s2 + 1]; ++j) {
+            const uint2 x2 = a.arcs2[j];
+            s_key[k] = ((u64)t << a.key_bits) | ((u64)x1.x << a.b2) | (u64)x2.x;
+            s_val[k] = __float_as_uint(__uint_as_float(x1.y) * __uint_as_float(x2.y));
+            ++k;
+          }
+        }
+      });
+    }
+    u32 n = 1;
+    while (n < R) n <<= 1;
+    for (u32 i = (u32)R + t; i < n; i += kSmallNT) s_key[i] = ~0ull;
+    __syncthreads();
+    // 3. sort, then runs: thread t takes records 2t, 2t + 1
+    small_sort(s_key, s_val, n);
+    u32 heads = 0;
+#pragma unroll
+    for (u32 h = 0; h < 2; ++h) {
+      const u32 i = 2 * t + h;
+      heads += (i < R && (i == 0 || s_key[i] != s_key[i - 1])) ? 1u : 0u;
+    }
+    u64 M;
+    u32 pos = (u32)block_exclusive_sum<kSmallNT, u64>(heads, s_scr, &M);
+#pragma unroll
+    for (u32 h = 0; h < 2; ++h) {
+      const u32 i = 2 * t + h;
+      if (i < R && (i == 0 || s_key[i] != s_key[i - 1])) {
+        double sum = 0.0;
+        for (u32 j = i; j < R && s_key[j] == s_key[i]; ++j) sum += (double)__uint_as_float(s_val[j]);
+        m_key[pos] = s_key[i];
+        m_w[pos] = (float)sum;
+        ++pos;
+      }
+    }
+    // 4. capacities first (the level is redone from the start by the host
+    // or by a later call when one does not suffice)
+    if (st.n_states + M > a.state_cap || st.arcs + M > a.arc_cap) {
+      st.reason = kSmallCapacity;
+      break;
+    }
+    __syncthreads();
+    for (u32 i = t; i < M; i += kSmallNT) {
+      const u64 key = m_key[i];
+      const u32 u = (u32)(key >> a.key_bits);
+      const u64 r = key & kmask;
+      const u32 p1 = a.part_base1[a.sq1[st.lo + u]] + (u32)(r >> a.b2);
+      const u32 p2 = a.part_base2[a.sq2[st.lo + u]] + (u32)(r & m2);
+      const u64 hk[1] = {((u64)a.parts1[p1].x << 32) | (u64)a.parts2[p2].x};
+      const bool act[1] = {true};
+      u32 slot[1], known[1];
+      bool is_new[1];
+      visit_batch<1>(a.va, hk, act, slot, is_new, known);
+      m_x[i] = slot[0] | (is_new[0] ? kNewFlag : 0u);
+    }
+    __syncthreads();
+    // the new pairs in (q1, q2) order: claimed entries (thread t: 2t, 2t+1)
+    u32 claims = 0;
+#pragma unroll
+    for (u32 h = 0; h < 2; ++h) {
+      const u32 i = 2 * t + h;
+      claims += (i < M && (m_x[i] & kNewFlag)) ? 1u : 0u;
+    }
+    u64 nnew;
+    u32 cpos = (u32)block_exclusive_sum<kSmallNT, u64>(claims, s_scr, &nnew);
+#pragma unroll
+    for (u32 h = 0; h < 2; ++h) {
+      const u32 i = 2 * t + h;
+      if (i < M && (m_x[i] & kNewFlag)) {
+        const u64 key = m_key[i];
+        const u32 u = (u32)(key >> a.key_bits);
+        const u64 r = key & kmask;
+        const u32 p1 = a.part_base1[a.sq1[st.lo + u]] + (u32)(r >> a.b2);
+        const u32 p2 = a.part_base2[a.sq2[st.lo + u]] + (u32)(r & m2);
+        s_key[cpos] = ((u64)a.parts1[p1].x << 32) | (u64)a.parts2[p2].x;
+        s_val[cpos] = m_x[i] & ~kNewFlag;
+        ++cpos;
+      }
+    }
+    u32 nc = 1;
+    while (nc < nnew) nc <<= 1;
+    for (u32 i = (u32)nnew + t; i < nc; i += kSmallNT) s_key[i] = ~0ull;
+    __syncthreads();
+    small_sort(s_key, s_val, nc);
+    for (u32 i = t; i < nnew; i += kSmallNT) {
+      const u32 id = (u32)(st.n_states + i);
+      a.va.vis[s_val[i]] = id;
+      a.sq1[id] = (u32)(s_key[i] >> 32);
+      a.sq2[id] = (u32)s_key[i];
+    }
+    __syncthreads();
+    // merged arcs with their targets' ids
+    for (u32 i = t; i < M; i += kSmallNT) {
+      const u64 key = m_key[i];
+      const u32 u = (u32)(key >> a.key_bits);
+      const u64 r = key & kmask;
+      const u32 p1 = a.part_base1[a.sq1[st.lo + u]] + (u32)(r >> a.b2);
+      const u32 p2 = a.part_base2[a.sq2[st.lo + u]] + (u32)(r & m2);
+      const u64 o = st.arcs + i;
+      a.out_src[o] = (u32)(st.lo + u);
+      a.out_dst[o] = a.va.vis[m_x[i] & ~kNewFlag];
+      a.out_il[o] = a.parts1[p1].y;
+      a.out_ol[o] = a.parts2[p2].y;
+      a.out_w[o] = m_w[i];
+    }
+    st.max_frontier = max<u64>(st.max_frontier, nsrc);
+    st.max_level_pre = max<u64>(st.max_level_pre, R);
+    st.premerge += R;
+    st.arcs += M;
+    st.lo = st.hi;
+    st.n_states += nnew;
+    st.hi = st.n_states;
+    ++st.depth;
+    ++st.levels;
+    if (nnew) ++st.new_levels;
+    __syncthreads();  // LDS reused by the next level
+  }
+  if (t == 0) *a.ss = st;
+}
+
+// ---------------------------------------------------------------------------
 // Fused expand + merge (the records of a tile never leave the chip).  The
 // matches of the tile's sources (moff[s0] .. moff[s1]) are staged in chunks
 // of kFuseChunk in LDS -- first element in the tile, first M1 and M2 arc, n2,
@@ -2420,6 +2651,10 @@ void launch_assign_direct(const MergeArgs &a, const u64 *newoff, u32 base, u32 *
   if (!a.nsrc) return;
   hipLaunchKernelGGL(k_assign_direct, dim3((unsigned)ceil_div((u64)a.nsrc * 4, 256)), dim3(256), 0,
                      s, a, newoff, base, sq1, sq2);
+}
+
+void launch_small_levels(const SmallArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(k_small_levels, dim3(1), dim3(kSmallNT), 0, s, a);
 }
 
 void launch_unreduced_product(const MergeArgs &a, const u64 *off, hipStream_t s) {

@@ -54,7 +54,8 @@ class FstcOpts(ctypes.Structure):
     _fields_ = [("max_levels", _u32), ("deterministic_ids", _u32), ("max_states", _u64),
                 ("max_arcs", _u64), ("alloc", ALLOC_FN), ("free", FREE_FN), ("alloc_ctx", _vp),
                 ("no_reduction", _u32), ("fused_merge", _u32), ("no_product_merge", _u32),
-                ("hash_visited", _u32), ("phase_timing", _u32), ("hash_min_log2", _u32)]
+                ("hash_visited", _u32), ("phase_timing", _u32), ("hash_min_log2", _u32),
+                ("no_small_levels", _u32)]
 
 
 class FstcResult(ctypes.Structure):
@@ -81,7 +82,7 @@ class FstcStats(ctypes.Structure):
                 ("total_product_sources", _u64), ("ms_product_kernel", ctypes.c_double),
                 ("product_launches", _u32), ("visited_form", _u32),
                 ("total_product_mfma_sources", _u64), ("direct_product_levels", _u32),
-                ("reserved1", _u32), ("peak_device_bytes", _u64)]
+                ("small_levels", _u32), ("peak_device_bytes", _u64)]
 
 
 EXPORTS = ("fstc_compose", "fstc_compose_eps", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",
@@ -186,11 +187,12 @@ class TorchAllocator:
 
     def opts(self, max_levels=0, deterministic_ids=False, max_states=0, max_arcs=0,
              reduce=True, fused=False, product=True, hash_visited=False,
-             phase_timing=False, hash_min_log2=0) -> FstcOpts:
+             phase_timing=False, hash_min_log2=0, small_levels=True) -> FstcOpts:
         return FstcOpts(int(max_levels), 1 if deterministic_ids else 0, int(max_states),
                         int(max_arcs), self._alloc, self._free, None, 0 if reduce else 1,
                         1 if fused else 0, 0 if product else 1, 1 if hash_visited else 0,
-                        1 if phase_timing else 0, int(hash_min_log2))
+                        1 if phase_timing else 0, int(hash_min_log2),
+                        0 if small_levels else 1)
 
 
 # ---------------------------------------------------------------------------
@@ -295,7 +297,7 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
                  stream=None, want_stats: bool = True, reduce: bool = True,
                  fused: bool = False, product: bool = True,
                  hash_visited: bool = False, phase_timing: bool = False,
-                 hash_min_log2: int = 0) -> Composed:
+                 hash_min_log2: int = 0, small_levels: bool = True) -> Composed:
     """Reachable composition m1 o m2 on the GPU (see fstc_compose in fstc.h).
     reduce=False keeps every joined arc pair as its own arc (opts.no_reduction);
     fused=True merges tiles without writing their composed arcs first
@@ -304,12 +306,14 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
     in the hash table even for small pair spaces (opts.hash_visited);
     phase_timing=True fills the per-phase times of the stats
     (opts.phase_timing; the kernel times are always there); hash_min_log2 > 0
-    gives the hash table at least 2^hash_min_log2 slots (opts.hash_min_log2)."""
+    gives the hash table at least 2^hash_min_log2 slots (opts.hash_min_log2);
+    small_levels=False sends every level through the per-level kernels
+    (opts.no_small_levels)."""
     lib = load_library()
     device = m1.src.device if m1.num_arcs else m1.final.device
     alloc = TorchAllocator(device)
     opts = alloc.opts(max_levels, deterministic_ids, max_states, max_arcs, reduce, fused, product,
-                      hash_visited, phase_timing, hash_min_log2)
+                      hash_visited, phase_timing, hash_min_log2, small_levels)
     s1, s2 = m1.struct(), m2.struct()
     res = FstcResult()
     st = FstcStats()

@@ -84,8 +84,8 @@ def test_phase_timing(env):
     F, lib, hip = env
     m1, m2 = W.config4(0)
     d1, d2 = F.DeviceFST.from_host(m1, "cuda"), F.DeviceFST.from_host(m2, "cuda")
-    a = F.fstc_compose(d1, d2, max_levels=3)
-    b = F.fstc_compose(d1, d2, max_levels=3, phase_timing=True)
+    a = F.fstc_compose(d1, d2, max_levels=3, small_levels=False)
+    b = F.fstc_compose(d1, d2, max_levels=3, phase_timing=True, small_levels=False)
     phases = ("ms_csr", "ms_count", "ms_expand", "ms_merge", "ms_assign")
     assert all(a.stats[k] == 0 for k in phases)
     assert all(b.stats[k] > 0 for k in ("ms_csr", "ms_count", "ms_merge", "ms_assign"))

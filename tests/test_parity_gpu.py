@@ -108,11 +108,14 @@ def test_figure2_csr(fstc):
                 assert segoff[k] - segoff[s0] == off and segoff[k + 1] - segoff[k] == n
 
 
+# small inputs run through the one-workgroup small-level kernel by default;
+# small=False keeps them on the per-level kernels, which larger levels take
+@pytest.mark.parametrize("small", [True, False])
 @pytest.mark.parametrize("seed", range(150))
-def test_tiny_random(fstc, seed):
+def test_tiny_random(fstc, seed, small):
     from test_oracle_pins import tiny_pair
     m1, m2 = tiny_pair(seed)
-    g = run_gpu(fstc, m1, m2)
+    g = run_gpu(fstc, m1, m2, small_levels=small)
     check_structure(g, m1, m2)
     ref = oracle.compose(m1, m2)
     compare(g, ref, f"tiny seed {seed}")
@@ -121,19 +124,21 @@ def test_tiny_random(fstc, seed):
     assert_same(canon_of(ref), canon_of(brute_force(m1, m2)), rtol=1e-6)
 
 
+@pytest.mark.parametrize("small", [True, False])
 @pytest.mark.parametrize("seed", range(200))
-def test_config1_seeds(fstc, seed):
+def test_config1_seeds(fstc, seed, small):
     m1, m2 = W.config1(seed)
-    g = run_gpu(fstc, m1, m2)
+    g = run_gpu(fstc, m1, m2, small_levels=small)
     check_structure(g, m1, m2)
     compare(g, oracle.compose(m1, m2), f"config1 seed {seed}")
 
 
+@pytest.mark.parametrize("small", [True, False])
 @pytest.mark.parametrize("seed", range(0, 200, 20))
 @pytest.mark.parametrize("cap", [1, 2, 3, 5, 8])
-def test_level_cap(fstc, seed, cap):
+def test_level_cap(fstc, seed, cap, small):
     m1, m2 = W.config1(seed)
-    g = run_gpu(fstc, m1, m2, max_levels=cap)
+    g = run_gpu(fstc, m1, m2, max_levels=cap, small_levels=small)
     ref = oracle.compose(m1, m2, max_levels=cap)
     compare(g, ref, f"config1 seed {seed} cap {cap}")
     ids_follow_depth(g, ref)
@@ -442,7 +447,10 @@ def test_config4_full(fstc, product):
     (m1, m2), ref, rc = config4_full_oracle()
     r = fstc.compose(m1, m2, product=product)
     if product:
-        assert r.stats["total_product_sources"] == ref.num_states
+        # every expanded state is a product source, but those of the levels
+        # the one-workgroup kernel ran (config 4's first, a single pair)
+        assert r.stats["total_product_sources"] == \
+            ref.num_states - int(np.sum(ref.depth < r.stats["small_levels"]))
     else:
         assert r.stats["total_product_sources"] == 0 and r.stats["write_launches"] > 0
     g = r.to_host()

@@ -43,7 +43,10 @@ FIELDS = ("q1", "q2", "final", "src", "dst", "a", "c")
 
 def product_vs_records(F, m1, m2, what, rtol=1e-6, **kw):
     """Deterministic ids: identical states, arcs and order with and without
-    the product merge; weights within rtol of each other."""
+    the product merge; weights within rtol of each other (every level on the
+    per-level kernels: the one-workgroup small-level kernel takes neither
+    path)."""
+    kw.setdefault("small_levels", False)
     pr = F.compose(m1, m2, product=True, deterministic_ids=True, **kw)
     rc = F.compose(m1, m2, product=False, deterministic_ids=True, **kw)
     x, y = pr.to_host(), rc.to_host()
@@ -137,7 +140,7 @@ def test_product_infinite_weights(fstc):
     w = m1.weight.copy()
     w[::997] = np.inf
     m1 = with_weights(m1, w)
-    g = fstc.compose(m1, m2, max_levels=3)
+    g = fstc.compose(m1, m2, max_levels=3, small_levels=False)
     assert g.stats["total_product_records"] > 0
     gc = canon_of(g.to_host())
     ref = canon_of(oracle.compose(m1, m2, max_levels=3))
@@ -153,7 +156,7 @@ def test_product_matrix_product(fstc):
     rng = np.random.default_rng(12)
     A = W.random_weights(rng, 4 * 40).reshape(4, 40)
     B = W.random_weights(rng, 40 * 12).reshape(40, 12)
-    g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B))
+    g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B), small_levels=False)
     assert g.stats["total_product_sources"] == 1
     assert g.stats["total_product_mfma_sources"] == 0  # 12 parts: the vector form
     g = g.to_host()
@@ -190,7 +193,7 @@ def test_product_single_entry(fstc, with_inf):
     B = W.random_weights(rng, 64).reshape(64, 1)
     if with_inf:
         A[0, 17] = np.inf
-    g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B))
+    g = fstc.compose(W.one_state_dense(A), W.one_state_dense(B), small_levels=False)
     assert g.stats["total_product_sources"] == 1
     # an infinite weight keeps the source off the matrix cores
     assert g.stats["total_product_mfma_sources"] == (0 if with_inf else 1)
@@ -222,7 +225,7 @@ def test_product_out_of_range_products(fstc, case):
         m1, m2 = scaled_states(m1, 3, 90), scaled_states(m2, 5, 45)
     else:
         m1, m2 = scaled_states(m1, 3, -100), scaled_states(m2, 5, -40)
-    g = fstc.compose(m1, m2, max_levels=3)
+    g = fstc.compose(m1, m2, max_levels=3, small_levels=False)
     st = g.stats
     assert 0 < st["total_product_mfma_sources"] < st["total_product_sources"]
     gc = canon_of(g.to_host())
@@ -291,7 +294,7 @@ def test_product_entries_without_terms(fstc, flip):
     assert st["total_product_records"] == pr.num_premerge_arcs
     g = pr.to_host()
     # the levels of product sources alone were written straight to the result
-    assert fstc.compose(m1, m2, max_levels=4).stats["direct_product_levels"] >= 3
+    assert fstc.compose(m1, m2, max_levels=4, small_levels=False).stats["direct_product_levels"] >= 3
     # fewer merged arcs than table entries: 8 of the 16 entries have terms
     assert g.num_arcs < 16 * len(np.unique(g.src))
     assert_same(canon_of(g), canon_of(oracle.compose(m1, m2, max_levels=4)), rtol=RTOL,
