@@ -145,7 +145,7 @@ typedef struct fstc_opts {
                                  above 31 give FSTC_ERR_INVALID_ARG       */
   uint32_t no_small_levels;   /* nonzero: every level takes the per-level
                                  kernels.  0: while a level has at most 512
-                                 pairs and 2,048 joined arc pairs, one
+                                 pairs and 1,024 joined arc pairs, one
                                  workgroup joins, merges, numbers the new
                                  pairs (in (q1, q2) order) and appends the
                                  arcs of it and of the levels after it in

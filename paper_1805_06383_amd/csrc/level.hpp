@@ -242,7 +242,7 @@ struct MergeArgs {
 // (too large, or a capacity below), at the depth cap, or when the search
 // ends, and leaves the loop state in *ss for the host.
 constexpr u32 kSmallSources = 512;
-constexpr u32 kSmallRecords = 2048;
+constexpr u32 kSmallRecords = 1024;
 enum : u32 { kSmallTooLarge = 1, kSmallCapacity = 2, kSmallDone = 3 };
 struct SmallState {
   u64 lo, hi, n_states, arcs, premerge;

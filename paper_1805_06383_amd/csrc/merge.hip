@@ -1494,8 +1494,35 @@ __global__ __launch_bounds__(256) void k_unreduced_product(MergeArgs a, const u6
 constexpr int kSmallNT = 1024;
 
 // Bitonic sort of key[0..n) (n a power of two, at most kSmallRecords) with
-// a 32-bit payload, by the whole workgroup; ends with a barrier.
+// a 32-bit payload, by the whole workgroup; ends with a barrier.  Up to 64
+// elements the first wave sorts them in registers (shuffles, no barrier).
 __device__ __forceinline__ void small_sort(u64 *key, u32 *val, u32 n) {
+  if (n <= (u32)kWave) {
+    if (threadIdx.x < (u32)kWave) {
+      const u32 l = threadIdx.x;
+      u64 x = l < n ? key[l] : ~0ull;
+      u32 v = l < n ? val[l] : 0u;
+      for (u32 k = 2; k <= n; k <<= 1) {
+        for (u32 j = k >> 1; j > 0; j >>= 1) {
+          const u64 y = __shfl_xor(x, (int)j, kWave);
+          const u32 w = __shfl_xor(v, (int)j, kWave);
+          // the lower lane of a pair keeps the smaller key when sorting up
+          const bool up = (l & k) == 0, lower = (l & j) == 0;
+          const bool take = lower == up ? y < x : y > x;
+          if (take) {
+            x = y;
+            v = w;
+          }
+        }
+      }
+      if (l < n) {
+        key[l] = x;
+        val[l] = v;
+      }
+    }
+    __syncthreads();
+    return;
+  }
   for (u32 k = 2; k <= n; k <<= 1) {
     for (u32 j = k >> 1; j > 0; j >>= 1) {
       for (u32 i = threadIdx.x; i < n; i += kSmallNT) {
@@ -1516,6 +1543,11 @@ __device__ __forceinline__ void small_sort(u64 *key, u32 *val, u32 n) {
     }
   }
 }
+
+// Joins the one-workgroup kernel takes: the shorter list at most this many
+// symbols, the longer at most kSmallLongList (a longer join is the per-level
+// kernels' work, done by many lanes).
+constexpr u32 kSmallShortList = 64, kSmallLongList = 4096;
 
 // Calls f(s1, s2) for every pair of segments with one symbol: s1 in
 // [b1, e1), s2 in [b2, e2), in increasing symbol order (the shorter list
@@ -1549,6 +1581,9 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
   __shared__ u64 m_key[kSmallRecords];
   __shared__ float m_w[kSmallRecords];
   __shared__ u32 m_x[kSmallRecords];    // target slot, kNewFlag when this insert claimed it
+  __shared__ u32 m_il[kSmallRecords], m_ol[kSmallRecords];  // merged arcs' labels
+  __shared__ u32 m_src[kSmallRecords];                      // and source indexes
+  __shared__ u32 s_pb1[kSmallSources], s_pb2[kSmallSources];  // sources' first parts
   __shared__ u64 s_scr[kSmallNT / kWave];
   const u32 t = threadIdx.x;
   SmallState st = *a.ss;
@@ -1568,10 +1603,20 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
     // 1. joined pairs per source
     u32 q1 = 0, q2 = 0, b1 = 0, e1 = 0, b2 = 0, e2 = 0;
     u64 cnt = 0;
+    bool long_join = false;
     if (t < nsrc) {
       q1 = a.sq1[st.lo + t];
       q2 = a.sq2[st.lo + t];
       b1 = a.row1[q1], e1 = a.row1[q1 + 1], b2 = a.row2[q2], e2 = a.row2[q2 + 1];
+      s_pb1[t] = a.part_base1[q1];
+      s_pb2[t] = a.part_base2[q2];
+      long_join = min(e1 - b1, e2 - b2) > kSmallShortList || max(e1 - b1, e2 - b2) > kSmallLongList;
+    }
+    if (__syncthreads_or(long_join)) {
+      st.reason = kSmallTooLarge;
+      break;
+    }
+    if (t < nsrc) {
       small_join(a.seg_sym1, b1, e1, a.seg_sym2, b2, e2, [&](u32 s1, u32 s2) {
         cnt += (u64)(a.seg_off1[s1 + 1] - a.seg_off1[s1]) * (a.seg_off2[s2 + 1] - a.seg_off2[s2]);
       });
@@ -1637,14 +1682,18 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
       const u64 key = m_key[i];
       const u32 u = (u32)(key >> a.key_bits);
       const u64 r = key & kmask;
-      const u32 p1 = a.part_base1[a.sq1[st.lo + u]] + (u32)(r >> a.b2);
-      const u32 p2 = a.part_base2[a.sq2[st.lo + u]] + (u32)(r & m2);
-      const u64 hk[1] = {((u64)a.parts1[p1].x << 32) | (u64)a.parts2[p2].x};
+      const uint2 P1 = a.parts1[s_pb1[u] + (u32)(r >> a.b2)];
+      const uint2 P2 = a.parts2[s_pb2[u] + (u32)(r & m2)];
+      m_il[i] = P1.y;
+      m_ol[i] = P2.y;
+      m_src[i] = u;
+      const u64 hk[1] = {((u64)P1.x << 32) | (u64)P2.x};
       const bool act[1] = {true};
       u32 slot[1], known[1];
       bool is_new[1];
       visit_batch<1>(a.va, hk, act, slot, is_new, known);
       m_x[i] = slot[0] | (is_new[0] ? kNewFlag : 0u);
+      m_key[i] = hk[0];  // from here on: the target pair
     }
     __syncthreads();
     // the new pairs in (q1, q2) order: claimed entries (thread t: 2t, 2t+1)
@@ -1660,12 +1709,7 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
     for (u32 h = 0; h < 2; ++h) {
       const u32 i = 2 * t + h;
       if (i < M && (m_x[i] & kNewFlag)) {
-        const u64 key = m_key[i];
-        const u32 u = (u32)(key >> a.key_bits);
-        const u64 r = key & kmask;
-        const u32 p1 = a.part_base1[a.sq1[st.lo + u]] + (u32)(r >> a.b2);
-        const u32 p2 = a.part_base2[a.sq2[st.lo + u]] + (u32)(r & m2);
-        s_key[cpos] = ((u64)a.parts1[p1].x << 32) | (u64)a.parts2[p2].x;
+        s_key[cpos] = m_key[i];  // the target pair (r1, r2)
         s_val[cpos] = m_x[i] & ~kNewFlag;
         ++cpos;
       }
@@ -1684,16 +1728,11 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
     __syncthreads();
     // merged arcs with their targets' ids
     for (u32 i = t; i < M; i += kSmallNT) {
-      const u64 key = m_key[i];
-      const u32 u = (u32)(key >> a.key_bits);
-      const u64 r = key & kmask;
-      const u32 p1 = a.part_base1[a.sq1[st.lo + u]] + (u32)(r >> a.b2);
-      const u32 p2 = a.part_base2[a.sq2[st.lo + u]] + (u32)(r & m2);
       const u64 o = st.arcs + i;
-      a.out_src[o] = (u32)(st.lo + u);
+      a.out_src[o] = (u32)st.lo + m_src[i];
       a.out_dst[o] = a.va.vis[m_x[i] & ~kNewFlag];
-      a.out_il[o] = a.parts1[p1].y;
-      a.out_ol[o] = a.parts2[p2].y;
+      a.out_il[o] = m_il[i];
+      a.out_ol[o] = m_ol[i];
       a.out_w[o] = m_w[i];
     }
     st.max_frontier = max<u64>(st.max_frontier, nsrc);
