@@ -1555,7 +1555,25 @@ constexpr u32 kSmallShortList = 64, kSmallLongList = 4096;
 template <class F>
 __device__ __forceinline__ void small_join(const u32 *sym1, u32 b1, u32 e1, const u32 *sym2,
                                            u32 b2, u32 e2, F &&f) {
-  const bool one = e1 - b1 <= e2 - b2;
+  const u32 n1 = e1 - b1, n2 = e2 - b2;
+  if (n1 <= 4 * n2 && n2 <= 4 * n1) {
+    // lists of similar lengths: a linear merge (consecutive loads, no search)
+    u32 i = b1, j = b2;
+    while (i < e1 && j < e2) {
+      const u32 x = sym1[i], y = sym2[j];
+      if (x == y) {
+        f(i, j);
+        ++i;
+        ++j;
+      } else if (x < y) {
+        ++i;
+      } else {
+        ++j;
+      }
+    }
+    return;
+  }
+  const bool one = n1 <= n2;
   const u32 *ss = one ? sym1 : sym2, *ls = one ? sym2 : sym1;
   const u32 sb = one ? b1 : b2, se = one ? e1 : e2, le = one ? e2 : e1;
   u32 lo = one ? b2 : b1;
