@@ -140,7 +140,7 @@ def product_flops(st: dict) -> float:
     return 2.0 * st["total_product_records"]
 
 
-def algorithmic_bytes(st: dict, R: int) -> dict:
+def algorithmic_bytes(st: dict, R: int, unreduced: bool = False) -> dict:
     """Bytes each of the three tile kernels must move, per compose call.
 
     write (k_expand): every unmerged record written once (key + float32
@@ -154,8 +154,11 @@ def algorithmic_bytes(st: dict, R: int) -> dict:
     R = R - st["total_product_records"]  # joined pairs written as records
     tile_records = R - st["total_big_records"]
     dense = st["total_dense_records"]
+    # without reduction, product-form levels write their joined pairs as
+    # result arcs (five 4-byte columns) in the write pass instead of records
+    direct_out = st["total_product_records"] * 20 if unreduced else 0
     return {
-        "write": R * rec + st["total_matches"] * 24,
+        "write": R * rec + st["total_matches"] * 24 + direct_out,
         "merge": dense * rec + st["total_dense_runs"] * 16,
         "sort": (tile_records - dense) * rec + st["total_sort_runs"] * 16,
     }
@@ -261,9 +264,10 @@ def main():
     def kernels_and_roofline(last, sums, traffic_key):
         R = last.num_premerge_arcs
         st = last.stats
-        ab = algorithmic_bytes(st, R)
+        ab = algorithmic_bytes(st, R, args.no_reduction)
         kern = {}
-        for name, kernel, ms_key, n_key in (("write", "k_expand", "ms_write_kernel", "write_launches"),
+        write_kernel = "k_expand" + (" / k_unreduced_product" if args.no_reduction else "")
+        for name, kernel, ms_key, n_key in (("write", write_kernel, "ms_write_kernel", "write_launches"),
                                             ("merge", "k_merge_dense", "ms_merge_kernel", "merge_launches"),
                                             ("sort", "k_merge_listed" if st["merge_launches"]
                                              else "k_merge_tiles", "ms_sort_kernel", "sort_launches")):

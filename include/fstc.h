@@ -145,8 +145,10 @@ typedef struct fstc_opts {
                                  above 31 give FSTC_ERR_INVALID_ARG       */
   uint32_t no_small_levels;   /* nonzero: every level takes the per-level
                                  kernels.  0: while a level has at most 512
-                                 pairs and 1,024 joined arc pairs, one
-                                 workgroup joins, merges, numbers the new
+                                 pairs and 1,024 joined arc pairs (at most
+                                 64 per pair, symbol lists of at most 32
+                                 and 4,096), one workgroup joins, merges,
+                                 numbers the new
                                  pairs (in (q1, q2) order) and appends the
                                  arcs of it and of the levels after it in
                                  one launch (composition with reduction only;

@@ -1545,9 +1545,10 @@ __device__ __forceinline__ void small_sort(u64 *key, u32 *val, u32 n) {
 }
 
 // Joins the one-workgroup kernel takes: the shorter list at most this many
-// symbols, the longer at most kSmallLongList (a longer join is the per-level
-// kernels' work, done by many lanes).
-constexpr u32 kSmallShortList = 64, kSmallLongList = 4096;
+// symbols, the longer at most kSmallLongList, at most kSmallPerSource joined
+// pairs per source (one thread joins and emits a source: longer joins and
+// larger sources are the per-level kernels' work, done by many lanes).
+constexpr u32 kSmallShortList = 32, kSmallLongList = 4096, kSmallPerSource = 64;
 
 // Calls f(s1, s2) for every pair of segments with one symbol: s1 in
 // [b1, e1), s2 in [b2, e2), in increasing symbol order (the shorter list
@@ -1638,6 +1639,10 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
       small_join(a.seg_sym1, b1, e1, a.seg_sym2, b2, e2, [&](u32 s1, u32 s2) {
         cnt += (u64)(a.seg_off1[s1 + 1] - a.seg_off1[s1]) * (a.seg_off2[s2 + 1] - a.seg_off2[s2]);
       });
+    }
+    if (__syncthreads_or(cnt > kSmallPerSource)) {
+      st.reason = kSmallTooLarge;
+      break;
     }
     u64 R;
     const u64 off = block_exclusive_sum<kSmallNT, u64>(cnt, s_scr, &R);
