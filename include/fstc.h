@@ -346,7 +346,7 @@ int fstc_exclusive_scan_u64(const uint64_t *in, uint64_t *out, uint64_t n, hipSt
  * tight serving loops, harnesses that forbid allocation).  It allocates
  * nothing: the scan's temporaries (tile counter, error word, look-back state
  * of every 2048-element tile) live in a file-scope device array of the
- * library, about 16.8 MB, that each GPU it runs on holds until the process
+ * library, about 17.8 MB, that each GPU it runs on holds until the process
  * ends.  The first call on a device looks the array up and clears it
  * (synchronising `stream`).  n is at most 2^28 (larger n: FSTC_ERR_RANGE,
  * nothing launched).  Every call on one GPU shares that GPU's array: calls

@@ -23,10 +23,11 @@ namespace {
 
 // Largest input of the no-allocation scan, and the scratch it needs: the
 // counter and error words, then the look-back state of ceil(n / 2048) tiles
-// (128 bytes a tile plus 256 bytes of slack, scan_lb_state_bytes).
+// (136 bytes a tile, status words rounded up to 256-byte lines, plus 256
+// bytes of slack: scan_lb_state_bytes).
 constexpr u64 kNoAllocMaxN = 1ull << 28;
 constexpr size_t kScratchWords = 256;  // counter, error word; the state starts 256 bytes in
-constexpr size_t kScratchStateBytes = ((kNoAllocMaxN + 2047) / 2048) * 128 + 256;
+constexpr size_t kScratchStateBytes = ((kNoAllocMaxN + 2047) / 2048) * 136 + 256 + 256;
 constexpr size_t kScratchBytes = kScratchWords + kScratchStateBytes;
 
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];

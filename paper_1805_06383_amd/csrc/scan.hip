@@ -78,27 +78,33 @@ __global__ __launch_bounds__(kScanNT) void k_tile_scan(const TI *in, TO *out, u6
 // Parallel Prefix Scan with Decoupled Look-back", 2016).  A workgroup takes
 // the next tile number from a counter, so every lower tile belongs to a
 // workgroup already running; it publishes its tile total ("aggregate"),
-// then wave 0 reads the states of the 64 tiles below it at once and adds
-// aggregates down to the nearest tile that has published its inclusive
-// prefix, publishes its own inclusive prefix, and the workgroup writes its
-// tile offset by that.
+// then wave 0 reads the status words of the 64 tiles below it at once and
+// adds aggregates down to the nearest tile that has published its
+// inclusive prefix, publishes its own inclusive prefix, and the workgroup
+// writes its tile offset by that.
 //
 // Published values need no memory fences: every 64-bit state word carries
-// the call's epoch in its high half and one half of a value in its low half,
-// and is written and read with relaxed device-scope atomics, which the
-// chip's eight L2 caches keep coherent (a release store or acquire load
-// would instead write back or invalidate the whole L2 of an XCD, once per
-// tile).  A value is two such words; a reader takes it once both carry the
-// current epoch, so words of other calls never match and no word depends on
-// the order in which another becomes visible.  Waits are bounded (kLbSpins
-// reads of a window): past that, kErrScan.
+// the call's epoch in its high half, and is written and read with relaxed
+// device-scope atomics, which the chip's eight L2 caches keep coherent (a
+// release store or acquire load would instead write back or invalidate the
+// whole L2 of an XCD, once per tile).  A tile has one status word (epoch,
+// bit 0: aggregate published, bit 1: inclusive prefix published), stored
+// after the values it announces, in an array of its own so that a wave
+// polls 64 neighbouring words; each value is two words (epoch and one half
+// of the value each).  A reader polls status words only, then reads the
+// values it needs once and takes them if every word carries the current
+// epoch (the value stores may become visible after the status store): words
+// of other calls never match, and no word depends on the order in which
+// another becomes visible.  Failed polls back off; waits are bounded
+// (kLbSpins polls of a window): past that, kErrScan.
 constexpr int kLbNT = 256;
 constexpr int kLbIT = 8;
 constexpr int kLbTile = kLbNT * kLbIT;
 constexpr u32 kLbSpins = 1u << 22;
 constexpr int kLbMax = 4;
-// State words per tile: [kLbMax values][aggregate, inclusive][lo, hi].
+// Value words per tile: [kLbMax values][aggregate, inclusive][lo, hi].
 constexpr int kLbWords = kLbMax * 4;
+constexpr u32 kLbAgg = 1u, kLbInc = 2u;
 
 struct LbArgs {
   const void *in[kLbMax];
@@ -111,23 +117,39 @@ struct LbArgs {
   ScanPublish pub;  // pub.dst == NULL: none
   u64 n;
   u32 nb, epoch;
-  u64 *state;   // [nb * kLbWords]
+  u64 *status;  // [nb] status words
+  u64 *vals;    // [nb * kLbWords] value words
   u32 *ctr, *err;
   const u64 *skip_if;  // nonzero *skip_if: nothing to do
 };
 
-__device__ __forceinline__ void put_out(const LbArgs &p, int k, u64 i, u64 v) {
-  if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[i] = (u32)v;
-  else p.out[k][i] = v;
-}
-
 // Publishes value v of array k of tile t as its aggregate (which = 0) or
 // inclusive prefix (which = 1).
 __device__ __forceinline__ void lb_put(const LbArgs &p, u32 t, int k, int which, u64 v) {
-  u64 *w = p.state + (u64)t * kLbWords + k * 4 + which * 2;
+  u64 *w = p.vals + (u64)t * kLbWords + k * 4 + which * 2;
   const u64 tag = (u64)p.epoch << 32;
   __hip_atomic_store(&w[0], tag | (v & 0xffffffffull), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(&w[1], tag | (v >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Publishes the K aggregates (which = 0) or inclusive prefixes (which = 1)
+// of tile t, then its status.
+template <int K>
+__device__ __forceinline__ void lb_publish(const LbArgs &p, u32 t, int which, const u64 (&v)[K]) {
+#pragma unroll
+  for (int k = 0; k < K; ++k) lb_put(p, t, k, which, v[k]);
+  const u64 st = ((u64)p.epoch << 32) | (which ? (kLbAgg | kLbInc) : kLbAgg);
+  __hip_atomic_store(&p.status[t], st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Reads value `which` of array k of tile j; false unless both words carry
+// this call's epoch.
+__device__ __forceinline__ bool lb_get(const LbArgs &p, u64 j, int k, int which, u64 *v) {
+  const u64 *w = p.vals + j * kLbWords + k * 4 + which * 2;
+  const u64 a = __hip_atomic_load(&w[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const u64 b = __hip_atomic_load(&w[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  *v = (a & 0xffffffffull) | (b << 32);
+  return (u32)(a >> 32) == p.epoch && (u32)(b >> 32) == p.epoch;
 }
 
 // LDS slot of tile element e: one u64 of padding every 32 elements keeps
@@ -135,16 +157,48 @@ __device__ __forceinline__ void lb_put(const LbArgs &p, u32 t, int k, int which,
 // kLbIT + j) accesses free of bank conflicts.
 __device__ __forceinline__ u32 lb_slot(u32 e) { return e + (e >> 5); }
 
-// STRIPED: loads and stores striped across the workgroup through LDS (full
-// coalescing, for scans of many tiles, where bandwidth counts); otherwise
-// each thread reads and writes its own elements (fewer registers and
-// barriers, for scans of few tiles, where the latency of one tile counts).
-template <int K, bool STRIPED>
+// Exclusive sums over the workgroup of K values at once (one barrier for
+// all K); tot[k]: the workgroup's total of array k.  scratch is read after
+// the barrier, so a caller that reuses it needs another barrier first.
+template <int K>
+__device__ __forceinline__ void block_exclusive_sums(u64 (&v)[K], u64 (*scratch)[kLbNT / kWave],
+                                                     u64 (&tot)[K]) {
+  constexpr int NW = kLbNT / kWave;
+  const u32 lane = lane_id(), wid = threadIdx.x / kWave;
+  u64 inc[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    inc[k] = wave_inclusive_sum(v[k]);
+    if (lane == kWave - 1) scratch[k][wid] = inc[k];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    u64 base = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const u64 s = scratch[k][w];
+      base += (u32)w < wid ? s : 0ull;
+      all += s;
+    }
+    v[k] = base + inc[k] - v[k];
+    tot[k] = all;
+  }
+}
+
+// Tile loads and stores are striped across the workgroup and pass through
+// LDS (full coalescing); each thread scans kLbIT consecutive elements.
+// Every load of a tile is issued before the first is used: the element
+// index is clamped into the array and the value zeroed past its end, so no
+// load sits behind a branch (a branch around each load makes the compiler
+// wait for every one in turn).
+template <int K>
 __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
+  constexpr int NW = kLbNT / kWave;
   __shared__ u32 s_t;
   __shared__ u64 s_off[kLbMax];
-  __shared__ u64 scratch[kLbNT / kWave];
-  __shared__ u64 s_x[STRIPED ? kLbTile + kLbTile / 32 : 1];  // one array of the tile, transposed
+  __shared__ u64 scratch[kLbMax][NW];
+  __shared__ u64 s_x[kLbTile + kLbTile / 32];  // one array of the tile, transposed
   const u32 lane = lane_id();
   if (p.skip_if && *p.skip_if != 0) return;  // uniform: every workgroup leaves before the counter
   // tile numbers from the counter (a single tile needs none)
@@ -156,106 +210,117 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   if (p.nb > 1) __syncthreads();
   const u32 t = p.nb > 1 ? s_t : 0u;
   const u64 tbase = (u64)t * kLbTile;
-  // thread i scans elements kLbIT i .. kLbIT i + kLbIT - 1 of the tile
-  // (blocked); loads and stores are striped across the workgroup and pass
-  // through s_x
-  u64 loc[K][kLbIT];
+  // element r of this thread in the striped layout: tile position r kLbNT + thread
+  u64 x[K][kLbIT];
+  if (p.n != 0) {  // uniform
+    const u64 last = p.n - 1;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if ((p.wide >> k) & 1u) {
+        const u64 *in = static_cast<const u64 *>(p.in[k]);
+#pragma unroll
+        for (int r = 0; r < kLbIT; ++r)
+          x[k][r] = in[min<u64>(tbase + (u32)r * kLbNT + threadIdx.x, last)];
+      } else {
+        const u32 *in = static_cast<const u32 *>(p.in[k]);
+#pragma unroll
+        for (int r = 0; r < kLbIT; ++r)
+          x[k][r] = in[min<u64>(tbase + (u32)r * kLbNT + threadIdx.x, last)];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (const u64 *sub = p.sub[k]) {
+#pragma unroll
+        for (int r = 0; r < kLbIT; ++r)
+          x[k][r] -= sub[min<u64>(tbase + (u32)r * kLbNT + threadIdx.x, last)];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r)
+        if (tbase + (u32)r * kLbNT + threadIdx.x > last) x[k][r] = 0;
+  } else {
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r) x[k][r] = 0;
+  }
+  // to the blocked layout (thread i: elements kLbIT i .. kLbIT i + kLbIT - 1),
+  // then x[k][j] becomes the exclusive sum within the thread's elements
   u64 ex[K], tot[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    const bool wide = (p.wide >> k) & 1u;
-    const u64 *sub = p.sub[k];
-    auto elem = [&](u64 i) {
-      u64 x = 0;
-      if (i < p.n) {
-        x = wide ? static_cast<const u64 *>(p.in[k])[i] : (u64) static_cast<const u32 *>(p.in[k])[i];
-        if (sub) x -= sub[i];
-      }
-      return x;
-    };
-    if (STRIPED) {
 #pragma unroll
-      for (int r = 0; r < kLbIT; ++r) {
-        const u32 e = (u32)r * kLbNT + threadIdx.x;
-        s_x[lb_slot(e)] = elem(tbase + e);
-      }
-      __syncthreads();
-    }
+    for (int r = 0; r < kLbIT; ++r) s_x[lb_slot((u32)r * kLbNT + threadIdx.x)] = x[k][r];
+    __syncthreads();
     u64 run = 0;
 #pragma unroll
     for (int j = 0; j < kLbIT; ++j) {
-      const u32 e = threadIdx.x * kLbIT + j;
-      const u64 x = STRIPED ? s_x[lb_slot(e)] : elem(tbase + e);
-      loc[k][j] = run;
-      run += x;
+      const u64 v = s_x[lb_slot(threadIdx.x * kLbIT + j)];
+      x[k][j] = run;
+      run += v;
     }
-    ex[k] = block_exclusive_sum<kLbNT, u64>(run, scratch, &tot[k]);
-    __syncthreads();  // scratch and s_x reused
+    ex[k] = run;
+    __syncthreads();  // s_x reused
   }
+  block_exclusive_sums<K>(ex, scratch, tot);
   if (threadIdx.x < (u32)kWave) {
     u64 off[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) off[k] = 0;
     if (t == 0) {
-      if (lane == 0 && p.nb > 1) {  // a single tile has no successor reading it
-#pragma unroll
-        for (int k = 0; k < K; ++k) lb_put(p, 0, k, 1, tot[k]);
-      }
+      if (lane == 0 && p.nb > 1) lb_publish<K>(p, 0, 1, tot);  // a single tile has no successor
     } else {
-      if (lane == 0) {
-#pragma unroll
-        for (int k = 0; k < K; ++k) lb_put(p, t, k, 0, tot[k]);
-      }
+      if (lane == 0) lb_publish<K>(p, t, 0, tot);
       long long hi = (long long)t - 1;  // nearest predecessor of the window
-      u32 spins = 0;
+      u32 spins = 0, nap = 1;
       bool failed = false;
       while (true) {
         const long long j = hi - (long long)lane;
         // lane's tile j: below tile 0, an empty inclusive prefix
-        bool isp = true, isa = true;
-        u64 av[K], iv[K];
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-          av[k] = 0;
-          iv[k] = 0;
-          if (j >= 0) {
-            const u64 *w = p.state + (u64)j * kLbWords + k * 4;
-            const u64 a0 = __hip_atomic_load(&w[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const u64 a1 = __hip_atomic_load(&w[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const u64 i0 = __hip_atomic_load(&w[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const u64 i1 = __hip_atomic_load(&w[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            isa = isa && (u32)(a0 >> 32) == p.epoch && (u32)(a1 >> 32) == p.epoch;
-            isp = isp && (u32)(i0 >> 32) == p.epoch && (u32)(i1 >> 32) == p.epoch;
-            av[k] = (a0 & 0xffffffffull) | (a1 << 32);
-            iv[k] = (i0 & 0xffffffffull) | (i1 << 32);
-          }
+        u32 fl = kLbAgg | kLbInc;
+        if (j >= 0) {
+          const u64 st = __hip_atomic_load(&p.status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          fl = (u32)(st >> 32) == p.epoch ? (u32)st : 0u;
         }
-        const bool ready = isp || isa;
-        const u64 pm = __ballot(isp), rm = __ballot(ready);
+        const u64 pm = __ballot((fl & kLbInc) != 0), rm = __ballot(fl != 0);
         const u32 lp = pm ? (u32)__builtin_ctzll(pm) : (u32)kWave;  // nearest inclusive prefix
         const u64 need = lp < (u32)kWave ? (lp == 63 ? ~0ull : (2ull << lp) - 1ull) : ~0ull;
-        if ((rm & need) != need) {  // a tile in between has not published yet
+        bool ok = (rm & need) == need;  // uniform
+        u64 v[K];
+        if (ok) {
+          // values of lanes below lp (aggregates) and of lane lp (its
+          // inclusive prefix); taken once every word carries the epoch
+          bool good = true;
+#pragma unroll
+          for (int k = 0; k < K; ++k) {
+            v[k] = 0;
+            if (j >= 0 && lane <= lp) good = lb_get(p, (u64)j, k, lane == lp ? 1 : 0, &v[k]) && good;
+          }
+          ok = __ballot(!good) == 0;
+        }
+        if (!ok) {  // a tile in between has not published yet
           if (++spins > kLbSpins) {
             failed = true;
             break;
           }
-          __builtin_amdgcn_s_sleep(1);
+          for (u32 i = 0; i < nap; ++i) __builtin_amdgcn_s_sleep(1);
+          nap = min(nap + 1, 32u);
           continue;
         }
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-          u64 x = 0;
-          if (j >= 0 && (u32)lane < lp) x = av[k];
-          else if (j >= 0 && (u32)lane == lp) x = iv[k];
-          off[k] += wave_sum(x);
-        }
+        for (int k = 0; k < K; ++k) off[k] += wave_sum(v[k]);
         if (lp < (u32)kWave) break;
         hi -= kWave;
       }
       if (failed && lane == 0) atomicOr(p.err, kErrScan);
       if (lane == 0) {
+        u64 inc[K];
 #pragma unroll
-        for (int k = 0; k < K; ++k) lb_put(p, t, k, 1, off[k] + tot[k]);
+        for (int k = 0; k < K; ++k) inc[k] = off[k] + tot[k];
+        lb_publish<K>(p, t, 1, inc);
       }
     }
     if (lane == 0) {
@@ -263,8 +328,10 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
       for (int k = 0; k < K; ++k) {
         s_off[k] = off[k];
         if (t == p.nb - 1) {
-          put_out(p, k, p.n, off[k] + tot[k]);
-          if (p.total_to[k]) *p.total_to[k] = off[k] + tot[k];
+          const u64 total = off[k] + tot[k];
+          if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[p.n] = (u32)total;
+          else p.out[k][p.n] = total;
+          if (p.total_to[k]) *p.total_to[k] = total;
         }
       }
     }
@@ -290,22 +357,18 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   for (int k = 0; k < K; ++k) {
     if ((p.tonly >> k) & 1u) continue;  // uniform
     const u64 o = s_off[k] + ex[k];
-    if (!STRIPED) {
 #pragma unroll
-      for (int j = 0; j < kLbIT; ++j) {
-        const u64 i = tbase + threadIdx.x * kLbIT + j;
-        if (i < p.n) put_out(p, k, i, o + loc[k][j]);
-      }
-      continue;
-    }
-#pragma unroll
-    for (int j = 0; j < kLbIT; ++j) s_x[lb_slot(threadIdx.x * kLbIT + j)] = o + loc[k][j];
+    for (int j = 0; j < kLbIT; ++j) s_x[lb_slot(threadIdx.x * kLbIT + j)] = o + x[k][j];
     __syncthreads();
+    const bool narrow = (p.narrow >> k) & 1u;
 #pragma unroll
     for (int r = 0; r < kLbIT; ++r) {
       const u32 e = (u32)r * kLbNT + threadIdx.x;
       const u64 i = tbase + e;
-      if (i < p.n) put_out(p, k, i, s_x[lb_slot(e)]);
+      if (i < p.n) {
+        if (narrow) reinterpret_cast<u32 *>(p.out[k])[i] = (u32)s_x[lb_slot(e)];
+        else p.out[k][i] = s_x[lb_slot(e)];
+      }
     }
     __syncthreads();
   }
@@ -373,9 +436,12 @@ void fill_u64(u64 *p, u64 v, u64 n, hipStream_t s) {
 
 size_t scan_temp_bytes(u64 n) { return temp_elems<u64>(n) * sizeof(u64) + 256; }
 
+// Status words (rounded up to whole 256-byte lines), then value words.
+static u64 lb_status_words(u64 nb) { return (nb + 31) / 32 * 32; }
+
 size_t scan_lb_state_bytes(u64 n) {
   const u64 nb = std::max<u64>(1, ceil_div(n, kLbTile));
-  return (size_t)nb * kLbWords * 8 + 256;
+  return (size_t)(lb_status_words(nb) + nb * kLbWords) * 8 + 256;
 }
 
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
@@ -401,23 +467,16 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   p.nb = (u32)nb;
   u32 e = epochs.fetch_add(1, std::memory_order_relaxed) + 1;
   p.epoch = e ? e : 1u;  // state words of zero-filled memory never match
-  p.state = static_cast<u64 *>(state);
+  p.status = static_cast<u64 *>(state);
+  p.vals = p.status + lb_status_words(nb);
   p.ctr = ctr;
   p.err = err;
   p.skip_if = skip_if;
   const dim3 g((unsigned)nb), bl(kLbNT);
-  // striped once the tiles outnumber the compute units
-  if (nb > (u64)compute_units()) {
-    if (k == 1) hipLaunchKernelGGL((k_scan_lb<1, true>), g, bl, 0, s, p);
-    else if (k == 2) hipLaunchKernelGGL((k_scan_lb<2, true>), g, bl, 0, s, p);
-    else if (k == 3) hipLaunchKernelGGL((k_scan_lb<3, true>), g, bl, 0, s, p);
-    else hipLaunchKernelGGL((k_scan_lb<4, true>), g, bl, 0, s, p);
-  } else {
-    if (k == 1) hipLaunchKernelGGL((k_scan_lb<1, false>), g, bl, 0, s, p);
-    else if (k == 2) hipLaunchKernelGGL((k_scan_lb<2, false>), g, bl, 0, s, p);
-    else if (k == 3) hipLaunchKernelGGL((k_scan_lb<3, false>), g, bl, 0, s, p);
-    else hipLaunchKernelGGL((k_scan_lb<4, false>), g, bl, 0, s, p);
-  }
+  if (k == 1) hipLaunchKernelGGL((k_scan_lb<1>), g, bl, 0, s, p);
+  else if (k == 2) hipLaunchKernelGGL((k_scan_lb<2>), g, bl, 0, s, p);
+  else if (k == 3) hipLaunchKernelGGL((k_scan_lb<3>), g, bl, 0, s, p);
+  else hipLaunchKernelGGL((k_scan_lb<4>), g, bl, 0, s, p);
 }
 
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s) {
