@@ -251,7 +251,7 @@ size_t scan_temp_bytes(u64 n);
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s);
 void exclusive_scan(const u32 *in, u64 *out, u64 n, void *temp, hipStream_t s);
 void exclusive_scan(const u32 *in, u32 *out, u64 n, void *temp, hipStream_t s);
-// Single-pass exclusive scans (decoupled look-back) of up to three arrays of
+// Single-pass exclusive scans (decoupled look-back) of up to four arrays of
 // the same length n at once, one launch: in[k] holds u64 when wide[k], else
 // u32; out[k] has n + 1 entries (u64).  `state` is scan_lb_state_bytes(n)
 // bytes that no other code writes and that were zero-filled once when
@@ -264,21 +264,27 @@ struct ScanJob {
   bool narrow_out = false;    // out holds u32 (sums must fit)
   const u64 *sub = nullptr;   // scans in[i] - sub[i] (in wide)
   bool total_only = false;    // writes out[n] alone
-  u64 *total_to = nullptr;    // the total is also stored here
+  u64 *total_to = nullptr;    // the total is also stored here (less *total_minus,
+  const u64 *total_minus = nullptr;  // when given; as a u32, saturated, when
+  bool total_narrow = false;         // total_narrow)
 };
 // After the last tile has stored the totals: `words` 32-bit words copied
 // from src to dst (host memory the device can write) except word seq_word,
 // a system-scope fence, then dst[seq_word] = seq (a publication the host
-// can wait for).
+// can wait for); then the words i of src with bit i of clear_mask set are
+// zeroed (words < 64).  when_skipped: a scan skipped by its skip_if word
+// still publishes src as it is (and clears nothing).
 struct ScanPublish {
   const void *src;
   void *dst;
   u32 words, seq_word, seq;
+  u64 clear_mask = 0;
+  bool when_skipped = false;
 };
 size_t scan_lb_state_bytes(u64 n);
 // skip_if (may be NULL): a device word read by every workgroup first; when it
-// is nonzero the scan does nothing at all (a scan enqueued before the host
-// knows whether it is needed).
+// is nonzero the scan does nothing (a scan enqueued before the host knows
+// whether it is needed) but the publication asked for with when_skipped.
 void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr, u32 *err,
                        hipStream_t s, const ScanPublish *pub = nullptr,
                        const u64 *skip_if = nullptr);

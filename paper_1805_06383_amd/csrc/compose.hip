@@ -667,6 +667,26 @@ void Composer::run(fstc_result *out) {
       exclusive_scan_lb(jobs, 4, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, &pub);
       T.at(kNone);
     };
+    // Scan of a direct product level: new pairs per source (ids), joined
+    // pairs per source (their total, less the level's records, is the
+    // product merge's joined pairs) and merged arcs per source; its last
+    // tile stores the level totals, publishes the counters as publication
+    // `seq` and clears them for the next level (what k_merged_total does
+    // for the other level forms).
+    auto direct_totals_scan = [&](ScanJob (&jobs)[3], ScanPublish &pub, u32 seq) {
+      jobs[0] = ScanJob{newc.p, false, newoff.as<u64>()};
+      jobs[1] = ScanJob{cnt.p, true, ptot.as<u64>()};
+      jobs[2] = ScanJob{mend.p, true, aoff.as<u64>()};
+      jobs[0].total_to = reinterpret_cast<u64 *>(&dst->nnew);
+      jobs[0].total_narrow = true;
+      jobs[1].total_only = true;
+      jobs[1].total_to = &dst->prod_records;
+      jobs[1].total_minus = &dst->R;
+      jobs[2].sub = tstart.as<u64>();
+      jobs[2].total_to = &dst->merged;
+      pub = ScanPublish{dst, hs_dev, (u32)(sizeof(Status) / 4), (u32)(offsetof(Status, seq) / 4), seq};
+      pub.clear_mask = level_clear_mask();
+    };
     const u32 seq1 = next_publication();
     count_and_scan(seq1);
     // Speculative product merge: with the dense visited array (no rehash
@@ -746,11 +766,16 @@ void Composer::run(fstc_result *out) {
       sq1b.grow_keep((n_states + newcap_b) * 4, n_states * 4);
       sq2b.grow_keep((n_states + newcap_b) * 4, n_states * 4);
       T.at(kAssign);
-      ScanJob jobs[3] = {{newc.p, false, newoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()},
-                         {mend.p, true, aoff.as<u64>()}};
-      jobs[1].total_only = true;
-      jobs[2].sub = tstart.as<u64>();
-      exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, nullptr,
+      // the scan's last tile stores the level totals (new pairs, joined
+      // pairs, merged arcs), publishes the counters and clears them for the
+      // next level; skipped (a level with records) it publishes the count's
+      // totals as they are
+      seq_wait = next_publication();
+      ScanJob jobs[3];
+      ScanPublish pub;
+      direct_totals_scan(jobs, pub, seq_wait);
+      pub.when_skipped = true;
+      exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, &pub,
                         roff.as<u64>() + nsrc);
       MergeArgs md{};  // the fields the direct-level kernels read
       md.R_dev = roff.as<u64>() + nsrc;
@@ -771,9 +796,6 @@ void Composer::run(fstc_result *out) {
       md.out_w = reinterpret_cast<float *>(out_arcs.col(4));
       md.out_base = arcs;
       launch_assign_direct(md, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
-      seq_wait = next_publication();
-      launch_merged_total(aoff.as<u64>() + nsrc, newoff.as<u64>() + nsrc, ptot.as<u64>() + nsrc, md,
-                          hs_dev, seq_wait, s);
       launch_fix_marked(md, (u64)nsrc * maxk, s);
       T.at(kNone);
     }
@@ -952,7 +974,7 @@ void Composer::run(fstc_result *out) {
     if (direct_level && ahead) {
       // everything ran before the wait: read the totals
       ++product_launches;
-      status_clear = true;  // k_merged_total cleared the level counters
+      status_clear = true;  // the totals scan cleared the level counters
       nnew = hs->st.nnew;
       merged = hs->st.merged;
       premerge += hs->st.prod_records;
@@ -978,12 +1000,12 @@ void Composer::run(fstc_result *out) {
       // a term), ids of the claimed entries, then the other new targets
       ++product_launches;
       T.at(kAssign);
+      const u32 seq2 = next_publication();
       {
-        ScanJob jobs[3] = {{newc.p, false, newoff.as<u64>()}, {cnt.p, true, ptot.as<u64>()},
-                           {mend.p, true, aoff.as<u64>()}};
-        jobs[1].total_only = true;
-        jobs[2].sub = tstart.as<u64>();
-        exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s);
+        ScanJob jobs[3];
+        ScanPublish pub;
+        direct_totals_scan(jobs, pub, seq2);
+        exclusive_scan_lb(jobs, 3, nsrc, lb(nsrc), &dst->scan_ctr, &dst->err, s, &pub);
       }
       ma.out_src = out_arcs.col(0);
       ma.out_dst = out_arcs.col(1);
@@ -994,13 +1016,10 @@ void Composer::run(fstc_result *out) {
       sq1b.grow_keep((n_states + newcap) * 4, n_states * 4);
       sq2b.grow_keep((n_states + newcap) * 4, n_states * 4);
       launch_assign_direct(ma, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
-      const u32 seq2 = next_publication();
-      launch_merged_total(aoff.as<u64>() + nsrc, newoff.as<u64>() + nsrc, ptot.as<u64>() + nsrc, ma,
-                          hs_dev, seq2, s);
       launch_fix_marked(ma, prodpos, s);
       T.at(kNone);
       wait_published(seq2);
-      status_clear = true;  // k_merged_total cleared the level counters
+      status_clear = true;  // the totals scan cleared the level counters
       nnew = hs->st.nnew;
       merged = hs->st.merged;
       premerge += hs->st.prod_records;
@@ -1156,7 +1175,7 @@ void Composer::run(fstc_result *out) {
                           pa, hs_dev, seq2, s);
       T.at(kNone);
       wait_published(seq2);
-      status_clear = true;  // k_merged_total cleared the level counters
+      status_clear = true;  // the totals scan cleared the level counters
       nnew = hs->st.nnew;
       merged = hs->st.merged;  // every joined pair is an arc
       premerge += merged;

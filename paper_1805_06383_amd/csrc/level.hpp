@@ -383,5 +383,8 @@ void launch_finals(const u32 *sq1, const u32 *sq2, u64 n, const uint8_t *f1, con
 void launch_merged_total(const u64 *a_total, const u64 *new_total, const u64 *pair_total,
                          const MergeArgs &a, Status *host, u32 seq, hipStream_t s);
 void launch_reset_level(Status *st, hipStream_t s);
+// The 32-bit words of Status that the level-counter clearing zeroes (bit i:
+// word i), for a publication that clears them itself (ScanPublish).
+u64 level_clear_mask();
 
 }  // namespace fstc

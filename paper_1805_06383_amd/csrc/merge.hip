@@ -2516,6 +2516,7 @@ __device__ __forceinline__ void publish(const Status *st, Status *host, u32 seq,
   if (t == 0) __hip_atomic_store(&host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// (level_clear_mask names the same fields, for publications that clear them)
 __device__ __forceinline__ void clear_level(Status *st) {
   st->R = st->M = st->merged = st->RB = 0;
   st->nwide = st->nheavy = st->nbig = st->nnew = 0;
@@ -2844,6 +2845,35 @@ void launch_merged_total(const u64 *a_total, const u64 *new_total, const u64 *pa
 
 void launch_reset_level(Status *st, hipStream_t s) {
   hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(1), 0, s, st);
+}
+
+u64 level_clear_mask() {
+  static_assert(sizeof(Status) <= 64 * 4, "one mask bit per word");
+  u64 m = 0;
+  auto add = [&](size_t off, size_t bytes) {
+    for (size_t w = off / 4; w < (off + bytes) / 4; ++w) m |= 1ull << w;
+  };
+  // the fields clear_level zeroes
+  add(offsetof(Status, R), 8);
+  add(offsetof(Status, M), 8);
+  add(offsetof(Status, merged), 8);
+  add(offsetof(Status, RB), 8);
+  add(offsetof(Status, nwide), 4);
+  add(offsetof(Status, nheavy), 4);
+  add(offsetof(Status, nbig), 4);
+  add(offsetof(Status, nnew), 4);
+  add(offsetof(Status, max_small), 4);
+  add(offsetof(Status, dense_records), 8);
+  add(offsetof(Status, dense_runs), 8);
+  add(offsetof(Status, sort_runs), 8);
+  add(offsetof(Status, nprod), 4);
+  add(offsetof(Status, nprod_mfma), 4);
+  add(offsetof(Status, prod_records), 8);
+  add(offsetof(Status, prod_entries), 8);
+  add(offsetof(Status, nsort), 4);
+  add(offsetof(Status, ngen), 4);
+  add(offsetof(Status, ngrp), 4);
+  return m;
 }
 
 }  // namespace fstc

@@ -112,8 +112,10 @@ struct LbArgs {
   u32 wide;    // bit k: in[k] holds u64
   u32 narrow;  // bit k: out[k] holds u32
   u32 tonly;   // bit k: only out[k][n] is written
+  u32 tnarrow;  // bit k: total_to[k] holds a u32
   const u64 *sub[kLbMax];
   u64 *total_to[kLbMax];
+  const u64 *tminus[kLbMax];
   ScanPublish pub;  // pub.dst == NULL: none
   u64 n;
   u32 nb, epoch;
@@ -186,6 +188,29 @@ __device__ __forceinline__ void block_exclusive_sums(u64 (&v)[K], u64 (*scratch)
   }
 }
 
+// The publication of p.pub by one wave, after the stores it announces (see
+// ScanPublish): lane i copies word i (once lane 0's total stores are
+// visible to the wave), then one lane writes the publication number once
+// every lane's copy has completed; then, when `clear`, the lanes zero the
+// words of clear_mask (each its own words, after copying them).
+__device__ __forceinline__ void lb_publish_counters(const LbArgs &p, bool clear) {
+  const u32 lane = lane_id();
+  u32 *src = const_cast<u32 *>(static_cast<const u32 *>(p.pub.src));
+  u32 *dst = static_cast<u32 *>(p.pub.dst);
+  __threadfence();
+  for (u32 i = lane; i < p.pub.words; i += kWave)
+    if (i != p.pub.seq_word) dst[i] = src[i];
+  __threadfence_system();
+  __builtin_amdgcn_wave_barrier();
+  if (lane == 0)
+    __hip_atomic_store(&dst[p.pub.seq_word], p.pub.seq, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+  if (clear && p.pub.clear_mask) {
+    for (u32 i = lane; i < p.pub.words && i < 64u; i += kWave)
+      if ((p.pub.clear_mask >> i) & 1ull) src[i] = 0u;
+  }
+}
+
 // Tile loads and stores are striped across the workgroup and pass through
 // LDS (full coalescing); each thread scans kLbIT consecutive elements.
 // Every load of a tile is issued before the first is used: the element
@@ -200,7 +225,11 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __shared__ u64 scratch[kLbMax][NW];
   __shared__ u64 s_x[kLbTile + kLbTile / 32];  // one array of the tile, transposed
   const u32 lane = lane_id();
-  if (p.skip_if && *p.skip_if != 0) return;  // uniform: every workgroup leaves before the counter
+  if (p.skip_if && *p.skip_if != 0) {  // uniform: every workgroup leaves before the counter
+    if (blockIdx.x == 0 && threadIdx.x < (u32)kWave && p.pub.dst && p.pub.when_skipped)
+      lb_publish_counters(p, false);
+    return;
+  }
   // tile numbers from the counter (a single tile needs none)
   if (threadIdx.x == 0 && p.nb > 1) {
     const u32 t = atomicAdd(p.ctr, 1u);
@@ -331,26 +360,18 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
           const u64 total = off[k] + tot[k];
           if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[p.n] = (u32)total;
           else p.out[k][p.n] = total;
-          if (p.total_to[k]) *p.total_to[k] = total;
+          if (p.total_to[k]) {
+            const u64 v = total - (p.tminus[k] ? *p.tminus[k] : 0ull);
+            if ((p.tnarrow >> k) & 1u)
+              *reinterpret_cast<u32 *>(p.total_to[k]) = (u32)min<u64>(v, 0xffffffffull);
+            else
+              *p.total_to[k] = v;
+          }
         }
       }
     }
-    if (t == p.nb - 1 && p.pub.dst) {
-      // every other tile has published its inclusive prefix: the totals
-      // are final.  Lane i copies word i (after lane 0's total stores are
-      // visible to the wave), then one lane writes the publication number
-      // once every lane's copy has completed.
-      const u32 *src = static_cast<const u32 *>(p.pub.src);
-      u32 *dst = static_cast<u32 *>(p.pub.dst);
-      __threadfence();
-      for (u32 i = lane; i < p.pub.words; i += kWave)
-        if (i != p.pub.seq_word) dst[i] = src[i];
-      __threadfence_system();
-      __builtin_amdgcn_wave_barrier();
-      if (lane == 0)
-        __hip_atomic_store(&dst[p.pub.seq_word], p.pub.seq, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_SYSTEM);
-    }
+    // every other tile has published its inclusive prefix: the totals are final
+    if (t == p.nb - 1 && p.pub.dst) lb_publish_counters(p, true);
   }
   __syncthreads();
 #pragma unroll
@@ -453,6 +474,7 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   p.wide = 0;
   p.narrow = 0;
   p.tonly = 0;
+  p.tnarrow = 0;
   for (int i = 0; i < k; ++i) {
     p.in[i] = jobs[i].in;
     p.out[i] = jobs[i].out;
@@ -461,6 +483,8 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
     p.tonly |= (jobs[i].total_only ? 1u : 0u) << i;
     p.sub[i] = jobs[i].sub;
     p.total_to[i] = jobs[i].total_to;
+    p.tminus[i] = jobs[i].total_minus;
+    p.tnarrow |= (jobs[i].total_narrow ? 1u : 0u) << i;
   }
   if (pub) p.pub = *pub;
   p.n = n;
