@@ -542,6 +542,10 @@ void Composer::run(fstc_result *out) {
   // or a capacity it must not exceed) takes the per-level kernels
   const bool small_ok = !o.no_reduction && !o.no_small_levels;
   u32 small_skip_depth = ~0u;  // the depth the one-workgroup kernel declined last
+  // set when it declined a source's shape: not tried again until a level
+  // taken by the per-level kernels has few sources of shapes it declines
+  // (the count kernels count them)
+  bool small_shape_off = false;
   u32 small_levels = 0;
   Buf ssb(&A);
   SmallState *ss_dev = small_ok ? static_cast<SmallState *>(ssb.ensure(sizeof(SmallState)))
@@ -550,7 +554,7 @@ void Composer::run(fstc_result *out) {
   while (true) {
     if (o.max_levels && depth >= o.max_levels) break;
     if (hi == lo) break;
-    if (small_ok && hi - lo <= kSmallSources && depth != small_skip_depth) {
+    if (small_ok && !small_shape_off && hi - lo <= kSmallSources && depth != small_skip_depth) {
       constexpr u64 kSmallGrow = 1u << 16;  // room for this many states and arcs past the current
       sq1b.grow_keep((n_states + kSmallGrow) * 4, n_states * 4);
       sq2b.grow_keep((n_states + kSmallGrow) * 4, n_states * 4);
@@ -612,7 +616,9 @@ void Composer::run(fstc_result *out) {
       max_frontier = std::max<u64>(max_frontier, out_st.max_frontier);
       max_level_pre = std::max<u64>(max_level_pre, out_st.max_level_pre);
       if (out_st.reason == kSmallDone) break;
-      if (out_st.reason == kSmallTooLarge || out_st.levels == 0) small_skip_depth = depth;
+      if (out_st.reason == kSmallShape) small_shape_off = true;
+      if (out_st.reason == kSmallTooLarge || out_st.reason == kSmallShape || out_st.levels == 0)
+        small_skip_depth = depth;
       continue;  // larger capacities (a capacity stop after progress) or the per-level path
     }
     const u32 nsrc = hi - lo;
@@ -811,6 +817,9 @@ void Composer::run(fstc_result *out) {
     }
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
+    // tried again once at most one source in eight of a level is of such a
+    // shape (then the next, smaller levels usually have none)
+    if (small_shape_off && (u64)hs->st.unfit * 8 < nsrc) small_shape_off = false;
     const u64 prodpos = nprod ? hs->st.prod_entries : 0;  // product-merge temp slots
     if (R == 0 && nprod == 0) break;  // no arc leaves this level: no new states either
     premerge += R;

@@ -146,11 +146,14 @@ __device__ __forceinline__ u32 join_class(const Ranges &r) {
 // in LDS: one device atomic per list per block.
 __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   constexpr int kLists = 5;
-  __shared__ u32 s_n[kLists], s_base[kLists], s_max;
+  __shared__ u32 s_n[kLists], s_base[kLists], s_max, s_unfit;
   const u32 lane = lane_id();
   const u64 u = (u64)blockIdx.x * blockDim.x + threadIdx.x;
   if (threadIdx.x < kLists) s_n[threadIdx.x] = 0;
-  if (threadIdx.x == 0) s_max = 0;
+  if (threadIdx.x == 0) s_max = s_unfit = 0;
+  // a source of a shape the one-workgroup small-level kernel declines
+  // (group joins: decided by their count); counted per level
+  bool unfit = false;
   // wide, heavy, big, one-per-wave product, 16-lane join
   bool pred[kLists] = {false, false, false, false, false};
   u64 cnt = 0;
@@ -165,6 +168,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     a.newc[u] = 0;
     r = Ranges{a.c1.row[q1], a.c1.row[q1 + 1], a.c2.row[q2], a.c2.row[q2 + 1]};
     const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
+    unfit = mn > kSmallShortList || max(r.e1 - r.b1, r.e2 - r.b2) > kSmallLongList;
     if (a.prod && mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(a, (u32)u, q1, q2, r, mf);
     if (pk && a.unred && !(a.quad && (a.phdr[2 * u].w & 4u))) pk = 0;  // records
     a.pk[u] = pk;
@@ -172,12 +176,15 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
     if (pk) {
       a.cnt[u] = 0;
       a.mc[u] = 0;
+      unfit = true;
       // strided sources go to the four-source kernel when it runs
       pred[3] = !(a.quad && (a.phdr[2 * u].w & 4u));
     } else if (mn > kHeavyMin) {
       pred[1] = true;
+      unfit = true;
     } else if (join_class(r) == kJoinWide) {
       pred[0] = true;
+      unfit = true;
     } else if (join_class(r) == kJoinGroup) {
       pred[4] = true;
     } else {
@@ -189,10 +196,13 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
       a.cnt[u] = cnt;
       a.mc[u] = mc;
       pred[2] = cnt > kMergeSmall;
+      unfit = unfit || cnt > kSmallPerSource;
     }
   }
   const u32 small_max = wave_max((u32)(pred[2] ? 0 : cnt));
+  const u32 nunfit = (u32)__popcll(__ballot(unfit));
   __syncthreads();
+  if (lane == 0 && nunfit) atomicAdd(&s_unfit, nunfit);
   u64 m[kLists];
   u32 woff[kLists];
 #pragma unroll
@@ -212,6 +222,7 @@ __global__ __launch_bounds__(kCountNT) void k_count_small(LevelArgs a) {
   if (threadIdx.x < kLists && s_n[threadIdx.x])
     s_base[threadIdx.x] = atomicAdd(counters[threadIdx.x], s_n[threadIdx.x]);
   if (threadIdx.x == kLists && s_max) atomicMax(&a.st->max_small, s_max);
+  if (threadIdx.x == kLists + 1 && s_unfit) atomicAdd(&a.st->unfit, s_unfit);
   __syncthreads();
   u32 *const lists[kLists] = {a.wide, a.heavy, a.big, a.glist, a.grp};
 #pragma unroll
@@ -486,6 +497,10 @@ __device__ __forceinline__ void count_group_sources(const LevelArgs &a, u32 blk,
       a.mc[u] = mc;
       note_count(a, u, cnt, run_max);
     }
+    // one atomic per wave for the sources the small-level kernel declines
+    const u64 big_join = __ballot(have && threadIdx.x % G == 0 && cnt > kSmallPerSource);
+    if (big_join && lane_id() == (u32)__builtin_ctzll(big_join))
+      atomicAdd(&a.st->unfit, (u32)__popcll(big_join));
   }
 }
 

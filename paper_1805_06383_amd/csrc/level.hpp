@@ -38,7 +38,8 @@ struct Status {
   u32 nsort;          // tiles k_merge_dense left to the sort kernel
   u32 scan_ctr;       // tile counter of the single-pass scans (0 between scans)
   u32 seq;            // host copy only: number of the last publication, written last
-  u32 pad0;
+  u32 unfit;          // sources of the level of a shape the one-workgroup
+                      // small-level kernel declines (kSmallShape)
   u32 nprod;          // sources of the product merge       } one u64, the total of
   u32 nprod_mfma;     // of those, summed on the matrix cores } the level's flag words
   u64 prod_records;   // their joined arc pairs (not written as records)
@@ -243,7 +244,16 @@ struct MergeArgs {
 // ends, and leaves the loop state in *ss for the host.
 constexpr u32 kSmallSources = 512;
 constexpr u32 kSmallRecords = 1024;
-enum : u32 { kSmallTooLarge = 1, kSmallCapacity = 2, kSmallDone = 3 };
+// Joins it takes: the shorter list at most kSmallShortList symbols, the
+// longer at most kSmallLongList, at most kSmallPerSource joined pairs per
+// source (one thread joins and emits a source: longer joins and larger
+// sources are the per-level kernels' work, done by many lanes).
+constexpr u32 kSmallShortList = 32, kSmallLongList = 4096, kSmallPerSource = 64;
+// Why it stopped: a level too large (sources, joined pairs), a capacity, the
+// end of the search, or a source of a shape it does not take (a long list
+// or many joined pairs: a property of the inputs' states more than of the
+// level).
+enum : u32 { kSmallTooLarge = 1, kSmallCapacity = 2, kSmallDone = 3, kSmallShape = 4 };
 struct SmallState {
   u64 lo, hi, n_states, arcs, premerge;
   u64 max_frontier, max_level_pre;

@@ -1544,11 +1544,7 @@ __device__ __forceinline__ void small_sort(u64 *key, u32 *val, u32 n) {
   }
 }
 
-// Joins the one-workgroup kernel takes: the shorter list at most this many
-// symbols, the longer at most kSmallLongList, at most kSmallPerSource joined
-// pairs per source (one thread joins and emits a source: longer joins and
-// larger sources are the per-level kernels' work, done by many lanes).
-constexpr u32 kSmallShortList = 32, kSmallLongList = 4096, kSmallPerSource = 64;
+
 
 // Calls f(s1, s2) for every pair of segments with one symbol: s1 in
 // [b1, e1), s2 in [b2, e2), in increasing symbol order (the shorter list
@@ -1632,7 +1628,7 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
       long_join = min(e1 - b1, e2 - b2) > kSmallShortList || max(e1 - b1, e2 - b2) > kSmallLongList;
     }
     if (__syncthreads_or(long_join)) {
-      st.reason = kSmallTooLarge;
+      st.reason = kSmallShape;
       break;
     }
     if (t < nsrc) {
@@ -1641,7 +1637,7 @@ __global__ __launch_bounds__(kSmallNT) void k_small_levels(SmallArgs a) {
       });
     }
     if (__syncthreads_or(cnt > kSmallPerSource)) {
-      st.reason = kSmallTooLarge;
+      st.reason = kSmallShape;
       break;
     }
     u64 R;
@@ -2527,6 +2523,7 @@ __device__ __forceinline__ void clear_level(Status *st) {
   st->nsort = 0;
   st->ngen = 0;
   st->ngrp = 0;
+  st->unfit = 0;
 }
 
 
@@ -2873,6 +2870,7 @@ u64 level_clear_mask() {
   add(offsetof(Status, nsort), 4);
   add(offsetof(Status, ngen), 4);
   add(offsetof(Status, ngrp), 4);
+  add(offsetof(Status, unfit), 4);
   return m;
 }
 
