@@ -7,6 +7,7 @@
 // tiles of 4096 elements, the tile sums are scanned recursively, and a second
 // pass scans each tile with its offset.  A single tile is one launch.
 #include <atomic>
+#include <type_traits>
 
 #include "common.hpp"
 
@@ -211,13 +212,114 @@ __device__ __forceinline__ void lb_publish_counters(const LbArgs &p, bool clear)
   }
 }
 
+// out[k][n] = total, and the total (less *tminus[k]) at total_to[k].
+__device__ __forceinline__ void lb_store_total(const LbArgs &p, int k, u64 total) {
+  if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[p.n] = (u32)total;
+  else p.out[k][p.n] = total;
+  if (p.total_to[k]) {
+    const u64 v = total - (p.tminus[k] ? *p.tminus[k] : 0ull);
+    if ((p.tnarrow >> k) & 1u)
+      *reinterpret_cast<u32 *>(p.total_to[k]) = (u32)min<u64>(v, 0xffffffffull);
+    else
+      *p.total_to[k] = v;
+  }
+}
+
+// Loads element pos(r) of each of the K arrays for r < kLbIT, every load
+// issued before the first is used: indices clamped into the arrays, values
+// zeroed past their end.  WM / SM: the wide and subtracted arrays as bit
+// masks when known at compile time (-1: read from p), so that no load sits
+// behind a branch (a branch around a load makes the compiler wait for
+// every earlier one).
+template <int K, int WM, int SM, class Pos>
+__device__ __forceinline__ void lb_load(const LbArgs &p, Pos pos, u64 (&x)[K][kLbIT]) {
+  if (p.n == 0) {  // uniform
+#pragma unroll
+    for (int k = 0; k < K; ++k)
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r) x[k][r] = 0;
+    return;
+  }
+  const u64 last = p.n - 1;
+  const u32 wide = WM >= 0 ? (u32)WM : p.wide;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    if ((wide >> k) & 1u) {
+      const u64 *in = static_cast<const u64 *>(p.in[k]);
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r) x[k][r] = in[min<u64>(pos(r), last)];
+    } else {
+      const u32 *in = static_cast<const u32 *>(p.in[k]);
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r) x[k][r] = in[min<u64>(pos(r), last)];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    const u64 *sub = p.sub[k];
+    if (SM >= 0 ? ((SM >> k) & 1) != 0 : sub != nullptr) {
+#pragma unroll
+      for (int r = 0; r < kLbIT; ++r) x[k][r] -= sub[min<u64>(pos(r), last)];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+#pragma unroll
+    for (int r = 0; r < kLbIT; ++r)
+      if (pos(r) > last) x[k][r] = 0;
+}
+
+// A scan of one tile (n <= kLbTile): each thread loads, scans and stores
+// its own kLbIT consecutive elements (no LDS staging, no look-back).
+template <int K, int WM, int SM>
+__global__ __launch_bounds__(kLbNT) void k_scan_one(LbArgs p) {
+  __shared__ u64 scratch[kLbMax][kLbNT / kWave];
+  const u32 lane = lane_id();
+  if (p.skip_if && *p.skip_if != 0) {  // uniform
+    if (threadIdx.x < (u32)kWave && p.pub.dst && p.pub.when_skipped) lb_publish_counters(p, false);
+    return;
+  }
+  const u64 base = (u64)threadIdx.x * kLbIT;
+  u64 x[K][kLbIT];
+  lb_load<K, WM, SM>(p, [&](int j) { return base + (u64)j; }, x);
+  u64 ex[K], tot[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    u64 run = 0;
+#pragma unroll
+    for (int j = 0; j < kLbIT; ++j) {
+      const u64 v = x[k][j];
+      x[k][j] = run;
+      run += v;
+    }
+    ex[k] = run;
+  }
+  block_exclusive_sums<K>(ex, scratch, tot);
+  if (threadIdx.x < (u32)kWave) {
+    if (lane == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k) lb_store_total(p, k, tot[k]);
+    }
+    if (p.pub.dst) lb_publish_counters(p, true);
+  }
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    if ((p.tonly >> k) & 1u) continue;  // uniform
+    const bool narrow = (p.narrow >> k) & 1u;
+#pragma unroll
+    for (int j = 0; j < kLbIT; ++j) {
+      const u64 i = base + j;
+      if (i < p.n) {
+        if (narrow) reinterpret_cast<u32 *>(p.out[k])[i] = (u32)(ex[k] + x[k][j]);
+        else p.out[k][i] = ex[k] + x[k][j];
+      }
+    }
+  }
+}
+
 // Tile loads and stores are striped across the workgroup and pass through
 // LDS (full coalescing); each thread scans kLbIT consecutive elements.
-// Every load of a tile is issued before the first is used: the element
-// index is clamped into the array and the value zeroed past its end, so no
-// load sits behind a branch (a branch around each load makes the compiler
-// wait for every one in turn).
-template <int K>
+template <int K, int WM, int SM>
 __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   constexpr int NW = kLbNT / kWave;
   __shared__ u32 s_t;
@@ -241,41 +343,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   const u64 tbase = (u64)t * kLbTile;
   // element r of this thread in the striped layout: tile position r kLbNT + thread
   u64 x[K][kLbIT];
-  if (p.n != 0) {  // uniform
-    const u64 last = p.n - 1;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      if ((p.wide >> k) & 1u) {
-        const u64 *in = static_cast<const u64 *>(p.in[k]);
-#pragma unroll
-        for (int r = 0; r < kLbIT; ++r)
-          x[k][r] = in[min<u64>(tbase + (u32)r * kLbNT + threadIdx.x, last)];
-      } else {
-        const u32 *in = static_cast<const u32 *>(p.in[k]);
-#pragma unroll
-        for (int r = 0; r < kLbIT; ++r)
-          x[k][r] = in[min<u64>(tbase + (u32)r * kLbNT + threadIdx.x, last)];
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      if (const u64 *sub = p.sub[k]) {
-#pragma unroll
-        for (int r = 0; r < kLbIT; ++r)
-          x[k][r] -= sub[min<u64>(tbase + (u32)r * kLbNT + threadIdx.x, last)];
-      }
-    }
-#pragma unroll
-    for (int k = 0; k < K; ++k)
-#pragma unroll
-      for (int r = 0; r < kLbIT; ++r)
-        if (tbase + (u32)r * kLbNT + threadIdx.x > last) x[k][r] = 0;
-  } else {
-#pragma unroll
-    for (int k = 0; k < K; ++k)
-#pragma unroll
-      for (int r = 0; r < kLbIT; ++r) x[k][r] = 0;
-  }
+  lb_load<K, WM, SM>(p, [&](int r) { return tbase + (u64)r * kLbNT + threadIdx.x; }, x);
   // to the blocked layout (thread i: elements kLbIT i .. kLbIT i + kLbIT - 1),
   // then x[k][j] becomes the exclusive sum within the thread's elements
   u64 ex[K], tot[K];
@@ -356,18 +424,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
 #pragma unroll
       for (int k = 0; k < K; ++k) {
         s_off[k] = off[k];
-        if (t == p.nb - 1) {
-          const u64 total = off[k] + tot[k];
-          if ((p.narrow >> k) & 1u) reinterpret_cast<u32 *>(p.out[k])[p.n] = (u32)total;
-          else p.out[k][p.n] = total;
-          if (p.total_to[k]) {
-            const u64 v = total - (p.tminus[k] ? *p.tminus[k] : 0ull);
-            if ((p.tnarrow >> k) & 1u)
-              *reinterpret_cast<u32 *>(p.total_to[k]) = (u32)min<u64>(v, 0xffffffffull);
-            else
-              *p.total_to[k] = v;
-          }
-        }
+        if (t == p.nb - 1) lb_store_total(p, k, off[k] + tot[k]);
       }
     }
     // every other tile has published its inclusive prefix: the totals are final
@@ -496,11 +553,27 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
   p.ctr = ctr;
   p.err = err;
   p.skip_if = skip_if;
+  u32 subm = 0;
+  for (int i = 0; i < k; ++i) subm |= (p.sub[i] ? 1u : 0u) << i;
   const dim3 g((unsigned)nb), bl(kLbNT);
-  if (k == 1) hipLaunchKernelGGL((k_scan_lb<1>), g, bl, 0, s, p);
-  else if (k == 2) hipLaunchKernelGGL((k_scan_lb<2>), g, bl, 0, s, p);
-  else if (k == 3) hipLaunchKernelGGL((k_scan_lb<3>), g, bl, 0, s, p);
-  else hipLaunchKernelGGL((k_scan_lb<4>), g, bl, 0, s, p);
+  // the column forms of the level scans compiled in (loads without
+  // branches); any other form reads them from the arguments
+  auto go = [&](auto kk, auto wm, auto sm) {
+    constexpr int K = decltype(kk)::value, WM = decltype(wm)::value, SM = decltype(sm)::value;
+    if (nb == 1) hipLaunchKernelGGL((k_scan_one<K, WM, SM>), g, bl, 0, s, p);
+    else hipLaunchKernelGGL((k_scan_lb<K, WM, SM>), g, bl, 0, s, p);
+  };
+  using I = std::integral_constant<int, -1>;
+  if (k == 4 && p.wide == 0b1001u && subm == 0)
+    go(std::integral_constant<int, 4>(), std::integral_constant<int, 0b1001>(), std::integral_constant<int, 0>());
+  else if (k == 3 && p.wide == 0b110u && subm == 0b100u)
+    go(std::integral_constant<int, 3>(), std::integral_constant<int, 0b110>(), std::integral_constant<int, 0b100>());
+  else if (k == 1 && p.wide == 1u && subm == 0)
+    go(std::integral_constant<int, 1>(), std::integral_constant<int, 1>(), std::integral_constant<int, 0>());
+  else if (k == 1) go(std::integral_constant<int, 1>(), I(), I());
+  else if (k == 2) go(std::integral_constant<int, 2>(), I(), I());
+  else if (k == 3) go(std::integral_constant<int, 3>(), I(), I());
+  else go(std::integral_constant<int, 4>(), I(), I());
 }
 
 void exclusive_scan(const u64 *in, u64 *out, u64 n, void *temp, hipStream_t s) {
