@@ -322,15 +322,20 @@ void copy_columns(const void *src, u64 sstride, void *dst, u64 dstride, u64 used
 // size: the result grows fastest in the levels where the search widens, and
 // a smaller factor copies large results several times over (without
 // reduction at config 4, 2x growth copied 25 GB for a 19.7 GB result).
+// When a growth would come within a factor of 4 of `limit` (every row the
+// search can produce, 0: unknown) it takes the limit at once, so that the
+// largest rows are never copied again.
 struct ArcCols {
   Buf b;
   u64 cap = 0;  // entries per column
+  u64 limit = 0;
   hipStream_t s = nullptr;
 
   explicit ArcCols(Allocator *A, hipStream_t st) : b(A), s(st) {}
   void grow(u64 need, u64 used) {
     if (need <= cap && b.p) return;
     u64 nc = std::max<u64>(std::max<u64>(kMinGrow, need), 4 * cap);
+    if (limit >= need && limit / 4 <= need) nc = std::max<u64>(nc, limit);
     nc = (nc + 63) & ~63ull;  // columns 256-byte aligned
     Buf nb(b.A);
     nb.ensure(5 * nc * 4);
@@ -513,6 +518,11 @@ void Composer::run(fstc_result *out) {
   bool last_direct = true;
 
   ArcCols out_arcs(&A, s);
+  // with reduction a state pair has at most maxp1 maxp2 merged arcs (one per
+  // pair of parts)
+  if (!o.no_reduction && maxp1 && maxp2 &&
+      maxp1 * maxp2 <= (~0ull >> 1) / std::max<u64>(pairspace, 1))
+    out_arcs.limit = std::min<u64>(pairspace, state_limit) * maxp1 * maxp2;
   // single-pass scan state: zero-filled when (re)allocated, then written
   // only by the scans
   Buf lbstate(&A);
