@@ -279,6 +279,15 @@ struct Timer {
   }
 };
 
+// out[0] = the inner-symbol list length of M1's start state, out[1] that of
+// M2's (read by the host with the CSR counts).
+__global__ void k_start_lists(const u32 *row1, u32 s1, const u32 *row2, u32 s2, u64 *out) {
+  if (threadIdx.x == 0) {
+    out[0] = row1[s1 + 1] - row1[s1];
+    out[1] = row2[s2 + 1] - row2[s2];
+  }
+}
+
 // Copies rows [0, used) of ncols columns of 4-byte entries, column i at
 // src + i * sstride (entries) to dst + i * dstride; 16-byte accesses (four
 // entries) when both strides are multiples of four and both bases 16-byte
@@ -463,9 +472,14 @@ void Composer::run(fstc_result *out) {
     if (product || unred_prod) build_cell_flags(c1, c1.cell_flag, s);
   }
   T.at(kNone);
-  FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 6 * sizeof(u64), hipMemcpyDeviceToHost, s));
+  if (m1.num_states && m2.num_states)
+    hipLaunchKernelGGL(k_start_lists, dim3(1), dim3(64), 0, s, c1.row, m1.start, c2.row, m2.start,
+                       dcounts + 6);
+  FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 8 * sizeof(u64), hipMemcpyDeviceToHost, s));
   sync_status();
   const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
+  const u64 start_list1 = m1.num_states && m2.num_states ? hs->words[6] : 0,
+            start_list2 = m1.num_states && m2.num_states ? hs->words[7] : 0;
   const int b1 = (int)bits_for(maxp1 ? maxp1 - 1 : 0);
   const int b2 = (int)bits_for(maxp2 ? maxp2 - 1 : 0);
   const int key_bits = b1 + b2;
@@ -555,7 +569,9 @@ void Composer::run(fstc_result *out) {
   // set when it declined a source's shape: not tried again until a level
   // taken by the per-level kernels has few sources of shapes it declines
   // (the count kernels count them)
-  bool small_shape_off = false;
+  // (known at once when the start pair's own lists have such a shape)
+  bool small_shape_off = std::min(start_list1, start_list2) > kSmallShortList ||
+                         std::max(start_list1, start_list2) > kSmallLongList;
   u32 small_levels = 0;
   Buf ssb(&A);
   SmallState *ss_dev = small_ok ? static_cast<SmallState *>(ssb.ensure(sizeof(SmallState)))

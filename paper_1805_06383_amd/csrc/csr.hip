@@ -119,17 +119,20 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 // are consecutive (the first plus the segment index).
 // The arcs' weight words as an array of their own (the product merge's
 // operand loads then fetch weights alone), zeros after the last arc.
-__global__ void k_arc_weights(const uint2 *arcs, u64 n, u32 *wts) {
-  for (u64 j = (u64)blockIdx.x * blockDim.x + threadIdx.x; j < n + kArcTail;
-       j += (u64)gridDim.x * blockDim.x)
-    wts[j] = j < n ? arcs[j].y : 0u;
-}
-
+// One launch: blocks [0, gw) copy the arcs' weight words into wts (zeros
+// after the last arc); the others set the cell flags, a wave per state.
 __global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_off,
-                             const uint2 *arcs, const u32 *part_base, u32 nq, u32 *flag) {
+                             const uint2 *arcs, const u32 *part_base, u32 nq, u32 *flag, u64 narcs,
+                             u32 *wts, u32 gw) {
+  if (blockIdx.x < gw) {
+    for (u64 j = (u64)blockIdx.x * blockDim.x + threadIdx.x; j < narcs + kArcTail;
+         j += (u64)gw * blockDim.x)
+      wts[j] = j < narcs ? arcs[j].y : 0u;
+    return;
+  }
   const u32 lane = lane_id();
-  const u64 nw = (u64)gridDim.x * blockDim.x / kWave;
-  for (u64 q = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
+  const u64 nw = (u64)(gridDim.x - gw) * blockDim.x / kWave;
+  for (u64 q = ((u64)(blockIdx.x - gw) * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
     bool bad = part_base[q + 1] - part_base[q] > kProdParts, special = false, shuffled = false;
     bool gap = false;  // a symbol other than the first plus its segment index
     u32 emax = 0, emin = 255;
@@ -143,8 +146,7 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_
           continue;
         }
         u64 m = 0;
-        for (u32 i = 0; i < n; ++i) {
-          const uint2 x = arcs[a0 + i];
+        auto take = [&](const uint2 x, u32 i) {
           m |= 1ull << (x.x & 63u);
           shuffled |= x.x != i;
           const u32 mag = x.y & 0x7fffffffu, e = mag >> 23;
@@ -153,7 +155,16 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_
             emax = max(emax, e);
             emin = min(emin, e);
           }
-        }
+        };
+        // the segment's first kArcTail arcs loaded at once (the arc array
+        // has kArcTail spare entries after its last arc), the rest one by one
+        uint2 x[kArcTail];
+#pragma unroll
+        for (u32 i = 0; i < kArcTail; ++i) x[i] = arcs[a0 + i];
+#pragma unroll
+        for (u32 i = 0; i < kArcTail; ++i)
+          if (i < n) take(x[i], i);
+        for (u32 i = kArcTail; i < n; ++i) take(arcs[a0 + i], i);
         bad |= (u32)__popcll(m) != n;
       }
     }
@@ -299,17 +310,18 @@ __device__ u32 local_runs(const u64 *k, u32 a0, u32 d, u32 *s_tmp, F &&f) {
   return carry;
 }
 
-// One workgroup per listed state (grid-stride over the list).
+// One workgroup per listed state: workgroup blk of nblk (stride over the
+// list).
 template <int NT, int IT>
-__global__ __launch_bounds__(NT) void k_state_local(LocalArgs a, const u32 *list,
-                                                    const u32 *list_len) {
+__device__ __forceinline__ void state_local(const LocalArgs &a, const u32 *list,
+                                            const u32 *list_len, u32 blk, u32 nblk) {
   __shared__ u32 s_cnt[(NT / kWave) * 256];
   __shared__ u32 s_base[256];
   __shared__ u32 s_run[256];
   __shared__ u32 s_tmp[NT / kWave];
   const u32 nlist = *list_len;
   const u64 omask = a.bo ? ((1ull << a.bo) - 1) : 0;
-  for (u32 li = blockIdx.x; li < nlist; li += gridDim.x) {
+  for (u32 li = blk; li < nlist; li += nblk) {
     const u32 q = list[li];
     const u32 a0 = a.abase[q], d = a.abase[q + 1] - a0;
     // parts: ranks of the distinct (target, outer) keys
@@ -385,18 +397,18 @@ __device__ __forceinline__ void group_sort(u64 &k, u32 &i) {
 }
 
 // A group of G lanes per listed state of at most G arcs (group lane =
-// element): the same two sorts as k_state_local, in registers.
+// element): the same two sorts as state_local, in registers; workgroup blk
+// of nblk (256 threads each).
 template <int G>
-__global__ __launch_bounds__(256) void k_state_group(LocalArgs a, const u32 *list,
-                                                     const u32 *list_len) {
+__device__ __forceinline__ void state_group(const LocalArgs &a, const u32 *list,
+                                            const u32 *list_len, u32 blk, u32 nblk) {
   constexpr u32 kPer = kWave / G;  // states per wavefront
   const u32 lane = lane_id(), gl = lane % G, gb = lane - gl;
   const u64 gmask = (G == kWave) ? ~0ull : (((1ull << G) - 1) << gb);
   const u32 nlist = *list_len;
   const u64 omask = a.bo ? ((1ull << a.bo) - 1) : 0;
-  const u32 nw = gridDim.x * (blockDim.x / kWave);
-  for (u32 wi = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; wi * kPer < nlist;
-       wi += nw) {
+  const u32 nw = nblk * (256 / kWave);
+  for (u32 wi = blk * (256 / kWave) + threadIdx.x / kWave; wi * kPer < nlist; wi += nw) {
     const u32 li = wi * kPer + lane / G;
     const u32 q = li < nlist ? list[li] : 0u;
     const u32 a0 = li < nlist ? a.abase[q] : 0u;
@@ -441,6 +453,28 @@ __global__ __launch_bounds__(256) void k_state_group(LocalArgs a, const u32 *lis
       note_max(a.maxp, np);
     }
   }
+}
+
+// The four size classes of 256-thread workgroups in one launch: blocks
+// [0, g.x) the groups of 16 lanes, then g.y blocks of groups of 64 lanes,
+// g.z workgroups with one item per thread and g.w with four (the lists of
+// classes 0 to 3, each nq entries apart).
+__global__ __launch_bounds__(256) void k_state_small(LocalArgs a, const u32 *lists,
+                                                     const u32 *list_len, u32 nq, uint4 g) {
+  u32 b = blockIdx.x;
+  if (b < g.x) return state_group<16>(a, lists, list_len, b, g.x);
+  b -= g.x;
+  if (b < g.y) return state_group<kWave>(a, lists + nq, list_len + 1, b, g.y);
+  b -= g.y;
+  if (b < g.z) return state_local<256, 1>(a, lists + 2 * (u64)nq, list_len + 2, b, g.z);
+  b -= g.z;
+  state_local<256, 4>(a, lists + 3 * (u64)nq, list_len + 3, b, g.w);
+}
+
+// Class 4: workgroups of 1024 threads with eight items per thread.
+__global__ __launch_bounds__(1024) void k_state_large(LocalArgs a, const u32 *list,
+                                                      const u32 *list_len) {
+  state_local<1024, 8>(a, list, list_len, blockIdx.x, gridDim.x);
 }
 
 // First position of every state in the sorted state keys; states with arcs
@@ -525,12 +559,10 @@ __global__ void k_csr_keys(const u32 *src, const u32 *dst, const u32 *il, const 
 
 void build_cell_flags(const Csr &c, u32 *cell_flag, hipStream_t s) {
   const u64 nw = c.num_arcs + kArcTail;
-  hipLaunchKernelGGL(k_arc_weights, dim3((unsigned)std::min<u64>(ceil_div(nw, kNT), 4096)),
-                     dim3(kNT), 0, s, c.arcs, c.num_arcs, c.wts);
-  if (!c.num_states) return;
+  const unsigned gw = (unsigned)std::min<u64>(ceil_div(nw, kNT), 4096);
   const unsigned g = (unsigned)std::min<u64>(ceil_div(c.num_states, kNT / kWave), 1u << 16);
-  hipLaunchKernelGGL(k_cell_flags, dim3(g), dim3(kNT), 0, s, c.row, c.seg_sym, c.seg_off, c.arcs,
-                     c.part_base, c.num_states, cell_flag);
+  hipLaunchKernelGGL(k_cell_flags, dim3(gw + g), dim3(kNT), 0, s, c.row, c.seg_sym, c.seg_off,
+                     c.arcs, c.part_base, c.num_states, cell_flag, c.num_arcs, c.wts, gw);
 }
 
 void check_csr_ranges(const fstc_fst &m, bool by_output) {
@@ -570,7 +602,7 @@ void alloc_csr(const fstc_fst &m, Buf &b, Csr &c) {
 
 namespace {
 
-// The per-state build (see k_state_local) for transducers of at most
+// The per-state build (see state_local) for transducers of at most
 // kLocMaxStates states whose arcs per state stay moderate on average; one
 // state with a very large share of the arcs goes through the global sorts.
 constexpr u32 kLocMaxStates = 1u << 17;
@@ -642,16 +674,13 @@ void build_csr_local(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, 
   a.maxp = d_counts + 2;
   // grids: at most one lane group (workgroup) per state of the list
   const u32 *L = lists.as<u32>();
-  hipLaunchKernelGGL(k_state_group<16>, dim3((unsigned)std::min<u64>(ceil_div(nq, 16), 4096)),
-                     dim3(256), 0, s, a, L, list_len);
-  hipLaunchKernelGGL(k_state_group<64>, dim3((unsigned)std::min<u64>(ceil_div(nq, 4), 4096)),
-                     dim3(256), 0, s, a, L + nq, list_len + 1);
-  hipLaunchKernelGGL((k_state_local<256, 1>), dim3((unsigned)std::min<u64>(nq, 4096)), dim3(256),
-                     0, s, a, L + 2 * (u64)nq, list_len + 2);
-  hipLaunchKernelGGL((k_state_local<256, 4>), dim3((unsigned)std::min<u64>(nq, 2048)), dim3(256),
-                     0, s, a, L + 3 * (u64)nq, list_len + 3);
-  hipLaunchKernelGGL((k_state_local<1024, 8>), dim3((unsigned)std::min<u64>(nq, 512)), dim3(1024),
-                     0, s, a, L + 4 * (u64)nq, list_len + 4);
+  const uint4 gs = make_uint4((unsigned)std::min<u64>(ceil_div(nq, 16), 4096),
+                              (unsigned)std::min<u64>(ceil_div(nq, 4), 4096),
+                              (unsigned)std::min<u64>(nq, 4096), (unsigned)std::min<u64>(nq, 2048));
+  hipLaunchKernelGGL(k_state_small, dim3(gs.x + gs.y + gs.z + gs.w), dim3(256), 0, s, a, L,
+                     list_len, nq, gs);
+  hipLaunchKernelGGL(k_state_large, dim3((unsigned)std::min<u64>(nq, 512)), dim3(1024), 0, s, a,
+                     L + 4 * (u64)nq, list_len + 4);
   const ScanJob jobs[2] = {{pcnt.p, false, (u64 *)c.part_base, true},
                            {scnt.p, false, (u64 *)c.row, true}};
   exclusive_scan_lb(jobs, 2, nq, lbstate, scan_ctr, d_err, s);

@@ -22,11 +22,14 @@ __global__ __launch_bounds__(kNT) void k_digit_hist(const u64 *keys, u64 n, int 
   h[threadIdx.x] = 0;
   __syncthreads();
   const u64 base = (u64)blockIdx.x * kTile;
+  // every load issued before the first is used (indices clamped into the
+  // array; n >= 2): a branch around each load would wait for every one
+  u64 k[kIT];
 #pragma unroll
-  for (int j = 0; j < kIT; ++j) {
-    u64 e = base + (u64)j * kNT + threadIdx.x;
-    if (e < n) atomicAdd(&h[(u32)(keys[e] >> shift) & mask], 1u);
-  }
+  for (int j = 0; j < kIT; ++j) k[j] = keys[min<u64>(base + (u64)j * kNT + threadIdx.x, n - 1)];
+#pragma unroll
+  for (int j = 0; j < kIT; ++j)
+    if (base + (u64)j * kNT + threadIdx.x < n) atomicAdd(&h[(u32)(k[j] >> shift) & mask], 1u);
   __syncthreads();
   hist[(u64)threadIdx.x * nb + blockIdx.x] = h[threadIdx.x];
 }

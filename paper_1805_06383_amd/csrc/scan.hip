@@ -29,11 +29,13 @@ __global__ __launch_bounds__(kScanNT) void k_tile_reduce(const TI *in, u64 n, TO
   __shared__ TO scratch[kScanNT / kWave];
   const u64 base = (u64)blockIdx.x * kScanTile;
   TO s = 0;
+  // every load issued before the first is used (indices clamped, n >= 1)
+  TI v[kScanIT];
 #pragma unroll
-  for (int j = 0; j < kScanIT; ++j) {
-    u64 i = base + (u64)j * kScanNT + threadIdx.x;
-    if (i < n) s += (TO)in[i];
-  }
+  for (int j = 0; j < kScanIT; ++j) v[j] = in[min<u64>(base + (u64)j * kScanNT + threadIdx.x, n - 1)];
+#pragma unroll
+  for (int j = 0; j < kScanIT; ++j)
+    if (base + (u64)j * kScanNT + threadIdx.x < n) s += (TO)v[j];
   s = block_sum<kScanNT, TO>(s, scratch);
   if (threadIdx.x == 0) tile_sums[blockIdx.x] = s;
 }
