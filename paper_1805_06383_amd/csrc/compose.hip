@@ -472,24 +472,8 @@ void Composer::run(fstc_result *out) {
     if (product || unred_prod) build_cell_flags(c1, c1.cell_flag, s);
   }
   T.at(kNone);
-  if (m1.num_states && m2.num_states)
-    hipLaunchKernelGGL(k_start_lists, dim3(1), dim3(64), 0, s, c1.row, m1.start, c2.row, m2.start,
-                       dcounts + 6);
-  FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 8 * sizeof(u64), hipMemcpyDeviceToHost, s));
-  sync_status();
-  const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
-  const u64 start_list1 = m1.num_states && m2.num_states ? hs->words[6] : 0,
-            start_list2 = m1.num_states && m2.num_states ? hs->words[7] : 0;
-  const int b1 = (int)bits_for(maxp1 ? maxp1 - 1 : 0);
-  const int b2 = (int)bits_for(maxp2 ? maxp2 - 1 : 0);
-  const int key_bits = b1 + b2;
-  if (key_bits > kMaxKeyBits)
-    throw Error(FSTC_ERR_RANGE, "per-state (target, outer symbol) ranks need " +
-                                    std::to_string(key_bits) + " > 40 key bits");
-  const bool wide_keys = key_bits > 32;
-  const size_t rec_bytes = wide_keys ? 8 : 4;
-
-  // (a1) states, visited table, start pair
+  // (a1) states, visited table, start pair (before the host reads the CSR
+  // counts: none of it depends on them)
   const u64 pairspace = (u64)m1.num_states * (u64)m2.num_states;
   u64 state_limit = std::min<u64>(pairspace, 0xffffffffull);
   if (o.max_states) state_limit = std::min<u64>(state_limit, o.max_states);
@@ -518,6 +502,23 @@ void Composer::run(fstc_result *out) {
   }
   launch_insert_start(hkb.as<u64>(), hcap - 1, hvb.as<u32>(), vn2, m1.start, m2.start,
                       sq1b.as<u32>(), sq2b.as<u32>(), &dst->err, s);
+
+  if (m1.num_states && m2.num_states)
+    hipLaunchKernelGGL(k_start_lists, dim3(1), dim3(64), 0, s, c1.row, m1.start, c2.row, m2.start,
+                       dcounts + 6);
+  FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 8 * sizeof(u64), hipMemcpyDeviceToHost, s));
+  sync_status();
+  const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
+  const u64 start_list1 = m1.num_states && m2.num_states ? hs->words[6] : 0,
+            start_list2 = m1.num_states && m2.num_states ? hs->words[7] : 0;
+  const int b1 = (int)bits_for(maxp1 ? maxp1 - 1 : 0);
+  const int b2 = (int)bits_for(maxp2 ? maxp2 - 1 : 0);
+  const int key_bits = b1 + b2;
+  if (key_bits > kMaxKeyBits)
+    throw Error(FSTC_ERR_RANGE, "per-state (target, outer symbol) ranks need " +
+                                    std::to_string(key_bits) + " > 40 key bits");
+  const bool wide_keys = key_bits > 32;
+  const size_t rec_bytes = wide_keys ? 8 : 4;
 
   u64 n_states = 1, arcs = 0, premerge = 0;
   u32 lo = 0, hi = 1, depth = 0, new_levels = 0, expanded_levels = 0;
