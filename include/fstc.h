@@ -225,6 +225,11 @@ typedef struct fstc_stats {
   uint64_t peak_device_bytes; /* largest amount of device memory the call held
                                  from its allocator at one time (result
                                  arrays and temporaries)                    */
+  uint32_t group_product_levels; /* direct product levels of at most 64
+                                    pairs that one workgroup took whole
+                                    (counted in direct_product_levels too;
+                                    off with opts.no_small_levels)          */
+  uint32_t reserved2;
 } fstc_stats;
 
 /*

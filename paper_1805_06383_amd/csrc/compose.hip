@@ -573,6 +573,11 @@ void Composer::run(fstc_result *out) {
   // (known at once when the start pair's own lists have such a shape)
   bool small_shape_off = std::min(start_list1, start_list2) > kSmallShortList ||
                          std::max(start_list1, start_list2) > kSmallLongList;
+  // one-workgroup product levels (launch_product_level): off with the small
+  // levels, and for the rest of the search once one declines
+  const bool tiny_ok = small_ok;
+  bool tiny_off = false;
+  u32 tiny_levels = 0;
   u32 small_levels = 0;
   Buf ssb(&A);
   SmallState *ss_dev = small_ok ? static_cast<SmallState *>(ssb.ensure(sizeof(SmallState)))
@@ -681,6 +686,76 @@ void Composer::run(fstc_result *out) {
     la.quad = quad ? 1u : 0u;
     la.glist = glist.as<u32>();
     la.grp = grp.as<u32>();
+    // A small level after a direct product level: one workgroup takes it
+    // whole when all its sources are strided product sources (level.hpp,
+    // launch_product_level), else it declines and the level takes the
+    // per-level kernels (and so do the later levels).
+    {
+      const u64 maxk_t = std::min<u64>(maxp1 * maxp2, 64);
+      if (tiny_ok && !tiny_off && product && dense_vis && last_direct && nsrc <= kTinySources &&
+          !o.deterministic_ids && !o.max_arcs && (arcs + (u64)nsrc * maxk_t) * 20 <= kEarlyBytes) {
+        out_arcs.grow(arcs + (u64)nsrc * maxk_t, arcs);
+        const u64 newcap_t = std::min<u64>((u64)nsrc * maxk_t, pairspace - n_states);
+        sq1b.grow_keep((n_states + newcap_t) * 4, n_states * 4);
+        sq2b.grow_keep((n_states + newcap_t) * 4, n_states * 4);
+        MergeArgs mt{};
+        mt.nsrc = nsrc;
+        mt.lo = lo;
+        mt.st = dst;
+        mt.pk = pk.as<u32>();
+        mt.phdr = phdr.as<uint4>();
+        mt.poff = poff.as<u64>();
+        mt.parts1 = c1.parts;
+        mt.parts2 = c2.parts;
+        mt.arcs1 = c1.arcs;
+        mt.arcs2 = c2.arcs;
+        mt.wts1 = c1.wts;
+        mt.wts2 = c2.wts;
+        mt.vis = hvb.as<u32>();
+        mt.vn2 = vn2;
+        mt.hmask = hcap - 1;
+        mt.pcnt = cnt.as<u64>();
+        mt.newc = newc.as<u32>();
+        mt.tstart = tstart.as<u64>();
+        mt.mend = mend.as<u64>();
+        mt.quad = 1u;
+        mt.out_src = out_arcs.col(0);
+        mt.out_dst = out_arcs.col(1);
+        mt.out_il = out_arcs.col(2);
+        mt.out_ol = out_arcs.col(3);
+        mt.out_w = reinterpret_cast<float *>(out_arcs.col(4));
+        mt.out_base = arcs;
+        const u32 seqt = next_publication();
+        T.at(kCount);
+        launch_product_level(la, mt, poff.as<u64>(), newoff.as<u64>(), (u32)n_states,
+                             sq1b.as<u32>(), sq2b.as<u32>(), hs_dev, seqt, s);
+        T.at(kNone);
+        wait_published(seqt);
+        if (!hs->st.declined) {
+          status_clear = true;  // the kernel cleared the level counters
+          const u64 nnew_t = hs->st.nnew, merged_t = hs->st.merged, pairs_t = hs->st.prod_records;
+          if (n_states + nnew_t > state_limit)
+            throw Error(FSTC_ERR_CAPACITY, "reachable states exceed the state limit");
+          premerge += pairs_t;
+          product_records += pairs_t;
+          max_level_pre = std::max(max_level_pre, pairs_t);
+          product_sources += nsrc;
+          product_mfma_sources += nsrc;
+          ++direct_levels;
+          ++tiny_levels;
+          arcs += merged_t;
+          n_states += nnew_t;
+          if (nnew_t) ++new_levels;
+          lo = hi;
+          hi = (u32)n_states;
+          ++depth;
+          last_direct = true;
+          continue;
+        }
+        tiny_off = true;
+        launch_reset_level(dst, s);  // clears the decline mark
+      }
+    }
     // count + level scan: records, matches and product-merge entries per
     // source; the product sources' flags summed; the scan's last tile stores
     // the level totals (R, M, product entries, product sources) and
@@ -1356,6 +1431,7 @@ void Composer::run(fstc_result *out) {
     stats->visited_form = vis_moves ? 2u : dense_vis ? 1u : 0u;
     stats->direct_product_levels = direct_levels;
     stats->peak_device_bytes = A.peak_bytes;
+    stats->group_product_levels = tiny_levels;
     stats->small_levels = small_levels;
     if (T.all) {
       stats->ms_csr = ms[kCsr];

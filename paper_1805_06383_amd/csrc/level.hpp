@@ -46,6 +46,8 @@ struct Status {
   u64 prod_entries;   // their (p1, p2) table entries: temp slots after the records
   u32 ngen;           // product-merge sources listed for the one-per-wave kernel
   u32 ngrp;           // sources listed for the 16-lane joins
+  u32 declined;       // nonzero: the one-workgroup product level did not take the level
+  u32 pad1;
 };
 static_assert(offsetof(Status, nprod) % 8 == 0 &&
                   offsetof(Status, nprod_mfma) == offsetof(Status, nprod) + 4,
@@ -396,5 +398,21 @@ void launch_reset_level(Status *st, hipStream_t s);
 // The 32-bit words of Status that the level-counter clearing zeroes (bit i:
 // word i), for a publication that clears them itself (ScanPublish).
 u64 level_clear_mask();
+
+// One-workgroup product level (merge.hip, k_product_level): a level of at
+// most kTinySources sources, every one a strided product source (the four-
+// source matrix-core form) with the dense visited array, taken whole by one
+// workgroup: selection, entry offsets, the product merge, id assignment,
+// target fix-up, the level totals and their publication (as `seq`, with the
+// counters cleared after), one launch instead of the per-level kernels.
+// It changes nothing but the sources' headers when a source is of another
+// form: then it publishes the counters with `declined` set (and clears
+// nothing) and the level takes the per-level kernels.  The result columns
+// must hold out_base + nsrc * 64 rows and the state arrays base + nsrc * 64
+// entries; la's pk, phdr, tstart, mend, newc and cnt arrays and poff (also
+// ma.poff, written here) nsrc + 1.
+constexpr u32 kTinySources = 64;
+void launch_product_level(const LevelArgs &la, const MergeArgs &ma, u64 *poff, u64 *newoff,
+                          u32 base, u32 *sq1, u32 *sq2, Status *host, u32 seq, hipStream_t s);
 
 }  // namespace fstc

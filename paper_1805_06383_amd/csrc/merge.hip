@@ -22,6 +22,7 @@
 //   * pairs claimed by the CAS are appended to a new-state list, and get the
 //     next ids once the level is merged (launch_assign).
 #include "level.hpp"
+#include "product.hpp"
 #include "radix_rank.hpp"
 
 namespace fstc {
@@ -1339,15 +1340,9 @@ __global__ __launch_bounds__(kProdNT) void k_prod_sources(MergeArgs a) {
 // (l / 16, l mod 4) of its source, so every lane owns one entry and the
 // claims and stores of four sources run side by side.  Sums and entry
 // order are those of the one-per-wave kernel's matrix-core form.
-template <bool NARROW>
-__global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
-  if (a.R_dev && *a.R_dev != 0) return;
-  if (!a.vn2) {  // impossible: launched with the dense visited array only
-    if (threadIdx.x == 0) set_error(&a.st->err, kErrBounds);
-    return;
-  }
+// The four sources 4 wv .. 4 wv + 3 (one wave; the dense visited array).
+__device__ __forceinline__ void quad_merge(const MergeArgs &a, u64 wv) {
   const u32 lane = lane_id();
-  const u64 wv = ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const u32 b = (lane >> 2) & 3u;
   const u64 u = wv * 4 + b;
   const bool in = u < a.nsrc;
@@ -1425,6 +1420,16 @@ __global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
     a.pcnt[u] = (u64)na * K;
     a.newc[u] = (u32)__popcll(cm & bmask);
   }
+}
+
+template <bool NARROW>
+__global__ __launch_bounds__(256) void k_prod_quad(MergeArgs a) {
+  if (a.R_dev && *a.R_dev != 0) return;
+  if (!a.vn2) {  // impossible: launched with the dense visited array only
+    if (threadIdx.x == 0) set_error(&a.st->err, kErrBounds);
+    return;
+  }
+  quad_merge(a, ((u64)blockIdx.x * blockDim.x + threadIdx.x) / kWave);
 }
 
 // Composition without reduction, a level of strided product sources whose
@@ -2148,10 +2153,9 @@ __global__ __launch_bounds__(256) void k_newlist_sources(MergeArgs a, const u64 
 // base + newoff[u], + 1, ..., written to the visited array, the state arrays
 // and the target column.  Lane j of a group holds entries j, j + 4, ... (a
 // source has at most 64), all loaded before any is assigned.
-__global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *newoff, u32 base,
-                                                       u32 *sq1, u32 *sq2) {
-  if (a.R_dev && *a.R_dev != 0) return;  // enqueued ahead: the level has records
-  const u64 t = (u64)blockIdx.x * blockDim.x + threadIdx.x;
+// Lane t of the four lanes of source t / 4 (whole waves).
+__device__ __forceinline__ void assign_direct_lanes(const MergeArgs &a, const u64 *newoff, u32 base,
+                                                    u32 *sq1, u32 *sq2, u64 t) {
   const u64 u = t / 4;
   const u32 j = (u32)(t % 4), lane = lane_id();
   const u32 nc = u < a.nsrc ? a.newc[u] : 0u;
@@ -2184,6 +2188,12 @@ __global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *n
     }
     id += (u32)__popcll(m);
   }
+}
+
+__global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *newoff, u32 base,
+                                                       u32 *sq1, u32 *sq2) {
+  if (a.R_dev && *a.R_dev != 0) return;  // enqueued ahead: the level has records
+  assign_direct_lanes(a, newoff, base, sq1, sq2, (u64)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 // Direct product level, after k_assign_direct: targets still marked
@@ -2524,6 +2534,7 @@ __device__ __forceinline__ void clear_level(Status *st) {
   st->ngen = 0;
   st->ngrp = 0;
   st->unfit = 0;
+  st->declined = 0;
 }
 
 
@@ -2576,6 +2587,110 @@ __global__ __launch_bounds__(1024) void k_merged_total(const u64 *at, const u64 
   __threadfence();
   publish(st, host, seq, threadIdx.x, blockDim.x);
   if (threadIdx.x == 0) clear_level(st);
+}
+
+// One-workgroup product level (level.hpp, launch_product_level).  Stages,
+// each ended by stage_barrier (the workgroup reads back what its other
+// threads wrote to global memory):
+//   1. thread per source: the product selection (the count kernels' rule);
+//      any source not in the strided four-source form declines the level;
+//   2. entry offsets (a workgroup scan of the table sizes);
+//   3. each wave merges quads of sources (the four-source kernel's code);
+//   4. new pairs and joined pairs per source scanned and summed;
+//   5. ids of the claimed targets, four lanes per source;
+//   6. the other marked targets of the level's entries;
+//   7. the level totals, their publication, the counters cleared.
+constexpr int kTinyNT = 1024;
+static_assert(kTinySources <= (u32)kTinyNT, "a thread per source");
+
+// End of a stage: every thread's stores are done (the barrier's release),
+// then each thread drops its CU's L1 lines (an agent-scope acquire), so its
+// next loads see what the others wrote; one workgroup shares one L2, so no
+// L2 write-back is needed.
+__device__ __forceinline__ void stage_barrier() {
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+__global__ __launch_bounds__(kTinyNT) void k_product_level(LevelArgs la, MergeArgs ma, u64 *poff,
+                                                           u64 *newoff, u32 base, u32 *sq1,
+                                                           u32 *sq2, Status *host, u32 seq) {
+  __shared__ u64 s_scr[kTinyNT / kWave];
+  const u32 t = threadIdx.x;
+  const u32 nsrc = la.nsrc;
+  Status *st = ma.st;
+  // 1. selection
+  u32 pk = 0;
+  bool ok = true;
+  if (t < nsrc) {
+    const u32 sid = la.lo + t;
+    const u32 q1 = la.sq1[sid], q2 = la.sq2[sid];
+    const Ranges r{la.c1.row[q1], la.c1.row[q1 + 1], la.c2.row[q2], la.c2.row[q2 + 1]};
+    const u32 mn = min(r.e1 - r.b1, r.e2 - r.b2);
+    bool mf = false, strided = false;
+    if (mn >= kProdMinSymbols && mn <= (u32)kWave) pk = select_product(la, t, q1, q2, r, mf, &strided);
+    ok = pk != 0 && strided;
+    la.pk[t] = ok ? pk : 0u;
+    la.tstart[t] = 0;
+    la.mend[t] = 0;
+    la.newc[t] = 0;
+    la.cnt[t] = 0;  // ma.pcnt
+  }
+  if (__syncthreads_or(!ok)) {
+    if (t == 0) st->declined = 1u;
+    __threadfence();
+    __syncthreads();
+    publish(st, host, seq, t, kTinyNT);
+    return;
+  }
+  // 2. entry offsets
+  u64 entries;
+  const u64 off = block_exclusive_sum<kTinyNT, u64>(t < nsrc ? pk : 0u, s_scr, &entries);
+  if (t < nsrc) poff[t] = off;  // ma.poff
+  if (t == 0) poff[nsrc] = entries;
+  stage_barrier();
+  // 3. the product merge, a quad of sources per wave at a time
+  const u32 nq = (nsrc + 3) / 4;
+  for (u32 wv = t / kWave; wv < nq; wv += kTinyNT / kWave) quad_merge(ma, wv);
+  stage_barrier();
+  // 4. new pairs (id offsets) and joined pairs
+  u32 nc = 0;
+  u64 pairs = 0;
+  if (t < nsrc) {
+    nc = __hip_atomic_load(&ma.newc[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    pairs = __hip_atomic_load(&ma.pcnt[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  u64 nnew;
+  const u64 noff = block_exclusive_sum<kTinyNT, u64>(nc, s_scr, &nnew);
+  __syncthreads();  // s_scr reused
+  const u64 npairs = block_sum<kTinyNT, u64>(pairs, s_scr);
+  if (t < nsrc) newoff[t] = noff;
+  if (t == 0) newoff[nsrc] = nnew;
+  stage_barrier();
+  // 5. ids of the claimed targets (whole waves: the lanes past the level
+  // have no new pairs)
+  for (u32 t0 = 0; t0 < 4 * nsrc; t0 += kTinyNT) assign_direct_lanes(ma, newoff, base, sq1, sq2, t0 + t);
+  stage_barrier();
+  // 6. the other marked targets (every entry has terms: entries rows)
+  u32 *dst = ma.out_dst + ma.out_base;
+  for (u64 e = t; e < entries; e += kTinyNT) {
+    const u32 x = __hip_atomic_load(&dst[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (x & kDstSlot) dst[e] = fixed_target(ma, x);
+  }
+  stage_barrier();
+  // 7. totals, publication, counters cleared
+  if (t == 0) {
+    st->merged = entries;
+    st->nnew = (u32)min<u64>(nnew, 0xffffffffull);
+    st->prod_records = npairs;
+    st->prod_entries = entries;
+    st->nprod = nsrc;
+    st->nprod_mfma = nsrc;
+  }
+  stage_barrier();
+  publish(st, host, seq, t, kTinyNT);
+  __syncthreads();
+  if (t == 0) clear_level(st);
 }
 
 __global__ void k_reset_level(Status *st) {
@@ -2844,6 +2959,14 @@ void launch_reset_level(Status *st, hipStream_t s) {
   hipLaunchKernelGGL(k_reset_level, dim3(1), dim3(1), 0, s, st);
 }
 
+void launch_product_level(const LevelArgs &la, const MergeArgs &ma, u64 *poff, u64 *newoff,
+                          u32 base, u32 *sq1, u32 *sq2, Status *host, u32 seq, hipStream_t s) {
+  if (la.nsrc == 0 || la.nsrc > kTinySources || !ma.vn2 || !ma.out_dst || ma.poff != poff)
+    throw Error(FSTC_ERR_INTERNAL, "one-workgroup product level out of its range");
+  hipLaunchKernelGGL(k_product_level, dim3(1), dim3(kTinyNT), 0, s, la, ma, poff, newoff, base, sq1,
+                     sq2, host, seq);
+}
+
 u64 level_clear_mask() {
   static_assert(sizeof(Status) <= 64 * 4, "one mask bit per word");
   u64 m = 0;
@@ -2871,6 +2994,7 @@ u64 level_clear_mask() {
   add(offsetof(Status, ngen), 4);
   add(offsetof(Status, ngrp), 4);
   add(offsetof(Status, unfit), 4);
+  add(offsetof(Status, declined), 4);
   return m;
 }
 

@@ -82,7 +82,8 @@ class FstcStats(ctypes.Structure):
                 ("total_product_sources", _u64), ("ms_product_kernel", ctypes.c_double),
                 ("product_launches", _u32), ("visited_form", _u32),
                 ("total_product_mfma_sources", _u64), ("direct_product_levels", _u32),
-                ("small_levels", _u32), ("peak_device_bytes", _u64)]
+                ("small_levels", _u32), ("peak_device_bytes", _u64),
+                ("group_product_levels", _u32), ("reserved2", _u32)]
 
 
 EXPORTS = ("fstc_compose", "fstc_compose_eps", "fstc_result_release", "fstc_build_csr", "fstc_sort_pairs",

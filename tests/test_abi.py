@@ -52,7 +52,7 @@ def test_struct_layouts_match_header(F):
     assert ctypes.sizeof(F.FstcFst) == 4 * 4 + 8 + 6 * 8
     assert ctypes.sizeof(F.FstcOpts) == 4 + 4 + 8 + 8 + 3 * 8 + 4 + 4 + 4 + 4 + 4 + 4 + 4 + 4
     assert ctypes.sizeof(F.FstcResult) == 3 * 8 + 4 + 4 + 8 * 8 + 8 * 8 + 8 * 8
-    assert ctypes.sizeof(F.FstcStats) == 4 + 4 + 4 * 8 + 8 * 8 + 4 + 4 + 8 + 8 + 4 + 4 + 8 + 4 + 4 + 5 * 8 + 8 + 4 + 4 + 8 + 4 + 4 + 8
+    assert ctypes.sizeof(F.FstcStats) == 4 + 4 + 4 * 8 + 8 * 8 + 4 + 4 + 8 + 8 + 4 + 4 + 8 + 4 + 4 + 5 * 8 + 8 + 4 + 4 + 8 + 4 + 4 + 8 + 4 + 4
 
 
 def test_struct_offsets_match_header(F, tmp_path):
