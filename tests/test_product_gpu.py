@@ -299,3 +299,48 @@ def test_product_entries_without_terms(fstc, flip):
     assert g.num_arcs < 16 * len(np.unique(g.src))
     assert_same(canon_of(g), canon_of(oracle.compose(m1, m2, max_levels=4)), rtol=RTOL,
                 what=f"config4 split halves flip={flip}")
+
+
+def _with_extra_arc(m, state):
+    """m with one more arc at `state`: a copy of its first arc (same inner
+    symbol, target and outer symbol, another weight), so that the state's
+    (part, symbol) cell holds two arcs and it takes no product merge."""
+    j = int(np.flatnonzero(m.src == state)[0])
+    def cat(a, v):
+        return np.concatenate([np.asarray(a), np.asarray([v], np.asarray(a).dtype)])
+    return W.FST(m.num_states, m.start, m.num_isyms, m.num_osyms, cat(m.src, m.src[j]),
+                 cat(m.dst, m.dst[j]), cat(m.ilabel, m.ilabel[j]), cat(m.olabel, m.olabel[j]),
+                 cat(m.weight, np.float32(0.25)), m.final)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_group_product_levels(fstc, seed):
+    """Config-4-shaped pairs: the first levels (at most 64 pairs, all strided
+    product sources) are taken whole by one workgroup; the composition equals
+    the per-level kernels' and the oracle's."""
+    m1, m2 = W.config4(seed, nq=60, m=16, nsym=8, slots=3)
+    on = fstc.compose(m1, m2)
+    off = fstc.compose(m1, m2, small_levels=False)
+    assert on.stats["group_product_levels"] >= 1
+    assert off.stats["group_product_levels"] == 0
+    a, b = on.to_host(), off.to_host()
+    assert_same(canon_of(a), canon_of(b), rtol=1e-6, what=f"seed {seed}: one workgroup / per level")
+    assert a.num_premerge == b.num_premerge and a.levels == b.levels
+    assert_same(canon_of(a), canon_of(oracle.compose(m1, m2)), rtol=RTOL, what=f"seed {seed} vs oracle")
+
+
+@pytest.mark.parametrize("depth", [0, 1])
+def test_group_product_level_declines(fstc, depth):
+    """A pair of another form at depth 0 or 1 (a state with two arcs in one
+    cell): the one-workgroup level declines there, the per-level kernels take
+    it and the later levels, and the result is unchanged."""
+    m1, m2 = W.config4(5, nq=60, m=16, nsym=8, slots=3)
+    state = m1.start if depth == 0 else int(m1.dst[np.flatnonzero(m1.src == m1.start)[0]])
+    m1 = _with_extra_arc(m1, state)
+    on = fstc.compose(m1, m2)
+    off = fstc.compose(m1, m2, small_levels=False)
+    a, b = on.to_host(), off.to_host()
+    assert_same(canon_of(a), canon_of(b), rtol=1e-6, what=f"depth {depth}: declined level")
+    assert_same(canon_of(a), canon_of(oracle.compose(m1, m2)), rtol=RTOL, what=f"depth {depth} vs oracle")
+    if depth == 0:
+        assert on.stats["group_product_levels"] == 0
