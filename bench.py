@@ -293,6 +293,19 @@ def main():
         rec_ms = {k: kern[k]["ms_per_step"] for k in ab}
         dom = max(rec_ms, key=rec_ms.get)
         exact = traffic_key and not args.max_levels and not args.no_reduction
+        if pms == 0 and rec_ms[dom] == 0:
+            # no per-level kernel ran: the one-workgroup kernels took every
+            # level; their bytes are the result they write (20 B per arc, 9 B
+            # per state), over the whole step
+            step_ms = secs * 1e3 / args.steps
+            nbytes = last.num_arcs * 20 + last.num_states * 9
+            gbs = nbytes / (step_ms * 1e-3) / 1e9
+            roof = {"bound": "hbm", "kernel": "k_small_levels",
+                    "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                    "limiter": "one workgroup runs every level (a few dozen pairs each): the "
+                               "latency of its dependent steps and the host's wait, not bandwidth"}
+            return kern, roof
         if pms > rec_ms[dom]:
             # the product merge dominates: its arithmetic is one multiply and
             # one add per joined pair, in float64 on the matrix cores when every

@@ -157,10 +157,12 @@ __device__ __forceinline__ bool lb_get(const LbArgs &p, u64 j, int k, int which,
   return (u32)(a >> 32) == p.epoch && (u32)(b >> 32) == p.epoch;
 }
 
-// LDS slot of tile element e: one u64 of padding every 32 elements keeps
-// both the striped (e = r * kLbNT + thread) and the blocked (e = thread *
-// kLbIT + j) accesses free of bank conflicts.
-__device__ __forceinline__ u32 lb_slot(u32 e) { return e + (e >> 5); }
+// LDS slot of tile element e (a permutation of the tile): the five low bits
+// of e flipped by bits 3 to 7, so that both the blocked rows (e = thread
+// kLbIT + j: without it every other thread's row starts on the same banks)
+// and the striped accesses (e = r kLbNT + thread) spread over all banks.
+static_assert(kLbIT == 8 && kLbTile % 256 == 0, "swizzle for rows of eight u64");
+__device__ __forceinline__ u32 lb_slot(u32 e) { return e ^ ((e >> 3) & 31u); }
 
 // Exclusive sums over the workgroup of K values at once (one barrier for
 // all K); tot[k]: the workgroup's total of array k.  scratch is read after
@@ -327,7 +329,7 @@ __global__ __launch_bounds__(kLbNT) void k_scan_lb(LbArgs p) {
   __shared__ u32 s_t;
   __shared__ u64 s_off[kLbMax];
   __shared__ u64 scratch[kLbMax][NW];
-  __shared__ u64 s_x[kLbTile + kLbTile / 32];  // one array of the tile, transposed
+  __shared__ u64 s_x[kLbTile];  // one array of the tile, transposed
   const u32 lane = lane_id();
   if (p.skip_if && *p.skip_if != 0) {  // uniform: every workgroup leaves before the counter
     if (blockIdx.x == 0 && threadIdx.x < (u32)kWave && p.pub.dst && p.pub.when_skipped)
