@@ -14,6 +14,7 @@ is the convenience entry point.
 from __future__ import annotations
 
 import ctypes
+import threading
 from dataclasses import dataclass, field
 from pathlib import Path
 
@@ -196,6 +197,23 @@ class TorchAllocator:
                         0 if small_levels else 1)
 
 
+_ALLOCATORS: dict = {}
+
+
+def _allocator(device: torch.device) -> TorchAllocator:
+    """One TorchAllocator per thread and device, reused by every call (making the two
+    ctypes callbacks costs tens of microseconds).  Between calls it holds no
+    allocation: a call's temporaries are freed by the library and its result
+    buffers taken out by _wrap."""
+    key = (threading.get_ident(), device.type,
+           device.index if device.index is not None else torch.cuda.current_device())
+    a = _ALLOCATORS.get(key)
+    if a is None:
+        a = _ALLOCATORS[key] = TorchAllocator(device)
+    a.live.clear()  # a call that failed may have left entries behind
+    return a
+
+
 # ---------------------------------------------------------------------------
 @dataclass
 class DeviceFST:
@@ -312,7 +330,7 @@ def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
     (opts.no_small_levels)."""
     lib = load_library()
     device = m1.src.device if m1.num_arcs else m1.final.device
-    alloc = TorchAllocator(device)
+    alloc = _allocator(device)
     opts = alloc.opts(max_levels, deterministic_ids, max_states, max_arcs, reduce, fused, product,
                       hash_visited, phase_timing, hash_min_log2, small_levels)
     s1, s2 = m1.struct(), m2.struct()
@@ -335,7 +353,7 @@ def fstc_compose_eps(m1: DeviceFST, m2: DeviceFST, eps: int, max_levels: int = 0
     filter state in ``state_filter``.  Options as for fstc_compose."""
     lib = load_library()
     device = m1.src.device if m1.num_arcs else m1.final.device
-    alloc = TorchAllocator(device)
+    alloc = _allocator(device)
     opts = alloc.opts(max_levels, deterministic_ids, max_states, max_arcs, reduce, fused, product,
                       hash_visited, False, 0)
     s1, s2 = m1.struct(), m2.struct()
