@@ -296,5 +296,17 @@ void exclusive_scan_lb(const ScanJob *jobs, int k, u64 n, void *state, u32 *ctr,
 size_t radix_temp_bytes(u64 n);
 void radix_sort_pairs(u64 *keys, u32 *vals, u64 *keys_alt, u32 *vals_alt, u64 n, int lo,
                       int hi, void *temp, hipStream_t s);
+// One or two independent sorts of the same kind run together: each pass's
+// histogram, scan and scatter are one launch for all the jobs still sorting
+// (when every job's digit histogram fits one workgroup's scan, n <= 2^20;
+// otherwise the sorts run one after the other).
+struct SortJob {
+  u64 *keys, *keys_alt;
+  u32 *vals, *vals_alt;
+  u64 n;
+  int lo, hi;
+  void *temp;  // radix_temp_bytes(n) bytes
+};
+void radix_sort_pairs_batch(const SortJob *jobs, int nj, hipStream_t s);
 
 }  // namespace fstc

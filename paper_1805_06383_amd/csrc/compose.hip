@@ -451,25 +451,29 @@ void Composer::run(fstc_result *out) {
                           !o.max_arcs;
   T.at(kCsr);
   {
-    // the two layouts are independent: M2's is built on a side stream
-    // while M1's is built on the call's stream (each of their kernels is
-    // short, so the two sequences overlap and fill each other's gaps); the
+    // the two layouts are independent: when both take the per-state build
+    // each of its steps is one launch for both inputs; otherwise M2's is
+    // built on a side stream while M1's is built on the call's stream (the
     // side stream's temporaries are allocated up front, in stream order on
-    // `s` before the fork
+    // `s` before the fork)
     check_csr_ranges(m1, true);
     check_csr_ranges(m2, false);
     Arena csr_tmp(&A), csr_tmp2(&A);
     csr_tmp.reserve(csr_temp_bytes(m1));
     csr_tmp2.reserve(csr_temp_bytes(m2));
-    csr_tmp2.fixed = true;
-    SideStream &side = side_stream();
-    FSTC_HIP(hipEventRecord(side.fork, s));
-    FSTC_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
-    SideJoin join{s, side};
-    build_csr(m2, false, csr_tmp2, c2, dcounts + 3, &dst->err, side.s);
-    if (product || unred_prod) build_cell_flags(c2, c2.cell_flag, side.s);
-    build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
-    if (product || unred_prod) build_cell_flags(c1, c1.cell_flag, s);
+    const bool flags = product || unred_prod;
+    if (!build_csr_pair(m1, true, csr_tmp, c1, dcounts + 0, m2, false, csr_tmp2, c2,
+                        dcounts + 3, flags, &dst->err, s)) {
+      csr_tmp2.fixed = true;
+      SideStream &side = side_stream();
+      FSTC_HIP(hipEventRecord(side.fork, s));
+      FSTC_HIP(hipStreamWaitEvent(side.s, side.fork, 0));
+      SideJoin join{s, side};
+      build_csr(m2, false, csr_tmp2, c2, dcounts + 3, &dst->err, side.s);
+      if (flags) build_cell_flags(c2, c2.cell_flag, side.s);
+      build_csr(m1, true, csr_tmp, c1, dcounts + 0, &dst->err, s);
+      if (flags) build_cell_flags(c1, c1.cell_flag, s);
+    }
   }
   T.at(kNone);
   // (a1) states, visited table, start pair (before the host reads the CSR

@@ -121,18 +121,20 @@ __global__ void k_copy_count(const u32 *src, u64 *dst) { *dst = *src; }
 // operand loads then fetch weights alone), zeros after the last arc.
 // One launch: blocks [0, gw) copy the arcs' weight words into wts (zeros
 // after the last arc); the others set the cell flags, a wave per state.
-__global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_off,
-                             const uint2 *arcs, const u32 *part_base, u32 nq, u32 *flag, u64 narcs,
-                             u32 *wts, u32 gw) {
-  if (blockIdx.x < gw) {
-    for (u64 j = (u64)blockIdx.x * blockDim.x + threadIdx.x; j < narcs + kArcTail;
+// Workgroup blk of nblk.
+__device__ __forceinline__ void cell_flags_body(const u32 *row, const u32 *seg_sym,
+                                                const u32 *seg_off, const uint2 *arcs,
+                                                const u32 *part_base, u32 nq, u32 *flag,
+                                                u64 narcs, u32 *wts, u32 gw, u32 blk, u32 nblk) {
+  if (blk < gw) {
+    for (u64 j = (u64)blk * blockDim.x + threadIdx.x; j < narcs + kArcTail;
          j += (u64)gw * blockDim.x)
       wts[j] = j < narcs ? arcs[j].y : 0u;
     return;
   }
   const u32 lane = lane_id();
-  const u64 nw = (u64)(gridDim.x - gw) * blockDim.x / kWave;
-  for (u64 q = ((u64)(blockIdx.x - gw) * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
+  const u64 nw = (u64)(nblk - gw) * blockDim.x / kWave;
+  for (u64 q = ((u64)(blk - gw) * blockDim.x + threadIdx.x) / kWave; q < nq; q += nw) {
     bool bad = part_base[q + 1] - part_base[q] > kProdParts, special = false, shuffled = false;
     bool gap = false;  // a symbol other than the first plus its segment index
     u32 emax = 0, emin = 255;
@@ -180,6 +182,13 @@ __global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_
                           (dense && ident ? kCellIdent : 0u) | (contig ? kCellContig : 0u) |
                           (emax << kCellEmaxShift) | (emin << kCellEminShift);
   }
+}
+
+__global__ void k_cell_flags(const u32 *row, const u32 *seg_sym, const u32 *seg_off,
+                             const uint2 *arcs, const u32 *part_base, u32 nq, u32 *flag, u64 narcs,
+                             u32 *wts, u32 gw) {
+  cell_flags_body(row, seg_sym, seg_off, arcs, part_base, nq, flag, narcs, wts, gw, blockIdx.x,
+                  gridDim.x);
 }
 
 // a[i] = v for i in [*count, n).
@@ -455,45 +464,81 @@ __device__ __forceinline__ void state_group(const LocalArgs &a, const u32 *list,
   }
 }
 
-// The four size classes of 256-thread workgroups in one launch: blocks
-// [0, g.x) the groups of 16 lanes, then g.y blocks of groups of 64 lanes,
-// g.z workgroups with one item per thread and g.w with four (the lists of
-// classes 0 to 3, each nq entries apart).
-__global__ __launch_bounds__(256) void k_state_small(LocalArgs a, const u32 *lists,
-                                                     const u32 *list_len, u32 nq, uint4 g) {
-  u32 b = blockIdx.x;
-  if (b < g.x) return state_group<16>(a, lists, list_len, b, g.x);
-  b -= g.x;
-  if (b < g.y) return state_group<kWave>(a, lists + nq, list_len + 1, b, g.y);
-  b -= g.y;
-  if (b < g.z) return state_local<256, 1>(a, lists + 2 * (u64)nq, list_len + 2, b, g.z);
-  b -= g.z;
-  state_local<256, 4>(a, lists + 3 * (u64)nq, list_len + 3, b, g.w);
+// One input of the per-state build as its kernels take it.  The build runs
+// one or two inputs (the two sides of a composition) in the same launches:
+// workgroups [0, split) of a launch take the first input, the rest the
+// second, so two short sequences of launches become one.
+struct LocalJob {
+  LocalArgs a;
+  u64 *skey;           // [n] source state of each position (a.skey, writable)
+  u32 *order;          // [n] arc index at each position (a.order, writable)
+  u32 *abase;          // [nq + 1] first position of each state (a.abase, writable)
+  const u32 *src, *il, *ol;  // input arcs (a.dst the targets)
+  u64 n;
+  u32 nq, nis, nos;
+  u32 *lists;          // [kLocClasses nq] states by size class
+  u32 *list_len;       // [kLocClasses] list lengths
+  u64 *counts;         // [3] segments, parts, largest part count (a.maxp)
+  u32 *row, *part_base, *seg_sym, *seg_off;
+  uint2 *parts;
+  uint4 gs;            // workgroups of the size classes 0..3 (k_loc_small)
+  u32 *cell_flag, *wts;  // cell flags and weight words (k_loc_flags)
+  u32 gw;              // workgroups of k_loc_flags copying the weights
+};
+struct LocalPair {
+  LocalJob j[2];
+};
+
+__device__ __forceinline__ const LocalJob &local_job(const LocalPair &p, u32 split, u32 &blk,
+                                                     u32 &nblk) {
+  if (blockIdx.x < split) {
+    blk = blockIdx.x;
+    nblk = split;
+    return p.j[0];
+  }
+  blk = blockIdx.x - split;
+  nblk = gridDim.x - split;
+  return p.j[1];
 }
 
-// Class 4: workgroups of 1024 threads with eight items per thread.
-__global__ __launch_bounds__(1024) void k_state_large(LocalArgs a, const u32 *list,
-                                                      const u32 *list_len) {
-  state_local<1024, 8>(a, list, list_len, blockIdx.x, gridDim.x);
+// Sort keys (the source state) and the identity order; checks every arc's
+// ids, and clears the job's counters and list lengths.
+__global__ void k_loc_keys(LocalPair p, u32 split, u32 *err) {
+  u32 blk, nblk;
+  const LocalJob &J = local_job(p, split, blk, nblk);
+  if (blk == 0) {
+    if (threadIdx.x < 3) J.counts[threadIdx.x] = 0;
+    if (threadIdx.x < (u32)kLocClasses) J.list_len[threadIdx.x] = 0;
+  }
+  for (u64 e = (u64)blk * blockDim.x + threadIdx.x; e < J.n; e += (u64)nblk * blockDim.x) {
+    u32 s = J.src[e];
+    if (s >= J.nq || J.a.dst[e] >= J.nq || J.il[e] >= J.nis || J.ol[e] >= J.nos) {
+      set_error(err, kErrBadArc);
+      s = 0;
+    }
+    J.skey[e] = s;
+    J.order[e] = (u32)e;
+  }
 }
 
 // First position of every state in the sorted state keys; states with arcs
 // are listed for the per-state kernels by size class (lists[c nq ..],
-// loc_class); states without arcs get zero counts.
-__global__ __launch_bounds__(256) void k_state_lists(const u64 *skey, u64 n, u32 nq, u32 *abase,
-                                                     u32 *pcnt, u32 *scnt, u32 *lists,
-                                                     u32 *list_len) {
+// loc_class); states without arcs get zero counts.  One thread per state
+// and one for nq.
+__global__ __launch_bounds__(256) void k_loc_lists(LocalPair p, u32 split) {
   __shared__ u32 s_n[kLocClasses], s_base[kLocClasses];
-  const u32 lane = lane_id();
-  const u64 q = (u64)blockIdx.x * blockDim.x + threadIdx.x;  // one pass: nq + 1 threads
+  u32 blk, nblk;
+  const LocalJob &J = local_job(p, split, blk, nblk);
+  const u32 lane = lane_id(), nq = J.nq;
+  const u64 q = (u64)blk * blockDim.x + threadIdx.x;
   if (threadIdx.x < (u32)kLocClasses) s_n[threadIdx.x] = 0;
   u32 d = 0;
   if (q <= nq) {
-    const u64 lo = lower_bound_dev<u64>(skey, n, q);
-    abase[q] = (u32)lo;
+    const u64 lo = lower_bound_dev<u64>(J.skey, J.n, q);
+    J.abase[q] = (u32)lo;
     if (q < nq) {
-      d = (u32)(lower_bound_dev<u64>(skey, n, q + 1) - lo);
-      if (d == 0) pcnt[q] = scnt[q] = 0;
+      d = (u32)(lower_bound_dev<u64>(J.skey, J.n, q + 1) - lo);
+      if (d == 0) J.a.pcnt[q] = J.a.scnt[q] = 0;
     }
   }
   __syncthreads();
@@ -512,47 +557,115 @@ __global__ __launch_bounds__(256) void k_state_lists(const u64 *skey, u64 n, u32
   }
   __syncthreads();
   if (threadIdx.x < (u32)kLocClasses && s_n[threadIdx.x])
-    s_base[threadIdx.x] = atomicAdd(&list_len[threadIdx.x], s_n[threadIdx.x]);
+    s_base[threadIdx.x] = atomicAdd(&J.list_len[threadIdx.x], s_n[threadIdx.x]);
   __syncthreads();
   if (d > 0) {
     const u32 l = loc_class(d);
-    lists[(u64)l * nq + s_base[l] + woff[l] + count_below(m[l])] = (u32)q;
+    J.lists[(u64)l * nq + s_base[l] + woff[l] + count_below(m[l])] = (u32)q;
+  }
+}
+
+// The four size classes of 256-thread workgroups in one launch: a job's
+// workgroups [0, g.x) the groups of 16 lanes, then g.y of groups of 64
+// lanes, g.z workgroups with one item per thread and g.w with four (the
+// lists of classes 0 to 3, each nq entries apart).
+__global__ __launch_bounds__(256) void k_loc_small(LocalPair p, u32 split) {
+  u32 b, nblk;
+  const LocalJob &J = local_job(p, split, b, nblk);
+  const uint4 g = J.gs;
+  const u32 nq = J.nq;
+  if (b < g.x) return state_group<16>(J.a, J.lists, J.list_len, b, g.x);
+  b -= g.x;
+  if (b < g.y) return state_group<kWave>(J.a, J.lists + nq, J.list_len + 1, b, g.y);
+  b -= g.y;
+  if (b < g.z) return state_local<256, 1>(J.a, J.lists + 2 * (u64)nq, J.list_len + 2, b, g.z);
+  b -= g.z;
+  state_local<256, 4>(J.a, J.lists + 3 * (u64)nq, J.list_len + 3, b, g.w);
+}
+
+// Class 4: workgroups of 1024 threads with eight items per thread.
+__global__ __launch_bounds__(1024) void k_loc_large(LocalPair p, u32 split) {
+  u32 blk, nblk;
+  const LocalJob &J = local_job(p, split, blk, nblk);
+  state_local<1024, 8>(J.a, J.lists + 4 * (u64)J.nq, J.list_len + 4, blk, nblk);
+}
+
+// part_base and row: exclusive sums of the parts and segments per state,
+// with the totals at [nq]; workgroup 2 i + c scans column c of job i.
+constexpr int kLocScanNT = 1024;
+__global__ __launch_bounds__(kLocScanNT) void k_loc_scan(LocalPair p) {
+  constexpr u32 kWaves = kLocScanNT / kWave, kBatch = 8;
+  __shared__ u32 s_tot[kWaves];
+  const LocalJob &J = p.j[blockIdx.x >> 1];
+  const bool segs = blockIdx.x & 1u;
+  const u32 *in = segs ? J.a.scnt : J.a.pcnt;
+  u32 *out = segs ? J.row : J.part_base;
+  const u32 n = J.nq;
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  // wave w sums, then scans, the entries [w S, w S + S), S a multiple of 64
+  const u32 seg = (n + kWaves * kWave - 1) / (kWaves * kWave) * kWave;
+  const u32 b = min(n, w * seg), e = min(n, b + seg);
+  u32 sum = 0;
+  for (u32 c = b; c < e; c += kBatch * kWave) {
+    u32 v[kBatch];
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) {
+      const u32 i = c + q * kWave + lane;
+      v[q] = i < e ? in[i] : 0u;
+    }
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) sum += v[q];
+  }
+  sum = wave_total(sum);
+  if (lane == 0) s_tot[w] = sum;
+  __syncthreads();
+  u32 carry = 0;
+  for (u32 k = 0; k < w; ++k) carry += s_tot[k];
+  if (w == kWaves - 1 && lane == 0) out[n] = carry + sum;
+  for (u32 c = b; c < e; c += kBatch * kWave) {  // wave-uniform bounds
+    u32 v[kBatch];
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) {
+      const u32 i = c + q * kWave + lane;
+      v[q] = i < e ? in[i] : 0u;
+    }
+#pragma unroll
+    for (u32 q = 0; q < kBatch; ++q) {
+      const u32 i = c + q * kWave + lane;
+      const u32 incl = wave_inclusive_total(v[q]);
+      if (i < e) out[i] = carry + incl - v[q];
+      carry += (u32)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+    }
   }
 }
 
 // Moves each state's parts and segments from its arc offset to their final
 // places; the totals go to counts[0] (segments) and counts[1] (parts).
-__global__ void k_state_place(const u64 *skey, const u32 *abase, u64 n, u32 nq, const u32 *pcnt,
-                              const u32 *scnt, const u32 *part_base, const u32 *row,
-                              const uint2 *ptmp, const u32 *ssym, const u32 *soff, uint2 *parts,
-                              u32 *seg_sym, u32 *seg_off, u64 *counts) {
-  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
-    const u32 q = (u32)skey[i];
-    const u32 j = (u32)i - abase[q];
-    if (j < pcnt[q]) parts[part_base[q] + j] = ptmp[i];
-    if (j < scnt[q]) {
-      seg_sym[row[q] + j] = ssym[i];
-      seg_off[row[q] + j] = soff[i];
+__global__ void k_loc_place(LocalPair p, u32 split) {
+  u32 blk, nblk;
+  const LocalJob &J = local_job(p, split, blk, nblk);
+  const u32 nq = J.nq;
+  for (u64 i = (u64)blk * blockDim.x + threadIdx.x; i < J.n; i += (u64)nblk * blockDim.x) {
+    const u32 q = (u32)J.skey[i];
+    const u32 j = (u32)i - J.a.abase[q];
+    if (j < J.a.pcnt[q]) J.parts[J.part_base[q] + j] = J.a.ptmp[i];
+    if (j < J.a.scnt[q]) {
+      J.seg_sym[J.row[q] + j] = J.a.ssym[i];
+      J.seg_off[J.row[q] + j] = J.a.soff[i];
     }
     if (i == 0) {
-      seg_off[row[nq]] = (u32)n;
-      counts[0] = row[nq];
-      counts[1] = part_base[nq];
+      J.seg_off[J.row[nq]] = (u32)J.n;
+      J.counts[0] = J.row[nq];
+      J.counts[1] = J.part_base[nq];
     }
   }
 }
 
-__global__ void k_csr_keys(const u32 *src, const u32 *dst, const u32 *il, const u32 *ol, u64 n,
-                           u32 nq, u32 nis, u32 nos, u64 *skey, u32 *order, u32 *err) {
-  for (u64 e = (u64)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (u64)gridDim.x * blockDim.x) {
-    u32 s = src[e];
-    if (s >= nq || dst[e] >= nq || il[e] >= nis || ol[e] >= nos) {
-      set_error(err, kErrBadArc);
-      s = 0;
-    }
-    skey[e] = s;
-    order[e] = (u32)e;
-  }
+__global__ void k_loc_flags(LocalPair p, u32 split) {
+  u32 blk, nblk;
+  const LocalJob &J = local_job(p, split, blk, nblk);
+  cell_flags_body(J.row, J.seg_sym, J.seg_off, J.a.arcs, J.part_base, J.nq, J.cell_flag, J.n,
+                  J.wts, J.gw, blk, nblk);
 }
 
 }  // namespace
@@ -619,74 +732,114 @@ size_t arena_bytes(std::initializer_list<size_t> sizes) {
   return t;
 }
 
-void build_csr_local(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d_counts,
-                     u32 *d_err, hipStream_t s, int bq, int bi, int bo) {
-  const u64 n = m.num_arcs;
-  const u32 nq = m.num_states;
-  Tmp skey(&T), order(&T), kalt(&T), valt(&T), kb(&T), ib(&T), part_of(&T), ptmp(&T), ssym(&T),
-      soff(&T), pcnt(&T), scnt(&T), abase(&T), lists(&T), ctl(&T), rtmp(&T);
-  skey.ensure(n * 8); order.ensure(n * 4); kalt.ensure(n * 8); valt.ensure(n * 4);
-  kb.ensure(n * 8); ib.ensure(n * 4); part_of.ensure(n * 4); ptmp.ensure(n * 8);
-  ssym.ensure(n * 4); soff.ensure(n * 4);
-  pcnt.ensure((u64)nq * 4); scnt.ensure((u64)nq * 4); abase.ensure(((u64)nq + 1) * 4);
-  lists.ensure(kLocClasses * (u64)nq * 4);
-  rtmp.ensure(radix_temp_bytes(n));
-  // control words (list lengths, scan counter) and the single-pass scan
-  // state, zero-filled together
-  constexpr size_t kCtl = 256;
-  const size_t lbb = scan_lb_state_bytes(nq);
-  ctl.ensure(kCtl + lbb);
-  fill_u32(ctl.as<u32>(), 0, (kCtl + lbb) / 4, s);
-  u32 *list_len = ctl.as<u32>(), *scan_ctr = list_len + kLocClasses;
-  void *lbstate = static_cast<char *>(ctl.p) + kCtl;
+// One input of build_csr_local.
+struct LocalIn {
+  const fstc_fst *m;
+  bool by_output;
+  Arena *T;         // its temporaries
+  const Csr *c;
+  u64 *counts;      // [3] device counters (segments, parts, largest part count)
+};
 
-  const unsigned g = grid_for(n);
-  hipLaunchKernelGGL(k_csr_keys, dim3(g), dim3(kNT), 0, s, m.src, m.dst, m.ilabel, m.olabel, n,
-                     nq, m.num_isyms, m.num_osyms, skey.as<u64>(), order.as<u32>(), d_err);
-  // stable: arcs of a state keep their input order
-  radix_sort_pairs(skey.as<u64>(), order.as<u32>(), kalt.as<u64>(), valt.as<u32>(), n, 0, bq,
-                   rtmp.p, s);
-  hipLaunchKernelGGL(k_state_lists, dim3((unsigned)ceil_div((u64)nq + 1, kNT)), dim3(kNT), 0, s,
-                     skey.as<u64>(), n, nq, abase.as<u32>(), pcnt.as<u32>(), scnt.as<u32>(),
-                     lists.as<u32>(), list_len);
-  LocalArgs a{};
-  a.skey = skey.as<u64>();
-  a.order = order.as<u32>();
-  a.abase = abase.as<u32>();
-  a.dst = m.dst;
-  a.inner = by_output ? m.olabel : m.ilabel;
-  a.outer = by_output ? m.ilabel : m.olabel;
-  a.w = m.weight;
-  a.bo = bo;
-  a.bp = bq + bo;
-  a.bi = bi;
-  a.ka = kalt.as<u64>();
-  a.kb = kb.as<u64>();
-  a.ia = valt.as<u32>();
-  a.ib = ib.as<u32>();
-  a.part_of = part_of.as<u32>();
-  a.ptmp = ptmp.as<uint2>();
-  a.ssym = ssym.as<u32>();
-  a.soff = soff.as<u32>();
-  a.arcs = c.arcs;
-  a.pcnt = pcnt.as<u32>();
-  a.scnt = scnt.as<u32>();
-  a.maxp = d_counts + 2;
-  // grids: at most one lane group (workgroup) per state of the list
-  const u32 *L = lists.as<u32>();
-  const uint4 gs = make_uint4((unsigned)std::min<u64>(ceil_div(nq, 16), 4096),
-                              (unsigned)std::min<u64>(ceil_div(nq, 4), 4096),
-                              (unsigned)std::min<u64>(nq, 4096), (unsigned)std::min<u64>(nq, 2048));
-  hipLaunchKernelGGL(k_state_small, dim3(gs.x + gs.y + gs.z + gs.w), dim3(256), 0, s, a, L,
-                     list_len, nq, gs);
-  hipLaunchKernelGGL(k_state_large, dim3((unsigned)std::min<u64>(nq, 512)), dim3(1024), 0, s, a,
-                     L + 4 * (u64)nq, list_len + 4);
-  const ScanJob jobs[2] = {{pcnt.p, false, (u64 *)c.part_base, true},
-                           {scnt.p, false, (u64 *)c.row, true}};
-  exclusive_scan_lb(jobs, 2, nq, lbstate, scan_ctr, d_err, s);
-  hipLaunchKernelGGL(k_state_place, dim3(g), dim3(kNT), 0, s, skey.as<u64>(), abase.as<u32>(), n,
-                     nq, pcnt.as<u32>(), scnt.as<u32>(), c.part_base, c.row, ptmp.as<uint2>(),
-                     ssym.as<u32>(), soff.as<u32>(), c.parts, c.seg_sym, c.seg_off, d_counts);
+// The per-state build of one or two inputs, every step one launch for both;
+// with `flags` the cell flags and weight words too (build_cell_flags).
+void build_csr_local(const LocalIn *in, int nj, bool flags, u32 *d_err, hipStream_t s) {
+  LocalPair p{};
+  SortJob sj[2];
+  for (int i = 0; i < nj; ++i) {
+    const fstc_fst &m = *in[i].m;
+    const Csr &c = *in[i].c;
+    Arena &T = *in[i].T;
+    const u64 n = m.num_arcs;
+    const u32 nq = m.num_states;
+    const int bq = (int)bits_for(nq - 1);
+    const u32 ninner = in[i].by_output ? m.num_osyms : m.num_isyms;
+    const u32 nouter = in[i].by_output ? m.num_isyms : m.num_osyms;
+    const int bi = (int)bits_for(ninner ? ninner - 1 : 0);
+    const int bo = (int)bits_for(nouter ? nouter - 1 : 0);
+    Tmp skey(&T), order(&T), kalt(&T), valt(&T), kb(&T), ib(&T), part_of(&T), ptmp(&T), ssym(&T),
+        soff(&T), pcnt(&T), scnt(&T), abase(&T), lists(&T), ctl(&T), rtmp(&T);
+    skey.ensure(n * 8); order.ensure(n * 4); kalt.ensure(n * 8); valt.ensure(n * 4);
+    kb.ensure(n * 8); ib.ensure(n * 4); part_of.ensure(n * 4); ptmp.ensure(n * 8);
+    ssym.ensure(n * 4); soff.ensure(n * 4);
+    pcnt.ensure((u64)nq * 4); scnt.ensure((u64)nq * 4); abase.ensure(((u64)nq + 1) * 4);
+    lists.ensure(kLocClasses * (u64)nq * 4);
+    rtmp.ensure(radix_temp_bytes(n));
+    ctl.ensure(256);  // list lengths
+    LocalJob &J = p.j[i];
+    LocalArgs &a = J.a;
+    a.skey = skey.as<u64>();
+    a.order = order.as<u32>();
+    a.abase = abase.as<u32>();
+    a.dst = m.dst;
+    a.inner = in[i].by_output ? m.olabel : m.ilabel;
+    a.outer = in[i].by_output ? m.ilabel : m.olabel;
+    a.w = m.weight;
+    a.bo = bo;
+    a.bp = bq + bo;
+    a.bi = bi;
+    a.ka = kalt.as<u64>();
+    a.kb = kb.as<u64>();
+    a.ia = valt.as<u32>();
+    a.ib = ib.as<u32>();
+    a.part_of = part_of.as<u32>();
+    a.ptmp = ptmp.as<uint2>();
+    a.ssym = ssym.as<u32>();
+    a.soff = soff.as<u32>();
+    a.arcs = c.arcs;
+    a.pcnt = pcnt.as<u32>();
+    a.scnt = scnt.as<u32>();
+    a.maxp = in[i].counts + 2;
+    J.skey = skey.as<u64>();
+    J.order = order.as<u32>();
+    J.abase = abase.as<u32>();
+    J.src = m.src;
+    J.il = m.ilabel;
+    J.ol = m.olabel;
+    J.n = n;
+    J.nq = nq;
+    J.nis = m.num_isyms;
+    J.nos = m.num_osyms;
+    J.lists = lists.as<u32>();
+    J.list_len = ctl.as<u32>();
+    J.counts = in[i].counts;
+    J.row = c.row;
+    J.part_base = c.part_base;
+    J.seg_sym = c.seg_sym;
+    J.seg_off = c.seg_off;
+    J.parts = c.parts;
+    // grids: at most one lane group (workgroup) per state of the list
+    J.gs = make_uint4((unsigned)std::min<u64>(ceil_div(nq, 16), 4096),
+                      (unsigned)std::min<u64>(ceil_div(nq, 4), 4096),
+                      (unsigned)std::min<u64>(nq, 4096), (unsigned)std::min<u64>(nq, 2048));
+    J.cell_flag = c.cell_flag;
+    J.wts = c.wts;
+    J.gw = (unsigned)std::min<u64>(ceil_div(n + kArcTail, kNT), 4096);
+    // stable: arcs of a state keep their input order
+    sj[i] = SortJob{skey.as<u64>(), kalt.as<u64>(), order.as<u32>(), valt.as<u32>(), n, 0, bq,
+                    rtmp.p};
+  }
+  // workgroups of each job for one step: the launch's grid and split
+  auto launch = [&](auto kern, auto blocks, unsigned nt) {
+    const unsigned g0 = blocks(p.j[0]), g1 = nj > 1 ? blocks(p.j[1]) : 0u;
+    hipLaunchKernelGGL(kern, dim3(g0 + g1), dim3(nt), 0, s, p, g0);
+  };
+  auto per_arc = [](const LocalJob &J) { return grid_for(J.n); };
+  {
+    const unsigned g0 = per_arc(p.j[0]), g1 = nj > 1 ? per_arc(p.j[1]) : 0u;
+    hipLaunchKernelGGL(k_loc_keys, dim3(g0 + g1), dim3(kNT), 0, s, p, g0, d_err);
+  }
+  radix_sort_pairs_batch(sj, nj, s);
+  launch(k_loc_lists, [](const LocalJob &J) { return (unsigned)ceil_div((u64)J.nq + 1, kNT); },
+         kNT);
+  launch(k_loc_small, [](const LocalJob &J) { return J.gs.x + J.gs.y + J.gs.z + J.gs.w; }, 256);
+  launch(k_loc_large, [](const LocalJob &J) { return (unsigned)std::min<u32>(J.nq, 512); }, 1024);
+  hipLaunchKernelGGL(k_loc_scan, dim3(2 * nj), dim3(kLocScanNT), 0, s, p);
+  launch(k_loc_place, per_arc, kNT);
+  if (flags)
+    launch(k_loc_flags, [](const LocalJob &J) {
+      return J.gw + (unsigned)std::min<u64>(ceil_div(J.nq, kNT / kWave), 1u << 16);
+    }, kNT);
 }
 
 }  // namespace
@@ -697,7 +850,7 @@ size_t csr_temp_bytes(const fstc_fst &m) {
   if (use_local_build(n, m.num_states))
     return arena_bytes({n * 8, n * 4, n * 8, n * 4, n * 8, n * 4, n * 4, n * 8, n * 4, n * 4,
                         nq * 4, nq * 4, (nq + 1) * 4, kLocClasses * nq * 4, radix_temp_bytes(n),
-                        256 + scan_lb_state_bytes(nq)});
+                        256});
   return arena_bytes({n * 8, n * 8, n * 4, n * 4, n * 8, n * 4, n * 4, (n + 1) * 4, n * 4, n * 4,
                       n * 4, std::max(radix_temp_bytes(n), scan_temp_bytes(n))});
 }
@@ -707,22 +860,24 @@ void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d
   check_csr_ranges(m, by_output);
   const u64 n = m.num_arcs;
   const u32 nq = m.num_states;
-  fill_u64(d_counts, 0, 3, s);
   if (n == 0) {
+    fill_u64(d_counts, 0, 3, s);
     fill_u32(c.row, 0, (u64)nq + 1, s);
     fill_u32(c.part_base, 0, (u64)nq + 1, s);
     fill_u32(c.seg_off, 0, 1, s);
     return;
   }
+  if (use_local_build(n, nq)) {  // its first kernel clears the counters
+    const LocalIn in{&m, by_output, &T, &c, d_counts};
+    build_csr_local(&in, 1, false, d_err, s);
+    return;
+  }
+  fill_u64(d_counts, 0, 3, s);
   const int bq = (int)bits_for(nq - 1);
   const u32 ninner = by_output ? m.num_osyms : m.num_isyms;
   const u32 nouter = by_output ? m.num_isyms : m.num_osyms;
   const int bi = (int)bits_for(ninner ? ninner - 1 : 0);
   const int bo = (int)bits_for(nouter ? nouter - 1 : 0);
-  if (use_local_build(n, nq)) {
-    build_csr_local(m, by_output, T, c, d_counts, d_err, s, bq, bi, bo);
-    return;
-  }
 
   Tmp kp(&T), kc(&T), v1(&T), v2(&T), kalt(&T), valt(&T), flags(&T), ex(&T), apg(&T),
       pstate(&T), sstate(&T), tmp(&T);
@@ -771,6 +926,20 @@ void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &c, u64 *d
                      (const u32 *)(ex.as<u32>() + n), n, 0xffffffffu);
   hipLaunchKernelGGL(k_state_offsets, dim3(grid_for((u64)nq + 1)), dim3(kNT), 0, s,
                      sstate.as<u32>(), n, nq, c.row);
+}
+
+bool build_csr_pair(const fstc_fst &m1, bool by_output1, Arena &T1, const Csr &c1,
+                    u64 *d_counts1, const fstc_fst &m2, bool by_output2, Arena &T2,
+                    const Csr &c2, u64 *d_counts2, bool flags, u32 *d_err, hipStream_t s) {
+  if (m1.num_arcs == 0 || m2.num_arcs == 0 || !use_local_build(m1.num_arcs, m1.num_states) ||
+      !use_local_build(m2.num_arcs, m2.num_states))
+    return false;
+  check_csr_ranges(m1, by_output1);
+  check_csr_ranges(m2, by_output2);
+  const LocalIn in[2] = {{&m1, by_output1, &T1, &c1, d_counts1},
+                         {&m2, by_output2, &T2, &c2, d_counts2}};
+  build_csr_local(in, 2, flags, d_err, s);
+  return true;
 }
 
 }  // namespace fstc

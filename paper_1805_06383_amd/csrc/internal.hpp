@@ -136,6 +136,14 @@ constexpr u32 kArcTail = 4;
 void build_csr(const fstc_fst &m, bool by_output, Arena &T, const Csr &out, u64 *d_counts,
                u32 *d_err, hipStream_t s);
 
+// Both inputs' layouts on stream s, the steps of the two builds sharing
+// their launches (with `flags` the cell flags and weight words too, see
+// build_cell_flags), when both inputs take the per-state build; otherwise
+// enqueues nothing and returns false.
+bool build_csr_pair(const fstc_fst &m1, bool by_output1, Arena &T1, const Csr &c1,
+                    u64 *d_counts1, const fstc_fst &m2, bool by_output2, Arena &T2,
+                    const Csr &c2, u64 *d_counts2, bool flags, u32 *d_err, hipStream_t s);
+
 // Largest part count of a state the product merge takes (level.hpp).
 constexpr u32 kProdParts = 64;
 
