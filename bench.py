@@ -243,15 +243,19 @@ def main():
             r = step()
             del r
         torch.cuda.synchronize()
-        sums = {}
+        every = []  # each step's stats, summed after the timed region
         last = None
         t0 = time.perf_counter()
         for _ in range(args.steps):
             last = step()
-            for k, v in last.stats.items():
-                sums[k] = sums.get(k, 0) + v
+            every.append(last.stats)
         torch.cuda.synchronize()
-        return time.perf_counter() - t0, last, sums
+        secs = time.perf_counter() - t0
+        sums = {}
+        for st in every:
+            for k, v in st.items():
+                sums[k] = sums.get(k, 0) + v
+        return secs, last, sums
 
     def phase_times(product: bool):
         if args.eps_pair:

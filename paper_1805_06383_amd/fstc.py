@@ -305,10 +305,13 @@ class HostComposed:
         return len(self.src)
 
 
+_ESIZE = {torch.int32: 4, torch.float32: 4, torch.uint8: 1}
+
+
 def _view(buf: torch.Tensor | None, n: int, dtype, device) -> torch.Tensor:
     if buf is None or n == 0:
         return torch.empty(0, dtype=dtype, device=device)
-    return buf[: n * torch.empty(0, dtype=dtype).element_size()].view(dtype)
+    return buf[: n * _ESIZE[dtype]].view(dtype)
 
 
 def fstc_compose(m1: DeviceFST, m2: DeviceFST, max_levels: int = 0,
@@ -375,15 +378,26 @@ def _wrap(res, st, alloc, device, filt_ptr=None) -> Composed:
     assert not alloc.live, f"library left {len(alloc.live)} temporaries allocated"
     i32, f32, u8 = torch.int32, torch.float32, torch.uint8
 
+    typed = {}  # (allocation, dtype) -> the allocation viewed as dtype
+
     def view(ptr, n, dtype):
         """Tensor of n elements at device address ptr, inside the allocation
-        that owns it (the result arrays may share allocations)."""
+        that owns it (the result arrays may share allocations): a slice of
+        that allocation viewed as dtype (one view per allocation and dtype;
+        allocations are whole multiples of 256 bytes)."""
         if not ptr or n == 0:
             return torch.empty(0, dtype=dtype, device=device)
         ptr = int(ptr)
-        for base, buf in owners:
+        es = _ESIZE[dtype]
+        for k, (base, buf) in enumerate(owners):
             if base <= ptr < base + buf.numel():
-                return _view(buf[ptr - base:], n, dtype, device)
+                off = ptr - base
+                if off % es or buf.numel() % es:
+                    return _view(buf[off:], n, dtype, device)
+                t = typed.get((k, dtype))
+                if t is None:
+                    t = typed[(k, dtype)] = buf.view(dtype)
+                return t[off // es: off // es + n]
         raise RuntimeError("result array outside its recorded allocations")
 
     stats = {k: getattr(st, k) for k, _ in FstcStats._fields_} if st is not None else {}
