@@ -300,12 +300,16 @@ void radix_sort_pairs(u64 *keys, u32 *vals, u64 *keys_alt, u32 *vals_alt, u64 n,
 // histogram, scan and scatter are one launch for all the jobs still sorting
 // (when every job's digit histogram fits one workgroup's scan, n <= 2^20;
 // otherwise the sorts run one after the other).
+// A job whose *unsorted word differs from `epoch` when its passes run is
+// already in order (the caller's check): its passes copy instead of sorting.
 struct SortJob {
   u64 *keys, *keys_alt;
   u32 *vals, *vals_alt;
   u64 n;
   int lo, hi;
   void *temp;  // radix_temp_bytes(n) bytes
+  const u32 *unsorted = nullptr;
+  u32 epoch = 0;
 };
 void radix_sort_pairs_batch(const SortJob *jobs, int nj, hipStream_t s);
 

@@ -15,6 +15,7 @@
 #include "internal.hpp"
 #include "radix_rank.hpp"
 
+#include <atomic>
 #include <initializer_list>
 
 namespace fstc {
@@ -484,6 +485,10 @@ struct LocalJob {
   uint4 gs;            // workgroups of the size classes 0..3 (k_loc_small)
   u32 *cell_flag, *wts;  // cell flags and weight words (k_loc_flags)
   u32 gw;              // workgroups of k_loc_flags copying the weights
+  // set to `epoch` by the key pass when an arc's source state is below its
+  // predecessor's (arcs not grouped by state: the state sort runs)
+  u32 *unsorted;
+  u32 epoch;
 };
 struct LocalPair {
   LocalJob j[2];
@@ -502,7 +507,9 @@ __device__ __forceinline__ const LocalJob &local_job(const LocalPair &p, u32 spl
 }
 
 // Sort keys (the source state) and the identity order; checks every arc's
-// ids, and clears the job's counters and list lengths.
+// ids, notes arcs not grouped by state (J.unsorted), and clears the job's
+// counters and list lengths.  Inputs stored state by state (as FST files
+// keep them) are already in the order the stable state sort gives.
 __global__ void k_loc_keys(LocalPair p, u32 split, u32 *err) {
   u32 blk, nblk;
   const LocalJob &J = local_job(p, split, blk, nblk);
@@ -510,8 +517,10 @@ __global__ void k_loc_keys(LocalPair p, u32 split, u32 *err) {
     if (threadIdx.x < 3) J.counts[threadIdx.x] = 0;
     if (threadIdx.x < (u32)kLocClasses) J.list_len[threadIdx.x] = 0;
   }
+  bool down = false;
   for (u64 e = (u64)blk * blockDim.x + threadIdx.x; e < J.n; e += (u64)nblk * blockDim.x) {
     u32 s = J.src[e];
+    down |= e > 0 && J.src[e - 1] > s;
     if (s >= J.nq || J.a.dst[e] >= J.nq || J.il[e] >= J.nis || J.ol[e] >= J.nos) {
       set_error(err, kErrBadArc);
       s = 0;
@@ -519,6 +528,7 @@ __global__ void k_loc_keys(LocalPair p, u32 split, u32 *err) {
     J.skey[e] = s;
     J.order[e] = (u32)e;
   }
+  if (__ballot(down) != 0 && lane_id() == 0) *J.unsorted = J.epoch;
 }
 
 // First position of every state in the sorted state keys; states with arcs
@@ -765,8 +775,11 @@ void build_csr_local(const LocalIn *in, int nj, bool flags, u32 *d_err, hipStrea
     pcnt.ensure((u64)nq * 4); scnt.ensure((u64)nq * 4); abase.ensure(((u64)nq + 1) * 4);
     lists.ensure(kLocClasses * (u64)nq * 4);
     rtmp.ensure(radix_temp_bytes(n));
-    ctl.ensure(256);  // list lengths
+    ctl.ensure(256);  // list lengths, then the unsorted word
     LocalJob &J = p.j[i];
+    static std::atomic<u32> epochs{0};
+    J.unsorted = ctl.as<u32>() + 16;
+    J.epoch = epochs.fetch_add(1, std::memory_order_relaxed) + 1;
     LocalArgs &a = J.a;
     a.skey = skey.as<u64>();
     a.order = order.as<u32>();
@@ -817,7 +830,7 @@ void build_csr_local(const LocalIn *in, int nj, bool flags, u32 *d_err, hipStrea
     J.gw = (unsigned)std::min<u64>(ceil_div(n + kArcTail, kNT), 4096);
     // stable: arcs of a state keep their input order
     sj[i] = SortJob{skey.as<u64>(), kalt.as<u64>(), order.as<u32>(), valt.as<u32>(), n, 0, bq,
-                    rtmp.p};
+                    rtmp.p, J.unsorted, J.epoch};
   }
   // workgroups of each job for one step: the launch's grid and split
   auto launch = [&](auto kern, auto blocks, unsigned nt) {

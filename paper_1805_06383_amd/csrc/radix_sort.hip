@@ -145,7 +145,15 @@ struct PassJob {
   int shift, bits;
   u32 *hist, *offs;
   u32 nb;
+  const u32 *unsorted;  // see SortJob
+  u32 epoch;
+  u32 copy;  // an ordered job's last pass of an odd number: ki copied to ko
 };
+
+// The job is already in order (see SortJob).
+__device__ __forceinline__ bool pass_in_order(const PassJob &J) {
+  return J.unsorted && *J.unsorted != J.epoch;
+}
 struct PassPair {
   PassJob j[2];
   u32 split;
@@ -163,18 +171,36 @@ __device__ __forceinline__ const PassJob &pass_job(const PassPair &p, u32 &blk) 
 __global__ __launch_bounds__(kNT) void k_digit_hist2(PassPair p) {
   u32 blk;
   const PassJob &J = pass_job(p, blk);
+  if (pass_in_order(J)) return;  // uniform
   digit_hist_tile(J.ki, J.n, J.shift, (1u << J.bits) - 1u, J.hist, J.nb, blk);
 }
 
 // workgroup i scans job i's histogram
 __global__ __launch_bounds__(kScan1NT) void k_hist_scan2(PassPair p) {
   const PassJob &J = p.j[blockIdx.x];
+  if (pass_in_order(J)) return;  // uniform
   hist_scan_block(J.hist, J.offs, 256u * J.nb);
 }
 
+// An ordered job's data stays where it is: in the last of an odd number of
+// passes it is copied to the output (the sort's result is then copied back
+// from there), otherwise nothing is done.
 __global__ __launch_bounds__(kNT) void k_digit_scatter2(PassPair p) {
   u32 blk;
   const PassJob &J = pass_job(p, blk);
+  if (pass_in_order(J)) {  // uniform
+    if (!J.copy) return;
+    const u64 base = (u64)blk * kTile;
+#pragma unroll
+    for (int j = 0; j < kIT; ++j) {
+      const u64 e = base + (u64)j * kNT + threadIdx.x;
+      if (e < J.n) {
+        J.ko[e] = J.ki[e];
+        J.vo[e] = J.vi[e];
+      }
+    }
+    return;
+  }
   digit_scatter_tile(J.ki, J.vi, J.ko, J.vo, J.n, J.shift, J.bits, J.offs, J.nb, blk);
 }
 
@@ -249,6 +275,10 @@ void radix_sort_pairs_batch(const SortJob *jobs, int nj, hipStream_t s) {
       J.nb = (u32)ceil_div(J.n, kTile);
       J.hist = (u32 *)jobs[i].temp;
       J.offs = J.hist + 256ull * J.nb;
+      J.unsorted = jobs[i].unsorted;
+      J.epoch = jobs[i].epoch;
+      const int passes = (jobs[i].hi - jobs[i].lo + 7) / 8;
+      J.copy = (passes & 1) && shift[i] + 8 >= jobs[i].hi ? 1u : 0u;
       if (na == 0) p.split = J.nb;
       grid += J.nb;
       who[na++] = i;

@@ -148,3 +148,18 @@ def test_csr_global_build(fstc):
                       ilabel=rng.integers(0, 70, 5000), olabel=rng.integers(0, 90, 5000),
                       weight=W.random_weights(rng, 5000), final=np.ones(1, np.uint8))
     check(fstc, one_small, "one state, 5000 arcs")
+
+
+@pytest.mark.parametrize("nq", [1, 200, 1000, 70_000])
+def test_csr_grouped_by_state(fstc, nq):
+    """Arcs already grouped by source state (as FST files store them): the
+    key pass finds them in order and the state sort's passes (none, one, two
+    or three 8-bit passes for these state counts) leave them as they are;
+    with one arc out of place the sort runs in full."""
+    m = skewed(nq, nq, 0, 40, 3)
+    order = np.argsort(m.src, kind="stable")
+    for k in ("src", "dst", "ilabel", "olabel", "weight"):
+        setattr(m, k, getattr(m, k)[order])
+    check(fstc, m, f"grouped, {nq} states")
+    m.src[0], m.src[-1] = m.src[-1], m.src[0]
+    check(fstc, m, f"grouped, {nq} states, one arc out of place")
