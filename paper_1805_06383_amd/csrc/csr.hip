@@ -383,6 +383,164 @@ __device__ __forceinline__ void state_local(const LocalArgs &a, const u32 *list,
   }
 }
 
+// One workgroup per listed state of at most NT IT arcs, every step in LDS:
+// the same two stable sorts and runs as state_local, with the state's arcs
+// gathered once (order, then targets, symbols and weights) and only the
+// results written to memory.  Items are wave-striped as block_rank_digits
+// takes them: item j of lane l of wave w is element w (64 IT) + 64 j + l.
+template <int IT>
+struct LdsState {
+  static constexpr int T = 256 * IT;
+  u64 key[T];     // sort keys by position
+  u32 el[T];      // element at each position
+  u32 inner[T];   // per element: inner symbol, weight bits, part rank
+  u32 wbits[T];
+  u32 part[T];
+  u32 cnt[(256 / kWave) * 256];  // block_rank_digits
+  u32 base[256];
+  u32 tmp[256 / kWave];
+  u32 wtot[256 / kWave];
+};
+
+template <int IT>
+__device__ __forceinline__ void lds_sort(LdsState<IT> &S, u64 (&key)[IT], u32 (&el)[IT],
+                                         u32 valid, int bits) {
+  constexpr u32 NT = 256;
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  for (int shift = 0; shift < bits; shift += 8) {
+    const int db = min(8, bits - shift);
+    const u32 mask = (1u << db) - 1u;
+    u32 dig[IT], rid[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) dig[j] = (u32)(key[j] >> shift) & mask;
+    block_rank_digits<NT, IT>(dig, valid, db, rid, S.cnt, S.base, S.tmp);
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      if ((valid >> j) & 1u) {
+        const u32 pos = S.base[dig[j]] + rid[j];
+        S.key[pos] = key[j];
+        S.el[pos] = el[j];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 i = w * (kWave * IT) + j * kWave + lane;
+      if ((valid >> j) & 1u) {
+        key[j] = S.key[i];
+        el[j] = S.el[i];
+      }
+    }
+    __syncthreads();  // S.key / S.el free for the next pass
+  }
+}
+
+// Run heads of the keys in position order: rank[j] = the number of heads at
+// or before item j's position, less one; returns the number of runs.  The
+// sorted keys are in S.key (written here for positions of valid items).
+template <int IT>
+__device__ __forceinline__ u32 lds_runs(LdsState<IT> &S, const u64 (&key)[IT], u32 valid,
+                                        bool (&head)[IT], u32 (&rank)[IT]) {
+  constexpr u32 NW = 256 / kWave;
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 i = w * (kWave * IT) + j * kWave + lane;
+    if ((valid >> j) & 1u) S.key[i] = key[j];
+  }
+  __syncthreads();
+  u32 wc = 0;
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const u32 i = w * (kWave * IT) + j * kWave + lane;
+    head[j] = ((valid >> j) & 1u) && (i == 0 || S.key[i - 1] != key[j]);
+    const u64 m = __ballot(head[j]);
+    rank[j] = wc + count_below(m) + (head[j] ? 1u : 0u);
+    wc += (u32)__popcll(m);
+  }
+  if (lane == 0) S.wtot[w] = wc;
+  __syncthreads();
+  u32 before = 0, all = 0;
+#pragma unroll
+  for (u32 v = 0; v < NW; ++v) {
+    const u32 c = S.wtot[v];
+    before += v < w ? c : 0u;
+    all += c;
+  }
+#pragma unroll
+  for (int j = 0; j < IT; ++j) rank[j] += before - 1u;
+  __syncthreads();  // S.wtot and S.key reads done
+  return all;
+}
+
+template <int IT>
+__device__ __forceinline__ void state_lds(const LocalArgs &a, const u32 *list, const u32 *list_len,
+                                          u32 blk, u32 nblk, LdsState<IT> &S) {
+  const u32 lane = lane_id(), w = threadIdx.x / kWave;
+  const u32 nlist = *list_len;
+  const u64 omask = a.bo ? ((1ull << a.bo) - 1) : 0;
+  for (u32 li = blk; li < nlist; li += nblk) {
+    const u32 q = list[li];
+    const u32 a0 = a.abase[q], d = a.abase[q + 1] - a0;
+    // the state's arcs: order, then their fields, every load issued first
+    u32 valid = 0, e[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 i = w * (kWave * IT) + j * kWave + lane;
+      valid |= (i < d ? 1u : 0u) << j;
+      e[j] = a.order[a0 + min(i, d - 1)];
+    }
+    u64 key[IT];
+    u32 el[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const u32 i = w * (kWave * IT) + j * kWave + lane;
+      const u32 t = a.dst[e[j]], o = a.outer[e[j]], in = a.inner[e[j]];
+      const u32 wb = __float_as_uint(a.w[e[j]]);
+      key[j] = ((u64)t << a.bo) | o;
+      el[j] = i;
+      if ((valid >> j) & 1u) {
+        S.inner[i] = in;
+        S.wbits[i] = wb;
+      }
+    }
+    // parts: ranks of the distinct (target, outer) keys
+    lds_sort<IT>(S, key, el, valid, a.bp);
+    bool head[IT];
+    u32 rank[IT];
+    const u32 np = lds_runs<IT>(S, key, valid, head, rank);
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      if (!((valid >> j) & 1u)) continue;
+      S.part[el[j]] = rank[j];
+      if (head[j])
+        a.ptmp[a0 + rank[j]] = make_uint2((u32)(key[j] >> a.bo), (u32)(key[j] & omask));
+    }
+    __syncthreads();  // S.part complete
+    // segments: the elements in part order, stably by inner symbol
+#pragma unroll
+    for (int j = 0; j < IT; ++j) key[j] = ((valid >> j) & 1u) ? (u64)S.inner[el[j]] : 0ull;
+    lds_sort<IT>(S, key, el, valid, a.bi);
+    const u32 ns = lds_runs<IT>(S, key, valid, head, rank);
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      if (!((valid >> j) & 1u)) continue;
+      const u32 i = w * (kWave * IT) + j * kWave + lane;
+      a.arcs[a0 + i] = make_uint2(S.part[el[j]], S.wbits[el[j]]);
+      if (head[j]) {
+        a.ssym[a0 + rank[j]] = (u32)key[j];
+        a.soff[a0 + rank[j]] = a0 + i;
+      }
+    }
+    if (threadIdx.x == 0) {
+      a.pcnt[q] = np;
+      a.scnt[q] = ns;
+      note_max(a.maxp, np);
+    }
+    __syncthreads();  // shared arrays free for the next state
+  }
+}
+
 // Bitonic sort of one (key, element) pair per lane within each group of G
 // lanes, ascending by key and then element number (so equal keys keep their
 // element order).
@@ -531,10 +689,59 @@ __global__ void k_loc_keys(LocalPair p, u32 split, u32 *err) {
   if (__ballot(down) != 0 && lane_id() == 0) *J.unsorted = J.epoch;
 }
 
+// First index i of the sorted keys a[0..n) with a[i] >= v (n when none),
+// searched outward from the guess g: a galloping search brackets the answer,
+// then a binary search finds it.  A good guess (states of even size) takes
+// two loads instead of the log2(n) dependent loads of a plain binary search.
+__device__ __forceinline__ u64 lower_bound_near(const u64 *a, u64 n, u64 v, u64 g) {
+  g = min(g, n);
+  u64 L, R;  // the answer lies in [L, R]
+  if (g == n || a[g] >= v) {
+    R = g;
+    u64 step = 1;
+    while (true) {
+      if (R < step) {
+        L = 0;
+        break;
+      }
+      const u64 q = R - step;
+      if (a[q] < v) {
+        L = q + 1;
+        break;
+      }
+      R = q;
+      step <<= 1;
+    }
+  } else {
+    L = g + 1;
+    u64 step = 1;
+    while (true) {
+      const u64 q = L + step - 1;
+      if (q >= n) {
+        R = n;
+        break;
+      }
+      if (a[q] >= v) {
+        R = q;
+        break;
+      }
+      L = q + 1;
+      step <<= 1;
+    }
+  }
+  while (L < R) {
+    const u64 mid = (L + R) >> 1;
+    if (a[mid] < v) L = mid + 1;
+    else R = mid;
+  }
+  return L;
+}
+
 // First position of every state in the sorted state keys; states with arcs
 // are listed for the per-state kernels by size class (lists[c nq ..],
 // loc_class); states without arcs get zero counts.  One thread per state
-// and one for nq.
+// and one for nq; the searches start from the position of a state of
+// average size.
 __global__ __launch_bounds__(256) void k_loc_lists(LocalPair p, u32 split) {
   __shared__ u32 s_n[kLocClasses], s_base[kLocClasses];
   u32 blk, nblk;
@@ -544,10 +751,10 @@ __global__ __launch_bounds__(256) void k_loc_lists(LocalPair p, u32 split) {
   if (threadIdx.x < (u32)kLocClasses) s_n[threadIdx.x] = 0;
   u32 d = 0;
   if (q <= nq) {
-    const u64 lo = lower_bound_dev<u64>(J.skey, J.n, q);
+    const u64 lo = lower_bound_near(J.skey, J.n, q, q * J.n / nq);
     J.abase[q] = (u32)lo;
     if (q < nq) {
-      d = (u32)(lower_bound_dev<u64>(J.skey, J.n, q + 1) - lo);
+      d = (u32)(lower_bound_near(J.skey, J.n, q + 1, (q + 1) * J.n / nq) - lo);
       if (d == 0) J.a.pcnt[q] = J.a.scnt[q] = 0;
     }
   }
@@ -584,13 +791,16 @@ __global__ __launch_bounds__(256) void k_loc_small(LocalPair p, u32 split) {
   const LocalJob &J = local_job(p, split, b, nblk);
   const uint4 g = J.gs;
   const u32 nq = J.nq;
+  __shared__ LdsState<4> s_state;  // classes 2 and 3 (class 2 uses its first quarter)
   if (b < g.x) return state_group<16>(J.a, J.lists, J.list_len, b, g.x);
   b -= g.x;
   if (b < g.y) return state_group<kWave>(J.a, J.lists + nq, J.list_len + 1, b, g.y);
   b -= g.y;
-  if (b < g.z) return state_local<256, 1>(J.a, J.lists + 2 * (u64)nq, J.list_len + 2, b, g.z);
+  if (b < g.z)
+    return state_lds<1>(J.a, J.lists + 2 * (u64)nq, J.list_len + 2, b, g.z,
+                        *reinterpret_cast<LdsState<1> *>(&s_state));
   b -= g.z;
-  state_local<256, 4>(J.a, J.lists + 3 * (u64)nq, J.list_len + 3, b, g.w);
+  state_lds<4>(J.a, J.lists + 3 * (u64)nq, J.list_len + 3, b, g.w, s_state);
 }
 
 // Class 4: workgroups of 1024 threads with eight items per thread.
