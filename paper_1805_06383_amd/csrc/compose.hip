@@ -866,8 +866,8 @@ void Composer::run(fstc_result *out) {
       T.at(kNone);
     }
     // Direct level enqueued whole: after the product kernel, the scans, id
-    // assignment, totals and target fix-up of a direct level go to the stream
-    // too, each reading the level's record count on the device and doing
+    // assignment and totals of a direct level go to the stream too (its
+    // marked targets are fixed after the last level), each reading the level's record count on the device and doing
     // nothing when it is not zero (k_merged_total then only publishes the
     // count's totals); the host waits once, at that publication, sized by
     // bounds: every source's largest table for the new pairs and arcs.
@@ -908,7 +908,6 @@ void Composer::run(fstc_result *out) {
       md.out_w = reinterpret_cast<float *>(out_arcs.col(4));
       md.out_base = arcs;
       launch_assign_direct(md, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
-      launch_fix_marked(md, (u64)nsrc * maxk, s);
       T.at(kNone);
     }
     wait_published(seq_wait);
@@ -1131,7 +1130,6 @@ void Composer::run(fstc_result *out) {
       sq1b.grow_keep((n_states + newcap) * 4, n_states * 4);
       sq2b.grow_keep((n_states + newcap) * 4, n_states * 4);
       launch_assign_direct(ma, newoff.as<u64>(), (u32)n_states, sq1b.as<u32>(), sq2b.as<u32>(), s);
-      launch_fix_marked(ma, prodpos, s);
       T.at(kNone);
       wait_published(seq2);
       status_clear = true;  // the totals scan cleared the level counters
@@ -1372,6 +1370,19 @@ void Composer::run(fstc_result *out) {
     ++depth;
   }
 
+  // Direct product levels leave the targets that another source of their
+  // level claimed marked with their visited-array slot: every slot has its
+  // id by now, so one pass over the result replaces them (the levels read
+  // no target of the result meanwhile).
+  if (direct_levels && arcs) {
+    MergeArgs mf{};
+    mf.st = dst;
+    mf.vis = hvb.as<u32>();
+    mf.hmask = hcap - 1;
+    mf.out_dst = out_arcs.col(1);
+    mf.out_base = 0;
+    launch_fix_marked(mf, arcs, s);
+  }
   // (a7) accept states
   Buf finb(&A);
   finb.ensure(n_states);

@@ -355,10 +355,13 @@ u64 newlist_waves(const MergeArgs &a, u64 RB);
 void launch_newlist_sources(const MergeArgs &a, const u64 *newoff, hipStream_t s);
 // Direct product level (see MergeArgs::out_src): ids base + newoff[u] + i for
 // the claimed entries of source u in entry order (visited array, state
-// arrays and the entries' target column), then every other marked target
-// replaced by its id from the visited array.
+// arrays and the entries' target column).  The other targets the level
+// marked with a slot keep the mark until launch_fix_marked.
 void launch_assign_direct(const MergeArgs &a, const u64 *newoff, u32 base, u32 *sq1, u32 *sq2,
                           hipStream_t s);
+// The n target entries from a.out_dst + a.out_base: every one still marked
+// with a visited-array slot replaced by that slot's id (once every level
+// that marked them has assigned its ids; several levels in one pass).
 void launch_fix_marked(const MergeArgs &a, u64 n, hipStream_t s);
 // Removes the entries without a term (src = kHoleSrc) from the n result rows
 // at out_base: source u's merged arcs move from out_base + poff[u] to
@@ -403,8 +406,9 @@ u64 level_clear_mask();
 // most kTinySources sources, every one a strided product source (the four-
 // source matrix-core form) with the dense visited array, taken whole by one
 // workgroup: selection, entry offsets, the product merge, id assignment,
-// target fix-up, the level totals and their publication (as `seq`, with the
-// counters cleared after), one launch instead of the per-level kernels.
+// the level totals and their publication (as `seq`, with the counters
+// cleared after), one launch instead of the per-level kernels (the targets
+// another source claimed stay marked until launch_fix_marked).
 // It changes nothing but the sources' headers when a source is of another
 // form: then it publishes the counters with `declined` set (and clears
 // nothing) and the level takes the per-level kernels.  The result columns

@@ -2196,9 +2196,10 @@ __global__ __launch_bounds__(256) void k_assign_direct(MergeArgs a, const u64 *n
   assign_direct_lanes(a, newoff, base, sq1, sq2, (u64)blockIdx.x * blockDim.x + threadIdx.x);
 }
 
-// Direct product level, after k_assign_direct: targets still marked
-// kDstSlot (claimed by another source of the level) get their ids.  Four
-// entries per thread, 16-byte accesses after a head of at most three.
+// After the id assignment of direct product levels: targets still marked
+// kDstSlot (claimed by another source of their level) get their ids from the
+// visited array.  Four entries per thread, 16-byte accesses after a head of
+// at most three.
 __device__ __forceinline__ u32 fixed_target(const MergeArgs &a, u32 x) {
   if (!(x & kDstSlot)) return x;
   const u64 slot = x & kDstSlotMask;
@@ -2210,11 +2211,6 @@ __device__ __forceinline__ u32 fixed_target(const MergeArgs &a, u32 x) {
 }
 
 __global__ void k_fix_marked(MergeArgs a, u64 n) {
-  if (a.R_dev) {  // enqueued ahead: n bounds the level's entries, whose count is the
-                  // total of the entry scan (the level counters are cleared by now)
-    if (*a.R_dev != 0) return;
-    n = min<u64>(n, a.poff[a.nsrc]);
-  }
   u32 *dst = a.out_dst + a.out_base;
   const u64 head = std::min<u64>(n, (4u - ((u32)(reinterpret_cast<uintptr_t>(dst) >> 2) & 3u)) & 3u);
   const u64 nv = (n - head) / 4;
@@ -2671,14 +2667,8 @@ __global__ __launch_bounds__(kTinyNT) void k_product_level(LevelArgs la, MergeAr
   // have no new pairs)
   for (u32 t0 = 0; t0 < 4 * nsrc; t0 += kTinyNT) assign_direct_lanes(ma, newoff, base, sq1, sq2, t0 + t);
   stage_barrier();
-  // 6. the other marked targets (every entry has terms: entries rows)
-  u32 *dst = ma.out_dst + ma.out_base;
-  for (u64 e = t; e < entries; e += kTinyNT) {
-    const u32 x = __hip_atomic_load(&dst[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (x & kDstSlot) dst[e] = fixed_target(ma, x);
-  }
-  stage_barrier();
-  // 7. totals, publication, counters cleared
+  // 6. totals, publication, counters cleared (the targets another source
+  // claimed keep their slot marks: the composition's last pass replaces them)
   if (t == 0) {
     st->merged = entries;
     st->nnew = (u32)min<u64>(nnew, 0xffffffffull);
