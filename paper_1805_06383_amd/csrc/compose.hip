@@ -535,6 +535,9 @@ void Composer::run(fstc_result *out) {
   // the previous level was a direct product level (or none has run): the
   // next one is enqueued whole before the host reads its counts
   bool last_direct = true;
+  // the previous per-level level had no listed sources: the list kernels
+  // get lean grids (see launch_count, launch_prod_sources)
+  bool lists_empty = false, listed_empty = false;
 
   ArcCols out_arcs(&A, s);
   // with reduction a state pair has at most maxp1 maxp2 merged arcs (one per
@@ -766,7 +769,7 @@ void Composer::run(fstc_result *out) {
     // publishes the counters as publication `seq`
     auto count_and_scan = [&](u32 seq) {
       T.at(kCount);
-      launch_count(la, s);
+      launch_count(la, s, lists_empty);
       ScanJob jobs[4] = {{cnt.p, true, roff.as<u64>()}, {mc.p, false, moff.as<u64>()},
                          {pk.p, false, poff.as<u64>()}, {pflag.p, true, ftot.as<u64>()}};
       jobs[3].total_only = true;
@@ -862,7 +865,8 @@ void Composer::run(fstc_result *out) {
         pm.out_base = arcs;
       }
       T.at(kProductKernel);
-      launch_prod_sources(pm, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s);
+      launch_prod_sources(pm, std::max(c1.num_arcs, c2.num_arcs) < (1ull << 29), s,
+                          listed_empty);
       T.at(kNone);
     }
     // Direct level enqueued whole: after the product kernel, the scans, id
@@ -922,6 +926,8 @@ void Composer::run(fstc_result *out) {
     }
     const u64 R = hs->st.R, M = hs->st.M;
     const u32 nbig = hs->st.nbig, nprod = hs->st.nprod;
+    lists_empty = hs->st.nwide == 0 && hs->st.nheavy == 0 && hs->st.ngrp == 0;
+    listed_empty = hs->st.ngen == 0;
     // tried again once at most one source in eight of a level is of such a
     // shape (then the next, smaller levels usually have none)
     if (small_shape_off && (u64)hs->st.unfit * 8 < nsrc) small_shape_off = false;

@@ -788,7 +788,10 @@ __global__ __launch_bounds__(kExpandNT) void k_expand(const uint4 *match, const 
 static unsigned wide_grid(u64 n) { return (unsigned)std::min<u64>(2048, ceil_div(n, 256 / kWave)); }
 static unsigned heavy_grid(u64 n) { return (unsigned)std::min<u64>(512, n); }
 
-void launch_count(const LevelArgs &a, hipStream_t s) {
+// Workgroups of each list kernel when the lists are expected empty.
+constexpr unsigned kLeanGrid = 64;
+
+void launch_count(const LevelArgs &a, hipStream_t s, bool lean) {
   const unsigned g = (unsigned)ceil_div(a.nsrc, kCountNT);
   hipLaunchKernelGGL(k_count_small, dim3(g), dim3(kCountNT), 0, s, a);
   // 16-lane joins: at most one group per source, at most as many waves as
@@ -796,10 +799,15 @@ void launch_count(const LevelArgs &a, hipStream_t s) {
   // source (1024 blocks of 8 waves at most); heavy: one block per source
   // (512 blocks at most)
   const u64 n = a.nsrc;
-  const unsigned gg = (unsigned)std::min<u64>((u64)compute_units() * 4,
-                                              ceil_div(n, kListNT / kGroupLanes));
-  const unsigned gw = (unsigned)std::min<u64>(1024, ceil_div(n, kListNT / kWave));
-  const unsigned gh = (unsigned)std::min<u64>(512, n);
+  unsigned gg = (unsigned)std::min<u64>((u64)compute_units() * 4,
+                                        ceil_div(n, kListNT / kGroupLanes));
+  unsigned gw = (unsigned)std::min<u64>(1024, ceil_div(n, kListNT / kWave));
+  unsigned gh = (unsigned)std::min<u64>(512, n);
+  if (lean) {
+    gg = std::min(gg, kLeanGrid);
+    gw = std::min(gw, kLeanGrid);
+    gh = std::min(gh, kLeanGrid);
+  }
   hipLaunchKernelGGL(k_count_lists, dim3(gg + gw + gh), dim3(kListNT), 0, s, a, gg, gw);
 }
 

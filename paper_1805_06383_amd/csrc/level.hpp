@@ -158,7 +158,10 @@ constexpr u32 kHoleSrc = 0xffffffffu;
 // (M1 part base, M2 part base, P1 | P2 << 16, matrix-core form), (M1 segment
 // range begin, end, M2 segment range begin, end).
 
-void launch_count(const LevelArgs &a, hipStream_t s);
+// lean: grids for lists expected empty (the previous level had none); the
+// list kernels loop over their lists, so a longer list is still counted,
+// by fewer workgroups.
+void launch_count(const LevelArgs &a, hipStream_t s, bool lean = false);
 // nwide / nheavy / ngrp: the list lengths the count kernels produced
 // (st->nwide, nheavy, ngrp).
 void launch_emit(const LevelArgs &a, u32 nwide, u32 nheavy, u32 ngrp, hipStream_t s);
@@ -300,7 +303,9 @@ void launch_fuse_merge(const MergeArgs &a, bool narrow, hipStream_t s);
 // direct level) and tstart / mend: with a.quad, the strided sources four per
 // wave and the listed ones (a.glist) one per wave; else every one of them
 // one per wave from the list.  narrow: both arc arrays below 2^29 arcs.
-void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s);
+// lean: a grid for a listed-source list expected empty (the previous level
+// had none; the waves loop over the list).
+void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s, bool lean = false);
 // Multi-block merge of the nbig sources listed in a.big; bigoff has nbig + 1
 // entries (exclusive scan of their record counts, total RB).
 void launch_big_counts(const u64 *roff, const u32 *big, u32 nbig, u64 *bigcnt, hipStream_t s);

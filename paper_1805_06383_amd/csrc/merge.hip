@@ -2788,7 +2788,7 @@ void launch_bitlist(const u32 *bits, u64 nwords, u32 *list, u64 cap, u32 *wcnt, 
   hipLaunchKernelGGL(k_new_total, dim3(1), dim3(1), 0, s, (const u64 *)(woff + nw), st);
 }
 
-void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s) {
+void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s, bool lean) {
   if (!a.nsrc) return;
   if (a.quad) {
     const unsigned gq = (unsigned)ceil_div(ceil_div(a.nsrc, 4), 256 / kWave);
@@ -2797,7 +2797,7 @@ void launch_prod_sources(const MergeArgs &a, bool narrow, hipStream_t s) {
   }
   // the listed sources: at most one wave per level source, and at most as
   // many waves as the chip holds at once (they loop over the list)
-  const u64 waves = std::min<u64>(a.nsrc, (u64)compute_units() * 32);
+  const u64 waves = std::min<u64>(a.nsrc, (u64)compute_units() * (lean ? 1 : 32));
   const unsigned g = (unsigned)ceil_div(waves, kProdWaves);
   if (narrow)
     hipLaunchKernelGGL(k_prod_sources<true>, dim3(g), dim3(kProdNT), 0, s, a);
