@@ -483,9 +483,26 @@ void Composer::run(fstc_result *out) {
   if (o.max_states) state_limit = std::min<u64>(state_limit, o.max_states);
   Buf sq1b(&A), sq2b(&A), hkb(&A), hvb(&A);
   // state and result arrays start at kMinGrow entries, so that small
-  // compositions never grow them
-  sq1b.ensure(kMinGrow * 4);
-  sq2b.ensure(kMinGrow * 4);
+  // compositions never grow them; when there are at most kStatePresize state
+  // pairs, the state arrays take them all (their growth copies are launches
+  // on the level loop's critical path)
+  const u64 state_start = state_limit <= kStatePresize ? std::max<u64>(kMinGrow, state_limit)
+                                                       : (u64)kMinGrow;
+  sq1b.ensure(state_start * 4);
+  sq2b.ensure(state_start * 4);
+  // single-pass scan state: zero-filled when (re)allocated, then written
+  // only by the scans; sized for levels of up to state_start sources here,
+  // while the CSR build runs
+  Buf lbstate(&A);
+  auto lb = [&](u64 n) {
+    const size_t b = scan_lb_state_bytes(n);
+    if (b > lbstate.cap) {
+      lbstate.ensure(std::max<size_t>(b, 2 * lbstate.cap));
+      fill_u32(lbstate.as<u32>(), 0, lbstate.cap / 4, s);
+    }
+    return lbstate.p;
+  };
+  (void)lb(state_start);
   // visited set: a dense array over all pairs when there are at most
   // kDensePairs of them (slot = q1 |Q2| + q2, no probing), else a hash table
   // (moved into a dense array later when that is no larger, see below)
@@ -545,17 +562,6 @@ void Composer::run(fstc_result *out) {
   if (!o.no_reduction && maxp1 && maxp2 &&
       maxp1 * maxp2 <= (~0ull >> 1) / std::max<u64>(pairspace, 1))
     out_arcs.limit = std::min<u64>(pairspace, state_limit) * maxp1 * maxp2;
-  // single-pass scan state: zero-filled when (re)allocated, then written
-  // only by the scans
-  Buf lbstate(&A);
-  auto lb = [&](u64 n) {
-    const size_t b = scan_lb_state_bytes(n);
-    if (b > lbstate.cap) {
-      lbstate.ensure(std::max<size_t>(b, 2 * lbstate.cap));
-      fill_u32(lbstate.as<u32>(), 0, lbstate.cap / 4, s);
-    }
-    return lbstate.p;
-  };
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),

@@ -23,6 +23,9 @@ struct Allocator {
 
 // Smallest capacity (in 4-byte entries) of a buffer grown with grow_keep.
 constexpr size_t kMinGrow = (size_t)1 << 18;
+// State arrays start with room for every state pair when there are at most
+// this many (16 MB per array).
+constexpr size_t kStatePresize = (size_t)1 << 22;
 
 // Grow-only device buffer owned by a compose call.
 struct Buf {
