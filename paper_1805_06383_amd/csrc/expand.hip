@@ -528,7 +528,6 @@ __global__ __launch_bounds__(256) void k_emit_group(LevelArgs a) {
 }
 
 __global__ __launch_bounds__(256) void k_emit_wide(LevelArgs a) {
-  const u32 lane = lane_id();
   const u32 gw = (blockIdx.x * blockDim.x + threadIdx.x) / kWave;
   const u32 nw = gridDim.x * blockDim.x / kWave;
   const u32 n = a.st->nwide;

@@ -113,32 +113,6 @@ __device__ __forceinline__ u32 block_offset(u32 wave_value, u32 *s_tmp, u32 *tot
   return base;
 }
 
-// Inclusive sum of v over the block in element order for wave-striped items;
-// *total receives the block total.  All threads must call it.
-__device__ __forceinline__ void striped_inclusive_sum(u32 (&v)[IT], u32 *s_tmp, u32 *total) {
-  const u32 lane = lane_id(), w = threadIdx.x / kWave;
-  u32 run = 0;
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    const u32 inc = wave_inclusive_sum(v[j]) + run;
-    run = __shfl(inc, kWave - 1, kWave);
-    v[j] = inc;
-  }
-  __syncthreads();
-  if (lane == 0) s_tmp[w] = run;
-  __syncthreads();
-  u32 base = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < NW; ++i) {
-    const u32 t = s_tmp[i];
-    if ((u32)i < w) base += t;
-    tot += t;
-  }
-#pragma unroll
-  for (int j = 0; j < IT; ++j) v[j] += base;
-  *total = tot;
-}
-
 // Linear-probing insert of B keys at once (lanes with act[i] unset skip
 // item i).  Each round issues the probe loads of all pending items before
 // testing any, so their latencies overlap.  Slots only ever change from
@@ -598,12 +572,6 @@ struct DenseRecs {
   float wt[IT];
 };
 
-// Tiles the dense-table merge takes (as far as its descriptor tells).
-__device__ __forceinline__ bool dense_ok(const MergeArgs &a, const uint4 &td) {
-  return td.x < td.y && td.w != 0 && dense_tile(td, a.key_bits) && td.w <= (u32)C &&
-         td.z <= (u32)C - td.w;
-}
-
 __device__ __forceinline__ void dense_load_offsets(const MergeArgs &a, const uint4 &td,
                                                    DenseRecs &in) {
 #pragma unroll
@@ -673,7 +641,8 @@ __device__ __forceinline__ void dense_list_runs(const MergeArgs &a, u32 tile, u6
   if (threadIdx.x == 0) a.tile_runs[tile] = nruns;
 }
 
-// Dense-table merge of tile `tile` (dense_ok) from its inputs `in`.
+// Dense-table merge of tile `tile` (a dense tile within the tile capacity,
+// as k_merge_dense checks) from its inputs `in`.
 __device__ __forceinline__ void dense_merge_tile(const MergeArgs &a, u32 tile, const uint4 td,
                                                  const DenseRecs &in, DenseLds &L) {
   unsigned long long *s_sum = L.sum;
