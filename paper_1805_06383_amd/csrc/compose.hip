@@ -279,13 +279,31 @@ struct Timer {
   }
 };
 
-// out[0] = the inner-symbol list length of M1's start state, out[1] that of
-// M2's (read by the host with the CSR counts).
-__global__ void k_start_lists(const u32 *row1, u32 s1, const u32 *row2, u32 s2, u64 *out) {
-  if (threadIdx.x == 0) {
-    out[0] = row1[s1 + 1] - row1[s1];
-    out[1] = row2[s2 + 1] - row2[s2];
+// One wave publishes to the host's staging block (coherent pinned memory):
+// nwords words (the CSR counts, then, with `lists`, the inner-symbol list
+// lengths of the two start states as words 6 and 7), the status words but
+// its sequence word, a system-scope fence, then the sequence word: the host
+// waits for it (wait_published) instead of a copy and a stream
+// synchronisation.
+__global__ __launch_bounds__(kWave) void k_publish_counts(const u32 *row1, u32 s1, const u32 *row2,
+                                                          u32 s2, int lists, const u64 *counts,
+                                                          u32 nwords, const Status *st,
+                                                          Status *host, u64 *host_words, u32 seq) {
+  const u32 lane = threadIdx.x;
+  u64 l1 = 0, l2 = 0;
+  if (lists) {  // uniform
+    l1 = row1[s1 + 1] - row1[s1];
+    l2 = row2[s2 + 1] - row2[s2];
   }
+  if (lane < nwords) host_words[lane] = lists && lane == 6 ? l1 : lists && lane == 7 ? l2 : counts[lane];
+  const u32 *src = reinterpret_cast<const u32 *>(st);
+  u32 *dst = reinterpret_cast<u32 *>(host);
+  constexpr u32 kSeqWord = offsetof(Status, seq) / 4;
+  for (u32 i = lane; i < sizeof(Status) / 4; i += kWave)
+    if (i != kSeqWord) dst[i] = src[i];
+  __threadfence_system();
+  __builtin_amdgcn_wave_barrier();
+  if (lane == 0) __hip_atomic_store(&host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // Copies rows [0, used) of ncols columns of 4-byte entries, column i at
@@ -524,11 +542,16 @@ void Composer::run(fstc_result *out) {
   launch_insert_start(hkb.as<u64>(), hcap - 1, hvb.as<u32>(), vn2, m1.start, m2.start,
                       sq1b.as<u32>(), sq2b.as<u32>(), &dst->err, s);
 
-  if (m1.num_states && m2.num_states)
-    hipLaunchKernelGGL(k_start_lists, dim3(1), dim3(64), 0, s, c1.row, m1.start, c2.row, m2.start,
-                       dcounts + 6);
-  FSTC_HIP(hipMemcpyAsync(hs->words, dcounts, 8 * sizeof(u64), hipMemcpyDeviceToHost, s));
-  sync_status();
+  u64 *hs_words_dev = reinterpret_cast<u64 *>(reinterpret_cast<char *>(hs_dev) +
+                                              offsetof(Staging, words));
+  {
+    const u32 seq0 = next_publication();
+    static_assert(sizeof(Staging::words) >= 8 * sizeof(u64), "the CSR counts fit the staging words");
+    hipLaunchKernelGGL(k_publish_counts, dim3(1), dim3(kWave), 0, s, c1.row, m1.start, c2.row,
+                       m2.start, (m1.num_states && m2.num_states) ? 1 : 0, dcounts, 8u, dst, hs_dev,
+                       hs_words_dev, seq0);
+    wait_published(seq0);
+  }
   const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
   const u64 start_list1 = m1.num_states && m2.num_states ? hs->words[6] : 0,
             start_list2 = m1.num_states && m2.num_states ? hs->words[7] : 0;
@@ -1399,7 +1422,12 @@ void Composer::run(fstc_result *out) {
   Buf finb(&A);
   finb.ensure(n_states);
   launch_finals(sq1b.as<u32>(), sq2b.as<u32>(), n_states, m1.final, m2.final, finb.as<uint8_t>(), s);
-  sync_status();
+  {
+    const u32 seqf = next_publication();
+    hipLaunchKernelGGL(k_publish_counts, dim3(1), dim3(kWave), 0, s, nullptr, 0u, nullptr, 0u, 0,
+                       nullptr, 0u, dst, hs_dev, hs_words_dev, seqf);
+    wait_published(seqf);
+  }
 
   std::memset(out, 0, sizeof(*out));
   out->num_states = n_states;
