@@ -782,30 +782,25 @@ __global__ __launch_bounds__(256) void k_loc_lists(LocalPair p, u32 split) {
   }
 }
 
-// Size classes 0 to 2 in one launch of 256-thread workgroups: a job's
+// The four size classes of 256-thread workgroups in one launch: a job's
 // workgroups [0, g.x) the groups of 16 lanes, then g.y of groups of 64
-// lanes, then g.z workgroups with one item per thread (the lists of classes
-// 0 to 2, each nq entries apart); class 3 takes g.w workgroups of k_loc_mid.
+// lanes, g.z workgroups with one item per thread and g.w with four (the
+// lists of classes 0 to 3, each nq entries apart).
 __global__ __launch_bounds__(256) void k_loc_small(LocalPair p, u32 split) {
   u32 b, nblk;
   const LocalJob &J = local_job(p, split, b, nblk);
   const uint4 g = J.gs;
   const u32 nq = J.nq;
-  __shared__ LdsState<1> s_state;  // class 2
+  __shared__ LdsState<4> s_state;  // classes 2 and 3 (class 2 uses its first quarter)
   if (b < g.x) return state_group<16>(J.a, J.lists, J.list_len, b, g.x);
   b -= g.x;
   if (b < g.y) return state_group<kWave>(J.a, J.lists + nq, J.list_len + 1, b, g.y);
   b -= g.y;
-  state_lds<1>(J.a, J.lists + 2 * (u64)nq, J.list_len + 2, b, g.z, s_state);
-}
-
-// Class 3 (257 to 1,024 arcs): its LDS state (four times class 2's) in a
-// launch of its own, so that the classes above fill the chip in one round.
-__global__ __launch_bounds__(256) void k_loc_mid(LocalPair p, u32 split) {
-  __shared__ LdsState<4> s_state;
-  u32 blk, nblk;
-  const LocalJob &J = local_job(p, split, blk, nblk);
-  state_lds<4>(J.a, J.lists + 3 * (u64)J.nq, J.list_len + 3, blk, nblk, s_state);
+  if (b < g.z)
+    return state_lds<1>(J.a, J.lists + 2 * (u64)nq, J.list_len + 2, b, g.z,
+                        *reinterpret_cast<LdsState<1> *>(&s_state));
+  b -= g.z;
+  state_lds<4>(J.a, J.lists + 3 * (u64)nq, J.list_len + 3, b, g.w, s_state);
 }
 
 // Class 4: workgroups of 1024 threads with eight items per thread.
@@ -1037,12 +1032,9 @@ void build_csr_local(const LocalIn *in, int nj, bool flags, u32 *d_err, hipStrea
     J.seg_off = c.seg_off;
     J.parts = c.parts;
     // grids: at most one lane group (workgroup) per state of the list
-    // (a state of class 3 has more than 256 arcs, one of class 4 more than
-    // 1,024: at most n / 257 and n / 1,025 of them)
     J.gs = make_uint4((unsigned)std::min<u64>(ceil_div(nq, 16), 4096),
                       (unsigned)std::min<u64>(ceil_div(nq, 4), 4096),
-                      (unsigned)std::min<u64>(nq, 4096),
-                      (unsigned)std::min<u64>(std::min<u64>(nq, n / 257 + 1), 512));
+                      (unsigned)std::min<u64>(nq, 4096), (unsigned)std::min<u64>(nq, 2048));
     J.cell_flag = c.cell_flag;
     J.wts = c.wts;
     J.gw = (unsigned)std::min<u64>(ceil_div(n + kArcTail, kNT), 4096);
@@ -1063,11 +1055,8 @@ void build_csr_local(const LocalIn *in, int nj, bool flags, u32 *d_err, hipStrea
   radix_sort_pairs_batch(sj, nj, s);
   launch(k_loc_lists, [](const LocalJob &J) { return (unsigned)ceil_div((u64)J.nq + 1, kNT); },
          kNT);
-  launch(k_loc_small, [](const LocalJob &J) { return J.gs.x + J.gs.y + J.gs.z; }, 256);
-  launch(k_loc_mid, [](const LocalJob &J) { return J.gs.w; }, 256);
-  launch(k_loc_large, [](const LocalJob &J) {
-    return (unsigned)std::min<u64>(std::min<u64>(J.nq, J.n / 1025 + 1), 512);
-  }, 1024);
+  launch(k_loc_small, [](const LocalJob &J) { return J.gs.x + J.gs.y + J.gs.z + J.gs.w; }, 256);
+  launch(k_loc_large, [](const LocalJob &J) { return (unsigned)std::min<u32>(J.nq, 512); }, 1024);
   hipLaunchKernelGGL(k_loc_scan, dim3(2 * nj), dim3(kLocScanNT), 0, s, p);
   launch(k_loc_place, per_arc, kNT);
   if (flags)
