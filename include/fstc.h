@@ -248,6 +248,11 @@ typedef struct fstc_stats {
  * P1 / P2 the largest number of distinct (target, outer symbol) pairs among
  * the arcs leaving one state of m1 / m2, bits(P1-1) + bits(P2-1) <= 40
  * (else FSTC_ERR_RANGE).
+ *
+ * Threads: calls made from different host threads, each on a stream of its
+ * own, may overlap on one GPU (the host-visible staging block, side streams
+ * and event pool are per thread, temporaries per call).  The same holds for
+ * fstc_compose_eps.
  */
 int fstc_compose(const fstc_fst *m1, const fstc_fst *m2, const fstc_opts *opts,
                  hipStream_t stream, fstc_result *out, fstc_stats *stats);
