@@ -62,6 +62,9 @@ void *Buf::ensure(size_t bytes) {
 // Growth factor of the grow-only arrays: 4 while they are small (fewer and
 // smaller copies of what they hold), 2 from kFastGrowBytes on.
 constexpr size_t kFastGrowBytes = size_t(1) << 28;
+// Largest inner alphabet for which a composition without reduction counts
+// the arcs per inner symbol to bound its result (two 16 MB histograms).
+constexpr u64 kJoinBoundSyms = u64(1) << 22;
 // Largest state or result arrays sized from the level's bounds (see the
 // early append in the level loop).
 constexpr u64 kEarlyBytes = u64(1) << 30;
@@ -306,6 +309,46 @@ __global__ __launch_bounds__(kWave) void k_publish_counts(const u32 *row1, u32 s
   if (lane == 0) __hip_atomic_store(&host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// Histogram of the labels lab[0, n) below nsym into h (added to it); per
+// workgroup in LDS first when the alphabet fits kHistLds entries.
+constexpr u32 kHistLds = 8192;
+__global__ __launch_bounds__(256) void k_label_hist(const u32 *lab, u64 n, u32 *h, u32 nsym) {
+  __shared__ u32 sh[kHistLds];
+  const bool lds = nsym <= kHistLds;  // uniform
+  if (lds) {
+    for (u32 i = threadIdx.x; i < nsym; i += blockDim.x) sh[i] = 0;
+    __syncthreads();
+  }
+  for (u64 i = (u64)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (u64)gridDim.x * blockDim.x) {
+    const u32 v = lab[i];
+    if (v < nsym) atomicAdd(lds ? &sh[v] : &h[v], 1u);
+  }
+  if (lds) {
+    __syncthreads();
+    for (u32 i = threadIdx.x; i < nsym; i += blockDim.x)
+      if (sh[i]) atomicAdd(&h[i], sh[i]);
+  }
+}
+
+// *out = sum over i < nsym of h1[i] h2[i] (one workgroup of 1024 threads).
+// With h1 / h2 the arc counts per inner symbol of the two inputs this is the
+// number of joined arc pairs over all pairs of states, which bounds the arcs
+// of a composition without reduction; it is below 2^64 because each input
+// has fewer than 2^32 arcs.
+__global__ __launch_bounds__(1024) void k_join_bound(const u32 *h1, const u32 *h2, u64 nsym,
+                                                     u64 *out) {
+  __shared__ u64 part[1024];
+  u64 acc = 0;
+  for (u64 i = threadIdx.x; i < nsym; i += 1024) acc += (u64)h1[i] * h2[i];
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  for (u32 w = 512; w; w >>= 1) {
+    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *out = part[0];
+}
+
 // Copies rows [0, used) of ncols columns of 4-byte entries, column i at
 // src + i * sstride (entries) to dst + i * dstride; 16-byte accesses (four
 // entries) when both strides are multiples of four and both bases 16-byte
@@ -452,7 +495,7 @@ void Composer::run(fstc_result *out) {
 
   static_assert(sizeof(Status) <= 256, "Status and the CSR counts share one allocation");
   Buf stb(&A);
-  dst = (Status *)stb.ensure(256 + 8 * sizeof(u64));
+  dst = (Status *)stb.ensure(256 + 16 * sizeof(u64));
   u64 *dcounts = reinterpret_cast<u64 *>(reinterpret_cast<char *>(dst) + 256);
   fill_u32((u32 *)dst, 0, sizeof(Status) / 4, s);
 
@@ -544,13 +587,33 @@ void Composer::run(fstc_result *out) {
 
   u64 *hs_words_dev = reinterpret_cast<u64 *>(reinterpret_cast<char *>(hs_dev) +
                                               offsetof(Staging, words));
+  // Without reduction every joined arc pair is an arc of the result, so the
+  // result has at most sum over inner symbols b of (arcs of m1 with output b)
+  // (arcs of m2 with input b) arcs, the count when every pair of states is
+  // reached; published in word 8 (see out_arcs.limit below).
+  const u64 nsym = m1.num_osyms;
+  const bool join_bound = o.no_reduction && nsym && nsym <= kJoinBoundSyms && m1.num_arcs &&
+                          m2.num_arcs;
+  Buf hb(&A);
+  if (join_bound) {
+    u32 *h = static_cast<u32 *>(hb.ensure(2 * nsym * 4));
+    fill_u32(h, 0, 2 * nsym, s);
+    auto hist = [&](const u32 *lab, u64 n, u32 *hh) {
+      const unsigned g = (unsigned)std::min<u64>((u64)compute_units() * 2, ceil_div(n, 256 * 16));
+      hipLaunchKernelGGL(k_label_hist, dim3(g), dim3(256), 0, s, lab, n, hh, (u32)nsym);
+    };
+    hist(m1.olabel, m1.num_arcs, h);
+    hist(m2.ilabel, m2.num_arcs, h + nsym);
+    hipLaunchKernelGGL(k_join_bound, dim3(1), dim3(1024), 0, s, h, h + nsym, nsym, dcounts + 8);
+  }
   {
     const u32 seq0 = next_publication();
-    static_assert(sizeof(Staging::words) >= 8 * sizeof(u64), "the CSR counts fit the staging words");
+    static_assert(sizeof(Staging::words) >= 9 * sizeof(u64), "the CSR counts fit the staging words");
     hipLaunchKernelGGL(k_publish_counts, dim3(1), dim3(kWave), 0, s, c1.row, m1.start, c2.row,
-                       m2.start, (m1.num_states && m2.num_states) ? 1 : 0, dcounts, 8u, dst, hs_dev,
-                       hs_words_dev, seq0);
+                       m2.start, (m1.num_states && m2.num_states) ? 1 : 0, dcounts,
+                       join_bound ? 9u : 8u, dst, hs_dev, hs_words_dev, seq0);
     wait_published(seq0);
+    hb.release();
   }
   const u64 maxp1 = hs->words[2], maxp2 = hs->words[5];
   const u64 start_list1 = m1.num_states && m2.num_states ? hs->words[6] : 0,
@@ -585,6 +648,7 @@ void Composer::run(fstc_result *out) {
   if (!o.no_reduction && maxp1 && maxp2 &&
       maxp1 * maxp2 <= (~0ull >> 1) / std::max<u64>(pairspace, 1))
     out_arcs.limit = std::min<u64>(pairspace, state_limit) * maxp1 * maxp2;
+  if (join_bound) out_arcs.limit = hs->words[8];
   // per-level temporaries, carved from one arena reset at every level
   Arena level_tmp(&A);
   Tmp cnt(&level_tmp), mc(&level_tmp), roff(&level_tmp), moff(&level_tmp), ptot(&level_tmp),

@@ -117,6 +117,14 @@ def test_unreduced_config4_full_sampled(fstc):
     dev = torch.device("cuda:0")
     d1, d2 = fstc.DeviceFST.from_host(m1, dev), fstc.DeviceFST.from_host(m2, dev)
     un = fstc.fstc_compose(d1, d2, reduce=False)
+    # the result columns stop at the joined-pair bound (sum over inner symbols
+    # of the two inputs' arc counts with that symbol, 1.024e9 arcs of 20 B)
+    # instead of growing past it
+    h1 = np.bincount(m1.olabel, minlength=m1.num_osyms).astype(np.uint64)
+    h2 = np.bincount(m2.ilabel, minlength=m2.num_isyms).astype(np.uint64)
+    bound = int((h1 * h2).sum())
+    assert un.num_arcs <= bound
+    assert un.stats["peak_device_bytes"] < bound * 20 + (2 << 30)
     red = fstc.fstc_compose(d1, d2)
     assert un.num_states == red.num_states
     assert un.num_arcs == un.num_premerge_arcs == red.num_premerge_arcs == 1024 * un.num_states
